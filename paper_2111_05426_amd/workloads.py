@@ -1,0 +1,104 @@
+"""Seeded synthetic workloads: model shapes, device constants and grid rules.
+
+Pure data, shared by the HIP path and by the tests' oracle calls.  Nothing in
+here computes any part of the simulation.
+
+The five workloads are the shapes the paper's evaluation works with, scaled
+to this project's configurations:
+
+* ``tiny_mlp``      4 dense 256-wide layers, batch 64, fp32, training with SGD;
+                    D,H,P,K in {1,2,4}, D*H*P <= 4 devices.
+* ``large_mlp``     16 dense 8192-wide layers, batch 8192, fp16, Adam;
+                    power-of-two D,H,P with D*H*P <= 16, K = 1..64.
+* ``gpt2_small``    12 layers, d_model 768, 12 heads, seq 1024, vocab 50257,
+                    batch 512 sequences, fp16, inference (the paper's GPT-2
+                    workload is inference, Sec. 4) -- also run in training;
+                    power-of-two D,H,P,K, D*H*P <= 64, K <= 128.
+* ``random_tables`` 1,000,000 random programs of 2,048 ops over 8 devices
+                    (70% compute, 20% send, 10% all-reduce), seed 0.
+* ``gpt3_175b``     96 layers, d_model 12288, 96 heads, seq 2048, vocab 50257,
+                    batch 1536 sequences, fp16 with fp32 master weights and
+                    Adam; power-of-two D,H,P with D*H*P <= 1024, K = 1..256,
+                    a 288e9-byte per-device memory cap and top-16 selection.
+
+The device constants (14e12 FLOP/s, 900e9 B/s memory, 25e9 B/s link, 5 us
+latency, 5 us launch) are the same for every workload.
+"""
+from dataclasses import dataclass, replace
+
+MLP, TRANSFORMER = 0, 1
+INFER, TRAIN_SGD, TRAIN_ADAM, TRAIN_ADAM_MIXED = 0, 1, 2, 3
+
+
+@dataclass(frozen=True)
+class ModelSpec:
+    family: int
+    mode: int
+    n_layers: int
+    n_heads: int
+    d_model: int
+    d_ff: int
+    seq_len: int
+    vocab: int
+    global_batch: int
+    elem_bytes: int
+
+
+@dataclass(frozen=True)
+class DeviceSpec:
+    flops_per_s: float = 14e12
+    mem_bytes_per_s: float = 900e9
+    link_bytes_per_s: float = 25e9
+    link_latency_s: float = 5e-6
+    launch_s: float = 5e-6
+    mem_cap_bytes: int = 0
+
+
+@dataclass(frozen=True)
+class GridSpec:
+    max_devices: int
+    exact_devices: int
+    k_mode: int          # 0: powers of two <= k_max, 1: 1..k_max, 2: K=1 if P=1 else 2..k_max pow2
+    k_max: int
+    require_k_divides: int = 0
+
+
+@dataclass(frozen=True)
+class RandomTablesSpec:
+    seed: int = 0
+    n_cand: int = 1_000_000
+    n_ops: int = 2048
+    n_dev: int = 8
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    model: ModelSpec = None
+    grid: GridSpec = None
+    device: DeviceSpec = DeviceSpec()
+    top_k: int = 1
+    tables: RandomTablesSpec = None
+
+
+def mlp(n_layers, d, batch, elem_bytes, mode):
+    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes)
+
+
+def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None):
+    return ModelSpec(TRANSFORMER, mode, n_layers, heads, d, d_ff or 4 * d, seq, vocab, batch, elem_bytes)
+
+
+TINY_MLP = Workload("tiny_mlp", mlp(4, 256, 64, 4, TRAIN_SGD), GridSpec(4, 0, 0, 4))
+LARGE_MLP = Workload("large_mlp", mlp(16, 8192, 8192, 2, TRAIN_ADAM), GridSpec(16, 0, 1, 64))
+GPT2_SMALL = Workload("gpt2_small", transformer(12, 768, 12, 1024, 50257, 512, 2, INFER),
+                      GridSpec(64, 0, 0, 128))
+GPT2_SMALL_TRAIN = replace(GPT2_SMALL, name="gpt2_small_train",
+                           model=replace(GPT2_SMALL.model, mode=TRAIN_ADAM))
+RANDOM_TABLES = Workload("random_tables", tables=RandomTablesSpec())
+GPT3_175B = Workload("gpt3_175b",
+                     transformer(96, 12288, 96, 2048, 50257, 1536, 2, TRAIN_ADAM_MIXED),
+                     GridSpec(1024, 0, 1, 256),
+                     DeviceSpec(mem_cap_bytes=288_000_000_000), top_k=16)
+
+ALL = {w.name: w for w in (TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN, RANDOM_TABLES, GPT3_175B)}
