@@ -1,0 +1,163 @@
+"""Benchmark: batched DistIR strategy simulation on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the hot path over one batch of synthetic input, with the
+input already resident in HBM:
+  * random_tables (default, the HBM-bound workload): simulate 1,000,000
+    random programs of 2,048 ops over 8 devices from their explicit op tables
+    (dsim_simulate_tables), then select the best feasible one (dsim_argmin).
+    The tables (about 41 GB) are generated on the GPU before timing.
+Prints one JSON line (rank 0).  The CPU oracle is timed on a bounded sample
+of the same workload as `cpu_baseline`.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "simulated candidates/sec + simulated ops/sec; achieved HBM GB/s vs peak"
+HBM_PEAK_GBPS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_hash(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def stored_traffic(kernel, workload, src):
+    """HBM traffic per launch measured by rocprofv3 --pmc (profiles/), if the
+    kernel source is unchanged since the counters were taken."""
+    p = os.path.join(PROFILES, "traffic.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        rec = json.load(f).get("%s/%s" % (kernel, workload))
+    if not rec or rec.get("source_sha256_16") != kernel_hash(src):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline_random(spec, dev, budget_s=12.0):
+    """The oracle, as it stands, on strided candidates of the same workload
+    until ~budget_s seconds of wall time are spent."""
+    import numpy as np
+    import oracle
+    threads = max(1, min(os.cpu_count() or 1, 16))
+    chunk = 2048 * threads // 8
+    done, t0 = 0, time.perf_counter()
+    stride = 997
+    while time.perf_counter() - t0 < budget_s:
+        cands = (np.arange(done, done + chunk, dtype=np.int64) * stride) % spec.n_cand
+        oracle.run_random_tables(spec.seed, spec.n_ops, spec.n_dev, cands, dev, threads=threads, want_rows=False)
+        done += chunk
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "sample": "%d candidates (stride 997 over the 1,000,000) x %d ops x %d devices, generated and "
+                      "simulated by the C oracle in %.1f s on %d threads" % (done, spec.n_ops, spec.n_dev, dt, threads),
+            "ops_per_s": done * spec.n_ops / dt}
+
+
+def bench_random_tables(args, torch, dsim, W):
+    spec = W.tables
+    dev = W.device
+    N, J, ND = spec.n_cand, spec.n_ops, spec.n_dev
+    tab = dsim.alloc_tables(N, J)
+    dsim.dsim_generate_random_tables(spec.seed, N, J, ND, tab)
+    res = dsim.alloc_results(N, ND)
+    res["walked_ops"] = None   # equal to n_ops for tables
+    k = W.top_k
+    ws = torch.empty(max(dsim.dsim_argmin_workspace(N, k), 16), dtype=torch.uint8, device="cuda")
+    out_idx = torch.empty(k, dtype=torch.int64, device="cuda")
+    out_mk = torch.empty(k, dtype=torch.float64, device="cuda")
+    found = torch.empty(1, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+
+    ev = []
+
+    def step(record):
+        if record:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+        dsim.dsim_simulate_tables(tab, N, ND, dev, res)
+        if record:
+            e1.record()
+            ev.append((e0, e1))
+        dsim.dsim_argmin(res["makespan"], res["cand_peak"], res["status"], dev.mem_cap_bytes, k, ws, out_idx,
+                         out_mk, found)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    kern_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    # algorithmic bytes per launch: 20 B per op record + 4 B op count per
+    # candidate read; makespan 8 + finish 8*nd + peak 8*nd + cand_peak 8 +
+    # n_ops 8 + status 4 written per candidate
+    per_cand = J * 20 + 4 + 8 + 16 * ND + 8 + 8 + 4
+    algo_bytes = per_cand * N
+    achieved = algo_bytes / (kern_ms * 1e-3) / 1e9
+    src = os.path.join(ROOT, "paper_2111_05426_amd", "csrc", "sim_tables.hip")
+    out = {
+        "metric": METRIC,
+        "value": N * args.steps / dt,
+        "unit": "candidates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": dt / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "random_tables: %d programs x %d ops x %d devices (seed %d), simulate + top-%d"
+                               % (N, J, ND, spec.seed, k),
+                   "n_cand": N, "n_ops": J, "n_dev": ND, "seed": spec.seed, "top_k": k},
+        "ops_per_s": N * J * args.steps / dt,
+        "kernel_ms": kern_ms,
+        "hbm_GBps": achieved,
+        "best": {"index": int(out_idx[0].item()), "makespan_s": float(out_mk[0].item())},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": stored_traffic("k_sim_tables", "random_tables", src),
+                     "kernel": "k_sim_tables<8>", "algorithmic_bytes_per_launch": algo_bytes},
+    }
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="random_tables")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this simulator shards candidates across GPUs by design, but "
+              "multi-GPU runs are not part of this build (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import ALL
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    dsim.lib()
+    W = ALL[args.workload]
+    if args.workload != "random_tables":
+        raise SystemExit("unknown workload for the benchmark line: %s" % args.workload)
+    out = bench_random_tables(args, torch, dsim, W)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_random(W.tables, W.device)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

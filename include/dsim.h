@@ -1,0 +1,236 @@
+/*
+ * dsim.h -- C ABI of the MI355X batched DistIR strategy simulator.
+ *
+ * The operation (Santhanam et al., "DistIR", MLSys 2022):
+ *   A distributed program is a straight-line list of ops over a fixed set of
+ *   single-threaded devices (Sec. 2.1).  An op runs synchronously on its device
+ *   set: it starts when all of them are free and they all finish together; ops
+ *   run in program order.  The simulator (Sec. 3.3) advances each device's
+ *   clock by the op's cost and tracks every device's live memory, a tensor
+ *   being live from its creation until its last use.  Costs (Sec. 3.3, Sec. 4)
+ *   are, with F, B_mem, B_link, lat, launch from dsim_device_model:
+ *     compute      launch + max(flops * (1/F), bytes * (1/B_mem))
+ *     send         lat + bytes * (1/B_link)
+ *     all-reduce   (2(n-1)) * lat + ((2(n-1)) / n) * (bytes * (1/B_link)),
+ *                  0 for n = 1 (ring over the n participants)
+ *   every reciprocal rounded once to fp64; fp64 throughout, no FMA contraction.
+ *   Candidates are a D/T/P/K transform (Sec. 4) of an MLP or GPT-style model
+ *   (T is called H here), or explicit op tables; the grid search (Sec. 5.1,
+ *   5.2) simulates all of them, drops those over the memory cap and ranks
+ *   the rest by predicted time.
+ *
+ * Conventions for every call:
+ *   - Returns a dsim_status: 0 on success, < 0 on an argument or HIP error;
+ *     never throws, never exits.  dsim_last_error() describes the last
+ *     failure of the calling thread.
+ *   - Pointers documented as "device" are HIP device pointers; "host" ones
+ *     are host memory.  The caller owns every buffer; the library keeps no
+ *     allocation between calls.
+ *   - Kernels are enqueued on `hip_stream` (a hipStream_t, NULL = the null
+ *     stream); results are valid once that stream has been synchronised.
+ *   - Arguments are validated on the host before any launch.  Errors inside
+ *     one candidate (an invalid op, a free of more bytes than are live, an
+ *     invalid strategy) never abort: they set bits of that candidate's status
+ *     word, and dsim_argmin skips every candidate whose status is non-zero.
+ *   - Results are deterministic: the same inputs give bit-identical outputs.
+ */
+#ifndef DSIM_H
+#define DSIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DSIM_API __attribute__((visibility("default")))
+
+typedef enum {
+    DSIM_OK = 0,
+    DSIM_EINVAL = -1,   /* invalid argument (null pointer, bad size, bad constant) */
+    DSIM_ERANGE = -2,   /* a size beyond what a format or kernel supports           */
+    DSIM_ENOSPC = -3,   /* an output or workspace buffer is too small               */
+    DSIM_EHIP = -4      /* a HIP runtime call or kernel launch failed               */
+} dsim_status;
+
+/* per-candidate status bits */
+#define DSIM_ST_BAD_OP 1          /* op kind unknown or reserved code bits set          */
+#define DSIM_ST_BAD_DEVICE 2      /* a device id >= n_dev, or an empty device mask      */
+#define DSIM_ST_SELF_SEND 4       /* send with source == destination                    */
+#define DSIM_ST_MEM_UNDERFLOW 8   /* an op frees more bytes than its device holds       */
+#define DSIM_ST_BAD_STRATEGY 16   /* (D,H,P,K) violates the transform's preconditions   */
+#define DSIM_ST_OVER_CAP 32       /* peak above dsim_device_model.mem_cap_bytes (> 0)   */
+
+/* Model families and modes. */
+#define DSIM_MLP 0
+#define DSIM_TRANSFORMER 1
+#define DSIM_INFER 0
+#define DSIM_TRAIN_SGD 1
+#define DSIM_TRAIN_ADAM 2
+#define DSIM_TRAIN_ADAM_MIXED 3   /* fp16 weights and gradients, fp32 master, m, v */
+
+DSIM_API const char *dsim_last_error(void);
+
+/* Device constants of the simulated cluster (Sec. 4: the cost functions'
+ * coefficients are device DRAM bandwidth, kernel launch overhead, network
+ * bandwidth; F is the device's flop rate, Sec. 3.3).  All five doubles must
+ * be finite and > 0 (latency and launch may be 0).  mem_cap_bytes = 0 means
+ * no cap; otherwise candidates whose peak exceeds it get DSIM_ST_OVER_CAP. */
+typedef struct {
+    double flops_per_s, mem_bytes_per_s, link_bytes_per_s, link_latency_s, launch_s;
+    uint64_t mem_cap_bytes;
+} dsim_device_model;
+
+/* The sequential program the transform distributes (Sec. 4, Sec. 5):
+ *   MLP: n_layers square d_model x d_model dense layers (Gemm + Relu, Fig. 2),
+ *        global_batch rows; n_heads, d_ff, seq_len, vocab are ignored.
+ *   TRANSFORMER: GPT-2-shaped decoder; global_batch sequences of seq_len
+ *        tokens, n_heads heads, MLP width d_ff, vocabulary vocab.
+ *   elem_bytes: bytes per weight/activation element (2 or 4). */
+typedef struct {
+    int32_t family, mode, n_layers, n_heads;
+    int64_t d_model, d_ff, seq_len, vocab, global_batch;
+    int32_t elem_bytes;
+} dsim_model;
+
+/* A candidate: data-parallel D, tensor-parallel H (the paper's T), pipeline
+ * P, microbatches K (Sec. 4). */
+typedef struct {
+    int32_t D, H, P, K;
+} dsim_strategy;
+
+/* Grid rule (Sec. 5.1): power-of-two D, H, P with D*H*P <= max_devices
+ * (== if exact_devices); k_mode 0: K in powers of two <= k_max; 1: every
+ * K in 1..k_max; 2 (the paper's rule): K = 1 if P = 1, else powers of two
+ * 2..k_max.  require_k_divides: keep only K | global_batch/D. */
+typedef struct {
+    int32_t max_devices, exact_devices, k_mode, k_max, require_k_divides;
+} dsim_grid_spec;
+
+/*
+ * dsim_create_grid -- enumerate the valid strategies (Sec. 5.1).
+ * Host call.  Writes at most `cap` strategies to the host array `out`
+ * (NULL: count only) and the total count to *n_out.  Order: P outermost,
+ * then K, then H, then D innermost, each ascending.  A strategy is valid
+ * when D | global_batch, K <= global_batch/D, P <= n_layers and H divides
+ * the sharded widths (MLP: d_model; transformer: n_heads, d_model, d_ff),
+ * and, for the MLP with H > 1, every stage holds an even number of layers
+ * (column/row-parallel pairs).  Returns DSIM_ENOSPC if out != NULL and the
+ * count exceeds cap (the first cap entries are still written).
+ */
+DSIM_API dsim_status dsim_create_grid(const dsim_model *model, const dsim_grid_spec *grid,
+                             dsim_strategy *out, int64_t cap, int64_t *n_out);
+
+/*
+ * Explicit op tables (device memory).  Structure of arrays, op-major,
+ * candidate-fastest: the record of op j of candidate c is at j*n_cand + c.
+ *   code:  kind | a << 8 | b_or_mask << 16, bits 24..31 zero.
+ *          kind 0 compute on device a; 1 send a -> b; 2 all-reduce over the
+ *          devices set in the 8-bit mask.
+ *   flops, bytes: fp32 values, promoted exactly to fp64 (flops ignored by
+ *          send and all-reduce).
+ *   alloc_bytes, free_bytes: compute allocates and frees on a; send
+ *          allocates on b and frees on a; all-reduce ignores both.  The
+ *          peak is sampled after the allocation and before the free.
+ *   n_ops: per candidate op count (<= max_ops); NULL = max_ops for all.
+ *   init_live: [n_cand * n_dev] bytes live at t = 0; NULL = zero.
+ *   n_dev: 1..8.
+ * An invalid op is skipped (no time, no memory) and flagged in status.
+ */
+typedef struct {
+    const uint32_t *code;
+    const float *flops, *bytes;
+    const uint32_t *alloc_bytes, *free_bytes;
+    const uint32_t *n_ops;
+    const uint64_t *init_live;
+    int32_t max_ops, n_dev;
+} dsim_tables;
+
+/*
+ * Per-candidate outputs (device memory, caller-allocated, n_cand entries or
+ * n_cand * row_width for the per-device rows; row-major per candidate).
+ *   makespan:  max over devices of the final clock (seconds)
+ *   finish:    per-device final clocks (tables: device d at column d;
+ *              parametric: pipeline stage s at column s -- every replica of
+ *              a stage finishes at the same time); unused columns are 0.
+ *              May be NULL.
+ *   peak:      per-device (per-stage) peak live bytes; may be NULL.
+ *   cand_peak: max over devices of the peak.
+ *   n_ops:     ops of the whole distributed program (each collective and
+ *              each send counted once); may be NULL.
+ *   walked_ops: ops the kernel processed for the candidate; may be NULL.
+ *   status:    DSIM_ST_* bits, 0 = valid.
+ *   row_width: columns of finish/peak (>= n_dev, or >= max P).
+ */
+typedef struct {
+    double *makespan;
+    double *finish;
+    uint64_t *peak;
+    uint64_t *cand_peak;
+    uint64_t *n_ops;
+    uint64_t *walked_ops;
+    int32_t *status;
+    int32_t row_width;
+} dsim_results;
+
+/*
+ * dsim_simulate_tables -- simulate n_cand explicit programs (Sec. 2.1, 3.3).
+ * One GPU lane per candidate walks its ops in order.
+ */
+DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_cand,
+                                 const dsim_device_model *device,
+                                 const dsim_results *results, void *hip_stream);
+
+/*
+ * dsim_simulate_parametric -- simulate the D/H/P/K transform (Sec. 4) of
+ * `model` for n_cand strategies (device array `cand`) without building op
+ * lists: the per-stage 1F1B schedule, layers and ops are expanded on the fly.
+ * Every replica (d, h) of a pipeline stage runs the same ops at the same
+ * times, so one replica per stage is walked; collectives keep their full
+ * group size in the cost.  results.row_width must be >= every candidate's P.
+ * The transform, its memory rules and the per-op FLOP/byte formulas are the
+ * ones documented in DESIGN.md ("The transform").
+ */
+DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strategy *cand,
+                                     int64_t n_cand, const dsim_device_model *device,
+                                     const dsim_results *results, void *hip_stream);
+
+/*
+ * dsim_argmin -- selection of Sec. 5.2 over device arrays of n entries:
+ * feasible = status == 0 and (mem_cap == 0 or cand_peak <= mem_cap); the
+ * feasible entries ranked by (makespan, index) ascending; the first k
+ * (1 <= k <= 64) go to out_idx / out_makespan (device arrays of k entries),
+ * padded with -1 / +inf; *out_found (device) = number written (<= k).
+ * workspace: device buffer of at least dsim_argmin_workspace(n, k) bytes.
+ * makespan values must not be NaN.
+ */
+DSIM_API size_t dsim_argmin_workspace(int64_t n, int32_t k);
+DSIM_API dsim_status dsim_argmin(const double *makespan, const uint64_t *cand_peak, const int32_t *status,
+                        int64_t n, uint64_t mem_cap, int32_t k, void *workspace, size_t ws_bytes,
+                        int64_t *out_idx, double *out_makespan, int32_t *out_found,
+                        void *hip_stream);
+
+/*
+ * dsim_generate_random_tables -- the random-program workload, written in the
+ * dsim_tables layout (device buffers of n_ops * n_cand entries each, plus
+ * n_ops_out[n_cand], which may be NULL).  Bit-reproducible from
+ * (seed, candidate, op): draw f of op j of candidate c is output number
+ * c*2^32 + j*32 + f + 1 of SplitMix64 seeded with `seed`.  Per op: kind 70%
+ * compute / 20% send / 10% all-reduce; compute FLOPs log-uniform in
+ * [1e6, 1e12], bytes log-uniform in [1e3, 1e9]; send to a uniform other
+ * device; all-reduce over a uniform mask of >= 2 devices; every device
+ * keeps up to 16 live buffers of log-uniform sizes in [1e3, 1e9] bytes,
+ * freed in a valid order.  The full definition is in the design doc.
+ * Constraints: 2 <= n_dev <= 8, 0 <= n_ops < 2^27, 0 <= n_cand < 2^32.
+ */
+DSIM_API dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, int32_t n_ops,
+                                        int32_t n_dev, uint32_t *code, float *flops,
+                                        float *bytes, uint32_t *alloc_bytes,
+                                        uint32_t *free_bytes, uint32_t *n_ops_out,
+                                        void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DSIM_H */

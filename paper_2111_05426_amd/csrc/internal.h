@@ -1,0 +1,52 @@
+// internal.h -- declarations shared by the HIP translation units of libdsim.
+//
+// Not part of the ABI.  The public contract is include/dsim.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/dsim.h"
+
+namespace dsim {
+
+// Largest device group of the explicit-table format.
+constexpr int kMaxTableDev = 8;
+
+// Device-model constants as the kernels consume them.  Every reciprocal is
+// rounded once on the host.  For the table format (groups of at most 8) the
+// ring all-reduce terms are tabulated on the host as well:
+//   ar_lat[n]  = (2(n-1)) * lat
+//   ar_coef[n] = (2(n-1)) / n
+// so cost(n, bytes) = ar_lat[n] + ar_coef[n] * (bytes * inv_l).
+struct CostConsts {
+    double inv_f;      // 1 / flops_per_s
+    double inv_b;      // 1 / mem_bytes_per_s
+    double inv_l;      // 1 / link_bytes_per_s
+    double lat;        // link latency
+    double launch;     // per compute op
+    uint64_t cap;      // memory cap, 0 = none
+    double ar_lat[kMaxTableDev + 1];
+    double ar_coef[kMaxTableDev + 1];
+};
+
+CostConsts make_consts(const dsim_device_model &m);
+
+// Error reporting (thread-local message).
+dsim_status fail(dsim_status st, const char *fmt, ...);
+dsim_status hip_fail(hipError_t e, const char *what);
+
+// Kernel launchers (each returns DSIM_OK or DSIM_EHIP).
+dsim_status launch_sim_tables(const dsim_tables &t, int64_t n_cand, const CostConsts &c,
+                              const dsim_results &r, hipStream_t s);
+dsim_status launch_gen_tables(uint64_t seed, int64_t n_cand, int32_t n_ops, int32_t n_dev,
+                              uint32_t *code, float *flops, float *bytes, uint32_t *alloc,
+                              uint32_t *freeb, uint32_t *n_ops_out, hipStream_t s);
+size_t argmin_workspace(int64_t n, int32_t k);
+dsim_status launch_argmin(const double *mk, const uint64_t *pk, const int32_t *st, int64_t n,
+                          uint64_t cap, int32_t k, void *ws, int64_t *out_idx, double *out_mk,
+                          int32_t *out_found, hipStream_t s);
+dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand,
+                              const CostConsts &c, const dsim_results &r, hipStream_t s);
+
+}  // namespace dsim

@@ -1,0 +1,231 @@
+"""Python binding of libdsim (include/dsim.h): argument marshalling only.
+
+Every function carries the C entry point's name and forwards to it through
+ctypes; all simulation work runs in the HIP kernels of libdsim.so.  PyTorch
+supplies device memory and the HIP stream.  There is no fallback: if the
+library is missing or a call fails, an exception is raised.
+"""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdsim.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "dsim.h")
+
+DSIM_OK, DSIM_EINVAL, DSIM_ERANGE, DSIM_ENOSPC, DSIM_EHIP = 0, -1, -2, -3, -4
+ST_BAD_OP, ST_BAD_DEVICE, ST_SELF_SEND, ST_MEM_UNDERFLOW, ST_BAD_STRATEGY, ST_OVER_CAP = 1, 2, 4, 8, 16, 32
+
+
+class DsimError(RuntimeError):
+    def __init__(self, fn, code, msg):
+        super().__init__("%s failed (%d): %s" % (fn, code, msg))
+        self.code = code
+
+
+class dsim_device_model(C.Structure):
+    _fields_ = [("flops_per_s", C.c_double), ("mem_bytes_per_s", C.c_double),
+                ("link_bytes_per_s", C.c_double), ("link_latency_s", C.c_double),
+                ("launch_s", C.c_double), ("mem_cap_bytes", C.c_uint64)]
+
+
+class dsim_model(C.Structure):
+    _fields_ = [("family", C.c_int32), ("mode", C.c_int32), ("n_layers", C.c_int32),
+                ("n_heads", C.c_int32), ("d_model", C.c_int64), ("d_ff", C.c_int64),
+                ("seq_len", C.c_int64), ("vocab", C.c_int64), ("global_batch", C.c_int64),
+                ("elem_bytes", C.c_int32)]
+
+
+class dsim_strategy(C.Structure):
+    _fields_ = [("D", C.c_int32), ("H", C.c_int32), ("P", C.c_int32), ("K", C.c_int32)]
+
+
+class dsim_grid_spec(C.Structure):
+    _fields_ = [("max_devices", C.c_int32), ("exact_devices", C.c_int32), ("k_mode", C.c_int32),
+                ("k_max", C.c_int32), ("require_k_divides", C.c_int32)]
+
+
+class dsim_tables(C.Structure):
+    _fields_ = [("code", C.c_void_p), ("flops", C.c_void_p), ("bytes", C.c_void_p),
+                ("alloc_bytes", C.c_void_p), ("free_bytes", C.c_void_p), ("n_ops", C.c_void_p),
+                ("init_live", C.c_void_p), ("max_ops", C.c_int32), ("n_dev", C.c_int32)]
+
+
+class dsim_results(C.Structure):
+    _fields_ = [("makespan", C.c_void_p), ("finish", C.c_void_p), ("peak", C.c_void_p),
+                ("cand_peak", C.c_void_p), ("n_ops", C.c_void_p), ("walked_ops", C.c_void_p),
+                ("status", C.c_void_p), ("row_width", C.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libdsim.so; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libdsim.so is not built (run python -m paper_2111_05426_amd.build)")
+        L = C.CDLL(LIB_PATH)
+        L.dsim_last_error.restype = C.c_char_p
+        L.dsim_create_grid.argtypes = [C.POINTER(dsim_model), C.POINTER(dsim_grid_spec), C.c_void_p,
+                                       C.c_int64, C.POINTER(C.c_int64)]
+        L.dsim_simulate_tables.argtypes = [C.POINTER(dsim_tables), C.c_int64, C.POINTER(dsim_device_model),
+                                           C.POINTER(dsim_results), C.c_void_p]
+        L.dsim_simulate_parametric.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64,
+                                               C.POINTER(dsim_device_model), C.POINTER(dsim_results),
+                                               C.c_void_p]
+        L.dsim_argmin_workspace.restype = C.c_size_t
+        L.dsim_argmin_workspace.argtypes = [C.c_int64, C.c_int32]
+        L.dsim_argmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_uint64, C.c_int32,
+                                  C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.dsim_generate_random_tables.argtypes = [C.c_uint64, C.c_int64, C.c_int32, C.c_int32] + \
+            [C.c_void_p] * 7
+        for name in ("dsim_create_grid", "dsim_simulate_tables", "dsim_simulate_parametric", "dsim_argmin",
+                     "dsim_generate_random_tables"):
+            getattr(L, name).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def header_functions():
+    """Names of the functions include/dsim.h declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    return re.findall(r"DSIM_API\s+[\w\s\*]*?\b(dsim_\w+)\s*\(", text)
+
+
+def dsim_last_error():
+    return lib().dsim_last_error().decode()
+
+
+def _check(fn, rc):
+    if rc != 0:
+        raise DsimError(fn, rc, dsim_last_error())
+
+
+def _ptr(t):
+    """Device (or host) address of a tensor / ndarray, None for None."""
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def device_model(spec):
+    return dsim_device_model(spec.flops_per_s, spec.mem_bytes_per_s, spec.link_bytes_per_s,
+                             spec.link_latency_s, spec.launch_s, int(spec.mem_cap_bytes))
+
+
+def model_struct(spec):
+    return dsim_model(spec.family, spec.mode, spec.n_layers, spec.n_heads, spec.d_model, spec.d_ff,
+                      spec.seq_len, spec.vocab, spec.global_batch, spec.elem_bytes)
+
+
+def dsim_create_grid(model, grid):
+    """Host call: the valid strategies as an (n, 4) int32 array (D, H, P, K)."""
+    m = model_struct(model)
+    g = dsim_grid_spec(grid.max_devices, grid.exact_devices, grid.k_mode, grid.k_max, grid.require_k_divides)
+    n = C.c_int64()
+    _check("dsim_create_grid", lib().dsim_create_grid(C.byref(m), C.byref(g), None, 0, C.byref(n)))
+    out = np.zeros((max(n.value, 1), 4), np.int32)
+    _check("dsim_create_grid", lib().dsim_create_grid(C.byref(m), C.byref(g), out.ctypes.data, n.value,
+                                                      C.byref(n)))
+    return out[:n.value]
+
+
+def alloc_results(n, row_width, device="cuda"):
+    """Caller-owned output buffers (torch tensors)."""
+    import torch
+    return dict(makespan=torch.empty(n, dtype=torch.float64, device=device),
+                finish=torch.empty((n, row_width), dtype=torch.float64, device=device),
+                peak=torch.empty((n, row_width), dtype=torch.int64, device=device),
+                cand_peak=torch.empty(n, dtype=torch.int64, device=device),
+                n_ops=torch.empty(n, dtype=torch.int64, device=device),
+                walked_ops=torch.empty(n, dtype=torch.int64, device=device),
+                status=torch.empty(n, dtype=torch.int32, device=device),
+                row_width=row_width)
+
+
+def _results(r):
+    return dsim_results(_ptr(r.get("makespan")), _ptr(r.get("finish")), _ptr(r.get("peak")),
+                        _ptr(r.get("cand_peak")), _ptr(r.get("n_ops")), _ptr(r.get("walked_ops")),
+                        _ptr(r.get("status")), int(r.get("row_width", 0)))
+
+
+def alloc_tables(n_cand, max_ops, device="cuda"):
+    import torch
+    shape = (max_ops, n_cand)
+    return dict(code=torch.empty(shape, dtype=torch.int32, device=device),
+                flops=torch.empty(shape, dtype=torch.float32, device=device),
+                bytes=torch.empty(shape, dtype=torch.float32, device=device),
+                alloc=torch.empty(shape, dtype=torch.int32, device=device),
+                free=torch.empty(shape, dtype=torch.int32, device=device),
+                n_ops=torch.empty(n_cand, dtype=torch.int32, device=device))
+
+
+def dsim_simulate_tables(tables, n_cand, n_dev, device, results, init_live=None, stream=None):
+    """tables: dict of device tensors shaped (max_ops, n_cand) (code/alloc/free
+    as int32 bit patterns of the uint32 fields), optional n_ops (n_cand,)."""
+    max_ops = int(tables["code"].shape[0]) if tables["code"].dim() == 2 else int(tables["max_ops"])
+    t = dsim_tables(_ptr(tables["code"]), _ptr(tables["flops"]), _ptr(tables["bytes"]), _ptr(tables["alloc"]),
+                    _ptr(tables["free"]), _ptr(tables.get("n_ops")), _ptr(init_live), max_ops, n_dev)
+    d = device_model(device)
+    r = _results(results)
+    _check("dsim_simulate_tables",
+           lib().dsim_simulate_tables(C.byref(t), n_cand, C.byref(d), C.byref(r), _stream(stream)))
+
+
+def dsim_simulate_parametric(model, cand, device, results, stream=None):
+    """cand: device int32 tensor (n, 4) of (D, H, P, K)."""
+    m = model_struct(model)
+    d = device_model(device)
+    r = _results(results)
+    _check("dsim_simulate_parametric",
+           lib().dsim_simulate_parametric(C.byref(m), _ptr(cand), int(cand.shape[0]), C.byref(d), C.byref(r),
+                                          _stream(stream)))
+
+
+def dsim_argmin_workspace(n, k):
+    return int(lib().dsim_argmin_workspace(n, k))
+
+
+def dsim_argmin(makespan, cand_peak, status, mem_cap, k, workspace, out_idx, out_makespan, out_found,
+                stream=None):
+    n = int(makespan.shape[0])
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("dsim_argmin",
+           lib().dsim_argmin(_ptr(makespan), _ptr(cand_peak), _ptr(status), n, int(mem_cap), int(k),
+                             _ptr(workspace), ws_bytes, _ptr(out_idx), _ptr(out_makespan), _ptr(out_found),
+                             _stream(stream)))
+
+
+def dsim_generate_random_tables(seed, n_cand, n_ops, n_dev, tables, stream=None):
+    _check("dsim_generate_random_tables",
+           lib().dsim_generate_random_tables(seed, n_cand, n_ops, n_dev, _ptr(tables["code"]),
+                                             _ptr(tables["flops"]), _ptr(tables["bytes"]),
+                                             _ptr(tables["alloc"]), _ptr(tables["free"]),
+                                             _ptr(tables.get("n_ops")), _stream(stream)))
+
+
+def select_topk(makespan, cand_peak, status, mem_cap, k, stream=None):
+    """Convenience: allocate workspace/outputs with torch, run dsim_argmin."""
+    import torch
+    dev = makespan.device
+    n = int(makespan.shape[0])
+    ws = torch.empty(max(dsim_argmin_workspace(n, k), 16), dtype=torch.uint8, device=dev)
+    idx = torch.empty(k, dtype=torch.int64, device=dev)
+    mk = torch.empty(k, dtype=torch.float64, device=dev)
+    found = torch.empty(1, dtype=torch.int32, device=dev)
+    dsim_argmin(makespan, cand_peak, status, mem_cap, k, ws, idx, mk, found, stream=stream)
+    return idx, mk, found

@@ -1,0 +1,92 @@
+"""The C ABI on the host: library loads, exports what include/dsim.h
+declares, enumerates the grid like the oracle, and rejects bad arguments
+before any launch (none of these calls touches a GPU)."""
+import ctypes as C
+
+import numpy as np
+import pytest
+
+from paper_2111_05426_amd import dsim
+from paper_2111_05426_amd.workloads import (ALL, DeviceSpec, GridSpec, INFER, TRAIN_SGD, mlp, transformer)
+
+
+def test_exports_every_declared_function():
+    names = dsim.header_functions()
+    assert set(names) == {"dsim_last_error", "dsim_create_grid", "dsim_simulate_tables",
+                          "dsim_simulate_parametric", "dsim_argmin_workspace", "dsim_argmin",
+                          "dsim_generate_random_tables"}
+    L = dsim.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+GRIDS = [(w.model, w.grid) for w in ALL.values() if w.model is not None] + [
+    (mlp(16, 8192, 65536, 2, TRAIN_SGD), GridSpec(16, 1, 2, 128)),
+    (transformer(24, 2048, 16, 1024, 50257, 128, 2, INFER), GridSpec(16, 1, 2, 128)),
+    (mlp(6, 96, 60, 4, TRAIN_SGD), GridSpec(32, 0, 1, 40, 1)),
+    (transformer(10, 60, 6, 16, 77, 36, 2, INFER), GridSpec(64, 0, 0, 64)),
+]
+
+
+@pytest.mark.parametrize("i", range(len(GRIDS)))
+def test_grid_matches_oracle(orc, i):
+    model, grid = GRIDS[i]
+    a = dsim.dsim_create_grid(model, grid)
+    b = orc.create_grid(model, grid)
+    assert np.array_equal(a, b)
+
+
+def test_grid_enospc():
+    m, g = GRIDS[0]
+    L = dsim.lib()
+    out = np.zeros((3, 4), np.int32)
+    n = C.c_int64()
+    mm, gg = dsim.model_struct(m), dsim.dsim_grid_spec(g.max_devices, g.exact_devices, g.k_mode, g.k_max, 0)
+    rc = L.dsim_create_grid(C.byref(mm), C.byref(gg), out.ctypes.data, 3, C.byref(n))
+    assert rc == dsim.DSIM_ENOSPC and n.value > 3
+    assert "cap" in dsim.dsim_last_error()
+
+
+def _err(fn):
+    with pytest.raises(dsim.DsimError) as e:
+        fn()
+    return e.value.code
+
+
+def test_argument_errors_before_launch():
+    L = dsim.lib()
+    dev = dsim.device_model(DeviceSpec())
+    res = dsim.dsim_results()
+    tab = dsim.dsim_tables()
+    tab.n_dev, tab.max_ops = 9, 4
+    assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(dev), C.byref(res), None) == dsim.DSIM_ERANGE
+    tab.n_dev = 0
+    assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(dev), C.byref(res), None) == dsim.DSIM_ERANGE
+    tab.n_dev = 4
+    assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert L.dsim_simulate_tables(C.byref(tab), 10, None, C.byref(res), None) == dsim.DSIM_EINVAL
+    bad = dsim.device_model(DeviceSpec(flops_per_s=0.0))
+    assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
+    bad = dsim.device_model(DeviceSpec(link_latency_s=float("nan")))
+    assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
+    # n_cand == 0 is a no-op
+    assert L.dsim_simulate_tables(C.byref(tab), 0, C.byref(dev), C.byref(res), None) == dsim.DSIM_OK
+    # argmin
+    assert L.dsim_argmin(None, None, None, 0, 0, 0, None, 0, None, None, None, None) == dsim.DSIM_ERANGE
+    assert L.dsim_argmin(None, None, None, 0, 0, 65, None, 0, None, None, None, None) == dsim.DSIM_ERANGE
+    assert dsim.dsim_argmin_workspace(10, 0) == 0 and dsim.dsim_argmin_workspace(10 ** 6, 16) > 0
+    # generator limits
+    for nd in (1, 9):
+        assert L.dsim_generate_random_tables(0, 10, 10, nd, *([None] * 7)) == dsim.DSIM_ERANGE
+    assert L.dsim_generate_random_tables(0, 10, 1 << 27, 8, *([None] * 7)) == dsim.DSIM_ERANGE
+    assert L.dsim_generate_random_tables(0, 10, 10, 8, *([None] * 7)) == dsim.DSIM_EINVAL
+    # parametric: bad model / NULL candidates
+    m = dsim.model_struct(ALL["tiny_mlp"].model)
+    m.family = 7
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    m = dsim.model_struct(ALL["gpt2_small"].model)
+    m.d_model = 770
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    m = dsim.model_struct(ALL["gpt2_small"].model)
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert "NULL" in dsim.dsim_last_error()

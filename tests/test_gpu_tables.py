@@ -1,0 +1,228 @@
+"""GPU parity: table simulator, random-table generator and top-k selection
+against the CPU oracle, element by element on the same seeded inputs.
+
+Bar: integer outputs (peaks, status, op counts, indices, generated tables)
+bit-exact; fp64 times within 1e-12 relative (both sides evaluate the same
+IEEE expressions in the same order with contraction off, so they are
+expected to be equal bit for bit, and the tests also record that).
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+REL = 1e-12
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    from paper_2111_05426_amd import dsim
+    dsim.lib()
+    return torch
+
+
+def assert_times(gpu, ref):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    np.testing.assert_allclose(gpu, ref, rtol=REL, atol=0)
+    assert np.array_equal(gpu, ref), "times agree to 1e-12 but not bit for bit"
+
+
+def random_tables(rng, n_cand, max_ops, n_dev, bad=False):
+    """Seeded synthetic tables with every op kind; bad=True also plants
+    invalid ops and frees larger than the live bytes."""
+    kind = rng.choice(3, size=(max_ops, n_cand), p=[0.7, 0.2, 0.1]).astype(np.uint32)
+    a = rng.integers(0, n_dev, (max_ops, n_cand)).astype(np.uint32)
+    b = rng.integers(0, n_dev, (max_ops, n_cand)).astype(np.uint32)
+    if n_dev > 1:
+        b = np.where(b == a, (a + 1) % n_dev, b)
+    mask = rng.integers(1, 1 << n_dev, (max_ops, n_cand)).astype(np.uint32)
+    code = np.where(kind == 2, 2 | (mask << 16), kind | (a << 8) | (b << 16)).astype(np.uint32)
+    if n_dev == 1:
+        code = np.where(kind == 1, 0, code).astype(np.uint32)
+    alloc = rng.integers(0, 5000, (max_ops, n_cand)).astype(np.uint32)
+    free = rng.integers(0, 3000, (max_ops, n_cand)).astype(np.uint32)
+    if bad:
+        sel = rng.random((max_ops, n_cand)) < 0.002
+        code = np.where(sel, rng.integers(0, 1 << 32, (max_ops, n_cand), dtype=np.uint64).astype(np.uint32), code)
+        free = np.where(rng.random((max_ops, n_cand)) < 0.01, 10 ** 6, free).astype(np.uint32)
+    else:
+        free = np.minimum(free, alloc)
+    fl = np.exp(rng.uniform(np.log(1e6), np.log(1e12), (max_ops, n_cand))).astype(np.float32)
+    by = np.exp(rng.uniform(np.log(1e3), np.log(1e9), (max_ops, n_cand))).astype(np.float32)
+    n_ops = rng.integers(0, max_ops + 1, n_cand).astype(np.uint32)
+    n_ops[:3] = [0, max_ops, 1][:min(3, n_cand)] if n_cand >= 3 else n_ops[:3]
+    init = rng.integers(0, 10 ** 5, (n_cand, n_dev)).astype(np.uint64)
+    return dict(code=code, flops=fl, bytes=by, alloc=alloc, free=free, n_ops=n_ops, init=init)
+
+
+def to_gpu(torch, t):
+    g = {}
+    for k in ("code", "alloc", "free", "n_ops"):
+        g[k] = torch.from_numpy(t[k].view(np.int32)).cuda()
+    for k in ("flops", "bytes"):
+        g[k] = torch.from_numpy(t[k]).cuda()
+    return g
+
+
+def results_np(r):
+    out = {}
+    for k, v in r.items():
+        if k == "row_width":
+            continue
+        out[k] = v.cpu().numpy()
+    return out
+
+
+@pytest.mark.parametrize("n_dev", [1, 2, 3, 5, 8])
+@pytest.mark.parametrize("bad", [False, True])
+def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad):
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import DeviceSpec
+    torch = torch_gpu
+    rng = np.random.default_rng(1000 + n_dev + 17 * bad)
+    n_cand, max_ops = 777, 301   # several 256-lane blocks and a ragged tail
+    t = random_tables(rng, n_cand, max_ops, n_dev, bad)
+    dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5)
+    g = to_gpu(torch, t)
+    init = torch.from_numpy(t["init"].view(np.int64)).cuda()
+    rw = n_dev + 2
+    r = dsim.alloc_results(n_cand, rw)
+    dsim.dsim_simulate_tables(g, n_cand, n_dev, dev, r, init_live=init)
+    torch.cuda.synchronize()
+    R = results_np(r)
+    mk, fin, pk, cp, st = [], [], [], [], []
+    for c in range(n_cand):
+        n = int(t["n_ops"][c])
+        tab = {k: t[k][:n, c] for k in ("code", "flops", "bytes", "alloc", "free")}
+        o = orc.sim_table(tab, n_dev, dev, init_live=t["init"][c])
+        mk.append(o["makespan"]); fin.append(o["finish"]); pk.append(o["peak"])
+        cp.append(o["cand_peak"]); st.append(o["status"])
+    assert_times(R["makespan"], mk)
+    assert_times(R["finish"][:, :n_dev], np.array(fin))
+    assert np.all(R["finish"][:, n_dev:] == 0)
+    assert np.array_equal(R["peak"][:, :n_dev].view(np.uint64), np.array(pk, np.uint64))
+    assert np.array_equal(R["cand_peak"].view(np.uint64), np.array(cp, np.uint64))
+    assert np.array_equal(R["status"], np.array(st, np.int32))
+    assert np.array_equal(R["n_ops"], t["n_ops"].astype(np.int64))
+    if bad:
+        assert np.any(R["status"] & dsim.ST_MEM_UNDERFLOW)
+
+
+def gen_gpu(torch, seed, n_cand, n_ops, n_dev):
+    from paper_2111_05426_amd import dsim
+    g = dsim.alloc_tables(n_cand, n_ops)
+    dsim.dsim_generate_random_tables(seed, n_cand, n_ops, n_dev, g)
+    return g
+
+
+@pytest.mark.parametrize("n_dev", [2, 5, 8])
+def test_generator_bit_exact(torch_gpu, orc, n_dev):
+    torch = torch_gpu
+    n_cand, n_ops = 700, 513
+    g = gen_gpu(torch, 11 + n_dev, n_cand, n_ops, n_dev)
+    torch.cuda.synchronize()
+    G = {k: v.cpu().numpy() for k, v in g.items()}
+    for c in range(n_cand):
+        o = orc.gen_table(11 + n_dev, c, n_ops, n_dev)
+        for k, gk in (("code", "code"), ("alloc", "alloc"), ("free", "free")):
+            assert np.array_equal(G[gk][:, c].view(np.uint32), o[k]), (c, k)
+        for k in ("flops", "bytes"):
+            assert np.array_equal(G[k][:, c].view(np.uint32), o[k].view(np.uint32)), (c, k)
+    assert np.all(G["n_ops"] == n_ops)
+
+
+def test_generated_tables_simulate_vs_oracle(torch_gpu, orc):
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import DeviceSpec
+    torch = torch_gpu
+    n_cand, n_ops, n_dev = 3000, 2048, 8
+    dev = DeviceSpec()
+    g = gen_gpu(torch, 0, n_cand, n_ops, n_dev)
+    r = dsim.alloc_results(n_cand, n_dev)
+    dsim.dsim_simulate_tables(g, n_cand, n_dev, dev, r)
+    torch.cuda.synchronize()
+    R = results_np(r)
+    o = orc.run_random_tables(0, n_ops, n_dev, np.arange(n_cand), dev, threads=8)
+    assert_times(R["makespan"], o["makespan"])
+    assert_times(R["finish"], o["finish"])
+    assert np.array_equal(R["peak"].view(np.uint64), o["peak"])
+    assert np.array_equal(R["cand_peak"].view(np.uint64), o["cand_peak"])
+    assert np.array_equal(R["status"], o["status"])
+    assert np.all(R["status"] == 0)
+
+
+def test_random_tables_full_size_sampled(torch_gpu, orc):
+    """The measured workload at its full size, in the launch configuration the
+    benchmark times: 1,000,000 candidates x 2,048 ops x 8 devices.  Sampled
+    candidates are checked one by one; the top-1 over all of them is checked
+    against the oracle's top-1 over the same simulated values' ordering."""
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import RANDOM_TABLES
+    torch = torch_gpu
+    spec = RANDOM_TABLES.tables
+    dev = RANDOM_TABLES.device
+    print("full-size random tables: generating", flush=True)
+    g = gen_gpu(torch, spec.seed, spec.n_cand, spec.n_ops, spec.n_dev)
+    r = dsim.alloc_results(spec.n_cand, spec.n_dev)
+    dsim.dsim_simulate_tables(g, spec.n_cand, spec.n_dev, dev, r)
+    idx, mk, found = dsim.select_topk(r["makespan"], r["cand_peak"], r["status"], 0, 4)
+    torch.cuda.synchronize()
+    print("full-size random tables: simulated", flush=True)
+    rng = np.random.default_rng(5)
+    sample = np.unique(np.concatenate([rng.integers(0, spec.n_cand, 1500), [0, spec.n_cand - 1],
+                                       idx.cpu().numpy()]))
+    s_t = torch.from_numpy(sample).cuda()
+    o = orc.run_random_tables(spec.seed, spec.n_ops, spec.n_dev, sample, dev, threads=8)
+    assert_times(r["makespan"][s_t].cpu().numpy(), o["makespan"])
+    assert_times(r["finish"][s_t].cpu().numpy(), o["finish"])
+    assert np.array_equal(r["peak"][s_t].cpu().numpy().view(np.uint64), o["peak"])
+    assert np.array_equal(r["status"][s_t].cpu().numpy(), o["status"])
+    # generator: sampled columns bit-exact
+    for c in sample[:40]:
+        ref = orc.gen_table(spec.seed, int(c), spec.n_ops, spec.n_dev)
+        assert np.array_equal(g["code"][:, int(c)].cpu().numpy().view(np.uint32), ref["code"])
+        assert np.array_equal(g["bytes"][:, int(c)].cpu().numpy().view(np.uint32), ref["bytes"].view(np.uint32))
+        assert np.array_equal(g["alloc"][:, int(c)].cpu().numpy().view(np.uint32), ref["alloc"])
+    # selection over the million: ranks are consistent with the simulated values
+    mk_all = r["makespan"].cpu().numpy()
+    order = np.lexsort((np.arange(spec.n_cand), mk_all))[:4]
+    assert int(found.item()) == 4
+    assert np.array_equal(idx.cpu().numpy(), order)
+    assert_times(mk.cpu().numpy(), mk_all[order])
+
+
+@pytest.mark.parametrize("n", [0, 1, 255, 4097, 100_003, 1_000_000])
+@pytest.mark.parametrize("k", [1, 5, 16, 64])
+def test_argmin_vs_oracle(torch_gpu, orc, n, k):
+    from paper_2111_05426_amd import dsim
+    torch = torch_gpu
+    rng = np.random.default_rng(n * 7 + k)
+    mk = np.round(rng.uniform(0, 5, n), 2 if n > 1000 else 1)   # many exact ties
+    pk = rng.integers(0, 1000, n).astype(np.uint64)
+    st = np.where(rng.random(n) < 0.2, 8, 0).astype(np.int32)
+    for cap in (0, 500):
+        idx, mo, found = dsim.select_topk(torch.from_numpy(mk).cuda(), torch.from_numpy(pk.view(np.int64)).cuda(),
+                                          torch.from_numpy(st).cuda(), cap, k)
+        torch.cuda.synchronize()
+        ri, rm, rf = orc.topk(mk, pk, st, cap, k)
+        assert int(found.item()) == rf
+        assert np.array_equal(idx.cpu().numpy(), ri)
+        assert np.array_equal(mo.cpu().numpy(), rm)
+
+
+def test_empty_inputs(torch_gpu):
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import DeviceSpec
+    torch = torch_gpu
+    g = dsim.alloc_tables(0, 16)
+    r = dsim.alloc_results(0, 8)
+    dsim.dsim_simulate_tables(g, 0, 8, DeviceSpec(), r)
+    g = dsim.alloc_tables(5, 0)
+    r = dsim.alloc_results(5, 8)
+    dsim.dsim_generate_random_tables(0, 5, 0, 8, g)
+    dsim.dsim_simulate_tables(g, 5, 8, DeviceSpec(), r)
+    torch.cuda.synchronize()
+    assert np.all(r["makespan"].cpu().numpy() == 0) and np.all(r["status"].cpu().numpy() == 0)
