@@ -53,14 +53,17 @@ def cpu_baseline_random(spec, dev, budget_s=12.0):
     chunk = 2048 * threads // 8
     done, t0 = 0, time.perf_counter()
     stride = 997
-    while time.perf_counter() - t0 < budget_s:
-        cands = (np.arange(done, done + chunk, dtype=np.int64) * stride) % spec.n_cand
+    # 997 is prime and does not divide n_cand, so the sample holds distinct candidates
+    while time.perf_counter() - t0 < budget_s and done < spec.n_cand:
+        n = min(chunk, spec.n_cand - done)
+        cands = (np.arange(done, done + n, dtype=np.int64) * stride) % spec.n_cand
         oracle.run_random_tables(spec.seed, spec.n_ops, spec.n_dev, cands, dev, threads=threads, want_rows=False)
-        done += chunk
+        done += n
     dt = time.perf_counter() - t0
     return {"value": done / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
-            "sample": "%d candidates (stride 997 over the 1,000,000) x %d ops x %d devices, generated and "
-                      "simulated by the C oracle in %.1f s on %d threads" % (done, spec.n_ops, spec.n_dev, dt, threads),
+            "sample": "%d distinct candidates (index i*997 mod %d) of the %d x %d ops x %d devices workload, "
+                      "generated and simulated by the C oracle in %.1f s on %d threads"
+                      % (done, spec.n_cand, spec.n_cand, spec.n_ops, spec.n_dev, dt, threads),
             "ops_per_s": done * spec.n_ops / dt}
 
 
@@ -131,6 +134,24 @@ def bench_random_tables(args, torch, dsim, W):
     return out
 
 
+def copy_calibration(torch, nbytes=4 << 30, reps=5):
+    """A plain device-to-device copy of known size: its time gives the
+    achievable streaming bandwidth; under rocprofv3 --pmc its FETCH_SIZE and
+    WRITE_SIZE calibrate the counters (it reads and writes nbytes)."""
+    a = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"bytes_read": nbytes, "bytes_written": nbytes, "ms": ms, "GBps": 2 * nbytes / (ms * 1e-3) / 1e9}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -138,6 +159,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="random_tables")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also time a plain 4 GiB device-to-device copy (counter and bandwidth calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this simulator shards candidates across GPUs by design, but "
@@ -154,6 +177,8 @@ def main():
     if args.workload != "random_tables":
         raise SystemExit("unknown workload for the benchmark line: %s" % args.workload)
     out = bench_random_tables(args, torch, dsim, W)
+    if args.copy_calibration:
+        out["copy_calibration"] = copy_calibration(torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_random(W.tables, W.device)
     print(json.dumps(out), flush=True)

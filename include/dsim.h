@@ -55,7 +55,8 @@ typedef enum {
 } dsim_status;
 
 /* per-candidate status bits */
-#define DSIM_ST_BAD_OP 1          /* op kind unknown or reserved code bits set          */
+#define DSIM_ST_BAD_OP 1          /* op kind unknown, reserved code bits set, or flops /
+                                     bytes not finite and >= 0                          */
 #define DSIM_ST_BAD_DEVICE 2      /* a device id >= n_dev, or an empty device mask      */
 #define DSIM_ST_SELF_SEND 4       /* send with source == destination                    */
 #define DSIM_ST_MEM_UNDERFLOW 8   /* an op frees more bytes than its device holds       */
@@ -129,7 +130,9 @@ DSIM_API dsim_status dsim_create_grid(const dsim_model *model, const dsim_grid_s
  *          kind 0 compute on device a; 1 send a -> b; 2 all-reduce over the
  *          devices set in the 8-bit mask.
  *   flops, bytes: fp32 values, promoted exactly to fp64 (flops ignored by
- *          send and all-reduce).
+ *          send and all-reduce); both must be finite and >= 0 (-0.0, NaN,
+ *          infinities and negative values make the op invalid), so that no
+ *          cost is negative or NaN.
  *   alloc_bytes, free_bytes: compute allocates and frees on a; send
  *          allocates on b and frees on a; all-reduce ignores both.  The
  *          peak is sampled after the allocation and before the free.

@@ -120,7 +120,8 @@ double or_cost(const or_device_model *m, int kind, double flops, double bytes, i
 
 /* ------------------------------------------------------------------------ */
 /* Explicit op tables (at most 8 devices): one candidate, per-op amounts.    */
-/* code = kind | a << 8 | b_or_mask << 16; bits 24..31 must be zero.         */
+/* code = kind | a << 8 | b_or_mask << 16; bits 24..31 must be zero; flops  */
+/* and bytes must be finite and >= 0 (costs are then never negative).       */
 /* compute: runs on a, allocates and frees on a.                             */
 /* send a->b: runs on {a,b}, allocates on b, frees on a.                     */
 /* allreduce: runs on the devices of the mask; alloc/free fields ignored.    */
@@ -150,7 +151,15 @@ int or_sim_table(int64_t n_ops, int n_dev,
         int kind = (int)(c & 0xffu), a = (int)((c >> 8) & 0xffu), b = (int)((c >> 16) & 0xffu);
         uint32_t mask;
         double start, end, cost;
-        if ((c >> 24) != 0 || kind > 2) { st |= ST_BAD_OP; continue; }
+        {
+            uint32_t fb, bb;
+            memcpy(&fb, &flops[o], 4);
+            memcpy(&bb, &bytes[o], 4);
+            if ((c >> 24) != 0 || kind > 2 || fb >= 0x7f800000u || bb >= 0x7f800000u) {
+                st |= ST_BAD_OP;
+                continue;
+            }
+        }
         if (kind == OR_COMPUTE) {
             if (a >= n_dev) { st |= ST_BAD_DEVICE; continue; }
             mask = 1u << a;

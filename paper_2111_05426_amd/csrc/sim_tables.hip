@@ -7,22 +7,33 @@
 //
 // Layout: the tables are op-major and candidate-fastest, so at every step the
 // 64 lanes of a wavefront read 64 consecutive records of each field (five
-// coalesced 256-byte loads per op).  The record stream is read once, with
-// non-temporal loads, `kUnroll` ops ahead of the arithmetic.
+// coalesced 256-byte loads per op).  The record stream is read once with
+// non-temporal raw buffer loads: one descriptor per field and group of ops,
+// based at the workgroup's first record, so the per-lane address is a 32-bit
+// byte offset and no lane does 64-bit address arithmetic.  Two register sets
+// of kUnroll ops alternate: one is processed while the other is in flight.
 //
 // Per-lane state: the device clocks live in VGPRs (n_dev <= 8 fp64) and are
-// selected with the op's device mask, so an op touching any subset of devices
-// costs the same branch-free instruction sequence; the per-device live and
-// peak byte counters are indexed by a per-lane device id and live in LDS,
+// combined with the op's device mask as 1.0/0.0 factors, so an op touching any
+// subset of devices runs the same branch-free sequence; the per-device live
+// and peak byte counters are indexed by a per-lane device id and live in LDS,
 // laid out [device][lane] so that the 64 lanes of a wavefront always hit 64
 // distinct 8-byte words.
+//
+// The kernel is bound by the op stream's HBM bandwidth once the per-op work
+// is short: it has a fast path for the ops every lane of a wavefront has,
+// which assumes valid ops (indices clamped, so even an invalid op stays in
+// bounds) and only tests whether each op is valid; a lane that meets an op it
+// cannot vouch for, and every lane's ops past the wavefront's common count,
+// go through the exact per-op path below it.
 #include "internal.h"
 
 namespace dsim {
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kUnroll = 4;
+constexpr int kBlock = 256;       // 4 wavefronts; 32 KB of LDS counters
+constexpr int kWavesPerSimd = 4;
+constexpr int kUnroll = 2;   // ops per register set; two sets in flight
 
 struct TabArgs {
     const uint32_t *code;
@@ -45,42 +56,72 @@ struct TabArgs {
     CostConsts c;
 };
 
-template <typename T>
-__device__ __forceinline__ T stream_load(const T *p)
+// Buffer resource covering one workgroup's 64 consecutive 4-byte records of
+// one op row (raw buffer, gfx9 descriptor word 3); the base is wave-uniform,
+// so the per-lane address is just a 32-bit byte offset.
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kNonTemporal = 2;   // streamed once: do not keep in the caches
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t group_rsrc(const void *base, uint32_t bytes)
 {
-    return __builtin_nontemporal_load(p);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
+__device__ __forceinline__ double bits_double(uint32_t lo, uint32_t hi)
+{
+    return __hiloint2double((int)hi, (int)lo);
+}
+
+// Status bits of one op, exactly as the table format defines validity.
+template <int ND>
+__device__ __forceinline__ uint32_t op_flags(uint32_t code, uint32_t flops_bits, uint32_t bytes_bits)
+{
+    const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
+    // kind, reserved bits, and flops/bytes finite and >= 0 (bit patterns
+    // below +inf)
+    if ((code >> 24) != 0u || kind > 2u || flops_bits >= 0x7f800000u || bytes_bits >= 0x7f800000u)
+        return DSIM_ST_BAD_OP;
+    if (kind == 0u) return ia < (uint32_t)ND ? 0u : (uint32_t)DSIM_ST_BAD_DEVICE;
+    if (kind == 1u) {
+        if (ia >= (uint32_t)ND || ib >= (uint32_t)ND) return DSIM_ST_BAD_DEVICE;
+        return ia == ib ? (uint32_t)DSIM_ST_SELF_SEND : 0u;
+    }
+    return (ib == 0u || (ib >> ND) != 0u) ? (uint32_t)DSIM_ST_BAD_DEVICE : 0u;
 }
 
 template <int ND>
-__global__ __launch_bounds__(kBlock) void k_sim_tables(const TabArgs a)
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPerSimd))) void k_sim_tables(
+    const TabArgs a)
 {
     __shared__ uint64_t s_live[ND][kBlock];
     __shared__ uint64_t s_peak[ND][kBlock];
-    __shared__ double s_arl[ND + 1];
-    __shared__ double s_arc[ND + 1];
+    __shared__ double2 s_ar[ND + 1];                 // (ar_lat[n], ar_coef[n])
 
     const int tid = threadIdx.x;
-    if (tid <= ND) {
-        s_arl[tid] = a.c.ar_lat[tid];
-        s_arc[tid] = a.c.ar_coef[tid];
-    }
+    if (tid <= ND) s_ar[tid] = make_double2(a.c.ar_lat[tid], a.c.ar_coef[tid]);
+
     const int64_t c = (int64_t)blockIdx.x * kBlock + tid;
     const bool active = c < a.n_cand;
+    uint64_t init[ND];
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
-        const uint64_t v = (active && a.init_live) ? a.init_live[c * ND + d] : 0;
-        s_live[d][tid] = v;
-        s_peak[d][tid] = v;
+        init[d] = (active && a.init_live) ? a.init_live[c * ND + d] : 0;
+        s_live[d][tid] = init[d];
+        s_peak[d][tid] = init[d];
     }
     __syncthreads();
-    if (!active) return;
 
-    uint32_t nops = a.n_ops ? a.n_ops[c] : (uint32_t)a.max_ops;
+    uint32_t nops = active ? (a.n_ops ? a.n_ops[c] : (uint32_t)a.max_ops) : 0xffffffffu;
     int32_t st = 0;
-    if (nops > (uint32_t)a.max_ops) {
+    if (active && nops > (uint32_t)a.max_ops) {
         st |= DSIM_ST_BAD_OP;
         nops = (uint32_t)a.max_ops;
     }
+    // ops every lane of the wavefront has (inactive lanes do not constrain it)
+    uint32_t wave_min = nops;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) wave_min = min(wave_min, (uint32_t)__shfl_xor((int)wave_min, off));
+    if (!active) return;
     double clk[ND];
 #pragma unroll
     for (int d = 0; d < ND; ++d) clk[d] = 0.0;
@@ -89,88 +130,174 @@ __global__ __launch_bounds__(kBlock) void k_sim_tables(const TabArgs a)
     const double lat = a.c.lat, launch = a.c.launch;
     const size_t N = (size_t)a.n_cand;
 
-    for (int32_t j0 = 0; j0 < a.max_ops; j0 += kUnroll) {
-        uint32_t cd[kUnroll], al[kUnroll], fr[kUnroll];
-        float fl[kUnroll], by[kUnroll];
+    // ---- fast path: the ops every lane of the wavefront has ------------------
+    // Ops are assumed valid; a cheap test marks any lane that meets an op it
+    // cannot vouch for, and that lane is re-simulated by the exact path below.
+    // Indices are clamped so that even an invalid op stays inside the arrays.
+    const int32_t fast_end = (int32_t)(__builtin_amdgcn_readfirstlane(wave_min) / kUnroll) * kUnroll;
+
+    const size_t blk = (size_t)blockIdx.x * kBlock;
+    const uint32_t lane_b = (uint32_t)tid * 4u;
+    bool suspect = false;
+
+    // two register sets of kUnroll op records: one is processed while the
+    // other is in flight
+    uint32_t cdA[kUnroll], flA[kUnroll], byA[kUnroll], alA[kUnroll], frA[kUnroll];
+    uint32_t cdB[kUnroll], flB[kUnroll], byB[kUnroll], alB[kUnroll], frB[kUnroll];
+    // One buffer descriptor per field and group of kUnroll op rows (based at
+    // this workgroup's first record); op u of the group is u*N records
+    // further, a scalar offset.
+    const uint32_t row_bytes = (uint32_t)(N * 4u);
+    const uint32_t grp_bytes = (uint32_t)min((size_t)0xffffffffu, (size_t)kUnroll * N * 4u);
+    auto load_group = [&](int32_t j0, uint32_t(&cd)[kUnroll], uint32_t(&fl)[kUnroll], uint32_t(&by)[kUnroll],
+                          uint32_t(&al)[kUnroll], uint32_t(&fr)[kUnroll]) {
+        const size_t base = (size_t)j0 * N + blk;
+        const __amdgpu_buffer_rsrc_t rc = group_rsrc(a.code + base, grp_bytes);
+        const __amdgpu_buffer_rsrc_t rf = group_rsrc(a.flops + base, grp_bytes);
+        const __amdgpu_buffer_rsrc_t rb = group_rsrc(a.bytes + base, grp_bytes);
+        const __amdgpu_buffer_rsrc_t ra = group_rsrc(a.alloc + base, grp_bytes);
+        const __amdgpu_buffer_rsrc_t rr = group_rsrc(a.freeb + base, grp_bytes);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int32_t j = j0 + u;
-            if (j < a.max_ops) {
-                const size_t o = (size_t)j * N + (size_t)c;
-                cd[u] = stream_load(a.code + o);
-                fl[u] = stream_load(a.flops + o);
-                by[u] = stream_load(a.bytes + o);
-                al[u] = stream_load(a.alloc + o);
-                fr[u] = stream_load(a.freeb + o);
-            } else {
-                cd[u] = 0; fl[u] = 0.f; by[u] = 0.f; al[u] = 0; fr[u] = 0;
-            }
+            const int so = (int)(u * row_bytes);
+            cd[u] = __builtin_amdgcn_raw_buffer_load_b32(rc, (int)lane_b, so, kNonTemporal);
+            fl[u] = __builtin_amdgcn_raw_buffer_load_b32(rf, (int)lane_b, so, kNonTemporal);
+            by[u] = __builtin_amdgcn_raw_buffer_load_b32(rb, (int)lane_b, so, kNonTemporal);
+            al[u] = __builtin_amdgcn_raw_buffer_load_b32(ra, (int)lane_b, so, kNonTemporal);
+            fr[u] = __builtin_amdgcn_raw_buffer_load_b32(rr, (int)lane_b, so, kNonTemporal);
         }
+    };
+    auto run_group = [&](const uint32_t(&cd)[kUnroll], const uint32_t(&fl)[kUnroll],
+                         const uint32_t(&by)[kUnroll], const uint32_t(&al)[kUnroll],
+                         const uint32_t(&fr)[kUnroll]) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            if ((uint32_t)(j0 + u) >= nops) break;
             const uint32_t code = cd[u];
             const uint32_t kind = code & 0xffu;
             const uint32_t ia = (code >> 8) & 0xffu;
             const uint32_t ib = (code >> 16) & 0xffu;
-            const bool a_ok = ia < (uint32_t)ND, b_ok = ib < (uint32_t)ND;
-            const uint32_t bit_a = a_ok ? (1u << ia) : 0u;
-            const uint32_t bit_b = b_ok ? (1u << ib) : 0u;
+            const bool is_c = kind == 0u, is_s = kind == 1u;
+            const bool fields_ok = (code < (1u << 24)) & (max(fl[u], by[u]) < 0x7f800000u);
+            const bool dev_ok = is_c ? (ia < (uint32_t)ND)
+                                     : (is_s ? ((ia < (uint32_t)ND) & (ib < (uint32_t)ND) & (ia != ib))
+                                             : ((kind == 2u) & (ib != 0u) & ((ib >> ND) == 0u)));
+            suspect |= !(fields_ok & dev_ok);
 
-            // validity, in the order the format defines it
-            uint32_t flag, m;
-            if ((code >> 24) != 0u || kind > 2u) {
-                flag = DSIM_ST_BAD_OP;
-                m = 0u;
-            } else if (kind == 0u) {
-                flag = a_ok ? 0u : (uint32_t)DSIM_ST_BAD_DEVICE;
-                m = bit_a;
-            } else if (kind == 1u) {
-                flag = (!a_ok || !b_ok) ? (uint32_t)DSIM_ST_BAD_DEVICE
-                                        : (ia == ib ? (uint32_t)DSIM_ST_SELF_SEND : 0u);
-                m = bit_a | bit_b;
-            } else {
-                flag = (ib == 0u || (ib >> ND) != 0u) ? (uint32_t)DSIM_ST_BAD_DEVICE : 0u;
-                m = ib;
-            }
-            if (flag) m = 0u;
-            st |= (int32_t)flag;
+            const uint32_t ias = min(ia, (uint32_t)ND - 1u), ibs = min(ib, (uint32_t)ND - 1u);
+            const uint32_t m = (is_c ? (1u << ias) : (is_s ? ((1u << ias) | (1u << ibs)) : ib)) &
+                               ((1u << ND) - 1u);
 
-            // op cost (Sec. 3.3 / Sec. 4 cost functions)
-            const double f = (double)fl[u], b = (double)by[u];
-            const double tf = f * inv_f, tb = b * inv_b;
-            const double t_comp = launch + (tf > tb ? tf : tb);
+            // op cost (Sec. 3.3 / Sec. 4 cost functions), blended without branches
+            const double2 ar = s_ar[__popc(m)];
+            const double f = (double)__uint_as_float(fl[u]), b = (double)__uint_as_float(by[u]);
+            const double t_comp = launch + __builtin_fmax(f * inv_f, b * inv_b);
             const double tl = b * inv_l;
             const double t_send = lat + tl;
-            const int n = __popc(m);
-            const double t_ar = s_arl[n] + s_arc[n] * tl;
-            const double cost = kind == 0u ? t_comp : (kind == 1u ? t_send : t_ar);
+            const double t_ar = ar.x + ar.y * tl;
+            const double cost = is_c ? t_comp : (is_s ? t_send : t_ar);
 
-            // synchronous start on the device set, common end
-            double start = 0.0;
+            // synchronous start on the device set, common end.  sel[d] is 1.0
+            // for a participant, 0.0 otherwise.  Clocks are >= 0, so
+            // max(start, clk*sel) is the participants' max; every participant
+            // has clk <= start <= end, so max(clk, end*sel) sets participants
+            // to end and leaves the others unchanged (bit-exact).
+            double sel[ND];
 #pragma unroll
-            for (int d = 0; d < ND; ++d) {
-                const double v = ((m >> d) & 1u) ? clk[d] : 0.0;
-                start = v > start ? v : start;
-            }
-            const double end = start + cost;
+            for (int d = 0; d < ND; ++d) sel[d] = (double)((m >> d) & 1u);
+            // pairwise max tree (max is exact, so the order does not matter)
+            double v[ND];
 #pragma unroll
-            for (int d = 0; d < ND; ++d) clk[d] = ((m >> d) & 1u) ? end : clk[d];
+            for (int d = 0; d < ND; ++d) v[d] = clk[d] * sel[d];
+#pragma unroll
+            for (int w = 1; w < ND; w *= 2)
+#pragma unroll
+                for (int d = 0; d + w < ND; d += 2 * w) v[d] = __builtin_fmax(v[d], v[d + w]);
+            // every product is +0.0 or positive, so the tree's max is already
+            // the max over the participants starting from 0.0
+            const double end = v[0] + cost;
+#pragma unroll
+            for (int d = 0; d < ND; ++d) clk[d] = __builtin_fmax(clk[d], end * sel[d]);
 
             // live memory: allocate on the target, sample, free on the source
-            const bool memop = flag == 0u && kind != 2u;
+            const bool memop = kind != 2u;
             const uint32_t alloc = memop ? al[u] : 0u;
             const uint32_t fre = memop ? fr[u] : 0u;
-            const uint32_t tdev = memop ? (kind == 1u ? ib : ia) : 0u;
-            const uint32_t fdev = memop ? ia : 0u;
-            const uint64_t lv = s_live[tdev][tid] + (uint64_t)alloc;
-            s_live[tdev][tid] = lv;
+            const uint32_t tdev = is_s ? ibs : ias;
+            const uint32_t fdev = ias;
+            const uint64_t lt0 = s_live[tdev][tid];
             const uint64_t pk = s_peak[tdev][tid];
-            s_peak[tdev][tid] = lv > pk ? lv : pk;
-            const uint64_t lf = s_live[fdev][tid];
+            const uint64_t lf0 = s_live[fdev][tid];
+            const uint64_t lt = lt0 + (uint64_t)alloc;
+            const uint64_t lf = tdev == fdev ? lt : lf0;
+            s_live[tdev][tid] = lt;
+            s_peak[tdev][tid] = lt > pk ? lt : pk;
             const bool under = (uint64_t)fre > lf;
             st |= under ? DSIM_ST_MEM_UNDERFLOW : 0;
             s_live[fdev][tid] = under ? 0ull : lf - (uint64_t)fre;
+        }
+    };
+    if (fast_end > 0) load_group(0, cdA, flA, byA, alA, frA);
+    for (int32_t j0 = 0; j0 < fast_end; j0 += 2 * kUnroll) {
+        if (j0 + kUnroll < fast_end) load_group(j0 + kUnroll, cdB, flB, byB, alB, frB);
+        run_group(cdA, flA, byA, alA, frA);
+        if (j0 + kUnroll >= fast_end) break;
+        if (j0 + 2 * kUnroll < fast_end) load_group(j0 + 2 * kUnroll, cdA, flA, byA, alA, frA);
+        run_group(cdB, flB, byB, alB, frB);
+    }
+
+    // ---- exact path: this lane's remaining ops, or all of them again if the
+    // fast path met an op it could not vouch for -------------------------------
+    int32_t j = fast_end;
+    if (suspect) {
+        j = 0;
+        st = 0;
+#pragma unroll
+        for (int d = 0; d < ND; ++d) {
+            clk[d] = 0.0;
+            s_live[d][tid] = init[d];
+            s_peak[d][tid] = init[d];
+        }
+    }
+    for (; j < (int32_t)nops; ++j) {
+        const size_t o = (size_t)j * N + (size_t)c;
+        const uint32_t code = a.code[o];
+        const float flf = a.flops[o], byf = a.bytes[o];
+        const uint32_t flag = op_flags<ND>(code, __float_as_uint(flf), __float_as_uint(byf));
+        st |= (int32_t)flag;
+        if (flag) continue;   // an invalid op is skipped: no time, no memory
+        const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
+        const uint32_t m = kind == 0u ? (1u << ia) : (kind == 1u ? ((1u << ia) | (1u << ib)) : ib);
+        const double f = (double)flf, b = (double)byf;
+        double cost;
+        if (kind == 0u) {
+            const double tf = f * inv_f, tb = b * inv_b;
+            cost = launch + (tf > tb ? tf : tb);
+        } else if (kind == 1u) {
+            cost = lat + b * inv_l;
+        } else {
+            const double2 ar = s_ar[__popc(m)];
+            cost = ar.x + ar.y * (b * inv_l);
+        }
+        double start = 0.0;
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+            if (((m >> d) & 1u) && clk[d] > start) start = clk[d];
+        const double end = start + cost;
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+            if ((m >> d) & 1u) clk[d] = end;
+        if (kind != 2u) {
+            const uint32_t tdev = kind == 1u ? ib : ia;
+            const uint64_t lt = s_live[tdev][tid] + (uint64_t)a.alloc[o];
+            s_live[tdev][tid] = lt;
+            if (lt > s_peak[tdev][tid]) s_peak[tdev][tid] = lt;
+            const uint64_t lf = s_live[ia][tid], fre = (uint64_t)a.freeb[o];
+            if (fre > lf) {
+                st |= DSIM_ST_MEM_UNDERFLOW;
+                s_live[ia][tid] = 0;
+            } else {
+                s_live[ia][tid] = lf - fre;
+            }
         }
     }
 

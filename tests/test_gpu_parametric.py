@@ -1,0 +1,180 @@
+"""GPU parity of the parametric D/H/P/K expander against the oracle.
+
+Small models: the oracle materialises the whole distributed program (every
+device of every replica).  Full-size grids: the oracle's projection onto one
+replica per stage (itself pinned to the full program in
+test_oracle_pins.py), on every candidate where that is cheap and on a seeded
+sample of the GPT-3-shaped grid.  Bar: status, op counts and peak bytes
+bit-exact; times within 1e-12 relative and expected bit-identical.
+"""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+from paper_2111_05426_amd.workloads import (ALL, DeviceSpec, GPT2_SMALL, GPT2_SMALL_TRAIN, GPT3_175B, INFER,
+                                            LARGE_MLP, TINY_MLP, TRAIN_ADAM, TRAIN_ADAM_MIXED, TRAIN_SGD, mlp,
+                                            transformer)
+
+pytestmark = pytest.mark.gpu
+REL = 1e-12
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    from paper_2111_05426_amd import dsim
+    dsim.lib()
+    return torch
+
+
+def run_gpu(torch, model, strat, dev, row_width=None):
+    from paper_2111_05426_amd import dsim
+    strat = np.ascontiguousarray(strat, np.int32).reshape(-1, 4)
+    rw = int(row_width or max(1, strat[:, 2].max()))
+    r = dsim.alloc_results(len(strat), rw)
+    cand = torch.from_numpy(strat).cuda()
+    dsim.dsim_simulate_parametric(model, cand, dev, r)
+    torch.cuda.synchronize()
+    out = {k: v.cpu().numpy() for k, v in r.items() if k != "row_width"}
+    out["cand"] = cand
+    out["gpu"] = r
+    return out
+
+
+def compare(g, o, strat):
+    bad = []
+    for name in ("status", "n_ops", "cand_peak"):
+        a = g[name].astype(np.int64) if name != "cand_peak" else g[name].view(np.uint64)
+        b = o[name].astype(np.int64) if name != "cand_peak" else o[name]
+        if not np.array_equal(a, b):
+            i = int(np.nonzero(a != b)[0][0])
+            bad.append("%s differs first at %s: gpu %s oracle %s" % (name, strat[i].tolist(), a[i], b[i]))
+    np.testing.assert_allclose(g["makespan"], o["makespan"], rtol=REL, atol=0)
+    rw = o["finish"].shape[1]
+    np.testing.assert_allclose(g["finish"][:, :rw], o["finish"], rtol=REL, atol=0)
+    if not np.array_equal(g["peak"][:, :rw].view(np.uint64), o["peak"]):
+        i = int(np.nonzero(np.any(g["peak"][:, :rw].view(np.uint64) != o["peak"], axis=1))[0][0])
+        bad.append("stage peak differs at %s: gpu %s oracle %s" % (strat[i].tolist(), g["peak"][i, :rw],
+                                                                  o["peak"][i]))
+    assert not bad, "\n".join(bad)
+    assert np.array_equal(g["makespan"], o["makespan"]), "within 1e-12 but not bit-identical"
+    assert np.array_equal(g["finish"][:, :rw], o["finish"])
+    ok = g["status"] == 0
+    assert np.all(g["walked_ops"][ok] > 0) and np.all(g["walked_ops"] <= g["n_ops"])
+
+
+def all_strats(D, H, P, K):
+    return np.array([(d, h, p, k) for d in D for h in H for p in P for k in K], np.int32)
+
+
+SMALL = [
+    ("mlp_sgd", mlp(4, 64, 48, 4, TRAIN_SGD), all_strats([1, 2, 3], [1, 2], [1, 2, 4], [1, 2, 3, 5])),
+    ("mlp_adam_uneven", mlp(6, 64, 40, 2, TRAIN_ADAM), all_strats([1, 2, 4], [1, 2], [1, 2, 3, 4, 5], [1, 3, 7])),
+    ("mlp_mixed", mlp(8, 32, 36, 2, TRAIN_ADAM_MIXED), all_strats([1, 2], [1, 2, 4], [1, 2, 4, 8], [1, 2, 6])),
+    ("mlp_infer", mlp(5, 64, 30, 4, INFER), all_strats([1, 2, 3], [1, 2], [1, 2, 3, 5], [1, 2, 4])),
+    ("tf_train", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM), all_strats([1, 2, 3], [1, 2, 4], [1, 2, 3, 4],
+                                                                             [1, 2, 5])),
+    ("tf_mixed", transformer(5, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED), all_strats([1, 2], [1, 2], [1, 2, 5], [1, 4])),
+    ("tf_infer", transformer(6, 48, 6, 16, 97, 9, 2, INFER), all_strats([1, 3], [1, 2, 3], [1, 2, 4], [1, 2, 3])),
+    ("tf_sgd", transformer(3, 32, 2, 8, 50, 6, 4, TRAIN_SGD), all_strats([1, 2], [1, 2], [1, 3], [1, 2, 3])),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_small_models_vs_full_program(torch_gpu, orc, case):
+    name, model, strat = SMALL[case]
+    dev = DeviceSpec(mem_cap_bytes=10 ** 6)
+    g = run_gpu(torch_gpu, model, strat, dev)
+    o = orc.run_strategies(model, strat, dev, slice=False, row_width=g["finish"].shape[1], threads=8)
+    assert np.any(o["status"] == 0)
+    compare(g, o, strat)
+
+
+GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
+         replace(LARGE_MLP, name="large_mlp_mixed", model=replace(LARGE_MLP.model, mode=TRAIN_ADAM_MIXED))]
+
+
+@pytest.mark.parametrize("w", GRIDS, ids=[w.name for w in GRIDS])
+def test_workload_grid_vs_oracle(torch_gpu, orc, w):
+    from paper_2111_05426_amd import dsim
+    strat = dsim.dsim_create_grid(w.model, w.grid)
+    rw = int(strat[:, 2].max())
+    print("%s: %d candidates" % (w.name, len(strat)), flush=True)
+    g = run_gpu(torch_gpu, w.model, strat, w.device, rw)
+    o = orc.run_strategies(w.model, strat, w.device, slice=True, row_width=rw, threads=8)
+    compare(g, o, strat)
+    # full-program oracle on the candidates whose program is small
+    small = np.nonzero(o["n_ops"] <= 20000)[0][:60]
+    if len(small):
+        of = orc.run_strategies(w.model, strat[small], w.device, slice=False, row_width=rw, threads=8)
+        sub = {k: (v[small] if isinstance(v, np.ndarray) else v) for k, v in g.items()}
+        compare(sub, of, strat[small])
+    # selection over the grid
+    k = w.top_k
+    idx, mk, found = dsim.select_topk(g["gpu"]["makespan"], g["gpu"]["cand_peak"], g["gpu"]["status"],
+                                      w.device.mem_cap_bytes, k)
+    ri, rm, rf = orc.topk(o["makespan"], o["cand_peak"], o["status"], w.device.mem_cap_bytes, k)
+    torch_gpu.cuda.synchronize()
+    assert int(found.item()) == rf and np.array_equal(idx.cpu().numpy(), ri)
+
+
+def test_gpt3_grid_sampled(torch_gpu, orc):
+    """The GPT-3-shaped grid at full size (39,965 strategies, one launch, the
+    288e9-byte cap, top-16): a seeded sample plus the selected top-16 and the
+    extreme microbatch counts are compared one by one with the oracle."""
+    from paper_2111_05426_amd import dsim
+    w = GPT3_175B
+    strat = dsim.dsim_create_grid(w.model, w.grid)
+    assert len(strat) == 39965
+    print("gpt3_175b: simulating %d candidates" % len(strat), flush=True)
+    g = run_gpu(torch_gpu, w.model, strat, w.device, 64)
+    idx, mk, found = dsim.select_topk(g["gpu"]["makespan"], g["gpu"]["cand_peak"], g["gpu"]["status"],
+                                      w.device.mem_cap_bytes, w.top_k)
+    torch_gpu.cuda.synchronize()
+    top = idx.cpu().numpy()
+    assert int(found.item()) == 16
+    rng = np.random.default_rng(175)
+    K = strat[:, 3]
+    pick = np.unique(np.concatenate([rng.choice(len(strat), 250, replace=False), top,
+                                     np.nonzero(K == K.max())[0][:5], np.nonzero(K == 1)[0][:5]]))
+    print("gpt3_175b: oracle on %d sampled candidates" % len(pick), flush=True)
+    o = orc.run_strategies(w.model, strat[pick], w.device, slice=True, row_width=64, threads=8)
+    sub = {k: (v[pick] if isinstance(v, np.ndarray) else v) for k, v in g.items()}
+    compare(sub, o, strat[pick])
+    # the selection is the ordered prefix of the feasible candidates
+    mk_all, st, cp = g["makespan"], g["status"], g["cand_peak"].view(np.uint64)
+    feas = np.nonzero((st == 0) & (cp <= w.device.mem_cap_bytes))[0]
+    order = feas[np.lexsort((feas, mk_all[feas]))][:16]
+    assert np.array_equal(top, order)
+    assert np.array_equal(mk.cpu().numpy(), mk_all[order])
+
+
+def test_invalid_strategies(torch_gpu, orc):
+    m = transformer(4, 32, 4, 8, 64, 12, 2, TRAIN_ADAM)
+    strat = np.array([(5, 1, 1, 1),     # D does not divide the batch
+                      (2, 1, 1, 7),     # K > B/D
+                      (1, 1, 5, 1),     # P > L
+                      (1, 3, 1, 1),     # H does not divide the heads
+                      (0, 1, 1, 1), (1, 1, 1, 0), (1, 1, 1, 1)], np.int32)
+    dev = DeviceSpec()
+    g = run_gpu(torch_gpu, m, strat, dev, 5)
+    o = orc.run_strategies(m, strat, dev, slice=False, row_width=5, threads=1)
+    assert list(g["status"][:-1]) == [16] * 6 and g["status"][-1] == 0
+    compare(g, o, strat)
+    mm = mlp(6, 64, 12, 2, TRAIN_SGD)
+    strat = np.array([(1, 2, 2, 1), (1, 2, 3, 1), (1, 2, 4, 1)], np.int32)   # pairs split by stages
+    g = run_gpu(torch_gpu, mm, strat, dev, 4)
+    o = orc.run_strategies(mm, strat, dev, slice=False, row_width=4, threads=1)
+    assert list(g["status"]) == [16, 0, 16]
+    compare(g, o, strat)
+
+
+def test_stage_limit_and_row_width(torch_gpu):
+    """More than 64 pipeline stages, or more than results.row_width, is
+    refused per candidate (DSIM_ST_BAD_STRATEGY), never overrun."""
+    m = mlp(80, 16, 8, 4, INFER)
+    strat = np.array([(1, 1, 70, 1), (1, 1, 8, 1), (1, 1, 9, 1)], np.int32)
+    g = run_gpu(torch_gpu, m, strat, DeviceSpec(), 8)
+    assert list(g["status"]) == [16, 0, 16]

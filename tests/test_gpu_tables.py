@@ -52,6 +52,10 @@ def random_tables(rng, n_cand, max_ops, n_dev, bad=False):
         free = np.minimum(free, alloc)
     fl = np.exp(rng.uniform(np.log(1e6), np.log(1e12), (max_ops, n_cand))).astype(np.float32)
     by = np.exp(rng.uniform(np.log(1e3), np.log(1e9), (max_ops, n_cand))).astype(np.float32)
+    if bad:   # fields that are not finite and >= 0 make an op invalid
+        for arr in (fl, by):
+            for v in (np.inf, -np.inf, np.nan, -0.0, -5.0):
+                arr[rng.random((max_ops, n_cand)) < 0.0005] = np.float32(v)
     n_ops = rng.integers(0, max_ops + 1, n_cand).astype(np.uint32)
     n_ops[:3] = [0, max_ops, 1][:min(3, n_cand)] if n_cand >= 3 else n_ops[:3]
     init = rng.integers(0, 10 ** 5, (n_cand, n_dev)).astype(np.uint64)

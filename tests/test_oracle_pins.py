@@ -547,7 +547,8 @@ def table_brute(tab, n_dev, dev, init=None):
     for c, fl, by, al, fr in zip(tab["code"], tab["flops"], tab["bytes"], tab["alloc"], tab["free"]):
         c = int(c)
         k, a, b = c & 255, (c >> 8) & 255, (c >> 16) & 255
-        if c >> 24 or k > 2:
+        fin = lambda x: math.isfinite(float(x)) and float(x) >= 0 and not math.copysign(1.0, float(x)) < 0
+        if c >> 24 or k > 2 or not fin(fl) or not fin(by):
             st |= 1
             continue
         if k == 0:
@@ -605,6 +606,11 @@ def test_table_brute_force(orc, seed):
                bytes=rng.uniform(1e3, 1e9, n).astype(np.float32),
                alloc=rng.integers(0, 1000, n).astype(np.uint32),
                free=rng.integers(0, 600, n).astype(np.uint32))
+    if seed % 4 == 1:
+        tab["bytes"][rng.integers(0, n)] = np.float32(np.inf)
+        tab["flops"][rng.integers(0, n)] = np.float32(-2.0)
+        tab["flops"][rng.integers(0, n)] = np.float32(-0.0)
+        tab["bytes"][rng.integers(0, n)] = np.float32(np.nan)
     init = rng.integers(0, 2000, n_dev).astype(np.uint64)
     r = orc.sim_table(tab, n_dev, DEV, init_live=init)
     clk, peak, st = table_brute(tab, n_dev, DEV, [int(v) for v in init])
