@@ -8,6 +8,9 @@ input already resident in HBM:
     random programs of 2,048 ops over 8 devices from their explicit op tables
     (dsim_simulate_tables), then select the best feasible one (dsim_argmin).
     The tables (about 41 GB) are generated on the GPU before timing.
+  * "parametric" (extra key of the same line): each strategy grid (tiny MLP,
+    large MLP, GPT-2-small inference and training, GPT-3-175B) simulated by
+    dsim_simulate_parametric + top-k, timed with HIP events.
 Prints one JSON line (rank 0).  The CPU oracle is timed on a bounded sample
 of the same workload as `cpu_baseline`.
 """
@@ -134,6 +137,56 @@ def bench_random_tables(args, torch, dsim, W):
     return out
 
 
+PARAMETRIC = ("tiny_mlp", "large_mlp", "gpt2_small", "gpt2_small_train", "gpt3_175b")
+
+
+def bench_parametric(torch, dsim, W, reps):
+    """One grid of the transform-driven path: dsim_simulate_parametric over
+    every strategy of the grid plus the top-k selection, with the strategies
+    resident on the device.  Walked ops are the ops the kernel processes (one
+    replica per stage); program ops count every op of the global program."""
+    strat = dsim.dsim_create_grid(W.model, W.grid)
+    n = len(strat)
+    rw = int(strat[:, 2].max())
+    cand = torch.from_numpy(strat).cuda()
+    res = dsim.alloc_results(n, rw)
+    k = W.top_k
+    ws = torch.empty(max(dsim.dsim_argmin_workspace(n, k), 16), dtype=torch.uint8, device="cuda")
+    out_idx = torch.empty(k, dtype=torch.int64, device="cuda")
+    out_mk = torch.empty(k, dtype=torch.float64, device="cuda")
+    found = torch.empty(1, dtype=torch.int32, device="cuda")
+    dev = W.device
+    ev = []
+
+    def step(record):
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        dsim.dsim_simulate_parametric(W.model, cand, dev, res)
+        e1.record()
+        dsim.dsim_argmin(res["makespan"], res["cand_peak"], res["status"], dev.mem_cap_bytes, k, ws, out_idx,
+                         out_mk, found)
+        e2.record()
+        if record:
+            ev.append((e0, e1, e2))
+
+    step(False)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        step(True)
+    torch.cuda.synchronize()
+    kern_ms = sum(a.elapsed_time(b) for a, b, _ in ev) / len(ev)
+    step_ms = sum(a.elapsed_time(c) for a, _, c in ev) / len(ev)
+    walked = int(res["walked_ops"].sum().item())
+    prog = int(res["n_ops"].sum().item())
+    ok = int((res["status"] == 0).sum().item())
+    return {"workload": W.name, "n_cand": n, "valid": ok, "top_k": k, "found": int(found.item()),
+            "best": {"index": int(out_idx[0].item()), "strategy_DHPK": strat[int(out_idx[0].item())].tolist(),
+                     "makespan_s": float(out_mk[0].item())} if int(found.item()) > 0 else None,
+            "kernel_ms": kern_ms, "step_ms": step_ms, "candidates_per_s": n / (step_ms * 1e-3),
+            "walked_ops": walked, "walked_ops_per_s": walked / (kern_ms * 1e-3),
+            "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3)}
+
+
 def copy_calibration(torch, nbytes=4 << 30, reps=5):
     """A plain device-to-device copy of known size: its time gives the
     achievable streaming bandwidth; under rocprofv3 --pmc its FETCH_SIZE and
@@ -159,6 +212,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="random_tables")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parametric", action="store_true",
+                    help="skip the per-grid timings of the transform-driven kernel")
+    ap.add_argument("--param-reps", type=int, default=5)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also time a plain 4 GiB device-to-device copy (counter and bandwidth calibration)")
     args = ap.parse_args()
@@ -177,6 +233,8 @@ def main():
     if args.workload != "random_tables":
         raise SystemExit("unknown workload for the benchmark line: %s" % args.workload)
     out = bench_random_tables(args, torch, dsim, W)
+    if not args.no_parametric:
+        out["parametric"] = [bench_parametric(torch, dsim, ALL[name], args.param_reps) for name in PARAMETRIC]
     if args.copy_calibration:
         out["copy_calibration"] = copy_calibration(torch)
     if not args.no_cpu_baseline:

@@ -1,0 +1,494 @@
+// model.h -- the ops of the D/H/P/K transform, written once for every
+// consumer in the library.
+//
+// The transform of Sec. 4 (Fig. 2 is its P = 2, K = 2 instance) turns a model
+// and a strategy into one straight-line distributed program.  The functions
+// here produce that program's ops for one pipeline stage, in program order,
+// and hand each to a sink:
+//
+//   o.local(flops, bytes, alloc, free)  compute op on every replica of the
+//                                        stage: allocate `alloc` bytes of
+//                                        outputs, then free `free` bytes of
+//                                        tensors whose last use this is
+//   o.ar_tp(bytes)                       all-reduce over the H ranks of each
+//                                        data replica (emitted only if H > 1)
+//   o.ar_dp(bytes)                       all-reduce over the D replicas of
+//                                        each tensor rank (only if D > 1)
+//
+// Sinks: the parametric simulator (one replica per stage), the per-layer
+// cost recorder and the table materialiser.  Memory follows def/use
+// liveness, in closed form per op: outputs are allocated, the peak is
+// sampled, then tensors at their last use are freed (a value with no use is
+// freed by the op that defines it).
+#pragma once
+
+#include "internal.h"
+
+namespace dsim {
+
+constexpr int kMaxStages = 64;
+constexpr int kMaxK = 16383;
+
+// Per-candidate constants.
+struct Ctx {
+    int D, H, P, K, L, q, r;
+    bool train, mlp;
+    int mode;
+    uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
+    uint64_t dH, FH, Vh, aH;
+    double inv_f, inv_b, inv_l, lat, launch;
+    double arl_h, arc_h, arl_d, arc_d;
+    uint64_t mult_dev, mult_tp, mult_dp;
+};
+
+// Preconditions of the transform (evenly divisible batch, heads and hidden
+// sizes; K <= rows per replica; P <= layers; with H > 1 every MLP stage holds
+// whole column/row layer pairs).
+__device__ inline bool strategy_ok(const dsim_model &m, int D, int H, int P, int K)
+{
+    if (D < 1 || H < 1 || P < 1 || K < 1) return false;
+    const int64_t B = m.global_batch;
+    if (B % D != 0 || (int64_t)K > B / D || P > m.n_layers) return false;
+    if (m.family == DSIM_MLP) {
+        if (m.d_model % H != 0) return false;
+        if (H > 1) {
+            const int q = m.n_layers / P, r = m.n_layers % P;
+            if ((q & 1) != 0 && r < P) return false;          // stages with q layers
+            if (r > 0 && ((q + 1) & 1) != 0) return false;    // stages with q + 1 layers
+        }
+        return true;
+    }
+    return m.n_heads % H == 0 && m.d_model % H == 0 && m.d_ff % H == 0;
+}
+
+__device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const dsim_strategy &st, Ctx &x)
+{
+    x.D = st.D;
+    x.H = st.H;
+    x.P = st.P;
+    x.K = st.K;
+    x.L = M.n_layers;
+    x.mlp = M.family == DSIM_MLP;
+    x.mode = M.mode;
+    x.train = M.mode != DSIM_INFER;
+    x.q = x.L / x.P;
+    x.r = x.L % x.P;
+    x.e = (uint64_t)M.elem_bytes;
+    x.d = (uint64_t)M.d_model;
+    x.dff = (uint64_t)M.d_ff;
+    x.seq = (uint64_t)M.seq_len;
+    x.vocab = (uint64_t)M.vocab;
+    x.heads = (uint64_t)M.n_heads;
+    x.rows = (uint64_t)M.global_batch / (uint64_t)x.D;
+    x.mq = x.rows / (uint64_t)x.K;
+    x.mr = x.rows % (uint64_t)x.K;
+    x.dH = x.d / (uint64_t)x.H;
+    x.FH = x.mlp ? 0 : x.dff / (uint64_t)x.H;
+    x.Vh = x.mlp ? 0 : (x.vocab + (uint64_t)x.H - 1) / (uint64_t)x.H;
+    x.aH = x.mlp ? 0 : x.heads / (uint64_t)x.H;
+    x.inv_f = c.inv_f;
+    x.inv_b = c.inv_b;
+    x.inv_l = c.inv_l;
+    x.lat = c.lat;
+    x.launch = c.launch;
+    const double ah = 2.0 * (double)(x.H - 1), ad = 2.0 * (double)(x.D - 1);
+    x.arl_h = ah * x.lat;
+    x.arc_h = ah / (double)x.H;
+    x.arl_d = ad * x.lat;
+    x.arc_d = ad / (double)x.D;
+    x.mult_dev = (uint64_t)x.D * (uint64_t)x.H;
+    x.mult_tp = (uint64_t)x.D;
+    x.mult_dp = (uint64_t)x.H;
+}
+
+// Op costs (Sec. 3.3 roofline form, ring all-reduce of the whole group).
+__device__ __forceinline__ double cost_local(const Ctx &x, uint64_t flops, uint64_t bytes)
+{
+    const double tf = (double)flops * x.inv_f;
+    const double tb = (double)bytes * x.inv_b;
+    return x.launch + (tf > tb ? tf : tb);
+}
+__device__ __forceinline__ double cost_ar_tp(const Ctx &x, uint64_t bytes)
+{
+    return x.arl_h + x.arc_h * ((double)bytes * x.inv_l);
+}
+__device__ __forceinline__ double cost_ar_dp(const Ctx &x, uint64_t bytes)
+{
+    return x.arl_d + x.arc_d * ((double)bytes * x.inv_l);
+}
+__device__ __forceinline__ double cost_send(const Ctx &x, uint64_t bytes)
+{
+    return x.lat + (double)bytes * x.inv_l;
+}
+
+// Uneven microbatches: the first rows % K get one extra row.
+__device__ __forceinline__ uint64_t mb_rows(const Ctx &x, int k)
+{
+    return x.mq + ((uint64_t)k < x.mr ? 1u : 0u);
+}
+
+// Contiguous stages: L = q*P + r, the first r stages get q + 1 layers.
+__device__ __forceinline__ int stage_l0(const Ctx &x, int s) { return s * x.q + (s < x.r ? s : x.r); }
+__device__ __forceinline__ int stage_nl(const Ctx &x, int s) { return x.q + (s < x.r ? 1 : 0); }
+
+// ---------------------------------------------------------------------------
+// MLP (Fig. 2: @dense = Gemm + Relu).  With H > 1 even layers are
+// column-parallel (W: d x d/H), odd layers row-parallel (W: d/H x d) with an
+// all-reduce of their output; dX of column-parallel layers is all-reduced in
+// the backward pass (layer 0's dX is computed and discarded).
+// ---------------------------------------------------------------------------
+enum MlpKind { kPlain = 0, kCol = 1, kRow = 2 };
+
+__device__ __forceinline__ int mlp_kind(const Ctx &x, int i) { return x.H <= 1 ? kPlain : ((i & 1) ? kRow : kCol); }
+
+__device__ __forceinline__ void mlp_dims(const Ctx &x, int kind, uint64_t &din, uint64_t &dout)
+{
+    din = kind == kRow ? x.d / (uint64_t)x.H : x.d;
+    dout = kind == kCol ? x.d / (uint64_t)x.H : x.d;
+}
+
+// One layer's forward.  dead_out: the model's last layer in inference, whose
+// output has no use.
+template <class S>
+__device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, int kind, bool dead_out)
+{
+    const uint64_t e = x.e;
+    uint64_t din, dout;
+    mlp_dims(x, kind, din, dout);
+    // Gemm: the layer input dies here in inference (training keeps it for
+    // the weight gradient)
+    o.local(2 * m * din * dout, e * (m * din + din * dout + m * dout), e * m * dout, x.train ? 0 : e * m * din);
+    if (kind == kRow) o.ar_tp(e * m * dout);
+    // Relu frees the pre-activation
+    o.local(m * dout, 2 * e * m * dout, e * m * dout, e * m * dout + (dead_out ? e * m * dout : 0));
+}
+
+// One layer's backward.  frees_input: the stage's first layer, where the
+// stage input dies at the weight gradient; layer0: the model's first layer,
+// whose dX has no use and is not all-reduced.
+template <class S>
+__device__ __forceinline__ void mlp_layer_bwd(const Ctx &x, S &o, uint64_t m, int kind, bool frees_input,
+                                              bool layer0, bool acc)
+{
+    const uint64_t e = x.e;
+    uint64_t din, dout;
+    mlp_dims(x, kind, din, dout);
+    o.local(m * dout, 3 * e * m * dout, e * m * dout, 2 * e * m * dout);                 // ReluGrad: da and a die
+    o.local(2 * m * din * dout, e * (m * din + m * dout + din * dout), e * din * dout,
+            frees_input ? e * m * din : 0);                                             // weight gradient
+    if (acc) o.local(din * dout, 3 * e * din * dout, 0, e * din * dout);                // accumulate
+    o.local(2 * m * din * dout, e * (m * dout + din * dout + m * din), e * m * din,
+            e * m * dout + (layer0 ? e * m * din : 0));                                 // input gradient
+    if (kind != kRow && x.H > 1 && !layer0) o.ar_tp(e * m * din);
+}
+
+template <class S>
+__device__ __forceinline__ void mlp_loss(const Ctx &x, S &o, uint64_t m)
+{
+    const uint64_t e = x.e;
+    o.local(3 * m * x.d, 3 * e * m * x.d, e * m * x.d, e * m * x.d);   // loss gradient; y_k dies
+}
+
+// bytes of the activation a stage sends forward / the gradient it sends back
+__device__ __forceinline__ uint64_t mlp_act_out(const Ctx &x, int s, int k)
+{
+    uint64_t din, dout;
+    mlp_dims(x, mlp_kind(x, stage_l0(x, s) + stage_nl(x, s) - 1), din, dout);
+    return x.e * mb_rows(x, k) * dout;
+}
+
+__device__ __forceinline__ uint64_t mlp_grad_out(const Ctx &x, int s, int k)
+{
+    uint64_t din, dout;
+    mlp_dims(x, mlp_kind(x, stage_l0(x, s)), din, dout);
+    return x.e * mb_rows(x, k) * din;
+}
+
+// ---------------------------------------------------------------------------
+// Transformer (GPT-2-shaped decoder, Megatron tensor parallelism: QKV and
+// fc1 column-parallel, out-proj and fc2 row-parallel with an all-reduce of
+// their output; vocabulary-parallel embedding and LM head, ceil(V/H) rows per
+// rank).
+// ---------------------------------------------------------------------------
+struct TfSz {
+    uint64_t m, T, ACT, QKV, OH, S2, FF, LOG, ST, IDS;
+};
+
+__device__ __forceinline__ TfSz tf_sizes(const Ctx &x, uint64_t m)
+{
+    TfSz z;
+    z.m = m;
+    z.T = z.m * x.seq;
+    z.ACT = x.e * z.T * x.d;
+    z.QKV = x.e * z.T * 3 * x.dH;
+    z.OH = x.e * z.T * x.dH;
+    z.S2 = x.e * z.m * x.aH * x.seq * x.seq;
+    z.FF = x.e * z.T * x.FH;
+    z.LOG = x.e * z.T * x.Vh;
+    z.ST = 12 * z.T;
+    z.IDS = 4 * z.T;
+    return z;
+}
+
+// stage 0, before its layers: embedding
+template <class S>
+__device__ __forceinline__ void tf_fwd_first(const Ctx &x, S &o, const TfSz &z)
+{
+    const uint64_t T = z.T, d = x.d;
+    o.local(T * d, 2 * z.ACT + z.IDS, z.ACT, x.train ? 0 : z.IDS);   // ids die in inference
+    o.ar_tp(z.ACT);
+}
+
+template <class S>
+__device__ __forceinline__ void tf_layer_fwd(const Ctx &x, S &o, const TfSz &z)
+{
+    const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
+    const bool tr = x.train;
+    o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                               // LN1
+    o.local(2 * T * d * 3 * dH, e * (T * d + d * 3 * dH + T * 3 * dH), z.QKV, tr ? 0 : z.ACT);  // QKV
+    o.local(2 * T * S_ * dH, 2 * z.OH + z.S2, z.S2, 0);                                    // scores
+    o.local(5 * z.m * x.aH * S_ * S_, 2 * z.S2, z.S2, z.S2);                               // softmax
+    o.local(2 * T * S_ * dH, z.S2 + 2 * z.OH, z.OH, tr ? 0 : z.S2 + z.QKV);               // P.V
+    o.local(2 * T * dH * d, e * (T * dH + dH * d + T * d), z.ACT, tr ? 0 : z.OH);          // out-proj
+    o.ar_tp(z.ACT);
+    o.local(T * d, 3 * z.ACT, z.ACT, tr ? z.ACT : 2 * z.ACT);                             // residual
+    o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                               // LN2
+    o.local(2 * T * d * FH, e * (T * d + d * FH + T * FH), z.FF, tr ? 0 : z.ACT);          // fc1
+    o.local(8 * T * FH, 2 * z.FF, z.FF, tr ? 0 : z.FF);                                   // GeLU
+    o.local(2 * T * FH * d, e * (T * FH + FH * d + T * d), z.ACT, tr ? 0 : z.FF);          // fc2
+    o.ar_tp(z.ACT);
+    o.local(T * d, 3 * z.ACT, z.ACT, tr ? z.ACT : 2 * z.ACT);                             // residual
+}
+
+// last stage, after its layers: final LN and LM head
+template <class S>
+__device__ __forceinline__ void tf_fwd_last(const Ctx &x, S &o, const TfSz &z)
+{
+    const uint64_t T = z.T, d = x.d, e = x.e;
+    const bool tr = x.train;
+    o.local(8 * T * d, 2 * z.ACT, z.ACT, tr ? 0 : z.ACT);                                  // final LN
+    o.local(2 * T * d * x.Vh, e * (T * d + d * x.Vh + T * x.Vh), z.LOG, tr ? 0 : z.ACT + z.LOG);  // LM head
+}
+
+// last stage, before its layers' backward: loss, LM head and final LN grads
+template <class S>
+__device__ __forceinline__ void tf_bwd_last(const Ctx &x, S &o, const TfSz &z, bool acc)
+{
+    const uint64_t T = z.T, d = x.d, e = x.e, Vh = x.Vh;
+    o.local(3 * T * Vh, z.LOG + z.ST, z.ST, 0);                                   // loss statistics
+    o.ar_tp(z.ST);
+    o.local(2 * T * Vh, 2 * z.LOG + z.ST + z.IDS, z.LOG, z.LOG + z.ST + z.IDS);   // dlogits
+    o.local(2 * T * d * Vh, e * (T * Vh + d * Vh + T * d), z.ACT, 0);             // LM head dX
+    o.ar_tp(z.ACT);
+    o.local(2 * T * d * Vh, e * (T * d + T * Vh + d * Vh), e * d * Vh, z.ACT + z.LOG);  // LM head dW
+    if (acc) o.local(d * Vh, 3 * e * d * Vh, 0, e * d * Vh);
+    o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                             // final LN grad
+}
+
+template <class S>
+__device__ __forceinline__ void tf_layer_bwd(const Ctx &x, S &o, const TfSz &z, bool acc)
+{
+    const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
+    o.local(2 * T * FH * d, e * (T * d + FH * d + T * FH), z.FF, 0);             // fc2 dX
+    o.local(2 * T * FH * d, e * (T * FH + T * d + FH * d), e * FH * d, z.FF);     // fc2 dW
+    if (acc) o.local(FH * d, 3 * e * FH * d, 0, e * FH * d);
+    o.local(8 * T * FH, 3 * z.FF, z.FF, 2 * z.FF);                                // GeLU grad
+    o.local(2 * T * d * FH, e * (T * FH + d * FH + T * d), z.ACT, 0);             // fc1 dX
+    o.ar_tp(z.ACT);
+    o.local(2 * T * d * FH, e * (T * d + T * FH + d * FH), e * d * FH, z.ACT + z.FF);  // fc1 dW
+    if (acc) o.local(d * FH, 3 * e * d * FH, 0, e * d * FH);
+    o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                              // LN2 grad
+    o.local(T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                  // residual merge
+    o.local(2 * T * dH * d, e * (T * d + dH * d + T * dH), z.OH, 0);              // out-proj dX
+    o.local(2 * T * dH * d, e * (T * dH + T * d + dH * d), e * dH * d, z.OH);     // out-proj dW
+    if (acc) o.local(dH * d, 3 * e * dH * d, 0, e * dH * d);
+    o.local(4 * T * S_ * dH, 2 * z.S2 + 3 * z.OH, z.S2 + z.QKV, z.OH);            // P.V grads
+    o.local(5 * z.m * x.aH * S_ * S_, 3 * z.S2, z.S2, 2 * z.S2);                  // softmax grad
+    o.local(4 * T * S_ * dH, z.S2 + 4 * z.OH, 0, z.S2 + z.QKV);                   // Q.K^T grads
+    o.local(2 * T * 3 * dH * d, e * (T * 3 * dH + 3 * dH * d + T * d), z.ACT, 0);  // QKV dX
+    o.ar_tp(z.ACT);
+    o.local(2 * T * d * 3 * dH, e * (T * d + T * 3 * dH + d * 3 * dH), e * d * 3 * dH, z.ACT + z.QKV);  // QKV dW
+    if (acc) o.local(d * 3 * dH, 3 * e * d * 3 * dH, 0, e * d * 3 * dH);
+    o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                              // LN1 grad
+    o.local(T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                  // residual merge
+}
+
+// stage 0, after its layers' backward: embedding gradient
+template <class S>
+__device__ __forceinline__ void tf_bwd_first(const Ctx &x, S &o, const TfSz &z, bool acc)
+{
+    const uint64_t T = z.T, d = x.d, e = x.e, Vh = x.Vh;
+    o.local(T * d, z.ACT + z.IDS + e * Vh * d, e * Vh * d, z.ACT + z.IDS);        // embedding dW
+    if (acc) o.local(Vh * d, 3 * e * Vh * d, 0, e * Vh * d);
+}
+
+// ---------------------------------------------------------------------------
+// Whole blocks (one microbatch's forward or backward on one stage), op by op
+// ---------------------------------------------------------------------------
+template <class S>
+__device__ void block_fwd(const Ctx &x, S &o, int s, int k)
+{
+    const uint64_t m = mb_rows(x, k);
+    if (x.mlp) {
+        const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
+        for (int i = l0; i < l1; ++i) mlp_layer_fwd(x, o, m, mlp_kind(x, i), !x.train && i == x.L - 1);
+        return;
+    }
+    const TfSz z = tf_sizes(x, m);
+    if (s == 0) tf_fwd_first(x, o, z);
+    const int nl = stage_nl(x, s);
+    for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z);
+    if (s == x.P - 1) tf_fwd_last(x, o, z);
+}
+
+template <class S>
+__device__ void block_bwd(const Ctx &x, S &o, int s, int k)
+{
+    const uint64_t m = mb_rows(x, k);
+    const bool acc = k >= 1;
+    if (x.mlp) {
+        const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
+        if (s == x.P - 1) mlp_loss(x, o, m);
+        for (int i = l1 - 1; i >= l0; --i) mlp_layer_bwd(x, o, m, mlp_kind(x, i), i == l0, i == 0, acc);
+        return;
+    }
+    const TfSz z = tf_sizes(x, m);
+    if (s == x.P - 1) tf_bwd_last(x, o, z, acc);
+    const int nl = stage_nl(x, s);
+    for (int i = 0; i < nl; ++i) tf_layer_bwd(x, o, z, acc);
+    if (s == 0) tf_bwd_first(x, o, z, acc);
+}
+
+// ---------------------------------------------------------------------------
+// Optimizer, resident memory, splits and the weight update
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void opt_cost(const Ctx &x, uint64_t N, uint64_t &flops, uint64_t &bytes)
+{
+    if (x.mode == DSIM_TRAIN_SGD) {
+        flops = 2 * N;
+        bytes = 3 * x.e * N;
+    } else if (x.mode == DSIM_TRAIN_ADAM) {
+        flops = 12 * N;
+        bytes = 7 * x.e * N;
+    } else {
+        flops = 12 * N;
+        bytes = 28 * N;
+    }
+}
+
+__device__ __forceinline__ uint64_t opt_state(const Ctx &x, uint64_t N)
+{
+    if (!x.train) return 0;
+    if (x.mode == DSIM_TRAIN_ADAM) return 2 * x.e * N;
+    if (x.mode == DSIM_TRAIN_ADAM_MIXED) return 12 * N;
+    return 0;
+}
+
+// one parameter tensor: all-reduce its gradient over the D replicas, then
+// the optimizer op (in place), after which the gradient dies
+template <class S>
+__device__ __forceinline__ void wu_param(const Ctx &x, S &o, uint64_t N)
+{
+    o.ar_dp(x.e * N);
+    uint64_t fl, by;
+    opt_cost(x, N, fl, by);
+    o.local(fl, by, 0, x.e * N);
+}
+
+// after the stage's last backward, layer by layer in ascending order
+template <class S>
+__device__ void weight_update(const Ctx &x, S &o, int s)
+{
+    const int l0 = stage_l0(x, s), nl = stage_nl(x, s);
+    if (x.mlp) {
+        for (int i = l0; i < l0 + nl; ++i) {
+            uint64_t din, dout;
+            mlp_dims(x, mlp_kind(x, i), din, dout);
+            wu_param(x, o, din * dout);
+        }
+        return;
+    }
+    const uint64_t d = x.d;
+    if (s == 0) wu_param(x, o, x.Vh * d);
+    for (int i = 0; i < nl; ++i) {
+        wu_param(x, o, d * 3 * x.dH);
+        wu_param(x, o, x.dH * d);
+        wu_param(x, o, d * x.FH);
+        wu_param(x, o, x.FH * d);
+    }
+    if (s == x.P - 1) wu_param(x, o, d * x.Vh);
+}
+
+// bytes of one row (sequence) of the stage-0 input / last-stage target
+__device__ __forceinline__ uint64_t input_row(const Ctx &x) { return x.mlp ? x.e * x.d : 4 * x.seq; }
+
+// bytes resident on a device of stage s at t = 0: weight shard, optimizer
+// state, the replica's input rows (stage 0) and targets (last stage, training)
+__device__ inline uint64_t resident(const Ctx &x, int s)
+{
+    const int l0 = stage_l0(x, s), nl = stage_nl(x, s);
+    uint64_t N = 0;
+    if (x.mlp) {
+        for (int i = l0; i < l0 + nl; ++i) {
+            uint64_t din, dout;
+            mlp_dims(x, mlp_kind(x, i), din, dout);
+            N += din * dout;
+        }
+    } else {
+        N = (uint64_t)nl * (x.d * 3 * x.dH + x.dH * x.d + x.d * x.FH + x.FH * x.d);
+        if (s == 0) N += x.Vh * x.d;
+        if (s == x.P - 1) N += x.d * x.Vh;
+    }
+    uint64_t b = x.e * N + opt_state(x, N);
+    if (s == 0) b += input_row(x) * x.rows;
+    if (s == x.P - 1 && x.train) b += input_row(x) * x.rows;
+    return b;
+}
+
+// K > 1: split the replica's whole input (stage 0) or target (last stage)
+// into microbatches; a copy whose source dies
+template <class S>
+__device__ __forceinline__ void split(const Ctx &x, S &o)
+{
+    const uint64_t whole = input_row(x) * x.rows;
+    o.local(0, 2 * whole, whole, whole);
+}
+
+// ---------------------------------------------------------------------------
+// Synchronous 1F1B (training) or forward-only (inference) block order
+// ---------------------------------------------------------------------------
+// position `pos` of stage s's block sequence -> (is_backward, microbatch)
+__device__ __forceinline__ void block_at(const Ctx &x, int s, int pos, bool &bwd, int &k)
+{
+    if (!x.train) {
+        bwd = false;
+        k = pos;
+        return;
+    }
+    const int w = (x.P - 1 - s) < x.K ? (x.P - 1 - s) : x.K;
+    if (pos < w) {
+        bwd = false;
+        k = pos;
+    } else if (pos < w + 2 * (x.K - w)) {
+        const int j = pos - w;
+        bwd = (j & 1) != 0;
+        k = bwd ? (j - 1) / 2 : w + j / 2;
+    } else {
+        bwd = true;
+        k = pos - w - (x.K - w);
+    }
+}
+
+// bytes sent after a block, and the bytes the sender frees
+__device__ __forceinline__ void send_size(const Ctx &x, int s, int k, bool bwd, uint64_t &sz, uint64_t &fre)
+{
+    if (x.mlp) {
+        sz = bwd ? mlp_grad_out(x, s, k) : mlp_act_out(x, s, k);
+        fre = (bwd || !x.train) ? sz : 0;
+    } else {
+        sz = x.e * mb_rows(x, k) * x.seq * x.d;
+        fre = sz;
+    }
+}
+
+}  // namespace dsim

@@ -1,35 +1,57 @@
 // parametric.hip -- simulate the D/H/P/K transform without building op lists.
 //
-// One lane per candidate.  The lane expands, on the fly and in program order,
-// the distributed program the transform of Sec. 4 produces (Fig. 2 is its
-// P = 2, K = 2 instance) and simulates it with the semantics of Sec. 2.1 and
-// the cost model of Sec. 3.3:
-//   * pipeline stages hold contiguous layer ranges (L = q*P + r: the first r
-//     stages get q + 1 layers) and run synchronous 1F1B: w = min(P-1-s, K)
-//     warm-up forwards, then forward/backward pairs, then w backwards;
-//   * the global order is slot by slot: every stage, ascending, runs its next
-//     block if the block's input was produced in an earlier slot, then the
-//     slot's Sends run ascending by source stage; the weight update follows;
+// Each candidate gets a segment of W = 2^ceil(log2 P) lanes of a wavefront,
+// one lane per pipeline stage; segments of equal width share wavefronts
+// (64 / W candidates each).  A lane expands, on the fly and in program order,
+// the ops of its stage of the distributed program the transform of Sec. 4
+// produces (ops in model.h) and simulates them with the semantics of Sec. 2.1
+// and the cost model of Sec. 3.3:
+//   * synchronous 1F1B (training) or forward-only (inference) per stage;
+//   * the global order is slot by slot: every stage runs its next block if
+//     the block's input was produced in an earlier slot (the stages of a slot
+//     touch disjoint devices, so they run in parallel lanes); then the slot's
+//     Sends run in ascending order of source stage, a serial chain of
+//     max-plus steps across neighbouring lanes (DPP wave shifts); the weight
+//     update follows the last slot;
 //   * every replica (d, h) of a stage runs the same ops at the same times, so
-//     the lane walks one replica per stage: a collective over the H ranks or
-//     the D replicas starts at the stage's own clock and costs the ring
+//     one replica per stage is walked: a collective over the H ranks or the
+//     D replicas starts at the stage's own clock and costs the ring
 //     all-reduce of its full group; a Send synchronises two stage clocks.
-// Live memory follows def/use liveness of the transform's tensors, written
-// here in closed form: every op allocates its outputs, the peak is sampled,
-// then the tensors whose last use is this op are freed.
 //
-// Stage state (clock, live and peak bytes, schedule counters) lives in LDS,
-// laid out [stage][lane] with one 64-lane wavefront per workgroup; the
-// per-op arithmetic stays in VGPRs.
-#include "internal.h"
+// The layers of a stage repeat one op sequence (for the MLP with H > 1, one
+// column/row layer pair), so each lane records that sequence's op costs once
+// per microbatch size and direction (LDS, [entry][lane]) together with its
+// memory summary (net bytes, peak above the starting live bytes, op counts),
+// and walks a block's layers as a chain of fp64 adds over the recorded costs.
+// Adding the same costs in the same order gives the same rounding as the op
+// by op walk, and the memory summary is exact integer arithmetic.  Ops outside
+// the repeating part (embedding, LM head, loss, the stage's first MLP layer in
+// backward, the last layer in inference) and backward blocks of microbatch 0
+// (which have no gradient accumulation) are walked op by op.
+//
+// A counting-sort pre-pass groups the candidates by segment width into a
+// temporary permutation (stable, so the grid's own order keeps wavefronts
+// uniform in K).
+#include "model.h"
 
 namespace dsim {
 namespace {
 
 constexpr int kLanes = 64;
-constexpr int kMaxStages = 64;
-constexpr int kMaxK = 16383;
-constexpr uint16_t kNoBlock = 0xffffu;
+constexpr int kClasses = 7;       // segment widths 1, 2, 4, ..., 64
+constexpr int kScanBlock = 256;
+constexpr int kPat2 = 12;         // pattern capacity per direction, in double2
+
+// pattern sizes (double2 entries) per model family
+template <bool TF> struct PatSize;
+template <> struct PatSize<true> {
+    static constexpr int F2 = 7;    // 12 compute ops + 2 all-reduces
+    static constexpr int B2 = 12;   // 17 compute + 4 accumulations + 2 all-reduces
+};
+template <> struct PatSize<false> {
+    static constexpr int F2 = 3;    // column layer (2 ops) + row layer (3)
+    static constexpr int B2 = 5;    // row layer (4 ops) + column layer (5)
+};
 
 struct ParArgs {
     dsim_model m;
@@ -37,6 +59,8 @@ struct ParArgs {
     int64_t n_cand;
     int32_t row_width;
     int32_t p_bound;
+    const uint32_t *perm;   // candidates grouped by segment class
+    const uint32_t *meta;   // [0,8) class totals, [8,16) first perm index, [16,24) first lane
     double *makespan;
     double *finish;
     uint64_t *peak;
@@ -47,570 +71,470 @@ struct ParArgs {
     CostConsts c;
 };
 
-// Per-candidate constants.
-struct Ctx {
-    int D, H, P, K, L, q, r;
-    bool train, mlp;
-    int mode;
-    uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
-    uint64_t dH, FH, Vh, aH;
-    double inv_f, inv_b, inv_l, lat, launch;
-    double arl_h, arc_h, arl_d, arc_d;
-    uint64_t mult_dev, mult_tp, mult_dp;
-};
+__device__ __forceinline__ int seg_class(const dsim_strategy &st, int p_bound)
+{
+    const int P = st.P;
+    if (P < 1 || P > p_bound) return 0;
+    int j = 0;
+    while ((1 << j) < P) ++j;
+    return j;
+}
 
-// One stage's running state while a block of its ops is walked.
-struct Acc {
+// ---------------------------------------------------------------------------
+// Sinks
+// ---------------------------------------------------------------------------
+// The lane's stage replica, op by op.
+struct Walk {
+    const Ctx &x;
     double clk;
-    uint64_t live, peak;
-};
-
-struct Counters {
+    int64_t live, peak;
     uint64_t walked, nops;
+
+    __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        clk = clk + cost_local(x, fl, by);
+        live += (int64_t)al;
+        peak = live > peak ? live : peak;
+        live -= (int64_t)fr;
+        walked += 1;
+        nops += x.mult_dev;
+    }
+    __device__ __forceinline__ void ar_tp(uint64_t by)
+    {
+        if (x.H <= 1) return;
+        clk = clk + cost_ar_tp(x, by);
+        walked += 1;
+        nops += x.mult_tp;
+    }
+    __device__ __forceinline__ void ar_dp(uint64_t by)
+    {
+        if (x.D <= 1) return;
+        clk = clk + cost_ar_dp(x, by);
+        walked += 1;
+        nops += x.mult_dp;
+    }
 };
 
-__device__ __forceinline__ uint64_t umax(uint64_t a, uint64_t b) { return a > b ? a : b; }
-
-// local compute op on every replica of the stage
-__device__ __forceinline__ void op_local(const Ctx &x, Acc &a, Counters &n, uint64_t flops, uint64_t bytes,
-                                         uint64_t alloc, uint64_t fre)
-{
-    const double tf = (double)flops * x.inv_f;
-    const double tb = (double)bytes * x.inv_b;
-    a.clk = a.clk + (x.launch + (tf > tb ? tf : tb));
-    a.live += alloc;
-    a.peak = umax(a.peak, a.live);
-    a.live -= fre;
-    n.walked += 1;
-    n.nops += x.mult_dev;
-}
-
-// all-reduce over the H ranks of each data replica (in place)
-__device__ __forceinline__ void op_ar_tp(const Ctx &x, Acc &a, Counters &n, uint64_t bytes)
-{
-    if (x.H <= 1) return;
-    a.clk = a.clk + (x.arl_h + x.arc_h * ((double)bytes * x.inv_l));
-    n.walked += 1;
-    n.nops += x.mult_tp;
-}
-
-// all-reduce over the D replicas of each tensor rank (in place)
-__device__ __forceinline__ void op_ar_dp(const Ctx &x, Acc &a, Counters &n, uint64_t bytes)
-{
-    if (x.D <= 1) return;
-    a.clk = a.clk + (x.arl_d + x.arc_d * ((double)bytes * x.inv_l));
-    n.walked += 1;
-    n.nops += x.mult_dp;
-}
-
-__device__ __forceinline__ uint64_t mb_rows(const Ctx &x, int k)
-{
-    return x.mq + ((uint64_t)k < x.mr ? 1u : 0u);
-}
-
-__device__ __forceinline__ int stage_l0(const Ctx &x, int s) { return s * x.q + (s < x.r ? s : x.r); }
-__device__ __forceinline__ int stage_nl(const Ctx &x, int s) { return x.q + (s < x.r ? 1 : 0); }
-
-// ---------------------------------------------------------------------------
-// MLP (Fig. 2: @dense = Gemm + Relu): with H > 1 even layers are
-// column-parallel (W: d x d/H), odd layers row-parallel (W: d/H x d) with an
-// all-reduce of their output; dX of column-parallel layers is all-reduced in
-// the backward pass (layer 0's dX is computed and discarded).
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void mlp_dims(const Ctx &x, int i, uint64_t &din, uint64_t &dout, bool &row)
-{
-    const bool col = x.H > 1 && (i & 1) == 0;
-    row = x.H > 1 && (i & 1) == 1;
-    din = row ? x.d / (uint64_t)x.H : x.d;
-    dout = col ? x.d / (uint64_t)x.H : x.d;
-}
-
-__device__ void mlp_fwd(const Ctx &x, Acc &a, Counters &n, int s, int k)
-{
-    const uint64_t m = mb_rows(x, k), e = x.e;
-    const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
-    for (int i = l0; i < l1; ++i) {
-        uint64_t din, dout;
-        bool row;
-        mlp_dims(x, i, din, dout, row);
-        // Gemm: the layer input dies here in inference (it is kept for the
-        // weight gradient in training)
-        op_local(x, a, n, 2 * m * din * dout, e * (m * din + din * dout + m * dout), e * m * dout,
-                 x.train ? 0 : e * m * din);
-        if (row) op_ar_tp(x, a, n, e * m * dout);
-        // Relu frees the pre-activation; the last layer's output has no use
-        // in inference
-        const bool dead_out = !x.train && i == x.L - 1;
-        op_local(x, a, n, m * dout, 2 * e * m * dout, e * m * dout, e * m * dout + (dead_out ? e * m * dout : 0));
-    }
-}
-
-__device__ void mlp_bwd(const Ctx &x, Acc &a, Counters &n, int s, int k)
-{
-    const uint64_t m = mb_rows(x, k), e = x.e;
-    const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
-    if (s == x.P - 1) op_local(x, a, n, 3 * m * x.d, 3 * e * m * x.d, e * m * x.d, e * m * x.d);   // loss grad, y_k dies
-    for (int i = l1 - 1; i >= l0; --i) {
-        uint64_t din, dout;
-        bool row;
-        mlp_dims(x, i, din, dout, row);
-        // ReluGrad(da, a): both die
-        op_local(x, a, n, m * dout, 3 * e * m * dout, e * m * dout, 2 * e * m * dout);
-        // weight gradient; the stage's input dies at its first layer
-        op_local(x, a, n, 2 * m * din * dout, e * (m * din + m * dout + din * dout), e * din * dout,
-                 i == l0 ? e * m * din : 0);
-        if (k >= 1) op_local(x, a, n, din * dout, 3 * e * din * dout, 0, e * din * dout);   // accumulate
-        // input gradient; dh dies; layer 0's dX has no use
-        op_local(x, a, n, 2 * m * din * dout, e * (m * dout + din * dout + m * din), e * m * din,
-                 e * m * dout + (i == 0 ? e * m * din : 0));
-        if (!row && x.H > 1 && i != 0) op_ar_tp(x, a, n, e * m * din);
-    }
-}
-
-// bytes of the activation a stage sends forward / backward
-__device__ __forceinline__ uint64_t mlp_act_out(const Ctx &x, int s, int k)
-{
-    uint64_t din, dout;
-    bool row;
-    mlp_dims(x, stage_l0(x, s) + stage_nl(x, s) - 1, din, dout, row);
-    return x.e * mb_rows(x, k) * dout;
-}
-
-__device__ __forceinline__ uint64_t mlp_grad_out(const Ctx &x, int s, int k)
-{
-    uint64_t din, dout;
-    bool row;
-    mlp_dims(x, stage_l0(x, s), din, dout, row);
-    return x.e * mb_rows(x, k) * din;
-}
-
-// ---------------------------------------------------------------------------
-// Transformer (GPT-2-shaped decoder, Megatron tensor parallelism: QKV and
-// fc1 column-parallel, out-proj and fc2 row-parallel with an all-reduce of
-// their output; vocabulary-parallel embedding and LM head, ceil(V/H) rows per
-// rank).
-// ---------------------------------------------------------------------------
-struct TfSz {
-    uint64_t m, T, ACT, QKV, OH, S2, FF, LOG, ST, IDS;
+// Memory and op-count summary of one repeating unit.
+struct Summary {
+    int64_t delta;     // live bytes after the unit minus before
+    int64_t top;       // max over the unit's ops of (live after alloc) minus live before
+    uint64_t walked;   // ops walked per unit
+    uint64_t nops;     // program ops per unit
 };
 
-__device__ __forceinline__ TfSz tf_sizes(const Ctx &x, int k)
-{
-    TfSz z;
-    z.m = mb_rows(x, k);
-    z.T = z.m * x.seq;
-    z.ACT = x.e * z.T * x.d;
-    z.QKV = x.e * z.T * 3 * x.dH;
-    z.OH = x.e * z.T * x.dH;
-    z.S2 = x.e * z.m * x.aH * x.seq * x.seq;
-    z.FF = x.e * z.T * x.FH;
-    z.LOG = x.e * z.T * x.Vh;
-    z.ST = 12 * z.T;
-    z.IDS = 4 * z.T;
-    return z;
-}
+// Records a unit's op costs into the lane's LDS pattern and summarises it.
+struct Record {
+    const Ctx &x;
+    double *base;      // entry j at base[(j / 2) * 2 * kLanes + (j & 1)]
+    int n;
+    int64_t cur, top;
+    uint64_t walked, nops;
 
-__device__ void tf_fwd(const Ctx &x, Acc &a, Counters &n, int s, int k)
-{
-    const TfSz z = tf_sizes(x, k);
-    const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S = x.seq;
-    const bool tr = x.train;
-    if (s == 0) {
-        op_local(x, a, n, T * d, 2 * z.ACT + z.IDS, z.ACT, tr ? 0 : z.IDS);   // embedding; ids die in inference
-        op_ar_tp(x, a, n, z.ACT);
+    __device__ __forceinline__ void put(double c)
+    {
+        base[(n >> 1) * 2 * kLanes + (n & 1)] = c;
+        ++n;
     }
-    const int nl = stage_nl(x, s);
-    for (int i = 0; i < nl; ++i) {
-        op_local(x, a, n, 8 * T * d, 2 * z.ACT, z.ACT, 0);                                               // LN1
-        op_local(x, a, n, 2 * T * d * 3 * dH, e * (T * d + d * 3 * dH + T * 3 * dH), z.QKV, tr ? 0 : z.ACT);  // QKV
-        op_local(x, a, n, 2 * T * S * dH, 2 * z.OH + z.S2, z.S2, 0);                                     // scores
-        op_local(x, a, n, 5 * z.m * x.aH * S * S, 2 * z.S2, z.S2, z.S2);                                 // softmax
-        op_local(x, a, n, 2 * T * S * dH, z.S2 + 2 * z.OH, z.OH, tr ? 0 : z.S2 + z.QKV);                // P.V
-        op_local(x, a, n, 2 * T * dH * d, e * (T * dH + dH * d + T * d), z.ACT, tr ? 0 : z.OH);          // out-proj
-        op_ar_tp(x, a, n, z.ACT);
-        op_local(x, a, n, T * d, 3 * z.ACT, z.ACT, tr ? z.ACT : 2 * z.ACT);                             // residual
-        op_local(x, a, n, 8 * T * d, 2 * z.ACT, z.ACT, 0);                                               // LN2
-        op_local(x, a, n, 2 * T * d * FH, e * (T * d + d * FH + T * FH), z.FF, tr ? 0 : z.ACT);          // fc1
-        op_local(x, a, n, 8 * T * FH, 2 * z.FF, z.FF, tr ? 0 : z.FF);                                   // GeLU
-        op_local(x, a, n, 2 * T * FH * d, e * (T * FH + FH * d + T * d), z.ACT, tr ? 0 : z.FF);          // fc2
-        op_ar_tp(x, a, n, z.ACT);
-        op_local(x, a, n, T * d, 3 * z.ACT, z.ACT, tr ? z.ACT : 2 * z.ACT);                             // residual
+    __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        put(cost_local(x, fl, by));
+        const int64_t a = cur + (int64_t)al;
+        top = a > top ? a : top;
+        cur = a - (int64_t)fr;
+        walked += 1;
+        nops += x.mult_dev;
     }
-    if (s == x.P - 1) {
-        op_local(x, a, n, 8 * T * d, 2 * z.ACT, z.ACT, tr ? 0 : z.ACT);                                  // final LN
-        op_local(x, a, n, 2 * T * d * x.Vh, e * (T * d + d * x.Vh + T * x.Vh), z.LOG,
-                 tr ? 0 : z.ACT + z.LOG);                                                                // LM head
+    __device__ __forceinline__ void ar_tp(uint64_t by)
+    {
+        if (x.H <= 1) return;
+        put(cost_ar_tp(x, by));
+        walked += 1;
+        nops += x.mult_tp;
     }
-}
+    __device__ __forceinline__ void ar_dp(uint64_t by)
+    {
+        if (x.D <= 1) return;
+        put(cost_ar_dp(x, by));
+        walked += 1;
+        nops += x.mult_dp;
+    }
+};
 
-__device__ void tf_bwd(const Ctx &x, Acc &a, Counters &n, int s, int k)
+// The repeating unit: one transformer layer; one MLP layer (H = 1) or one
+// column/row pair (H > 1), in the block's walk order.  Records with
+// accumulation (microbatches >= 1), outside every stage boundary.
+template <bool TF>
+__device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, double *base, Summary &out)
 {
-    const TfSz z = tf_sizes(x, k);
-    const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S = x.seq, Vh = x.Vh;
-    const bool acc = k >= 1;
-    if (s == x.P - 1) {
-        op_local(x, a, n, 3 * T * Vh, z.LOG + z.ST, z.ST, 0);                                 // loss statistics
-        op_ar_tp(x, a, n, z.ST);
-        op_local(x, a, n, 2 * T * Vh, 2 * z.LOG + z.ST + z.IDS, z.LOG, z.LOG + z.ST + z.IDS); // dlogits
-        op_local(x, a, n, 2 * T * d * Vh, e * (T * Vh + d * Vh + T * d), z.ACT, 0);           // LM head dX
-        op_ar_tp(x, a, n, z.ACT);
-        op_local(x, a, n, 2 * T * d * Vh, e * (T * d + T * Vh + d * Vh), e * d * Vh, z.ACT + z.LOG);  // LM head dW
-        if (acc) op_local(x, a, n, d * Vh, 3 * e * d * Vh, 0, e * d * Vh);
-        op_local(x, a, n, 8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                           // final LN grad
-    }
-    const int nl = stage_nl(x, s);
-    for (int i = 0; i < nl; ++i) {
-        op_local(x, a, n, 2 * T * FH * d, e * (T * d + FH * d + T * FH), z.FF, 0);            // fc2 dX
-        op_local(x, a, n, 2 * T * FH * d, e * (T * FH + T * d + FH * d), e * FH * d, z.FF);   // fc2 dW
-        if (acc) op_local(x, a, n, FH * d, 3 * e * FH * d, 0, e * FH * d);
-        op_local(x, a, n, 8 * T * FH, 3 * z.FF, z.FF, 2 * z.FF);                              // GeLU grad
-        op_local(x, a, n, 2 * T * d * FH, e * (T * FH + d * FH + T * d), z.ACT, 0);           // fc1 dX
-        op_ar_tp(x, a, n, z.ACT);
-        op_local(x, a, n, 2 * T * d * FH, e * (T * d + T * FH + d * FH), e * d * FH, z.ACT + z.FF);  // fc1 dW
-        if (acc) op_local(x, a, n, d * FH, 3 * e * d * FH, 0, e * d * FH);
-        op_local(x, a, n, 8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                            // LN2 grad
-        op_local(x, a, n, T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                // residual merge
-        op_local(x, a, n, 2 * T * dH * d, e * (T * d + dH * d + T * dH), z.OH, 0);            // out-proj dX
-        op_local(x, a, n, 2 * T * dH * d, e * (T * dH + T * d + dH * d), e * dH * d, z.OH);   // out-proj dW
-        if (acc) op_local(x, a, n, dH * d, 3 * e * dH * d, 0, e * dH * d);
-        op_local(x, a, n, 4 * T * S * dH, 2 * z.S2 + 3 * z.OH, z.S2 + z.QKV, z.OH);           // P.V grads
-        op_local(x, a, n, 5 * z.m * x.aH * S * S, 3 * z.S2, z.S2, 2 * z.S2);                  // softmax grad
-        op_local(x, a, n, 4 * T * S * dH, z.S2 + 4 * z.OH, 0, z.S2 + z.QKV);                  // Q.K^T grads
-        op_local(x, a, n, 2 * T * 3 * dH * d, e * (T * 3 * dH + 3 * dH * d + T * d), z.ACT, 0);  // QKV dX
-        op_ar_tp(x, a, n, z.ACT);
-        op_local(x, a, n, 2 * T * d * 3 * dH, e * (T * d + T * 3 * dH + d * 3 * dH), e * d * 3 * dH,
-                 z.ACT + z.QKV);                                                               // QKV dW
-        if (acc) op_local(x, a, n, d * 3 * dH, 3 * e * d * 3 * dH, 0, e * d * 3 * dH);
-        op_local(x, a, n, 8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                            // LN1 grad
-        op_local(x, a, n, T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                // residual merge
-    }
-    if (s == 0) {
-        op_local(x, a, n, T * d, z.ACT + z.IDS + e * Vh * d, e * Vh * d, z.ACT + z.IDS);      // embedding dW
-        if (acc) op_local(x, a, n, Vh * d, 3 * e * Vh * d, 0, e * Vh * d);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Optimizer, inputs, splits and the weight update
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void opt_cost(const Ctx &x, uint64_t N, uint64_t &flops, uint64_t &bytes)
-{
-    if (x.mode == DSIM_TRAIN_SGD) {
-        flops = 2 * N;
-        bytes = 3 * x.e * N;
-    } else if (x.mode == DSIM_TRAIN_ADAM) {
-        flops = 12 * N;
-        bytes = 7 * x.e * N;
-    } else {
-        flops = 12 * N;
-        bytes = 28 * N;
-    }
-}
-
-__device__ __forceinline__ uint64_t opt_state(const Ctx &x, uint64_t N)
-{
-    if (!x.train) return 0;
-    if (x.mode == DSIM_TRAIN_ADAM) return 2 * x.e * N;
-    if (x.mode == DSIM_TRAIN_ADAM_MIXED) return 12 * N;
-    return 0;
-}
-
-__device__ __forceinline__ void wu_param(const Ctx &x, Acc &a, Counters &n, uint64_t N)
-{
-    op_ar_dp(x, a, n, x.e * N);
-    uint64_t fl, by;
-    opt_cost(x, N, fl, by);
-    op_local(x, a, n, fl, by, 0, x.e * N);   // the gradient dies
-}
-
-__device__ void weight_update(const Ctx &x, Acc &a, Counters &n, int s)
-{
-    const int l0 = stage_l0(x, s), nl = stage_nl(x, s);
-    if (x.mlp) {
-        for (int i = l0; i < l0 + nl; ++i) {
-            uint64_t din, dout;
-            bool row;
-            mlp_dims(x, i, din, dout, row);
-            wu_param(x, a, n, din * dout);
-        }
-        return;
-    }
-    const uint64_t d = x.d;
-    if (s == 0) wu_param(x, a, n, x.Vh * d);
-    for (int i = 0; i < nl; ++i) {
-        wu_param(x, a, n, d * 3 * x.dH);
-        wu_param(x, a, n, x.dH * d);
-        wu_param(x, a, n, d * x.FH);
-        wu_param(x, a, n, x.FH * d);
-    }
-    if (s == x.P - 1) wu_param(x, a, n, d * x.Vh);
-}
-
-// bytes of one row (sequence) of the stage-0 input / last-stage target
-__device__ __forceinline__ uint64_t input_row(const Ctx &x) { return x.mlp ? x.e * x.d : 4 * x.seq; }
-
-__device__ uint64_t resident(const Ctx &x, int s)
-{
-    const int l0 = stage_l0(x, s), nl = stage_nl(x, s);
-    uint64_t N = 0;
-    if (x.mlp) {
-        for (int i = l0; i < l0 + nl; ++i) {
-            uint64_t din, dout;
-            bool row;
-            mlp_dims(x, i, din, dout, row);
-            N += din * dout;
+    Record r{x, base, 0, 0, 0, 0, 0};
+    if (TF) {
+        const TfSz z = tf_sizes(x, m);
+        if (bwd) tf_layer_bwd(x, r, z, true);
+        else tf_layer_fwd(x, r, z);
+    } else if (bwd) {
+        if (x.H > 1) {
+            mlp_layer_bwd(x, r, m, kRow, false, false, true);
+            mlp_layer_bwd(x, r, m, kCol, false, false, true);
+        } else {
+            mlp_layer_bwd(x, r, m, kPlain, false, false, true);
         }
     } else {
-        N = (uint64_t)nl * (x.d * 3 * x.dH + x.dH * x.d + x.d * x.FH + x.FH * x.d);
-        if (s == 0) N += x.Vh * x.d;
-        if (s == x.P - 1) N += x.d * x.Vh;
-    }
-    uint64_t b = x.e * N + opt_state(x, N);
-    if (s == 0) b += input_row(x) * x.rows;
-    if (s == x.P - 1 && x.train) b += input_row(x) * x.rows;
-    return b;
-}
-
-__device__ __forceinline__ void split(const Ctx &x, Acc &a, Counters &n)
-{
-    const uint64_t whole = input_row(x) * x.rows;
-    op_local(x, a, n, 0, 2 * whole, whole, whole);
-}
-
-// ---------------------------------------------------------------------------
-// The kernel
-// ---------------------------------------------------------------------------
-__device__ bool strategy_ok(const dsim_model &m, int D, int H, int P, int K)
-{
-    if (D < 1 || H < 1 || P < 1 || K < 1) return false;
-    const int64_t B = m.global_batch;
-    if (B % D != 0 || (int64_t)K > B / D || P > m.n_layers) return false;
-    if (m.family == DSIM_MLP) {
-        if (m.d_model % H != 0) return false;
-        if (H > 1) {
-            const int q = m.n_layers / P, r = m.n_layers % P;
-            if ((q & 1) != 0 && r < P) return false;          // stages with q layers
-            if (r > 0 && ((q + 1) & 1) != 0) return false;    // stages with q + 1 layers
+        if (x.H > 1) {
+            mlp_layer_fwd(x, r, m, kCol, false);
+            mlp_layer_fwd(x, r, m, kRow, false);
+        } else {
+            mlp_layer_fwd(x, r, m, kPlain, false);
         }
-        return true;
     }
-    return m.n_heads % H == 0 && m.d_model % H == 0 && m.d_ff % H == 0;
+    while (r.n < 2 * PatSize<TF>::B2) r.put(0.0);   // x + 0.0 == x for the clocks
+    out.delta = r.cur;
+    out.top = r.top;
+    out.walked = r.walked;
+    out.nops = r.nops;
 }
 
-// position `pos` of stage s's block sequence -> (is_backward, microbatch)
-__device__ __forceinline__ void block_at(const Ctx &x, int s, int pos, bool &bwd, int &k)
+// n repetitions of a unit: clocks by the recorded adds, memory in closed form
+template <int N2>
+__device__ __forceinline__ void walk_units(Walk &w, const double2 *pp, const Summary &sm, int n)
 {
-    if (!x.train) {
-        bwd = false;
-        k = pos;
-        return;
+    if (n <= 0) return;
+    double2 r[N2];
+#pragma unroll
+    for (int j = 0; j < N2; ++j) r[j] = pp[j * kLanes];
+    double clk = w.clk;
+    for (int u = 0; u < n; ++u) {
+#pragma unroll
+        for (int j = 0; j < N2; ++j) {
+            clk = clk + r[j].x;
+            clk = clk + r[j].y;
+        }
     }
-    const int w = (x.P - 1 - s) < x.K ? (x.P - 1 - s) : x.K;
-    if (pos < w) {
-        bwd = false;
-        k = pos;
-    } else if (pos < w + 2 * (x.K - w)) {
-        const int j = pos - w;
-        bwd = (j & 1) != 0;
-        k = bwd ? (j - 1) / 2 : w + j / 2;
-    } else {
-        bwd = true;
-        k = pos - w - (x.K - w);
-    }
+    w.clk = clk;
+    // unit u starts at live + u * delta; its highest point is that plus top
+    const int64_t hi = w.live + sm.top + (sm.delta > 0 ? (int64_t)(n - 1) * sm.delta : 0);
+    w.peak = hi > w.peak ? hi : w.peak;
+    w.live += (int64_t)n * sm.delta;
+    w.walked += (uint64_t)n * sm.walked;
+    w.nops += (uint64_t)n * sm.nops;
 }
 
+// ---------------------------------------------------------------------------
+// Cross-lane helpers
+// ---------------------------------------------------------------------------
+// lane i receives lane i-1's value (0 at lane 0) / lane i+1's (0 at lane 63)
+__device__ __forceinline__ int shr1(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x138, 0xf, 0xf, true); }
+__device__ __forceinline__ int shl1(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x130, 0xf, 0xf, true); }
+__device__ __forceinline__ double shr1(double v)
+{
+    return __hiloint2double(shr1(__double2hiint(v)), shr1(__double2loint(v)));
+}
+__device__ __forceinline__ double shl1(double v)
+{
+    return __hiloint2double(shl1(__double2hiint(v)), shl1(__double2loint(v)));
+}
+__device__ __forceinline__ uint64_t shr1(uint64_t v)
+{
+    return ((uint64_t)(uint32_t)shr1((int)(v >> 32)) << 32) | (uint32_t)shr1((int)(uint32_t)v);
+}
+__device__ __forceinline__ uint64_t shl1(uint64_t v)
+{
+    return ((uint64_t)(uint32_t)shl1((int)(v >> 32)) << 32) | (uint32_t)shl1((int)(uint32_t)v);
+}
+
+__device__ __forceinline__ uint64_t ballot(bool b) { return __ballot(b); }
+
+// OR of the W-bit segments of a wave mask, in the low W bits
+__device__ __forceinline__ uint64_t fold_segments(uint64_t m, int W)
+{
+    for (int sh = 32; sh >= W; sh >>= 1) m |= m >> sh;
+    return W == 64 ? m : (m & ((1ull << W) - 1));
+}
+
+template <class T, class Op>
+__device__ __forceinline__ T seg_reduce(T v, int W, Op op)
+{
+    for (int o = 1; o < W; o <<= 1) v = op(v, __shfl_xor(v, o, kLanes));
+    return v;
+}
+
+// ---------------------------------------------------------------------------
+// The simulation kernel
+// ---------------------------------------------------------------------------
+template <bool TF>
 __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
 {
-    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int F2 = PatSize<TF>::F2, B2 = PatSize<TF>::B2;
+    __shared__ double2 s_pat[2][kPat2][kLanes];   // [backward][entry pair][lane]
+
     const int lane = threadIdx.x;
-    const int PB = g.p_bound;
-    double *s_clk = reinterpret_cast<double *>(smem);
-    uint64_t *s_live = reinterpret_cast<uint64_t *>(s_clk + PB * kLanes);
-    uint64_t *s_peak = s_live + PB * kLanes;
-    uint16_t *s_pos = reinterpret_cast<uint16_t *>(s_peak + PB * kLanes);
-    uint16_t *s_nf = s_pos + PB * kLanes;
-    uint16_t *s_nb = s_nf + PB * kLanes;
-    uint16_t *s_em = s_nb + PB * kLanes;
-#define AT(s) ((s) * kLanes + lane)
+    const uint32_t gl = blockIdx.x * (uint32_t)kLanes;
+    if (gl >= g.meta[16 + kClasses]) return;      // beyond the last class (whole wave)
+    int cls = 0;
+    while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
+    const int W = 1 << cls;
+    const uint32_t local = gl + lane - g.meta[16 + cls];
+    const uint32_t slot = local >> cls;
+    const int li = (int)(local & (uint32_t)(W - 1));   // stage of this lane
+    const int64_t c = slot < g.meta[cls] ? (int64_t)g.perm[g.meta[8 + cls] + slot] : -1;
 
-    const int64_t c = (int64_t)blockIdx.x * kLanes + lane;
-    if (c >= g.n_cand) return;
-    const dsim_strategy st = g.cand[c];
     const dsim_model &M = g.m;
-    int32_t status = 0;
-    const bool ok = strategy_ok(M, st.D, st.H, st.P, st.K) && st.P <= PB && st.K <= kMaxK;
+    Ctx x = {};
+    bool ok = false;
+    if (c >= 0) {
+        const dsim_strategy st = g.cand[c];
+        ok = strategy_ok(M, st.D, st.H, st.P, st.K) && st.P <= g.p_bound && st.P <= W && st.K <= kMaxK;
+        if (ok) make_ctx(M, g.c, st, x);
+    }
+    const int P = ok ? x.P : 0;
+    const int s = li;
+    bool live_stage = s < P;
+    int32_t status = (c >= 0 && !ok) ? DSIM_ST_BAD_STRATEGY : 0;
 
-    Ctx x;
-    x.D = st.D; x.H = st.H; x.P = st.P; x.K = st.K;
-    x.L = M.n_layers;
-    x.mlp = M.family == DSIM_MLP;
-    x.mode = M.mode;
-    x.train = M.mode != DSIM_INFER;
-    double mk = 0.0;
-    uint64_t cp = 0;
-    Counters n{0, 0};
-    if (!ok) {
-        status = DSIM_ST_BAD_STRATEGY;
-    } else {
-        x.q = x.L / x.P;
-        x.r = x.L % x.P;
-        x.e = (uint64_t)M.elem_bytes;
-        x.d = (uint64_t)M.d_model;
-        x.dff = (uint64_t)M.d_ff;
-        x.seq = (uint64_t)M.seq_len;
-        x.vocab = (uint64_t)M.vocab;
-        x.heads = (uint64_t)M.n_heads;
-        x.rows = (uint64_t)M.global_batch / (uint64_t)x.D;
-        x.mq = x.rows / (uint64_t)x.K;
-        x.mr = x.rows % (uint64_t)x.K;
-        x.dH = x.d / (uint64_t)x.H;
-        x.FH = x.mlp ? 0 : x.dff / (uint64_t)x.H;
-        x.Vh = x.mlp ? 0 : (x.vocab + (uint64_t)x.H - 1) / (uint64_t)x.H;
-        x.aH = x.mlp ? 0 : x.heads / (uint64_t)x.H;
-        x.inv_f = g.c.inv_f;
-        x.inv_b = g.c.inv_b;
-        x.inv_l = g.c.inv_l;
-        x.lat = g.c.lat;
-        x.launch = g.c.launch;
-        {
-            const double ah = 2.0 * (double)(x.H - 1), ad = 2.0 * (double)(x.D - 1);
-            x.arl_h = ah * x.lat;
-            x.arc_h = ah / (double)x.H;
-            x.arl_d = ad * x.lat;
-            x.arc_d = ad / (double)x.D;
-        }
-        x.mult_dev = (uint64_t)x.D * (uint64_t)x.H;
-        x.mult_tp = (uint64_t)x.D;
-        x.mult_dp = (uint64_t)x.H;
-
-        for (int s = 0; s < x.P; ++s) {
-            const uint64_t r0 = resident(x, s);
-            s_clk[AT(s)] = 0.0;
-            s_live[AT(s)] = r0;
-            s_peak[AT(s)] = r0;
-            s_pos[AT(s)] = 0;
-            s_nf[AT(s)] = 0;
-            s_nb[AT(s)] = 0;
-        }
+    Walk w{x, 0.0, 0, 0, 0, 0};
+    int pos = 0, nf = 0, nb = 0, len = 0;
+    int pat_f = -1, pat_b = -1;   // microbatch size class each pattern was recorded for
+    Summary sum_f{}, sum_b{};
+    if (live_stage) {
+        const int64_t r0 = (int64_t)resident(x, s);
+        w.live = r0;
+        w.peak = r0;
+        len = x.train ? 2 * x.K : x.K;
         // microbatch splits before the pipeline
         if (x.K > 1) {
-            Acc a{s_clk[AT(0)], s_live[AT(0)], s_peak[AT(0)]};
-            split(x, a, n);
-            s_clk[AT(0)] = a.clk; s_live[AT(0)] = a.live; s_peak[AT(0)] = a.peak;
-            if (x.train) {
-                const int t = x.P - 1;
-                Acc b{s_clk[AT(t)], s_live[AT(t)], s_peak[AT(t)]};
-                split(x, b, n);
-                s_clk[AT(t)] = b.clk; s_live[AT(t)] = b.live; s_peak[AT(t)] = b.peak;
-            }
+            if (s == 0) split(x, w);
+            if (x.train && s == x.P - 1) split(x, w);
         }
-        const int len = x.train ? 2 * x.K : x.K;
-        // slots
-        for (;;) {
-            bool left = false, any = false;
-            uint16_t prev_nf0 = 0;
-            for (int s = 0; s < x.P; ++s) {
-                uint16_t pos = s_pos[AT(s)], nf = s_nf[AT(s)], nb = s_nb[AT(s)];
-                const uint16_t nf0 = nf;
-                uint16_t em = kNoBlock;
-                if (pos < len) {
-                    left = true;
-                    bool bwd;
-                    int k;
-                    block_at(x, s, pos, bwd, k);
-                    bool ready;
-                    if (!bwd) ready = s == 0 || prev_nf0 > k;
-                    else ready = (s == x.P - 1) ? nf0 > k : s_nb[AT(s + 1)] > k;
-                    if (ready) {
-                        Acc a{s_clk[AT(s)], s_live[AT(s)], s_peak[AT(s)]};
-                        if (x.mlp) {
-                            if (bwd) mlp_bwd(x, a, n, s, k);
-                            else mlp_fwd(x, a, n, s, k);
-                        } else {
-                            if (bwd) tf_bwd(x, a, n, s, k);
-                            else tf_fwd(x, a, n, s, k);
-                        }
-                        s_clk[AT(s)] = a.clk; s_live[AT(s)] = a.live; s_peak[AT(s)] = a.peak;
-                        ++pos;
-                        if (bwd) ++nb;
-                        else ++nf;
-                        em = (uint16_t)((k << 1) | (bwd ? 1 : 0));
-                        any = true;
+    }
+    const uint64_t segmask = W == 64 ? ~0ull : (((1ull << W) - 1) << (lane & ~(W - 1)));
+
+    for (;;) {
+        const bool active = live_stage && pos < len;
+        const uint64_t act_mask = ballot(active);
+        if (act_mask == 0) break;
+        const int nf_left = shr1(nf), nb_right = shl1(nb);   // slot-start counters
+        bool bwd = false, ready = false;
+        int k = 0;
+        if (active) {
+            block_at(x, s, pos, bwd, k);
+            ready = !bwd ? (s == 0 || nf_left > k) : (s == x.P - 1 ? nf > k : nb_right > k);
+        }
+        const uint64_t rdy_mask = ballot(ready);
+        if ((act_mask & segmask) != 0 && (rdy_mask & segmask) == 0) {
+            // no stage can proceed: impossible for 1F1B, stops the candidate
+            status |= DSIM_ST_BAD_STRATEGY;
+            live_stage = false;
+        }
+        const bool all_fwd = ballot(ready && bwd) == 0;
+
+        if (ready) {
+            const int d = bwd ? 1 : 0;
+            const uint64_t m = mb_rows(x, k);
+            const int mc = (uint64_t)k < x.mr ? 1 : 0;
+            double2 *pp = &s_pat[d][0][lane];
+            if (bwd && k == 0) {
+                block_bwd(x, w, s, k);   // no accumulation: op by op
+            } else {
+                if ((bwd ? pat_b : pat_f) != mc) {
+                    Summary t;
+                    record_unit<TF>(x, bwd, m, reinterpret_cast<double *>(pp), t);
+                    if (bwd) {
+                        sum_b = t;
+                        pat_b = mc;
+                    } else {
+                        sum_f = t;
+                        pat_f = mc;
                     }
                 }
-                s_pos[AT(s)] = pos;
-                s_nf[AT(s)] = nf;
-                s_nb[AT(s)] = nb;
-                s_em[AT(s)] = em;
-                prev_nf0 = nf0;
-            }
-            if (!left) break;
-            if (!any) {   // cannot happen for 1F1B; guarantees termination
-                status |= DSIM_ST_BAD_STRATEGY;
-                break;
-            }
-            // the slot's sends, ascending by source stage
-            for (int s = 0; s < x.P; ++s) {
-                const uint16_t em = s_em[AT(s)];
-                if (em == kNoBlock) continue;
-                const bool bwd = em & 1;
-                const int k = em >> 1;
-                if (!bwd && s == x.P - 1) continue;
-                if (bwd && s == 0) continue;
-                const int t = bwd ? s - 1 : s + 1;
-                uint64_t sz, fre;
-                if (x.mlp) {
-                    sz = bwd ? mlp_grad_out(x, s, k) : mlp_act_out(x, s, k);
-                    fre = (bwd || !x.train) ? sz : 0;
+                const Summary sm = bwd ? sum_b : sum_f;
+                const int nl = stage_nl(x, s);
+                if (TF) {
+                    const TfSz z = tf_sizes(x, m);
+                    if (!bwd && s == 0) tf_fwd_first(x, w, z);
+                    if (bwd && s == x.P - 1) tf_bwd_last(x, w, z, true);
+                    if (all_fwd) walk_units<F2>(w, pp, sm, nl);
+                    else walk_units<B2>(w, pp, sm, nl);
+                    if (!bwd && s == x.P - 1) tf_fwd_last(x, w, z);
+                    if (bwd && s == 0) tf_bwd_first(x, w, z, true);
                 } else {
-                    sz = x.e * mb_rows(x, k) * x.seq * x.d;
-                    fre = sz;
+                    const int per = x.H > 1 ? 2 : 1;
+                    const int units = nl / per;
+                    const int l0 = stage_l0(x, s);
+                    if (!bwd) {
+                        const bool dead = !x.train && s == x.P - 1;
+                        if (all_fwd) walk_units<F2>(w, pp, sm, units - (dead ? 1 : 0));
+                        else walk_units<B2>(w, pp, sm, units - (dead ? 1 : 0));
+                        if (dead) {
+                            for (int i = l0 + nl - per; i < l0 + nl; ++i)
+                                mlp_layer_fwd(x, w, m, mlp_kind(x, i), i == x.L - 1);
+                        }
+                    } else {
+                        if (s == x.P - 1) mlp_loss(x, w, m);
+                        walk_units<B2>(w, pp, sm, units - 1);
+                        for (int i = l0 + per - 1; i >= l0; --i)
+                            mlp_layer_bwd(x, w, m, mlp_kind(x, i), i == l0, i == 0, true);
+                    }
                 }
-                const double c0 = s_clk[AT(s)], c1 = s_clk[AT(t)];
-                double start = 0.0;
-                start = c0 > start ? c0 : start;
-                start = c1 > start ? c1 : start;
-                const double end = start + (x.lat + (double)sz * x.inv_l);
-                s_clk[AT(s)] = end;
-                s_clk[AT(t)] = end;
-                const uint64_t lt = s_live[AT(t)] + sz;
-                s_live[AT(t)] = lt;
-                s_peak[AT(t)] = umax(s_peak[AT(t)], lt);
-                s_live[AT(s)] -= fre;
-                n.walked += 1;
-                n.nops += x.mult_dev;
+            }
+            ++pos;
+            if (bwd) ++nb;
+            else ++nf;
+        }
+
+        // the slot's sends, ascending by source stage
+        int sdir = 0;
+        double scost = 0.0;
+        uint64_t ssz = 0, sfre = 0;
+        if (ready && ((!bwd && s < x.P - 1) || (bwd && s > 0))) {
+            sdir = bwd ? -1 : 1;
+            send_size(x, s, k, bwd, ssz, sfre);
+            scost = cost_send(x, ssz);
+        }
+        const int l_dir = shr1(sdir), r_dir = shl1(sdir);
+        const double l_cost = shr1(scost), r_cost = shl1(scost);
+        const uint64_t l_sz = shr1(ssz), r_sz = shl1(ssz);
+        const bool from_left = live_stage && s >= 1 && l_dir == 1;
+        const bool from_right = live_stage && s + 1 < P && r_dir == -1;
+        uint64_t steps = fold_segments(ballot(sdir != 0), W);
+        while (steps != 0) {
+            const int st = __builtin_ctzll(steps);
+            steps &= steps - 1;
+            const double cl = shr1(w.clk), cr = shl1(w.clk);
+            const bool src = s == st && sdir != 0;
+            const bool tl = s == st + 1 && from_left;
+            const bool tr = s == st - 1 && from_right;
+            const double a = ((src && sdir < 0) || tl) ? cl : cr;
+            const double mx = a > w.clk ? a : w.clk;
+            const double e = mx + (src ? scost : (tl ? l_cost : r_cost));
+            if (src || tl || tr) w.clk = e;
+        }
+        if (live_stage) {
+            if (from_left) {
+                w.live += (int64_t)l_sz;
+                w.peak = w.live > w.peak ? w.live : w.peak;
+            }
+            if (sdir != 0) {
+                w.live -= (int64_t)sfre;
+                w.walked += 1;
+                w.nops += x.mult_dev;
+            }
+            if (from_right) {
+                w.live += (int64_t)r_sz;
+                w.peak = w.live > w.peak ? w.live : w.peak;
             }
         }
-        if (x.train) {
-            for (int s = 0; s < x.P; ++s) {
-                Acc a{s_clk[AT(s)], s_live[AT(s)], s_peak[AT(s)]};
-                weight_update(x, a, n, s);
-                s_clk[AT(s)] = a.clk; s_live[AT(s)] = a.live; s_peak[AT(s)] = a.peak;
-            }
-        }
-        for (int s = 0; s < x.P; ++s) {
-            const double cl = s_clk[AT(s)];
-            const uint64_t pk = s_peak[AT(s)];
-            mk = cl > mk ? cl : mk;
-            cp = umax(cp, pk);
-        }
-        if (g.c.cap != 0 && cp > g.c.cap) status |= DSIM_ST_OVER_CAP;
     }
-    g.makespan[c] = mk;
-    g.cand_peak[c] = cp;
-    g.status[c] = status;
-    if (g.n_ops) g.n_ops[c] = n.nops;
-    if (g.walked) g.walked[c] = n.walked;
-    const int P = ok ? x.P : 0;
+    if (live_stage && x.train && status == 0) weight_update(x, w, s);
+
+    // per-candidate results: reductions over the segment
+    const bool contributes = s < P && status == 0;
+    const double mk = seg_reduce(contributes ? w.clk : 0.0, W, [](double a, double b) { return a > b ? a : b; });
+    const uint64_t cp = seg_reduce(contributes ? (uint64_t)w.peak : 0ull, W,
+                                   [](uint64_t a, uint64_t b) { return a > b ? a : b; });
+    const uint64_t nops = seg_reduce(contributes ? w.nops : 0ull, W, [](uint64_t a, uint64_t b) { return a + b; });
+    const uint64_t walked = seg_reduce(contributes ? w.walked : 0ull, W,
+                                       [](uint64_t a, uint64_t b) { return a + b; });
+    status = seg_reduce(status, W, [](int32_t a, int32_t b) { return a | b; });
+    if (c < 0) return;
+    const bool valid = status == 0;
+    if (s == 0) {
+        int32_t st = status;
+        if (valid && g.c.cap != 0 && cp > g.c.cap) st |= DSIM_ST_OVER_CAP;
+        g.makespan[c] = valid ? mk : 0.0;
+        g.cand_peak[c] = valid ? cp : 0;
+        g.status[c] = st;
+        if (g.n_ops) g.n_ops[c] = valid ? nops : 0;
+        if (g.walked) g.walked[c] = valid ? walked : 0;
+    }
+    const bool mine = valid && s < P;
     if (g.finish) {
         double *row = g.finish + (size_t)c * g.row_width;
-        for (int s = 0; s < g.row_width; ++s) row[s] = s < P ? s_clk[AT(s)] : 0.0;
+        for (int j = s; j < g.row_width; j += W) row[j] = (mine && j == s) ? w.clk : 0.0;
     }
     if (g.peak) {
         uint64_t *row = g.peak + (size_t)c * g.row_width;
-        for (int s = 0; s < g.row_width; ++s) row[s] = s < P ? s_peak[AT(s)] : 0;
+        for (int j = s; j < g.row_width; j += W) row[j] = (mine && j == s) ? (uint64_t)w.peak : 0;
     }
-#undef AT
+}
+
+// ---------------------------------------------------------------------------
+// Pre-pass: stable counting sort of the candidates by segment class
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kScanBlock) void k_class_count(const dsim_strategy *cand, int64_t n, int p_bound,
+                                                           uint32_t *counts)
+{
+    __shared__ uint32_t s_cnt[8];
+    if (threadIdx.x < 8) s_cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t c = (int64_t)blockIdx.x * kScanBlock + threadIdx.x;
+    if (c < n) atomicAdd(&s_cnt[seg_class(cand[c], p_bound)], 1u);
+    __syncthreads();
+    if (threadIdx.x < 8) counts[(size_t)blockIdx.x * 8 + threadIdx.x] = s_cnt[threadIdx.x];
+}
+
+// counts[b][j] -> exclusive prefix over blocks b, per class j; meta as in
+// ParArgs.  One block.
+__global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int64_t nb, uint32_t *meta)
+{
+    __shared__ uint32_t s_v[kScanBlock];
+    __shared__ uint32_t s_total[8];
+    const int t = threadIdx.x;
+    for (int j = 0; j < kClasses; ++j) {
+        uint32_t carry = 0;
+        for (int64_t b0 = 0; b0 < nb; b0 += kScanBlock) {
+            const int64_t b = b0 + t;
+            const uint32_t v = b < nb ? counts[(size_t)b * 8 + j] : 0;
+            s_v[t] = v;
+            __syncthreads();
+            for (int o = 1; o < kScanBlock; o <<= 1) {
+                const uint32_t add = t >= o ? s_v[t - o] : 0;
+                __syncthreads();
+                s_v[t] += add;
+                __syncthreads();
+            }
+            if (b < nb) counts[(size_t)b * 8 + j] = carry + s_v[t] - v;
+            carry += s_v[kScanBlock - 1];
+            __syncthreads();
+        }
+        if (t == 0) s_total[j] = carry;
+        __syncthreads();
+    }
+    if (t == 0) {
+        uint32_t rank = 0, lane = 0;
+        for (int j = 0; j < kClasses; ++j) {
+            meta[j] = s_total[j];
+            meta[8 + j] = rank;
+            meta[16 + j] = lane;
+            rank += s_total[j];
+            lane += ((s_total[j] << j) + kLanes - 1) / kLanes * kLanes;
+        }
+        meta[kClasses] = 0;
+        meta[8 + kClasses] = rank;
+        meta[16 + kClasses] = lane;
+    }
+}
+
+__global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strategy *cand, int64_t n, int p_bound,
+                                                             const uint32_t *offsets, const uint32_t *meta,
+                                                             uint32_t *perm)
+{
+    constexpr int kWaves = kScanBlock / kLanes;
+    __shared__ uint32_t s_wcnt[kWaves][8];
+    const int t = threadIdx.x, wv = t / kLanes, lane = t % kLanes;
+    const int64_t c = (int64_t)blockIdx.x * kScanBlock + t;
+    const int j = c < n ? seg_class(cand[c], p_bound) : kClasses;
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    uint32_t rank = 0;
+    for (int jj = 0; jj < kClasses; ++jj) {
+        const uint64_t b = __ballot(j == jj);
+        if (lane == 0) s_wcnt[wv][jj] = (uint32_t)__popcll(b);
+        if (j == jj) rank = (uint32_t)__popcll(b & below);
+    }
+    __syncthreads();
+    if (j < kClasses) {
+        for (int v = 0; v < wv; ++v) rank += s_wcnt[v][j];
+        perm[meta[8 + j] + offsets[(size_t)blockIdx.x * 8 + j] + rank] = (uint32_t)c;
+    }
 }
 
 }  // namespace
@@ -618,6 +542,8 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
 dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, const CostConsts &c,
                               const dsim_results &r, hipStream_t s)
 {
+    if (n_cand > (int64_t)0x7fffffff)
+        return fail(DSIM_ERANGE, "parametric: at most 2^31 - 1 candidates per call");
     ParArgs g;
     g.m = m;
     g.cand = cand;
@@ -627,6 +553,8 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     if (pb > kMaxStages) pb = kMaxStages;
     if (pb > m.n_layers) pb = m.n_layers;
     g.p_bound = pb;
+    int wmax = 1;
+    while (wmax < pb) wmax <<= 1;
     g.makespan = r.makespan;
     g.finish = r.finish;
     g.peak = r.peak;
@@ -635,23 +563,36 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     g.walked = r.walked_ops;
     g.status = r.status;
     g.c = c;
-    const size_t lds = (size_t)pb * kLanes * (3 * sizeof(uint64_t) + 4 * sizeof(uint16_t));
-    int dev = 0, lds_max = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-    if (e != hipSuccess) return hip_fail(e, "parametric: device query");
-    if (lds > (size_t)lds_max)
-        return fail(DSIM_ERANGE, "parametric: %d pipeline stages need %zu bytes of LDS, the device allows %d "
-                    "(lower results.row_width)", pb, lds, lds_max);
-    if (lds > 65536) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void *>(k_parametric),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return hip_fail(e, "parametric: LDS attribute");
-    }
-    const int64_t blocks = (n_cand + kLanes - 1) / kLanes;
-    hipLaunchKernelGGL(k_parametric, dim3((unsigned)blocks), dim3(kLanes), lds, s, g);
+
+    // temporary: per-block class counts, class table, permutation
+    const int64_t nb = (n_cand + kScanBlock - 1) / kScanBlock;
+    const size_t counts_b = (size_t)nb * 8 * sizeof(uint32_t), meta_b = 32 * sizeof(uint32_t);
+    const size_t perm_b = (size_t)n_cand * sizeof(uint32_t);
+    void *ws = nullptr;
+    hipError_t e = hipMallocAsync(&ws, counts_b + meta_b + perm_b, s);
+    if (e != hipSuccess) return hip_fail(e, "parametric: temporary buffer");
+    uint32_t *counts = static_cast<uint32_t *>(ws);
+    uint32_t *meta = counts + (size_t)nb * 8;
+    uint32_t *perm = meta + 32;
+    g.perm = perm;
+    g.meta = meta;
+
+    hipLaunchKernelGGL(k_class_count, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb, counts);
+    hipLaunchKernelGGL(k_class_scan, dim3(1), dim3(kScanBlock), 0, s, counts, nb, meta);
+    hipLaunchKernelGGL(k_class_scatter, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb,
+                       (const uint32_t *)counts, (const uint32_t *)meta, perm);
+    // every class's lanes round up to whole wavefronts: at most one partial
+    // wavefront per class beyond n * wmax lanes
+    const int64_t waves = (n_cand * wmax + kLanes - 1) / kLanes + kClasses;
+    if (m.family == DSIM_MLP)
+        hipLaunchKernelGGL(k_parametric<false>, dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+    else
+        hipLaunchKernelGGL(k_parametric<true>, dim3((unsigned)waves), dim3(kLanes), 0, s, g);
     e = hipGetLastError();
-    return e == hipSuccess ? DSIM_OK : hip_fail(e, "parametric launch");
+    const hipError_t e2 = hipFreeAsync(ws, s);
+    if (e != hipSuccess) return hip_fail(e, "parametric launch");
+    if (e2 != hipSuccess) return hip_fail(e2, "parametric: temporary buffer release");
+    return DSIM_OK;
 }
 
 }  // namespace dsim
