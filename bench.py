@@ -2,6 +2,10 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
+NAME is random_tables (default) or one of the strategy grids (tiny_mlp,
+large_mlp, gpt2_small, gpt2_small_train, gpt3_175b); a grid's line times
+dsim_simulate_parametric + top-k over the whole grid.
+
 A step is one pass of the hot path over one batch of synthetic input, with the
 input already resident in HBM:
   * random_tables (default, the HBM-bound workload): simulate 1,000,000
@@ -140,7 +144,7 @@ def bench_random_tables(args, torch, dsim, W):
 PARAMETRIC = ("tiny_mlp", "large_mlp", "gpt2_small", "gpt2_small_train", "gpt3_175b")
 
 
-def bench_parametric(torch, dsim, W, reps):
+def bench_parametric(torch, dsim, W, reps, warmup=1):
     """One grid of the transform-driven path: dsim_simulate_parametric over
     every strategy of the grid plus the top-k selection, with the strategies
     resident on the device.  Walked ops are the ops the kernel processes (one
@@ -169,11 +173,14 @@ def bench_parametric(torch, dsim, W, reps):
         if record:
             ev.append((e0, e1, e2))
 
-    step(False)
+    for _ in range(max(1, warmup)):
+        step(False)
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
     for _ in range(reps):
         step(True)
     torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t0
     kern_ms = sum(a.elapsed_time(b) for a, b, _ in ev) / len(ev)
     step_ms = sum(a.elapsed_time(c) for a, _, c in ev) / len(ev)
     walked = int(res["walked_ops"].sum().item())
@@ -184,7 +191,55 @@ def bench_parametric(torch, dsim, W, reps):
                      "makespan_s": float(out_mk[0].item())} if int(found.item()) > 0 else None,
             "kernel_ms": kern_ms, "step_ms": step_ms, "candidates_per_s": n / (step_ms * 1e-3),
             "walked_ops": walked, "walked_ops_per_s": walked / (kern_ms * 1e-3),
-            "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3)}
+            "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3), "wall_s": wall_s, "reps": reps}
+
+
+# fp64 add rate of the chip: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (half the
+# 78.6 TFLOP/s FMA figure, which counts two flops per lane-cycle)
+FP64_ADD_PEAK_T = 256 * 4 * 16 * 2.4e9 / 1e12
+
+
+def cpu_baseline_parametric(W, strat, budget_s=10.0):
+    """The oracle (projection mode), as it stands, on strided candidates of
+    the grid until ~budget_s seconds of wall time are spent."""
+    import numpy as np
+    import oracle
+    threads = max(1, min(os.cpu_count() or 1, 16))
+    order = np.arange(len(strat))[::7]
+    done, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < budget_s and done < len(order):
+        pick = order[done:done + 4 * threads]
+        oracle.run_strategies(W.model, strat[pick], W.device, slice=True, row_width=int(strat[:, 2].max()),
+                              threads=threads)
+        done += len(pick)
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of the %d strategies (every 7th, grid order), simulated by the C oracle (one replica "
+                      "per stage) in %.1f s on %d threads" % (done, len(strat), dt, threads)}
+
+
+def bench_parametric_line(args, torch, dsim, W):
+    """The benchmark line for a strategy grid: a step is one
+    dsim_simulate_parametric over the whole grid plus the top-k selection."""
+    r = bench_parametric(torch, dsim, W, args.steps, args.warmup)
+    walked_T = r["walked_ops_per_s"] / 1e12
+    out = {
+        "metric": METRIC, "value": r["n_cand"] * r["reps"] / r["wall_s"], "unit": "candidates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": r["wall_s"] / r["reps"] * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "%s: %d strategies, simulate + top-%d" % (W.name, r["n_cand"], W.top_k),
+                   "n_cand": r["n_cand"], "top_k": W.top_k},
+        "ops_per_s": r["walked_ops_per_s"], "program_ops_per_s": r["program_ops_per_s"],
+        "kernel_ms": r["kernel_ms"], "best": r["best"],
+        # every walked op is at least one dependent fp64 add in one lane
+        "roofline": {"bound": "alu", "achieved": walked_T, "peak": FP64_ADD_PEAK_T, "unit": "TFLOP/s",
+                     "frac": walked_T / FP64_ADD_PEAK_T, "traffic": None, "kernel": "k_parametric",
+                     "walked_ops_per_launch": r["walked_ops"]},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_parametric(W, dsim.dsim_create_grid(W.model, W.grid))
+    return out
 
 
 def copy_calibration(torch, nbytes=4 << 30, reps=5):
@@ -229,9 +284,12 @@ def main():
         print("bench.py needs a HIP device", file=sys.stderr)
         sys.exit(1)
     dsim.lib()
+    if args.workload not in ALL:
+        raise SystemExit("unknown workload %s (one of %s)" % (args.workload, ", ".join(ALL)))
     W = ALL[args.workload]
-    if args.workload != "random_tables":
-        raise SystemExit("unknown workload for the benchmark line: %s" % args.workload)
+    if W.tables is None:
+        print(json.dumps(bench_parametric_line(args, torch, dsim, W)), flush=True)
+        return
     out = bench_random_tables(args, torch, dsim, W)
     if not args.no_parametric:
         out["parametric"] = [bench_parametric(torch, dsim, ALL[name], args.param_reps) for name in PARAMETRIC]

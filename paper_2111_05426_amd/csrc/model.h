@@ -190,18 +190,19 @@ __device__ __forceinline__ void mlp_loss(const Ctx &x, S &o, uint64_t m)
 }
 
 // bytes of the activation a stage sends forward / the gradient it sends back
-__device__ __forceinline__ uint64_t mlp_act_out(const Ctx &x, int s, int k)
+// for a microbatch of m rows
+__device__ __forceinline__ uint64_t mlp_act_out(const Ctx &x, int s, uint64_t m)
 {
     uint64_t din, dout;
     mlp_dims(x, mlp_kind(x, stage_l0(x, s) + stage_nl(x, s) - 1), din, dout);
-    return x.e * mb_rows(x, k) * dout;
+    return x.e * m * dout;
 }
 
-__device__ __forceinline__ uint64_t mlp_grad_out(const Ctx &x, int s, int k)
+__device__ __forceinline__ uint64_t mlp_grad_out(const Ctx &x, int s, uint64_t m)
 {
     uint64_t din, dout;
     mlp_dims(x, mlp_kind(x, stage_l0(x, s)), din, dout);
-    return x.e * mb_rows(x, k) * din;
+    return x.e * m * din;
 }
 
 // ---------------------------------------------------------------------------
@@ -326,7 +327,7 @@ __device__ __forceinline__ void tf_bwd_first(const Ctx &x, S &o, const TfSz &z, 
 // Whole blocks (one microbatch's forward or backward on one stage), op by op
 // ---------------------------------------------------------------------------
 template <class S>
-__device__ void block_fwd(const Ctx &x, S &o, int s, int k)
+__device__ __forceinline__ void block_fwd(const Ctx &x, S &o, int s, int k)
 {
     const uint64_t m = mb_rows(x, k);
     if (x.mlp) {
@@ -342,7 +343,7 @@ __device__ void block_fwd(const Ctx &x, S &o, int s, int k)
 }
 
 template <class S>
-__device__ void block_bwd(const Ctx &x, S &o, int s, int k)
+__device__ __forceinline__ void block_bwd(const Ctx &x, S &o, int s, int k)
 {
     const uint64_t m = mb_rows(x, k);
     const bool acc = k >= 1;
@@ -397,7 +398,7 @@ __device__ __forceinline__ void wu_param(const Ctx &x, S &o, uint64_t N)
 
 // after the stage's last backward, layer by layer in ascending order
 template <class S>
-__device__ void weight_update(const Ctx &x, S &o, int s)
+__device__ __forceinline__ void weight_update(const Ctx &x, S &o, int s)
 {
     const int l0 = stage_l0(x, s), nl = stage_nl(x, s);
     if (x.mlp) {
@@ -424,7 +425,7 @@ __device__ __forceinline__ uint64_t input_row(const Ctx &x) { return x.mlp ? x.e
 
 // bytes resident on a device of stage s at t = 0: weight shard, optimizer
 // state, the replica's input rows (stage 0) and targets (last stage, training)
-__device__ inline uint64_t resident(const Ctx &x, int s)
+__device__ __forceinline__ uint64_t resident(const Ctx &x, int s)
 {
     const int l0 = stage_l0(x, s), nl = stage_nl(x, s);
     uint64_t N = 0;
@@ -479,14 +480,14 @@ __device__ __forceinline__ void block_at(const Ctx &x, int s, int pos, bool &bwd
     }
 }
 
-// bytes sent after a block, and the bytes the sender frees
-__device__ __forceinline__ void send_size(const Ctx &x, int s, int k, bool bwd, uint64_t &sz, uint64_t &fre)
+// bytes sent after a block of m rows, and the bytes the sender frees
+__device__ __forceinline__ void send_size(const Ctx &x, int s, uint64_t m, bool bwd, uint64_t &sz, uint64_t &fre)
 {
     if (x.mlp) {
-        sz = bwd ? mlp_grad_out(x, s, k) : mlp_act_out(x, s, k);
+        sz = bwd ? mlp_grad_out(x, s, m) : mlp_act_out(x, s, m);
         fre = (bwd || !x.train) ? sz : 0;
     } else {
-        sz = x.e * mb_rows(x, k) * x.seq * x.d;
+        sz = x.e * m * x.seq * x.d;
         fre = sz;
     }
 }

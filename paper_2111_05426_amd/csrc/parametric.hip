@@ -40,17 +40,27 @@ namespace {
 constexpr int kLanes = 64;
 constexpr int kClasses = 7;       // segment widths 1, 2, 4, ..., 64
 constexpr int kScanBlock = 256;
-constexpr int kPat2 = 12;         // pattern capacity per direction, in double2
 
-// pattern sizes (double2 entries) per model family
-template <bool TF> struct PatSize;
-template <> struct PatSize<true> {
-    static constexpr int F2 = 7;    // 12 compute ops + 2 all-reduces
-    static constexpr int B2 = 12;   // 17 compute + 4 accumulations + 2 all-reduces
+// Recorded block program of one lane and direction, in double2 entries:
+// ops before the repeating units, one unit, ops after the units.  The
+// regions are sized for the larger (backward) block; forward blocks use the
+// F_* prefix of each region.
+template <bool TF> struct Shape;
+template <> struct Shape<true> {
+    static constexpr int PRE2 = 4;    // last stage backward: loss .. final LN grad (8 ops)
+    static constexpr int U2 = 12;     // one layer backward: 17 compute + 4 accumulations + 2 all-reduces
+    static constexpr int SUF2 = 1;    // stage 0 backward: embedding grad + accumulation
+    static constexpr int F_PRE2 = 1;  // stage 0 forward: embedding + all-reduce
+    static constexpr int F_U2 = 7;    // one layer forward: 12 compute + 2 all-reduces
+    static constexpr int F_SUF2 = 1;  // last stage forward: final LN + LM head
 };
-template <> struct PatSize<false> {
-    static constexpr int F2 = 3;    // column layer (2 ops) + row layer (3)
-    static constexpr int B2 = 5;    // row layer (4 ops) + column layer (5)
+template <> struct Shape<false> {
+    static constexpr int PRE2 = 1;    // last stage backward: loss gradient
+    static constexpr int U2 = 5;      // row layer (4 ops) + column layer (5) backward
+    static constexpr int SUF2 = 5;    // the stage's first unit backward (frees the stage input)
+    static constexpr int F_PRE2 = 0;
+    static constexpr int F_U2 = 3;    // column layer (2 ops) + row layer (3) forward
+    static constexpr int F_SUF2 = 3;  // the model's last unit in inference (dead output)
 };
 
 struct ParArgs {
@@ -83,7 +93,7 @@ __device__ __forceinline__ int seg_class(const dsim_strategy &st, int p_bound)
 // ---------------------------------------------------------------------------
 // Sinks
 // ---------------------------------------------------------------------------
-// The lane's stage replica, op by op.
+// The lane's stage replica, op by op (splits and the weight update).
 struct Walk {
     const Ctx &x;
     double clk;
@@ -115,26 +125,23 @@ struct Walk {
     }
 };
 
-// Memory and op-count summary of one repeating unit.
-struct Summary {
-    int64_t delta;     // live bytes after the unit minus before
-    int64_t top;       // max over the unit's ops of (live after alloc) minus live before
-    uint64_t walked;   // ops walked per unit
-    uint64_t nops;     // program ops per unit
-};
-
-// Records a unit's op costs into the lane's LDS pattern and summarises it.
+// Records ops' costs into a region of LDS and summarises their memory effect
+// relative to the live bytes at the region's start.
 struct Record {
     const Ctx &x;
-    double *base;      // entry j at base[(j / 2) * 2 * kLanes + (j & 1)]
+    double *base;      // entry j at base[(j / 2) * step + (j & 1)]
+    int step;          // doubles between consecutive entry pairs
     int n;
-    int64_t cur, top;
-    uint64_t walked, nops;
+    int64_t cur, top;  // net bytes so far; max of (bytes after an op's allocation)
 
     __device__ __forceinline__ void put(double c)
     {
-        base[(n >> 1) * 2 * kLanes + (n & 1)] = c;
+        base[(n >> 1) * step + (n & 1)] = c;
         ++n;
+    }
+    __device__ __forceinline__ void pad(int entries2)
+    {
+        while (n < 2 * entries2) put(0.0);   // clock + 0.0 == clock
     }
     __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
     {
@@ -142,81 +149,169 @@ struct Record {
         const int64_t a = cur + (int64_t)al;
         top = a > top ? a : top;
         cur = a - (int64_t)fr;
-        walked += 1;
-        nops += x.mult_dev;
     }
     __device__ __forceinline__ void ar_tp(uint64_t by)
     {
         if (x.H <= 1) return;
         put(cost_ar_tp(x, by));
-        walked += 1;
-        nops += x.mult_tp;
     }
     __device__ __forceinline__ void ar_dp(uint64_t by)
     {
         if (x.D <= 1) return;
         put(cost_ar_dp(x, by));
+    }
+};
+
+// The repeating unit of a block for microbatches of m rows: one transformer
+// layer; one MLP layer (H = 1) or column/row pair (H > 1), in walk order.
+// acc: with gradient accumulation (every backward microbatch but the first).
+template <bool TF>
+__device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, bool acc, Record &r)
+{
+    if (TF) {
+        const TfSz z = tf_sizes(x, m);
+        if (bwd) tf_layer_bwd(x, r, z, acc);
+        else tf_layer_fwd(x, r, z);
+    } else if (bwd) {
+        if (x.H > 1) {
+            mlp_layer_bwd(x, r, m, kRow, false, false, acc);
+            mlp_layer_bwd(x, r, m, kCol, false, false, acc);
+        } else {
+            mlp_layer_bwd(x, r, m, kPlain, false, false, acc);
+        }
+    } else if (x.H > 1) {
+        mlp_layer_fwd(x, r, m, kCol, false);
+        mlp_layer_fwd(x, r, m, kRow, false);
+    } else {
+        mlp_layer_fwd(x, r, m, kPlain, false);
+    }
+}
+
+// The ops of stage s's block before (pre) and after (suf) its repeating
+// units: embedding, LM head, loss (transformer); loss, the last unit in
+// inference and the stage's first unit in backward (MLP).
+template <bool TF>
+__device__ void record_edges(const Ctx &x, int s, bool bwd, uint64_t m, bool acc, Record &rp, Record &rs)
+{
+    if (TF) {
+        const TfSz z = tf_sizes(x, m);
+        if (!bwd) {
+            if (s == 0) tf_fwd_first(x, rp, z);
+            if (s == x.P - 1) tf_fwd_last(x, rs, z);
+        } else {
+            if (s == x.P - 1) tf_bwd_last(x, rp, z, acc);
+            if (s == 0) tf_bwd_first(x, rs, z, acc);
+        }
+        return;
+    }
+    const int per = x.H > 1 ? 2 : 1, l0 = stage_l0(x, s), nl = stage_nl(x, s);
+    if (!bwd) {
+        if (!x.train && s == x.P - 1)
+            for (int i = l0 + nl - per; i < l0 + nl; ++i) mlp_layer_fwd(x, rs, m, mlp_kind(x, i), i == x.L - 1);
+    } else {
+        if (s == x.P - 1) mlp_loss(x, rp, m);
+        for (int i = l0 + per - 1; i >= l0; --i) mlp_layer_bwd(x, rs, m, mlp_kind(x, i), i == l0, i == 0, acc);
+    }
+}
+
+// memory effect of pre, n units, suf: unit u starts at pre's net + u * ud;
+// top >= 0 is enough (the running peak is never below the live bytes)
+__device__ __forceinline__ void compose(int64_t pd, int64_t pt, int64_t ud, int64_t ut, int n, int64_t sd,
+                                        int64_t st, int64_t &delta, int64_t &top)
+{
+    int64_t cur = pd, t = pt;
+    if (n > 0) {
+        const int64_t hi = cur + ut + (ud > 0 ? (int64_t)(n - 1) * ud : 0);
+        t = hi > t ? hi : t;
+        cur += (int64_t)n * ud;
+    }
+    t = cur + st > t ? cur + st : t;
+    delta = cur + sd;
+    top = t;
+}
+
+// Units walked per block: every layer (transformer); every layer or layer
+// pair (MLP) except the last unit in inference (last stage) and the
+// stage's first unit in backward, which the block records separately.
+__device__ __forceinline__ int block_units(const dsim_model &M, int P, int H, int s, bool bwd, bool TF)
+{
+    const int L = M.n_layers, nl = L / P + (s < L % P ? 1 : 0);
+    if (TF) return nl;
+    const int per = H > 1 ? 2 : 1;
+    if (bwd) return nl / per - 1;
+    return nl / per - ((M.mode == DSIM_INFER && s == P - 1) ? 1 : 0);
+}
+
+// Counts ops (walked and program ops) without simulating them.
+struct Count {
+    const Ctx &x;
+    uint64_t walked, nops;
+    __device__ __forceinline__ void local(uint64_t, uint64_t, uint64_t, uint64_t)
+    {
+        walked += 1;
+        nops += x.mult_dev;
+    }
+    __device__ __forceinline__ void ar_tp(uint64_t)
+    {
+        if (x.H <= 1) return;
+        walked += 1;
+        nops += x.mult_tp;
+    }
+    __device__ __forceinline__ void ar_dp(uint64_t)
+    {
+        if (x.D <= 1) return;
         walked += 1;
         nops += x.mult_dp;
     }
 };
 
-// The repeating unit: one transformer layer; one MLP layer (H = 1) or one
-// column/row pair (H > 1), in the block's walk order.  Records with
-// accumulation (microbatches >= 1), outside every stage boundary.
-template <bool TF>
-__device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, double *base, Summary &out)
+// ops of stage s's blocks and sends: K forward blocks; in training one
+// backward block without and K - 1 with gradient accumulation.  Op counts do
+// not depend on the microbatch size.
+__device__ __forceinline__ void count_blocks(const Ctx &x, int s, uint64_t &walked, uint64_t &nops)
 {
-    Record r{x, base, 0, 0, 0, 0, 0};
-    if (TF) {
-        const TfSz z = tf_sizes(x, m);
-        if (bwd) tf_layer_bwd(x, r, z, true);
-        else tf_layer_fwd(x, r, z);
-    } else if (bwd) {
-        if (x.H > 1) {
-            mlp_layer_bwd(x, r, m, kRow, false, false, true);
-            mlp_layer_bwd(x, r, m, kCol, false, false, true);
-        } else {
-            mlp_layer_bwd(x, r, m, kPlain, false, false, true);
-        }
-    } else {
-        if (x.H > 1) {
-            mlp_layer_fwd(x, r, m, kCol, false);
-            mlp_layer_fwd(x, r, m, kRow, false);
-        } else {
-            mlp_layer_fwd(x, r, m, kPlain, false);
-        }
-    }
-    while (r.n < 2 * PatSize<TF>::B2) r.put(0.0);   // x + 0.0 == x for the clocks
-    out.delta = r.cur;
-    out.top = r.top;
-    out.walked = r.walked;
-    out.nops = r.nops;
+    Count f{x, 0, 0}, b0{x, 0, 0}, b1{x, 0, 0};
+    block_fwd(x, f, s, 0);
+    const uint64_t K = (uint64_t)x.K;
+    const uint64_t fs = s < x.P - 1 ? 1 : 0;   // Send after each forward block
+    walked += K * (f.walked + fs);
+    nops += K * (f.nops + fs * x.mult_dev);
+    if (!x.train) return;
+    block_bwd(x, b0, s, 0);
+    block_bwd(x, b1, s, 1);
+    const uint64_t bs = s > 0 ? 1 : 0;         // Send after each backward block
+    walked += b0.walked + (K - 1) * b1.walked + K * bs;
+    nops += b0.nops + (K - 1) * b1.nops + K * bs * x.mult_dev;
 }
 
-// n repetitions of a unit: clocks by the recorded adds, memory in closed form
-template <int N2>
-__device__ __forceinline__ void walk_units(Walk &w, const double2 *pp, const Summary &sm, int n)
+// the clock part of a block: pre, n units, suf (entry counts per region;
+// PST / UST: double2 stride of the edge / unit entries)
+template <int P2, int U2n, int S2, int PST, int UST>
+__device__ __forceinline__ double walk3(const double2 *pre, const double2 *unit, const double2 *suf, double clk, int n)
 {
-    if (n <= 0) return;
-    double2 r[N2];
 #pragma unroll
-    for (int j = 0; j < N2; ++j) r[j] = pp[j * kLanes];
-    double clk = w.clk;
+    for (int j = 0; j < P2; ++j) {
+        const double2 v = pre[j * PST];
+        clk = clk + v.x;
+        clk = clk + v.y;
+    }
+    double2 r[U2n];
+#pragma unroll
+    for (int j = 0; j < U2n; ++j) r[j] = unit[j * UST];
     for (int u = 0; u < n; ++u) {
 #pragma unroll
-        for (int j = 0; j < N2; ++j) {
+        for (int j = 0; j < U2n; ++j) {
             clk = clk + r[j].x;
             clk = clk + r[j].y;
         }
     }
-    w.clk = clk;
-    // unit u starts at live + u * delta; its highest point is that plus top
-    const int64_t hi = w.live + sm.top + (sm.delta > 0 ? (int64_t)(n - 1) * sm.delta : 0);
-    w.peak = hi > w.peak ? hi : w.peak;
-    w.live += (int64_t)n * sm.delta;
-    w.walked += (uint64_t)n * sm.walked;
-    w.nops += (uint64_t)n * sm.nops;
+#pragma unroll
+    for (int j = 0; j < S2; ++j) {
+        const double2 v = suf[j * PST];
+        clk = clk + v.x;
+        clk = clk + v.y;
+    }
+    return clk;
 }
 
 // ---------------------------------------------------------------------------
@@ -244,13 +339,6 @@ __device__ __forceinline__ uint64_t shl1(uint64_t v)
 
 __device__ __forceinline__ uint64_t ballot(bool b) { return __ballot(b); }
 
-// OR of the W-bit segments of a wave mask, in the low W bits
-__device__ __forceinline__ uint64_t fold_segments(uint64_t m, int W)
-{
-    for (int sh = 32; sh >= W; sh >>= 1) m |= m >> sh;
-    return W == 64 ? m : (m & ((1ull << W) - 1));
-}
-
 template <class T, class Op>
 __device__ __forceinline__ T seg_reduce(T v, int W, Op op)
 {
@@ -261,11 +349,35 @@ __device__ __forceinline__ T seg_reduce(T v, int W, Op op)
 // ---------------------------------------------------------------------------
 // The simulation kernel
 // ---------------------------------------------------------------------------
+constexpr int kKeys = 6;          // forward: 2 row classes; backward: 2 row classes x accumulation
+constexpr int kMaxSegShared = 16; // segments of >= 4 lanes per wavefront
+
+// Per-lane programs (segments of 1 or 2 lanes): each lane records its own
+// block program per direction, again whenever the microbatch size class or
+// the accumulation changes, with the block's composed memory summary.
+template <bool TF> struct LdsLane {
+    double2 prog[2][Shape<TF>::PRE2 + Shape<TF>::U2 + Shape<TF>::SUF2][kLanes];
+    int64_t sum[2][2][kLanes];   // [backward][delta, top][lane]
+};
+// Shared programs (segments of >= 4 lanes): the repeating unit does not
+// depend on the stage, so each segment records the unit of every key once,
+// cooperatively; the stage edges stay per lane (transformer: stages 0 and
+// P-1 only).
+template <bool TF> struct LdsSeg {
+    double2 unit[kMaxSegShared][kKeys][Shape<TF>::U2];
+    int64_t usum[kMaxSegShared][kKeys][2];
+    double2 edge[2][Shape<TF>::PRE2 + Shape<TF>::SUF2][kLanes];
+    int64_t esum[2][4][kLanes];  // [backward][pre delta, pre top, suf delta, suf top][lane]
+};
+
 template <bool TF>
 __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
 {
-    constexpr int F2 = PatSize<TF>::F2, B2 = PatSize<TF>::B2;
-    __shared__ double2 s_pat[2][kPat2][kLanes];   // [backward][entry pair][lane]
+    using Sh = Shape<TF>;
+    __shared__ union {
+        LdsLane<TF> a;
+        LdsSeg<TF> b;
+    } L;
 
     const int lane = threadIdx.x;
     const uint32_t gl = blockIdx.x * (uint32_t)kLanes;
@@ -273,40 +385,83 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
     int cls = 0;
     while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
     const int W = 1 << cls;
+    const bool shared = W >= 4;
     const uint32_t local = gl + lane - g.meta[16 + cls];
     const uint32_t slot = local >> cls;
-    const int li = (int)(local & (uint32_t)(W - 1));   // stage of this lane
+    const int s = (int)(local & (uint32_t)(W - 1));   // stage of this lane
+    const int seg = lane >> cls;
     const int64_t c = slot < g.meta[cls] ? (int64_t)g.perm[g.meta[8 + cls] + slot] : -1;
 
     const dsim_model &M = g.m;
-    Ctx x = {};
+    dsim_strategy st = {1, 1, 1, 1};
     bool ok = false;
     if (c >= 0) {
-        const dsim_strategy st = g.cand[c];
+        st = g.cand[c];
         ok = strategy_ok(M, st.D, st.H, st.P, st.K) && st.P <= g.p_bound && st.P <= W && st.K <= kMaxK;
-        if (ok) make_ctx(M, g.c, st, x);
     }
-    const int P = ok ? x.P : 0;
-    const int s = li;
+    const int P = ok ? st.P : 0, K = st.K;
+    const bool train = M.mode != DSIM_INFER;
     bool live_stage = s < P;
     int32_t status = (c >= 0 && !ok) ? DSIM_ST_BAD_STRATEGY : 0;
 
-    Walk w{x, 0.0, 0, 0, 0, 0};
-    int pos = 0, nf = 0, nb = 0, len = 0;
-    int pat_f = -1, pat_b = -1;   // microbatch size class each pattern was recorded for
-    Summary sum_f{}, sum_b{};
+    double clk = 0.0;
+    int64_t live = 0, peak = 0;
+    uint64_t walked = 0, nops = 0;
+    uint64_t mq = 0, rb_f = 0, rb_b = 0;   // rows of a short microbatch; Send bytes per row
+    int pos = 0, nf = 0, nb = 0, len = 0, mr = 0, n_f = 0, n_b = 0;
     if (live_stage) {
-        const int64_t r0 = (int64_t)resident(x, s);
-        w.live = r0;
-        w.peak = r0;
-        len = x.train ? 2 * x.K : x.K;
+        Ctx x = {};
+        make_ctx(M, g.c, st, x);
+        x.mlp = !TF;   // the family is uniform per launch: compiles out the other
+        Walk w{x, 0.0, (int64_t)resident(x, s), 0, 0, 0};
+        w.peak = w.live;
         // microbatch splits before the pipeline
         if (x.K > 1) {
             if (s == 0) split(x, w);
             if (x.train && s == x.P - 1) split(x, w);
         }
+        clk = w.clk;
+        live = w.live;
+        peak = w.peak;
+        walked = w.walked;
+        nops = w.nops;
+        len = train ? 2 * K : K;
+        mq = x.mq;
+        mr = (int)x.mr;
+        n_f = block_units(M, P, st.H, s, false, TF);
+        n_b = block_units(M, P, st.H, s, true, TF);
+        uint64_t sz, fre;
+        send_size(x, s, 1, false, sz, fre);
+        rb_f = sz;
+        send_size(x, s, 1, true, sz, fre);
+        rb_b = sz;
+        if (shared) {
+            // empty edges unless a later record fills them
+            for (int d = 0; d < 2; ++d) {
+                Record e{x, reinterpret_cast<double *>(&L.b.edge[d][0][lane]), 2 * kLanes, 0, 0, 0};
+                e.pad(Sh::PRE2 + Sh::SUF2);
+                for (int f = 0; f < 4; ++f) L.b.esum[d][f][lane] = 0;
+            }
+        }
     }
-    const uint64_t segmask = W == 64 ? ~0ull : (((1ull << W) - 1) << (lane & ~(W - 1)));
+    if (shared) {
+        if (ok) {
+            Ctx x = {};
+            make_ctx(M, g.c, st, x);
+            x.mlp = !TF;
+            for (int key = s; key < kKeys; key += W) {
+                const bool bwd = key >= 2;
+                const int mc = bwd ? ((key - 2) & 1) : key;
+                Record r{x, reinterpret_cast<double *>(&L.b.unit[seg][key][0]), 2, 0, 0, 0};
+                record_unit<TF>(x, bwd, x.mq + (uint64_t)mc, key >= 4, r);
+                r.pad(Sh::U2);
+                L.b.usum[seg][key][0] = r.cur;
+                L.b.usum[seg][key][1] = r.top;
+            }
+        }
+        __syncthreads();
+    }
+    int key_f = -1, key_b = -1;   // key each lane-owned program was recorded for
 
     for (;;) {
         const bool active = live_stage && pos < len;
@@ -316,10 +471,26 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
         bool bwd = false, ready = false;
         int k = 0;
         if (active) {
-            block_at(x, s, pos, bwd, k);
-            ready = !bwd ? (s == 0 || nf_left > k) : (s == x.P - 1 ? nf > k : nb_right > k);
+            // synchronous 1F1B / forward-only position -> (direction, microbatch)
+            if (!train) {
+                k = pos;
+            } else {
+                const int wu = (P - 1 - s) < K ? (P - 1 - s) : K;
+                if (pos < wu) {
+                    k = pos;
+                } else if (pos < wu + 2 * (K - wu)) {
+                    const int j = pos - wu;
+                    bwd = (j & 1) != 0;
+                    k = bwd ? (j - 1) / 2 : wu + j / 2;
+                } else {
+                    bwd = true;
+                    k = pos - wu - (K - wu);
+                }
+            }
+            ready = !bwd ? (s == 0 || nf_left > k) : (s == P - 1 ? nf > k : nb_right > k);
         }
         const uint64_t rdy_mask = ballot(ready);
+        const uint64_t segmask = W == 64 ? ~0ull : (((1ull << W) - 1) << (lane & ~(W - 1)));
         if ((act_mask & segmask) != 0 && (rdy_mask & segmask) == 0) {
             // no stage can proceed: impossible for 1F1B, stops the candidate
             status |= DSIM_ST_BAD_STRATEGY;
@@ -327,55 +498,71 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
         }
         const bool all_fwd = ballot(ready && bwd) == 0;
 
+        const int d = bwd ? 1 : 0;
+        const int mc = k < mr ? 1 : 0;
+        const uint64_t m = mq + (uint64_t)mc;
         if (ready) {
-            const int d = bwd ? 1 : 0;
-            const uint64_t m = mb_rows(x, k);
-            const int mc = (uint64_t)k < x.mr ? 1 : 0;
-            double2 *pp = &s_pat[d][0][lane];
-            if (bwd && k == 0) {
-                block_bwd(x, w, s, k);   // no accumulation: op by op
+            const bool acc = bwd && k >= 1;
+            const int key = bwd ? 2 + mc + (acc ? 2 : 0) : mc;
+            const int n = bwd ? n_b : n_f;
+            int64_t delta, top;
+            if (!shared) {
+                double2 *pp = &L.a.prog[d][0][lane];
+                if ((bwd ? key_b : key_f) != key) {
+                    Ctx x = {};
+                    make_ctx(M, g.c, st, x);
+                    x.mlp = !TF;
+                    double *base = reinterpret_cast<double *>(pp);
+                    Record rp{x, base, 2 * kLanes, 0, 0, 0};
+                    Record ru{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+                    Record rs{x, base + (Sh::PRE2 + Sh::U2) * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+                    record_edges<TF>(x, s, bwd, m, acc, rp, rs);
+                    record_unit<TF>(x, bwd, m, acc, ru);
+                    rp.pad(Sh::PRE2);
+                    ru.pad(Sh::U2);
+                    rs.pad(Sh::SUF2);
+                    compose(rp.cur, rp.top, ru.cur, ru.top, n, rs.cur, rs.top, delta, top);
+                    L.a.sum[d][0][lane] = delta;
+                    L.a.sum[d][1][lane] = top;
+                    if (bwd) key_b = key;
+                    else key_f = key;
+                }
+                const double2 *up = pp + Sh::PRE2 * kLanes, *sp = pp + (Sh::PRE2 + Sh::U2) * kLanes;
+                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, kLanes>(pp, up, sp, clk, n);
+                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, kLanes>(pp, up, sp, clk, n);
+                delta = L.a.sum[d][0][lane];
+                top = L.a.sum[d][1][lane];
             } else {
-                if ((bwd ? pat_b : pat_f) != mc) {
-                    Summary t;
-                    record_unit<TF>(x, bwd, m, reinterpret_cast<double *>(pp), t);
-                    if (bwd) {
-                        sum_b = t;
-                        pat_b = mc;
-                    } else {
-                        sum_f = t;
-                        pat_f = mc;
-                    }
+                double2 *ep = &L.b.edge[d][0][lane];
+                // transformer edges sit on stages 0 and P-1 only; every MLP
+                // stage ends its backward with its first unit
+                const bool has_edges = !TF || s == 0 || s == P - 1;
+                if (has_edges && (bwd ? key_b : key_f) != key) {
+                    Ctx x = {};
+                    make_ctx(M, g.c, st, x);
+                    x.mlp = !TF;
+                    double *base = reinterpret_cast<double *>(ep);
+                    Record rp{x, base, 2 * kLanes, 0, 0, 0};
+                    Record rs{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+                    record_edges<TF>(x, s, bwd, m, acc, rp, rs);
+                    rp.pad(Sh::PRE2);
+                    rs.pad(Sh::SUF2);
+                    L.b.esum[d][0][lane] = rp.cur;
+                    L.b.esum[d][1][lane] = rp.top;
+                    L.b.esum[d][2][lane] = rs.cur;
+                    L.b.esum[d][3][lane] = rs.top;
+                    if (bwd) key_b = key;
+                    else key_f = key;
                 }
-                const Summary sm = bwd ? sum_b : sum_f;
-                const int nl = stage_nl(x, s);
-                if (TF) {
-                    const TfSz z = tf_sizes(x, m);
-                    if (!bwd && s == 0) tf_fwd_first(x, w, z);
-                    if (bwd && s == x.P - 1) tf_bwd_last(x, w, z, true);
-                    if (all_fwd) walk_units<F2>(w, pp, sm, nl);
-                    else walk_units<B2>(w, pp, sm, nl);
-                    if (!bwd && s == x.P - 1) tf_fwd_last(x, w, z);
-                    if (bwd && s == 0) tf_bwd_first(x, w, z, true);
-                } else {
-                    const int per = x.H > 1 ? 2 : 1;
-                    const int units = nl / per;
-                    const int l0 = stage_l0(x, s);
-                    if (!bwd) {
-                        const bool dead = !x.train && s == x.P - 1;
-                        if (all_fwd) walk_units<F2>(w, pp, sm, units - (dead ? 1 : 0));
-                        else walk_units<B2>(w, pp, sm, units - (dead ? 1 : 0));
-                        if (dead) {
-                            for (int i = l0 + nl - per; i < l0 + nl; ++i)
-                                mlp_layer_fwd(x, w, m, mlp_kind(x, i), i == x.L - 1);
-                        }
-                    } else {
-                        if (s == x.P - 1) mlp_loss(x, w, m);
-                        walk_units<B2>(w, pp, sm, units - 1);
-                        for (int i = l0 + per - 1; i >= l0; --i)
-                            mlp_layer_bwd(x, w, m, mlp_kind(x, i), i == l0, i == 0, true);
-                    }
-                }
+                const double2 *up = &L.b.unit[seg][key][0], *sp = ep + Sh::PRE2 * kLanes;
+                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, 1>(ep, up, sp, clk, n);
+                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, 1>(ep, up, sp, clk, n);
+                compose(L.b.esum[d][0][lane], L.b.esum[d][1][lane], L.b.usum[seg][key][0], L.b.usum[seg][key][1],
+                        n, L.b.esum[d][2][lane], L.b.esum[d][3][lane], delta, top);
             }
+            const int64_t hi = live + top;
+            peak = hi > peak ? hi : peak;
+            live += delta;
             ++pos;
             if (bwd) ++nb;
             else ++nf;
@@ -385,75 +572,91 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
         int sdir = 0;
         double scost = 0.0;
         uint64_t ssz = 0, sfre = 0;
-        if (ready && ((!bwd && s < x.P - 1) || (bwd && s > 0))) {
+        if (ready && ((!bwd && s < P - 1) || (bwd && s > 0))) {
             sdir = bwd ? -1 : 1;
-            send_size(x, s, k, bwd, ssz, sfre);
-            scost = cost_send(x, ssz);
+            ssz = m * (bwd ? rb_b : rb_f);
+            sfre = (TF || bwd || !train) ? ssz : 0;
+            scost = g.c.lat + (double)ssz * g.c.inv_l;
         }
         const int l_dir = shr1(sdir), r_dir = shl1(sdir);
         const double l_cost = shr1(scost), r_cost = shl1(scost);
         const uint64_t l_sz = shr1(ssz), r_sz = shl1(ssz);
         const bool from_left = live_stage && s >= 1 && l_dir == 1;
         const bool from_right = live_stage && s + 1 < P && r_dir == -1;
-        uint64_t steps = fold_segments(ballot(sdir != 0), W);
-        while (steps != 0) {
-            const int st = __builtin_ctzll(steps);
-            steps &= steps - 1;
-            const double cl = shr1(w.clk), cr = shl1(w.clk);
-            const bool src = s == st && sdir != 0;
-            const bool tl = s == st + 1 && from_left;
-            const bool tr = s == st - 1 && from_right;
+        // Send s depends on send s-1 only if s-1 went forward (it moved clock
+        // s) or s goes backward (it reads clock s-1); elsewhere the chain
+        // splits into runs that touch disjoint clocks and proceed in parallel.
+        // rpos = position of the stage in its run.
+        const bool linked = s >= 1 && s < P && (l_dir == 1 || sdir == -1);
+        const uint64_t starts = ballot(!linked);
+        const uint64_t upto = starts & (lane == 63 ? ~0ull : ((2ull << lane) - 1));
+        const int rpos = lane - (63 - __builtin_clzll(upto));
+        for (int r = 0;; ++r) {
+            const bool src = rpos == r && sdir != 0;
+            const uint64_t srcs = ballot(src), more = ballot(rpos > r);
+            if (srcs == 0 && more == 0) break;
+            if (srcs == 0) continue;
+            const double cl = shr1(clk), cr = shl1(clk);
+            const bool tl = rpos == r + 1 && from_left;
+            const bool tr = rpos == r - 1 && from_right;
             const double a = ((src && sdir < 0) || tl) ? cl : cr;
-            const double mx = a > w.clk ? a : w.clk;
+            const double mx = a > clk ? a : clk;
             const double e = mx + (src ? scost : (tl ? l_cost : r_cost));
-            if (src || tl || tr) w.clk = e;
+            if (src || tl || tr) clk = e;
         }
         if (live_stage) {
             if (from_left) {
-                w.live += (int64_t)l_sz;
-                w.peak = w.live > w.peak ? w.live : w.peak;
+                live += (int64_t)l_sz;
+                peak = live > peak ? live : peak;
             }
-            if (sdir != 0) {
-                w.live -= (int64_t)sfre;
-                w.walked += 1;
-                w.nops += x.mult_dev;
-            }
+            if (sdir != 0) live -= (int64_t)sfre;
             if (from_right) {
-                w.live += (int64_t)r_sz;
-                w.peak = w.live > w.peak ? w.live : w.peak;
+                live += (int64_t)r_sz;
+                peak = live > peak ? live : peak;
             }
         }
     }
-    if (live_stage && x.train && status == 0) weight_update(x, w, s);
+    if (live_stage && status == 0) {
+        Ctx x = {};
+        make_ctx(M, g.c, st, x);
+        x.mlp = !TF;
+        Walk w{x, clk, live, peak, walked, nops};
+        if (train) weight_update(x, w, s);
+        clk = w.clk;
+        live = w.live;
+        peak = w.peak;
+        walked = w.walked;
+        nops = w.nops;
+        count_blocks(x, s, walked, nops);
+    }
 
     // per-candidate results: reductions over the segment
     const bool contributes = s < P && status == 0;
-    const double mk = seg_reduce(contributes ? w.clk : 0.0, W, [](double a, double b) { return a > b ? a : b; });
-    const uint64_t cp = seg_reduce(contributes ? (uint64_t)w.peak : 0ull, W,
+    const double mk = seg_reduce(contributes ? clk : 0.0, W, [](double a, double b) { return a > b ? a : b; });
+    const uint64_t cp = seg_reduce(contributes ? (uint64_t)peak : 0ull, W,
                                    [](uint64_t a, uint64_t b) { return a > b ? a : b; });
-    const uint64_t nops = seg_reduce(contributes ? w.nops : 0ull, W, [](uint64_t a, uint64_t b) { return a + b; });
-    const uint64_t walked = seg_reduce(contributes ? w.walked : 0ull, W,
-                                       [](uint64_t a, uint64_t b) { return a + b; });
+    const uint64_t tops = seg_reduce(contributes ? nops : 0ull, W, [](uint64_t a, uint64_t b) { return a + b; });
+    const uint64_t twalk = seg_reduce(contributes ? walked : 0ull, W, [](uint64_t a, uint64_t b) { return a + b; });
     status = seg_reduce(status, W, [](int32_t a, int32_t b) { return a | b; });
     if (c < 0) return;
     const bool valid = status == 0;
     if (s == 0) {
-        int32_t st = status;
-        if (valid && g.c.cap != 0 && cp > g.c.cap) st |= DSIM_ST_OVER_CAP;
+        int32_t stt = status;
+        if (valid && g.c.cap != 0 && cp > g.c.cap) stt |= DSIM_ST_OVER_CAP;
         g.makespan[c] = valid ? mk : 0.0;
         g.cand_peak[c] = valid ? cp : 0;
-        g.status[c] = st;
-        if (g.n_ops) g.n_ops[c] = valid ? nops : 0;
-        if (g.walked) g.walked[c] = valid ? walked : 0;
+        g.status[c] = stt;
+        if (g.n_ops) g.n_ops[c] = valid ? tops : 0;
+        if (g.walked) g.walked[c] = valid ? twalk : 0;
     }
     const bool mine = valid && s < P;
     if (g.finish) {
         double *row = g.finish + (size_t)c * g.row_width;
-        for (int j = s; j < g.row_width; j += W) row[j] = (mine && j == s) ? w.clk : 0.0;
+        for (int j = s; j < g.row_width; j += W) row[j] = (mine && j == s) ? clk : 0.0;
     }
     if (g.peak) {
         uint64_t *row = g.peak + (size_t)c * g.row_width;
-        for (int j = s; j < g.row_width; j += W) row[j] = (mine && j == s) ? (uint64_t)w.peak : 0;
+        for (int j = s; j < g.row_width; j += W) row[j] = (mine && j == s) ? (uint64_t)peak : 0;
     }
 }
 
