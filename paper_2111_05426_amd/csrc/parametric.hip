@@ -284,10 +284,81 @@ __device__ __forceinline__ void count_blocks(const Ctx &x, int s, uint64_t &walk
     nops += b0.nops + (K - 1) * b1.nops + K * bs * x.mult_dev;
 }
 
+// n repetitions of a unit of costs r: the same value as n * 2 * U2n
+// sequential fp64 additions, with far fewer dependent steps.
+//
+// While the clock t stays in one binade [2^e, 2^(e+1)), it is a multiple
+// of ulp = 2^(e-52), and rounding t + c to nearest lands on t plus c rounded
+// to a multiple of ulp, whatever t is, unless c sits exactly half way
+// between two multiples (then ties-to-even depends on t's last bit).  So
+// each unit adds the same whole number I of ulps, and q units add q * I
+// exactly, as long as t + q * I ulps stays below 2^(e+1).  The unit that
+// crosses into the next binade, tiny clocks and the units of a binade in
+// which some cost is a half-way case are added op by op.
+template <int U2n>
+__device__ __forceinline__ double units_seq(const double2 (&r)[U2n], double clk)
+{
+#pragma unroll
+    for (int j = 0; j < U2n; ++j) {
+        clk = clk + r[j].x;
+        clk = clk + r[j].y;
+    }
+    return clk;
+}
+
+template <int U2n>
+__device__ __forceinline__ double units_exact(const double2 (&r)[U2n], double clk, int n)
+{
+    while (n > 0) {
+        if (clk >= 0x1p-500) {
+            const int e = ilogb(clk);
+            const double sc = ldexp(1.0, 52 - e);
+            const double k = clk * sc;                 // integer in [2^52, 2^53)
+            const double room = 0x1p53 - k;            // ulps left in the binade
+            double part[U2n];
+            bool tie = false;
+#pragma unroll
+            for (int j = 0; j < U2n; ++j) {
+                const double tx = r[j].x * sc, ty = r[j].y * sc;
+                const double rx = rint(tx), ry = rint(ty);
+                tie = tie || fabs(tx - rx) == 0.5 || fabs(ty - ry) == 0.5;
+                part[j] = rx + ry;
+            }
+            // whole numbers: exact while below 2^53 (larger sums cannot fit)
+#pragma unroll
+            for (int w = 1; w < U2n; w <<= 1)
+#pragma unroll
+                for (int j = 0; j + w < U2n; j += 2 * w) part[j] = part[j] + part[j + w];
+            const double I = part[0];
+            if (tie) {
+                // op by op until the clock leaves this binade (ties become
+                // half as likely with every binade)
+                const double top = ldexp(1.0, e + 1);
+                for (; n > 0 && clk < top; --n) clk = units_seq(r, clk);
+                continue;
+            }
+            if (I == 0.0) return clk;
+            if ((double)n * I <= room - 1.0) return ldexp(k + (double)n * I, e - 52);
+            double q = floor((room - 1.0) / I);
+            const double rem = fma(-q, I, room - 1.0);   // exact: |rem| < 2^53
+            if (rem < 0.0) q -= 1.0;
+            else if (rem >= I) q += 1.0;
+            if (q > 0.0) {
+                clk = ldexp(k + q * I, e - 52);
+                n -= (int)q;
+            }
+        }
+        clk = units_seq(r, clk);   // crosses into the next binade (or a tiny clock)
+        --n;
+    }
+    return clk;
+}
+
 // the clock part of a block: pre, n units, suf (entry counts per region;
 // PST / UST: double2 stride of the edge / unit entries)
 template <int P2, int U2n, int S2, int PST, int UST>
-__device__ __forceinline__ double walk3(const double2 *pre, const double2 *unit, const double2 *suf, double clk, int n)
+__device__ __forceinline__ double walk3(const double2 *pre, const double2 *unit, const double2 *suf, double clk, int n,
+                                        bool fast)
 {
 #pragma unroll
     for (int j = 0; j < P2; ++j) {
@@ -298,12 +369,10 @@ __device__ __forceinline__ double walk3(const double2 *pre, const double2 *unit,
     double2 r[U2n];
 #pragma unroll
     for (int j = 0; j < U2n; ++j) r[j] = unit[j * UST];
-    for (int u = 0; u < n; ++u) {
-#pragma unroll
-        for (int j = 0; j < U2n; ++j) {
-            clk = clk + r[j].x;
-            clk = clk + r[j].y;
-        }
+    if (fast) {
+        clk = units_exact(r, clk, n);
+    } else {
+        for (int u = 0; u < n; ++u) clk = units_seq(r, clk);
     }
 #pragma unroll
     for (int j = 0; j < S2; ++j) {
@@ -498,6 +567,8 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
         }
         const bool all_fwd = ballot(ready && bwd) == 0;
 
+        // long unit runs take the binade-wise path (uniform per wavefront)
+        const bool fast = ballot(ready && (bwd ? n_b : n_f) >= 3) != 0;
         const int d = bwd ? 1 : 0;
         const int mc = k < mr ? 1 : 0;
         const uint64_t m = mq + (uint64_t)mc;
@@ -528,8 +599,8 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
                     else key_f = key;
                 }
                 const double2 *up = pp + Sh::PRE2 * kLanes, *sp = pp + (Sh::PRE2 + Sh::U2) * kLanes;
-                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, kLanes>(pp, up, sp, clk, n);
-                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, kLanes>(pp, up, sp, clk, n);
+                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
+                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
                 delta = L.a.sum[d][0][lane];
                 top = L.a.sum[d][1][lane];
             } else {
@@ -555,8 +626,8 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
                     else key_f = key;
                 }
                 const double2 *up = &L.b.unit[seg][key][0], *sp = ep + Sh::PRE2 * kLanes;
-                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, 1>(ep, up, sp, clk, n);
-                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, 1>(ep, up, sp, clk, n);
+                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, 1>(ep, up, sp, clk, n, fast);
+                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, 1>(ep, up, sp, clk, n, fast);
                 compose(L.b.esum[d][0][lane], L.b.esum[d][1][lane], L.b.usum[seg][key][0], L.b.usum[seg][key][1],
                         n, L.b.esum[d][2][lane], L.b.esum[d][3][lane], delta, top);
             }

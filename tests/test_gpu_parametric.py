@@ -178,3 +178,30 @@ def test_stage_limit_and_row_width(torch_gpu):
     strat = np.array([(1, 1, 70, 1), (1, 1, 8, 1), (1, 1, 9, 1)], np.int32)
     g = run_gpu(torch_gpu, m, strat, DeviceSpec(), 8)
     assert list(g["status"]) == [16, 0, 16]
+
+
+# Device constants that are powers of two make every cost a short dyadic
+# fraction, so clock + cost often lands exactly half way between two doubles
+# (ties-to-even then depends on the clock's last bit); a large LM head beside
+# tiny layers with no launch cost makes whole layers round away against the
+# clock.  Both stress the exact long-run summation of repeated layers.
+EDGE_DEVICES = [
+    ("pow2", DeviceSpec(2.0 ** 40, 2.0 ** 36, 2.0 ** 30, 2.0 ** -18, 2.0 ** -16, 0)),
+    ("pow2_nolaunch", DeviceSpec(2.0 ** 44, 2.0 ** 40, 2.0 ** 32, 0.0, 0.0, 0)),
+]
+EDGE_MODELS = [
+    ("tf_long", transformer(24, 64, 4, 16, 1000, 16, 2, TRAIN_ADAM), all_strats([1, 2], [1, 2, 4], [1, 2, 3], [1, 2, 5, 16])),
+    ("tf_tiny_layers", transformer(16, 8, 2, 2, 4_000_000, 8, 2, TRAIN_SGD), all_strats([1, 2], [1, 2], [1, 2], [1, 4, 8])),
+    ("mlp_long", mlp(32, 128, 64, 2, TRAIN_ADAM), all_strats([1, 2], [1, 2], [1, 2, 4], [1, 3, 8, 32])),
+    ("tf_infer_long", transformer(40, 32, 2, 8, 512, 32, 4, INFER), all_strats([1, 2], [1, 2], [1, 5], [1, 4, 32])),
+]
+
+
+@pytest.mark.parametrize("dev", EDGE_DEVICES, ids=[d[0] for d in EDGE_DEVICES])
+@pytest.mark.parametrize("case", EDGE_MODELS, ids=[c[0] for c in EDGE_MODELS])
+def test_exact_long_runs(torch_gpu, orc, case, dev):
+    name, model, strat = case
+    g = run_gpu(torch_gpu, model, strat, dev[1])
+    o = orc.run_strategies(model, strat, dev[1], slice=True, row_width=g["finish"].shape[1], threads=8)
+    assert np.any(o["status"] == 0)
+    compare(g, o, strat)
