@@ -15,17 +15,22 @@
 //
 // Per-lane state: the device clocks live in VGPRs (n_dev <= 8 fp64) and are
 // combined with the op's device mask as 1.0/0.0 factors, so an op touching any
-// subset of devices runs the same branch-free sequence; the per-device live
-// and peak byte counters are indexed by a per-lane device id and live in LDS,
-// laid out [device][lane] so that the 64 lanes of a wavefront always hit 64
-// distinct 8-byte words.
+// subset of devices runs the same branch-free sequence; the per-device (live,
+// peak) byte counters are indexed by a per-lane device id and live in LDS as
+// 16-byte pairs laid out [device][lane], so the 64 lanes of a wavefront
+// always hit 64 distinct pairs.  An op's cost is base + coef * x with
+// x = max(flops / F, bytes * w): (base, coef, w) comes from a small LDS table
+// indexed by the op class (compute: launch, 1, 1/B; send: latency, 1, 1/L;
+// all-reduce over n devices: the ring terms for n, 1/L), and a non-compute
+// op's flops are taken as 0, so every lane runs one straight sequence.
 //
-// The kernel is bound by the op stream's HBM bandwidth once the per-op work
-// is short: it has a fast path for the ops every lane of a wavefront has,
-// which assumes valid ops (indices clamped, so even an invalid op stays in
-// bounds) and only tests whether each op is valid; a lane that meets an op it
-// cannot vouch for, and every lane's ops past the wavefront's common count,
-// go through the exact per-op path below it.
+// The kernel is bound by issue rate (about 100 vector instructions per op)
+// more than by HBM: it has a fast path for the ops every lane of a wavefront
+// has, which assumes valid ops (indices clamped, so even an invalid op stays
+// in bounds) and only tests whether each op is valid; a lane that meets an
+// op it cannot vouch for (or a free that would underflow), and every lane's
+// ops past the wavefront's common count, go through the exact per-op path
+// below it.
 #include "internal.h"
 
 namespace dsim {
@@ -33,7 +38,7 @@ namespace {
 
 constexpr int kBlock = 256;       // 4 wavefronts; 32 KB of LDS counters
 constexpr int kWavesPerSimd = 4;
-constexpr int kUnroll = 2;   // ops per register set; two sets in flight
+constexpr int kUnroll = 4;   // ops per register set; two sets in flight
 
 struct TabArgs {
     const uint32_t *code;
@@ -67,6 +72,17 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t group_rsrc(const void *base, u
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRsrcWord3);
 }
 
+// max of two finite non-negative doubles.  The compiler's fmax first
+// canonicalizes an operand it cannot prove canonical (a loop-carried clock),
+// one extra instruction per device and op; these operands are never NaN or
+// denormal-sensitive, so the bare instruction gives the same value.
+__device__ __forceinline__ double max_nn(double a, double b)
+{
+    double r;
+    asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
 __device__ __forceinline__ double bits_double(uint32_t lo, uint32_t hi)
 {
     return __hiloint2double((int)hi, (int)lo);
@@ -93,21 +109,24 @@ template <int ND>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPerSimd))) void k_sim_tables(
     const TabArgs a)
 {
-    __shared__ uint64_t s_live[ND][kBlock];
-    __shared__ uint64_t s_peak[ND][kBlock];
-    __shared__ double2 s_ar[ND + 1];                 // (ar_lat[n], ar_coef[n])
+    __shared__ ulonglong2 s_mem[ND][kBlock];   // (live, peak) bytes
+    // (base, coef) of an op's cost: all-reduce over n = 0..ND devices, then
+    // compute, then send
+    __shared__ double2 s_cost[ND + 3];
+    __shared__ double s_ibw[ND + 3];
 
     const int tid = threadIdx.x;
-    if (tid <= ND) s_ar[tid] = make_double2(a.c.ar_lat[tid], a.c.ar_coef[tid]);
+    if (tid <= ND) s_cost[tid] = make_double2(a.c.ar_lat[tid], a.c.ar_coef[tid]);
+    if (tid == ND + 1) s_cost[tid] = make_double2(a.c.launch, 1.0);
+    if (tid == ND + 2) s_cost[tid] = make_double2(a.c.lat, 1.0);
+    if (tid < ND + 3) s_ibw[tid] = tid == ND + 1 ? a.c.inv_b : a.c.inv_l;
 
     const int64_t c = (int64_t)blockIdx.x * kBlock + tid;
     const bool active = c < a.n_cand;
-    uint64_t init[ND];
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
-        init[d] = (active && a.init_live) ? a.init_live[c * ND + d] : 0;
-        s_live[d][tid] = init[d];
-        s_peak[d][tid] = init[d];
+        const uint64_t init = (active && a.init_live) ? a.init_live[c * ND + d] : 0;
+        s_mem[d][tid] = make_ulonglong2(init, init);
     }
     __syncthreads();
 
@@ -172,29 +191,29 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
                          const uint32_t(&fr)[kUnroll]) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
+            // Everything below is computed for every lane and combined with
+            // selects, so the wavefront runs one straight sequence whatever
+            // the op kinds of its lanes.
             const uint32_t code = cd[u];
-            const uint32_t kind = code & 0xffu;
-            const uint32_t ia = (code >> 8) & 0xffu;
-            const uint32_t ib = (code >> 16) & 0xffu;
-            const bool is_c = kind == 0u, is_s = kind == 1u;
-            const bool fields_ok = (code < (1u << 24)) & (max(fl[u], by[u]) < 0x7f800000u);
-            const bool dev_ok = is_c ? (ia < (uint32_t)ND)
-                                     : (is_s ? ((ia < (uint32_t)ND) & (ib < (uint32_t)ND) & (ia != ib))
-                                             : ((kind == 2u) & (ib != 0u) & ((ib >> ND) == 0u)));
-            suspect |= !(fields_ok & dev_ok);
-
+            const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
+            const bool is_c = kind == 0u, is_s = kind == 1u, is_a = kind == 2u;
             const uint32_t ias = min(ia, (uint32_t)ND - 1u), ibs = min(ib, (uint32_t)ND - 1u);
-            const uint32_t m = (is_c ? (1u << ias) : (is_s ? ((1u << ias) | (1u << ibs)) : ib)) &
-                               ((1u << ND) - 1u);
+            const uint32_t mc = 1u << ias, ms = mc | (1u << ibs), ma = ib & ((1u << ND) - 1u);
+            const uint32_t m = is_c ? mc : (is_s ? ms : ma);
+            const bool bad = (code >= (1u << 24)) | (kind > 2u) | (max(fl[u], by[u]) >= 0x7f800000u) |
+                             ((ia >= (uint32_t)ND) & !is_a) | (is_s & ((ib >= (uint32_t)ND) | (ia == ib))) |
+                             (is_a & ((ib == 0u) | (ib >= (1u << ND))));
+            suspect |= bad;
 
-            // op cost (Sec. 3.3 / Sec. 4 cost functions), blended without branches
-            const double2 ar = s_ar[__popc(m)];
-            const double f = (double)__uint_as_float(fl[u]), b = (double)__uint_as_float(by[u]);
-            const double t_comp = launch + __builtin_fmax(f * inv_f, b * inv_b);
-            const double tl = b * inv_l;
-            const double t_send = lat + tl;
-            const double t_ar = ar.x + ar.y * tl;
-            const double cost = is_c ? t_comp : (is_s ? t_send : t_ar);
+            // op cost (Sec. 3.3 / Sec. 4 cost functions) as base + coef * x:
+            // compute (launch, 1, max(flops/F, bytes/B)), send (lat, 1,
+            // bytes/L), all-reduce over n devices (ar_lat[n], ar_coef[n],
+            // bytes/L); multiplying by 1.0 is exact
+            const uint32_t idx = is_c ? (uint32_t)ND + 1u : (is_s ? (uint32_t)ND + 2u : (uint32_t)__popc(m));
+            const double2 bc = s_cost[idx];
+            const double ibw = s_ibw[idx];
+            const double f = (double)__uint_as_float(is_c ? fl[u] : 0u), b = (double)__uint_as_float(by[u]);
+            const double cost = bc.x + bc.y * max_nn(f * inv_f, b * ibw);
 
             // synchronous start on the device set, common end.  sel[d] is 1.0
             // for a participant, 0.0 otherwise.  Clocks are >= 0, so
@@ -216,24 +235,22 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             // the max over the participants starting from 0.0
             const double end = v[0] + cost;
 #pragma unroll
-            for (int d = 0; d < ND; ++d) clk[d] = __builtin_fmax(clk[d], end * sel[d]);
+            for (int d = 0; d < ND; ++d) clk[d] = max_nn(clk[d], end * sel[d]);
 
-            // live memory: allocate on the target, sample, free on the source
-            const bool memop = kind != 2u;
-            const uint32_t alloc = memop ? al[u] : 0u;
-            const uint32_t fre = memop ? fr[u] : 0u;
+            // live memory: allocate on the target, sample, free on the
+            // source (an all-reduce moves no memory).  A free that would
+            // underflow marks the lane for the exact path.
+            const uint32_t alloc = is_a ? 0u : al[u];
+            const uint32_t fre = is_a ? 0u : fr[u];
             const uint32_t tdev = is_s ? ibs : ias;
             const uint32_t fdev = ias;
-            const uint64_t lt0 = s_live[tdev][tid];
-            const uint64_t pk = s_peak[tdev][tid];
-            const uint64_t lf0 = s_live[fdev][tid];
-            const uint64_t lt = lt0 + (uint64_t)alloc;
+            const ulonglong2 tm = s_mem[tdev][tid];
+            const uint64_t lf0 = s_mem[fdev][tid].x;
+            const uint64_t lt = tm.x + (uint64_t)alloc;
             const uint64_t lf = tdev == fdev ? lt : lf0;
-            s_live[tdev][tid] = lt;
-            s_peak[tdev][tid] = lt > pk ? lt : pk;
-            const bool under = (uint64_t)fre > lf;
-            st |= under ? DSIM_ST_MEM_UNDERFLOW : 0;
-            s_live[fdev][tid] = under ? 0ull : lf - (uint64_t)fre;
+            s_mem[tdev][tid] = make_ulonglong2(lt, lt > tm.y ? lt : tm.y);
+            suspect |= (uint64_t)fre > lf;
+            s_mem[fdev][tid].x = lf - (uint64_t)fre;
         }
     };
     if (fast_end > 0) load_group(0, cdA, flA, byA, alA, frA);
@@ -254,8 +271,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
 #pragma unroll
         for (int d = 0; d < ND; ++d) {
             clk[d] = 0.0;
-            s_live[d][tid] = init[d];
-            s_peak[d][tid] = init[d];
+            // read again rather than kept in registers across the fast path
+            const uint64_t init = a.init_live ? a.init_live[c * ND + d] : 0;
+            s_mem[d][tid] = make_ulonglong2(init, init);
         }
     }
     for (; j < (int32_t)nops; ++j) {
@@ -275,7 +293,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
         } else if (kind == 1u) {
             cost = lat + b * inv_l;
         } else {
-            const double2 ar = s_ar[__popc(m)];
+            const double2 ar = s_cost[__popc(m)];
             cost = ar.x + ar.y * (b * inv_l);
         }
         double start = 0.0;
@@ -288,15 +306,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             if ((m >> d) & 1u) clk[d] = end;
         if (kind != 2u) {
             const uint32_t tdev = kind == 1u ? ib : ia;
-            const uint64_t lt = s_live[tdev][tid] + (uint64_t)a.alloc[o];
-            s_live[tdev][tid] = lt;
-            if (lt > s_peak[tdev][tid]) s_peak[tdev][tid] = lt;
-            const uint64_t lf = s_live[ia][tid], fre = (uint64_t)a.freeb[o];
+            const uint64_t lt = s_mem[tdev][tid].x + (uint64_t)a.alloc[o];
+            s_mem[tdev][tid].x = lt;
+            if (lt > s_mem[tdev][tid].y) s_mem[tdev][tid].y = lt;
+            const uint64_t lf = s_mem[ia][tid].x, fre = (uint64_t)a.freeb[o];
             if (fre > lf) {
                 st |= DSIM_ST_MEM_UNDERFLOW;
-                s_live[ia][tid] = 0;
+                s_mem[ia][tid].x = 0;
             } else {
-                s_live[ia][tid] = lf - fre;
+                s_mem[ia][tid].x = lf - fre;
             }
         }
     }
@@ -306,7 +324,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
         mk = clk[d] > mk ? clk[d] : mk;
-        const uint64_t p = s_peak[d][tid];
+        const uint64_t p = s_mem[d][tid].y;
         cp = p > cp ? p : cp;
     }
     if (a.c.cap != 0 && cp > a.c.cap) st |= DSIM_ST_OVER_CAP;
@@ -324,7 +342,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     if (a.peak) {
         uint64_t *row = a.peak + (size_t)c * a.row_width;
 #pragma unroll
-        for (int d = 0; d < ND; ++d) row[d] = s_peak[d][tid];
+        for (int d = 0; d < ND; ++d) row[d] = s_mem[d][tid].y;
         for (int d = ND; d < a.row_width; ++d) row[d] = 0;
     }
 }
