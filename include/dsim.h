@@ -191,9 +191,20 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * lists: the per-stage 1F1B schedule, layers and ops are expanded on the fly.
  * Every replica (d, h) of a pipeline stage runs the same ops at the same
  * times, so one replica per stage is walked; collectives keep their full
- * group size in the cost.  results.row_width must be >= every candidate's P.
- * The transform, its memory rules and the per-op FLOP/byte formulas are the
- * ones documented in DESIGN.md ("The transform").
+ * group size in the cost.  results.row_width must be >= every candidate's P;
+ * a candidate with P > min(row_width, 64, n_layers) or K > 16383 gets
+ * DSIM_ST_BAD_STRATEGY.  The transform: device p*(D*H) + d*H + h runs stage
+ * p of data replica d, tensor rank h; contiguous stages (the first L mod P
+ * get one extra layer); synchronous 1F1B (forward only in inference) with
+ * uneven microbatches (the first rows mod K get one extra row); Megatron
+ * column/row tensor parallelism; each gradient is all-reduced over the D
+ * replicas before its optimizer op; memory by def/use liveness (outputs
+ * allocated, peak sampled, inputs at their last use freed; weights,
+ * optimizer state and the replica's inputs resident from t = 0).
+ * Candidates are simulated one pipeline stage per GPU lane, grouped by P;
+ * the grouping uses a temporary device buffer of about 4 bytes per
+ * candidate, taken from and returned to the stream's memory pool
+ * (hipMallocAsync / hipFreeAsync) inside the call.  n_cand < 2^31.
  */
 DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strategy *cand,
                                      int64_t n_cand, const dsim_device_model *device,
@@ -224,7 +235,12 @@ DSIM_API dsim_status dsim_argmin(const double *makespan, const uint64_t *cand_pe
  * [1e6, 1e12], bytes log-uniform in [1e3, 1e9]; send to a uniform other
  * device; all-reduce over a uniform mask of >= 2 devices; every device
  * keeps up to 16 live buffers of log-uniform sizes in [1e3, 1e9] bytes,
- * freed in a valid order.  The full definition is in the design doc.
+ * freed in a valid order: a compute op or send first frees a uniformly
+ * chosen live buffer of its (source) device with probability 1/2; a compute
+ * op then allocates a new buffer with probability 1/2, and a send's message
+ * (its bytes) becomes a live buffer of the destination, each only while the
+ * device holds fewer than 16.
+ * Log-uniform means uniform over the fp32 bit patterns between the bounds.
  * Constraints: 2 <= n_dev <= 8, 0 <= n_ops < 2^27, 0 <= n_cand < 2^32.
  */
 DSIM_API dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, int32_t n_ops,

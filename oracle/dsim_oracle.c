@@ -32,8 +32,8 @@
  *    budget, microbatch counts, a per-device memory filter and the top-k by
  *    predicted time.
  *
- * Every reading taken where the paper is silent is listed in the design doc
- * ("Readings of the paper").  Parity of the transformer FLOP/byte formulas,
+ * Where the paper is silent, the reading taken is stated at the code that
+ * implements it.  Parity of the transformer FLOP/byte formulas,
  * of the slot order for P >= 3 and of the random-table generator is unpinned
  * by the paper itself (they are this project's definitions); the pins that do
  * exist are exercised by tests/test_oracle_pins.py.
