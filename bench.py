@@ -14,7 +14,9 @@ input already resident in HBM:
     The tables (about 41 GB) are generated on the GPU before timing.
   * "parametric" (extra key of the same line): each strategy grid (tiny MLP,
     large MLP, GPT-2-small inference and training, GPT-3-175B) simulated by
-    dsim_simulate_parametric + top-k, timed with HIP events.
+    dsim_simulate_parametric + top-k, timed with HIP events;
+  * "grids_as_tables": the tiny MLP grid written as explicit op tables
+    (dsim_materialize_tables) and simulated by dsim_simulate_tables + top-k.
 Prints one JSON line (rank 0).  The CPU oracle is timed on a bounded sample
 of the same workload as `cpu_baseline`.
 """
@@ -194,6 +196,42 @@ def bench_parametric(torch, dsim, W, reps, warmup=1):
             "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3), "wall_s": wall_s, "reps": reps}
 
 
+def bench_grid_as_tables(torch, dsim, W, reps, n_dev=8):
+    """A strategy grid as explicit op tables: dsim_materialize_tables writes
+    every op of every device (untimed, once), then a step is
+    dsim_simulate_tables + top-k over those tables."""
+    strat = dsim.dsim_create_grid(W.model, W.grid)
+    n = len(strat)
+    cand = torch.from_numpy(strat).cuda()
+    t, mst = dsim.dsim_materialize_tables(W.model, cand, n_dev, 4096)
+    torch.cuda.synchronize()
+    max_ops = int(t["n_ops"].max().item())
+    res = dsim.alloc_results(n, n_dev)
+    k = W.top_k
+    ws = torch.empty(max(dsim.dsim_argmin_workspace(n, k), 16), dtype=torch.uint8, device="cuda")
+    out_idx = torch.empty(k, dtype=torch.int64, device="cuda")
+    out_mk = torch.empty(k, dtype=torch.float64, device="cuda")
+    found = torch.empty(1, dtype=torch.int32, device="cuda")
+    ev = []
+    for i in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dsim.dsim_simulate_tables(t, n, n_dev, W.device, res, init_live=t["init_live"])
+        dsim.dsim_argmin(res["makespan"], res["cand_peak"], res["status"], W.device.mem_cap_bytes, k, ws, out_idx,
+                         out_mk, found)
+        e1.record()
+        if i:
+            ev.append((e0, e1))
+    torch.cuda.synchronize()
+    step_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    ops = int(t["n_ops"].sum().item())
+    best = int(out_idx[0].item())
+    return {"workload": W.name + " as explicit tables", "n_cand": n, "ops_per_table_max": max_ops,
+            "program_ops": ops, "materialize_status_nonzero": int((mst != 0).sum().item()),
+            "step_ms": step_ms, "candidates_per_s": n / (step_ms * 1e-3),
+            "best": {"index": best, "strategy_DHPK": strat[best].tolist(), "makespan_s": float(out_mk[0].item())}}
+
+
 # fp64 add rate of the chip: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (half the
 # 78.6 TFLOP/s FMA figure, which counts two flops per lane-cycle)
 FP64_ADD_PEAK_T = 256 * 4 * 16 * 2.4e9 / 1e12
@@ -293,6 +331,7 @@ def main():
     out = bench_random_tables(args, torch, dsim, W)
     if not args.no_parametric:
         out["parametric"] = [bench_parametric(torch, dsim, ALL[name], args.param_reps) for name in PARAMETRIC]
+        out["grids_as_tables"] = [bench_grid_as_tables(torch, dsim, ALL["tiny_mlp"], args.param_reps)]
     if args.copy_calibration:
         out["copy_calibration"] = copy_calibration(torch)
     if not args.no_cpu_baseline:

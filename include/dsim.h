@@ -62,6 +62,8 @@ typedef enum {
 #define DSIM_ST_MEM_UNDERFLOW 8   /* an op frees more bytes than its device holds       */
 #define DSIM_ST_BAD_STRATEGY 16   /* (D,H,P,K) violates the transform's preconditions   */
 #define DSIM_ST_OVER_CAP 32       /* peak above dsim_device_model.mem_cap_bytes (> 0)   */
+#define DSIM_ST_NOT_TABLE 64      /* dsim_materialize_tables: the program does not fit  */
+                                  /* the table format (see there)                       */
 
 /* Model families and modes. */
 #define DSIM_MLP 0
@@ -209,6 +211,38 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
 DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strategy *cand,
                                      int64_t n_cand, const dsim_device_model *device,
                                      const dsim_results *results, void *hip_stream);
+
+/*
+ * dsim_materialize_tables -- write the whole distributed program of each of
+ * n_cand strategies (device array `cand`) of `model` -- every op of every
+ * device, the transform of Sec. 4 executed with the semantics of Sec. 2.1 --
+ * as explicit op tables in the dsim_tables layout (op j of candidate c at
+ * j * n_cand + c), so that dsim_simulate_tables simulates it.  Device
+ * p*(D*H) + d*H + h runs stage p of data replica d, tensor rank h.  The
+ * program order interleaves devices, but each device's own op sequence is
+ * the transform's: splits, then slot by slot the ready stages' blocks (a
+ * compute op once per replica device, a tensor-parallel all-reduce once per
+ * data replica over its H ranks) and the slot's Sends in ascending source
+ * stage (one per replica), then the weight update (a gradient all-reduce
+ * once per tensor rank over the D replicas, an optimizer op per device).
+ * The record fields are those of dsim_tables: compute on a, send a -> b
+ * (alloc on b, free on a), all-reduce over a device mask.
+ *   code, flops, bytes, alloc_bytes, free_bytes: device arrays of
+ *     max_ops * n_cand records, written for j < n_ops[c];
+ *   n_ops:     device array [n_cand], the program's op count (0 on error);
+ *   init_live: device array [n_cand * n_dev], bytes resident on each device
+ *     at t = 0 (0 for devices the candidate does not use);
+ *   status:    device array [n_cand]: 0, DSIM_ST_BAD_STRATEGY (the
+ *     transform's preconditions fail, D*H*P > n_dev or K > 16383), or
+ *     DSIM_ST_NOT_TABLE (more than max_ops ops, a FLOP or byte count not
+ *     exact in fp32, or an alloc / free size above 2^32 - 1).
+ * 1 <= n_dev <= 8, max_ops >= 0.  One GPU lane per candidate.
+ */
+DSIM_API dsim_status dsim_materialize_tables(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
+                                    int32_t max_ops, int32_t n_dev, uint32_t *code, float *flops,
+                                    float *bytes, uint32_t *alloc_bytes, uint32_t *free_bytes,
+                                    uint32_t *n_ops, uint64_t *init_live, int32_t *status,
+                                    void *hip_stream);
 
 /*
  * dsim_argmin -- selection of Sec. 5.2 over device arrays of n entries:

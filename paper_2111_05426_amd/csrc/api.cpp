@@ -204,6 +204,24 @@ dsim_status dsim_argmin(const double *makespan, const uint64_t *cand_peak, const
                          (hipStream_t)hip_stream);
 }
 
+dsim_status dsim_materialize_tables(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
+                                    int32_t max_ops, int32_t n_dev, uint32_t *code, float *flops, float *bytes,
+                                    uint32_t *alloc_bytes, uint32_t *free_bytes, uint32_t *n_ops,
+                                    uint64_t *init_live, int32_t *status, void *hip_stream)
+{
+    dsim_status st = check_model(model);
+    if (st) return st;
+    if (n_dev < 1 || n_dev > kMaxTableDev) return fail(DSIM_ERANGE, "n_dev must be 1..%d", kMaxTableDev);
+    if (max_ops < 0) return fail(DSIM_ERANGE, "max_ops must be >= 0");
+    if (n_cand < 0 || n_cand > ((int64_t)1 << 40)) return fail(DSIM_EINVAL, "bad n_cand");
+    if (n_cand == 0) return DSIM_OK;
+    if (!cand || !n_ops || !init_live || !status) return fail(DSIM_EINVAL, "cand, n_ops, init_live and status must not be NULL");
+    if (max_ops > 0 && (!code || !flops || !bytes || !alloc_bytes || !free_bytes))
+        return fail(DSIM_EINVAL, "table buffers must not be NULL");
+    return launch_materialize(*model, cand, n_cand, max_ops, n_dev, code, flops, bytes, alloc_bytes, free_bytes,
+                              n_ops, init_live, status, (hipStream_t)hip_stream);
+}
+
 dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, int32_t n_ops, int32_t n_dev,
                                         uint32_t *code, float *flops, float *bytes, uint32_t *alloc_bytes,
                                         uint32_t *free_bytes, uint32_t *n_ops_out, void *hip_stream)

@@ -1,0 +1,217 @@
+// materialize.hip -- write the whole distributed program of a strategy as an
+// explicit op table.
+//
+// One lane per candidate expands the transform of Sec. 4 for every device
+// (device p*(D*H) + d*H + h runs stage p of data replica d, tensor rank h)
+// in a program order whose per-device projections are those of the
+// transform (Sec. 2.1 semantics depend on nothing else): the splits, then
+// slot by slot every ready stage's block (each compute op once per replica
+// device, each tensor-parallel all-reduce once per data replica over its H
+// ranks) followed by the slot's Sends in ascending source order (one per
+// replica), then every stage's weight update (each gradient all-reduce once
+// per tensor rank over the D replicas, each optimizer op once per device).
+// The records go to the op-major, candidate-fastest table layout that
+// dsim_simulate_tables reads.
+#include "model.h"
+
+namespace dsim {
+namespace {
+
+constexpr int kLanes = 64;
+constexpr uint16_t kNoBlock = 0xffffu;
+
+struct MatArgs {
+    dsim_model m;
+    const dsim_strategy *cand;
+    int64_t n_cand;
+    int32_t max_ops;
+    int32_t n_dev;
+    uint32_t *code;
+    float *flops;
+    float *bytes;
+    uint32_t *alloc;
+    uint32_t *freeb;
+    uint32_t *n_ops;
+    uint64_t *init_live;
+    int32_t *status;
+};
+
+// Appends records for one stage's ops on every replica device.
+struct Emit {
+    const Ctx &x;
+    const MatArgs &g;
+    int64_t c;
+    int64_t j;          // records emitted so far (may pass max_ops: counted, not written)
+    bool inexact;       // a value does not fit the record format exactly
+    int base;           // first device of the stage
+
+    __device__ __forceinline__ void put(uint32_t code, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        // flops and bytes must be exact in fp32, alloc and free in u32
+        const float ff = (float)fl, fb = (float)by;
+        inexact |= fl >= (1ull << 62) || by >= (1ull << 62) || (uint64_t)ff != fl || (uint64_t)fb != by ||
+                   al > 0xffffffffull || fr > 0xffffffffull;
+        if (j < (int64_t)g.max_ops) {
+            const size_t o = (size_t)j * (size_t)g.n_cand + (size_t)c;
+            g.code[o] = code;
+            g.flops[o] = ff;
+            g.bytes[o] = fb;
+            g.alloc[o] = (uint32_t)al;
+            g.freeb[o] = (uint32_t)fr;
+        }
+        ++j;
+    }
+    __device__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        for (int dev = base; dev < base + x.D * x.H; ++dev) put((uint32_t)dev << 8, fl, by, al, fr);
+    }
+    __device__ void ar_tp(uint64_t by)
+    {
+        if (x.H <= 1) return;
+        for (int d = 0; d < x.D; ++d) {
+            const uint32_t mask = ((1u << x.H) - 1u) << (base + d * x.H);
+            put(2u | (mask << 16), 0, by, 0, 0);
+        }
+    }
+    __device__ void ar_dp(uint64_t by)
+    {
+        if (x.D <= 1) return;
+        for (int h = 0; h < x.H; ++h) {
+            uint32_t mask = 0;
+            for (int d = 0; d < x.D; ++d) mask |= 1u << (base + d * x.H + h);
+            put(2u | (mask << 16), 0, by, 0, 0);
+        }
+    }
+    __device__ void send(int t, uint64_t sz, uint64_t fre)
+    {
+        const int tbase = t * x.D * x.H;
+        for (int r = 0; r < x.D * x.H; ++r)
+            put(1u | ((uint32_t)(base + r) << 8) | ((uint32_t)(tbase + r) << 16), 0, sz, sz, fre);
+    }
+};
+
+__global__ __launch_bounds__(kLanes) void k_materialize(const MatArgs g)
+{
+    __shared__ uint16_t s_pos[kMaxTableDev][kLanes], s_nf[kMaxTableDev][kLanes], s_nb[kMaxTableDev][kLanes],
+        s_em[kMaxTableDev][kLanes];
+    const int lane = threadIdx.x;
+    const int64_t c = (int64_t)blockIdx.x * kLanes + lane;
+    if (c >= g.n_cand) return;
+    const dsim_strategy st = g.cand[c];
+    for (int dev = 0; dev < g.n_dev; ++dev) g.init_live[c * g.n_dev + dev] = 0;
+    const bool ok = strategy_ok(g.m, st.D, st.H, st.P, st.K) && st.K <= kMaxK &&
+                    (int64_t)st.D * st.H * st.P <= (int64_t)g.n_dev;
+    if (!ok) {
+        g.n_ops[c] = 0;
+        g.status[c] = DSIM_ST_BAD_STRATEGY;
+        return;
+    }
+    CostConsts none = {};
+    Ctx x = {};
+    make_ctx(g.m, none, st, x);
+    const int DH = x.D * x.H;
+    Emit e{x, g, c, 0, false, 0};
+    for (int s = 0; s < x.P; ++s) {
+        const uint64_t r0 = resident(x, s);
+        for (int r = 0; r < DH; ++r) g.init_live[c * g.n_dev + s * DH + r] = r0;
+        s_pos[s][lane] = 0;
+        s_nf[s][lane] = 0;
+        s_nb[s][lane] = 0;
+    }
+    // microbatch splits before the pipeline
+    if (x.K > 1) {
+        e.base = 0;
+        split(x, e);
+        if (x.train) {
+            e.base = (x.P - 1) * DH;
+            split(x, e);
+        }
+    }
+    const int len = x.train ? 2 * x.K : x.K;
+    for (;;) {
+        bool left = false, any = false;
+        int prev_nf0 = 0;
+        for (int s = 0; s < x.P; ++s) {
+            int pos = s_pos[s][lane], nf = s_nf[s][lane], nb = s_nb[s][lane];
+            const int nf0 = nf;
+            uint16_t em = kNoBlock;
+            if (pos < len) {
+                left = true;
+                bool bwd;
+                int k;
+                block_at(x, s, pos, bwd, k);
+                const bool ready = !bwd ? (s == 0 || prev_nf0 > k) : (s == x.P - 1 ? nf0 > k : s_nb[s + 1][lane] > k);
+                if (ready) {
+                    e.base = s * DH;
+                    if (bwd) block_bwd(x, e, s, k);
+                    else block_fwd(x, e, s, k);
+                    ++pos;
+                    if (bwd) ++nb;
+                    else ++nf;
+                    em = (uint16_t)((k << 1) | (bwd ? 1 : 0));
+                    any = true;
+                }
+            }
+            s_pos[s][lane] = (uint16_t)pos;
+            s_nf[s][lane] = (uint16_t)nf;
+            s_nb[s][lane] = (uint16_t)nb;
+            s_em[s][lane] = em;
+            prev_nf0 = nf0;
+        }
+        if (!left) break;
+        if (!any) {   // no stage can proceed: impossible for 1F1B
+            g.n_ops[c] = 0;
+            g.status[c] = DSIM_ST_BAD_STRATEGY;
+            return;
+        }
+        for (int s = 0; s < x.P; ++s) {
+            const uint16_t em = s_em[s][lane];
+            if (em == kNoBlock) continue;
+            const bool bwd = em & 1;
+            const int k = em >> 1;
+            if ((!bwd && s == x.P - 1) || (bwd && s == 0)) continue;
+            uint64_t sz, fre;
+            send_size(x, s, mb_rows(x, k), bwd, sz, fre);
+            e.base = s * DH;
+            e.send(bwd ? s - 1 : s + 1, sz, fre);
+        }
+    }
+    if (x.train) {
+        for (int s = 0; s < x.P; ++s) {
+            e.base = s * DH;
+            weight_update(x, e, s);
+        }
+    }
+    const bool fits = e.j <= (int64_t)g.max_ops && !e.inexact;
+    g.n_ops[c] = fits ? (uint32_t)e.j : 0u;
+    g.status[c] = fits ? 0 : DSIM_ST_NOT_TABLE;
+}
+
+}  // namespace
+
+dsim_status launch_materialize(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, int32_t max_ops,
+                               int32_t n_dev, uint32_t *code, float *flops, float *bytes, uint32_t *alloc,
+                               uint32_t *freeb, uint32_t *n_ops, uint64_t *init_live, int32_t *status,
+                               hipStream_t s)
+{
+    MatArgs g;
+    g.m = m;
+    g.cand = cand;
+    g.n_cand = n_cand;
+    g.max_ops = max_ops;
+    g.n_dev = n_dev;
+    g.code = code;
+    g.flops = flops;
+    g.bytes = bytes;
+    g.alloc = alloc;
+    g.freeb = freeb;
+    g.n_ops = n_ops;
+    g.init_live = init_live;
+    g.status = status;
+    const int64_t blocks = (n_cand + kLanes - 1) / kLanes;
+    hipLaunchKernelGGL(k_materialize, dim3((unsigned)blocks), dim3(kLanes), 0, s, g);
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? DSIM_OK : hip_fail(e, "materialize launch");
+}
+
+}  // namespace dsim

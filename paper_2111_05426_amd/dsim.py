@@ -83,8 +83,10 @@ def lib():
                                   C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.dsim_generate_random_tables.argtypes = [C.c_uint64, C.c_int64, C.c_int32, C.c_int32] + \
             [C.c_void_p] * 7
+        L.dsim_materialize_tables.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64, C.c_int32,
+                                              C.c_int32] + [C.c_void_p] * 9
         for name in ("dsim_create_grid", "dsim_simulate_tables", "dsim_simulate_parametric", "dsim_argmin",
-                     "dsim_generate_random_tables"):
+                     "dsim_generate_random_tables", "dsim_materialize_tables"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -216,6 +218,23 @@ def dsim_generate_random_tables(seed, n_cand, n_ops, n_dev, tables, stream=None)
                                              _ptr(tables["flops"]), _ptr(tables["bytes"]),
                                              _ptr(tables["alloc"]), _ptr(tables["free"]),
                                              _ptr(tables.get("n_ops")), _stream(stream)))
+
+
+def dsim_materialize_tables(model, cand, n_dev, max_ops, stream=None):
+    """Explicit op tables of the whole distributed program of each strategy
+    (device int32 tensor of shape (n, 4)); returns the tables dict (with
+    init_live, shape (n, n_dev)) and the per-candidate status tensor."""
+    import torch
+    n = int(cand.shape[0])
+    t = alloc_tables(n, max_ops, device=cand.device)
+    t["init_live"] = torch.empty((n, n_dev), dtype=torch.int64, device=cand.device)
+    status = torch.empty(n, dtype=torch.int32, device=cand.device)
+    m = model_struct(model)
+    _check("dsim_materialize_tables",
+           lib().dsim_materialize_tables(C.byref(m), _ptr(cand), n, max_ops, n_dev, _ptr(t["code"]),
+                                         _ptr(t["flops"]), _ptr(t["bytes"]), _ptr(t["alloc"]), _ptr(t["free"]),
+                                         _ptr(t["n_ops"]), _ptr(t["init_live"]), _ptr(status), _stream(stream)))
+    return t, status
 
 
 def select_topk(makespan, cand_peak, status, mem_cap, k, stream=None):

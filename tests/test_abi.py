@@ -14,7 +14,7 @@ def test_exports_every_declared_function():
     names = dsim.header_functions()
     assert set(names) == {"dsim_last_error", "dsim_create_grid", "dsim_simulate_tables",
                           "dsim_simulate_parametric", "dsim_argmin_workspace", "dsim_argmin",
-                          "dsim_generate_random_tables"}
+                          "dsim_generate_random_tables", "dsim_materialize_tables"}
     L = dsim.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -90,3 +90,12 @@ def test_argument_errors_before_launch():
     m = dsim.model_struct(ALL["gpt2_small"].model)
     assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
     assert "NULL" in dsim.dsim_last_error()
+    # materialiser: device count, op capacity, NULL buffers, bad model
+    m = dsim.model_struct(ALL["tiny_mlp"].model)
+    for nd in (0, 9):
+        assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, nd, *([None] * 9)) == dsim.DSIM_ERANGE
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, -1, 4, *([None] * 9)) == dsim.DSIM_ERANGE
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_EINVAL
+    assert L.dsim_materialize_tables(C.byref(m), None, 0, 10, 4, *([None] * 9)) == dsim.DSIM_OK
+    m.family = 7
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_EINVAL
