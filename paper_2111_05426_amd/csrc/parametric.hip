@@ -32,6 +32,9 @@
 // A counting-sort pre-pass groups the candidates by segment width into a
 // temporary permutation (stable, so the grid's own order keeps wavefronts
 // uniform in K).
+#include <mutex>
+#include <type_traits>
+
 #include "model.h"
 
 namespace dsim {
@@ -71,6 +74,7 @@ struct ParArgs {
     int32_t p_bound;
     const uint32_t *perm;   // candidates grouped by segment class
     const uint32_t *meta;   // [0,8) class totals, [8,16) first perm index, [16,24) first lane
+    int32_t narrow_end;     // classes the narrow launch takes: [0, narrow_end)
     double *makespan;
     double *finish;
     uint64_t *peak;
@@ -439,22 +443,44 @@ template <bool TF> struct LdsSeg {
     int64_t esum[2][4][kLanes];  // [backward][pre delta, pre top, suf delta, suf top][lane]
 };
 
-template <bool TF>
-__global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
+template <bool TF> union LdsNarrow {
+    LdsLane<TF> a;
+    LdsSeg<TF> b;
+};
+
+// Wide segments (>= 8 lanes, transformer): at most 8 segments per
+// wavefront, and only stages 0 and P-1 have edge ops, so the edge programs
+// are kept per segment; middle stages walk a zero program.  About 14 KB,
+// which lets two wavefronts share a SIMD.
+constexpr int kMaxSegWide = 8;
+constexpr int kFirstWideClass = 3;   // segment width 8
+constexpr int64_t kSplitMinCand = 8192;
+template <bool TF> struct LdsWide {
+    double2 unit[kMaxSegWide][kKeys][Shape<TF>::U2];
+    int64_t usum[kMaxSegWide][kKeys][2];
+    double2 edge[kMaxSegWide][2][2][Shape<TF>::PRE2 + Shape<TF>::SUF2];   // [segment][stage 0, P-1][backward]
+    int64_t esum[kMaxSegWide][2][2][4];
+    double2 zero[Shape<TF>::PRE2 + Shape<TF>::SUF2];
+    int64_t zsum[4];
+};
+
+// WIDE: the launch for wide segments of a transformer; otherwise every class
+// of an MLP, or the narrow classes of a transformer.
+template <bool TF, bool WIDE>
+__device__ __forceinline__ void parametric_body(const ParArgs &g)
 {
     using Sh = Shape<TF>;
-    __shared__ union {
-        LdsLane<TF> a;
-        LdsSeg<TF> b;
-    } L;
+    constexpr int PST = WIDE ? 1 : kLanes;   // double2 stride of a lane's edge program
+    __shared__ typename std::conditional<WIDE, LdsWide<TF>, LdsNarrow<TF>>::type L;
 
     const int lane = threadIdx.x;
     const uint32_t gl = blockIdx.x * (uint32_t)kLanes;
     if (gl >= g.meta[16 + kClasses]) return;      // beyond the last class (whole wave)
     int cls = 0;
     while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
+    if (WIDE ? cls < kFirstWideClass : cls >= g.narrow_end) return;   // the other launch's classes
     const int W = 1 << cls;
-    const bool shared = W >= 4;
+    const bool shared = WIDE || W >= 4;
     const uint32_t local = gl + lane - g.meta[16 + cls];
     const uint32_t slot = local >> cls;
     const int s = (int)(local & (uint32_t)(W - 1));   // stage of this lane
@@ -504,12 +530,14 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
         rb_f = sz;
         send_size(x, s, 1, true, sz, fre);
         rb_b = sz;
-        if (shared) {
-            // empty edges unless a later record fills them
-            for (int d = 0; d < 2; ++d) {
-                Record e{x, reinterpret_cast<double *>(&L.b.edge[d][0][lane]), 2 * kLanes, 0, 0, 0};
-                e.pad(Sh::PRE2 + Sh::SUF2);
-                for (int f = 0; f < 4; ++f) L.b.esum[d][f][lane] = 0;
+        if constexpr (!WIDE) {
+            if (shared) {
+                // empty edges unless a later record fills them
+                for (int d = 0; d < 2; ++d) {
+                    Record e{x, reinterpret_cast<double *>(&L.b.edge[d][0][lane]), 2 * kLanes, 0, 0, 0};
+                    e.pad(Sh::PRE2 + Sh::SUF2);
+                    for (int f = 0; f < 4; ++f) L.b.esum[d][f][lane] = 0;
+                }
             }
         }
     }
@@ -521,12 +549,25 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
             for (int key = s; key < kKeys; key += W) {
                 const bool bwd = key >= 2;
                 const int mc = bwd ? ((key - 2) & 1) : key;
-                Record r{x, reinterpret_cast<double *>(&L.b.unit[seg][key][0]), 2, 0, 0, 0};
+                double2 *u;
+                int64_t *us;
+                if constexpr (WIDE) {
+                    u = &L.unit[seg][key][0];
+                    us = &L.usum[seg][key][0];
+                } else {
+                    u = &L.b.unit[seg][key][0];
+                    us = &L.b.usum[seg][key][0];
+                }
+                Record r{x, reinterpret_cast<double *>(u), 2, 0, 0, 0};
                 record_unit<TF>(x, bwd, x.mq + (uint64_t)mc, key >= 4, r);
                 r.pad(Sh::U2);
-                L.b.usum[seg][key][0] = r.cur;
-                L.b.usum[seg][key][1] = r.top;
+                us[0] = r.cur;
+                us[1] = r.top;
             }
+        }
+        if constexpr (WIDE) {
+            if (lane < Sh::PRE2 + Sh::SUF2) L.zero[lane] = make_double2(0.0, 0.0);
+            if (lane < 4) L.zsum[lane] = 0;
         }
         __syncthreads();
     }
@@ -577,59 +618,84 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
             const int key = bwd ? 2 + mc + (acc ? 2 : 0) : mc;
             const int n = bwd ? n_b : n_f;
             int64_t delta, top;
-            if (!shared) {
-                double2 *pp = &L.a.prog[d][0][lane];
-                if ((bwd ? key_b : key_f) != key) {
-                    Ctx x = {};
-                    make_ctx(M, g.c, st, x);
-                    x.mlp = !TF;
-                    double *base = reinterpret_cast<double *>(pp);
-                    Record rp{x, base, 2 * kLanes, 0, 0, 0};
-                    Record ru{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
-                    Record rs{x, base + (Sh::PRE2 + Sh::U2) * 2 * kLanes, 2 * kLanes, 0, 0, 0};
-                    record_edges<TF>(x, s, bwd, m, acc, rp, rs);
-                    record_unit<TF>(x, bwd, m, acc, ru);
-                    rp.pad(Sh::PRE2);
-                    ru.pad(Sh::U2);
-                    rs.pad(Sh::SUF2);
-                    compose(rp.cur, rp.top, ru.cur, ru.top, n, rs.cur, rs.top, delta, top);
-                    L.a.sum[d][0][lane] = delta;
-                    L.a.sum[d][1][lane] = top;
-                    if (bwd) key_b = key;
-                    else key_f = key;
+            bool lane_done = false;
+            if constexpr (!WIDE) {
+                if (!shared) {
+                    double2 *pp = &L.a.prog[d][0][lane];
+                    if ((bwd ? key_b : key_f) != key) {
+                        Ctx x = {};
+                        make_ctx(M, g.c, st, x);
+                        x.mlp = !TF;
+                        double *base = reinterpret_cast<double *>(pp);
+                        Record rp{x, base, 2 * kLanes, 0, 0, 0};
+                        Record ru{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+                        Record rs{x, base + (Sh::PRE2 + Sh::U2) * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+                        record_edges<TF>(x, s, bwd, m, acc, rp, rs);
+                        record_unit<TF>(x, bwd, m, acc, ru);
+                        rp.pad(Sh::PRE2);
+                        ru.pad(Sh::U2);
+                        rs.pad(Sh::SUF2);
+                        compose(rp.cur, rp.top, ru.cur, ru.top, n, rs.cur, rs.top, delta, top);
+                        L.a.sum[d][0][lane] = delta;
+                        L.a.sum[d][1][lane] = top;
+                        if (bwd) key_b = key;
+                        else key_f = key;
+                    }
+                    const double2 *up = pp + Sh::PRE2 * kLanes, *sp = pp + (Sh::PRE2 + Sh::U2) * kLanes;
+                    if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
+                    else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
+                    delta = L.a.sum[d][0][lane];
+                    top = L.a.sum[d][1][lane];
+                    lane_done = true;
                 }
-                const double2 *up = pp + Sh::PRE2 * kLanes, *sp = pp + (Sh::PRE2 + Sh::U2) * kLanes;
-                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
-                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
-                delta = L.a.sum[d][0][lane];
-                top = L.a.sum[d][1][lane];
-            } else {
-                double2 *ep = &L.b.edge[d][0][lane];
+            }
+            if (!lane_done) {
+                // edge program and summary of this lane and direction
+                const bool has_edges = !TF || s == 0 || s == P - 1;
+                double2 *ep;
+                int64_t *es;
+                int es_stride;
+                if constexpr (WIDE) {
+                    const int slot = s == 0 ? 0 : 1;
+                    ep = has_edges ? &L.edge[seg][slot][d][0] : &L.zero[0];
+                    es = has_edges ? &L.esum[seg][slot][d][0] : &L.zsum[0];
+                    es_stride = 1;
+                } else {
+                    ep = &L.b.edge[d][0][lane];
+                    es = &L.b.esum[d][0][lane];
+                    es_stride = kLanes;
+                }
                 // transformer edges sit on stages 0 and P-1 only; every MLP
                 // stage ends its backward with its first unit
-                const bool has_edges = !TF || s == 0 || s == P - 1;
                 if (has_edges && (bwd ? key_b : key_f) != key) {
                     Ctx x = {};
                     make_ctx(M, g.c, st, x);
                     x.mlp = !TF;
                     double *base = reinterpret_cast<double *>(ep);
-                    Record rp{x, base, 2 * kLanes, 0, 0, 0};
-                    Record rs{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+                    Record rp{x, base, 2 * PST, 0, 0, 0};
+                    Record rs{x, base + Sh::PRE2 * 2 * PST, 2 * PST, 0, 0, 0};
                     record_edges<TF>(x, s, bwd, m, acc, rp, rs);
                     rp.pad(Sh::PRE2);
                     rs.pad(Sh::SUF2);
-                    L.b.esum[d][0][lane] = rp.cur;
-                    L.b.esum[d][1][lane] = rp.top;
-                    L.b.esum[d][2][lane] = rs.cur;
-                    L.b.esum[d][3][lane] = rs.top;
+                    es[0 * es_stride] = rp.cur;
+                    es[1 * es_stride] = rp.top;
+                    es[2 * es_stride] = rs.cur;
+                    es[3 * es_stride] = rs.top;
                     if (bwd) key_b = key;
                     else key_f = key;
                 }
-                const double2 *up = &L.b.unit[seg][key][0], *sp = ep + Sh::PRE2 * kLanes;
-                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, 1>(ep, up, sp, clk, n, fast);
-                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, 1>(ep, up, sp, clk, n, fast);
-                compose(L.b.esum[d][0][lane], L.b.esum[d][1][lane], L.b.usum[seg][key][0], L.b.usum[seg][key][1],
-                        n, L.b.esum[d][2][lane], L.b.esum[d][3][lane], delta, top);
+                const double2 *up, *sp = ep + Sh::PRE2 * PST;
+                const int64_t *us;
+                if constexpr (WIDE) {
+                    up = &L.unit[seg][key][0];
+                    us = &L.usum[seg][key][0];
+                } else {
+                    up = &L.b.unit[seg][key][0];
+                    us = &L.b.usum[seg][key][0];
+                }
+                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, PST, 1>(ep, up, sp, clk, n, fast);
+                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, PST, 1>(ep, up, sp, clk, n, fast);
+                compose(es[0], es[1 * es_stride], us[0], us[1], n, es[2 * es_stride], es[3 * es_stride], delta, top);
             }
             const int64_t hi = live + top;
             peak = hi > peak ? hi : peak;
@@ -731,6 +797,18 @@ __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
     }
 }
 
+template <bool TF>
+__global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
+{
+    parametric_body<TF, false>(g);
+}
+
+// wide segments of a transformer: two wavefronts per SIMD
+__global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(2))) void k_parametric_wide(const ParArgs g)
+{
+    parametric_body<true, true>(g);
+}
+
 // ---------------------------------------------------------------------------
 // Pre-pass: stable counting sort of the candidates by segment class
 // ---------------------------------------------------------------------------
@@ -813,6 +891,32 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strateg
 
 }  // namespace
 
+namespace {
+
+// One side stream per device (default priority), created on first use and
+// kept until the process ends.
+hipError_t side_stream(hipStream_t *out)
+{
+    static std::mutex mu;
+    static hipStream_t streams[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!streams[dev]) {
+        e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            streams[dev] = nullptr;
+            return e;
+        }
+    }
+    *out = streams[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
 dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, const CostConsts &c,
                               const dsim_results &r, hipStream_t s)
 {
@@ -858,10 +962,47 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     // every class's lanes round up to whole wavefronts: at most one partial
     // wavefront per class beyond n * wmax lanes
     const int64_t waves = (n_cand * wmax + kLanes - 1) / kLanes + kClasses;
-    if (m.family == DSIM_MLP)
-        hipLaunchKernelGGL(k_parametric<false>, dim3((unsigned)waves), dim3(kLanes), 0, s, g);
-    else
-        hipLaunchKernelGGL(k_parametric<true>, dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+    // A large transformer grid splits: the narrow classes run beside the
+    // wide ones (whose smaller LDS footprint lets two wavefronts share a
+    // SIMD).  Small grids and MLPs take one launch for every class.
+    const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
+    g.narrow_end = split ? kFirstWideClass : kClasses;
+    if (m.family == DSIM_MLP) {
+        hipLaunchKernelGGL((k_parametric<false>), dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+    } else if (!split) {
+        hipLaunchKernelGGL((k_parametric<true>), dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+    } else {
+        // narrow segments on a side stream, wide ones on the caller's: the
+        // two launches need different amounts of LDS per wavefront and run
+        // side by side; the caller's stream waits for both
+        hipStream_t side = nullptr;
+        e = side_stream(&side);
+        hipEvent_t fork = nullptr, join = nullptr;
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventRecord(fork, s);
+        if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
+        bool side_launched = false;
+        if (e == hipSuccess) {
+            hipLaunchKernelGGL((k_parametric<true>), dim3((unsigned)waves), dim3(kLanes), 0, side, g);
+            e = hipGetLastError();
+            side_launched = e == hipSuccess;
+        }
+        if (e == hipSuccess) {
+            hipLaunchKernelGGL(k_parametric_wide, dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+            e = hipGetLastError();
+        }
+        if (e == hipSuccess) e = hipEventRecord(join, side);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+        if (fork) (void)hipEventDestroy(fork);
+        if (join) (void)hipEventDestroy(join);
+        if (e != hipSuccess) {
+            // the side launch may still read the temporary buffer
+            if (side_launched) (void)hipStreamSynchronize(side);
+            (void)hipFreeAsync(ws, s);
+            return hip_fail(e, "parametric launch");
+        }
+    }
     e = hipGetLastError();
     const hipError_t e2 = hipFreeAsync(ws, s);
     if (e != hipSuccess) return hip_fail(e, "parametric launch");
