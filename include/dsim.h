@@ -72,6 +72,8 @@ typedef enum {
 #define DSIM_TRAIN_SGD 1
 #define DSIM_TRAIN_ADAM 2
 #define DSIM_TRAIN_ADAM_MIXED 3   /* fp16 weights and gradients, fp32 master, m, v */
+#define DSIM_SCHED_1F1B 0
+#define DSIM_SCHED_GPIPE 1
 
 DSIM_API const char *dsim_last_error(void);
 
@@ -90,11 +92,18 @@ typedef struct {
  *        global_batch rows; n_heads, d_ff, seq_len, vocab are ignored.
  *   TRANSFORMER: GPT-2-shaped decoder; global_batch sequences of seq_len
  *        tokens, n_heads heads, MLP width d_ff, vocabulary vocab.
- *   elem_bytes: bytes per weight/activation element (2 or 4). */
+ *   elem_bytes: bytes per weight/activation element (2 or 4).
+ *   schedule: pipeline schedule of each stage's microbatch blocks in
+ *        training: DSIM_SCHED_1F1B (the paper's synchronous 1F1B,
+ *        w = min(P-1-s, K) warm-up forwards, then forward/backward pairs,
+ *        then w backwards) or DSIM_SCHED_GPIPE (all K forwards, then all K
+ *        backwards, both in microbatch order).  Inference runs the K
+ *        forwards either way. */
 typedef struct {
     int32_t family, mode, n_layers, n_heads;
     int64_t d_model, d_ff, seq_len, vocab, global_batch;
     int32_t elem_bytes;
+    int32_t schedule;
 } dsim_model;
 
 /* A candidate: data-parallel D, tensor-parallel H (the paper's T), pipeline

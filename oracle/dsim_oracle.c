@@ -81,6 +81,7 @@ typedef struct {
     int32_t family, mode, n_layers, n_heads;
     int64_t d_model, d_ff, seq_len, vocab, global_batch;
     int32_t elem_bytes;
+    int32_t schedule;   /* 0: synchronous 1F1B (Sec. 4); 1: GPipe (all forwards, then all backwards) */
 } or_model;
 
 /* ------------------------------------------------------------------------ */
@@ -584,7 +585,8 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
 /* L = q*P + r the first r stages get q+1 layers.  Replica d gets B/D rows  */
 /* (sequences); microbatch k gets (B/D)/K rows plus one for k < (B/D)%K.    */
 /* Each stage runs synchronous 1F1B: w = min(P-1-s, K) warm-up forwards,    */
-/* then F/B pairs, then w backwards; inference runs the K forwards.         */
+/* then F/B pairs, then w backwards (or, with the GPipe schedule, all K     */
+/* forwards then all K backwards); inference runs the K forwards.           */
 /* The global op order follows slots: in slot t every stage, ascending,     */
 /* emits its next block if the block's input was produced in an earlier     */
 /* slot; then the Sends of the slot's results are emitted, ascending by     */
@@ -1299,6 +1301,10 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
         int *tt = seq_t + (size_t)s * 2 * K, *kk = seq_k + (size_t)s * 2 * K, n = 0, i;
         if (!x.train) {
             for (i = 0; i < K; i++) { tt[n] = 0; kk[n++] = i; }
+        } else if (M->schedule == 1) {
+            /* GPipe: every forward, then every backward, in microbatch order */
+            for (i = 0; i < K; i++) { tt[n] = 0; kk[n++] = i; }
+            for (i = 0; i < K; i++) { tt[n] = 1; kk[n++] = i; }
         } else {
             int w = P - 1 - s < K ? P - 1 - s : K;
             for (i = 0; i < w; i++) { tt[n] = 0; kk[n++] = i; }

@@ -28,6 +28,7 @@ from dataclasses import dataclass, replace
 
 MLP, TRANSFORMER = 0, 1
 INFER, TRAIN_SGD, TRAIN_ADAM, TRAIN_ADAM_MIXED = 0, 1, 2, 3
+SCHED_1F1B, SCHED_GPIPE = 0, 1
 
 
 @dataclass(frozen=True)
@@ -42,6 +43,7 @@ class ModelSpec:
     vocab: int
     global_batch: int
     elem_bytes: int
+    schedule: int = 0   # SCHED_1F1B or SCHED_GPIPE
 
 
 @dataclass(frozen=True)
@@ -81,12 +83,12 @@ class Workload:
     tables: RandomTablesSpec = None
 
 
-def mlp(n_layers, d, batch, elem_bytes, mode):
-    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes)
+def mlp(n_layers, d, batch, elem_bytes, mode, schedule=0):
+    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes, schedule)
 
 
-def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None):
-    return ModelSpec(TRANSFORMER, mode, n_layers, heads, d, d_ff or 4 * d, seq, vocab, batch, elem_bytes)
+def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None, schedule=0):
+    return ModelSpec(TRANSFORMER, mode, n_layers, heads, d, d_ff or 4 * d, seq, vocab, batch, elem_bytes, schedule)
 
 
 TINY_MLP = Workload("tiny_mlp", mlp(4, 256, 64, 4, TRAIN_SGD), GridSpec(4, 0, 0, 4))

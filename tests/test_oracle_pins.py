@@ -14,7 +14,7 @@ from dataclasses import replace
 import numpy as np
 import pytest
 
-from paper_2111_05426_amd.workloads import (DeviceSpec, GridSpec, INFER, TRAIN_ADAM, TRAIN_ADAM_MIXED,
+from paper_2111_05426_amd.workloads import (DeviceSpec, GridSpec, INFER, SCHED_GPIPE, TRAIN_ADAM, TRAIN_ADAM_MIXED,
                                             TRAIN_SGD, mlp, transformer, TINY_MLP, LARGE_MLP,
                                             GPT2_SMALL, GPT3_175B)
 
@@ -178,6 +178,58 @@ def test_1f1b_uniform_stages(orc, P, K):
     m = mlp(P, 64, 64, 4, TRAIN_SGD)
     r = orc.sim_strategy(m, 1, 1, P, K, DEV, type_cost=cost)
     assert r["makespan"] == (K + P - 1) * (tf + tb)
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 4, 8])
+@pytest.mark.parametrize("K", [1, 2, 3, 5, 8, 16])
+def test_gpipe_uniform_stages(orc, P, K):
+    """All forwards then all backwards: the forward wave ends at (K+P-1) t_f
+    on the last stage, the backward wave needs another (K+P-1) t_b."""
+    tf, tb = 1.0, 2.0
+    cost = {k: 0.0 for k in orc.TYPES}
+    cost.update(GEMM=tf, GEMMDW=tb)
+    m = mlp(P, 64, 64, 4, TRAIN_SGD, schedule=SCHED_GPIPE)
+    r = orc.sim_strategy(m, 1, 1, P, K, DEV, type_cost=cost)
+    assert r["makespan"] == (K + P - 1) * (tf + tb)
+
+
+@pytest.mark.parametrize("K", [2, 3, 4, 5])
+def test_gpipe_keeps_every_microbatch(orc, K):
+    """Peak memory of one stage (D=H=P=1) by hand from the liveness rule:
+    every layer keeps its Relu output a = e*m*d for the backward, and the
+    peak is sampled after each op's allocation.  GPipe holds all K
+    microbatches' L outputs when the last forward's last Relu (or the first
+    loss gradient) allocates one more: R + (K*L + 1) a.  1F1B never holds
+    more than one microbatch: R + (L + 1) a (with m >> d, so that the L
+    gradient buffers e*d*d stay below 2a, and K <= L + 1, so that the split
+    copy of the inputs, R + K a, is not higher)."""
+    L, d, m_rows, e = 4, 8, 256, 4
+    a, W = e * m_rows * d, e * d * d
+    assert L * W < 2 * a
+    rows = K * m_rows
+    R = L * W + 2 * e * rows * d          # weights, inputs x, targets y
+    one = orc.sim_strategy(mlp(L, d, rows, e, TRAIN_SGD), 1, 1, 1, K, DEV)
+    gp = orc.sim_strategy(mlp(L, d, rows, e, TRAIN_SGD, schedule=SCHED_GPIPE), 1, 1, 1, K, DEV)
+    assert int(one["cand_peak"]) == R + (L + 1) * a
+    assert int(gp["cand_peak"]) == R + (K * L + 1) * a
+    # one stage walks the same ops in both orders: the same op count and,
+    # up to the order of the additions, the same time
+    assert gp["n_ops"] == one["n_ops"]
+    assert gp["makespan"] == pytest.approx(one["makespan"], rel=1e-12)
+
+
+@pytest.mark.parametrize("case", [(mlp(4, 64, 48, 4, INFER), 1, 1, 2, 3), (mlp(6, 64, 40, 2, TRAIN_ADAM), 2, 2, 3, 1),
+                                  (transformer(4, 32, 4, 8, 101, 12, 2, INFER), 2, 2, 2, 4),
+                                  (transformer(3, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED), 1, 2, 3, 1)])
+def test_gpipe_equals_1f1b_when_orders_coincide(orc, case):
+    """Inference runs the K forwards under either schedule, and with K = 1
+    both are F then B: the results are identical."""
+    m, D, H, P, K = case
+    a = orc.sim_strategy(m, D, H, P, K, DEV)
+    b = orc.sim_strategy(replace(m, schedule=SCHED_GPIPE), D, H, P, K, DEV)
+    for key in ("makespan", "cand_peak", "n_ops", "status"):
+        assert a[key] == b[key]
+    assert np.array_equal(a["dev_finish"], b["dev_finish"]) and np.array_equal(a["dev_peak"], b["dev_peak"])
 
 
 @pytest.mark.parametrize("K", [1, 2, 3, 7, 16])
@@ -355,6 +407,8 @@ SYM_CASES = [
     (transformer(4, 32, 4, 8, 100, 12, 2, TRAIN_ADAM_MIXED), 2, 2, 2, 3),
     (transformer(5, 32, 4, 8, 101, 8, 2, INFER), 2, 4, 2, 3),
     (transformer(3, 32, 2, 8, 64, 6, 4, TRAIN_SGD), 3, 2, 3, 2),
+    (mlp(6, 64, 40, 2, TRAIN_ADAM, schedule=SCHED_GPIPE), 2, 2, 3, 5),
+    (transformer(4, 32, 4, 8, 100, 12, 2, TRAIN_ADAM_MIXED, schedule=SCHED_GPIPE), 2, 2, 2, 3),
 ]
 
 
