@@ -34,6 +34,7 @@ struct Ctx {
     int D, H, P, K, L, q, r;
     bool train, mlp;
     int mode;
+    int schedule;   // DSIM_SCHED_1F1B or DSIM_SCHED_GPIPE
     uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
     uint64_t dH, FH, Vh, aH;
     double inv_f, inv_b, inv_l, lat, launch;
@@ -70,6 +71,7 @@ __device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const 
     x.L = M.n_layers;
     x.mlp = M.family == DSIM_MLP;
     x.mode = M.mode;
+    x.schedule = M.schedule;
     x.train = M.mode != DSIM_INFER;
     x.q = x.L / x.P;
     x.r = x.L % x.P;
@@ -456,7 +458,7 @@ __device__ __forceinline__ void split(const Ctx &x, S &o)
 }
 
 // ---------------------------------------------------------------------------
-// Synchronous 1F1B (training) or forward-only (inference) block order
+// Block order of a stage: forward-only (inference); synchronous 1F1B; GPipe
 // ---------------------------------------------------------------------------
 // position `pos` of stage s's block sequence -> (is_backward, microbatch)
 __device__ __forceinline__ void block_at(const Ctx &x, int s, int pos, bool &bwd, int &k)
@@ -464,6 +466,11 @@ __device__ __forceinline__ void block_at(const Ctx &x, int s, int pos, bool &bwd
     if (!x.train) {
         bwd = false;
         k = pos;
+        return;
+    }
+    if (x.schedule == DSIM_SCHED_GPIPE) {   // all forwards, then all backwards
+        bwd = pos >= x.K;
+        k = bwd ? pos - x.K : pos;
         return;
     }
     const int w = (x.P - 1 - s) < x.K ? (x.P - 1 - s) : x.K;

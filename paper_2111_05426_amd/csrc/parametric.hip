@@ -6,7 +6,8 @@
 // the ops of its stage of the distributed program the transform of Sec. 4
 // produces (ops in model.h) and simulates them with the semantics of Sec. 2.1
 // and the cost model of Sec. 3.3:
-//   * synchronous 1F1B (training) or forward-only (inference) per stage;
+//   * synchronous 1F1B or GPipe (training), forward-only (inference) per
+//     stage;
 //   * the global order is slot by slot: every stage runs its next block if
 //     the block's input was produced in an earlier slot (the stages of a slot
 //     touch disjoint devices, so they run in parallel lanes); then the slot's
@@ -581,9 +582,12 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         bool bwd = false, ready = false;
         int k = 0;
         if (active) {
-            // synchronous 1F1B / forward-only position -> (direction, microbatch)
+            // forward-only / GPipe / synchronous 1F1B position -> (direction, microbatch)
             if (!train) {
                 k = pos;
+            } else if (M.schedule == DSIM_SCHED_GPIPE) {
+                bwd = pos >= K;
+                k = bwd ? pos - K : pos;
             } else {
                 const int wu = (P - 1 - s) < K ? (P - 1 - s) : K;
                 if (pos < wu) {

@@ -103,4 +103,8 @@ GPT3_175B = Workload("gpt3_175b",
                      GridSpec(1024, 0, 1, 256),
                      DeviceSpec(mem_cap_bytes=288_000_000_000), top_k=16)
 
-ALL = {w.name: w for w in (TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN, RANDOM_TABLES, GPT3_175B)}
+# the same grid under the GPipe schedule (all forwards, then all backwards)
+GPT3_175B_GPIPE = replace(GPT3_175B, name="gpt3_175b_gpipe", model=replace(GPT3_175B.model, schedule=SCHED_GPIPE))
+
+ALL = {w.name: w for w in (TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN, RANDOM_TABLES, GPT3_175B,
+                           GPT3_175B_GPIPE)}

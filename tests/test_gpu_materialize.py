@@ -7,7 +7,8 @@ parametric path on the same strategies."""
 import numpy as np
 import pytest
 
-from paper_2111_05426_amd.workloads import (DeviceSpec, INFER, TINY_MLP, TRAIN_ADAM, TRAIN_ADAM_MIXED, TRAIN_SGD,
+from paper_2111_05426_amd.workloads import (DeviceSpec, INFER, SCHED_GPIPE, TINY_MLP, TRAIN_ADAM, TRAIN_ADAM_MIXED,
+                                            TRAIN_SGD,
                                             mlp, transformer)
 
 pytestmark = pytest.mark.gpu
@@ -96,6 +97,9 @@ CASES = [
     ("tf_train", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM), all_strats([1, 2], [1, 2, 4], [1, 2], [1, 2, 5], 8)),
     ("tf_mixed", transformer(3, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED), all_strats([1, 2], [1, 2], [1, 3], [1, 4], 8)),
     ("tf_infer", transformer(4, 48, 6, 16, 97, 9, 2, INFER), all_strats([1, 3], [1, 2], [1, 2, 4], [1, 3], 8)),
+    ("mlp_gpipe", mlp(6, 64, 40, 2, TRAIN_ADAM, schedule=SCHED_GPIPE), all_strats([1, 2], [1, 2], [1, 2, 3], [1, 3, 7], 8)),
+    ("tf_gpipe", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, schedule=SCHED_GPIPE),
+     all_strats([1, 2], [1, 2, 4], [1, 2], [1, 2, 5], 8)),
 ]
 
 

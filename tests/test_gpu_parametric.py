@@ -12,7 +12,7 @@ from dataclasses import replace
 import numpy as np
 import pytest
 
-from paper_2111_05426_amd.workloads import (ALL, DeviceSpec, GPT2_SMALL, GPT2_SMALL_TRAIN, GPT3_175B, INFER,
+from paper_2111_05426_amd.workloads import (ALL, DeviceSpec, GPT2_SMALL, GPT2_SMALL_TRAIN, GPT3_175B, INFER, SCHED_GPIPE,
                                             LARGE_MLP, TINY_MLP, TRAIN_ADAM, TRAIN_ADAM_MIXED, TRAIN_SGD, mlp,
                                             transformer)
 
@@ -79,6 +79,10 @@ SMALL = [
     ("tf_mixed", transformer(5, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED), all_strats([1, 2], [1, 2], [1, 2, 5], [1, 4])),
     ("tf_infer", transformer(6, 48, 6, 16, 97, 9, 2, INFER), all_strats([1, 3], [1, 2, 3], [1, 2, 4], [1, 2, 3])),
     ("tf_sgd", transformer(3, 32, 2, 8, 50, 6, 4, TRAIN_SGD), all_strats([1, 2], [1, 2], [1, 3], [1, 2, 3])),
+    ("mlp_adam_gpipe", mlp(6, 64, 40, 2, TRAIN_ADAM, schedule=SCHED_GPIPE),
+     all_strats([1, 2, 4], [1, 2], [1, 2, 3, 4, 5], [1, 3, 7])),
+    ("tf_train_gpipe", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, schedule=SCHED_GPIPE),
+     all_strats([1, 2, 3], [1, 2, 4], [1, 2, 3, 4], [1, 2, 5])),
 ]
 
 
@@ -93,7 +97,10 @@ def test_small_models_vs_full_program(torch_gpu, orc, case):
 
 
 GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
-         replace(LARGE_MLP, name="large_mlp_mixed", model=replace(LARGE_MLP.model, mode=TRAIN_ADAM_MIXED))]
+         replace(LARGE_MLP, name="large_mlp_mixed", model=replace(LARGE_MLP.model, mode=TRAIN_ADAM_MIXED)),
+         replace(LARGE_MLP, name="large_mlp_gpipe", model=replace(LARGE_MLP.model, schedule=SCHED_GPIPE)),
+         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_gpipe",
+                 model=replace(GPT2_SMALL_TRAIN.model, schedule=SCHED_GPIPE))]
 
 
 @pytest.mark.parametrize("w", GRIDS, ids=[w.name for w in GRIDS])
