@@ -50,7 +50,7 @@ class _Model(C.Structure):
     _fields_ = [("family", C.c_int32), ("mode", C.c_int32), ("n_layers", C.c_int32),
                 ("n_heads", C.c_int32), ("d_model", C.c_int64), ("d_ff", C.c_int64),
                 ("seq_len", C.c_int64), ("vocab", C.c_int64), ("global_batch", C.c_int64),
-                ("elem_bytes", C.c_int32), ("schedule", C.c_int32)]
+                ("elem_bytes", C.c_int32), ("schedule", C.c_int32), ("recompute", C.c_int32)]
 
 
 _lib = None
@@ -72,7 +72,8 @@ def _dev(d):
 
 def _model(m):
     return _Model(m.family, m.mode, m.n_layers, m.n_heads, m.d_model, m.d_ff, m.seq_len,
-                  m.vocab, m.global_batch, m.elem_bytes, getattr(m, "schedule", 0))
+                  m.vocab, m.global_batch, m.elem_bytes, getattr(m, "schedule", 0),
+                  getattr(m, "recompute", 0))
 
 
 def _p(a):

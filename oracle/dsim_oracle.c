@@ -82,6 +82,7 @@ typedef struct {
     int64_t d_model, d_ff, seq_len, vocab, global_batch;
     int32_t elem_bytes;
     int32_t schedule;   /* 0: synchronous 1F1B (Sec. 4); 1: GPipe (all forwards, then all backwards) */
+    int32_t recompute;  /* 1: activation recomputation (gradient checkpointing, Fig. 8), training only */
 } or_model;
 
 /* ------------------------------------------------------------------------ */
@@ -594,6 +595,21 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
 /* Within a block every template op is emitted for all replicas of the      */
 /* stage before the next one (collectives once per group).                  */
 /*                                                                          */
+/* Activation recomputation (gradient checkpointing, Fig. 8): the forward   */
+/* block is unchanged, but the backward no longer reads the activations it  */
+/* produced inside the stage's layers, so def/use liveness frees them at    */
+/* their last forward use; the block input (the checkpoint) and the block   */
+/* output (read by the loss / the last stage's final LN) stay live.  The    */
+/* backward block first runs what precedes the layers' backward (the loss   */
+/* gradient; the transformer's head gradients), then replays from the       */
+/* checkpoint, in forward order, every forward op of the stage's layers     */
+/* whose result the layers' backward reads directly or through another     */
+/* replayed op, and then runs the layers' backward on the replayed tensors. */
+/* Ops whose results nothing would read are not replayed: the MLP's last    */
+/* layer (its output is still live) and, in the transformer's last layer,  */
+/* fc2, its all-reduce and the residual add.  For one stage of the 2-layer  */
+/* MLP this is exactly the program of Fig. 8.                               */
+/*                                                                          */
 /* In projection mode only the devices of replica (0,0) of every stage are  */
 /* materialised (Sec. 3.2 projects a program onto devices by dropping the   */
 /* ops that do not touch them); collectives keep their full group size for  */
@@ -627,7 +643,7 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
 typedef struct {
     const or_model *M;
     or_prog *g;
-    int D, H, P, K, slice, train, fam, mode;
+    int D, H, P, K, slice, train, fam, mode, rc;
     int R;                /* replicas materialised per stage */
     int64_t e, rows;      /* element bytes, rows (sequences) per replica */
     int *l0;              /* P+1 stage boundaries */
@@ -773,11 +789,26 @@ static void mlp_dims(const mat *x, int i, int64_t *din, int64_t *dout, int *row)
     *dout = col ? d / x->H : d;
 }
 
-static void mlp_fwd(mat *x, int s, int k)
+/* layer i forward on microbatch k: cur (layer input ids) -> cur (output) */
+static void mlp_layer(mat *x, int s, int k, int i, int32_t *cur, int32_t *tmp)
 {
     int64_t m = mb_rows(x, k), e = x->e, din, dout;
+    int32_t w[1024];
+    int row;
+    mlp_dims(x, i, &din, &dout, &row);
+    gather_pw(x, x->W, s, i - x->l0[s], w);
+    emit_local(x, s, T_GEMM, (double)(2 * m * din * dout), (double)(e * (m * din + din * dout + m * dout)),
+               cur, w, NULL, (uint64_t)(e * m * dout), tmp, 0, NULL);
+    if (row) emit_ar_tp(x, s, T_AR_TP, (double)(e * m * dout), tmp);
+    emit_local(x, s, T_RELU, (double)(m * dout), (double)(2 * e * m * dout),
+               tmp, NULL, NULL, (uint64_t)(e * m * dout), cur, 0, NULL);
+    store_sv(x, s, k, F_LAYER0 + (i - x->l0[s]) * NLF + L_A, cur);
+}
+
+static void mlp_fwd(mat *x, int s, int k)
+{
     int32_t *cur = x->cur, *tmp = x->tmp;
-    int i, r, row;
+    int i, r;
     if (s == 0) {
         if (x->K > 1) gather_sv(x, s, k, F_XK, cur);
         else for (r = 0; r < x->R; r++) cur[r] = x->X[s * x->R + r];
@@ -785,17 +816,7 @@ static void mlp_fwd(mat *x, int s, int k)
         gather_sv(x, s, k, F_RECVA, cur);
     }
     store_sv(x, s, k, F_IN, cur);
-    for (i = x->l0[s]; i < x->l0[s + 1]; i++) {
-        int32_t w[1024];
-        mlp_dims(x, i, &din, &dout, &row);
-        gather_pw(x, x->W, s, i - x->l0[s], w);
-        emit_local(x, s, T_GEMM, (double)(2 * m * din * dout), (double)(e * (m * din + din * dout + m * dout)),
-                   cur, w, NULL, (uint64_t)(e * m * dout), tmp, 0, NULL);
-        if (row) emit_ar_tp(x, s, T_AR_TP, (double)(e * m * dout), tmp);
-        emit_local(x, s, T_RELU, (double)(m * dout), (double)(2 * e * m * dout),
-                   tmp, NULL, NULL, (uint64_t)(e * m * dout), cur, 0, NULL);
-        store_sv(x, s, k, F_LAYER0 + (i - x->l0[s]) * NLF + L_A, cur);
-    }
+    for (i = x->l0[s]; i < x->l0[s + 1]; i++) mlp_layer(x, s, k, i, cur, tmp);
     store_sv(x, s, k, F_OUTA, cur);
 }
 
@@ -814,6 +835,13 @@ static void mlp_bwd(mat *x, int s, int k)
                    a, y, NULL, (uint64_t)(e * m * d), cur, 0, NULL);
     } else {
         gather_sv(x, s, k, F_RECVG, cur);
+    }
+    if (x->rc) {
+        /* replay every layer but the last from the checkpoint; the replayed
+         * outputs replace the saved ones the layers' backward reads */
+        int32_t ra[1024], rt[1024];
+        gather_sv(x, s, k, F_IN, ra);
+        for (i = x->l0[s]; i < x->l0[s + 1] - 1; i++) mlp_layer(x, s, k, i, ra, rt);
     }
     for (i = x->l0[s + 1] - 1; i >= x->l0[s]; i--) {
         int li = i - x->l0[s];
@@ -893,12 +921,62 @@ static uint64_t tf_param(const mat *x, int s, int p)
 static int tf_slot_emb(const mat *x) { return 4 * x->nl_max; }
 static int tf_slot_head(const mat *x) { return 4 * x->nl_max + 1; }
 
+/* layer li of stage s on microbatch k: cur (layer input ids) -> cur
+ * (output), storing the activations the layer's backward reads.  full == 0
+ * stops after GeLU: fc2, its all-reduce and the residual add only produce
+ * the layer output. */
+static void tf_layer(mat *x, int s, int k, int li, const tfdims *tp, int32_t *cur, int full)
+{
+    const tfdims t = *tp;
+    int32_t w[1024], y1[1024], qkv[1024], S[1024], pm[1024], o[1024], z[1024], x2[1024],
+            y2[1024], u[1024], ge[1024], v[1024];
+    int base = F_LAYER0 + li * NLF;
+    store_sv(x, s, k, base + L_X, cur);
+    emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), cur, NULL, NULL, (uint64_t)t.ACT, y1, 0, NULL);
+    gather_pw(x, x->W, s, 4 * li + 0, w);
+    emit_local(x, s, T_QKV, (double)(2 * t.T * t.d * 3 * t.dH),
+               (double)(t.e * (t.T * t.d + t.d * 3 * t.dH + t.T * 3 * t.dH)),
+               y1, w, NULL, (uint64_t)t.QKV, qkv, 0, NULL);
+    emit_local(x, s, T_SCORES, (double)(2 * t.T * t.s * t.dH), (double)(2 * t.OH + t.S2),
+               qkv, NULL, NULL, (uint64_t)t.S2, S, 0, NULL);
+    emit_local(x, s, T_SOFTMAX, (double)(5 * t.m * t.aH * t.s * t.s), (double)(2 * t.S2),
+               S, NULL, NULL, (uint64_t)t.S2, pm, 0, NULL);
+    emit_local(x, s, T_AV, (double)(2 * t.T * t.s * t.dH), (double)(t.S2 + 2 * t.OH),
+               pm, qkv, NULL, (uint64_t)t.OH, o, 0, NULL);
+    gather_pw(x, x->W, s, 4 * li + 1, w);
+    emit_local(x, s, T_OUTPROJ, (double)(2 * t.T * t.dH * t.d),
+               (double)(t.e * (t.T * t.dH + t.dH * t.d + t.T * t.d)),
+               o, w, NULL, (uint64_t)t.ACT, z, 0, NULL);
+    emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, z);
+    emit_local(x, s, T_RESADD, (double)(t.T * t.d), (double)(3 * t.ACT), cur, z, NULL, (uint64_t)t.ACT, x2, 0, NULL);
+    emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), x2, NULL, NULL, (uint64_t)t.ACT, y2, 0, NULL);
+    gather_pw(x, x->W, s, 4 * li + 2, w);
+    emit_local(x, s, T_FC1, (double)(2 * t.T * t.d * t.FH),
+               (double)(t.e * (t.T * t.d + t.d * t.FH + t.T * t.FH)),
+               y2, w, NULL, (uint64_t)t.FF, u, 0, NULL);
+    emit_local(x, s, T_GELU, (double)(8 * t.T * t.FH), (double)(2 * t.FF), u, NULL, NULL, (uint64_t)t.FF, ge, 0, NULL);
+    store_sv(x, s, k, base + L_Y1, y1);
+    store_sv(x, s, k, base + L_QKV, qkv);
+    store_sv(x, s, k, base + L_PM, pm);
+    store_sv(x, s, k, base + L_O, o);
+    store_sv(x, s, k, base + L_X2, x2);
+    store_sv(x, s, k, base + L_Y2, y2);
+    store_sv(x, s, k, base + L_U, u);
+    store_sv(x, s, k, base + L_GE, ge);
+    if (!full) return;
+    gather_pw(x, x->W, s, 4 * li + 3, w);
+    emit_local(x, s, T_FC2, (double)(2 * t.T * t.FH * t.d),
+               (double)(t.e * (t.T * t.FH + t.FH * t.d + t.T * t.d)),
+               ge, w, NULL, (uint64_t)t.ACT, v, 0, NULL);
+    emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, v);
+    emit_local(x, s, T_RESADD, (double)(t.T * t.d), (double)(3 * t.ACT), x2, v, NULL, (uint64_t)t.ACT, cur, 0, NULL);
+}
+
 static void tf_fwd(mat *x, int s, int k)
 {
     tfdims t;
     int32_t *cur = x->cur;
-    int32_t w[1024], y1[1024], qkv[1024], S[1024], pm[1024], o[1024], z[1024], x2[1024],
-            y2[1024], u[1024], ge[1024], v[1024];
+    int32_t w[1024];
     int i, r;
     tf_dims(x, k, &t);
     if (s == 0) {
@@ -913,47 +991,7 @@ static void tf_fwd(mat *x, int s, int k)
         gather_sv(x, s, k, F_RECVA, cur);
     }
     store_sv(x, s, k, F_IN, cur);
-    for (i = x->l0[s]; i < x->l0[s + 1]; i++) {
-        int li = i - x->l0[s], base = F_LAYER0 + li * NLF;
-        store_sv(x, s, k, base + L_X, cur);
-        emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), cur, NULL, NULL, (uint64_t)t.ACT, y1, 0, NULL);
-        gather_pw(x, x->W, s, 4 * li + 0, w);
-        emit_local(x, s, T_QKV, (double)(2 * t.T * t.d * 3 * t.dH),
-                   (double)(t.e * (t.T * t.d + t.d * 3 * t.dH + t.T * 3 * t.dH)),
-                   y1, w, NULL, (uint64_t)t.QKV, qkv, 0, NULL);
-        emit_local(x, s, T_SCORES, (double)(2 * t.T * t.s * t.dH), (double)(2 * t.OH + t.S2),
-                   qkv, NULL, NULL, (uint64_t)t.S2, S, 0, NULL);
-        emit_local(x, s, T_SOFTMAX, (double)(5 * t.m * t.aH * t.s * t.s), (double)(2 * t.S2),
-                   S, NULL, NULL, (uint64_t)t.S2, pm, 0, NULL);
-        emit_local(x, s, T_AV, (double)(2 * t.T * t.s * t.dH), (double)(t.S2 + 2 * t.OH),
-                   pm, qkv, NULL, (uint64_t)t.OH, o, 0, NULL);
-        gather_pw(x, x->W, s, 4 * li + 1, w);
-        emit_local(x, s, T_OUTPROJ, (double)(2 * t.T * t.dH * t.d),
-                   (double)(t.e * (t.T * t.dH + t.dH * t.d + t.T * t.d)),
-                   o, w, NULL, (uint64_t)t.ACT, z, 0, NULL);
-        emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, z);
-        emit_local(x, s, T_RESADD, (double)(t.T * t.d), (double)(3 * t.ACT), cur, z, NULL, (uint64_t)t.ACT, x2, 0, NULL);
-        emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), x2, NULL, NULL, (uint64_t)t.ACT, y2, 0, NULL);
-        gather_pw(x, x->W, s, 4 * li + 2, w);
-        emit_local(x, s, T_FC1, (double)(2 * t.T * t.d * t.FH),
-                   (double)(t.e * (t.T * t.d + t.d * t.FH + t.T * t.FH)),
-                   y2, w, NULL, (uint64_t)t.FF, u, 0, NULL);
-        emit_local(x, s, T_GELU, (double)(8 * t.T * t.FH), (double)(2 * t.FF), u, NULL, NULL, (uint64_t)t.FF, ge, 0, NULL);
-        gather_pw(x, x->W, s, 4 * li + 3, w);
-        emit_local(x, s, T_FC2, (double)(2 * t.T * t.FH * t.d),
-                   (double)(t.e * (t.T * t.FH + t.FH * t.d + t.T * t.d)),
-                   ge, w, NULL, (uint64_t)t.ACT, v, 0, NULL);
-        emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, v);
-        emit_local(x, s, T_RESADD, (double)(t.T * t.d), (double)(3 * t.ACT), x2, v, NULL, (uint64_t)t.ACT, cur, 0, NULL);
-        store_sv(x, s, k, base + L_Y1, y1);
-        store_sv(x, s, k, base + L_QKV, qkv);
-        store_sv(x, s, k, base + L_PM, pm);
-        store_sv(x, s, k, base + L_O, o);
-        store_sv(x, s, k, base + L_X2, x2);
-        store_sv(x, s, k, base + L_Y2, y2);
-        store_sv(x, s, k, base + L_U, u);
-        store_sv(x, s, k, base + L_GE, ge);
-    }
+    for (i = x->l0[s]; i < x->l0[s + 1]; i++) tf_layer(x, s, k, i - x->l0[s], &t, cur, 1);
     if (s == x->P - 1) {
         int32_t yf[1024], lg[1024];
         store_sv(x, s, k, F_XL, cur);
@@ -1002,6 +1040,14 @@ static void tf_bwd(mat *x, int s, int k)
                    dy, xl, NULL, (uint64_t)t.ACT, cur, 0, NULL);
     } else {
         gather_sv(x, s, k, F_RECVG, cur);
+    }
+    if (x->rc) {
+        /* replay the stage's layers from the checkpoint; the last one stops
+         * after GeLU (nothing reads the rest) */
+        int32_t ra[1024];
+        int nl = x->l0[s + 1] - x->l0[s];
+        gather_sv(x, s, k, F_IN, ra);
+        for (i = 0; i < nl; i++) tf_layer(x, s, k, i, &t, ra, i < nl - 1);
     }
     for (i = x->l0[s + 1] - 1; i >= x->l0[s]; i--) {
         int li = i - x->l0[s], base = F_LAYER0 + li * NLF;
@@ -1226,6 +1272,7 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     prog_init(&g);
     x.M = M; x.g = &g; x.D = D; x.H = H; x.P = P; x.K = K; x.slice = slice;
     x.fam = M->family; x.mode = M->mode; x.train = M->mode != MODE_INFER;
+    x.rc = x.train && M->recompute;
     x.R = slice ? 1 : D * H;
     x.e = M->elem_bytes;
     x.rows = M->global_batch / D;

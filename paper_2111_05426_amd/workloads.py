@@ -44,6 +44,7 @@ class ModelSpec:
     global_batch: int
     elem_bytes: int
     schedule: int = 0   # SCHED_1F1B or SCHED_GPIPE
+    recompute: int = 0  # 1: activation recomputation (gradient checkpointing), training only
 
 
 @dataclass(frozen=True)
@@ -83,12 +84,13 @@ class Workload:
     tables: RandomTablesSpec = None
 
 
-def mlp(n_layers, d, batch, elem_bytes, mode, schedule=0):
-    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes, schedule)
+def mlp(n_layers, d, batch, elem_bytes, mode, schedule=0, recompute=0):
+    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes, schedule, recompute)
 
 
-def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None, schedule=0):
-    return ModelSpec(TRANSFORMER, mode, n_layers, heads, d, d_ff or 4 * d, seq, vocab, batch, elem_bytes, schedule)
+def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None, schedule=0, recompute=0):
+    return ModelSpec(TRANSFORMER, mode, n_layers, heads, d, d_ff or 4 * d, seq, vocab, batch, elem_bytes, schedule,
+                     recompute)
 
 
 TINY_MLP = Workload("tiny_mlp", mlp(4, 256, 64, 4, TRAIN_SGD), GridSpec(4, 0, 0, 4))

@@ -218,6 +218,119 @@ def test_gpipe_keeps_every_microbatch(orc, K):
     assert gp["makespan"] == pytest.approx(one["makespan"], rel=1e-12)
 
 
+
+# ---------------------------------------------------------------------------
+# Activation recomputation (gradient checkpointing, Fig. 8)
+# ---------------------------------------------------------------------------
+def _op_multiset(orc, r, types):
+    """Decode per-type op counts from a one-device makespan whose type costs
+    are distinct powers of 8 (every count < 8)."""
+    left, out = int(r["makespan"]), {}
+    for i, t in enumerate(types):
+        out[t] = (left >> (3 * i)) & 7
+    assert left < 8 ** len(types)
+    return out
+
+
+def test_recompute_fig8_program(orc):
+    """One stage of the 2-layer MLP, one microbatch: with recomputation the
+    program holds Fig. 8's ops, i.e. one extra dense layer (Gemm + Relu)
+    replayed in the backward, and nothing else changes."""
+    types = ["GEMM", "RELU", "LOSSGRAD", "RELUGRAD", "GEMMDW", "GEMMDX", "OPT"]
+    cost = {k: 0.0 for k in orc.TYPES}
+    cost.update({t: float(8 ** i) for i, t in enumerate(types)})
+    m = mlp(2, 8, 64, 4, TRAIN_SGD)
+    plain = _op_multiset(orc, orc.sim_strategy(m, 1, 1, 1, 1, DEV, type_cost=cost), types)
+    ck = _op_multiset(orc, orc.sim_strategy(replace(m, recompute=1), 1, 1, 1, 1, DEV, type_cost=cost), types)
+    assert plain == dict(GEMM=2, RELU=2, LOSSGRAD=1, RELUGRAD=2, GEMMDW=2, GEMMDX=2, OPT=2)
+    assert ck == dict(plain, GEMM=3, RELU=3)
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 4])
+@pytest.mark.parametrize("K", [1, 2, 5, 8])
+@pytest.mark.parametrize("sched", [0, SCHED_GPIPE])
+def test_recompute_uniform_stages(orc, P, K, sched):
+    """Two layers per stage: the forward block costs 2 t_f, the backward
+    block replays the first layer (t_f) before its two weight gradients
+    (2 t_b), so both schedules give (K+P-1)(3 t_f + 2 t_b)."""
+    tf, tb = 1.0, 4.0
+    cost = {k: 0.0 for k in orc.TYPES}
+    cost.update(GEMM=tf, GEMMDW=tb)
+    m = mlp(2 * P, 64, 64, 4, TRAIN_SGD, schedule=sched, recompute=1)
+    r = orc.sim_strategy(m, 1, 1, P, K, DEV, type_cost=cost)
+    assert r["makespan"] == (K + P - 1) * (3 * tf + 2 * tb)
+
+
+@pytest.mark.parametrize("K", [2, 3, 4, 5])
+def test_recompute_gpipe_peak(orc, K):
+    """Peak of one stage (D=H=P=1) under GPipe by hand from the liveness
+    rule.  Without recomputation the stage holds all K*L Relu outputs
+    (R + (K*L+1) a).  With it, each forward keeps only its last layer's
+    output (its input chunk is resident anyway), so after the K forwards
+    R + K a are live; the first backward adds its loss gradient and the L-1
+    replayed outputs before its first ReluGrad frees anything:
+    R + (K+L) a, with L W + W < a so that the weight gradients never
+    matter."""
+    L, d, m_rows, e = 4, 8, 256, 4
+    a, W = e * m_rows * d, e * d * d
+    assert (L + 1) * W < a
+    rows = K * m_rows
+    R = L * W + 2 * e * rows * d
+    base = mlp(L, d, rows, e, TRAIN_SGD, schedule=SCHED_GPIPE)
+    gp = orc.sim_strategy(base, 1, 1, 1, K, DEV)
+    rc = orc.sim_strategy(replace(base, recompute=1), 1, 1, 1, K, DEV)
+    assert int(gp["cand_peak"]) == R + (K * L + 1) * a
+    assert int(rc["cand_peak"]) == R + (K + L) * a
+
+
+@pytest.mark.parametrize("case", [(mlp(4, 64, 48, 4, TRAIN_SGD), 1, 1, 4, 3), (mlp(6, 64, 40, 2, TRAIN_ADAM), 2, 1, 6, 4),
+                                  (mlp(4, 64, 48, 4, INFER), 1, 2, 2, 3),
+                                  (transformer(4, 32, 4, 8, 101, 12, 2, INFER), 2, 2, 2, 4)])
+def test_recompute_changes_nothing_without_replay(orc, case):
+    """One MLP layer per stage leaves nothing to replay (the checkpoint and
+    the output are live anyway), and inference has no backward: every
+    output is identical."""
+    m, D, H, P, K = case
+    a = orc.sim_strategy(m, D, H, P, K, DEV)
+    b = orc.sim_strategy(replace(m, recompute=1), D, H, P, K, DEV)
+    for key in ("makespan", "cand_peak", "n_ops", "status"):
+        assert a[key] == b[key]
+    assert np.array_equal(a["dev_finish"], b["dev_finish"]) and np.array_equal(a["dev_peak"], b["dev_peak"])
+
+
+@pytest.mark.parametrize("L,P,H", [(4, 1, 1), (6, 2, 2), (5, 3, 1), (8, 4, 2)])
+def test_recompute_transformer_replays_layers(orc, L, P, H):
+    """The replay repeats every forward op of the stage's layers except the
+    last layer's fc2, its all-reduce and residual add; the embedding, the
+    head and every backward op are not repeated.  Per type, the FLOPs with
+    recomputation are those without, plus the forward share of the replayed
+    ops (one layer's FLOPs are the same in every layer)."""
+    m = transformer(L, 32, 4, 8, 101, 12, 2, TRAIN_ADAM)
+    a = orc.sim_strategy(m, 1, H, P, 2, DEV)["flops_by_type"]
+    b = orc.sim_strategy(replace(m, recompute=1), 1, H, P, 2, DEV)["flops_by_type"]
+    for t in ("QKV", "SCORES", "SOFTMAX", "AV", "OUTPROJ", "FC1", "GELU"):
+        assert b[t] == 2 * a[t], t
+    assert b["FC2"] == a["FC2"] * (2 * L - P) / L
+    # two residual adds per layer, of which the last layer of each stage
+    # replays one; LN: two per layer, plus the final LN which is not replayed
+    per_add = a["RESADD"] / (2 * L)
+    assert b["RESADD"] == a["RESADD"] + per_add * (2 * L - P)
+    per_ln = a["LN"] / (2 * L + 1)
+    assert b["LN"] == a["LN"] + per_ln * 2 * L
+    for t in ("EMBED", "LMHEAD", "XENT_STATS", "XENT_GRAD", "GEMMDW", "GEMMDX", "LN_B", "GELU_B", "AV_B",
+              "SOFTMAX_B", "SCORES_B", "RESADD_B", "EMBED_DW", "OPT"):
+        assert b[t] == a[t], t
+
+
+def test_recompute_lowers_pipeline_peak(orc):
+    """1F1B holds P - s microbatches in flight on stage s; with
+    recomputation each holds its checkpoint and output instead of every
+    activation, so the peak drops (and the time grows by the replay)."""
+    for m in (mlp(16, 256, 256, 2, TRAIN_ADAM), transformer(8, 64, 4, 16, 101, 32, 2, TRAIN_ADAM_MIXED)):
+        a = orc.sim_strategy(m, 1, 1, 4, 8, DEV)
+        b = orc.sim_strategy(replace(m, recompute=1), 1, 1, 4, 8, DEV)
+        assert b["cand_peak"] < a["cand_peak"] and b["makespan"] > a["makespan"]
+
 @pytest.mark.parametrize("case", [(mlp(4, 64, 48, 4, INFER), 1, 1, 2, 3), (mlp(6, 64, 40, 2, TRAIN_ADAM), 2, 2, 3, 1),
                                   (transformer(4, 32, 4, 8, 101, 12, 2, INFER), 2, 2, 2, 4),
                                   (transformer(3, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED), 1, 2, 3, 1)])
