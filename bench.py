@@ -143,7 +143,8 @@ def bench_random_tables(args, torch, dsim, W):
     return out
 
 
-PARAMETRIC = ("tiny_mlp", "large_mlp", "gpt2_small", "gpt2_small_train", "gpt3_175b", "gpt3_175b_gpipe")
+PARAMETRIC = ("tiny_mlp", "large_mlp", "gpt2_small", "gpt2_small_train", "gpt3_175b", "gpt3_175b_gpipe",
+              "gpt3_175b_recompute")
 
 
 def bench_parametric(torch, dsim, W, reps, warmup=1):

@@ -98,12 +98,22 @@ typedef struct {
  *        w = min(P-1-s, K) warm-up forwards, then forward/backward pairs,
  *        then w backwards) or DSIM_SCHED_GPIPE (all K forwards, then all K
  *        backwards, both in microbatch order).  Inference runs the K
- *        forwards either way. */
+ *        forwards either way.
+ *   recompute: 0 or 1.  1 = activation recomputation (gradient
+ *        checkpointing, the appendix's Fig. 8), training only: a forward
+ *        block keeps its input (the checkpoint) and its output live, and the
+ *        activations produced inside the stage's layers die at their last
+ *        forward use; a backward block runs the loss / LM-head gradients,
+ *        then replays from the checkpoint the forward ops of the stage's
+ *        layers whose results the layers' backward reads (all but the last
+ *        MLP layer; every transformer layer, the last one up to its GeLU),
+ *        then the layers' backward. */
 typedef struct {
     int32_t family, mode, n_layers, n_heads;
     int64_t d_model, d_ff, seq_len, vocab, global_batch;
     int32_t elem_bytes;
     int32_t schedule;
+    int32_t recompute;
 } dsim_model;
 
 /* A candidate: data-parallel D, tensor-parallel H (the paper's T), pipeline

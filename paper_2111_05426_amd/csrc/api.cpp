@@ -74,6 +74,7 @@ static dsim_status check_model(const dsim_model *m)
     if (m->elem_bytes < 1 || m->elem_bytes > 8) return fail(DSIM_EINVAL, "elem_bytes must be 1..8");
     if (m->schedule != DSIM_SCHED_1F1B && m->schedule != DSIM_SCHED_GPIPE)
         return fail(DSIM_EINVAL, "unknown schedule %d", m->schedule);
+    if (m->recompute != 0 && m->recompute != 1) return fail(DSIM_EINVAL, "recompute must be 0 or 1");
     if (m->family == DSIM_TRANSFORMER) {
         if (m->n_heads < 1 || m->d_ff < 1 || m->seq_len < 1 || m->vocab < 1)
             return fail(DSIM_EINVAL, "transformer needs n_heads, d_ff, seq_len, vocab >= 1");

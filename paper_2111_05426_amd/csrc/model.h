@@ -35,6 +35,7 @@ struct Ctx {
     bool train, mlp;
     int mode;
     int schedule;   // DSIM_SCHED_1F1B or DSIM_SCHED_GPIPE
+    bool rc;        // activation recomputation (training only)
     uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
     uint64_t dH, FH, Vh, aH;
     double inv_f, inv_b, inv_l, lat, launch;
@@ -73,6 +74,7 @@ __device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const 
     x.mode = M.mode;
     x.schedule = M.schedule;
     x.train = M.mode != DSIM_INFER;
+    x.rc = x.train && M.recompute != 0;
     x.q = x.L / x.P;
     x.r = x.L % x.P;
     x.e = (uint64_t)M.elem_bytes;
@@ -149,17 +151,17 @@ __device__ __forceinline__ void mlp_dims(const Ctx &x, int kind, uint64_t &din, 
     dout = kind == kCol ? x.d / (uint64_t)x.H : x.d;
 }
 
-// One layer's forward.  dead_out: the model's last layer in inference, whose
+// One layer's forward.  free_in: the layer input dies at the Gemm (inference,
+// and layers after the first under recomputation; otherwise the weight
+// gradient reads it); dead_out: the model's last layer in inference, whose
 // output has no use.
 template <class S>
-__device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, int kind, bool dead_out)
+__device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, int kind, bool free_in, bool dead_out)
 {
     const uint64_t e = x.e;
     uint64_t din, dout;
     mlp_dims(x, kind, din, dout);
-    // Gemm: the layer input dies here in inference (training keeps it for
-    // the weight gradient)
-    o.local(2 * m * din * dout, e * (m * din + din * dout + m * dout), e * m * dout, x.train ? 0 : e * m * din);
+    o.local(2 * m * din * dout, e * (m * din + din * dout + m * dout), e * m * dout, free_in ? e * m * din : 0);
     if (kind == kRow) o.ar_tp(e * m * dout);
     // Relu frees the pre-activation
     o.local(m * dout, 2 * e * m * dout, e * m * dout, e * m * dout + (dead_out ? e * m * dout : 0));
@@ -242,25 +244,30 @@ __device__ __forceinline__ void tf_fwd_first(const Ctx &x, S &o, const TfSz &z)
     o.ar_tp(z.ACT);
 }
 
+// One layer's forward.  save: the activations the layer's backward reads
+// stay live (training without recomputation, and the replay); keep_in: the
+// layer input stays live (save, or the checkpoint of a recomputed stage);
+// full = false stops after GeLU (the replay of a stage's last layer, whose
+// output nothing reads).
 template <class S>
-__device__ __forceinline__ void tf_layer_fwd(const Ctx &x, S &o, const TfSz &z)
+__device__ __forceinline__ void tf_layer_fwd(const Ctx &x, S &o, const TfSz &z, bool save, bool keep_in, bool full)
 {
     const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
-    const bool tr = x.train;
-    o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                               // LN1
-    o.local(2 * T * d * 3 * dH, e * (T * d + d * 3 * dH + T * 3 * dH), z.QKV, tr ? 0 : z.ACT);  // QKV
-    o.local(2 * T * S_ * dH, 2 * z.OH + z.S2, z.S2, 0);                                    // scores
-    o.local(5 * z.m * x.aH * S_ * S_, 2 * z.S2, z.S2, z.S2);                               // softmax
-    o.local(2 * T * S_ * dH, z.S2 + 2 * z.OH, z.OH, tr ? 0 : z.S2 + z.QKV);               // P.V
-    o.local(2 * T * dH * d, e * (T * dH + dH * d + T * d), z.ACT, tr ? 0 : z.OH);          // out-proj
+    o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                                  // LN1
+    o.local(2 * T * d * 3 * dH, e * (T * d + d * 3 * dH + T * 3 * dH), z.QKV, save ? 0 : z.ACT);  // QKV
+    o.local(2 * T * S_ * dH, 2 * z.OH + z.S2, z.S2, 0);                                       // scores
+    o.local(5 * z.m * x.aH * S_ * S_, 2 * z.S2, z.S2, z.S2);                                  // softmax
+    o.local(2 * T * S_ * dH, z.S2 + 2 * z.OH, z.OH, save ? 0 : z.S2 + z.QKV);                // P.V
+    o.local(2 * T * dH * d, e * (T * dH + dH * d + T * d), z.ACT, save ? 0 : z.OH);           // out-proj
     o.ar_tp(z.ACT);
-    o.local(T * d, 3 * z.ACT, z.ACT, tr ? z.ACT : 2 * z.ACT);                             // residual
-    o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                               // LN2
-    o.local(2 * T * d * FH, e * (T * d + d * FH + T * FH), z.FF, tr ? 0 : z.ACT);          // fc1
-    o.local(8 * T * FH, 2 * z.FF, z.FF, tr ? 0 : z.FF);                                   // GeLU
-    o.local(2 * T * FH * d, e * (T * FH + FH * d + T * d), z.ACT, tr ? 0 : z.FF);          // fc2
+    o.local(T * d, 3 * z.ACT, z.ACT, keep_in ? z.ACT : 2 * z.ACT);                           // residual
+    o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                                  // LN2
+    o.local(2 * T * d * FH, e * (T * d + d * FH + T * FH), z.FF, save ? 0 : z.ACT);           // fc1
+    o.local(8 * T * FH, 2 * z.FF, z.FF, save ? 0 : z.FF);                                    // GeLU
+    if (!full) return;
+    o.local(2 * T * FH * d, e * (T * FH + FH * d + T * d), z.ACT, save ? 0 : z.FF);           // fc2
     o.ar_tp(z.ACT);
-    o.local(T * d, 3 * z.ACT, z.ACT, tr ? z.ACT : 2 * z.ACT);                             // residual
+    o.local(T * d, 3 * z.ACT, z.ACT, save ? z.ACT : 2 * z.ACT);                              // residual
 }
 
 // last stage, after its layers: final LN and LM head
@@ -334,13 +341,15 @@ __device__ __forceinline__ void block_fwd(const Ctx &x, S &o, int s, int k)
     const uint64_t m = mb_rows(x, k);
     if (x.mlp) {
         const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
-        for (int i = l0; i < l1; ++i) mlp_layer_fwd(x, o, m, mlp_kind(x, i), !x.train && i == x.L - 1);
+        for (int i = l0; i < l1; ++i)
+            mlp_layer_fwd(x, o, m, mlp_kind(x, i), !x.train || (x.rc && i > l0), !x.train && i == x.L - 1);
         return;
     }
     const TfSz z = tf_sizes(x, m);
     if (s == 0) tf_fwd_first(x, o, z);
     const int nl = stage_nl(x, s);
-    for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z);
+    const bool save = x.train && !x.rc;
+    for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z, save, save || (x.rc && i == 0), true);
     if (s == x.P - 1) tf_fwd_last(x, o, z);
 }
 
@@ -352,12 +361,16 @@ __device__ __forceinline__ void block_bwd(const Ctx &x, S &o, int s, int k)
     if (x.mlp) {
         const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
         if (s == x.P - 1) mlp_loss(x, o, m);
+        if (x.rc)   // replay every layer but the last from the checkpoint
+            for (int i = l0; i < l1 - 1; ++i) mlp_layer_fwd(x, o, m, mlp_kind(x, i), false, false);
         for (int i = l1 - 1; i >= l0; --i) mlp_layer_bwd(x, o, m, mlp_kind(x, i), i == l0, i == 0, acc);
         return;
     }
     const TfSz z = tf_sizes(x, m);
     if (s == x.P - 1) tf_bwd_last(x, o, z, acc);
     const int nl = stage_nl(x, s);
+    if (x.rc)   // replay the layers from the checkpoint, the last one up to its GeLU
+        for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z, true, true, i < nl - 1);
     for (int i = 0; i < nl; ++i) tf_layer_bwd(x, o, z, acc);
     if (s == 0) tf_bwd_first(x, o, z, acc);
 }

@@ -167,16 +167,41 @@ struct Record {
     }
 };
 
+// Memory summary only (net bytes, peak above the start), no costs.
+struct Mem {
+    const Ctx &x;
+    int64_t cur, top;
+    __device__ __forceinline__ void local(uint64_t, uint64_t, uint64_t al, uint64_t fr)
+    {
+        const int64_t a = cur + (int64_t)al;
+        top = a > top ? a : top;
+        cur = a - (int64_t)fr;
+    }
+    __device__ __forceinline__ void ar_tp(uint64_t) {}
+    __device__ __forceinline__ void ar_dp(uint64_t) {}
+};
+
+// Liveness of a forward unit.  kFwdBlock: as in a forward block (training
+// keeps what the backward reads; inference and recomputation drop it);
+// kFwdFirst: the first unit of a forward block under recomputation (its
+// input is the checkpoint); kFwdReplay: the backward block's replay, which
+// keeps what the backward reads.  Every variant has the same op costs.
+enum FwdLive { kFwdBlock = 0, kFwdFirst = 1, kFwdReplay = 2 };
+
 // The repeating unit of a block for microbatches of m rows: one transformer
 // layer; one MLP layer (H = 1) or column/row pair (H > 1), in walk order.
 // acc: with gradient accumulation (every backward microbatch but the first).
-template <bool TF>
-__device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, bool acc, Record &r)
+template <bool TF, class S>
+__device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, bool acc, S &r, int live = kFwdBlock)
 {
     if (TF) {
         const TfSz z = tf_sizes(x, m);
-        if (bwd) tf_layer_bwd(x, r, z, acc);
-        else tf_layer_fwd(x, r, z);
+        if (bwd) {
+            tf_layer_bwd(x, r, z, acc);
+        } else {
+            const bool save = live == kFwdReplay || (live == kFwdBlock && x.train && !x.rc);
+            tf_layer_fwd(x, r, z, save, save || live == kFwdFirst, true);
+        }
     } else if (bwd) {
         if (x.H > 1) {
             mlp_layer_bwd(x, r, m, kRow, false, false, acc);
@@ -184,12 +209,27 @@ __device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, bool acc, Record
         } else {
             mlp_layer_bwd(x, r, m, kPlain, false, false, acc);
         }
-    } else if (x.H > 1) {
-        mlp_layer_fwd(x, r, m, kCol, false);
-        mlp_layer_fwd(x, r, m, kRow, false);
     } else {
-        mlp_layer_fwd(x, r, m, kPlain, false);
+        // free_in of the unit's first layer and of its second (pair) layer
+        const bool fi_rest = live != kFwdReplay && (!x.train || x.rc);
+        const bool fi_first = live == kFwdBlock && fi_rest;
+        if (x.H > 1) {
+            mlp_layer_fwd(x, r, m, kCol, fi_first, false);
+            mlp_layer_fwd(x, r, m, kRow, fi_rest, false);
+        } else {
+            mlp_layer_fwd(x, r, m, kPlain, fi_first, false);
+        }
     }
+}
+
+// The replay's last, partial unit: a transformer layer up to its GeLU; the
+// column layer of the MLP's last pair (H > 1); nothing for H = 1.  Its ops
+// are the first ops of a forward unit, with the same costs.
+template <bool TF, class S>
+__device__ void record_partial(const Ctx &x, uint64_t m, S &r)
+{
+    if (TF) tf_layer_fwd(x, r, tf_sizes(x, m), true, true, false);
+    else if (x.H > 1) mlp_layer_fwd(x, r, m, kCol, false, false);
 }
 
 // The ops of stage s's block before (pre) and after (suf) its repeating
@@ -212,7 +252,7 @@ __device__ void record_edges(const Ctx &x, int s, bool bwd, uint64_t m, bool acc
     const int per = x.H > 1 ? 2 : 1, l0 = stage_l0(x, s), nl = stage_nl(x, s);
     if (!bwd) {
         if (!x.train && s == x.P - 1)
-            for (int i = l0 + nl - per; i < l0 + nl; ++i) mlp_layer_fwd(x, rs, m, mlp_kind(x, i), i == x.L - 1);
+            for (int i = l0 + nl - per; i < l0 + nl; ++i) mlp_layer_fwd(x, rs, m, mlp_kind(x, i), true, i == x.L - 1);
     } else {
         if (s == x.P - 1) mlp_loss(x, rp, m);
         for (int i = l0 + per - 1; i >= l0; --i) mlp_layer_bwd(x, rs, m, mlp_kind(x, i), i == l0, i == 0, acc);
@@ -233,6 +273,23 @@ __device__ __forceinline__ void compose(int64_t pd, int64_t pt, int64_t ud, int6
     t = cur + st > t ? cur + st : t;
     delta = cur + sd;
     top = t;
+}
+
+// appends a summary (d2, t2) to (delta, top)
+__device__ __forceinline__ void chain(int64_t &delta, int64_t &top, int64_t d2, int64_t t2)
+{
+    const int64_t t = delta + t2;
+    top = t > top ? t : top;
+    delta += d2;
+}
+
+// pre, a first unit with its own summary, n - 1 units, suf (n >= 1)
+__device__ __forceinline__ void compose_first(int64_t pd, int64_t pt, int64_t fd, int64_t ft, int64_t ud, int64_t ut,
+                                              int n, int64_t sd, int64_t st, int64_t &delta, int64_t &top)
+{
+    int64_t d = pd, t = pt;
+    chain(d, t, fd, ft);
+    compose(d, t, ud, ut, n - 1, sd, st, delta, top);
 }
 
 // Units walked per block: every layer (transformer); every layer or layer
@@ -388,6 +445,17 @@ __device__ __forceinline__ double walk3(const double2 *pre, const double2 *unit,
     return clk;
 }
 
+// the first n entries of a unit program (the replay's partial unit)
+template <int UST>
+__device__ __forceinline__ double walk_prefix(const double2 *unit, int n, double clk)
+{
+    for (int j = 0; j < n; ++j) {
+        const double2 v = unit[(j >> 1) * UST];
+        clk = clk + ((j & 1) ? v.y : v.x);
+    }
+    return clk;
+}
+
 // ---------------------------------------------------------------------------
 // Cross-lane helpers
 // ---------------------------------------------------------------------------
@@ -440,6 +508,7 @@ template <bool TF> struct LdsLane {
 template <bool TF> struct LdsSeg {
     double2 unit[kMaxSegShared][kKeys][Shape<TF>::U2];
     int64_t usum[kMaxSegShared][kKeys][2];
+    int64_t xsum[kMaxSegShared][2][6];   // recomputation, per forward key: first unit, replay unit, partial
     double2 edge[2][Shape<TF>::PRE2 + Shape<TF>::SUF2][kLanes];
     int64_t esum[2][4][kLanes];  // [backward][pre delta, pre top, suf delta, suf top][lane]
 };
@@ -459,15 +528,57 @@ constexpr int64_t kSplitMinCand = 8192;
 template <bool TF> struct LdsWide {
     double2 unit[kMaxSegWide][kKeys][Shape<TF>::U2];
     int64_t usum[kMaxSegWide][kKeys][2];
+    int64_t xsum[kMaxSegWide][2][6];
     double2 edge[kMaxSegWide][2][2][Shape<TF>::PRE2 + Shape<TF>::SUF2];   // [segment][stage 0, P-1][backward]
     int64_t esum[kMaxSegWide][2][2][4];
     double2 zero[Shape<TF>::PRE2 + Shape<TF>::SUF2];
     int64_t zsum[4];
 };
 
+// Records a lane-owned block program of one direction (pre, unit, suf
+// regions from pp, lane stride kLanes) and its composed memory summary: n
+// units; under recomputation the forward block's first unit keeps its input
+// and the backward block replays n_r forward units and the partial unit
+// after its pre ops.
+template <bool TF>
+__device__ void record_lane(const Ctx &x, int s, bool bwd, uint64_t m, bool acc, int n, int n_r, double2 *pp,
+                            int64_t &delta, int64_t &top)
+{
+    using Sh = Shape<TF>;
+    double *base = reinterpret_cast<double *>(pp);
+    Record rp{x, base, 2 * kLanes, 0, 0, 0};
+    Record ru{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+    Record rs{x, base + (Sh::PRE2 + Sh::U2) * 2 * kLanes, 2 * kLanes, 0, 0, 0};
+    record_edges<TF>(x, s, bwd, m, acc, rp, rs);
+    record_unit<TF>(x, bwd, m, acc, ru);
+    rp.pad(Sh::PRE2);
+    ru.pad(Sh::U2);
+    rs.pad(Sh::SUF2);
+    int64_t d = 0, t = 0;
+    if (!x.rc || (!bwd && n < 1)) {
+        compose(rp.cur, rp.top, ru.cur, ru.top, n, rs.cur, rs.top, d, t);
+    } else if (!bwd) {
+        Mem f{x, 0, 0};
+        record_unit<TF>(x, false, m, false, f, kFwdFirst);
+        compose_first(rp.cur, rp.top, f.cur, f.top, ru.cur, ru.top, n, rs.cur, rs.top, d, t);
+    } else {
+        Mem u{x, 0, 0}, q{x, 0, 0};
+        record_unit<TF>(x, false, m, false, u, kFwdReplay);
+        record_partial<TF>(x, m, q);
+        compose(rp.cur, rp.top, u.cur, u.top, n_r, q.cur, q.top, d, t);
+        int64_t d2, t2;
+        compose(0, 0, ru.cur, ru.top, n, rs.cur, rs.top, d2, t2);
+        chain(d, t, d2, t2);
+    }
+    delta = d;
+    top = t;
+}
+
 // WIDE: the launch for wide segments of a transformer; otherwise every class
-// of an MLP, or the narrow classes of a transformer.
-template <bool TF, bool WIDE>
+// of an MLP, or the narrow classes of a transformer.  RC: training with
+// activation recomputation (a separate instantiation keeps the replay out of
+// the other kernels).
+template <bool TF, bool WIDE, bool RC>
 __device__ __forceinline__ void parametric_body(const ParArgs &g)
 {
     using Sh = Shape<TF>;
@@ -505,6 +616,8 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     uint64_t walked = 0, nops = 0;
     uint64_t mq = 0, rb_f = 0, rb_b = 0;   // rows of a short microbatch; Send bytes per row
     int pos = 0, nf = 0, nb = 0, len = 0, mr = 0, n_f = 0, n_b = 0;
+    constexpr bool rc = RC;   // the launch checks it against the model
+    int n_r = 0, n_part = 0;                     // replayed units, entries of the partial unit
     if (live_stage) {
         Ctx x = {};
         make_ctx(M, g.c, st, x);
@@ -526,6 +639,13 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         mr = (int)x.mr;
         n_f = block_units(M, P, st.H, s, false, TF);
         n_b = block_units(M, P, st.H, s, true, TF);
+        if (rc) {
+            const int nl = stage_nl(x, s);
+            n_r = TF ? nl - 1 : nl / (st.H > 1 ? 2 : 1) - 1;
+            Count c{x, 0, 0};
+            record_partial<TF>(x, 1, c);
+            n_part = (int)c.walked;
+        }
         uint64_t sz, fre;
         send_size(x, s, 1, false, sz, fre);
         rb_f = sz;
@@ -560,10 +680,26 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                     us = &L.b.usum[seg][key][0];
                 }
                 Record r{x, reinterpret_cast<double *>(u), 2, 0, 0, 0};
-                record_unit<TF>(x, bwd, x.mq + (uint64_t)mc, key >= 4, r);
+                const uint64_t m = x.mq + (uint64_t)mc;
+                record_unit<TF>(x, bwd, m, key >= 4, r);
                 r.pad(Sh::U2);
                 us[0] = r.cur;
                 us[1] = r.top;
+                if (rc && !bwd) {
+                    int64_t *xs;
+                    if constexpr (WIDE) xs = &L.xsum[seg][key][0];
+                    else xs = &L.b.xsum[seg][key][0];
+                    Mem f{x, 0, 0}, u2{x, 0, 0}, q{x, 0, 0};
+                    record_unit<TF>(x, false, m, false, f, kFwdFirst);
+                    record_unit<TF>(x, false, m, false, u2, kFwdReplay);
+                    record_partial<TF>(x, m, q);
+                    xs[0] = f.cur;
+                    xs[1] = f.top;
+                    xs[2] = u2.cur;
+                    xs[3] = u2.top;
+                    xs[4] = q.cur;
+                    xs[5] = q.top;
+                }
             }
         }
         if constexpr (WIDE) {
@@ -614,6 +750,11 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
 
         // long unit runs take the binade-wise path (uniform per wavefront)
         const bool fast = ballot(ready && (bwd ? n_b : n_f) >= 3) != 0;
+        // under recomputation a wave with backward blocks walks the pre ops
+        // and the replay first (forward lanes: their pre ops, no units), then
+        // every lane's units and suf
+        const bool replay = rc && !all_fwd;
+        const bool fast_r = replay && ballot(ready && bwd && n_r >= 3) != 0;
         const int d = bwd ? 1 : 0;
         const int mc = k < mr ? 1 : 0;
         const uint64_t m = mq + (uint64_t)mc;
@@ -621,33 +762,38 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
             const bool acc = bwd && k >= 1;
             const int key = bwd ? 2 + mc + (acc ? 2 : 0) : mc;
             const int n = bwd ? n_b : n_f;
-            int64_t delta, top;
+            const int nr = bwd ? n_r : 0, np = bwd ? n_part : 0;
+            int64_t delta = 0, top = 0;
             bool lane_done = false;
             if constexpr (!WIDE) {
                 if (!shared) {
                     double2 *pp = &L.a.prog[d][0][lane];
-                    if ((bwd ? key_b : key_f) != key) {
+                    if ((bwd ? key_b : key_f) != key || (replay && bwd && key_f != mc)) {
                         Ctx x = {};
                         make_ctx(M, g.c, st, x);
                         x.mlp = !TF;
-                        double *base = reinterpret_cast<double *>(pp);
-                        Record rp{x, base, 2 * kLanes, 0, 0, 0};
-                        Record ru{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
-                        Record rs{x, base + (Sh::PRE2 + Sh::U2) * 2 * kLanes, 2 * kLanes, 0, 0, 0};
-                        record_edges<TF>(x, s, bwd, m, acc, rp, rs);
-                        record_unit<TF>(x, bwd, m, acc, ru);
-                        rp.pad(Sh::PRE2);
-                        ru.pad(Sh::U2);
-                        rs.pad(Sh::SUF2);
-                        compose(rp.cur, rp.top, ru.cur, ru.top, n, rs.cur, rs.top, delta, top);
-                        L.a.sum[d][0][lane] = delta;
-                        L.a.sum[d][1][lane] = top;
-                        if (bwd) key_b = key;
-                        else key_f = key;
+                        if ((bwd ? key_b : key_f) != key) {
+                            record_lane<TF>(x, s, bwd, m, acc, n, n_r, pp, L.a.sum[d][0][lane], L.a.sum[d][1][lane]);
+                            if (bwd) key_b = key;
+                            else key_f = key;
+                        }
+                        if (replay && bwd && key_f != mc) {   // the replay walks the forward unit of this size
+                            record_lane<TF>(x, s, false, m, false, n_f, n_r, &L.a.prog[0][0][lane], L.a.sum[0][0][lane],
+                                            L.a.sum[0][1][lane]);
+                            key_f = mc;
+                        }
                     }
                     const double2 *up = pp + Sh::PRE2 * kLanes, *sp = pp + (Sh::PRE2 + Sh::U2) * kLanes;
-                    if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
-                    else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
+                    if (replay) {
+                        const double2 *fu = &L.a.prog[0][Sh::PRE2][lane];
+                        clk = walk3<Sh::PRE2, Sh::F_U2, 0, kLanes, kLanes>(pp, fu, nullptr, clk, nr, fast_r);
+                        clk = walk_prefix<kLanes>(fu, np, clk);
+                        clk = walk3<0, Sh::U2, Sh::SUF2, kLanes, kLanes>(nullptr, up, sp, clk, n, fast);
+                    } else if (all_fwd) {
+                        clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
+                    } else {
+                        clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, kLanes, kLanes>(pp, up, sp, clk, n, fast);
+                    }
                     delta = L.a.sum[d][0][lane];
                     top = L.a.sum[d][1][lane];
                     lane_done = true;
@@ -688,18 +834,39 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                     if (bwd) key_b = key;
                     else key_f = key;
                 }
-                const double2 *up, *sp = ep + Sh::PRE2 * PST;
-                const int64_t *us;
+                const double2 *up, *fu, *sp = ep + Sh::PRE2 * PST;
+                const int64_t *us, *xs;
                 if constexpr (WIDE) {
                     up = &L.unit[seg][key][0];
                     us = &L.usum[seg][key][0];
+                    fu = &L.unit[seg][mc][0];
+                    xs = &L.xsum[seg][mc][0];
                 } else {
                     up = &L.b.unit[seg][key][0];
                     us = &L.b.usum[seg][key][0];
+                    fu = &L.b.unit[seg][mc][0];
+                    xs = &L.b.xsum[seg][mc][0];
                 }
-                if (all_fwd) clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, PST, 1>(ep, up, sp, clk, n, fast);
-                else clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, PST, 1>(ep, up, sp, clk, n, fast);
-                compose(es[0], es[1 * es_stride], us[0], us[1], n, es[2 * es_stride], es[3 * es_stride], delta, top);
+                if (replay) {
+                    clk = walk3<Sh::PRE2, Sh::F_U2, 0, PST, 1>(ep, fu, nullptr, clk, nr, fast_r);
+                    clk = walk_prefix<1>(fu, np, clk);
+                    clk = walk3<0, Sh::U2, Sh::SUF2, PST, 1>(nullptr, up, sp, clk, n, fast);
+                } else if (all_fwd) {
+                    clk = walk3<Sh::F_PRE2, Sh::F_U2, Sh::F_SUF2, PST, 1>(ep, up, sp, clk, n, fast);
+                } else {
+                    clk = walk3<Sh::PRE2, Sh::U2, Sh::SUF2, PST, 1>(ep, up, sp, clk, n, fast);
+                }
+                const int64_t pd = es[0], pt = es[1 * es_stride], sd = es[2 * es_stride], st2 = es[3 * es_stride];
+                if (!rc) {
+                    compose(pd, pt, us[0], us[1], n, sd, st2, delta, top);
+                } else if (!bwd) {
+                    compose_first(pd, pt, xs[0], xs[1], us[0], us[1], n, sd, st2, delta, top);
+                } else {
+                    compose(pd, pt, xs[2], xs[3], n_r, xs[4], xs[5], delta, top);
+                    int64_t d2, t2;
+                    compose(0, 0, us[0], us[1], n, sd, st2, d2, t2);
+                    chain(delta, top, d2, t2);
+                }
             }
             const int64_t hi = live + top;
             peak = hi > peak ? hi : peak;
@@ -801,16 +968,17 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     }
 }
 
-template <bool TF>
+template <bool TF, bool RC>
 __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
 {
-    parametric_body<TF, false>(g);
+    parametric_body<TF, false, RC>(g);
 }
 
 // wide segments of a transformer: two wavefronts per SIMD
+template <bool RC>
 __global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(2))) void k_parametric_wide(const ParArgs g)
 {
-    parametric_body<true, true>(g);
+    parametric_body<true, true, RC>(g);
 }
 
 // ---------------------------------------------------------------------------
@@ -971,10 +1139,14 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     // SIMD).  Small grids and MLPs take one launch for every class.
     const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
     g.narrow_end = split ? kFirstWideClass : kClasses;
+    const bool rc = m.mode != DSIM_INFER && m.recompute != 0;
+    const dim3 grid((unsigned)waves), block(kLanes);
     if (m.family == DSIM_MLP) {
-        hipLaunchKernelGGL((k_parametric<false>), dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+        if (rc) hipLaunchKernelGGL((k_parametric<false, true>), grid, block, 0, s, g);
+        else hipLaunchKernelGGL((k_parametric<false, false>), grid, block, 0, s, g);
     } else if (!split) {
-        hipLaunchKernelGGL((k_parametric<true>), dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+        if (rc) hipLaunchKernelGGL((k_parametric<true, true>), grid, block, 0, s, g);
+        else hipLaunchKernelGGL((k_parametric<true, false>), grid, block, 0, s, g);
     } else {
         // narrow segments on a side stream, wide ones on the caller's: the
         // two launches need different amounts of LDS per wavefront and run
@@ -988,12 +1160,14 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
         if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
         bool side_launched = false;
         if (e == hipSuccess) {
-            hipLaunchKernelGGL((k_parametric<true>), dim3((unsigned)waves), dim3(kLanes), 0, side, g);
+            if (rc) hipLaunchKernelGGL((k_parametric<true, true>), grid, block, 0, side, g);
+            else hipLaunchKernelGGL((k_parametric<true, false>), grid, block, 0, side, g);
             e = hipGetLastError();
             side_launched = e == hipSuccess;
         }
         if (e == hipSuccess) {
-            hipLaunchKernelGGL(k_parametric_wide, dim3((unsigned)waves), dim3(kLanes), 0, s, g);
+            if (rc) hipLaunchKernelGGL((k_parametric_wide<true>), grid, block, 0, s, g);
+            else hipLaunchKernelGGL((k_parametric_wide<false>), grid, block, 0, s, g);
             e = hipGetLastError();
         }
         if (e == hipSuccess) e = hipEventRecord(join, side);

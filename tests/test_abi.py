@@ -90,6 +90,11 @@ def test_argument_errors_before_launch():
     m = dsim.model_struct(ALL["gpt2_small"].model)
     assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
     assert "NULL" in dsim.dsim_last_error()
+    for field, bad in (("schedule", 2), ("recompute", 2), ("recompute", -1)):
+        m = dsim.model_struct(ALL["gpt2_small_train"].model)
+        setattr(m, field, bad)
+        assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+        assert field in dsim.dsim_last_error()
     # materialiser: device count, op capacity, NULL buffers, bad model
     m = dsim.model_struct(ALL["tiny_mlp"].model)
     for nd in (0, 9):

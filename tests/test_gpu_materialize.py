@@ -100,6 +100,11 @@ CASES = [
     ("mlp_gpipe", mlp(6, 64, 40, 2, TRAIN_ADAM, schedule=SCHED_GPIPE), all_strats([1, 2], [1, 2], [1, 2, 3], [1, 3, 7], 8)),
     ("tf_gpipe", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, schedule=SCHED_GPIPE),
      all_strats([1, 2], [1, 2, 4], [1, 2], [1, 2, 5], 8)),
+    ("mlp_recompute", mlp(8, 64, 40, 2, TRAIN_ADAM, recompute=1), all_strats([1, 2], [1, 2], [1, 2, 3], [1, 3, 7], 8)),
+    ("tf_recompute", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM_MIXED, recompute=1),
+     all_strats([1, 2], [1, 2, 4], [1, 2], [1, 2, 5], 8)),
+    ("tf_gpipe_recompute", transformer(5, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, schedule=SCHED_GPIPE, recompute=1),
+     all_strats([1, 2], [1, 2], [1, 2, 3], [1, 3], 8)),
 ]
 
 

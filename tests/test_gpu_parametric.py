@@ -83,6 +83,16 @@ SMALL = [
      all_strats([1, 2, 4], [1, 2], [1, 2, 3, 4, 5], [1, 3, 7])),
     ("tf_train_gpipe", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, schedule=SCHED_GPIPE),
      all_strats([1, 2, 3], [1, 2, 4], [1, 2, 3, 4], [1, 2, 5])),
+    ("mlp_adam_rc", mlp(7, 64, 40, 2, TRAIN_ADAM, recompute=1), all_strats([1, 2, 4], [1], [1, 2, 3, 4, 7], [1, 3, 7])),
+    ("mlp_mixed_rc", mlp(8, 32, 36, 2, TRAIN_ADAM_MIXED, recompute=1), all_strats([1, 2], [1, 2, 4], [1, 2, 4, 8],
+                                                                                    [1, 2, 6])),
+    ("mlp_sgd_gpipe_rc", mlp(12, 64, 48, 4, TRAIN_SGD, schedule=SCHED_GPIPE, recompute=1),
+     all_strats([1, 3], [1, 2], [1, 2, 3, 5], [1, 2, 5])),
+    ("tf_train_rc", transformer(5, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, recompute=1), all_strats([1, 2, 3], [1, 2, 4],
+                                                                                            [1, 2, 3, 5], [1, 2, 5])),
+    ("tf_mixed_gpipe_rc", transformer(6, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED, schedule=SCHED_GPIPE, recompute=1),
+     all_strats([1, 2], [1, 2], [1, 2, 4, 5], [1, 4])),
+    ("tf_infer_rc", transformer(6, 48, 6, 16, 97, 9, 2, INFER, recompute=1), all_strats([1, 3], [1, 2], [1, 4], [1, 3])),
 ]
 
 
@@ -100,7 +110,9 @@ GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(LARGE_MLP, name="large_mlp_mixed", model=replace(LARGE_MLP.model, mode=TRAIN_ADAM_MIXED)),
          replace(LARGE_MLP, name="large_mlp_gpipe", model=replace(LARGE_MLP.model, schedule=SCHED_GPIPE)),
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_gpipe",
-                 model=replace(GPT2_SMALL_TRAIN.model, schedule=SCHED_GPIPE))]
+                 model=replace(GPT2_SMALL_TRAIN.model, schedule=SCHED_GPIPE)),
+         replace(LARGE_MLP, name="large_mlp_recompute", model=replace(LARGE_MLP.model, recompute=1)),
+         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_recompute", model=replace(GPT2_SMALL_TRAIN.model, recompute=1))]
 
 
 @pytest.mark.parametrize("w", GRIDS, ids=[w.name for w in GRIDS])
@@ -127,15 +139,16 @@ def test_workload_grid_vs_oracle(torch_gpu, orc, w):
     assert int(found.item()) == rf and np.array_equal(idx.cpu().numpy(), ri)
 
 
-def test_gpt3_grid_sampled(torch_gpu, orc):
-    """The GPT-3-shaped grid at full size (39,965 strategies, one launch, the
-    288e9-byte cap, top-16): a seeded sample plus the selected top-16 and the
-    extreme microbatch counts are compared one by one with the oracle."""
+@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"]], ids=["1f1b", "recompute"])
+def test_gpt3_grid_sampled(torch_gpu, orc, w):
+    """The GPT-3-shaped grid at full size (39,965 strategies, the launch
+    configuration the benchmark times, the 288e9-byte cap, top-16): a seeded
+    sample plus the selected top-16 and the extreme microbatch counts are
+    compared one by one with the oracle."""
     from paper_2111_05426_amd import dsim
-    w = GPT3_175B
     strat = dsim.dsim_create_grid(w.model, w.grid)
     assert len(strat) == 39965
-    print("gpt3_175b: simulating %d candidates" % len(strat), flush=True)
+    print("%s: simulating %d candidates" % (w.name, len(strat)), flush=True)
     g = run_gpu(torch_gpu, w.model, strat, w.device, 64)
     idx, mk, found = dsim.select_topk(g["gpu"]["makespan"], g["gpu"]["cand_peak"], g["gpu"]["status"],
                                       w.device.mem_cap_bytes, w.top_k)
@@ -146,7 +159,7 @@ def test_gpt3_grid_sampled(torch_gpu, orc):
     K = strat[:, 3]
     pick = np.unique(np.concatenate([rng.choice(len(strat), 250, replace=False), top,
                                      np.nonzero(K == K.max())[0][:5], np.nonzero(K == 1)[0][:5]]))
-    print("gpt3_175b: oracle on %d sampled candidates" % len(pick), flush=True)
+    print("%s: oracle on %d sampled candidates" % (w.name, len(pick)), flush=True)
     o = orc.run_strategies(w.model, strat[pick], w.device, slice=True, row_width=64, threads=8)
     sub = {k: (v[pick] if isinstance(v, np.ndarray) else v) for k, v in g.items()}
     compare(sub, o, strat[pick])
@@ -201,6 +214,9 @@ EDGE_MODELS = [
     ("tf_tiny_layers", transformer(16, 8, 2, 2, 4_000_000, 8, 2, TRAIN_SGD), all_strats([1, 2], [1, 2], [1, 2], [1, 4, 8])),
     ("mlp_long", mlp(32, 128, 64, 2, TRAIN_ADAM), all_strats([1, 2], [1, 2], [1, 2, 4], [1, 3, 8, 32])),
     ("tf_infer_long", transformer(40, 32, 2, 8, 512, 32, 4, INFER), all_strats([1, 2], [1, 2], [1, 5], [1, 4, 32])),
+    ("tf_long_rc", transformer(24, 64, 4, 16, 1000, 16, 2, TRAIN_ADAM, recompute=1),
+     all_strats([1, 2], [1, 2, 4], [1, 2, 3], [1, 2, 5, 16])),
+    ("mlp_long_rc", mlp(32, 128, 64, 2, TRAIN_ADAM, recompute=1), all_strats([1, 2], [1, 2], [1, 2, 4], [1, 3, 8, 32])),
 ]
 
 
