@@ -16,7 +16,7 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 # status bits
 ST_BAD_OP, ST_BAD_DEVICE, ST_SELF_SEND, ST_MEM_UNDERFLOW, ST_BAD_STRATEGY, ST_OVER_CAP = 1, 2, 4, 8, 16, 32
-COMPUTE, SEND, ALLREDUCE = 0, 1, 2
+COMPUTE, SEND, ALLREDUCE, BCAST, REDUCE = 0, 1, 2, 3, 4
 TF_RESIDENT, TF_KEEP = 1, 2
 
 # op type tags (same order as the enum in dsim_oracle.c)
@@ -24,7 +24,7 @@ TYPES = ["SPLIT", "GEMM", "RELU", "AR_TP", "LOSSGRAD", "RELUGRAD", "GEMMDW", "AD
          "GEMMDX", "SEND_F", "SEND_B", "AR_DP", "OPT",
          "LN", "QKV", "SCORES", "SOFTMAX", "AV", "OUTPROJ", "RESADD", "FC1", "GELU", "FC2",
          "EMBED", "LMHEAD", "XENT_STATS", "XENT_GRAD", "LN_B", "RESADD_B", "GELU_B", "AV_B",
-         "SOFTMAX_B", "SCORES_B", "EMBED_DW", "GENERIC"]
+         "SOFTMAX_B", "SCORES_B", "EMBED_DW", "BCAST", "REDUCE", "GENERIC"]
 T = {name: i for i, name in enumerate(TYPES)}
 N_TYPES = len(TYPES)
 
@@ -50,7 +50,8 @@ class _Model(C.Structure):
     _fields_ = [("family", C.c_int32), ("mode", C.c_int32), ("n_layers", C.c_int32),
                 ("n_heads", C.c_int32), ("d_model", C.c_int64), ("d_ff", C.c_int64),
                 ("seq_len", C.c_int64), ("vocab", C.c_int64), ("global_batch", C.c_int64),
-                ("elem_bytes", C.c_int32), ("schedule", C.c_int32), ("recompute", C.c_int32)]
+                ("elem_bytes", C.c_int32), ("schedule", C.c_int32), ("recompute", C.c_int32),
+                ("zero", C.c_int32)]
 
 
 _lib = None
@@ -73,7 +74,7 @@ def _dev(d):
 def _model(m):
     return _Model(m.family, m.mode, m.n_layers, m.n_heads, m.d_model, m.d_ff, m.seq_len,
                   m.vocab, m.global_batch, m.elem_bytes, getattr(m, "schedule", 0),
-                  getattr(m, "recompute", 0))
+                  getattr(m, "recompute", 0), getattr(m, "zero", 0))
 
 
 def _p(a):

@@ -50,7 +50,7 @@
 /* ------------------------------------------------------------------------ */
 /* Public enums (mirrored by value, not by code, in the Python wrapper).     */
 /* ------------------------------------------------------------------------ */
-enum { OR_COMPUTE = 0, OR_SEND = 1, OR_ALLREDUCE = 2 };
+enum { OR_COMPUTE = 0, OR_SEND = 1, OR_ALLREDUCE = 2, OR_BCAST = 3, OR_REDUCE = 4 };
 
 enum {
     ST_BAD_OP = 1, ST_BAD_DEVICE = 2, ST_SELF_SEND = 4, ST_MEM_UNDERFLOW = 8,
@@ -69,6 +69,8 @@ enum {
     T_LN, T_QKV, T_SCORES, T_SOFTMAX, T_AV, T_OUTPROJ, T_RESADD, T_FC1,
     T_GELU, T_FC2, T_EMBED, T_LMHEAD, T_XENT_STATS, T_XENT_GRAD, T_LN_B,
     T_RESADD_B, T_GELU_B, T_AV_B, T_SOFTMAX_B, T_SCORES_B, T_EMBED_DW,
+    /* ZeRO */
+    T_BCAST, T_REDUCE,
     T_GENERIC, T_NTYPES
 };
 
@@ -83,6 +85,7 @@ typedef struct {
     int32_t elem_bytes;
     int32_t schedule;   /* 0: synchronous 1F1B (Sec. 4); 1: GPipe (all forwards, then all backwards) */
     int32_t recompute;  /* 1: activation recomputation (gradient checkpointing, Fig. 8), training only */
+    int32_t zero;       /* 1: ZeRO parameter and gradient partitioning (Fig. 9), training only */
 } or_model;
 
 /* ------------------------------------------------------------------------ */
@@ -113,10 +116,24 @@ static double cost_allreduce(const or_device_model *m, double bytes, int n)
     return two_a * m->link_latency_s + (two_a / (double)n) * (bytes * inv_l);
 }
 
+/* Broadcast from one member of a group to the others, and reduce of the
+ * members' tensors onto one member (the weight distribution and gradient
+ * reduction of Fig. 9): a pipelined chain, (n-1) link latencies plus the
+ * bytes crossing one link once.  With two devices this is the Send of
+ * Sec. 2.1 / Fig. 9; one device costs nothing. */
+static double cost_chain(const or_device_model *m, double bytes, int n)
+{
+    double inv_l;
+    if (n <= 1) return 0.0;
+    inv_l = 1.0 / m->link_bytes_per_s;
+    return (double)(n - 1) * m->link_latency_s + bytes * inv_l;
+}
+
 double or_cost(const or_device_model *m, int kind, double flops, double bytes, int n)
 {
     if (kind == OR_COMPUTE) return cost_compute(m, flops, bytes);
     if (kind == OR_SEND) return cost_send(m, bytes);
+    if (kind == OR_BCAST || kind == OR_REDUCE) return cost_chain(m, bytes, n);
     return cost_allreduce(m, bytes, n);
 }
 
@@ -610,6 +627,18 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
 /* fc2, its all-reduce and the residual add.  For one stage of the 2-layer  */
 /* MLP this is exactly the program of Fig. 8.                               */
 /*                                                                          */
+/* ZeRO partitioning (Fig. 9, training): every parameter group -- in model  */
+/* order the embedding, each layer (an MLP column/row pair when H > 1) and  */
+/* the LM head -- belongs to data replica (group index mod D), which alone  */
+/* holds its weights and optimizer state.  Right before every op that reads */
+/* a weight, its owner broadcasts it to the other replicas of the stage's   */
+/* data-parallel group (one collective per tensor rank; for D = 2 the Send  */
+/* of Fig. 9), and the copies die after that op.  Gradients accumulate on   */
+/* every replica as before; at the weight update each is reduced onto its   */
+/* owner (replacing the all-reduce), whose optimizer step consumes it.      */
+/* Fig. 9's listing computes the owner's first layer before sending the     */
+/* weight; the transform broadcasts before the op on every replica.         */
+/*                                                                          */
 /* In projection mode only the devices of replica (0,0) of every stage are  */
 /* materialised (Sec. 3.2 projects a program onto devices by dropping the   */
 /* ops that do not touch them); collectives keep their full group size for  */
@@ -643,7 +672,7 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
 typedef struct {
     const or_model *M;
     or_prog *g;
-    int D, H, P, K, slice, train, fam, mode, rc;
+    int D, H, P, K, slice, train, fam, mode, rc, zero;
     int R;                /* replicas materialised per stage */
     int64_t e, rows;      /* element bytes, rows (sequences) per replica */
     int *l0;              /* P+1 stage boundaries */
@@ -655,10 +684,25 @@ typedef struct {
     int32_t *tmp;         /* per r scratch */
 } mat;
 
+/* Materialised replicas r of a stage: every (d, h) as r = d*H + h; in
+ * projection mode replica (0,0) alone, or with ZeRO (whose replicas differ
+ * in what they own) every data replica d of tensor rank 0 as r = d. */
+static int rep_of(const mat *x, int d, int h)
+{
+    if (!x->slice) return d * x->H + h;
+    return x->zero ? d : 0;
+}
+
 static int dev_of(const mat *x, int s, int r)
 {
-    /* r indexes d*H + h; in projection mode r = 0 is replica (0,0) */
+    if (x->slice && x->zero) return s * x->D * x->H + r * x->H;
     return s * x->D * x->H + r;
+}
+
+static int data_rep(const mat *x, int r)
+{
+    if (!x->slice) return r / x->H;
+    return x->zero ? r : 0;
 }
 
 static int32_t *SV(mat *x, int s, int r, int k, int f)
@@ -677,8 +721,8 @@ static int64_t mb_rows(const mat *x, int k)
 }
 
 /* multiplicities of one emitted op in projection mode */
-static int64_t mult_dev(const mat *x) { return x->slice ? (int64_t)x->D * x->H : 1; }
-static int64_t mult_tp(const mat *x) { return x->slice ? (int64_t)x->D : 1; }
+static int64_t mult_dev(const mat *x) { return x->slice ? (int64_t)(x->zero ? 1 : x->D) * x->H : 1; }
+static int64_t mult_tp(const mat *x) { return x->slice && !x->zero ? (int64_t)x->D : 1; }
 static int64_t mult_dp(const mat *x) { return x->slice ? (int64_t)x->H : 1; }
 
 /* one local compute op on every materialised replica: in1/in2/in3 arrays of
@@ -710,12 +754,12 @@ static void emit_local(mat *x, int s, int type, double flops, double bytes,
 /* all-reduce over the tensor-parallel group of every data replica */
 static void emit_ar_tp(mat *x, int s, int type, double bytes, const int32_t *t)
 {
-    int d, h, nd = x->slice ? 1 : x->D, nh = x->slice ? 1 : x->H;
+    int d, h, nd = x->slice && !x->zero ? 1 : x->D, nh = x->slice ? 1 : x->H;
     if (x->H <= 1) return;
     for (d = 0; d < nd; d++) {
         op_begin(x->g, OR_ALLREDUCE, type, 0.0, bytes);
         for (h = 0; h < nh; h++) {
-            int r = d * x->H + h;
+            int r = rep_of(x, d, h);
             op_dev(x->g, dev_of(x, s, r));
             op_in(x->g, t[r]);
         }
@@ -776,6 +820,8 @@ static void gather_pw(mat *x, int32_t *a, int s, int p, int32_t *dst)
     for (r = 0; r < x->R; r++) dst[r] = *PW(a, x, s, r, p);
 }
 
+static void use_weight(mat *x, int s, int p, int32_t *dst);
+
 /* ---- MLP: square d x d layers, @dense = Gemm + Relu (Fig. 2) ----------- */
 /* With H > 1 even layers are column-parallel (W: d x d/H, local Relu) and  */
 /* odd layers row-parallel (W: d/H x d, AllReduce of the output over the H  */
@@ -796,7 +842,7 @@ static void mlp_layer(mat *x, int s, int k, int i, int32_t *cur, int32_t *tmp)
     int32_t w[1024];
     int row;
     mlp_dims(x, i, &din, &dout, &row);
-    gather_pw(x, x->W, s, i - x->l0[s], w);
+    use_weight(x, s, i - x->l0[s], w);
     emit_local(x, s, T_GEMM, (double)(2 * m * din * dout), (double)(e * (m * din + din * dout + m * dout)),
                cur, w, NULL, (uint64_t)(e * m * dout), tmp, 0, NULL);
     if (row) emit_ar_tp(x, s, T_AR_TP, (double)(e * m * dout), tmp);
@@ -854,7 +900,7 @@ static void mlp_bwd(mat *x, int s, int k)
         emit_local(x, s, T_GEMMDW, (double)(2 * m * din * dout), (double)(e * (m * din + m * dout + din * dout)),
                    xin, tmp, NULL, (uint64_t)(e * din * dout), gw, 0, NULL);
         accumulate(x, s, li, (uint64_t)(din * dout), gw);
-        gather_pw(x, x->W, s, li, w);
+        use_weight(x, s, li, w);
         emit_local(x, s, T_GEMMDX, (double)(2 * m * din * dout), (double)(e * (m * dout + din * dout + m * din)),
                    tmp, w, NULL, (uint64_t)(e * m * din), cur, 0, NULL);
         if (!row && x->H > 1 && i != 0) emit_ar_tp(x, s, T_AR_TP, (double)(e * m * din), cur);
@@ -921,6 +967,52 @@ static uint64_t tf_param(const mat *x, int s, int p)
 static int tf_slot_emb(const mat *x) { return 4 * x->nl_max; }
 static int tf_slot_head(const mat *x) { return 4 * x->nl_max + 1; }
 
+/* ZeRO (Fig. 9 gives each weight and its gradient to one device): the
+ * model's parameters form groups in model order -- the transformer's
+ * embedding, every layer (with H > 1 an MLP column/row pair), the LM head --
+ * and group g belongs to data replica g mod D of every stage replica set. */
+static int owner_of(const mat *x, int s, int p)
+{
+    int g;
+    if (x->fam == FAM_MLP) {
+        int i = x->l0[s] + p;
+        g = x->H > 1 ? i / 2 : i;
+    } else if (p == tf_slot_emb(x)) {
+        g = 0;
+    } else if (p == tf_slot_head(x)) {
+        g = x->M->n_layers + 1;
+    } else {
+        g = x->l0[s] + p / 4 + 1;
+    }
+    return g % x->D;
+}
+
+/* The weight of slot p as every materialised replica reads it: its own
+ * tensor, or with ZeRO on a non-owner a copy that the owner broadcasts to
+ * the other replicas of its data-parallel group right before the use (the
+ * Sends of Fig. 9 for D = 2); the copy dies after that use. */
+static void use_weight(mat *x, int s, int p, int32_t *dst)
+{
+    int d, h, o, nh;
+    if (!x->zero || x->D == 1) { gather_pw(x, x->W, s, p, dst); return; }
+    o = owner_of(x, s, p);
+    nh = x->slice ? 1 : x->H;
+    for (h = 0; h < nh; h++) {
+        int32_t src = *PW(x->W, x, s, rep_of(x, o, h), p);
+        uint64_t sz = x->g->failed ? 0 : x->g->t_size[src];
+        for (d = 0; d < x->D; d++) {
+            int r = rep_of(x, d, h);
+            dst[r] = d == o ? src : prog_tensor(x->g, dev_of(x, s, r), sz, 0);
+        }
+        op_begin(x->g, OR_BCAST, T_BCAST, 0.0, (double)sz);
+        for (d = 0; d < x->D; d++) op_dev(x->g, dev_of(x, s, rep_of(x, d, h)));
+        op_in(x->g, src);
+        for (d = 0; d < x->D; d++)
+            if (d != o) op_out(x->g, dst[rep_of(x, d, h)]);
+        op_end(x->g, 0, mult_dp(x));
+    }
+}
+
 /* layer li of stage s on microbatch k: cur (layer input ids) -> cur
  * (output), storing the activations the layer's backward reads.  full == 0
  * stops after GeLU: fc2, its all-reduce and the residual add only produce
@@ -933,7 +1025,7 @@ static void tf_layer(mat *x, int s, int k, int li, const tfdims *tp, int32_t *cu
     int base = F_LAYER0 + li * NLF;
     store_sv(x, s, k, base + L_X, cur);
     emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), cur, NULL, NULL, (uint64_t)t.ACT, y1, 0, NULL);
-    gather_pw(x, x->W, s, 4 * li + 0, w);
+    use_weight(x, s, 4 * li + 0, w);
     emit_local(x, s, T_QKV, (double)(2 * t.T * t.d * 3 * t.dH),
                (double)(t.e * (t.T * t.d + t.d * 3 * t.dH + t.T * 3 * t.dH)),
                y1, w, NULL, (uint64_t)t.QKV, qkv, 0, NULL);
@@ -943,14 +1035,14 @@ static void tf_layer(mat *x, int s, int k, int li, const tfdims *tp, int32_t *cu
                S, NULL, NULL, (uint64_t)t.S2, pm, 0, NULL);
     emit_local(x, s, T_AV, (double)(2 * t.T * t.s * t.dH), (double)(t.S2 + 2 * t.OH),
                pm, qkv, NULL, (uint64_t)t.OH, o, 0, NULL);
-    gather_pw(x, x->W, s, 4 * li + 1, w);
+    use_weight(x, s, 4 * li + 1, w);
     emit_local(x, s, T_OUTPROJ, (double)(2 * t.T * t.dH * t.d),
                (double)(t.e * (t.T * t.dH + t.dH * t.d + t.T * t.d)),
                o, w, NULL, (uint64_t)t.ACT, z, 0, NULL);
     emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, z);
     emit_local(x, s, T_RESADD, (double)(t.T * t.d), (double)(3 * t.ACT), cur, z, NULL, (uint64_t)t.ACT, x2, 0, NULL);
     emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), x2, NULL, NULL, (uint64_t)t.ACT, y2, 0, NULL);
-    gather_pw(x, x->W, s, 4 * li + 2, w);
+    use_weight(x, s, 4 * li + 2, w);
     emit_local(x, s, T_FC1, (double)(2 * t.T * t.d * t.FH),
                (double)(t.e * (t.T * t.d + t.d * t.FH + t.T * t.FH)),
                y2, w, NULL, (uint64_t)t.FF, u, 0, NULL);
@@ -964,7 +1056,7 @@ static void tf_layer(mat *x, int s, int k, int li, const tfdims *tp, int32_t *cu
     store_sv(x, s, k, base + L_U, u);
     store_sv(x, s, k, base + L_GE, ge);
     if (!full) return;
-    gather_pw(x, x->W, s, 4 * li + 3, w);
+    use_weight(x, s, 4 * li + 3, w);
     emit_local(x, s, T_FC2, (double)(2 * t.T * t.FH * t.d),
                (double)(t.e * (t.T * t.FH + t.FH * t.d + t.T * t.d)),
                ge, w, NULL, (uint64_t)t.ACT, v, 0, NULL);
@@ -983,7 +1075,7 @@ static void tf_fwd(mat *x, int s, int k)
         int32_t tok[1024];
         if (x->K > 1) gather_sv(x, s, k, F_XK, tok);
         else for (r = 0; r < x->R; r++) tok[r] = x->X[s * x->R + r];
-        gather_pw(x, x->W, s, tf_slot_emb(x), w);
+        use_weight(x, s, tf_slot_emb(x), w);
         emit_local(x, s, T_EMBED, (double)(t.T * t.d), (double)(2 * t.ACT + t.IDS),
                    tok, w, NULL, (uint64_t)t.ACT, cur, 0, NULL);
         emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, cur);
@@ -996,7 +1088,7 @@ static void tf_fwd(mat *x, int s, int k)
         int32_t yf[1024], lg[1024];
         store_sv(x, s, k, F_XL, cur);
         emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), cur, NULL, NULL, (uint64_t)t.ACT, yf, 0, NULL);
-        gather_pw(x, x->W, s, tf_slot_head(x), w);
+        use_weight(x, s, tf_slot_head(x), w);
         emit_local(x, s, T_LMHEAD, (double)(2 * t.T * t.d * t.Vh),
                    (double)(t.e * (t.T * t.d + t.d * t.Vh + t.T * t.Vh)),
                    yf, w, NULL, (uint64_t)t.LOG, lg, 0, NULL);
@@ -1025,7 +1117,7 @@ static void tf_bwd(mat *x, int s, int k)
         else for (r = 0; r < x->R; r++) lab[r] = x->Y[s * x->R + r];
         emit_local(x, s, T_XENT_GRAD, (double)(2 * t.T * t.Vh), (double)(2 * t.LOG + t.ST + t.IDS),
                    lg, st, lab, (uint64_t)t.LOG, dl, 0, NULL);
-        gather_pw(x, x->W, s, tf_slot_head(x), w);
+        use_weight(x, s, tf_slot_head(x), w);
         emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.d * t.Vh),
                    (double)(t.e * (t.T * t.Vh + t.d * t.Vh + t.T * t.d)),
                    dl, w, NULL, (uint64_t)t.ACT, dy, 0, NULL);
@@ -1051,7 +1143,7 @@ static void tf_bwd(mat *x, int s, int k)
     }
     for (i = x->l0[s + 1] - 1; i >= x->l0[s]; i--) {
         int li = i - x->l0[s], base = F_LAYER0 + li * NLF;
-        gather_pw(x, x->W, s, 4 * li + 3, w);
+        use_weight(x, s, 4 * li + 3, w);
         emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.FH * t.d),
                    (double)(t.e * (t.T * t.d + t.FH * t.d + t.T * t.FH)),
                    cur, w, NULL, (uint64_t)t.FF, dg, 0, NULL);
@@ -1063,7 +1155,7 @@ static void tf_bwd(mat *x, int s, int k)
         gather_sv(x, s, k, base + L_U, a1);
         emit_local(x, s, T_GELU_B, (double)(8 * t.T * t.FH), (double)(3 * t.FF),
                    dg, a1, NULL, (uint64_t)t.FF, du, 0, NULL);
-        gather_pw(x, x->W, s, 4 * li + 2, w);
+        use_weight(x, s, 4 * li + 2, w);
         emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.d * t.FH),
                    (double)(t.e * (t.T * t.FH + t.d * t.FH + t.T * t.d)),
                    du, w, NULL, (uint64_t)t.ACT, dy, 0, NULL);
@@ -1078,7 +1170,7 @@ static void tf_bwd(mat *x, int s, int k)
                    dy, a1, NULL, (uint64_t)t.ACT, dxa, 0, NULL);
         emit_local(x, s, T_RESADD_B, (double)(t.T * t.d), (double)(3 * t.ACT),
                    cur, dxa, NULL, (uint64_t)t.ACT, dx2, 0, NULL);
-        gather_pw(x, x->W, s, 4 * li + 1, w);
+        use_weight(x, s, 4 * li + 1, w);
         emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.dH * t.d),
                    (double)(t.e * (t.T * t.d + t.dH * t.d + t.T * t.dH)),
                    dx2, w, NULL, (uint64_t)t.OH, dO, 0, NULL);
@@ -1095,7 +1187,7 @@ static void tf_bwd(mat *x, int s, int k)
                    dP, a1, NULL, (uint64_t)t.S2, dS, 0, NULL);
         emit_local(x, s, T_SCORES_B, (double)(4 * t.T * t.s * t.dH), (double)(t.S2 + 4 * t.OH),
                    dS, a2, dq, 0, NULL, 0, NULL);
-        gather_pw(x, x->W, s, 4 * li + 0, w);
+        use_weight(x, s, 4 * li + 0, w);
         emit_local(x, s, T_GEMMDX, (double)(2 * t.T * 3 * t.dH * t.d),
                    (double)(t.e * (t.T * 3 * t.dH + 3 * t.dH * t.d + t.T * t.d)),
                    dq, w, NULL, (uint64_t)t.ACT, dy, 0, NULL);
@@ -1184,8 +1276,30 @@ static void emit_wu_slot(mat *x, int s, int p, uint64_t n)
 {
     double fl, by;
     int r;
-    emit_ar_dp(x, s, (double)((uint64_t)x->e * n), p);
     opt_cost(x, n, &fl, &by);
+    if (x->zero && x->D > 1) {
+        /* ZeRO (Fig. 9): reduce the gradient onto its owner (every
+         * replica's accumulated gradient dies there), then the owner's
+         * optimizer step consumes the reduced gradient */
+        int d, h, o = owner_of(x, s, p), nh = x->slice ? 1 : x->H;
+        for (h = 0; h < nh; h++) {
+            int ro = rep_of(x, o, h);
+            int32_t red = prog_tensor(x->g, dev_of(x, s, ro), (uint64_t)x->e * n, 0);
+            op_begin(x->g, OR_REDUCE, T_REDUCE, 0.0, (double)((uint64_t)x->e * n));
+            for (d = 0; d < x->D; d++) op_dev(x->g, dev_of(x, s, rep_of(x, d, h)));
+            for (d = 0; d < x->D; d++) op_in(x->g, *PW(x->G, x, s, rep_of(x, d, h), p));
+            op_out(x->g, red);
+            op_end(x->g, 0, mult_dp(x));
+            op_begin(x->g, OR_COMPUTE, T_OPT, fl, by);
+            op_dev(x->g, dev_of(x, s, ro));
+            op_in(x->g, *PW(x->W, x, s, ro, p));
+            op_in(x->g, red);
+            if (*PW(x->OS, x, s, ro, p) >= 0) op_in(x->g, *PW(x->OS, x, s, ro, p));
+            op_end(x->g, 0, mult_dp(x));
+        }
+        return;
+    }
+    emit_ar_dp(x, s, (double)((uint64_t)x->e * n), p);
     for (r = 0; r < x->R; r++) {
         op_begin(x->g, OR_COMPUTE, T_OPT, fl, by);
         op_dev(x->g, dev_of(x, s, r));
@@ -1273,7 +1387,8 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     x.M = M; x.g = &g; x.D = D; x.H = H; x.P = P; x.K = K; x.slice = slice;
     x.fam = M->family; x.mode = M->mode; x.train = M->mode != MODE_INFER;
     x.rc = x.train && M->recompute;
-    x.R = slice ? 1 : D * H;
+    x.zero = x.train && M->zero;
+    x.R = slice ? (x.zero ? D : 1) : D * H;
     x.e = M->elem_bytes;
     x.rows = M->global_batch / D;
     n_dev = D * H * P;
@@ -1332,6 +1447,7 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
                     if (p != tf_slot_emb(&x) && p != tf_slot_head(&x)) continue;
                 }
                 n = x.fam == FAM_MLP ? mlp_param(&x, s, p) : tf_param(&x, s, p);
+                if (x.zero && owner_of(&x, s, p) != data_rep(&x, r)) continue;   /* held by its owner only */
                 *PW(x.W, &x, s, r, p) = prog_tensor(&g, dv, (uint64_t)x.e * n, TF_RESIDENT | TF_KEEP);
                 if (x.train && opt_state_bytes(&x, n) > 0)
                     *PW(x.OS, &x, s, r, p) = prog_tensor(&g, dv, opt_state_bytes(&x, n), TF_RESIDENT | TF_KEEP);
@@ -1412,16 +1528,23 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     }
     rc = prog_simulate(&g, n_dev, dm, type_cost, fin, pk, dev_resident, NULL, NULL);
     if (rc) goto out;
+    /* devices a projection does not materialise stay at 0; per stage, the
+     * latest finish and the highest peak of its devices */
     res->makespan = 0.0;
     res->cand_peak = 0;
     for (s = 0; s < n_dev; s++) {
-        if (slice && (s % (D * H)) != 0) continue;
         if (fin[s] > res->makespan) res->makespan = fin[s];
         if (pk[s] > res->cand_peak) res->cand_peak = pk[s];
     }
     for (s = 0; s < P; s++) {
-        if (stage_finish) stage_finish[s] = fin[s * D * H];
-        if (stage_peak) stage_peak[s] = pk[s * D * H];
+        double f = 0.0;
+        uint64_t q = 0;
+        for (r = 0; r < D * H; r++) {
+            if (fin[s * D * H + r] > f) f = fin[s * D * H + r];
+            if (pk[s * D * H + r] > q) q = pk[s * D * H + r];
+        }
+        if (stage_finish) stage_finish[s] = f;
+        if (stage_peak) stage_peak[s] = q;
     }
     if (dev_finish) memcpy(dev_finish, fin, sizeof(double) * (size_t)n_dev);
     if (dev_peak) memcpy(dev_peak, pk, sizeof(uint64_t) * (size_t)n_dev);

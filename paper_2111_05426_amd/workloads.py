@@ -45,6 +45,7 @@ class ModelSpec:
     elem_bytes: int
     schedule: int = 0   # SCHED_1F1B or SCHED_GPIPE
     recompute: int = 0  # 1: activation recomputation (gradient checkpointing), training only
+    zero: int = 0       # 1: ZeRO parameter/gradient partitioning over the data-parallel replicas, training only
 
 
 @dataclass(frozen=True)
@@ -84,13 +85,13 @@ class Workload:
     tables: RandomTablesSpec = None
 
 
-def mlp(n_layers, d, batch, elem_bytes, mode, schedule=0, recompute=0):
-    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes, schedule, recompute)
+def mlp(n_layers, d, batch, elem_bytes, mode, schedule=0, recompute=0, zero=0):
+    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes, schedule, recompute, zero)
 
 
-def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None, schedule=0, recompute=0):
+def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None, schedule=0, recompute=0, zero=0):
     return ModelSpec(TRANSFORMER, mode, n_layers, heads, d, d_ff or 4 * d, seq, vocab, batch, elem_bytes, schedule,
-                     recompute)
+                     recompute, zero)
 
 
 TINY_MLP = Workload("tiny_mlp", mlp(4, 256, 64, 4, TRAIN_SGD), GridSpec(4, 0, 0, 4))

@@ -331,6 +331,115 @@ def test_recompute_lowers_pipeline_peak(orc):
         b = orc.sim_strategy(replace(m, recompute=1), 1, 1, 4, 8, DEV)
         assert b["cand_peak"] < a["cand_peak"] and b["makespan"] > a["makespan"]
 
+
+# ---------------------------------------------------------------------------
+# ZeRO partitioning (Fig. 9)
+# ---------------------------------------------------------------------------
+def test_zero_chain_with_two_devices_is_a_send(orc):
+    """Fig. 9 moves a weight between its two devices with a Send: the
+    broadcast and the reduce over two devices cost exactly that, and over
+    one device nothing."""
+    for nbytes in (0.0, 1.0, 3e6, 7.77e9):
+        send = orc.cost(DEV, orc.SEND, 0.0, nbytes, 2)
+        assert orc.cost(DEV, orc.BCAST, 0.0, nbytes, 2) == send
+        assert orc.cost(DEV, orc.REDUCE, 0.0, nbytes, 2) == send
+        assert orc.cost(DEV, orc.BCAST, 0.0, nbytes, 1) == 0.0
+
+
+@pytest.mark.parametrize("case", [(mlp(4, 64, 48, 4, TRAIN_ADAM), 1, 2, 2, 3), (mlp(6, 64, 40, 2, TRAIN_SGD), 1, 1, 3, 4),
+                                  (transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM_MIXED), 1, 2, 2, 2),
+                                  (mlp(4, 64, 48, 4, INFER), 2, 2, 2, 3)])
+def test_zero_without_partners_changes_nothing(orc, case):
+    """One data replica owns everything and has nobody to send to; inference
+    has no gradients to partition: every output is identical."""
+    m, D, H, P, K = case
+    a = orc.sim_strategy(m, D, H, P, K, DEV)
+    b = orc.sim_strategy(replace(m, zero=1), D, H, P, K, DEV)
+    for key in ("makespan", "cand_peak", "n_ops", "status"):
+        assert a[key] == b[key]
+    assert np.array_equal(a["dev_finish"], b["dev_finish"]) and np.array_equal(a["dev_peak"], b["dev_peak"])
+
+
+def test_zero_two_replicas_by_hand(orc):
+    """Fig. 9's setting through the transform: the 2-layer MLP on D = 2
+    replicas (P = H = K = 1, Adam), layer i owned by replica i.  Memory by
+    hand from the liveness rule, with W = e d^2 the weight (and each
+    gradient), 2W its Adam state, a = e m d an activation and W > 4a:
+      replica 0 peaks when its layer-0 gradient is reduced onto it: its own
+        W and state (3W), both accumulated gradients and the reduced one: 6W;
+      replica 1 peaks at the discarded input gradient of layer 0: its 3W,
+        both gradients, the broadcast copy of layer 0's weight, and the two
+        activations dh0 and dX: 6W + 2a;
+      plain data parallelism holds both weights and states (6W), both
+        gradients and the same two activations on each replica: 8W + 2a.
+    Time, with broadcast c_b, reduce c_r, optimizer o, Gemm t and every
+    other op free: four broadcasts and two Gemms, then reduce 0, replica 0's
+    step, reduce 1 (which waits for it), replica 1's step."""
+    d, m, e = 64, 8, 4
+    W, a = e * d * d, e * m * d
+    assert W > 4 * a
+    base = mlp(2, d, 2 * m, e, TRAIN_ADAM)
+    z = orc.sim_strategy(replace(base, zero=1), 2, 1, 1, 1, DEV)
+    p = orc.sim_strategy(base, 2, 1, 1, 1, DEV)
+    assert [int(v) for v in z["dev_peak"]] == [6 * W, 6 * W + 2 * a]
+    assert [int(v) for v in p["dev_peak"]] == [8 * W + 2 * a] * 2
+    cb, cr, o, t = 1.0, 8.0, 64.0, 512.0
+    cost = {k: 0.0 for k in orc.TYPES}
+    cost.update(BCAST=cb, REDUCE=cr, OPT=o, GEMM=t)
+    z = orc.sim_strategy(replace(base, zero=1), 2, 1, 1, 1, DEV, type_cost=cost)
+    T = 2 * t + 4 * cb + 2 * cr
+    assert list(z["dev_finish"]) == [T + o, T + 2 * o]
+
+
+def test_zero_owners_in_model_order(orc):
+    """Parameter groups in model order -- embedding, layers 0..L-1, LM head
+    -- go round-robin over the data replicas (Fig. 9: the first layer's
+    weight to the first device, the second's to the second).  A 3-layer
+    transformer on D = 2 replicas, one stage: replica 0 owns the embedding,
+    layer 1 and the head, replica 1 layers 0 and 2.  With Adam each
+    parameter holds 3e bytes; a layer has 12 d^2 parameters, the embedding
+    and the head V d each; stage 0's input rows are 4 s bytes, the targets
+    the same."""
+    d, V, S, e, B = 32, 101, 8, 2, 12
+    m = transformer(3, d, 4, S, V, B, e, TRAIN_ADAM, zero=1)
+    r = orc.sim_strategy(m, 2, 1, 1, 1, DEV)
+    rows = B // 2
+    io = 2 * rows * 4 * S
+    assert [int(v) for v in r["dev_resident"]] == [3 * e * (2 * V * d + 12 * d * d) + io,
+                                                   3 * e * (24 * d * d) + io]
+
+
+@pytest.mark.parametrize("case", [(mlp(4, 64, 48, 4, TRAIN_ADAM), 2, 2, 2, 3), (mlp(8, 32, 48, 2, TRAIN_ADAM_MIXED), 3, 1, 2, 2),
+                                  (mlp(8, 32, 48, 2, TRAIN_SGD), 4, 2, 2, 4),
+                                  (transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM), 2, 2, 2, 3),
+                                  (transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM), 3, 2, 4, 2),
+                                  (transformer(5, 32, 4, 8, 64, 12, 2, TRAIN_SGD), 3, 1, 2, 2)])
+def test_zero_op_counts_and_ownership(orc, case):
+    """Every op that reads a weight gets a broadcast per tensor rank: per
+    microbatch the MLP's L Gemms and L input gradients; the transformer's
+    4 layer weights twice per layer, the embedding, and the LM head twice.
+    Each parameter's all-reduce becomes a reduce and only its owner steps
+    the optimizer, so the program has H K (reads) - (D-1) H (params) more
+    ops.  The owners partition the weights: summed over the D replicas of
+    a stage and tensor rank, the resident bytes are one plain replica's
+    weights and state plus every replica's input rows."""
+    m, D, H, P, K = case
+    z = orc.sim_strategy(replace(m, zero=1), D, H, P, K, DEV)
+    p = orc.sim_strategy(m, D, H, P, K, DEV)
+    assert z["status"] == 0 and p["status"] == 0
+    L = m.n_layers
+    reads, params = (2 * L, L) if m.family == 0 else (8 * L + 3, 4 * L + 2)
+    assert z["n_ops"] - p["n_ops"] == H * K * reads - (D - 1) * H * params
+    rows = m.global_batch // D
+    row_bytes = m.elem_bytes * m.d_model if m.family == 0 else 4 * m.seq_len
+    zr = z["dev_resident"].reshape(P, D, H).astype(np.int64)
+    pr = p["dev_resident"].reshape(P, D, H).astype(np.int64)
+    for s in range(P):
+        inputs = rows * row_bytes * ((s == 0) + (s == P - 1))
+        for h in range(H):
+            assert zr[s, :, h].sum() == pr[s, 0, h] + (D - 1) * inputs
+    assert z["cand_peak"] <= p["cand_peak"]
+
 @pytest.mark.parametrize("case", [(mlp(4, 64, 48, 4, INFER), 1, 1, 2, 3), (mlp(6, 64, 40, 2, TRAIN_ADAM), 2, 2, 3, 1),
                                   (transformer(4, 32, 4, 8, 101, 12, 2, INFER), 2, 2, 2, 4),
                                   (transformer(3, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED), 1, 2, 3, 1)])
