@@ -144,6 +144,15 @@ double or_cost(const or_device_model *m, int kind, double flops, double bytes, i
 /* compute: runs on a, allocates and frees on a.                             */
 /* send a->b: runs on {a,b}, allocates on b, frees on a.                     */
 /* allreduce: runs on the devices of the mask; alloc/free fields ignored.    */
+/* broadcast (ZeRO's weight distribution, Fig. 9): root a sends to the other */
+/* devices of the mask (a must be in it); each of them allocates `alloc`     */
+/* bytes (its copy), then a frees `free` bytes.                              */
+/* reduce (ZeRO's gradient reduction onto the owner, Fig. 9): the devices of */
+/* the mask send to root a (a in the mask), which allocates `alloc` bytes    */
+/* (the reduced tensor); then every member frees `free` bytes (its own      */
+/* contribution dies there).  Both cost the pipelined chain over the mask.  */
+/* Every touched device samples its peak after the allocation and before    */
+/* the free.                                                                 */
 /* An invalid op is skipped and flagged in the status word.                  */
 /* ------------------------------------------------------------------------ */
 int or_sim_table(int64_t n_ops, int n_dev,
@@ -174,7 +183,7 @@ int or_sim_table(int64_t n_ops, int n_dev,
             uint32_t fb, bb;
             memcpy(&fb, &flops[o], 4);
             memcpy(&bb, &bytes[o], 4);
-            if ((c >> 24) != 0 || kind > 2 || fb >= 0x7f800000u || bb >= 0x7f800000u) {
+            if ((c >> 24) != 0 || kind > 4 || fb >= 0x7f800000u || bb >= 0x7f800000u) {
                 st |= ST_BAD_OP;
                 continue;
             }
@@ -188,12 +197,18 @@ int or_sim_table(int64_t n_ops, int n_dev,
             if (a == b) { st |= ST_SELF_SEND; continue; }
             mask = (1u << a) | (1u << b);
             cost = cost_send(m, (double)bytes[o]);
-        } else {
+        } else if (kind == OR_ALLREDUCE) {
             int n = 0;
             mask = (uint32_t)b;
             if (mask == 0 || (mask >> n_dev) != 0) { st |= ST_BAD_DEVICE; continue; }
             for (d = 0; d < n_dev; d++) if (mask & (1u << d)) n++;
             cost = cost_allreduce(m, (double)bytes[o], n);
+        } else {
+            int n = 0;
+            mask = (uint32_t)b;
+            if (a >= n_dev || (mask >> n_dev) != 0 || !(mask & (1u << a))) { st |= ST_BAD_DEVICE; continue; }
+            for (d = 0; d < n_dev; d++) if (mask & (1u << d)) n++;
+            cost = cost_chain(m, (double)bytes[o], n);
         }
         start = 0.0;
         for (d = 0; d < n_dev; d++)
@@ -201,12 +216,26 @@ int or_sim_table(int64_t n_ops, int n_dev,
         end = start + cost;
         for (d = 0; d < n_dev; d++)
             if (mask & (1u << d)) clk[d] = end;
-        if (kind != OR_ALLREDUCE) {
+        if (kind == OR_COMPUTE || kind == OR_SEND) {
             int tgt = (kind == OR_SEND) ? b : a;
             live[tgt] += (uint64_t)alloc[o];
             if (live[tgt] > pk[tgt]) pk[tgt] = live[tgt];
             if ((uint64_t)freeb[o] > live[a]) { st |= ST_MEM_UNDERFLOW; live[a] = 0; }
             else live[a] -= (uint64_t)freeb[o];
+        } else if (kind == OR_BCAST || kind == OR_REDUCE) {
+            /* allocate on the receivers (broadcast) or the root (reduce),
+             * sample every member, then free on the root (broadcast) or on
+             * every member (reduce) */
+            for (d = 0; d < n_dev; d++) {
+                if (!(mask & (1u << d))) continue;
+                if (kind == OR_BCAST ? d != a : d == a) live[d] += (uint64_t)alloc[o];
+                if (live[d] > pk[d]) pk[d] = live[d];
+            }
+            for (d = 0; d < n_dev; d++) {
+                if (!(mask & (1u << d)) || (kind == OR_BCAST && d != a)) continue;
+                if ((uint64_t)freeb[o] > live[d]) { st |= ST_MEM_UNDERFLOW; live[d] = 0; }
+                else live[d] -= (uint64_t)freeb[o];
+            }
         }
     }
     {

@@ -824,7 +824,7 @@ def table_brute(tab, n_dev, dev, init=None):
         c = int(c)
         k, a, b = c & 255, (c >> 8) & 255, (c >> 16) & 255
         fin = lambda x: math.isfinite(float(x)) and float(x) >= 0 and not math.copysign(1.0, float(x)) < 0
-        if c >> 24 or k > 2 or not fin(fl) or not fin(by):
+        if c >> 24 or k > 4 or not fin(fl) or not fin(by):
             st |= 1
             continue
         if k == 0:
@@ -843,7 +843,7 @@ def table_brute(tab, n_dev, dev, init=None):
                 continue
             devs = [a, b]
             cost = dev.link_latency_s + float(by) * inv(dev.link_bytes_per_s)
-        else:
+        elif k == 2:
             if b == 0 or b >> n_dev:
                 st |= 2
                 continue
@@ -851,10 +851,34 @@ def table_brute(tab, n_dev, dev, init=None):
             n = len(devs)
             cost = 0.0 if n == 1 else 2.0 * (n - 1) * dev.link_latency_s + \
                 (2.0 * (n - 1) / n) * (float(by) * inv(dev.link_bytes_per_s))
+        else:
+            # broadcast from / reduce onto a over the mask b: a chain of n - 1
+            # hops, the bytes crossing one link once
+            if a >= n_dev or b >> n_dev or not (b >> a & 1):
+                st |= 2
+                continue
+            devs = [d for d in range(n_dev) if b >> d & 1]
+            n = len(devs)
+            cost = 0.0 if n == 1 else float(n - 1) * dev.link_latency_s + float(by) * inv(dev.link_bytes_per_s)
         s = max(clk[d] for d in devs)
         for d in devs:
             clk[d] = s + cost
-        if k != 2:
+        if k >= 3:
+            # receivers (broadcast) or the root (reduce) allocate, every
+            # member samples, then the root (broadcast) or every member
+            # (reduce) frees
+            gets = [d for d in devs if (d != a) == (k == 3)]
+            for d in gets:
+                live[d] += int(al)
+            for d in devs:
+                peak[d] = max(peak[d], live[d])
+            for d in ([a] if k == 3 else devs):
+                if int(fr) > live[d]:
+                    st |= 8
+                    live[d] = 0
+                else:
+                    live[d] -= int(fr)
+        elif k != 2:
             t = b if k == 1 else a
             live[t] += int(al)
             peak[t] = max(peak[t], live[t])
@@ -866,16 +890,19 @@ def table_brute(tab, n_dev, dev, init=None):
     return clk, peak, st
 
 
-@pytest.mark.parametrize("seed", range(30))
+@pytest.mark.parametrize("seed", range(40))
 def test_table_brute_force(orc, seed):
     rng = np.random.default_rng(seed)
     n_dev = int(rng.integers(1, 9))
     n = int(rng.integers(1, 40))
-    kind = rng.integers(0, 3, n)
+    kind = rng.integers(0, 5 if seed >= 10 else 3, n)
     a = rng.integers(0, n_dev + (1 if seed % 3 == 0 else 0), n)
     b = rng.integers(0, n_dev, n)
     mask = rng.integers(0, 1 << n_dev, n)
-    code = np.where(kind == 2, 2 | (mask << 16), kind | (a << 8) | (b << 16)).astype(np.uint32)
+    # collectives with a root: mostly valid masks that hold the root
+    mask_r = np.where(rng.random(n) < 0.8, mask | (1 << np.minimum(a, n_dev - 1)), mask)
+    code = np.where(kind == 2, 2 | (mask << 16),
+                    np.where(kind >= 3, kind | (a << 8) | (mask_r << 16), kind | (a << 8) | (b << 16))).astype(np.uint32)
     if seed % 7 == 0:
         code[0] = 7
     tab = dict(code=code, flops=rng.uniform(1e6, 1e12, n).astype(np.float32),
@@ -909,6 +936,45 @@ def test_table_hand_trace(orc):
     # AR over 3: start 4.75, + 4*0.5 + (4/3)*(6/4) = 2 + 2 = 4 -> 8.75 everywhere
     assert list(r["finish"]) == [8.75, 8.75, 8.75]
     assert [int(v) for v in r["peak"]] == [5, 7, 9]
+
+
+def test_table_broadcast_reduce_hand_trace(orc):
+    """ZeRO's two collectives in table form (Fig. 9): device 0 broadcasts
+    a 6-byte weight to devices 1 and 2, device 1 computes with its copy and
+    frees it, then devices 0..2 reduce 4-byte gradients onto device 1.
+    Chain costs: (n - 1) latencies plus bytes over one link."""
+    dev = DeviceSpec(flops_per_s=1.0, mem_bytes_per_s=2.0, link_bytes_per_s=4.0,
+                     link_latency_s=0.5, launch_s=0.25)
+    code = np.array([0 | 2 << 8, 3 | 0 << 8 | 0b111 << 16, 0 | 1 << 8, 4 | 1 << 8 | 0b111 << 16], np.uint32)
+    tab = dict(code=code, flops=np.array([2, 0, 1, 0], np.float32), bytes=np.array([0, 6, 0, 8], np.float32),
+               alloc=np.array([0, 6, 3, 4], np.uint32), free=np.array([0, 0, 6, 4], np.uint32))
+    r = orc.sim_table(tab, 3, dev, init_live=np.array([10, 4, 4], np.uint64))
+    # d2: 0.25 + 2 = 2.25; broadcast starts at 2.25: 2 * 0.5 + 6/4 = 2.5 -> 4.75
+    # d1: 4.75 + 0.25 + 1 = 6.0; reduce starts at 6.0: 1 + 2 = 3 -> 9.0
+    assert list(r["finish"]) == [9.0, 9.0, 9.0]
+    # d0 only sends and frees its gradient: 10 -> 6; d1: 4 + 6 (copy) + 3 = 13,
+    # then the copy dies (7), + 4 reduced = 11, - 4 = 7; d2: 4 + 6 = 10
+    assert [int(v) for v in r["peak"]] == [10, 13, 10]
+    assert r["status"] == 0
+
+
+def test_table_broadcast_over_two_is_a_send(orc):
+    """Over two devices a broadcast is Fig. 9's Send: the same clocks and
+    peaks as the send record with the same bytes and sizes."""
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        a, b = (int(v) for v in rng.choice(4, 2, replace=False))
+        pre = np.array([0 | int(rng.integers(0, 4)) << 8], np.uint32)
+        fl, by = np.float32(rng.uniform(1e6, 1e9)), np.float32(rng.uniform(1e3, 1e8))
+        al, fr = np.uint32(rng.integers(0, 1000)), np.uint32(rng.integers(0, 50))
+        init = rng.integers(100, 2000, 4).astype(np.uint64)
+        t = lambda c: dict(code=np.array([pre[0], c], np.uint32), flops=np.array([fl, 0], np.float32),
+                           bytes=np.array([by, by], np.float32), alloc=np.array([al, al], np.uint32),
+                           free=np.array([0, fr], np.uint32))
+        s = orc.sim_table(t(1 | a << 8 | b << 16), 4, DEV, init_live=init)
+        z = orc.sim_table(t(3 | a << 8 | (1 << a | 1 << b) << 16), 4, DEV, init_live=init)
+        assert list(s["finish"]) == list(z["finish"])
+        assert list(s["peak"]) == list(z["peak"]) and s["status"] == z["status"] == 0
 
 
 # ---------------------------------------------------------------------------
