@@ -107,13 +107,29 @@ typedef struct {
  *        then replays from the checkpoint the forward ops of the stage's
  *        layers whose results the layers' backward reads (all but the last
  *        MLP layer; every transformer layer, the last one up to its GeLU),
- *        then the layers' backward. */
+ *        then the layers' backward.
+ *   zero: 0 or 1.  1 = ZeRO partitioning of weights, gradients and
+ *        optimizer state over the D data-parallel replicas (the appendix's
+ *        Fig. 9), training only, D > 1: the parameter groups in model order
+ *        (the transformer's embedding, each layer -- for the MLP with H > 1
+ *        each column/row layer pair -- and the LM head) belong to replica
+ *        (group index mod D), which alone holds their weights and optimizer
+ *        state from t = 0.  Right before every op that reads a weight, its
+ *        owner broadcasts it over the stage's D replicas of that tensor rank
+ *        (one collective per tensor rank); each other replica's copy dies
+ *        after that op.  Gradients accumulate on every replica; at the
+ *        weight update each one is reduced onto its owner (replacing the
+ *        all-reduce; every replica's gradient dies there) and only the owner
+ *        runs the optimizer op, which consumes the reduced gradient.
+ *        Broadcast and reduce over n devices cost (n-1) * lat +
+ *        bytes * (1/B_link) (a pipelined chain; a Send for n = 2). */
 typedef struct {
     int32_t family, mode, n_layers, n_heads;
     int64_t d_model, d_ff, seq_len, vocab, global_batch;
     int32_t elem_bytes;
     int32_t schedule;
     int32_t recompute;
+    int32_t zero;
 } dsim_model;
 
 /* A candidate: data-parallel D, tensor-parallel H (the paper's T), pipeline
@@ -149,14 +165,21 @@ DSIM_API dsim_status dsim_create_grid(const dsim_model *model, const dsim_grid_s
  * candidate-fastest: the record of op j of candidate c is at j*n_cand + c.
  *   code:  kind | a << 8 | b_or_mask << 16, bits 24..31 zero.
  *          kind 0 compute on device a; 1 send a -> b; 2 all-reduce over the
- *          devices set in the 8-bit mask.
+ *          devices set in the 8-bit mask; 3 broadcast from root a to the
+ *          other devices of the mask; 4 reduce over the mask onto root a
+ *          (3 and 4: a must be in the mask; ZeRO's collectives, Fig. 9).
+ *          Broadcast and reduce over n devices cost
+ *          (n-1) * lat + bytes * (1/B_link), 0 for n = 1.
  *   flops, bytes: fp32 values, promoted exactly to fp64 (flops ignored by
- *          send and all-reduce); both must be finite and >= 0 (-0.0, NaN,
- *          infinities and negative values make the op invalid), so that no
- *          cost is negative or NaN.
+ *          every kind but compute); both must be finite and >= 0 (-0.0,
+ *          NaN, infinities and negative values make the op invalid), so
+ *          that no cost is negative or NaN.
  *   alloc_bytes, free_bytes: compute allocates and frees on a; send
- *          allocates on b and frees on a; all-reduce ignores both.  The
- *          peak is sampled after the allocation and before the free.
+ *          allocates on b and frees on a; all-reduce ignores both;
+ *          broadcast allocates on every member but a and frees on a;
+ *          reduce allocates on a and frees on every member.  Every touched
+ *          device samples its peak after the allocation and before the
+ *          free.
  *   n_ops: per candidate op count (<= max_ops); NULL = max_ops for all.
  *   init_live: [n_cand * n_dev] bytes live at t = 0; NULL = zero.
  *   n_dev: 1..8.
@@ -176,10 +199,12 @@ typedef struct {
  * n_cand * row_width for the per-device rows; row-major per candidate).
  *   makespan:  max over devices of the final clock (seconds)
  *   finish:    per-device final clocks (tables: device d at column d;
- *              parametric: pipeline stage s at column s -- every replica of
- *              a stage finishes at the same time); unused columns are 0.
- *              May be NULL.
- *   peak:      per-device (per-stage) peak live bytes; may be NULL.
+ *              parametric: pipeline stage s at column s, the latest of its
+ *              devices -- every replica of a stage finishes at the same
+ *              time unless ZeRO leaves the last optimizer op to one owner);
+ *              unused columns are 0.  May be NULL.
+ *   peak:      per-device (per-stage: the highest of the stage's devices)
+ *              peak live bytes; may be NULL.
  *   cand_peak: max over devices of the peak.
  *   n_ops:     ops of the whole distributed program (each collective and
  *              each send counted once); may be NULL.
@@ -212,7 +237,10 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * lists: the per-stage 1F1B schedule, layers and ops are expanded on the fly.
  * Every replica (d, h) of a pipeline stage runs the same ops at the same
  * times, so one replica per stage is walked; collectives keep their full
- * group size in the cost.  results.row_width must be >= every candidate's P;
+ * group size in the cost.  With model.zero the replicas own different
+ * parameter groups: the stage's memory is the maximum over its replicas,
+ * taken in closed form per block, and its finish time is that of the owner
+ * of its last parameter.  results.row_width must be >= every candidate's P;
  * a candidate with P > min(row_width, 64, n_layers) or K > 16383 gets
  * DSIM_ST_BAD_STRATEGY.  The transform: device p*(D*H) + d*H + h runs stage
  * p of data replica d, tensor rank h; contiguous stages (the first L mod P

@@ -75,6 +75,7 @@ static dsim_status check_model(const dsim_model *m)
     if (m->schedule != DSIM_SCHED_1F1B && m->schedule != DSIM_SCHED_GPIPE)
         return fail(DSIM_EINVAL, "unknown schedule %d", m->schedule);
     if (m->recompute != 0 && m->recompute != 1) return fail(DSIM_EINVAL, "recompute must be 0 or 1");
+    if (m->zero != 0 && m->zero != 1) return fail(DSIM_EINVAL, "zero must be 0 or 1");
     if (m->family == DSIM_TRANSFORMER) {
         if (m->n_heads < 1 || m->d_ff < 1 || m->seq_len < 1 || m->vocab < 1)
             return fail(DSIM_EINVAL, "transformer needs n_heads, d_ff, seq_len, vocab >= 1");

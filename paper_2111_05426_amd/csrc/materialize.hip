@@ -10,6 +10,10 @@
 // ranks) followed by the slot's Sends in ascending source order (one per
 // replica), then every stage's weight update (each gradient all-reduce once
 // per tensor rank over the D replicas, each optimizer op once per device).
+// With ZeRO (Fig. 9) a weight read is preceded by a broadcast record from
+// its owner per tensor rank, the reading op also frees the copy on the other
+// replicas, and each gradient all-reduce becomes a reduce record onto the
+// owner followed by the owner's optimizer op.
 // The records go to the op-major, candidate-fastest table layout that
 // dsim_simulate_tables reads.
 #include "model.h"
@@ -44,6 +48,8 @@ struct Emit {
     int64_t j;          // records emitted so far (may pass max_ops: counted, not written)
     bool inexact;       // a value does not fit the record format exactly
     int base;           // first device of the stage
+    uint64_t pend;      // ZeRO: bytes of the broadcast copy the next op frees on non-owners
+    int pend_owner;     // ZeRO: the replica that owns it
 
     __device__ __forceinline__ void put(uint32_t code, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
     {
@@ -63,7 +69,42 @@ struct Emit {
     }
     __device__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
     {
-        for (int dev = base; dev < base + x.D * x.H; ++dev) put((uint32_t)dev << 8, fl, by, al, fr);
+        for (int r = 0; r < x.D * x.H; ++r) {
+            const uint64_t copy = (pend != 0 && r / x.H != pend_owner) ? pend : 0;
+            put((uint32_t)(base + r) << 8, fl, by, al, fr + copy);
+        }
+        pend = 0;
+    }
+    // ZeRO: the owner's broadcast over the D replicas of each tensor rank
+    // (kind 3, root = the owner: the others allocate their copy)
+    __device__ void bcast(uint64_t by, int grp)
+    {
+        if (!x.zero) return;
+        const int o = grp % x.D;
+        for (int h = 0; h < x.H; ++h)
+            put(3u | ((uint32_t)(base + o * x.H + h) << 8) | (dp_mask(h) << 16), 0, by, by, 0);
+        pend = by;
+        pend_owner = o;
+    }
+    // ZeRO: reduce onto the owner (kind 4: the owner allocates the reduced
+    // gradient, every member frees its own)
+    __device__ void reduce(uint64_t by, int grp)
+    {
+        const int o = grp % x.D;
+        for (int h = 0; h < x.H; ++h)
+            put(4u | ((uint32_t)(base + o * x.H + h) << 8) | (dp_mask(h) << 16), 0, by, by, by);
+    }
+    __device__ void owner_local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, int grp)
+    {
+        const int o = grp % x.D;
+        for (int h = 0; h < x.H; ++h) put((uint32_t)(base + o * x.H + h) << 8, fl, by, al, fr);
+    }
+    // the D replicas of tensor rank h on this stage
+    __device__ uint32_t dp_mask(int h) const
+    {
+        uint32_t mask = 0;
+        for (int d = 0; d < x.D; ++d) mask |= 1u << (base + d * x.H + h);
+        return mask;
     }
     __device__ void ar_tp(uint64_t by)
     {
@@ -76,11 +117,7 @@ struct Emit {
     __device__ void ar_dp(uint64_t by)
     {
         if (x.D <= 1) return;
-        for (int h = 0; h < x.H; ++h) {
-            uint32_t mask = 0;
-            for (int d = 0; d < x.D; ++d) mask |= 1u << (base + d * x.H + h);
-            put(2u | (mask << 16), 0, by, 0, 0);
-        }
+        for (int h = 0; h < x.H; ++h) put(2u | (dp_mask(h) << 16), 0, by, 0, 0);
     }
     __device__ void send(int t, uint64_t sz, uint64_t fre)
     {
@@ -110,10 +147,18 @@ __global__ __launch_bounds__(kLanes) void k_materialize(const MatArgs g)
     Ctx x = {};
     make_ctx(g.m, none, st, x);
     const int DH = x.D * x.H;
-    Emit e{x, g, c, 0, false, 0};
+    Emit e{x, g, c, 0, false, 0, 0, 0};
     for (int s = 0; s < x.P; ++s) {
-        const uint64_t r0 = resident(x, s);
-        for (int r = 0; r < DH; ++r) g.init_live[c * g.n_dev + s * DH + r] = r0;
+        if (x.zero) {
+            // each data replica holds the groups it owns
+            ZStage zs;
+            z_stage(x, s, zs);
+            const uint64_t in = resident_inputs(x, s);
+            for (int r = 0; r < DH; ++r) g.init_live[c * g.n_dev + s * DH + r] = in + z_owned(x, zs, r / x.H);
+        } else {
+            const uint64_t r0 = resident(x, s);
+            for (int r = 0; r < DH; ++r) g.init_live[c * g.n_dev + s * DH + r] = r0;
+        }
         s_pos[s][lane] = 0;
         s_nf[s][lane] = 0;
         s_nb[s][lane] = 0;

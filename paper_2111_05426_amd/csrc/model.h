@@ -14,6 +14,18 @@
 //                                        data replica (emitted only if H > 1)
 //   o.ar_dp(bytes)                       all-reduce over the D replicas of
 //                                        each tensor rank (only if D > 1)
+//   o.bcast(bytes, grp)                  ZeRO: the owner of parameter group
+//                                        grp broadcasts a weight of `bytes`
+//                                        over the D replicas of each tensor
+//                                        rank; the next o.local is the op that
+//                                        reads it, after which the other
+//                                        replicas' copies die
+//   o.reduce(bytes, grp)                 ZeRO: every replica's gradient of
+//                                        group grp is reduced onto the owner
+//                                        (which allocates the reduced tensor;
+//                                        the gradients die there)
+//   o.owner_local(fl, by, al, fr, grp)   ZeRO: compute op on the owner of
+//                                        group grp only (its optimizer step)
 //
 // Sinks: the parametric simulator (one replica per stage), the per-layer
 // cost recorder and the table materialiser.  Memory follows def/use
@@ -36,10 +48,12 @@ struct Ctx {
     int mode;
     int schedule;   // DSIM_SCHED_1F1B or DSIM_SCHED_GPIPE
     bool rc;        // activation recomputation (training only)
+    bool zero;      // ZeRO partitioning (training only, D > 1)
     uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
     uint64_t dH, FH, Vh, aH;
     double inv_f, inv_b, inv_l, lat, launch;
     double arl_h, arc_h, arl_d, arc_d;
+    double chl_d;   // (D - 1) * lat: latency part of a broadcast / reduce over the D replicas
     uint64_t mult_dev, mult_tp, mult_dp;
 };
 
@@ -75,6 +89,7 @@ __device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const 
     x.schedule = M.schedule;
     x.train = M.mode != DSIM_INFER;
     x.rc = x.train && M.recompute != 0;
+    x.zero = x.train && M.zero != 0 && x.D > 1;
     x.q = x.L / x.P;
     x.r = x.L % x.P;
     x.e = (uint64_t)M.elem_bytes;
@@ -100,6 +115,7 @@ __device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const 
     x.arc_h = ah / (double)x.H;
     x.arl_d = ad * x.lat;
     x.arc_d = ad / (double)x.D;
+    x.chl_d = (double)(x.D - 1) * x.lat;
     x.mult_dev = (uint64_t)x.D * (uint64_t)x.H;
     x.mult_tp = (uint64_t)x.D;
     x.mult_dp = (uint64_t)x.H;
@@ -124,6 +140,12 @@ __device__ __forceinline__ double cost_send(const Ctx &x, uint64_t bytes)
 {
     return x.lat + (double)bytes * x.inv_l;
 }
+// broadcast / reduce over the D replicas (ZeRO, Fig. 9): a pipelined chain,
+// D - 1 link latencies plus the bytes crossing one link once
+__device__ __forceinline__ double cost_chain_d(const Ctx &x, uint64_t bytes)
+{
+    return x.chl_d + (double)bytes * x.inv_l;
+}
 
 // Uneven microbatches: the first rows % K get one extra row.
 __device__ __forceinline__ uint64_t mb_rows(const Ctx &x, int k)
@@ -145,6 +167,10 @@ enum MlpKind { kPlain = 0, kCol = 1, kRow = 2 };
 
 __device__ __forceinline__ int mlp_kind(const Ctx &x, int i) { return x.H <= 1 ? kPlain : ((i & 1) ? kRow : kCol); }
 
+// ZeRO parameter group of MLP layer i: the layer, or with H > 1 its
+// column/row pair
+__device__ __forceinline__ int mlp_group(const Ctx &x, int i) { return x.H > 1 ? i / 2 : i; }
+
 __device__ __forceinline__ void mlp_dims(const Ctx &x, int kind, uint64_t &din, uint64_t &dout)
 {
     din = kind == kRow ? x.d / (uint64_t)x.H : x.d;
@@ -154,13 +180,15 @@ __device__ __forceinline__ void mlp_dims(const Ctx &x, int kind, uint64_t &din, 
 // One layer's forward.  free_in: the layer input dies at the Gemm (inference,
 // and layers after the first under recomputation; otherwise the weight
 // gradient reads it); dead_out: the model's last layer in inference, whose
-// output has no use.
+// output has no use; grp: the layer's parameter group.
 template <class S>
-__device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, int kind, bool free_in, bool dead_out)
+__device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, int kind, bool free_in, bool dead_out,
+                                              int grp)
 {
     const uint64_t e = x.e;
     uint64_t din, dout;
     mlp_dims(x, kind, din, dout);
+    o.bcast(e * din * dout, grp);
     o.local(2 * m * din * dout, e * (m * din + din * dout + m * dout), e * m * dout, free_in ? e * m * din : 0);
     if (kind == kRow) o.ar_tp(e * m * dout);
     // Relu frees the pre-activation
@@ -169,10 +197,10 @@ __device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, in
 
 // One layer's backward.  frees_input: the stage's first layer, where the
 // stage input dies at the weight gradient; layer0: the model's first layer,
-// whose dX has no use and is not all-reduced.
+// whose dX has no use and is not all-reduced; grp: the parameter group.
 template <class S>
 __device__ __forceinline__ void mlp_layer_bwd(const Ctx &x, S &o, uint64_t m, int kind, bool frees_input,
-                                              bool layer0, bool acc)
+                                              bool layer0, bool acc, int grp)
 {
     const uint64_t e = x.e;
     uint64_t din, dout;
@@ -181,6 +209,7 @@ __device__ __forceinline__ void mlp_layer_bwd(const Ctx &x, S &o, uint64_t m, in
     o.local(2 * m * din * dout, e * (m * din + m * dout + din * dout), e * din * dout,
             frees_input ? e * m * din : 0);                                             // weight gradient
     if (acc) o.local(din * dout, 3 * e * din * dout, 0, e * din * dout);                // accumulate
+    o.bcast(e * din * dout, grp);
     o.local(2 * m * din * dout, e * (m * dout + din * dout + m * din), e * m * din,
             e * m * dout + (layer0 ? e * m * din : 0));                                 // input gradient
     if (kind != kRow && x.H > 1 && !layer0) o.ar_tp(e * m * din);
@@ -235,11 +264,17 @@ __device__ __forceinline__ TfSz tf_sizes(const Ctx &x, uint64_t m)
     return z;
 }
 
+// ZeRO parameter groups of the transformer in model order: the embedding,
+// layer i, the LM head
+__device__ __forceinline__ int tf_group_layer(int i) { return i + 1; }
+__device__ __forceinline__ int tf_group_head(const Ctx &x) { return x.L + 1; }
+
 // stage 0, before its layers: embedding
 template <class S>
 __device__ __forceinline__ void tf_fwd_first(const Ctx &x, S &o, const TfSz &z)
 {
     const uint64_t T = z.T, d = x.d;
+    o.bcast(x.e * x.Vh * d, 0);
     o.local(T * d, 2 * z.ACT + z.IDS, z.ACT, x.train ? 0 : z.IDS);   // ids die in inference
     o.ar_tp(z.ACT);
 }
@@ -248,23 +283,28 @@ __device__ __forceinline__ void tf_fwd_first(const Ctx &x, S &o, const TfSz &z)
 // stay live (training without recomputation, and the replay); keep_in: the
 // layer input stays live (save, or the checkpoint of a recomputed stage);
 // full = false stops after GeLU (the replay of a stage's last layer, whose
-// output nothing reads).
+// output nothing reads); grp: the layer's parameter group.
 template <class S>
-__device__ __forceinline__ void tf_layer_fwd(const Ctx &x, S &o, const TfSz &z, bool save, bool keep_in, bool full)
+__device__ __forceinline__ void tf_layer_fwd(const Ctx &x, S &o, const TfSz &z, bool save, bool keep_in, bool full,
+                                             int grp)
 {
     const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
     o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                                  // LN1
+    o.bcast(e * d * 3 * dH, grp);
     o.local(2 * T * d * 3 * dH, e * (T * d + d * 3 * dH + T * 3 * dH), z.QKV, save ? 0 : z.ACT);  // QKV
     o.local(2 * T * S_ * dH, 2 * z.OH + z.S2, z.S2, 0);                                       // scores
     o.local(5 * z.m * x.aH * S_ * S_, 2 * z.S2, z.S2, z.S2);                                  // softmax
     o.local(2 * T * S_ * dH, z.S2 + 2 * z.OH, z.OH, save ? 0 : z.S2 + z.QKV);                // P.V
+    o.bcast(e * dH * d, grp);
     o.local(2 * T * dH * d, e * (T * dH + dH * d + T * d), z.ACT, save ? 0 : z.OH);           // out-proj
     o.ar_tp(z.ACT);
     o.local(T * d, 3 * z.ACT, z.ACT, keep_in ? z.ACT : 2 * z.ACT);                           // residual
     o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                                  // LN2
+    o.bcast(e * d * FH, grp);
     o.local(2 * T * d * FH, e * (T * d + d * FH + T * FH), z.FF, save ? 0 : z.ACT);           // fc1
     o.local(8 * T * FH, 2 * z.FF, z.FF, save ? 0 : z.FF);                                    // GeLU
     if (!full) return;
+    o.bcast(e * FH * d, grp);
     o.local(2 * T * FH * d, e * (T * FH + FH * d + T * d), z.ACT, save ? 0 : z.FF);           // fc2
     o.ar_tp(z.ACT);
     o.local(T * d, 3 * z.ACT, z.ACT, save ? z.ACT : 2 * z.ACT);                              // residual
@@ -277,6 +317,7 @@ __device__ __forceinline__ void tf_fwd_last(const Ctx &x, S &o, const TfSz &z)
     const uint64_t T = z.T, d = x.d, e = x.e;
     const bool tr = x.train;
     o.local(8 * T * d, 2 * z.ACT, z.ACT, tr ? 0 : z.ACT);                                  // final LN
+    o.bcast(e * d * x.Vh, tf_group_head(x));
     o.local(2 * T * d * x.Vh, e * (T * d + d * x.Vh + T * x.Vh), z.LOG, tr ? 0 : z.ACT + z.LOG);  // LM head
 }
 
@@ -288,6 +329,7 @@ __device__ __forceinline__ void tf_bwd_last(const Ctx &x, S &o, const TfSz &z, b
     o.local(3 * T * Vh, z.LOG + z.ST, z.ST, 0);                                   // loss statistics
     o.ar_tp(z.ST);
     o.local(2 * T * Vh, 2 * z.LOG + z.ST + z.IDS, z.LOG, z.LOG + z.ST + z.IDS);   // dlogits
+    o.bcast(e * d * Vh, tf_group_head(x));
     o.local(2 * T * d * Vh, e * (T * Vh + d * Vh + T * d), z.ACT, 0);             // LM head dX
     o.ar_tp(z.ACT);
     o.local(2 * T * d * Vh, e * (T * d + T * Vh + d * Vh), e * d * Vh, z.ACT + z.LOG);  // LM head dW
@@ -296,25 +338,29 @@ __device__ __forceinline__ void tf_bwd_last(const Ctx &x, S &o, const TfSz &z, b
 }
 
 template <class S>
-__device__ __forceinline__ void tf_layer_bwd(const Ctx &x, S &o, const TfSz &z, bool acc)
+__device__ __forceinline__ void tf_layer_bwd(const Ctx &x, S &o, const TfSz &z, bool acc, int grp)
 {
     const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
+    o.bcast(e * FH * d, grp);
     o.local(2 * T * FH * d, e * (T * d + FH * d + T * FH), z.FF, 0);             // fc2 dX
     o.local(2 * T * FH * d, e * (T * FH + T * d + FH * d), e * FH * d, z.FF);     // fc2 dW
     if (acc) o.local(FH * d, 3 * e * FH * d, 0, e * FH * d);
     o.local(8 * T * FH, 3 * z.FF, z.FF, 2 * z.FF);                                // GeLU grad
+    o.bcast(e * d * FH, grp);
     o.local(2 * T * d * FH, e * (T * FH + d * FH + T * d), z.ACT, 0);             // fc1 dX
     o.ar_tp(z.ACT);
     o.local(2 * T * d * FH, e * (T * d + T * FH + d * FH), e * d * FH, z.ACT + z.FF);  // fc1 dW
     if (acc) o.local(d * FH, 3 * e * d * FH, 0, e * d * FH);
     o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                              // LN2 grad
     o.local(T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                  // residual merge
+    o.bcast(e * dH * d, grp);
     o.local(2 * T * dH * d, e * (T * d + dH * d + T * dH), z.OH, 0);              // out-proj dX
     o.local(2 * T * dH * d, e * (T * dH + T * d + dH * d), e * dH * d, z.OH);     // out-proj dW
     if (acc) o.local(dH * d, 3 * e * dH * d, 0, e * dH * d);
     o.local(4 * T * S_ * dH, 2 * z.S2 + 3 * z.OH, z.S2 + z.QKV, z.OH);            // P.V grads
     o.local(5 * z.m * x.aH * S_ * S_, 3 * z.S2, z.S2, 2 * z.S2);                  // softmax grad
     o.local(4 * T * S_ * dH, z.S2 + 4 * z.OH, 0, z.S2 + z.QKV);                   // Q.K^T grads
+    o.bcast(e * d * 3 * dH, grp);
     o.local(2 * T * 3 * dH * d, e * (T * 3 * dH + 3 * dH * d + T * d), z.ACT, 0);  // QKV dX
     o.ar_tp(z.ACT);
     o.local(2 * T * d * 3 * dH, e * (T * d + T * 3 * dH + d * 3 * dH), e * d * 3 * dH, z.ACT + z.QKV);  // QKV dW
@@ -342,14 +388,15 @@ __device__ __forceinline__ void block_fwd(const Ctx &x, S &o, int s, int k)
     if (x.mlp) {
         const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
         for (int i = l0; i < l1; ++i)
-            mlp_layer_fwd(x, o, m, mlp_kind(x, i), !x.train || (x.rc && i > l0), !x.train && i == x.L - 1);
+            mlp_layer_fwd(x, o, m, mlp_kind(x, i), !x.train || (x.rc && i > l0), !x.train && i == x.L - 1,
+                          mlp_group(x, i));
         return;
     }
     const TfSz z = tf_sizes(x, m);
     if (s == 0) tf_fwd_first(x, o, z);
-    const int nl = stage_nl(x, s);
+    const int nl = stage_nl(x, s), l0 = stage_l0(x, s);
     const bool save = x.train && !x.rc;
-    for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z, save, save || (x.rc && i == 0), true);
+    for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z, save, save || (x.rc && i == 0), true, tf_group_layer(l0 + i));
     if (s == x.P - 1) tf_fwd_last(x, o, z);
 }
 
@@ -362,16 +409,17 @@ __device__ __forceinline__ void block_bwd(const Ctx &x, S &o, int s, int k)
         const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
         if (s == x.P - 1) mlp_loss(x, o, m);
         if (x.rc)   // replay every layer but the last from the checkpoint
-            for (int i = l0; i < l1 - 1; ++i) mlp_layer_fwd(x, o, m, mlp_kind(x, i), false, false);
-        for (int i = l1 - 1; i >= l0; --i) mlp_layer_bwd(x, o, m, mlp_kind(x, i), i == l0, i == 0, acc);
+            for (int i = l0; i < l1 - 1; ++i) mlp_layer_fwd(x, o, m, mlp_kind(x, i), false, false, mlp_group(x, i));
+        for (int i = l1 - 1; i >= l0; --i)
+            mlp_layer_bwd(x, o, m, mlp_kind(x, i), i == l0, i == 0, acc, mlp_group(x, i));
         return;
     }
     const TfSz z = tf_sizes(x, m);
     if (s == x.P - 1) tf_bwd_last(x, o, z, acc);
-    const int nl = stage_nl(x, s);
+    const int nl = stage_nl(x, s), l0 = stage_l0(x, s);
     if (x.rc)   // replay the layers from the checkpoint, the last one up to its GeLU
-        for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z, true, true, i < nl - 1);
-    for (int i = 0; i < nl; ++i) tf_layer_bwd(x, o, z, acc);
+        for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z, true, true, i < nl - 1, tf_group_layer(l0 + i));
+    for (int i = nl - 1; i >= 0; --i) tf_layer_bwd(x, o, z, acc, tf_group_layer(l0 + i));
     if (s == 0) tf_bwd_first(x, o, z, acc);
 }
 
@@ -400,14 +448,21 @@ __device__ __forceinline__ uint64_t opt_state(const Ctx &x, uint64_t N)
     return 0;
 }
 
-// one parameter tensor: all-reduce its gradient over the D replicas, then
-// the optimizer op (in place), after which the gradient dies
+// one parameter tensor of group grp: all-reduce its gradient over the D
+// replicas, then the optimizer op (in place), after which the gradient dies.
+// ZeRO: reduce the gradients onto the owner (they die there), whose
+// optimizer op consumes the reduced gradient.
 template <class S>
-__device__ __forceinline__ void wu_param(const Ctx &x, S &o, uint64_t N)
+__device__ __forceinline__ void wu_param(const Ctx &x, S &o, uint64_t N, int grp)
 {
-    o.ar_dp(x.e * N);
     uint64_t fl, by;
     opt_cost(x, N, fl, by);
+    if (x.zero) {
+        o.reduce(x.e * N, grp);
+        o.owner_local(fl, by, 0, x.e * N, grp);
+        return;
+    }
+    o.ar_dp(x.e * N);
     o.local(fl, by, 0, x.e * N);
 }
 
@@ -420,26 +475,37 @@ __device__ __forceinline__ void weight_update(const Ctx &x, S &o, int s)
         for (int i = l0; i < l0 + nl; ++i) {
             uint64_t din, dout;
             mlp_dims(x, mlp_kind(x, i), din, dout);
-            wu_param(x, o, din * dout);
+            wu_param(x, o, din * dout, mlp_group(x, i));
         }
         return;
     }
     const uint64_t d = x.d;
-    if (s == 0) wu_param(x, o, x.Vh * d);
+    if (s == 0) wu_param(x, o, x.Vh * d, 0);
     for (int i = 0; i < nl; ++i) {
-        wu_param(x, o, d * 3 * x.dH);
-        wu_param(x, o, x.dH * d);
-        wu_param(x, o, d * x.FH);
-        wu_param(x, o, x.FH * d);
+        const int g = tf_group_layer(l0 + i);
+        wu_param(x, o, d * 3 * x.dH, g);
+        wu_param(x, o, x.dH * d, g);
+        wu_param(x, o, d * x.FH, g);
+        wu_param(x, o, x.FH * d, g);
     }
-    if (s == x.P - 1) wu_param(x, o, d * x.Vh);
+    if (s == x.P - 1) wu_param(x, o, d * x.Vh, tf_group_head(x));
 }
 
 // bytes of one row (sequence) of the stage-0 input / last-stage target
 __device__ __forceinline__ uint64_t input_row(const Ctx &x) { return x.mlp ? x.e * x.d : 4 * x.seq; }
 
-// bytes resident on a device of stage s at t = 0: weight shard, optimizer
-// state, the replica's input rows (stage 0) and targets (last stage, training)
+// bytes of the replica's input rows (stage 0) and targets (last stage,
+// training), resident from t = 0
+__device__ __forceinline__ uint64_t resident_inputs(const Ctx &x, int s)
+{
+    uint64_t b = 0;
+    if (s == 0) b += input_row(x) * x.rows;
+    if (s == x.P - 1 && x.train) b += input_row(x) * x.rows;
+    return b;
+}
+
+// bytes resident on a device of stage s at t = 0 without ZeRO: weight
+// shard, optimizer state, the replica's inputs
 __device__ __forceinline__ uint64_t resident(const Ctx &x, int s)
 {
     const int l0 = stage_l0(x, s), nl = stage_nl(x, s);
@@ -455,10 +521,81 @@ __device__ __forceinline__ uint64_t resident(const Ctx &x, int s)
         if (s == 0) N += x.Vh * x.d;
         if (s == x.P - 1) N += x.d * x.Vh;
     }
-    uint64_t b = x.e * N + opt_state(x, N);
-    if (s == 0) b += input_row(x) * x.rows;
-    if (s == x.P - 1 && x.train) b += input_row(x) * x.rows;
+    return x.e * N + opt_state(x, N) + resident_inputs(x, s);
+}
+
+// ---------------------------------------------------------------------------
+// ZeRO ownership (Fig. 9): the parameter groups of stage s are a contiguous
+// range of the model order (transformer: the embedding on stage 0, layer
+// groups l0+1 .. l1, the head L+1 on the last stage; MLP: its layers or
+// column/row pairs), and group g belongs to data replica g mod D.
+// ---------------------------------------------------------------------------
+struct ZStage {
+    int gl_lo, gl_hi;     // layer groups of the stage [gl_lo, gl_hi)
+    bool emb, head;       // holds the embedding (group 0) / the LM head (group L+1)
+    int g_head;
+    uint64_t GL, GE;      // resident bytes (weights + optimizer state) of a layer group / the embedding or head
+    uint64_t rmax, rsec;  // largest owned bytes over the D replicas; over the replicas other than `arg`
+    int arg;
+};
+
+// groups g in [lo, hi) with g mod D == d (0 <= d < D)
+__device__ __forceinline__ int64_t count_mod(int lo, int hi, int d, int D)
+{
+    auto upto = [&](int n) -> int64_t { return n > d ? (int64_t)(n - d - 1) / D + 1 : 0; };
+    return hi > lo ? upto(hi) - upto(lo) : 0;
+}
+
+// bytes of weights and optimizer state that replica d owns on stage s
+__device__ __forceinline__ uint64_t z_owned(const Ctx &x, const ZStage &z, int d)
+{
+    uint64_t b = (uint64_t)count_mod(z.gl_lo, z.gl_hi, d, x.D) * z.GL;
+    if (z.emb && d == 0) b += z.GE;
+    if (z.head && z.g_head % x.D == d) b += z.GE;
     return b;
+}
+
+__device__ inline void z_stage(const Ctx &x, int s, ZStage &z)
+{
+    const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
+    uint64_t NL, NE = 0;
+    if (x.mlp) {
+        z.gl_lo = mlp_group(x, l0);
+        z.gl_hi = mlp_group(x, l1 - 1) + 1;
+        NL = x.H > 1 ? 2 * x.d * (x.d / (uint64_t)x.H) : x.d * x.d;
+        z.emb = z.head = false;
+    } else {
+        z.gl_lo = tf_group_layer(l0);
+        z.gl_hi = tf_group_layer(l1 - 1) + 1;
+        NL = x.d * 3 * x.dH + x.dH * x.d + x.d * x.FH + x.FH * x.d;
+        NE = x.Vh * x.d;
+        z.emb = s == 0;
+        z.head = s == x.P - 1;
+    }
+    z.g_head = x.L + 1;
+    z.GL = x.e * NL + opt_state(x, NL);
+    z.GE = x.e * NE + opt_state(x, NE);
+    // the replicas that own something here are the owners of the stage's
+    // first min(D, #groups) groups; the others own nothing
+    const int g_lo = z.emb ? 0 : z.gl_lo, g_hi = z.head ? z.g_head + 1 : z.gl_hi;
+    const int n_own = (g_hi - g_lo) < x.D ? (g_hi - g_lo) : x.D;
+    uint64_t m1 = 0, m2 = 0;
+    int a1 = -1;
+    for (int j = 0; j < n_own; ++j) {
+        const int d = (g_lo + j) % x.D;
+        const uint64_t b = z_owned(x, z, d);
+        if (a1 < 0 || b > m1) {
+            m2 = a1 < 0 ? 0 : m1;
+            m1 = b;
+            a1 = d;
+        } else if (b > m2) {
+            m2 = b;
+        }
+    }
+    // a replica owning nothing has 0 bytes, already the floor of m2
+    z.rmax = m1;
+    z.rsec = m2;
+    z.arg = a1;
 }
 
 // K > 1: split the replica's whole input (stage 0) or target (last stage)

@@ -18,6 +18,14 @@
 //     one replica per stage is walked: a collective over the H ranks or the
 //     D replicas starts at the stage's own clock and costs the ring
 //     all-reduce of its full group; a Send synchronises two stage clocks.
+//   * with ZeRO (Fig. 9) the replicas still run the same ops at the same
+//     times, except that only a parameter's owner runs its optimizer op; the
+//     next gradient reduce waits for it, so the stage's latest device finishes
+//     at the lane's clock.  Their memory differs: each holds only the groups
+//     it owns and a copy of every other weight while an op reads it.  The
+//     lane tracks the live bytes that do not depend on ownership plus the
+//     largest owned resident, and each block kind's highest point is taken
+//     as the maximum over the replicas in closed form (see zero_block).
 //
 // The layers of a stage repeat one op sequence (for the MLP with H > 1, one
 // column/row layer pair), so each lane records that sequence's op costs once
@@ -49,8 +57,8 @@ constexpr int kScanBlock = 256;
 // ops before the repeating units, one unit, ops after the units.  The
 // regions are sized for the larger (backward) block; forward blocks use the
 // F_* prefix of each region.
-template <bool TF> struct Shape;
-template <> struct Shape<true> {
+template <bool TF, bool Z> struct Shape;
+template <> struct Shape<true, false> {
     static constexpr int PRE2 = 4;    // last stage backward: loss .. final LN grad (8 ops)
     static constexpr int U2 = 12;     // one layer backward: 17 compute + 4 accumulations + 2 all-reduces
     static constexpr int SUF2 = 1;    // stage 0 backward: embedding grad + accumulation
@@ -58,7 +66,7 @@ template <> struct Shape<true> {
     static constexpr int F_U2 = 7;    // one layer forward: 12 compute + 2 all-reduces
     static constexpr int F_SUF2 = 1;  // last stage forward: final LN + LM head
 };
-template <> struct Shape<false> {
+template <> struct Shape<false, false> {
     static constexpr int PRE2 = 1;    // last stage backward: loss gradient
     static constexpr int U2 = 5;      // row layer (4 ops) + column layer (5) backward
     static constexpr int SUF2 = 5;    // the stage's first unit backward (frees the stage input)
@@ -66,6 +74,31 @@ template <> struct Shape<false> {
     static constexpr int F_U2 = 3;    // column layer (2 ops) + row layer (3) forward
     static constexpr int F_SUF2 = 3;  // the model's last unit in inference (dead output)
 };
+// ZeRO adds one broadcast before every op that reads a weight
+template <> struct Shape<true, true> {
+    static constexpr int PRE2 = 5;    // 8 ops + 1 broadcast
+    static constexpr int U2 = 14;     // 22 ops + 4 broadcasts
+    static constexpr int SUF2 = 2;    // the forward suffix is the larger one here
+    static constexpr int F_PRE2 = 2;  // 2 ops + 1 broadcast
+    static constexpr int F_U2 = 9;    // 14 ops + 4 broadcasts
+    static constexpr int F_SUF2 = 2;  // 2 ops + 1 broadcast
+};
+template <> struct Shape<false, true> {
+    static constexpr int PRE2 = 1;
+    static constexpr int U2 = 6;      // 9 ops + 2 broadcasts
+    static constexpr int SUF2 = 6;    // 9 ops + 2 broadcasts
+    static constexpr int F_PRE2 = 0;
+    static constexpr int F_U2 = 4;    // 5 ops + 2 broadcasts
+    static constexpr int F_SUF2 = 3;  // inference only: no ZeRO
+};
+// a forward block's regions are prefixes of the backward block's
+template <class Sh> constexpr bool shape_nested()
+{
+    return Sh::F_PRE2 <= Sh::PRE2 && Sh::F_U2 <= Sh::U2 && Sh::F_SUF2 <= Sh::SUF2;
+}
+static_assert(shape_nested<Shape<true, false>>() && shape_nested<Shape<false, false>>() &&
+                  shape_nested<Shape<true, true>>() && shape_nested<Shape<false, true>>(),
+              "forward regions must fit the backward ones");
 
 struct ParArgs {
     dsim_model m;
@@ -98,12 +131,17 @@ __device__ __forceinline__ int seg_class(const dsim_strategy &st, int p_bound)
 // ---------------------------------------------------------------------------
 // Sinks
 // ---------------------------------------------------------------------------
-// The lane's stage replica, op by op (splits and the weight update).
+// The lane's stage replica, op by op (splits and the weight update).  With
+// ZeRO, live counts the largest owned resident and z describes the stage's
+// ownership: a reduce samples the owner holding the reduced gradient and the
+// other replicas, then every gradient dies; the owner's optimizer op frees
+// the reduced gradient again (below that sample).
 struct Walk {
     const Ctx &x;
     double clk;
     int64_t live, peak;
     uint64_t walked, nops;
+    const ZStage *z;
 
     __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
     {
@@ -125,6 +163,31 @@ struct Walk {
     {
         if (x.D <= 1) return;
         clk = clk + cost_ar_dp(x, by);
+        walked += 1;
+        nops += x.mult_dp;
+    }
+    __device__ __forceinline__ void bcast(uint64_t by, int)
+    {
+        if (!x.zero) return;
+        clk = clk + cost_chain_d(x, by);
+        walked += 1;
+        nops += x.mult_dp;
+    }
+    __device__ __forceinline__ void reduce(uint64_t by, int grp)
+    {
+        clk = clk + cost_chain_d(x, by);
+        walked += 1;
+        nops += x.mult_dp;
+        const int o = grp % x.D;
+        const int64_t own = (int64_t)z_owned(x, *z, o) + (int64_t)by;
+        const int64_t other = (int64_t)(o == z->arg ? z->rsec : z->rmax);
+        const int64_t hi = live - (int64_t)z->rmax + (own > other ? own : other);
+        peak = hi > peak ? hi : peak;
+        live -= (int64_t)by;
+    }
+    __device__ __forceinline__ void owner_local(uint64_t fl, uint64_t by, uint64_t, uint64_t, int)
+    {
+        clk = clk + cost_local(x, fl, by);
         walked += 1;
         nops += x.mult_dp;
     }
@@ -165,6 +228,17 @@ struct Record {
         if (x.D <= 1) return;
         put(cost_ar_dp(x, by));
     }
+    // a broadcast's cost; with ZeRO the memory summary comes from MemZ
+    __device__ __forceinline__ void bcast(uint64_t by, int)
+    {
+        if (!x.zero) return;
+        put(cost_chain_d(x, by));
+    }
+    __device__ __forceinline__ void reduce(uint64_t by, int) { put(cost_chain_d(x, by)); }
+    __device__ __forceinline__ void owner_local(uint64_t fl, uint64_t by, uint64_t, uint64_t, int)
+    {
+        put(cost_local(x, fl, by));
+    }
 };
 
 // Memory summary only (net bytes, peak above the start), no costs.
@@ -179,6 +253,38 @@ struct Mem {
     }
     __device__ __forceinline__ void ar_tp(uint64_t) {}
     __device__ __forceinline__ void ar_dp(uint64_t) {}
+    __device__ __forceinline__ void bcast(uint64_t, int) {}
+    __device__ __forceinline__ void reduce(uint64_t, int) {}
+    __device__ __forceinline__ void owner_local(uint64_t, uint64_t, uint64_t, uint64_t, int) {}
+};
+
+// ZeRO memory summary of ops that read the weights of one parameter group:
+// net bytes and the highest point above the start, seen by a replica that
+// does not own the group (tn: it holds each broadcast copy from the
+// broadcast until the op that reads it) and by the owner (to: no copies).
+// Copies die inside the summarised ops, so the net is the same for both.
+struct MemZ {
+    const Ctx &x;
+    int64_t cur, tn, to, pend;
+    __device__ __forceinline__ void local(uint64_t, uint64_t, uint64_t al, uint64_t fr)
+    {
+        const int64_t a = cur + (int64_t)al;
+        tn = a + pend > tn ? a + pend : tn;
+        to = a > to ? a : to;
+        cur = a - (int64_t)fr;
+        pend = 0;
+    }
+    __device__ __forceinline__ void ar_tp(uint64_t) {}
+    __device__ __forceinline__ void ar_dp(uint64_t) {}
+    __device__ __forceinline__ void bcast(uint64_t by, int)
+    {
+        if (!x.zero) return;
+        tn = cur + (int64_t)by > tn ? cur + (int64_t)by : tn;
+        to = cur > to ? cur : to;
+        pend = (int64_t)by;
+    }
+    __device__ __forceinline__ void reduce(uint64_t, int) {}
+    __device__ __forceinline__ void owner_local(uint64_t, uint64_t, uint64_t, uint64_t, int) {}
 };
 
 // Liveness of a forward unit.  kFwdBlock: as in a forward block (training
@@ -197,27 +303,27 @@ __device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, bool acc, S &r, 
     if (TF) {
         const TfSz z = tf_sizes(x, m);
         if (bwd) {
-            tf_layer_bwd(x, r, z, acc);
+            tf_layer_bwd(x, r, z, acc, 0);
         } else {
             const bool save = live == kFwdReplay || (live == kFwdBlock && x.train && !x.rc);
-            tf_layer_fwd(x, r, z, save, save || live == kFwdFirst, true);
+            tf_layer_fwd(x, r, z, save, save || live == kFwdFirst, true, 0);
         }
     } else if (bwd) {
         if (x.H > 1) {
-            mlp_layer_bwd(x, r, m, kRow, false, false, acc);
-            mlp_layer_bwd(x, r, m, kCol, false, false, acc);
+            mlp_layer_bwd(x, r, m, kRow, false, false, acc, 0);
+            mlp_layer_bwd(x, r, m, kCol, false, false, acc, 0);
         } else {
-            mlp_layer_bwd(x, r, m, kPlain, false, false, acc);
+            mlp_layer_bwd(x, r, m, kPlain, false, false, acc, 0);
         }
     } else {
         // free_in of the unit's first layer and of its second (pair) layer
         const bool fi_rest = live != kFwdReplay && (!x.train || x.rc);
         const bool fi_first = live == kFwdBlock && fi_rest;
         if (x.H > 1) {
-            mlp_layer_fwd(x, r, m, kCol, fi_first, false);
-            mlp_layer_fwd(x, r, m, kRow, fi_rest, false);
+            mlp_layer_fwd(x, r, m, kCol, fi_first, false, 0);
+            mlp_layer_fwd(x, r, m, kRow, fi_rest, false, 0);
         } else {
-            mlp_layer_fwd(x, r, m, kPlain, fi_first, false);
+            mlp_layer_fwd(x, r, m, kPlain, fi_first, false, 0);
         }
     }
 }
@@ -228,15 +334,15 @@ __device__ void record_unit(const Ctx &x, bool bwd, uint64_t m, bool acc, S &r, 
 template <bool TF, class S>
 __device__ void record_partial(const Ctx &x, uint64_t m, S &r)
 {
-    if (TF) tf_layer_fwd(x, r, tf_sizes(x, m), true, true, false);
-    else if (x.H > 1) mlp_layer_fwd(x, r, m, kCol, false, false);
+    if (TF) tf_layer_fwd(x, r, tf_sizes(x, m), true, true, false, 0);
+    else if (x.H > 1) mlp_layer_fwd(x, r, m, kCol, false, false, 0);
 }
 
 // The ops of stage s's block before (pre) and after (suf) its repeating
 // units: embedding, LM head, loss (transformer); loss, the last unit in
 // inference and the stage's first unit in backward (MLP).
-template <bool TF>
-__device__ void record_edges(const Ctx &x, int s, bool bwd, uint64_t m, bool acc, Record &rp, Record &rs)
+template <bool TF, class SP, class SS>
+__device__ void record_edges(const Ctx &x, int s, bool bwd, uint64_t m, bool acc, SP &rp, SS &rs)
 {
     if (TF) {
         const TfSz z = tf_sizes(x, m);
@@ -252,10 +358,11 @@ __device__ void record_edges(const Ctx &x, int s, bool bwd, uint64_t m, bool acc
     const int per = x.H > 1 ? 2 : 1, l0 = stage_l0(x, s), nl = stage_nl(x, s);
     if (!bwd) {
         if (!x.train && s == x.P - 1)
-            for (int i = l0 + nl - per; i < l0 + nl; ++i) mlp_layer_fwd(x, rs, m, mlp_kind(x, i), true, i == x.L - 1);
+            for (int i = l0 + nl - per; i < l0 + nl; ++i)
+                mlp_layer_fwd(x, rs, m, mlp_kind(x, i), true, i == x.L - 1, 0);
     } else {
         if (s == x.P - 1) mlp_loss(x, rp, m);
-        for (int i = l0 + per - 1; i >= l0; --i) mlp_layer_bwd(x, rs, m, mlp_kind(x, i), i == l0, i == 0, acc);
+        for (int i = l0 + per - 1; i >= l0; --i) mlp_layer_bwd(x, rs, m, mlp_kind(x, i), i == l0, i == 0, acc, 0);
     }
 }
 
@@ -325,6 +432,23 @@ struct Count {
         walked += 1;
         nops += x.mult_dp;
     }
+    // ZeRO collectives: one per tensor rank
+    __device__ __forceinline__ void bcast(uint64_t, int)
+    {
+        if (!x.zero) return;
+        walked += 1;
+        nops += x.mult_dp;
+    }
+    __device__ __forceinline__ void reduce(uint64_t, int)
+    {
+        walked += 1;
+        nops += x.mult_dp;
+    }
+    __device__ __forceinline__ void owner_local(uint64_t, uint64_t, uint64_t, uint64_t, int)
+    {
+        walked += 1;
+        nops += x.mult_dp;
+    }
 };
 
 // ops of stage s's blocks and sends: K forward blocks; in training one
@@ -344,6 +468,126 @@ __device__ __forceinline__ void count_blocks(const Ctx &x, int s, uint64_t &walk
     const uint64_t bs = s > 0 ? 1 : 0;         // Send after each backward block
     walked += b0.walked + (K - 1) * b1.walked + K * bs;
     nops += b0.nops + (K - 1) * b1.nops + K * bs * x.mult_dev;
+}
+
+// ---------------------------------------------------------------------------
+// ZeRO: one block kind's memory over the D replicas of a stage
+// ---------------------------------------------------------------------------
+// A run of n equal units (an edge is a run of one): net bytes d per unit,
+// highest points tn (a replica that does not own the unit's group) and to
+// (its owner) above the unit's start; unit u reads the weights of group
+// gs + dir * u (gs < 0: no weight is read).
+struct ZSeg {
+    int n;
+    int64_t d, tn, to;
+    int gs, dir;
+};
+
+// highest point of a run above its start as replica d sees it (d < 0: a
+// replica owning none of the groups).  Unit u starts at u * d; over the
+// units a replica owns (u = r mod D) and those it does not, the highest
+// start is the last one (d >= 0) or the first one (d < 0).
+__device__ __forceinline__ int64_t run_top(const ZSeg &g, int d, int D)
+{
+    const int n = g.n;
+    const int64_t ud = g.d;
+    int r = -1;
+    if (d >= 0 && g.gs >= 0) {
+        r = (g.dir > 0 ? d - g.gs : g.gs - d) % D;
+        if (r < 0) r += D;
+    }
+    int64_t best = INT64_MIN;
+    if (ud >= 0) {
+        if (r >= 0 && r <= n - 1) {
+            const int64_t t = (int64_t)(r + ((n - 1 - r) / D) * D) * ud + g.to;
+            best = t > best ? t : best;
+        }
+        const int un = (r >= 0 && (n - 1) % D == r) ? n - 2 : n - 1;   // D >= 2: n - 2 is not owned
+        if (un >= 0) {
+            const int64_t t = (int64_t)un * ud + g.tn;
+            best = t > best ? t : best;
+        }
+    } else {
+        if (r >= 0 && r <= n - 1) {
+            const int64_t t = (int64_t)r * ud + g.to;
+            best = t > best ? t : best;
+        }
+        const int un = r == 0 ? 1 : 0;
+        if (un <= n - 1) {
+            const int64_t t = (int64_t)un * ud + g.tn;
+            best = t > best ? t : best;
+        }
+    }
+    return best;
+}
+
+// Net bytes (delta) and highest point (top) of a block of stage s, relative
+// to the live bytes at its start counted with the largest owned resident
+// (z.rmax): top = max over replicas d of owned(d) - rmax + the highest point
+// of d's own walk through the block.  n: units of the block; n_r: replayed
+// units (recomputation, backward).  Replicas owning nothing on the stage
+// all walk alike, so the owners of the stage's groups plus one of them are
+// enough.
+template <bool TF>
+__device__ void zero_block(const Ctx &x, int s, const ZStage &z, bool bwd, uint64_t m, bool acc, int n, int n_r,
+                           int64_t &delta, int64_t &top)
+{
+    ZSeg seg[5];
+    int ns = 0;
+    MemZ pre{x, 0, 0, 0, 0}, suf{x, 0, 0, 0, 0};
+    record_edges<TF>(x, s, bwd, m, acc, pre, suf);
+    int g_pre = -1, g_suf = -1;
+    if (TF) {
+        if (!bwd && s == 0) g_pre = 0;
+        if (!bwd && s == x.P - 1) g_suf = z.g_head;
+        if (bwd && s == x.P - 1) g_pre = z.g_head;
+    } else if (bwd) {
+        g_suf = z.gl_lo;   // the stage's first unit
+    }
+    seg[ns++] = ZSeg{1, pre.cur, pre.tn, pre.to, g_pre, 1};
+    if (!bwd) {
+        MemZ u{x, 0, 0, 0, 0};
+        record_unit<TF>(x, false, m, false, u);
+        if (x.rc && n >= 1) {
+            MemZ f{x, 0, 0, 0, 0};
+            record_unit<TF>(x, false, m, false, f, kFwdFirst);
+            seg[ns++] = ZSeg{1, f.cur, f.tn, f.to, z.gl_lo, 1};
+            seg[ns++] = ZSeg{n - 1, u.cur, u.tn, u.to, z.gl_lo + 1, 1};
+        } else {
+            seg[ns++] = ZSeg{n, u.cur, u.tn, u.to, z.gl_lo, 1};
+        }
+    } else {
+        if (x.rc) {
+            MemZ u{x, 0, 0, 0, 0}, q{x, 0, 0, 0, 0};
+            record_unit<TF>(x, false, m, false, u, kFwdReplay);
+            record_partial<TF>(x, m, q);
+            seg[ns++] = ZSeg{n_r, u.cur, u.tn, u.to, z.gl_lo, 1};
+            seg[ns++] = ZSeg{1, q.cur, q.tn, q.to, z.gl_hi - 1, 1};
+        }
+        MemZ u{x, 0, 0, 0, 0};
+        record_unit<TF>(x, true, m, acc, u);
+        seg[ns++] = ZSeg{n, u.cur, u.tn, u.to, z.gl_hi - 1, -1};
+    }
+    seg[ns++] = ZSeg{1, suf.cur, suf.tn, suf.to, g_suf, 1};
+    int64_t dl = 0;
+    for (int i = 0; i < ns; ++i) dl += seg[i].n > 0 ? (int64_t)seg[i].n * seg[i].d : 0;
+    const int g_lo = z.emb ? 0 : z.gl_lo, g_hi = z.head ? z.g_head + 1 : z.gl_hi;
+    const int n_own = (g_hi - g_lo) < x.D ? (g_hi - g_lo) : x.D;
+    const int n_cls = n_own + ((g_hi - g_lo) < x.D ? 1 : 0);
+    int64_t best = INT64_MIN;
+    for (int j = 0; j < n_cls; ++j) {
+        const int d = j < n_own ? (g_lo + j) % x.D : -1;
+        int64_t at = (d >= 0 ? (int64_t)z_owned(x, z, d) : 0) - (int64_t)z.rmax, t = INT64_MIN;
+        for (int i = 0; i < ns; ++i) {
+            if (seg[i].n <= 0) continue;
+            const int64_t v = at + run_top(seg[i], d, x.D);
+            t = v > t ? v : t;
+            at += (int64_t)seg[i].n * seg[i].d;
+        }
+        best = t > best ? t : best;
+    }
+    delta = dl;
+    top = best;
 }
 
 // n repetitions of a unit of costs r: the same value as n * 2 * U2n
@@ -497,25 +741,25 @@ constexpr int kMaxSegShared = 16; // segments of >= 4 lanes per wavefront
 // Per-lane programs (segments of 1 or 2 lanes): each lane records its own
 // block program per direction, again whenever the microbatch size class or
 // the accumulation changes, with the block's composed memory summary.
-template <bool TF> struct LdsLane {
-    double2 prog[2][Shape<TF>::PRE2 + Shape<TF>::U2 + Shape<TF>::SUF2][kLanes];
+template <class Sh> struct LdsLane {
+    double2 prog[2][Sh::PRE2 + Sh::U2 + Sh::SUF2][kLanes];
     int64_t sum[2][2][kLanes];   // [backward][delta, top][lane]
 };
 // Shared programs (segments of >= 4 lanes): the repeating unit does not
 // depend on the stage, so each segment records the unit of every key once,
 // cooperatively; the stage edges stay per lane (transformer: stages 0 and
 // P-1 only).
-template <bool TF> struct LdsSeg {
-    double2 unit[kMaxSegShared][kKeys][Shape<TF>::U2];
+template <class Sh> struct LdsSeg {
+    double2 unit[kMaxSegShared][kKeys][Sh::U2];
     int64_t usum[kMaxSegShared][kKeys][2];
     int64_t xsum[kMaxSegShared][2][6];   // recomputation, per forward key: first unit, replay unit, partial
-    double2 edge[2][Shape<TF>::PRE2 + Shape<TF>::SUF2][kLanes];
+    double2 edge[2][Sh::PRE2 + Sh::SUF2][kLanes];
     int64_t esum[2][4][kLanes];  // [backward][pre delta, pre top, suf delta, suf top][lane]
 };
 
-template <bool TF> union LdsNarrow {
-    LdsLane<TF> a;
-    LdsSeg<TF> b;
+template <class Sh> union LdsNarrow {
+    LdsLane<Sh> a;
+    LdsSeg<Sh> b;
 };
 
 // Wide segments (>= 8 lanes, transformer): at most 8 segments per
@@ -525,13 +769,13 @@ template <bool TF> union LdsNarrow {
 constexpr int kMaxSegWide = 8;
 constexpr int kFirstWideClass = 3;   // segment width 8
 constexpr int64_t kSplitMinCand = 8192;
-template <bool TF> struct LdsWide {
-    double2 unit[kMaxSegWide][kKeys][Shape<TF>::U2];
+template <class Sh> struct LdsWide {
+    double2 unit[kMaxSegWide][kKeys][Sh::U2];
     int64_t usum[kMaxSegWide][kKeys][2];
     int64_t xsum[kMaxSegWide][2][6];
-    double2 edge[kMaxSegWide][2][2][Shape<TF>::PRE2 + Shape<TF>::SUF2];   // [segment][stage 0, P-1][backward]
+    double2 edge[kMaxSegWide][2][2][Sh::PRE2 + Sh::SUF2];   // [segment][stage 0, P-1][backward]
     int64_t esum[kMaxSegWide][2][2][4];
-    double2 zero[Shape<TF>::PRE2 + Shape<TF>::SUF2];
+    double2 zero[Sh::PRE2 + Sh::SUF2];
     int64_t zsum[4];
 };
 
@@ -540,11 +784,10 @@ template <bool TF> struct LdsWide {
 // units; under recomputation the forward block's first unit keeps its input
 // and the backward block replays n_r forward units and the partial unit
 // after its pre ops.
-template <bool TF>
+template <bool TF, class Sh>
 __device__ void record_lane(const Ctx &x, int s, bool bwd, uint64_t m, bool acc, int n, int n_r, double2 *pp,
                             int64_t &delta, int64_t &top)
 {
-    using Sh = Shape<TF>;
     double *base = reinterpret_cast<double *>(pp);
     Record rp{x, base, 2 * kLanes, 0, 0, 0};
     Record ru{x, base + Sh::PRE2 * 2 * kLanes, 2 * kLanes, 0, 0, 0};
@@ -576,14 +819,14 @@ __device__ void record_lane(const Ctx &x, int s, bool bwd, uint64_t m, bool acc,
 
 // WIDE: the launch for wide segments of a transformer; otherwise every class
 // of an MLP, or the narrow classes of a transformer.  RC: training with
-// activation recomputation (a separate instantiation keeps the replay out of
-// the other kernels).
-template <bool TF, bool WIDE, bool RC>
+// activation recomputation; ZR: training with ZeRO (separate instantiations
+// keep the replay and the broadcasts out of the other kernels).
+template <bool TF, bool WIDE, bool RC, bool ZR>
 __device__ __forceinline__ void parametric_body(const ParArgs &g)
 {
-    using Sh = Shape<TF>;
+    using Sh = Shape<TF, ZR>;
     constexpr int PST = WIDE ? 1 : kLanes;   // double2 stride of a lane's edge program
-    __shared__ typename std::conditional<WIDE, LdsWide<TF>, LdsNarrow<TF>>::type L;
+    __shared__ typename std::conditional<WIDE, LdsWide<Sh>, LdsNarrow<Sh>>::type L;
 
     const int lane = threadIdx.x;
     const uint32_t gl = blockIdx.x * (uint32_t)kLanes;
@@ -618,11 +861,23 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     int pos = 0, nf = 0, nb = 0, len = 0, mr = 0, n_f = 0, n_b = 0;
     constexpr bool rc = RC;   // the launch checks it against the model
     int n_r = 0, n_part = 0;                     // replayed units, entries of the partial unit
+    // ZeRO: memory summaries of the last forward / backward block kind
+    const bool zero_c = ZR && train && M.zero != 0 && st.D > 1;
+    int zk_f = -1, zk_b = -1;
+    int64_t zd_f = 0, zt_f = 0, zd_b = 0, zt_b = 0;
     if (live_stage) {
         Ctx x = {};
         make_ctx(M, g.c, st, x);
         x.mlp = !TF;   // the family is uniform per launch: compiles out the other
-        Walk w{x, 0.0, (int64_t)resident(x, s), 0, 0, 0};
+        uint64_t res0;
+        if (ZR && x.zero) {
+            ZStage zs;
+            z_stage(x, s, zs);
+            res0 = resident_inputs(x, s) + zs.rmax;
+        } else {
+            res0 = resident(x, s);
+        }
+        Walk w{x, 0.0, (int64_t)res0, 0, 0, 0, nullptr};
         w.peak = w.live;
         // microbatch splits before the pipeline
         if (x.K > 1) {
@@ -773,12 +1028,12 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                         make_ctx(M, g.c, st, x);
                         x.mlp = !TF;
                         if ((bwd ? key_b : key_f) != key) {
-                            record_lane<TF>(x, s, bwd, m, acc, n, n_r, pp, L.a.sum[d][0][lane], L.a.sum[d][1][lane]);
+                            record_lane<TF, Sh>(x, s, bwd, m, acc, n, n_r, pp, L.a.sum[d][0][lane], L.a.sum[d][1][lane]);
                             if (bwd) key_b = key;
                             else key_f = key;
                         }
                         if (replay && bwd && key_f != mc) {   // the replay walks the forward unit of this size
-                            record_lane<TF>(x, s, false, m, false, n_f, n_r, &L.a.prog[0][0][lane], L.a.sum[0][0][lane],
+                            record_lane<TF, Sh>(x, s, false, m, false, n_f, n_r, &L.a.prog[0][0][lane], L.a.sum[0][0][lane],
                                             L.a.sum[0][1][lane]);
                             key_f = mc;
                         }
@@ -868,6 +1123,30 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                     chain(delta, top, d2, t2);
                 }
             }
+            if constexpr (ZR) {
+                if (zero_c) {
+                    if ((bwd ? zk_b : zk_f) != key) {
+                        Ctx x = {};
+                        make_ctx(M, g.c, st, x);
+                        x.mlp = !TF;
+                        ZStage zs;
+                        z_stage(x, s, zs);
+                        int64_t zd, zt;
+                        zero_block<TF>(x, s, zs, bwd, m, acc, n, nr, zd, zt);
+                        if (bwd) {
+                            zk_b = key;
+                            zd_b = zd;
+                            zt_b = zt;
+                        } else {
+                            zk_f = key;
+                            zd_f = zd;
+                            zt_f = zt;
+                        }
+                    }
+                    delta = bwd ? zd_b : zd_f;
+                    top = bwd ? zt_b : zt_f;
+                }
+            }
             const int64_t hi = live + top;
             peak = hi > peak ? hi : peak;
             live += delta;
@@ -928,7 +1207,9 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         Ctx x = {};
         make_ctx(M, g.c, st, x);
         x.mlp = !TF;
-        Walk w{x, clk, live, peak, walked, nops};
+        ZStage zs;
+        if (ZR && x.zero) z_stage(x, s, zs);
+        Walk w{x, clk, live, peak, walked, nops, &zs};
         if (train) weight_update(x, w, s);
         clk = w.clk;
         live = w.live;
@@ -968,17 +1249,37 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     }
 }
 
-template <bool TF, bool RC>
+template <bool TF, bool RC, bool ZR>
 __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
 {
-    parametric_body<TF, false, RC>(g);
+    parametric_body<TF, false, RC, ZR>(g);
 }
 
 // wide segments of a transformer: two wavefronts per SIMD
-template <bool RC>
+template <bool RC, bool ZR>
 __global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(2))) void k_parametric_wide(const ParArgs g)
 {
-    parametric_body<true, true, RC>(g);
+    parametric_body<true, true, RC, ZR>(g);
+}
+
+// the kernel of a launch, by family, width class and model options
+template <bool RC, bool ZR>
+void launch_variant(bool tf, bool wide, dim3 grid, dim3 block, hipStream_t s, const ParArgs &g)
+{
+    if (!tf) hipLaunchKernelGGL((k_parametric<false, RC, ZR>), grid, block, 0, s, g);
+    else if (!wide) hipLaunchKernelGGL((k_parametric<true, RC, ZR>), grid, block, 0, s, g);
+    else hipLaunchKernelGGL((k_parametric_wide<RC, ZR>), grid, block, 0, s, g);
+}
+
+void launch_kernel(bool rc, bool zr, bool tf, bool wide, dim3 grid, dim3 block, hipStream_t s, const ParArgs &g)
+{
+    if (rc) {
+        if (zr) launch_variant<true, true>(tf, wide, grid, block, s, g);
+        else launch_variant<true, false>(tf, wide, grid, block, s, g);
+    } else {
+        if (zr) launch_variant<false, true>(tf, wide, grid, block, s, g);
+        else launch_variant<false, false>(tf, wide, grid, block, s, g);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1140,13 +1441,11 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
     g.narrow_end = split ? kFirstWideClass : kClasses;
     const bool rc = m.mode != DSIM_INFER && m.recompute != 0;
+    const bool zr = m.mode != DSIM_INFER && m.zero != 0;
+    const bool tf = m.family == DSIM_TRANSFORMER;
     const dim3 grid((unsigned)waves), block(kLanes);
-    if (m.family == DSIM_MLP) {
-        if (rc) hipLaunchKernelGGL((k_parametric<false, true>), grid, block, 0, s, g);
-        else hipLaunchKernelGGL((k_parametric<false, false>), grid, block, 0, s, g);
-    } else if (!split) {
-        if (rc) hipLaunchKernelGGL((k_parametric<true, true>), grid, block, 0, s, g);
-        else hipLaunchKernelGGL((k_parametric<true, false>), grid, block, 0, s, g);
+    if (!split) {
+        launch_kernel(rc, zr, tf, false, grid, block, s, g);
     } else {
         // narrow segments on a side stream, wide ones on the caller's: the
         // two launches need different amounts of LDS per wavefront and run
@@ -1160,14 +1459,12 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
         if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
         bool side_launched = false;
         if (e == hipSuccess) {
-            if (rc) hipLaunchKernelGGL((k_parametric<true, true>), grid, block, 0, side, g);
-            else hipLaunchKernelGGL((k_parametric<true, false>), grid, block, 0, side, g);
+            launch_kernel(rc, zr, true, false, grid, block, side, g);
             e = hipGetLastError();
             side_launched = e == hipSuccess;
         }
         if (e == hipSuccess) {
-            if (rc) hipLaunchKernelGGL((k_parametric_wide<true>), grid, block, 0, s, g);
-            else hipLaunchKernelGGL((k_parametric_wide<false>), grid, block, 0, s, g);
+            launch_kernel(rc, zr, true, true, grid, block, s, g);
             e = hipGetLastError();
         }
         if (e == hipSuccess) e = hipEventRecord(join, side);

@@ -26,11 +26,11 @@
 //
 // The kernel is bound by issue rate (about 100 vector instructions per op)
 // more than by HBM: it has a fast path for the ops every lane of a wavefront
-// has, which assumes valid ops (indices clamped, so even an invalid op stays
-// in bounds) and only tests whether each op is valid; a lane that meets an
-// op it cannot vouch for (or a free that would underflow), and every lane's
-// ops past the wavefront's common count, go through the exact per-op path
-// below it.
+// has, which assumes valid compute, send and all-reduce ops (indices
+// clamped, so even an invalid op stays in bounds) and only tests whether
+// each op is one; a lane that meets an op it cannot vouch for (a free that
+// would underflow, a broadcast or reduce record), and every lane's ops past
+// the wavefront's common count, go through the exact per-op path below it.
 #include "internal.h"
 
 namespace dsim {
@@ -95,14 +95,16 @@ __device__ __forceinline__ uint32_t op_flags(uint32_t code, uint32_t flops_bits,
     const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
     // kind, reserved bits, and flops/bytes finite and >= 0 (bit patterns
     // below +inf)
-    if ((code >> 24) != 0u || kind > 2u || flops_bits >= 0x7f800000u || bytes_bits >= 0x7f800000u)
+    if ((code >> 24) != 0u || kind > 4u || flops_bits >= 0x7f800000u || bytes_bits >= 0x7f800000u)
         return DSIM_ST_BAD_OP;
     if (kind == 0u) return ia < (uint32_t)ND ? 0u : (uint32_t)DSIM_ST_BAD_DEVICE;
     if (kind == 1u) {
         if (ia >= (uint32_t)ND || ib >= (uint32_t)ND) return DSIM_ST_BAD_DEVICE;
         return ia == ib ? (uint32_t)DSIM_ST_SELF_SEND : 0u;
     }
-    return (ib == 0u || (ib >> ND) != 0u) ? (uint32_t)DSIM_ST_BAD_DEVICE : 0u;
+    if (kind == 2u) return (ib == 0u || (ib >> ND) != 0u) ? (uint32_t)DSIM_ST_BAD_DEVICE : 0u;
+    // broadcast / reduce: the root is a member of the mask
+    return (ia >= (uint32_t)ND || (ib >> ND) != 0u || ((ib >> ia) & 1u) == 0u) ? (uint32_t)DSIM_ST_BAD_DEVICE : 0u;
 }
 
 template <int ND>
@@ -292,9 +294,13 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             cost = launch + (tf > tb ? tf : tb);
         } else if (kind == 1u) {
             cost = lat + b * inv_l;
-        } else {
+        } else if (kind == 2u) {
             const double2 ar = s_cost[__popc(m)];
             cost = ar.x + ar.y * (b * inv_l);
+        } else {
+            // broadcast / reduce: a chain of n - 1 hops (Fig. 9's Send for n = 2)
+            const int n = __popc(m);
+            cost = n > 1 ? (double)(n - 1) * lat + b * inv_l : 0.0;
         }
         double start = 0.0;
 #pragma unroll
@@ -304,7 +310,31 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
 #pragma unroll
         for (int d = 0; d < ND; ++d)
             if ((m >> d) & 1u) clk[d] = end;
-        if (kind != 2u) {
+        if (kind >= 3u) {
+            // the receivers (broadcast) or the root (reduce) allocate, every
+            // member samples its peak, then the root (broadcast) or every
+            // member (reduce) frees
+            const uint64_t al = a.alloc[o], fr = a.freeb[o];
+#pragma unroll
+            for (int d = 0; d < ND; ++d) {
+                if (((m >> d) & 1u) == 0u) continue;
+                const bool gets = kind == 3u ? (uint32_t)d != ia : (uint32_t)d == ia;
+                const uint64_t lt = s_mem[d][tid].x + (gets ? al : 0u);
+                s_mem[d][tid].x = lt;
+                if (lt > s_mem[d][tid].y) s_mem[d][tid].y = lt;
+            }
+#pragma unroll
+            for (int d = 0; d < ND; ++d) {
+                if (((m >> d) & 1u) == 0u || (kind == 3u && (uint32_t)d != ia)) continue;
+                const uint64_t lf = s_mem[d][tid].x;
+                if (fr > lf) {
+                    st |= DSIM_ST_MEM_UNDERFLOW;
+                    s_mem[d][tid].x = 0;
+                } else {
+                    s_mem[d][tid].x = lf - fr;
+                }
+            }
+        } else if (kind != 2u) {
             const uint32_t tdev = kind == 1u ? ib : ia;
             const uint64_t lt = s_mem[tdev][tid].x + (uint64_t)a.alloc[o];
             s_mem[tdev][tid].x = lt;

@@ -35,7 +35,8 @@ class dsim_model(C.Structure):
     _fields_ = [("family", C.c_int32), ("mode", C.c_int32), ("n_layers", C.c_int32),
                 ("n_heads", C.c_int32), ("d_model", C.c_int64), ("d_ff", C.c_int64),
                 ("seq_len", C.c_int64), ("vocab", C.c_int64), ("global_batch", C.c_int64),
-                ("elem_bytes", C.c_int32), ("schedule", C.c_int32), ("recompute", C.c_int32)]
+                ("elem_bytes", C.c_int32), ("schedule", C.c_int32), ("recompute", C.c_int32),
+                ("zero", C.c_int32)]
 
 
 class dsim_strategy(C.Structure):
@@ -132,7 +133,7 @@ def device_model(spec):
 def model_struct(spec):
     return dsim_model(spec.family, spec.mode, spec.n_layers, spec.n_heads, spec.d_model, spec.d_ff,
                       spec.seq_len, spec.vocab, spec.global_batch, spec.elem_bytes, spec.schedule,
-                      spec.recompute)
+                      spec.recompute, spec.zero)
 
 
 def dsim_create_grid(model, grid):

@@ -110,6 +110,8 @@ GPT3_175B = Workload("gpt3_175b",
 GPT3_175B_GPIPE = replace(GPT3_175B, name="gpt3_175b_gpipe", model=replace(GPT3_175B.model, schedule=SCHED_GPIPE))
 # the same grid with activation recomputation (gradient checkpointing)
 GPT3_175B_RECOMPUTE = replace(GPT3_175B, name="gpt3_175b_recompute", model=replace(GPT3_175B.model, recompute=1))
+# the same grid with ZeRO partitioning of weights, gradients and optimizer state
+GPT3_175B_ZERO = replace(GPT3_175B, name="gpt3_175b_zero", model=replace(GPT3_175B.model, zero=1))
 
 ALL = {w.name: w for w in (TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN, RANDOM_TABLES, GPT3_175B,
-                           GPT3_175B_GPIPE, GPT3_175B_RECOMPUTE)}
+                           GPT3_175B_GPIPE, GPT3_175B_RECOMPUTE, GPT3_175B_ZERO)}

@@ -108,6 +108,43 @@ CASES = [
 ]
 
 
+ZERO_CASES = [
+    ("mlp_zero", mlp(4, 64, 48, 4, TRAIN_ADAM, zero=1), all_strats([2, 3, 4, 8], [1, 2], [1, 2], [1, 2, 3], 8)),
+    ("mlp_zero_sgd_rc", mlp(6, 32, 48, 2, TRAIN_SGD, recompute=1, zero=1),
+     all_strats([2, 4], [1, 2], [1, 3], [1, 2, 5], 8)),
+    ("tf_zero", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, zero=1), all_strats([2, 3, 4], [1, 2], [1, 2], [1, 2, 3], 8)),
+    ("tf_zero_mixed_gpipe", transformer(3, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED, schedule=SCHED_GPIPE, zero=1),
+     all_strats([2, 4], [1, 2], [1, 2, 3], [1, 2], 8)),
+    ("tf_zero_rc", transformer(5, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, recompute=1, zero=1),
+     all_strats([2, 3], [1, 2], [1, 2], [1, 3], 8)),
+]
+
+
+@pytest.mark.parametrize("case", ZERO_CASES, ids=[c[0] for c in ZERO_CASES])
+def test_zero_programs_as_tables(torch_gpu, orc, case):
+    """ZeRO programs hold broadcast and reduce records; their data replicas
+    own different parameter groups, so finish times, peaks and resident
+    bytes are compared device by device with the oracle's full program."""
+    name, model, strat = case
+    dev = DeviceSpec(mem_cap_bytes=10 ** 6)
+    o = orc.run_strategies(model, strat, dev, slice=False, row_width=int(strat[:, 2].max()), threads=8)
+    assert np.all(o["status"] == 0)
+    g = materialize_and_simulate(torch_gpu, model, strat, dev, 8, int(o["n_ops"].max()))
+    assert np.all(g["mat_status"] == 0) and np.all(g["status"] == 0)
+    assert np.array_equal(g["table_ops"], o["n_ops"].astype(np.int64))
+    assert np.array_equal(g["makespan"], o["makespan"])
+    assert np.array_equal(g["cand_peak"].view(np.uint64), o["cand_peak"])
+    differ = 0
+    for i, (D, H, P, K) in enumerate(strat.tolist()):
+        r = orc.sim_strategy(model, D, H, P, K, dev)
+        n = D * H * P
+        assert np.array_equal(g["finish"][i, :n], r["dev_finish"]), (name, strat[i].tolist())
+        assert np.array_equal(g["peak"][i, :n].view(np.uint64), r["dev_peak"]), (name, strat[i].tolist())
+        assert np.array_equal(g["init_live"][i, :n].view(np.uint64), r["dev_resident"]), (name, strat[i].tolist())
+        differ += len(set(r["dev_peak"][:D * H].tolist())) > 1
+    assert differ > 0   # the replicas really differ somewhere
+
+
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_small_programs_as_tables(torch_gpu, orc, case):
     name, model, strat = case

@@ -93,6 +93,20 @@ SMALL = [
     ("tf_mixed_gpipe_rc", transformer(6, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED, schedule=SCHED_GPIPE, recompute=1),
      all_strats([1, 2], [1, 2], [1, 2, 4, 5], [1, 4])),
     ("tf_infer_rc", transformer(6, 48, 6, 16, 97, 9, 2, INFER, recompute=1), all_strats([1, 3], [1, 2], [1, 4], [1, 3])),
+    # ZeRO: replicas own different groups; D up to twice the groups of a stage
+    ("mlp_adam_zero", mlp(6, 64, 48, 2, TRAIN_ADAM, zero=1), all_strats([1, 2, 3, 4, 8, 16], [1, 2], [1, 2, 3],
+                                                                        [1, 3])),
+    ("mlp_sgd_zero_rc", mlp(8, 32, 48, 4, TRAIN_SGD, recompute=1, zero=1), all_strats([2, 3, 4, 6], [1, 2], [1, 2, 4],
+                                                                                     [1, 2, 5])),
+    ("mlp_mixed_zero_gpipe", mlp(8, 32, 48, 2, TRAIN_ADAM_MIXED, schedule=SCHED_GPIPE, zero=1),
+     all_strats([2, 4, 12], [1, 2], [1, 2, 4], [1, 4])),
+    ("tf_train_zero", transformer(4, 32, 4, 8, 101, 24, 2, TRAIN_ADAM, zero=1), all_strats([1, 2, 3, 4, 8], [1, 2],
+                                                                                        [1, 2, 4], [1, 2, 3])),
+    ("tf_mixed_zero_rc", transformer(5, 32, 4, 8, 64, 12, 2, TRAIN_ADAM_MIXED, recompute=1, zero=1),
+     all_strats([2, 3, 6], [1, 2], [1, 2, 5], [1, 2])),
+    ("tf_sgd_zero_gpipe", transformer(6, 32, 2, 8, 50, 16, 4, TRAIN_SGD, schedule=SCHED_GPIPE, zero=1),
+     all_strats([2, 4, 8, 16], [1, 2], [1, 3, 6], [1, 2])),
+    ("tf_infer_zero", transformer(6, 48, 6, 16, 97, 9, 2, INFER, zero=1), all_strats([1, 3], [1, 2], [1, 4], [1, 3])),
 ]
 
 
@@ -112,7 +126,9 @@ GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_gpipe",
                  model=replace(GPT2_SMALL_TRAIN.model, schedule=SCHED_GPIPE)),
          replace(LARGE_MLP, name="large_mlp_recompute", model=replace(LARGE_MLP.model, recompute=1)),
-         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_recompute", model=replace(GPT2_SMALL_TRAIN.model, recompute=1))]
+         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_recompute", model=replace(GPT2_SMALL_TRAIN.model, recompute=1)),
+         replace(LARGE_MLP, name="large_mlp_zero", model=replace(LARGE_MLP.model, zero=1)),
+         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_zero", model=replace(GPT2_SMALL_TRAIN.model, zero=1))]
 
 
 @pytest.mark.parametrize("w", GRIDS, ids=[w.name for w in GRIDS])
@@ -139,7 +155,8 @@ def test_workload_grid_vs_oracle(torch_gpu, orc, w):
     assert int(found.item()) == rf and np.array_equal(idx.cpu().numpy(), ri)
 
 
-@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"]], ids=["1f1b", "recompute"])
+@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"], ALL["gpt3_175b_zero"]],
+                         ids=["1f1b", "recompute", "zero"])
 def test_gpt3_grid_sampled(torch_gpu, orc, w):
     """The GPT-3-shaped grid at full size (39,965 strategies, the launch
     configuration the benchmark times, the 288e9-byte cap, top-16): a seeded
@@ -217,6 +234,8 @@ EDGE_MODELS = [
     ("tf_long_rc", transformer(24, 64, 4, 16, 1000, 16, 2, TRAIN_ADAM, recompute=1),
      all_strats([1, 2], [1, 2, 4], [1, 2, 3], [1, 2, 5, 16])),
     ("mlp_long_rc", mlp(32, 128, 64, 2, TRAIN_ADAM, recompute=1), all_strats([1, 2], [1, 2], [1, 2, 4], [1, 3, 8, 32])),
+    ("tf_long_zero", transformer(24, 64, 4, 16, 1000, 16, 2, TRAIN_ADAM, zero=1),
+     all_strats([2, 4], [1, 2, 4], [1, 2, 3], [1, 2, 4])),
 ]
 
 

@@ -30,16 +30,19 @@ def assert_times(gpu, ref):
     assert np.array_equal(gpu, ref), "times agree to 1e-12 but not bit for bit"
 
 
-def random_tables(rng, n_cand, max_ops, n_dev, bad=False):
+def random_tables(rng, n_cand, max_ops, n_dev, bad=False, rooted=False):
     """Seeded synthetic tables with every op kind; bad=True also plants
-    invalid ops and frees larger than the live bytes."""
-    kind = rng.choice(3, size=(max_ops, n_cand), p=[0.7, 0.2, 0.1]).astype(np.uint32)
+    invalid ops and frees larger than the live bytes; rooted=True adds
+    broadcast and reduce records (their masks hold the root)."""
+    p = [0.6, 0.15, 0.1, 0.08, 0.07] if rooted else [0.7, 0.2, 0.1]
+    kind = rng.choice(len(p), size=(max_ops, n_cand), p=p).astype(np.uint32)
     a = rng.integers(0, n_dev, (max_ops, n_cand)).astype(np.uint32)
     b = rng.integers(0, n_dev, (max_ops, n_cand)).astype(np.uint32)
     if n_dev > 1:
         b = np.where(b == a, (a + 1) % n_dev, b)
     mask = rng.integers(1, 1 << n_dev, (max_ops, n_cand)).astype(np.uint32)
     code = np.where(kind == 2, 2 | (mask << 16), kind | (a << 8) | (b << 16)).astype(np.uint32)
+    code = np.where(kind >= 3, kind | (a << 8) | ((mask | (1 << a)) << 16), code).astype(np.uint32)
     if n_dev == 1:
         code = np.where(kind == 1, 0, code).astype(np.uint32)
     alloc = rng.integers(0, 5000, (max_ops, n_cand)).astype(np.uint32)
@@ -80,15 +83,16 @@ def results_np(r):
     return out
 
 
+@pytest.mark.parametrize("rooted", [False, True], ids=["plain", "bcast_reduce"])
 @pytest.mark.parametrize("n_dev", [1, 2, 3, 5, 8])
 @pytest.mark.parametrize("bad", [False, True])
-def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad):
+def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, rooted):
     from paper_2111_05426_amd import dsim
     from paper_2111_05426_amd.workloads import DeviceSpec
     torch = torch_gpu
-    rng = np.random.default_rng(1000 + n_dev + 17 * bad)
+    rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted)
     n_cand, max_ops = 777, 301   # several 256-lane blocks and a ragged tail
-    t = random_tables(rng, n_cand, max_ops, n_dev, bad)
+    t = random_tables(rng, n_cand, max_ops, n_dev, bad, rooted)
     dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5)
     g = to_gpu(torch, t)
     init = torch.from_numpy(t["init"].view(np.int64)).cuda()

@@ -649,6 +649,49 @@ def test_projection_matches_full_program(orc, case):
     assert proj["n_ops"] == full["n_ops"] and proj["cand_peak"] == full["cand_peak"]
 
 
+ZERO_SYM_CASES = [
+    (mlp(6, 64, 48, 2, TRAIN_ADAM, zero=1), 4, 2, 3, 5), (mlp(4, 32, 48, 4, TRAIN_SGD, zero=1), 8, 1, 2, 3),
+    (transformer(4, 32, 4, 8, 100, 12, 2, TRAIN_ADAM_MIXED, zero=1), 3, 2, 2, 3),
+    (transformer(5, 32, 4, 8, 101, 16, 2, TRAIN_ADAM, recompute=1, zero=1), 4, 2, 2, 2),
+    (transformer(3, 32, 2, 8, 64, 24, 4, TRAIN_SGD, schedule=SCHED_GPIPE, zero=1), 6, 2, 3, 2),
+]
+
+
+@pytest.mark.parametrize("case", range(len(ZERO_SYM_CASES)))
+def test_zero_projection_matches_full_program(orc, case):
+    """With ZeRO the data replicas of a stage differ, the tensor ranks of a
+    replica do not: the projection onto every data replica of tensor rank 0
+    gives the full program's stage finish times, stage peaks, makespan and
+    op count."""
+    m, D, H, P, K = ZERO_SYM_CASES[case]
+    full = orc.sim_strategy(m, D, H, P, K, DEV)
+    proj = orc.sim_strategy(m, D, H, P, K, DEV, slice=True)
+    assert full["status"] == 0
+    fin = full["dev_finish"].reshape(P, D, H)
+    pk = full["dev_peak"].reshape(P, D, H)
+    assert np.all(fin == fin[:, :, :1]) and np.all(pk == pk[:, :, :1])
+    assert proj["makespan"] == full["makespan"]
+    assert np.array_equal(proj["stage_finish"], full["stage_finish"])
+    assert np.array_equal(proj["stage_peak"], full["stage_peak"])
+    assert proj["n_ops"] == full["n_ops"] and proj["cand_peak"] == full["cand_peak"]
+
+
+def test_zero_stage_finishes_with_its_last_owner(orc):
+    """Only a parameter's owner runs its optimizer op, and the next reduce
+    waits for it: every replica of a stage but the owner of its last
+    parameter ends one optimizer op earlier, and the stage's time is the
+    owner's, the same as if every replica had run every optimizer op."""
+    cost = {k: 0.0 for k in orc.TYPES}
+    cost.update(GEMM=1.0, GEMMDW=2.0, GEMMDX=4.0, REDUCE=8.0, OPT=16.0, BCAST=0.5)
+    m = mlp(3, 64, 48, 4, TRAIN_ADAM, zero=1)
+    r = orc.sim_strategy(m, 3, 1, 1, 1, DEV, type_cost=cost)
+    # 3 forward and 3 input-gradient broadcasts, 3 Gemm, 3 GemmDW, 3 GemmDX
+    body = 6 * 0.5 + 3 * 1.0 + 3 * 2.0 + 3 * 4.0
+    # layer 2 (the last parameter) belongs to replica 2
+    assert list(r["dev_finish"]) == [body + 3 * 8.0 + 2 * 16.0] * 2 + [body + 3 * (8.0 + 16.0)]
+    assert r["makespan"] == body + 3 * (8.0 + 16.0)
+
+
 def test_op_count_by_hand(orc):
     L = 4
     m = mlp(L, 64, 64, 4, TRAIN_SGD)
