@@ -19,10 +19,12 @@
 // peak) byte counters are indexed by a per-lane device id and live in LDS as
 // 16-byte pairs laid out [device][lane], so the 64 lanes of a wavefront
 // always hit 64 distinct pairs.  An op's cost is base + coef * x with
-// x = max(flops / F, bytes * w): (base, coef, w) comes from a small LDS table
-// indexed by the op class (compute: launch, 1, 1/B; send: latency, 1, 1/L;
-// all-reduce over n devices: the ring terms for n, 1/L), and a non-compute
-// op's flops are taken as 0, so every lane runs one straight sequence.
+// x = max(flops * g, bytes * w): (base, coef) and (w, g) come from small LDS
+// tables indexed by the op class (compute: launch, 1, 1/B, 1/F; send:
+// latency, 1, 1/L, 0; all-reduce over n devices: the ring terms for n, 1/L,
+// 0), so every lane runs one straight sequence.  The tables hold one copy per
+// lane of a 16-lane LDS phase: lanes of one phase reading different classes
+// then never meet in a bank.
 //
 // The kernel is bound by issue rate (about 100 vector instructions per op)
 // more than by HBM: it has a fast path for the ops every lane of a wavefront
@@ -39,6 +41,7 @@ namespace {
 constexpr int kBlock = 256;       // 4 wavefronts; 32 KB of LDS counters
 constexpr int kWavesPerSimd = 4;
 constexpr int kUnroll = 4;   // ops per register set; two sets in flight
+constexpr int kCopies = 16;  // copies of the per-class cost rows (one per lane of an LDS phase)
 
 struct TabArgs {
     const uint32_t *code;
@@ -83,6 +86,14 @@ __device__ __forceinline__ double max_nn(double a, double b)
     return r;
 }
 
+// max of two byte counts below 2^63 as one fp64 max of their bit patterns:
+// those are non-negative doubles (denormal below 2^52; fp64 denormals are
+// preserved in this kernel's float mode), which order like the integers
+__device__ __forceinline__ uint64_t max_bits(uint64_t a, uint64_t b)
+{
+    return (uint64_t)__double_as_longlong(max_nn(__longlong_as_double((long long)a), __longlong_as_double((long long)b)));
+}
+
 __device__ __forceinline__ double bits_double(uint32_t lo, uint32_t hi)
 {
     return __hiloint2double((int)hi, (int)lo);
@@ -112,16 +123,21 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     const TabArgs a)
 {
     __shared__ ulonglong2 s_mem[ND][kBlock];   // (live, peak) bytes
-    // (base, coef) of an op's cost: all-reduce over n = 0..ND devices, then
-    // compute, then send
-    __shared__ double2 s_cost[ND + 3];
-    __shared__ double s_ibw[ND + 3];
+    // per op class -- all-reduce over n = 0..ND devices, then compute, then
+    // send -- the cost terms (base, coef) and (1/bandwidth, 1/flop rate or 0)
+    __shared__ double2 s_c1[ND + 3][kCopies], s_c2[ND + 3][kCopies];
+    __shared__ double2 s_cost[ND + 3];   // (base, coef) for the exact path
 
     const int tid = threadIdx.x;
     if (tid <= ND) s_cost[tid] = make_double2(a.c.ar_lat[tid], a.c.ar_coef[tid]);
     if (tid == ND + 1) s_cost[tid] = make_double2(a.c.launch, 1.0);
     if (tid == ND + 2) s_cost[tid] = make_double2(a.c.lat, 1.0);
-    if (tid < ND + 3) s_ibw[tid] = tid == ND + 1 ? a.c.inv_b : a.c.inv_l;
+    for (int i = tid; i < (ND + 3) * kCopies; i += kBlock) {
+        const int e = i / kCopies, k = i % kCopies;
+        const bool cmp = e == ND + 1;
+        s_c1[e][k] = make_double2(e <= ND ? a.c.ar_lat[e] : (cmp ? a.c.launch : a.c.lat), e <= ND ? a.c.ar_coef[e] : 1.0);
+        s_c2[e][k] = make_double2(cmp ? a.c.inv_b : a.c.inv_l, cmp ? a.c.inv_f : 0.0);
+    }
 
     const int64_t c = (int64_t)blockIdx.x * kBlock + tid;
     const bool active = c < a.n_cand;
@@ -202,9 +218,20 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             const uint32_t ias = min(ia, (uint32_t)ND - 1u), ibs = min(ib, (uint32_t)ND - 1u);
             const uint32_t mc = 1u << ias, ms = mc | (1u << ibs), ma = ib & ((1u << ND) - 1u);
             const uint32_t m = is_c ? mc : (is_s ? ms : ma);
-            const bool bad = (code >= (1u << 24)) | (kind > 2u) | (max(fl[u], by[u]) >= 0x7f800000u) |
-                             ((ia >= (uint32_t)ND) & !is_a) | (is_s & ((ib >= (uint32_t)ND) | (ia == ib))) |
-                             (is_a & ((ib == 0u) | (ib >= (1u << ND))));
+            bool bad;
+            if constexpr ((ND & (ND - 1)) == 0) {
+                // one masked compare per kind: the reserved byte, the kind
+                // and the device fields that must be < ND
+                constexpr uint32_t hi = ~(uint32_t)(ND - 1) & 0xffu;
+                constexpr uint32_t m0 = 0xff0000ffu | (hi << 8), m1 = m0 | (hi << 16), m2 = 0xff0000ffu;
+                const bool ok = ((code & m0) == 0u) | (((code & m1) == 1u) & (ia != ib)) |
+                                (((code & m2) == 2u) & (ma != 0u) & (ib == ma));
+                bad = !ok | (max(fl[u], by[u]) >= 0x7f800000u);
+            } else {
+                bad = (code >= (1u << 24)) | (kind > 2u) | (max(fl[u], by[u]) >= 0x7f800000u) |
+                      ((ia >= (uint32_t)ND) & !is_a) | (is_s & ((ib >= (uint32_t)ND) | (ia == ib))) |
+                      (is_a & ((ib == 0u) | (ib >= (1u << ND))));
+            }
             suspect |= bad;
 
             // op cost (Sec. 3.3 / Sec. 4 cost functions) as base + coef * x:
@@ -212,10 +239,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             // bytes/L), all-reduce over n devices (ar_lat[n], ar_coef[n],
             // bytes/L); multiplying by 1.0 is exact
             const uint32_t idx = is_c ? (uint32_t)ND + 1u : (is_s ? (uint32_t)ND + 2u : (uint32_t)__popc(m));
-            const double2 bc = s_cost[idx];
-            const double ibw = s_ibw[idx];
-            const double f = (double)__uint_as_float(is_c ? fl[u] : 0u), b = (double)__uint_as_float(by[u]);
-            const double cost = bc.x + bc.y * max_nn(f * inv_f, b * ibw);
+            const double2 bc = s_c1[idx][tid & (kCopies - 1)], rw = s_c2[idx][tid & (kCopies - 1)];
+            // a non-compute class carries 0 as its flop reciprocal: a valid
+            // op's flops are finite, so that term is +0 and the max is the
+            // bandwidth term, as in the per-kind formulas
+            const double f = (double)__uint_as_float(fl[u]), b = (double)__uint_as_float(by[u]);
+            const double cost = bc.x + bc.y * max_nn(f * rw.y, b * rw.x);
 
             // synchronous start on the device set, common end.  sel[d] is 1.0
             // for a participant, 0.0 otherwise.  Clocks are >= 0, so
@@ -249,8 +278,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             const ulonglong2 tm = s_mem[tdev][tid];
             const uint64_t lf0 = s_mem[fdev][tid].x;
             const uint64_t lt = tm.x + (uint64_t)alloc;
-            const uint64_t lf = tdev == fdev ? lt : lf0;
-            s_mem[tdev][tid] = make_ulonglong2(lt, lt > tm.y ? lt : tm.y);
+            // a compute op frees on the device it allocated on (lf0 == tm.x)
+            const uint64_t lf = lf0 + (uint64_t)(is_c ? alloc : 0u);
+            s_mem[tdev][tid] = make_ulonglong2(lt, max_bits(lt, tm.y));
             suspect |= (uint64_t)fre > lf;
             s_mem[fdev][tid].x = lf - (uint64_t)fre;
         }
