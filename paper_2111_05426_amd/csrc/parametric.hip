@@ -521,16 +521,21 @@ __device__ __forceinline__ int64_t run_top(const ZSeg &g, int d, int D)
     return best;
 }
 
-// Net bytes (delta) and highest point (top) of a block of stage s, relative
-// to the live bytes at its start counted with the largest owned resident
-// (z.rmax): top = max over replicas d of owned(d) - rmax + the highest point
-// of d's own walk through the block.  n: units of the block; n_r: replayed
-// units (recomputation, backward).  Replicas owning nothing on the stage
-// all walk alike, so the owners of the stage's groups plus one of them are
-// enough.
+// Highest point of a block of stage s with ZeRO, relative to the live bytes
+// at its start counted with the largest owned resident (z.rmax): the maximum
+// over replicas d of owned(d) - rmax + the highest point of d's own walk
+// through the block's segments (edge ops, replayed units and the partial
+// unit under recomputation, units, edge ops).  n: units of the block; n_r:
+// replayed units.  The block's net bytes do not depend on ownership.
+//
+// A replica's walk never rises above that of a replica owning none of the
+// segments' groups (A), and reaches A unless it owns every unit at which A is
+// reached.  Those units have one owner at most (consecutive groups belong to
+// different replicas), so every other replica reaches A, the largest of them
+// holding the largest owned resident besides that owner's, and only the
+// owner's walk needs composing.
 template <bool TF>
-__device__ void zero_block(const Ctx &x, int s, const ZStage &z, bool bwd, uint64_t m, bool acc, int n, int n_r,
-                           int64_t &delta, int64_t &top)
+__device__ int64_t zero_top(const Ctx &x, int s, const ZStage &z, bool bwd, uint64_t m, bool acc, int n, int n_r)
 {
     ZSeg seg[5];
     int ns = 0;
@@ -569,25 +574,45 @@ __device__ void zero_block(const Ctx &x, int s, const ZStage &z, bool bwd, uint6
         seg[ns++] = ZSeg{n, u.cur, u.tn, u.to, z.gl_hi - 1, -1};
     }
     seg[ns++] = ZSeg{1, suf.cur, suf.tn, suf.to, g_suf, 1};
-    int64_t dl = 0;
-    for (int i = 0; i < ns; ++i) dl += seg[i].n > 0 ? (int64_t)seg[i].n * seg[i].d : 0;
-    const int g_lo = z.emb ? 0 : z.gl_lo, g_hi = z.head ? z.g_head + 1 : z.gl_hi;
-    const int n_own = (g_hi - g_lo) < x.D ? (g_hi - g_lo) : x.D;
-    const int n_cls = n_own + ((g_hi - g_lo) < x.D ? 1 : 0);
-    int64_t best = INT64_MIN;
-    for (int j = 0; j < n_cls; ++j) {
-        const int d = j < n_own ? (g_lo + j) % x.D : -1;
-        int64_t at = (d >= 0 ? (int64_t)z_owned(x, z, d) : 0) - (int64_t)z.rmax, t = INT64_MIN;
-        for (int i = 0; i < ns; ++i) {
-            if (seg[i].n <= 0) continue;
-            const int64_t v = at + run_top(seg[i], d, x.D);
-            t = v > t ? v : t;
-            at += (int64_t)seg[i].n * seg[i].d;
-        }
-        best = t > best ? t : best;
+    const int D = x.D;
+    // A, and the owner of the units at which it is reached
+    int64_t a_none = INT64_MIN, at = 0;
+    for (int i = 0; i < ns; ++i) {
+        if (seg[i].n <= 0) continue;
+        const int64_t v = at + run_top(seg[i], -1, D);
+        a_none = v > a_none ? v : a_none;
+        at += (int64_t)seg[i].n * seg[i].d;
     }
-    delta = dl;
-    top = best;
+    int owner = -1;
+    bool shared = false;   // reached where every replica reaches it
+    at = 0;
+    for (int i = 0; i < ns; ++i) {
+        if (seg[i].n <= 0) continue;
+        if (at + run_top(seg[i], -1, D) == a_none) {
+            if (seg[i].gs < 0 || (seg[i].d == 0 && seg[i].n >= 2)) {
+                shared = true;
+            } else {
+                int o = (seg[i].gs + seg[i].dir * (seg[i].d > 0 ? seg[i].n - 1 : 0)) % D;
+                if (o < 0) o += D;
+                shared = shared || (owner >= 0 && owner != o);
+                owner = o;
+            }
+        }
+        at += (int64_t)seg[i].n * seg[i].d;
+    }
+    if (shared || owner < 0) return a_none;
+    int64_t t_o = INT64_MIN;
+    at = 0;
+    for (int i = 0; i < ns; ++i) {
+        if (seg[i].n <= 0) continue;
+        const int64_t v = at + run_top(seg[i], owner, D);
+        t_o = v > t_o ? v : t_o;
+        at += (int64_t)seg[i].n * seg[i].d;
+    }
+    const int64_t rmax = (int64_t)z.rmax;
+    const int64_t others = (int64_t)(owner == z.arg ? z.rsec : z.rmax) - rmax + a_none;
+    const int64_t own = (int64_t)z_owned(x, z, owner) - rmax + t_o;
+    return others > own ? others : own;
 }
 
 // n repetitions of a unit of costs r: the same value as n * 2 * U2n
@@ -861,17 +886,16 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     int pos = 0, nf = 0, nb = 0, len = 0, mr = 0, n_f = 0, n_b = 0;
     constexpr bool rc = RC;   // the launch checks it against the model
     int n_r = 0, n_part = 0;                     // replayed units, entries of the partial unit
-    // ZeRO: memory summaries of the last forward / backward block kind
+    // ZeRO: the highest point of every block kind over the stage's replicas
     const bool zero_c = ZR && train && M.zero != 0 && st.D > 1;
-    int zk_f = -1, zk_b = -1;
-    int64_t zd_f = 0, zt_f = 0, zd_b = 0, zt_b = 0;
+    __shared__ int64_t s_ztop[ZR ? kKeys : 1][kLanes];
     if (live_stage) {
         Ctx x = {};
         make_ctx(M, g.c, st, x);
         x.mlp = !TF;   // the family is uniform per launch: compiles out the other
         uint64_t res0;
+        ZStage zs;
         if (ZR && x.zero) {
-            ZStage zs;
             z_stage(x, s, zs);
             res0 = resident_inputs(x, s) + zs.rmax;
         } else {
@@ -900,6 +924,16 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
             Count c{x, 0, 0};
             record_partial<TF>(x, 1, c);
             n_part = (int)c.walked;
+        }
+        if constexpr (ZR) {
+            if (zero_c) {
+                // all six kinds up front: every lane of the wavefront at once
+                for (int key = 0; key < kKeys; ++key) {
+                    const bool bwd = key >= 2;
+                    const int mc = bwd ? ((key - 2) & 1) : key;
+                    s_ztop[key][lane] = zero_top<TF>(x, s, zs, bwd, x.mq + (uint64_t)mc, key >= 4, bwd ? n_b : n_f, n_r);
+                }
+            }
         }
         uint64_t sz, fre;
         send_size(x, s, 1, false, sz, fre);
@@ -1124,28 +1158,8 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                 }
             }
             if constexpr (ZR) {
-                if (zero_c) {
-                    if ((bwd ? zk_b : zk_f) != key) {
-                        Ctx x = {};
-                        make_ctx(M, g.c, st, x);
-                        x.mlp = !TF;
-                        ZStage zs;
-                        z_stage(x, s, zs);
-                        int64_t zd, zt;
-                        zero_block<TF>(x, s, zs, bwd, m, acc, n, nr, zd, zt);
-                        if (bwd) {
-                            zk_b = key;
-                            zd_b = zd;
-                            zt_b = zt;
-                        } else {
-                            zk_f = key;
-                            zd_f = zd;
-                            zt_f = zt;
-                        }
-                    }
-                    delta = bwd ? zd_b : zd_f;
-                    top = bwd ? zt_b : zt_f;
-                }
+                // the net bytes do not depend on ownership; the highest point does
+                if (zero_c) top = s_ztop[key][lane];
             }
             const int64_t hi = live + top;
             peak = hi > peak ? hi : peak;
