@@ -174,12 +174,19 @@ def test_gpt3_grid_sampled(torch_gpu, orc, w):
     assert int(found.item()) == 16
     rng = np.random.default_rng(175)
     K = strat[:, 3]
-    pick = np.unique(np.concatenate([rng.choice(len(strat), 250, replace=False), top,
+    # the ZeRO oracle walks every data replica, so it samples fewer
+    n_pick = 100 if w.model.zero else 250
+    pick = np.unique(np.concatenate([rng.choice(len(strat), n_pick, replace=False), top,
                                      np.nonzero(K == K.max())[0][:5], np.nonzero(K == 1)[0][:5]]))
     print("%s: oracle on %d sampled candidates" % (w.name, len(pick)), flush=True)
     o = orc.run_strategies(w.model, strat[pick], w.device, slice=True, row_width=64, threads=8)
     sub = {k: (v[pick] if isinstance(v, np.ndarray) else v) for k, v in g.items()}
     compare(sub, o, strat[pick])
+    # the projection itself against the full program, where that is small
+    small = pick[np.nonzero(o["n_ops"] <= 300_000)[0]][:24]
+    assert len(small) >= 5
+    of = orc.run_strategies(w.model, strat[small], w.device, slice=False, row_width=64, threads=8)
+    compare({k: (v[small] if isinstance(v, np.ndarray) else v) for k, v in g.items()}, of, strat[small])
     # the selection is the ordered prefix of the feasible candidates
     mk_all, st, cp = g["makespan"], g["status"], g["cand_peak"].view(np.uint64)
     feas = np.nonzero((st == 0) & (cp <= w.device.mem_cap_bytes))[0]
