@@ -43,7 +43,8 @@ def build(force=True):
 class _Dev(C.Structure):
     _fields_ = [("flops_per_s", C.c_double), ("mem_bytes_per_s", C.c_double),
                 ("link_bytes_per_s", C.c_double), ("link_latency_s", C.c_double),
-                ("launch_s", C.c_double), ("mem_cap_bytes", C.c_uint64)]
+                ("launch_s", C.c_double), ("mem_cap_bytes", C.c_uint64),
+                ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double)]
 
 
 class _Model(C.Structure):
@@ -67,8 +68,10 @@ def lib():
 
 
 def _dev(d):
+    mm = getattr(d, "matmul", None)
     return _Dev(d.flops_per_s, d.mem_bytes_per_s, d.link_bytes_per_s, d.link_latency_s,
-                d.launch_s, int(d.mem_cap_bytes))
+                d.launch_s, int(d.mem_cap_bytes), 1 if mm is not None else 0,
+                *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))))
 
 
 def _model(m):
@@ -81,12 +84,19 @@ def _p(a):
     return a.ctypes.data_as(C.c_void_p) if a is not None else None
 
 
-def cost(dev, kind, flops, nbytes, n):
-    f = lib().or_cost
-    f.restype = C.c_double
-    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_double, C.c_double, C.c_int]
+def cost(dev, kind, flops, nbytes, n, type=None):
+    """Cost of one op; with an op type name (TYPES), matrix multiplications
+    take the device's empirical MatMul regression when it has one."""
     d = _dev(dev)
-    return f(C.byref(d), kind, float(flops), float(nbytes), int(n))
+    if type is None:
+        f = lib().or_cost
+        f.restype = C.c_double
+        f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_double, C.c_double, C.c_int]
+        return f(C.byref(d), kind, float(flops), float(nbytes), int(n))
+    f = lib().or_cost_typed
+    f.restype = C.c_double
+    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_int, C.c_double, C.c_double, C.c_int]
+    return f(C.byref(d), kind, TYPES.index(type), float(flops), float(nbytes), int(n))
 
 
 def gen_table(seed, cand, n_ops, n_dev):

@@ -77,6 +77,12 @@ enum {
 typedef struct {
     double flops_per_s, mem_bytes_per_s, link_bytes_per_s, link_latency_s, launch_s;
     uint64_t mem_cap_bytes;
+    /* Empirical MatMul cost (Sec. 4: MatMul gets a linear regression in its
+     * input sizes, fitted on single-op microbenchmarks): when mm_enabled,
+     * a matrix multiplication of `flops` flops touching `bytes` bytes costs
+     * (mm_c0 + mm_c1 * flops) + mm_c2 * bytes instead of the roofline. */
+    int32_t mm_enabled;
+    double mm_c0, mm_c1, mm_c2;
 } or_device_model;
 
 typedef struct {
@@ -129,6 +135,26 @@ static double cost_chain(const or_device_model *m, double bytes, int n)
     return (double)(n - 1) * m->link_latency_s + bytes * inv_l;
 }
 
+/* The op types that multiply two matrices: the dense layer's Gemm and its
+ * two gradients, the transformer's projections, MLP and LM-head products,
+ * the attention scores and P.V products, and their gradients. */
+static int is_matmul(int type)
+{
+    switch (type) {
+    case T_GEMM: case T_GEMMDW: case T_GEMMDX: case T_QKV: case T_SCORES: case T_AV: case T_OUTPROJ:
+    case T_FC1: case T_FC2: case T_LMHEAD: case T_AV_B: case T_SCORES_B:
+        return 1;
+    default:
+        return 0;
+    }
+}
+
+/* linear regression cost of a matrix multiplication (Sec. 4) */
+static double cost_matmul(const or_device_model *m, double flops, double bytes)
+{
+    return (m->mm_c0 + m->mm_c1 * flops) + m->mm_c2 * bytes;
+}
+
 double or_cost(const or_device_model *m, int kind, double flops, double bytes, int n)
 {
     if (kind == OR_COMPUTE) return cost_compute(m, flops, bytes);
@@ -137,10 +163,22 @@ double or_cost(const or_device_model *m, int kind, double flops, double bytes, i
     return cost_allreduce(m, bytes, n);
 }
 
+/* cost of an op of a given type: matrix multiplications take the empirical
+ * regression when the device model carries one */
+double or_cost_typed(const or_device_model *m, int kind, int type, double flops, double bytes, int n)
+{
+    if (kind == OR_COMPUTE && m->mm_enabled && is_matmul(type)) return cost_matmul(m, flops, bytes);
+    return or_cost(m, kind, flops, bytes, n);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Explicit op tables (at most 8 devices): one candidate, per-op amounts.    */
-/* code = kind | a << 8 | b_or_mask << 16; bits 24..31 must be zero; flops  */
-/* and bytes must be finite and >= 0 (costs are then never negative).       */
+/* code = kind | a << 8 | b_or_mask << 16 | cost class << 24; flops and     */
+/* bytes must be finite and >= 0 (costs are then never negative).  Cost     */
+/* class 0 is the model's own cost; class 1, on a compute op only, marks a  */
+/* matrix multiplication, which takes the empirical MatMul regression when  */
+/* the device model carries one (the roofline otherwise).  Any other class  */
+/* is invalid.                                                               */
 /* compute: runs on a, allocates and frees on a.                             */
 /* send a->b: runs on {a,b}, allocates on b, frees on a.                     */
 /* allreduce: runs on the devices of the mask; alloc/free fields ignored.    */
@@ -177,13 +215,14 @@ int or_sim_table(int64_t n_ops, int n_dev,
         int64_t o = j * stride;
         uint32_t c = code[o];
         int kind = (int)(c & 0xffu), a = (int)((c >> 8) & 0xffu), b = (int)((c >> 16) & 0xffu);
+        int cls = (int)(c >> 24);
         uint32_t mask;
         double start, end, cost;
         {
             uint32_t fb, bb;
             memcpy(&fb, &flops[o], 4);
             memcpy(&bb, &bytes[o], 4);
-            if ((c >> 24) != 0 || kind > 4 || fb >= 0x7f800000u || bb >= 0x7f800000u) {
+            if (cls > 1 || (cls == 1 && kind != OR_COMPUTE) || kind > 4 || fb >= 0x7f800000u || bb >= 0x7f800000u) {
                 st |= ST_BAD_OP;
                 continue;
             }
@@ -191,7 +230,8 @@ int or_sim_table(int64_t n_ops, int n_dev,
         if (kind == OR_COMPUTE) {
             if (a >= n_dev) { st |= ST_BAD_DEVICE; continue; }
             mask = 1u << a;
-            cost = cost_compute(m, (double)flops[o], (double)bytes[o]);
+            if (cls == 1 && m->mm_enabled) cost = cost_matmul(m, (double)flops[o], (double)bytes[o]);
+            else cost = cost_compute(m, (double)flops[o], (double)bytes[o]);
         } else if (kind == OR_SEND) {
             if (a >= n_dev || b >= n_dev) { st |= ST_BAD_DEVICE; continue; }
             if (a == b) { st |= ST_SELF_SEND; continue; }
@@ -545,7 +585,7 @@ static int prog_simulate(const or_prog *g, int n_dev, const or_device_model *m,
         double start = 0.0, end, cost;
         if (type_cost && type_cost[g->type[i]] >= 0.0) cost = type_cost[g->type[i]];
         else if (g->ocost[i] >= 0.0) cost = g->ocost[i];
-        else cost = or_cost(m, g->kind[i], g->flops[i], g->bytes[i], g->nsz[i]);
+        else cost = or_cost_typed(m, g->kind[i], g->type[i], g->flops[i], g->bytes[i], g->nsz[i]);
         for (q = g->dev_beg[i]; q < g->dev_beg[i + 1]; q++) {
             d = g->devs[q];
             if (d < 0 || d >= n_dev) { rc = -2; goto out; }

@@ -56,6 +56,9 @@ class DeviceSpec:
     link_latency_s: float = 5e-6
     launch_s: float = 5e-6
     mem_cap_bytes: int = 0
+    # (c0, c1, c2): matrix multiplications cost c0 + c1 * flops + c2 * bytes
+    # (an empirical regression fitted on microbenchmarks); None: the roofline
+    matmul: tuple = None
 
 
 @dataclass(frozen=True)

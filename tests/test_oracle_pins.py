@@ -865,9 +865,9 @@ def table_brute(tab, n_dev, dev, init=None):
     st = 0
     for c, fl, by, al, fr in zip(tab["code"], tab["flops"], tab["bytes"], tab["alloc"], tab["free"]):
         c = int(c)
-        k, a, b = c & 255, (c >> 8) & 255, (c >> 16) & 255
+        k, a, b, cls = c & 255, (c >> 8) & 255, (c >> 16) & 255, c >> 24
         fin = lambda x: math.isfinite(float(x)) and float(x) >= 0 and not math.copysign(1.0, float(x)) < 0
-        if c >> 24 or k > 4 or not fin(fl) or not fin(by):
+        if cls > 1 or (cls == 1 and k != 0) or k > 4 or not fin(fl) or not fin(by):
             st |= 1
             continue
         if k == 0:
@@ -875,8 +875,12 @@ def table_brute(tab, n_dev, dev, init=None):
                 st |= 2
                 continue
             devs = [a]
-            x, y = float(fl) * inv(dev.flops_per_s), float(by) * inv(dev.mem_bytes_per_s)
-            cost = dev.launch_s + max(x, y)
+            if cls == 1 and dev.matmul is not None:
+                c0, c1, c2 = dev.matmul
+                cost = (c0 + c1 * float(fl)) + c2 * float(by)
+            else:
+                x, y = float(fl) * inv(dev.flops_per_s), float(by) * inv(dev.mem_bytes_per_s)
+                cost = dev.launch_s + max(x, y)
         elif k == 1:
             if a >= n_dev or b >= n_dev:
                 st |= 2
@@ -946,6 +950,11 @@ def test_table_brute_force(orc, seed):
     mask_r = np.where(rng.random(n) < 0.8, mask | (1 << np.minimum(a, n_dev - 1)), mask)
     code = np.where(kind == 2, 2 | (mask << 16),
                     np.where(kind >= 3, kind | (a << 8) | (mask_r << 16), kind | (a << 8) | (b << 16))).astype(np.uint32)
+    if seed >= 20:
+        # cost classes: 1 (matrix multiplication) on compute ops, and a few
+        # invalid ones (2, or 1 on other kinds)
+        cls = np.where(kind == 0, rng.integers(0, 2, n), 0) | np.where(rng.random(n) < 0.05, rng.integers(1, 3, n), 0)
+        code = (code | (cls.astype(np.uint32) << 24)).astype(np.uint32)
     if seed % 7 == 0:
         code[0] = 7
     tab = dict(code=code, flops=rng.uniform(1e6, 1e12, n).astype(np.float32),
@@ -958,8 +967,9 @@ def test_table_brute_force(orc, seed):
         tab["flops"][rng.integers(0, n)] = np.float32(-0.0)
         tab["bytes"][rng.integers(0, n)] = np.float32(np.nan)
     init = rng.integers(0, 2000, n_dev).astype(np.uint64)
-    r = orc.sim_table(tab, n_dev, DEV, init_live=init)
-    clk, peak, st = table_brute(tab, n_dev, DEV, [int(v) for v in init])
+    dev = DEV if seed % 2 == 0 else replace(DEV, matmul=(3e-6, 1.3e-14, 2.1e-12))
+    r = orc.sim_table(tab, n_dev, dev, init_live=init)
+    clk, peak, st = table_brute(tab, n_dev, dev, [int(v) for v in init])
     assert list(r["finish"]) == clk
     assert [int(v) for v in r["peak"]] == peak
     assert r["status"] == st
@@ -979,6 +989,82 @@ def test_table_hand_trace(orc):
     # AR over 3: start 4.75, + 4*0.5 + (4/3)*(6/4) = 2 + 2 = 4 -> 8.75 everywhere
     assert list(r["finish"]) == [8.75, 8.75, 8.75]
     assert [int(v) for v in r["peak"]] == [5, 7, 9]
+
+
+# ---------------------------------------------------------------------------
+# Empirical MatMul cost (Sec. 4: a linear regression in the input sizes)
+# ---------------------------------------------------------------------------
+def test_matmul_regression_cost(orc):
+    """A matrix multiplication costs c0 + c1 * flops + c2 * bytes when the
+    device carries the regression; every other op, and every op without a
+    regression, keeps the roofline."""
+    c0, c1, c2 = 7e-6, 3.1e-15, 1.7e-12
+    dev = replace(DEV, matmul=(c0, c1, c2))
+    for fl, by in ((0.0, 0.0), (2e9, 3e6), (1e15, 1e3), (5.0, 7e11)):
+        roof = orc.cost(DEV, orc.COMPUTE, fl, by, 1)
+        for t in ("GEMM", "GEMMDW", "GEMMDX", "QKV", "SCORES", "AV", "OUTPROJ", "FC1", "FC2", "LMHEAD", "AV_B", "SCORES_B"):
+            assert orc.cost(dev, orc.COMPUTE, fl, by, 1, type=t) == (c0 + c1 * fl) + c2 * by
+            assert orc.cost(DEV, orc.COMPUTE, fl, by, 1, type=t) == roof
+        for t in ("RELU", "RELUGRAD", "LOSSGRAD", "ADDGRAD", "OPT", "SPLIT", "LN", "SOFTMAX", "RESADD", "GELU",
+                  "EMBED", "XENT_STATS", "XENT_GRAD", "LN_B", "RESADD_B", "GELU_B", "SOFTMAX_B", "EMBED_DW"):
+            assert orc.cost(dev, orc.COMPUTE, fl, by, 1, type=t) == roof
+
+
+@pytest.mark.parametrize("case", [(mlp(4, 256, 1024, 2, TRAIN_ADAM), [(1, 1, 1, 1), (2, 2, 2, 1), (4, 1, 2, 2)], "flops"),
+                                  (mlp(4, 8, 4096, 4, TRAIN_SGD), [(1, 1, 1, 1), (2, 2, 2, 2), (1, 1, 4, 4)], "bytes")])
+def test_matmul_regression_reduces_to_roofline(orc, case):
+    """With c = (launch, 1/F, 0) on matrix multiplications that are all
+    compute bound, or c = (launch, 0, 1/B) on ones that are all memory bound,
+    the regression is the roofline's value in the same rounding: every
+    output is identical."""
+    m, strats, bound = case
+    for D, H, P, K in strats:
+        c = (DEV.launch_s, 1.0 / DEV.flops_per_s, 0.0) if bound == "flops" else \
+            (DEV.launch_s, 0.0, 1.0 / DEV.mem_bytes_per_s)
+        a = orc.sim_strategy(m, D, H, P, K, DEV)
+        b = orc.sim_strategy(m, D, H, P, K, replace(DEV, matmul=c))
+        assert a["status"] == 0
+        assert a["makespan"] == b["makespan"] and np.array_equal(a["dev_finish"], b["dev_finish"])
+        assert np.array_equal(a["dev_peak"], b["dev_peak"]) and a["n_ops"] == b["n_ops"]
+
+
+@pytest.mark.parametrize("case", [(mlp(3, 64, 32, 4, TRAIN_SGD), 3 * 3), (mlp(5, 32, 16, 2, INFER), 5),
+                                  (transformer(2, 32, 4, 8, 64, 4, 2, TRAIN_ADAM), 16 * 2 + 3),
+                                  (transformer(3, 32, 2, 8, 50, 2, 2, INFER), 6 * 3 + 1)])
+def test_matmul_count_on_one_device(orc, case):
+    """Every matrix multiplication takes the regression: on one device
+    (a sequential program) with power-of-two costs, raising c0 by d raises
+    the makespan by exactly (number of matrix multiplications) * d -- per
+    MLP layer the Gemm, and in training its two gradients; per transformer
+    layer the QKV, score, P.V, output, fc1 and fc2 products, and in training
+    ten gradient products, plus the LM head (three in training)."""
+    m, n_mm = case
+    dev = DeviceSpec(2.0 ** 40, 2.0 ** 36, 2.0 ** 30, 2.0 ** -16, 2.0 ** -14, 0)
+    d = 2.0 ** -10
+    a = orc.sim_strategy(m, 1, 1, 1, 1, replace(dev, matmul=(2.0 ** -12, 2.0 ** -42, 2.0 ** -38)))
+    b = orc.sim_strategy(m, 1, 1, 1, 1, replace(dev, matmul=(2.0 ** -12 + d, 2.0 ** -42, 2.0 ** -38)))
+    assert b["makespan"] - a["makespan"] == n_mm * d
+
+
+def test_table_matmul_class(orc):
+    """Table records carry a cost class in their top byte: class 1 marks a
+    compute op as a matrix multiplication, which takes the regression when
+    the device has one and the roofline otherwise."""
+    c0, c1, c2 = 1e-5, 2e-14, 3e-12
+    tab = dict(code=np.array([0 | 1 << 24, 0, 0 | 1 << 8 | 1 << 24], np.uint32),
+               flops=np.array([4e9, 4e9, 1e3], np.float32), bytes=np.array([2e6, 2e6, 8e8], np.float32),
+               alloc=np.zeros(3, np.uint32), free=np.zeros(3, np.uint32))
+    r = orc.sim_table(tab, 2, replace(DEV, matmul=(c0, c1, c2)))
+    f, b = float(np.float32(4e9)), float(np.float32(2e6))
+    mm = (c0 + c1 * f) + c2 * b
+    roof = orc.cost(DEV, orc.COMPUTE, f, b, 1)
+    assert r["finish"][0] == mm + roof and r["status"] == 0
+    assert r["finish"][1] == (c0 + c1 * float(np.float32(1e3))) + c2 * float(np.float32(8e8))
+    plain = orc.sim_table(tab, 2, DEV)
+    assert plain["finish"][0] == roof + roof
+    for bad in (2 << 24, 1 | 1 << 8 | 1 << 24, 2 | 3 << 16 | 1 << 24):
+        t = dict(tab, code=np.array([bad, 0, 0], np.uint32))
+        assert orc.sim_table(t, 2, DEV)["status"] & 1
 
 
 def test_table_broadcast_reduce_hand_trace(orc):
