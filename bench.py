@@ -4,7 +4,7 @@
 
 NAME is random_tables (default) or one of the strategy grids (tiny_mlp,
 large_mlp, gpt2_small, gpt2_small_train, gpt3_175b, gpt3_175b_gpipe,
-gpt3_175b_recompute, gpt3_175b_zero); a grid's line times
+gpt3_175b_recompute, gpt3_175b_zero, gpt3_175b_mi355x); a grid's line times
 dsim_simulate_parametric + top-k over the whole grid.
 
 A step is one pass of the hot path over one batch of synthetic input, with the
@@ -145,7 +145,7 @@ def bench_random_tables(args, torch, dsim, W):
 
 
 PARAMETRIC = ("tiny_mlp", "large_mlp", "gpt2_small", "gpt2_small_train", "gpt3_175b", "gpt3_175b_gpipe",
-              "gpt3_175b_recompute", "gpt3_175b_zero")
+              "gpt3_175b_recompute", "gpt3_175b_zero", "gpt3_175b_mi355x")
 
 
 def bench_parametric(torch, dsim, W, reps, warmup=1):

@@ -81,10 +81,20 @@ DSIM_API const char *dsim_last_error(void);
  * coefficients are device DRAM bandwidth, kernel launch overhead, network
  * bandwidth; F is the device's flop rate, Sec. 3.3).  All five doubles must
  * be finite and > 0 (latency and launch may be 0).  mem_cap_bytes = 0 means
- * no cap; otherwise candidates whose peak exceeds it get DSIM_ST_OVER_CAP. */
+ * no cap; otherwise candidates whose peak exceeds it get DSIM_ST_OVER_CAP.
+ * mm_enabled = 1 gives matrix multiplications the empirical cost of Sec. 4
+ * (a linear regression in the input sizes, fitted on single-op
+ * microbenchmarks): (mm_c0 + mm_c1 * flops) + mm_c2 * bytes, coefficients
+ * finite and >= 0.  The transform's matrix multiplications are the dense
+ * layer's Gemm and its two gradients, the transformer's QKV, output, fc1,
+ * fc2 and LM-head products, the attention score and P.V products, and
+ * their gradients; in explicit tables, compute records of cost class 1.
+ * mm_enabled = 0: every compute op takes the roofline. */
 typedef struct {
     double flops_per_s, mem_bytes_per_s, link_bytes_per_s, link_latency_s, launch_s;
     uint64_t mem_cap_bytes;
+    int32_t mm_enabled;
+    double mm_c0, mm_c1, mm_c2;
 } dsim_device_model;
 
 /* The sequential program the transform distributes (Sec. 4, Sec. 5):
@@ -163,7 +173,11 @@ DSIM_API dsim_status dsim_create_grid(const dsim_model *model, const dsim_grid_s
 /*
  * Explicit op tables (device memory).  Structure of arrays, op-major,
  * candidate-fastest: the record of op j of candidate c is at j*n_cand + c.
- *   code:  kind | a << 8 | b_or_mask << 16, bits 24..31 zero.
+ *   code:  kind | a << 8 | b_or_mask << 16 | cost_class << 24.  Cost class
+ *          0: the op's own cost; 1 (compute records only): a matrix
+ *          multiplication, costed by the device model's MatMul regression
+ *          when it has one (the roofline otherwise); any other class, or
+ *          class 1 on another kind, makes the op invalid.
  *          kind 0 compute on device a; 1 send a -> b; 2 all-reduce over the
  *          devices set in the 8-bit mask; 3 broadcast from root a to the
  *          other devices of the mask; 4 reduce over the mask onto root a

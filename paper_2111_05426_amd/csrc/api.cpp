@@ -39,6 +39,10 @@ CostConsts make_consts(const dsim_device_model &m)
     c.lat = m.link_latency_s;
     c.launch = m.launch_s;
     c.cap = m.mem_cap_bytes;
+    c.mm = m.mm_enabled;
+    c.mm_c0 = m.mm_enabled ? m.mm_c0 : 0.0;
+    c.mm_c1 = m.mm_enabled ? m.mm_c1 : 0.0;
+    c.mm_c2 = m.mm_enabled ? m.mm_c2 : 0.0;
     c.ar_lat[0] = 0.0;
     c.ar_coef[0] = 0.0;
     for (int n = 1; n <= kMaxTableDev; ++n) {
@@ -59,6 +63,9 @@ static dsim_status check_device(const dsim_device_model *m)
         return fail(DSIM_EINVAL, "device rates must be finite and > 0");
     if (!finite_nonneg(m->link_latency_s) || !finite_nonneg(m->launch_s))
         return fail(DSIM_EINVAL, "latency and launch must be finite and >= 0");
+    if (m->mm_enabled != 0 && m->mm_enabled != 1) return fail(DSIM_EINVAL, "mm_enabled must be 0 or 1");
+    if (m->mm_enabled && (!finite_nonneg(m->mm_c0) || !finite_nonneg(m->mm_c1) || !finite_nonneg(m->mm_c2)))
+        return fail(DSIM_EINVAL, "MatMul regression coefficients must be finite and >= 0");
     return DSIM_OK;
 }
 

@@ -26,6 +26,8 @@ struct CostConsts {
     double lat;        // link latency
     double launch;     // per compute op
     uint64_t cap;      // memory cap, 0 = none
+    int32_t mm;        // matrix multiplications take the regression below
+    double mm_c0, mm_c1, mm_c2;
     double ar_lat[kMaxTableDev + 1];
     double ar_coef[kMaxTableDev + 1];
 };

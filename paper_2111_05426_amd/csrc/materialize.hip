@@ -67,14 +67,17 @@ struct Emit {
         }
         ++j;
     }
-    __device__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    __device__ void compute(uint32_t cls, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
     {
         for (int r = 0; r < x.D * x.H; ++r) {
             const uint64_t copy = (pend != 0 && r / x.H != pend_owner) ? pend : 0;
-            put((uint32_t)(base + r) << 8, fl, by, al, fr + copy);
+            put(((uint32_t)(base + r) << 8) | (cls << 24), fl, by, al, fr + copy);
         }
         pend = 0;
     }
+    __device__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { compute(0u, fl, by, al, fr); }
+    // a matrix multiplication: cost class 1 of the table format
+    __device__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { compute(1u, fl, by, al, fr); }
     // ZeRO: the owner's broadcast over the D replicas of each tensor rank
     // (kind 3, root = the owner: the others allocate their copy)
     __device__ void bcast(uint64_t by, int grp)

@@ -143,14 +143,22 @@ struct Walk {
     uint64_t walked, nops;
     const ZStage *z;
 
-    __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    __device__ __forceinline__ void op(double c, uint64_t al, uint64_t fr)
     {
-        clk = clk + cost_local(x, fl, by);
+        clk = clk + c;
         live += (int64_t)al;
         peak = live > peak ? live : peak;
         live -= (int64_t)fr;
         walked += 1;
         nops += x.mult_dev;
+    }
+    __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        op(cost_local(x, fl, by), al, fr);
+    }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        op(cost_mm(x, fl, by), al, fr);
     }
     __device__ __forceinline__ void ar_tp(uint64_t by)
     {
@@ -211,12 +219,20 @@ struct Record {
     {
         while (n < 2 * entries2) put(0.0);   // clock + 0.0 == clock
     }
-    __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    __device__ __forceinline__ void op(double c, uint64_t al, uint64_t fr)
     {
-        put(cost_local(x, fl, by));
+        put(c);
         const int64_t a = cur + (int64_t)al;
         top = a > top ? a : top;
         cur = a - (int64_t)fr;
+    }
+    __device__ __forceinline__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        op(cost_local(x, fl, by), al, fr);
+    }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    {
+        op(cost_mm(x, fl, by), al, fr);
     }
     __device__ __forceinline__ void ar_tp(uint64_t by)
     {
@@ -251,6 +267,7 @@ struct Mem {
         top = a > top ? a : top;
         cur = a - (int64_t)fr;
     }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { local(fl, by, al, fr); }
     __device__ __forceinline__ void ar_tp(uint64_t) {}
     __device__ __forceinline__ void ar_dp(uint64_t) {}
     __device__ __forceinline__ void bcast(uint64_t, int) {}
@@ -274,6 +291,7 @@ struct MemZ {
         cur = a - (int64_t)fr;
         pend = 0;
     }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { local(fl, by, al, fr); }
     __device__ __forceinline__ void ar_tp(uint64_t) {}
     __device__ __forceinline__ void ar_dp(uint64_t) {}
     __device__ __forceinline__ void bcast(uint64_t by, int)
@@ -420,6 +438,7 @@ struct Count {
         walked += 1;
         nops += x.mult_dev;
     }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { local(fl, by, al, fr); }
     __device__ __forceinline__ void ar_tp(uint64_t)
     {
         if (x.H <= 1) return;

@@ -28,11 +28,12 @@
 //
 // The kernel is bound by issue rate (about 100 vector instructions per op)
 // more than by HBM: it has a fast path for the ops every lane of a wavefront
-// has, which assumes valid compute, send and all-reduce ops (indices
-// clamped, so even an invalid op stays in bounds) and only tests whether
-// each op is one; a lane that meets an op it cannot vouch for (a free that
-// would underflow, a broadcast or reduce record), and every lane's ops past
-// the wavefront's common count, go through the exact per-op path below it.
+// has, which assumes valid compute, send and all-reduce ops of cost class 0
+// (indices clamped, so even an invalid op stays in bounds) and only tests
+// whether each op is one; a lane that meets an op it cannot vouch for (a
+// free that would underflow, a broadcast or reduce record, a matrix
+// multiplication record), and every lane's ops past the wavefront's common
+// count, go through the exact per-op path below it.
 #include "internal.h"
 
 namespace dsim {
@@ -103,10 +104,10 @@ __device__ __forceinline__ double bits_double(uint32_t lo, uint32_t hi)
 template <int ND>
 __device__ __forceinline__ uint32_t op_flags(uint32_t code, uint32_t flops_bits, uint32_t bytes_bits)
 {
-    const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
-    // kind, reserved bits, and flops/bytes finite and >= 0 (bit patterns
-    // below +inf)
-    if ((code >> 24) != 0u || kind > 4u || flops_bits >= 0x7f800000u || bytes_bits >= 0x7f800000u)
+    const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu, cls = code >> 24;
+    // kind, cost class (1 only on compute records), and flops/bytes finite
+    // and >= 0 (bit patterns below +inf)
+    if (cls > 1u || (cls == 1u && kind != 0u) || kind > 4u || flops_bits >= 0x7f800000u || bytes_bits >= 0x7f800000u)
         return DSIM_ST_BAD_OP;
     if (kind == 0u) return ia < (uint32_t)ND ? 0u : (uint32_t)DSIM_ST_BAD_DEVICE;
     if (kind == 1u) {
@@ -319,7 +320,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
         const uint32_t m = kind == 0u ? (1u << ia) : (kind == 1u ? ((1u << ia) | (1u << ib)) : ib);
         const double f = (double)flf, b = (double)byf;
         double cost;
-        if (kind == 0u) {
+        if (kind == 0u && (code >> 24) == 1u && a.c.mm) {
+            // a matrix multiplication: the empirical regression of Sec. 4
+            cost = (a.c.mm_c0 + a.c.mm_c1 * f) + a.c.mm_c2 * b;
+        } else if (kind == 0u) {
             const double tf = f * inv_f, tb = b * inv_b;
             cost = launch + (tf > tb ? tf : tb);
         } else if (kind == 1u) {

@@ -116,5 +116,17 @@ GPT3_175B_RECOMPUTE = replace(GPT3_175B, name="gpt3_175b_recompute", model=repla
 # the same grid with ZeRO partitioning of weights, gradients and optimizer state
 GPT3_175B_ZERO = replace(GPT3_175B, name="gpt3_175b_zero", model=replace(GPT3_175B.model, zero=1))
 
+# A cluster of MI355X: fp16 matrix multiplications take the regression fitted
+# on this GPU by `python -m paper_2111_05426_amd.calibrate --dtype fp16`
+# (c0 = per-product dispatch, 1/c1 = 1.49 PFLOP/s, 1/c2 = 5.7 TB/s); other
+# compute ops the roofline with F = 1/c1, the bandwidth of a 4 GiB
+# device-to-device copy measured on the same GPU (4.94 TB/s, read + write)
+# and the same dispatch cost; links are one xGMI link's 153 GB/s with 5 us
+# latency (specification values: a single GPU cannot measure them); 288 GB
+# of HBM per device.
+MI355X = DeviceSpec(flops_per_s=1.493e15, mem_bytes_per_s=4.94e12, link_bytes_per_s=153e9, link_latency_s=5e-6,
+                    launch_s=1.557e-5, mem_cap_bytes=288_000_000_000, matmul=(1.557e-5, 6.699e-16, 1.743e-13))
+GPT3_175B_MI355X = replace(GPT3_175B, name="gpt3_175b_mi355x", device=MI355X)
+
 ALL = {w.name: w for w in (TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN, RANDOM_TABLES, GPT3_175B,
-                           GPT3_175B_GPIPE, GPT3_175B_RECOMPUTE, GPT3_175B_ZERO)}
+                           GPT3_175B_GPIPE, GPT3_175B_RECOMPUTE, GPT3_175B_ZERO, GPT3_175B_MI355X)}

@@ -106,6 +106,7 @@ CASES = [
     ("tf_gpipe_recompute", transformer(5, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, schedule=SCHED_GPIPE, recompute=1),
      all_strats([1, 2], [1, 2], [1, 2, 3], [1, 3], 8)),
 ]
+MM = (6.1e-6, 2.3e-14, 7.7e-13)   # empirical MatMul cost: matrix multiplications are class-1 records
 
 
 ZERO_CASES = [
@@ -145,10 +146,11 @@ def test_zero_programs_as_tables(torch_gpu, orc, case):
     assert differ > 0   # the replicas really differ somewhere
 
 
+@pytest.mark.parametrize("mm", [False, True], ids=["roofline", "matmul"])
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_small_programs_as_tables(torch_gpu, orc, case):
+def test_small_programs_as_tables(torch_gpu, orc, case, mm):
     name, model, strat = case
-    dev = DeviceSpec(mem_cap_bytes=10 ** 6)
+    dev = DeviceSpec(mem_cap_bytes=10 ** 6, matmul=MM if mm else None)
     o = orc.run_strategies(model, strat, dev, slice=False, row_width=int(strat[:, 2].max()), threads=8)
     assert np.any(o["status"] == 0)
     g = materialize_and_simulate(torch_gpu, model, strat, dev, 8, int(o["n_ops"].max()))

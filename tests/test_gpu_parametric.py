@@ -120,6 +120,25 @@ def test_small_models_vs_full_program(torch_gpu, orc, case):
     compare(g, o, strat)
 
 
+# empirical MatMul costs: random regression coefficients (and ones that make
+# matrix multiplications cheap or dominant) on models of every family/mode
+MM_DEVICES = [DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(6.1e-6, 2.3e-14, 7.7e-13)),
+              DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(0.0, 3.3e-16, 0.0)),
+              DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(2.0e-4, 1.9e-12, 4.1e-10))]
+MM_CASES = [SMALL[0], SMALL[1], SMALL[3], SMALL[4], SMALL[6], SMALL[10], SMALL[13], SMALL[16], SMALL[19]]
+
+
+@pytest.mark.parametrize("dev", range(len(MM_DEVICES)))
+@pytest.mark.parametrize("case", range(len(MM_CASES)), ids=[c[0] for c in MM_CASES])
+def test_matmul_regression_vs_full_program(torch_gpu, orc, case, dev):
+    name, model, strat = MM_CASES[case]
+    d = MM_DEVICES[dev]
+    g = run_gpu(torch_gpu, model, strat, d)
+    o = orc.run_strategies(model, strat, d, slice=False, row_width=g["finish"].shape[1], threads=8)
+    assert np.any(o["status"] == 0)
+    compare(g, o, strat)
+
+
 GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(LARGE_MLP, name="large_mlp_mixed", model=replace(LARGE_MLP.model, mode=TRAIN_ADAM_MIXED)),
          replace(LARGE_MLP, name="large_mlp_gpipe", model=replace(LARGE_MLP.model, schedule=SCHED_GPIPE)),
@@ -128,7 +147,10 @@ GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(LARGE_MLP, name="large_mlp_recompute", model=replace(LARGE_MLP.model, recompute=1)),
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_recompute", model=replace(GPT2_SMALL_TRAIN.model, recompute=1)),
          replace(LARGE_MLP, name="large_mlp_zero", model=replace(LARGE_MLP.model, zero=1)),
-         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_zero", model=replace(GPT2_SMALL_TRAIN.model, zero=1))]
+         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_zero", model=replace(GPT2_SMALL_TRAIN.model, zero=1)),
+         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_matmul",
+                 device=replace(GPT2_SMALL_TRAIN.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13))),
+         replace(LARGE_MLP, name="large_mlp_matmul", device=replace(LARGE_MLP.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13)))]
 
 
 @pytest.mark.parametrize("w", GRIDS, ids=[w.name for w in GRIDS])
@@ -155,8 +177,8 @@ def test_workload_grid_vs_oracle(torch_gpu, orc, w):
     assert int(found.item()) == rf and np.array_equal(idx.cpu().numpy(), ri)
 
 
-@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"], ALL["gpt3_175b_zero"]],
-                         ids=["1f1b", "recompute", "zero"])
+@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"], ALL["gpt3_175b_zero"], ALL["gpt3_175b_mi355x"]],
+                         ids=["1f1b", "recompute", "zero", "mi355x_calibrated"])
 def test_gpt3_grid_sampled(torch_gpu, orc, w):
     """The GPT-3-shaped grid at full size (39,965 strategies, the launch
     configuration the benchmark times, the 288e9-byte cap, top-16): a seeded

@@ -30,7 +30,7 @@ def assert_times(gpu, ref):
     assert np.array_equal(gpu, ref), "times agree to 1e-12 but not bit for bit"
 
 
-def random_tables(rng, n_cand, max_ops, n_dev, bad=False, rooted=False):
+def random_tables(rng, n_cand, max_ops, n_dev, bad=False, rooted=False, classes=False):
     """Seeded synthetic tables with every op kind; bad=True also plants
     invalid ops and frees larger than the live bytes; rooted=True adds
     broadcast and reduce records (their masks hold the root)."""
@@ -43,6 +43,8 @@ def random_tables(rng, n_cand, max_ops, n_dev, bad=False, rooted=False):
     mask = rng.integers(1, 1 << n_dev, (max_ops, n_cand)).astype(np.uint32)
     code = np.where(kind == 2, 2 | (mask << 16), kind | (a << 8) | (b << 16)).astype(np.uint32)
     code = np.where(kind >= 3, kind | (a << 8) | ((mask | (1 << a)) << 16), code).astype(np.uint32)
+    if classes:   # matrix multiplication records (cost class 1) among the compute ops
+        code = np.where((kind == 0) & (rng.random((max_ops, n_cand)) < 0.5), code | (1 << 24), code).astype(np.uint32)
     if n_dev == 1:
         code = np.where(kind == 1, 0, code).astype(np.uint32)
     alloc = rng.integers(0, 5000, (max_ops, n_cand)).astype(np.uint32)
@@ -83,17 +85,18 @@ def results_np(r):
     return out
 
 
-@pytest.mark.parametrize("rooted", [False, True], ids=["plain", "bcast_reduce"])
+@pytest.mark.parametrize("kinds", ["plain", "bcast_reduce", "matmul"])
 @pytest.mark.parametrize("n_dev", [1, 2, 3, 5, 8])
 @pytest.mark.parametrize("bad", [False, True])
-def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, rooted):
+def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, kinds):
     from paper_2111_05426_amd import dsim
     from paper_2111_05426_amd.workloads import DeviceSpec
     torch = torch_gpu
-    rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted)
+    rooted, classes = kinds == "bcast_reduce", kinds == "matmul"
+    rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted + 211 * classes)
     n_cand, max_ops = 777, 301   # several 256-lane blocks and a ragged tail
-    t = random_tables(rng, n_cand, max_ops, n_dev, bad, rooted)
-    dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5)
+    t = random_tables(rng, n_cand, max_ops, n_dev, bad, rooted, classes)
+    dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5, matmul=(4.5e-6, 9.1e-15, 1.3e-12) if classes else None)
     g = to_gpu(torch, t)
     init = torch.from_numpy(t["init"].view(np.int64)).cuda()
     rw = n_dev + 2
