@@ -44,7 +44,8 @@ class _Dev(C.Structure):
     _fields_ = [("flops_per_s", C.c_double), ("mem_bytes_per_s", C.c_double),
                 ("link_bytes_per_s", C.c_double), ("link_latency_s", C.c_double),
                 ("launch_s", C.c_double), ("mem_cap_bytes", C.c_uint64),
-                ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double)]
+                ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double),
+                ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double)]
 
 
 class _Model(C.Structure):
@@ -69,9 +70,11 @@ def lib():
 
 def _dev(d):
     mm = getattr(d, "matmul", None)
+    net = getattr(d, "network", None)
     return _Dev(d.flops_per_s, d.mem_bytes_per_s, d.link_bytes_per_s, d.link_latency_s,
                 d.launch_s, int(d.mem_cap_bytes), 1 if mm is not None else 0,
-                *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))))
+                *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))),
+                *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)))
 
 
 def _model(m):
@@ -95,8 +98,17 @@ def cost(dev, kind, flops, nbytes, n, type=None):
         return f(C.byref(d), kind, float(flops), float(nbytes), int(n))
     f = lib().or_cost_typed
     f.restype = C.c_double
-    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_int, C.c_double, C.c_double, C.c_int]
-    return f(C.byref(d), kind, TYPES.index(type), float(flops), float(nbytes), int(n))
+    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_int, C.c_double, C.c_double, C.c_int, C.c_int]
+    return f(C.byref(d), kind, TYPES.index(type), float(flops), float(nbytes), int(n), 0)
+
+
+def cost_between_nodes(dev, kind, nbytes, n):
+    """Cost of a communication op whose devices lie in more than one node."""
+    d = _dev(dev)
+    f = lib().or_cost_spans
+    f.restype = C.c_double
+    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_double, C.c_double, C.c_int, C.c_int]
+    return f(C.byref(d), kind, 0.0, float(nbytes), int(n), 1)
 
 
 def gen_table(seed, cand, n_ops, n_dev):

@@ -83,6 +83,15 @@ typedef struct {
      * (mm_c0 + mm_c1 * flops) + mm_c2 * bytes instead of the roofline. */
     int32_t mm_enabled;
     double mm_c0, mm_c1, mm_c2;
+    /* Two-tier interconnect (hardware topologies, Sec. 1; the paper models
+     * communication by network bandwidth coefficients, Sec. 4): with
+     * node_size > 0, device d lies in node d / node_size, and a send or
+     * collective whose devices lie in more than one node crosses the
+     * network (net_bytes_per_s, net_latency_s) instead of the node's links
+     * (link_bytes_per_s, link_latency_s).  node_size = 0: one uniform
+     * interconnect. */
+    int32_t node_size;
+    double net_bytes_per_s, net_latency_s;
 } or_device_model;
 
 typedef struct {
@@ -106,20 +115,31 @@ static double cost_compute(const or_device_model *m, double flops, double bytes)
     return m->launch_s + (tf > tb ? tf : tb);
 }
 
-static double cost_send(const or_device_model *m, double bytes)
+/* the link a communication op crosses: the network when its devices span
+ * more than one node, the node's own links otherwise */
+static double link_lat(const or_device_model *m, int spans)
 {
-    double inv_l = 1.0 / m->link_bytes_per_s;
-    return m->link_latency_s + bytes * inv_l;
+    return spans && m->node_size > 0 ? m->net_latency_s : m->link_latency_s;
+}
+static double link_bw(const or_device_model *m, int spans)
+{
+    return spans && m->node_size > 0 ? m->net_bytes_per_s : m->link_bytes_per_s;
 }
 
-static double cost_allreduce(const or_device_model *m, double bytes, int n)
+static double cost_send(const or_device_model *m, double bytes, int spans)
+{
+    double inv_l = 1.0 / link_bw(m, spans);
+    return link_lat(m, spans) + bytes * inv_l;
+}
+
+static double cost_allreduce(const or_device_model *m, double bytes, int n, int spans)
 {
     double inv_l, a, two_a;
     if (n <= 1) return 0.0;
-    inv_l = 1.0 / m->link_bytes_per_s;
+    inv_l = 1.0 / link_bw(m, spans);
     a = (double)(n - 1);
     two_a = 2.0 * a;
-    return two_a * m->link_latency_s + (two_a / (double)n) * (bytes * inv_l);
+    return two_a * link_lat(m, spans) + (two_a / (double)n) * (bytes * inv_l);
 }
 
 /* Broadcast from one member of a group to the others, and reduce of the
@@ -127,12 +147,30 @@ static double cost_allreduce(const or_device_model *m, double bytes, int n)
  * reduction of Fig. 9): a pipelined chain, (n-1) link latencies plus the
  * bytes crossing one link once.  With two devices this is the Send of
  * Sec. 2.1 / Fig. 9; one device costs nothing. */
-static double cost_chain(const or_device_model *m, double bytes, int n)
+static double cost_chain(const or_device_model *m, double bytes, int n, int spans)
 {
     double inv_l;
     if (n <= 1) return 0.0;
-    inv_l = 1.0 / m->link_bytes_per_s;
-    return (double)(n - 1) * m->link_latency_s + bytes * inv_l;
+    inv_l = 1.0 / link_bw(m, spans);
+    return (double)(n - 1) * link_lat(m, spans) + bytes * inv_l;
+}
+
+/* whether devices lie in more than one node (always 0 without nodes) */
+static int spans_nodes(const or_device_model *m, const int32_t *devs, int64_t n)
+{
+    int64_t q;
+    if (m->node_size <= 0 || n < 2) return 0;
+    for (q = 1; q < n; q++)
+        if (devs[q] / m->node_size != devs[0] / m->node_size) return 1;
+    return 0;
+}
+static int mask_spans_nodes(const or_device_model *m, uint32_t mask)
+{
+    int32_t devs[32];
+    int n = 0, d;
+    for (d = 0; d < 32; d++)
+        if (mask & (1u << d)) devs[n++] = d;
+    return spans_nodes(m, devs, n);
 }
 
 /* The op types that multiply two matrices: the dense layer's Gemm and its
@@ -155,20 +193,26 @@ static double cost_matmul(const or_device_model *m, double flops, double bytes)
     return (m->mm_c0 + m->mm_c1 * flops) + m->mm_c2 * bytes;
 }
 
-double or_cost(const or_device_model *m, int kind, double flops, double bytes, int n)
+/* cost of an op; spans: its devices lie in more than one node */
+double or_cost_spans(const or_device_model *m, int kind, double flops, double bytes, int n, int spans)
 {
     if (kind == OR_COMPUTE) return cost_compute(m, flops, bytes);
-    if (kind == OR_SEND) return cost_send(m, bytes);
-    if (kind == OR_BCAST || kind == OR_REDUCE) return cost_chain(m, bytes, n);
-    return cost_allreduce(m, bytes, n);
+    if (kind == OR_SEND) return cost_send(m, bytes, spans);
+    if (kind == OR_BCAST || kind == OR_REDUCE) return cost_chain(m, bytes, n, spans);
+    return cost_allreduce(m, bytes, n, spans);
+}
+
+double or_cost(const or_device_model *m, int kind, double flops, double bytes, int n)
+{
+    return or_cost_spans(m, kind, flops, bytes, n, 0);
 }
 
 /* cost of an op of a given type: matrix multiplications take the empirical
  * regression when the device model carries one */
-double or_cost_typed(const or_device_model *m, int kind, int type, double flops, double bytes, int n)
+double or_cost_typed(const or_device_model *m, int kind, int type, double flops, double bytes, int n, int spans)
 {
     if (kind == OR_COMPUTE && m->mm_enabled && is_matmul(type)) return cost_matmul(m, flops, bytes);
-    return or_cost(m, kind, flops, bytes, n);
+    return or_cost_spans(m, kind, flops, bytes, n, spans);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -236,19 +280,19 @@ int or_sim_table(int64_t n_ops, int n_dev,
             if (a >= n_dev || b >= n_dev) { st |= ST_BAD_DEVICE; continue; }
             if (a == b) { st |= ST_SELF_SEND; continue; }
             mask = (1u << a) | (1u << b);
-            cost = cost_send(m, (double)bytes[o]);
+            cost = cost_send(m, (double)bytes[o], mask_spans_nodes(m, mask));
         } else if (kind == OR_ALLREDUCE) {
             int n = 0;
             mask = (uint32_t)b;
             if (mask == 0 || (mask >> n_dev) != 0) { st |= ST_BAD_DEVICE; continue; }
             for (d = 0; d < n_dev; d++) if (mask & (1u << d)) n++;
-            cost = cost_allreduce(m, (double)bytes[o], n);
+            cost = cost_allreduce(m, (double)bytes[o], n, mask_spans_nodes(m, mask));
         } else {
             int n = 0;
             mask = (uint32_t)b;
             if (a >= n_dev || (mask >> n_dev) != 0 || !(mask & (1u << a))) { st |= ST_BAD_DEVICE; continue; }
             for (d = 0; d < n_dev; d++) if (mask & (1u << d)) n++;
-            cost = cost_chain(m, (double)bytes[o], n);
+            cost = cost_chain(m, (double)bytes[o], n, mask_spans_nodes(m, mask));
         }
         start = 0.0;
         for (d = 0; d < n_dev; d++)
@@ -585,7 +629,8 @@ static int prog_simulate(const or_prog *g, int n_dev, const or_device_model *m,
         double start = 0.0, end, cost;
         if (type_cost && type_cost[g->type[i]] >= 0.0) cost = type_cost[g->type[i]];
         else if (g->ocost[i] >= 0.0) cost = g->ocost[i];
-        else cost = or_cost_typed(m, g->kind[i], g->type[i], g->flops[i], g->bytes[i], g->nsz[i]);
+        else cost = or_cost_typed(m, g->kind[i], g->type[i], g->flops[i], g->bytes[i], g->nsz[i],
+                                  spans_nodes(m, g->devs + g->dev_beg[i], g->dev_beg[i + 1] - g->dev_beg[i]));
         for (q = g->dev_beg[i]; q < g->dev_beg[i + 1]; q++) {
             d = g->devs[q];
             if (d < 0 || d >= n_dev) { rc = -2; goto out; }
@@ -1450,6 +1495,16 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     uint64_t *pk = NULL;
     memset(res, 0, sizeof *res);
     if (strategy_invalid(M, D, H, P, K)) { res->status = ST_BAD_STRATEGY; return 0; }
+    if (dm->node_size > 0) {
+        /* nodes must cut every tensor-parallel group, data-parallel group
+         * and stage alike: node_size and D*H, and node_size and H, divide
+         * one another (always so for powers of two) */
+        int G = dm->node_size, DH = D * H;
+        if (!(G % DH == 0 || DH % G == 0) || !(G % H == 0 || H % G == 0)) {
+            res->status = ST_BAD_STRATEGY;
+            return 0;
+        }
+    }
     if ((int64_t)D * H > 1024 || K > 4096) return -1;
     memset(&x, 0, sizeof x);
     prog_init(&g);

@@ -59,6 +59,10 @@ class DeviceSpec:
     # (c0, c1, c2): matrix multiplications cost c0 + c1 * flops + c2 * bytes
     # (an empirical regression fitted on microbenchmarks); None: the roofline
     matmul: tuple = None
+    # (node_size, bytes/s, latency s): devices d lie in node d // node_size,
+    # and sends and collectives spanning nodes cross this network link;
+    # None: one uniform interconnect
+    network: tuple = None
 
 
 @dataclass(frozen=True)

@@ -857,6 +857,15 @@ def test_bounds(orc, case):
 # ---------------------------------------------------------------------------
 # Explicit tables: brute force on small random tables (incl. invalid ops)
 # ---------------------------------------------------------------------------
+def link(dev, devs):
+    """(latency, bandwidth) of the link a communication op crosses: the
+    network when its devices lie in more than one node."""
+    net = dev.network
+    if net is not None and net[0] > 0 and len({d // net[0] for d in devs}) > 1:
+        return net[2], net[1]
+    return dev.link_latency_s, dev.link_bytes_per_s
+
+
 def table_brute(tab, n_dev, dev, init=None):
     inv = lambda v: 1.0 / v
     clk = [0.0] * n_dev
@@ -889,15 +898,16 @@ def table_brute(tab, n_dev, dev, init=None):
                 st |= 4
                 continue
             devs = [a, b]
-            cost = dev.link_latency_s + float(by) * inv(dev.link_bytes_per_s)
+            lat, bw = link(dev, devs)
+            cost = lat + float(by) * inv(bw)
         elif k == 2:
             if b == 0 or b >> n_dev:
                 st |= 2
                 continue
             devs = [d for d in range(n_dev) if b >> d & 1]
             n = len(devs)
-            cost = 0.0 if n == 1 else 2.0 * (n - 1) * dev.link_latency_s + \
-                (2.0 * (n - 1) / n) * (float(by) * inv(dev.link_bytes_per_s))
+            lat, bw = link(dev, devs)
+            cost = 0.0 if n == 1 else 2.0 * (n - 1) * lat + (2.0 * (n - 1) / n) * (float(by) * inv(bw))
         else:
             # broadcast from / reduce onto a over the mask b: a chain of n - 1
             # hops, the bytes crossing one link once
@@ -906,7 +916,8 @@ def table_brute(tab, n_dev, dev, init=None):
                 continue
             devs = [d for d in range(n_dev) if b >> d & 1]
             n = len(devs)
-            cost = 0.0 if n == 1 else float(n - 1) * dev.link_latency_s + float(by) * inv(dev.link_bytes_per_s)
+            lat, bw = link(dev, devs)
+            cost = 0.0 if n == 1 else float(n - 1) * lat + float(by) * inv(bw)
         s = max(clk[d] for d in devs)
         for d in devs:
             clk[d] = s + cost
@@ -968,6 +979,8 @@ def test_table_brute_force(orc, seed):
         tab["bytes"][rng.integers(0, n)] = np.float32(np.nan)
     init = rng.integers(0, 2000, n_dev).astype(np.uint64)
     dev = DEV if seed % 2 == 0 else replace(DEV, matmul=(3e-6, 1.3e-14, 2.1e-12))
+    if seed % 3 == 1:
+        dev = replace(dev, network=(int(rng.integers(1, 5)), 3.1e9, 1.7e-5))
     r = orc.sim_table(tab, n_dev, dev, init_live=init)
     clk, peak, st = table_brute(tab, n_dev, dev, [int(v) for v in init])
     assert list(r["finish"]) == clk
@@ -1065,6 +1078,88 @@ def test_table_matmul_class(orc):
     for bad in (2 << 24, 1 | 1 << 8 | 1 << 24, 2 | 3 << 16 | 1 << 24):
         t = dict(tab, code=np.array([bad, 0, 0], np.uint32))
         assert orc.sim_table(t, 2, DEV)["status"] & 1
+
+
+# ---------------------------------------------------------------------------
+# Two-tier interconnect: nodes of node_size devices, a network between them
+# ---------------------------------------------------------------------------
+NET = (7e9, 2.2e-5)   # network bytes/s and latency, slower than the node links
+
+
+def test_network_is_used_only_across_nodes(orc):
+    """Everything in one node, or a network that is the node link, changes
+    nothing; every device in its own node is the flat model with the
+    network's constants."""
+    cases = [(mlp(4, 64, 48, 4, TRAIN_ADAM), 2, 2, 2, 3), (transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM_MIXED), 2, 2, 2, 2),
+             (mlp(6, 64, 48, 2, TRAIN_SGD, zero=1), 2, 1, 3, 2)]
+    for m, D, H, P, K in cases:
+        flat = orc.sim_strategy(m, D, H, P, K, DEV)
+        one = orc.sim_strategy(m, D, H, P, K, replace(DEV, network=(D * H * P, *NET)))
+        same = orc.sim_strategy(m, D, H, P, K, replace(DEV, network=(1, DEV.link_bytes_per_s, DEV.link_latency_s)))
+        every = orc.sim_strategy(m, D, H, P, K, replace(DEV, network=(1, *NET)))
+        slow = orc.sim_strategy(m, D, H, P, K, replace(DEV, link_bytes_per_s=NET[0], link_latency_s=NET[1]))
+        for r in (one, same):
+            assert r["makespan"] == flat["makespan"] and np.array_equal(r["dev_finish"], flat["dev_finish"])
+        assert every["makespan"] == slow["makespan"] and np.array_equal(every["dev_finish"], slow["dev_finish"])
+        assert np.array_equal(every["dev_peak"], flat["dev_peak"])
+        assert flat["makespan"] < every["makespan"]
+
+
+@pytest.mark.parametrize("L", [2, 4, 6])
+def test_network_tensor_groups_stay_in_node(orc, L):
+    """Nodes of H devices hold the tensor-parallel groups: with latency-only
+    communication (bandwidths so large the byte terms round away) and free
+    compute, D = H = 2, P = K = 1, the MLP's L - 1 tensor-parallel
+    all-reduces (L/2 forward, L/2 - 1 backward) cost 2*lat_node each and its
+    L gradient all-reduces cross the network at 2*lat_net each."""
+    m = mlp(L, 64, 16, 4, TRAIN_SGD)
+    lat, lat_net = 2.0 ** -12, 2.0 ** -6
+    base = DeviceSpec(2.0 ** 40, 2.0 ** 36, 2.0 ** 200, lat, 0.0, 0)
+    cost = {k: 0.0 for k in orc.TYPES if k not in ("AR_TP", "AR_DP")}
+    r = orc.sim_strategy(m, 2, 2, 1, 1, replace(base, network=(2, 2.0 ** 200, lat_net)), type_cost=cost)
+    assert r["makespan"] == (L - 1) * 2 * lat + L * 2 * lat_net
+    r = orc.sim_strategy(m, 2, 2, 1, 1, replace(base, network=(1, 2.0 ** 200, lat_net)), type_cost=cost)
+    assert r["makespan"] == (L - 1) * 2 * lat_net + L * 2 * lat_net
+
+
+def test_network_pipeline_sends_cross_nodes(orc):
+    """Nodes of D*H devices hold one stage each: every Send between stages
+    crosses the network and nothing else does (latency-only communication,
+    free compute; forward pipeline of P = 2 stages, K microbatches: the
+    K sends are the only cost.)"""
+    m = mlp(4, 64, 16, 4, INFER)
+    lat, lat_net = 2.0 ** -12, 2.0 ** -6
+    base = DeviceSpec(2.0 ** 40, 2.0 ** 36, 2.0 ** 200, lat, 0.0, 0)
+    cost = {k: 0.0 for k in orc.TYPES if k not in ("SEND_F", "SEND_B")}
+    for K in (1, 2, 4):
+        r = orc.sim_strategy(m, 1, 1, 2, K, replace(base, network=(1, 2.0 ** 200, lat_net)), type_cost=cost)
+        assert r["makespan"] == K * lat_net
+        r = orc.sim_strategy(m, 1, 1, 2, K, replace(base, network=(2, 2.0 ** 200, lat_net)), type_cost=cost)
+        assert r["makespan"] == K * lat
+
+
+def test_network_placement_must_be_uniform(orc):
+    """Nodes must cut every tensor group, data group and stage alike
+    (node_size and D*H, node_size and H divide one another)."""
+    m = mlp(4, 64, 48, 4, TRAIN_ADAM)
+    for (D, H, G), ok in (((2, 2, 3), False), ((3, 1, 2), False), ((2, 2, 8), True), ((2, 4, 2), True),
+                          ((4, 2, 8), True), ((2, 2, 1), True), ((3, 2, 6), True), ((3, 2, 4), False)):
+        r = orc.sim_strategy(m, D, H, 2, 1, replace(DEV, network=(G, *NET)))
+        assert (r["status"] == 0) == ok, (D, H, G)
+
+
+def test_table_network_hand_trace(orc):
+    """Four devices in nodes of two: a send inside node 0, a send from node
+    0 to node 1, an all-reduce inside node 1 and one over all four."""
+    dev = DeviceSpec(1.0, 1.0, 4.0, 0.5, 0.25, 0, network=(2, 2.0, 1.5))
+    code = np.array([1 | 0 << 8 | 1 << 16, 1 | 1 << 8 | 2 << 16, 2 | 0b1100 << 16, 2 | 0b1111 << 16], np.uint32)
+    tab = dict(code=code, flops=np.zeros(4, np.float32), bytes=np.array([8, 8, 8, 8], np.float32),
+               alloc=np.zeros(4, np.uint32), free=np.zeros(4, np.uint32))
+    r = orc.sim_table(tab, 4, dev)
+    # send 0->1: 0.5 + 8/4 = 2.5; send 1->2 (network): 2.5 + 1.5 + 8/2 = 8.0 on d1, d2
+    # AR {2,3} in node 1: 8.0 + 2*0.5 + (2/2)*(8/4) = 11.0 on d2, d3
+    # AR over all (network): 11.0 + 6*1.5 + (6/4)*(8/2) = 26.0
+    assert list(r["finish"]) == [26.0] * 4
 
 
 def test_table_broadcast_reduce_hand_trace(orc):
