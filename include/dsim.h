@@ -89,12 +89,19 @@ DSIM_API const char *dsim_last_error(void);
  * layer's Gemm and its two gradients, the transformer's QKV, output, fc1,
  * fc2 and LM-head products, the attention score and P.V products, and
  * their gradients; in explicit tables, compute records of cost class 1.
- * mm_enabled = 0: every compute op takes the roofline. */
+ * mm_enabled = 0: every compute op takes the roofline.
+ * node_size > 0 makes the interconnect two-tier: device d lies in node
+ * d / node_size, and a send or collective whose devices lie in more than one
+ * node crosses the network (net_bytes_per_s > 0, net_latency_s >= 0, both
+ * finite) instead of the node's links (link_bytes_per_s, link_latency_s).
+ * node_size = 0: one uniform interconnect, net_* ignored. */
 typedef struct {
     double flops_per_s, mem_bytes_per_s, link_bytes_per_s, link_latency_s, launch_s;
     uint64_t mem_cap_bytes;
     int32_t mm_enabled;
     double mm_c0, mm_c1, mm_c2;
+    int32_t node_size;
+    double net_bytes_per_s, net_latency_s;
 } dsim_device_model;
 
 /* The sequential program the transform distributes (Sec. 4, Sec. 5):
@@ -251,7 +258,10 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * lists: the per-stage 1F1B schedule, layers and ops are expanded on the fly.
  * Every replica (d, h) of a pipeline stage runs the same ops at the same
  * times, so one replica per stage is walked; collectives keep their full
- * group size in the cost.  With model.zero the replicas own different
+ * group size in the cost.  With device.node_size > 0, nodes must cut every
+ * tensor-parallel group, data-parallel group and stage alike: node_size and
+ * D*H, and node_size and H, divide one another (always so for powers of
+ * two), otherwise DSIM_ST_BAD_STRATEGY.  With model.zero the replicas own different
  * parameter groups: the stage's memory is the maximum over its replicas,
  * taken in closed form per block, and its finish time is that of the owner
  * of its last parameter.  results.row_width must be >= every candidate's P;

@@ -463,6 +463,9 @@ typedef struct {
     int64_t n_ops, cap_ops;
     uint8_t *kind, *type;
     int32_t *nsz;          /* group size used by the all-reduce cost */
+    int32_t *gfirst, *glast;  /* device range of the whole group of a collective
+                                 (a projection materialises part of it); -1: its
+                                 devices as listed */
     double *flops, *bytes;
     double *ocost;         /* per-op duration override (< 0: cost model) */
     int64_t *dev_beg, *in_beg, *out_beg;
@@ -493,7 +496,8 @@ static void prog_init(or_prog *g) { memset(g, 0, sizeof *g); }
 
 static void prog_free(or_prog *g)
 {
-    free(g->kind); free(g->type); free(g->nsz); free(g->flops); free(g->bytes); free(g->ocost);
+    free(g->kind); free(g->type); free(g->nsz); free(g->gfirst); free(g->glast);
+    free(g->flops); free(g->bytes); free(g->ocost);
     free(g->dev_beg); free(g->in_beg); free(g->out_beg);
     free(g->devs); free(g->ins); free(g->outs);
     free(g->t_dev); free(g->t_size); free(g->t_flags);
@@ -526,6 +530,8 @@ static void op_begin(or_prog *g, int kind, int type, double flops, double bytes)
         g->kind = grow(g->kind, g->cap_ops, i + 2, 1, &c, &g->failed);
         g->type = grow(g->type, g->cap_ops, i + 2, 1, &c, &g->failed);
         g->nsz = grow(g->nsz, g->cap_ops, i + 2, sizeof(int32_t), &c, &g->failed);
+        g->gfirst = grow(g->gfirst, g->cap_ops, i + 2, sizeof(int32_t), &c, &g->failed);
+        g->glast = grow(g->glast, g->cap_ops, i + 2, sizeof(int32_t), &c, &g->failed);
         g->flops = grow(g->flops, g->cap_ops, i + 2, sizeof(double), &c, &g->failed);
         g->bytes = grow(g->bytes, g->cap_ops, i + 2, sizeof(double), &c, &g->failed);
         g->ocost = grow(g->ocost, g->cap_ops, i + 2, sizeof(double), &c, &g->failed);
@@ -538,12 +544,22 @@ static void op_begin(or_prog *g, int kind, int type, double flops, double bytes)
     g->kind[i] = (uint8_t)kind;
     g->type[i] = (uint8_t)type;
     g->nsz[i] = 0;
+    g->gfirst[i] = -1;
+    g->glast[i] = -1;
     g->flops[i] = flops;
     g->bytes[i] = bytes;
     g->ocost[i] = -1.0;
     g->dev_beg[i] = g->n_devs;
     g->in_beg[i] = g->n_ins;
     g->out_beg[i] = g->n_outs;
+}
+
+/* the whole group of the op being built spans devices first..last */
+static void op_group(or_prog *g, int first, int last)
+{
+    if (g->failed) return;
+    g->gfirst[g->n_ops] = first;
+    g->glast[g->n_ops] = last;
 }
 
 static void op_dev(or_prog *g, int d)
@@ -629,8 +645,18 @@ static int prog_simulate(const or_prog *g, int n_dev, const or_device_model *m,
         double start = 0.0, end, cost;
         if (type_cost && type_cost[g->type[i]] >= 0.0) cost = type_cost[g->type[i]];
         else if (g->ocost[i] >= 0.0) cost = g->ocost[i];
-        else cost = or_cost_typed(m, g->kind[i], g->type[i], g->flops[i], g->bytes[i], g->nsz[i],
-                                  spans_nodes(m, g->devs + g->dev_beg[i], g->dev_beg[i + 1] - g->dev_beg[i]));
+        else {
+            int spans;
+            if (g->gfirst[i] >= 0) {
+                int32_t ends[2];
+                ends[0] = g->gfirst[i];
+                ends[1] = g->glast[i];
+                spans = spans_nodes(m, ends, 2);
+            } else {
+                spans = spans_nodes(m, g->devs + g->dev_beg[i], g->dev_beg[i + 1] - g->dev_beg[i]);
+            }
+            cost = or_cost_typed(m, g->kind[i], g->type[i], g->flops[i], g->bytes[i], g->nsz[i], spans);
+        }
         for (q = g->dev_beg[i]; q < g->dev_beg[i + 1]; q++) {
             d = g->devs[q];
             if (d < 0 || d >= n_dev) { rc = -2; goto out; }
@@ -871,7 +897,9 @@ static void emit_ar_tp(mat *x, int s, int type, double bytes, const int32_t *t)
     int d, h, nd = x->slice && !x->zero ? 1 : x->D, nh = x->slice ? 1 : x->H;
     if (x->H <= 1) return;
     for (d = 0; d < nd; d++) {
+        int first = s * x->D * x->H + d * x->H;
         op_begin(x->g, OR_ALLREDUCE, type, 0.0, bytes);
+        op_group(x->g, first, first + x->H - 1);
         for (h = 0; h < nh; h++) {
             int r = rep_of(x, d, h);
             op_dev(x->g, dev_of(x, s, r));
@@ -881,6 +909,13 @@ static void emit_ar_tp(mat *x, int s, int type, double bytes, const int32_t *t)
     }
 }
 
+/* the op being built runs over the D data replicas of tensor rank h */
+static void dp_group(mat *x, int s, int h)
+{
+    int base = s * x->D * x->H;
+    op_group(x->g, base + h, base + (x->D - 1) * x->H + h);
+}
+
 /* all-reduce over the data-parallel group of every tensor rank */
 static void emit_ar_dp(mat *x, int s, double bytes, int p)
 {
@@ -888,6 +923,7 @@ static void emit_ar_dp(mat *x, int s, double bytes, int p)
     if (x->D <= 1) return;
     for (h = 0; h < nh; h++) {
         op_begin(x->g, OR_ALLREDUCE, T_AR_DP, 0.0, bytes);
+        dp_group(x, s, h);
         for (d = 0; d < nd; d++) {
             int r = d * x->H + h;
             op_dev(x->g, dev_of(x, s, r));
@@ -1119,6 +1155,7 @@ static void use_weight(mat *x, int s, int p, int32_t *dst)
             dst[r] = d == o ? src : prog_tensor(x->g, dev_of(x, s, r), sz, 0);
         }
         op_begin(x->g, OR_BCAST, T_BCAST, 0.0, (double)sz);
+        dp_group(x, s, h);
         for (d = 0; d < x->D; d++) op_dev(x->g, dev_of(x, s, rep_of(x, d, h)));
         op_in(x->g, src);
         for (d = 0; d < x->D; d++)
@@ -1400,6 +1437,7 @@ static void emit_wu_slot(mat *x, int s, int p, uint64_t n)
             int ro = rep_of(x, o, h);
             int32_t red = prog_tensor(x->g, dev_of(x, s, ro), (uint64_t)x->e * n, 0);
             op_begin(x->g, OR_REDUCE, T_REDUCE, 0.0, (double)((uint64_t)x->e * n));
+            dp_group(x, s, h);
             for (d = 0; d < x->D; d++) op_dev(x->g, dev_of(x, s, rep_of(x, d, h)));
             for (d = 0; d < x->D; d++) op_in(x->g, *PW(x->G, x, s, rep_of(x, d, h), p));
             op_out(x->g, red);

@@ -43,12 +43,16 @@ CostConsts make_consts(const dsim_device_model &m)
     c.mm_c0 = m.mm_enabled ? m.mm_c0 : 0.0;
     c.mm_c1 = m.mm_enabled ? m.mm_c1 : 0.0;
     c.mm_c2 = m.mm_enabled ? m.mm_c2 : 0.0;
+    c.node = m.node_size > 0 ? m.node_size : 0;
+    c.net_lat = c.node ? m.net_latency_s : 0.0;
+    c.net_inv_l = c.node ? 1.0 / m.net_bytes_per_s : 0.0;
     c.ar_lat[0] = 0.0;
     c.ar_coef[0] = 0.0;
     for (int n = 1; n <= kMaxTableDev; ++n) {
         const double two_a = 2.0 * (double)(n - 1);
         c.ar_lat[n] = two_a * m.link_latency_s;
         c.ar_coef[n] = two_a / (double)n;
+        c.ar_lat_net[n] = two_a * c.net_lat;
     }
     return c;
 }
@@ -66,6 +70,9 @@ static dsim_status check_device(const dsim_device_model *m)
     if (m->mm_enabled != 0 && m->mm_enabled != 1) return fail(DSIM_EINVAL, "mm_enabled must be 0 or 1");
     if (m->mm_enabled && (!finite_nonneg(m->mm_c0) || !finite_nonneg(m->mm_c1) || !finite_nonneg(m->mm_c2)))
         return fail(DSIM_EINVAL, "MatMul regression coefficients must be finite and >= 0");
+    if (m->node_size < 0) return fail(DSIM_EINVAL, "node_size must be >= 0");
+    if (m->node_size > 0 && (!finite_pos(m->net_bytes_per_s) || !finite_nonneg(m->net_latency_s)))
+        return fail(DSIM_EINVAL, "network bandwidth must be finite and > 0, latency finite and >= 0");
     return DSIM_OK;
 }
 

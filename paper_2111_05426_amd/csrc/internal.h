@@ -28,8 +28,12 @@ struct CostConsts {
     uint64_t cap;      // memory cap, 0 = none
     int32_t mm;        // matrix multiplications take the regression below
     double mm_c0, mm_c1, mm_c2;
+    int32_t node;      // devices per node, 0 = one uniform interconnect
+    double net_lat;    // network latency (ops spanning nodes)
+    double net_inv_l;  // 1 / network bytes per second
     double ar_lat[kMaxTableDev + 1];
     double ar_coef[kMaxTableDev + 1];
+    double ar_lat_net[kMaxTableDev + 1];   // (2(n-1)) * net_lat
 };
 
 CostConsts make_consts(const dsim_device_model &m);

@@ -54,6 +54,8 @@ struct Ctx {
     uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
     uint64_t dH, FH, Vh, aH;
     double inv_f, inv_b, inv_l, lat, launch;
+    double inv_l_h, inv_l_d;   // 1 / bandwidth of the tensor- / data-parallel groups' link
+    double lat_d;              // latency of the data-parallel groups' link
     double arl_h, arc_h, arl_d, arc_d;
     double chl_d;   // (D - 1) * lat: latency part of a broadcast / reduce over the D replicas
     bool mm;        // matrix multiplications take the regression mm0 + mm1 * flops + mm2 * bytes
@@ -114,12 +116,21 @@ __device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const 
     x.inv_l = c.inv_l;
     x.lat = c.lat;
     x.launch = c.launch;
+    // with nodes (placement uniform, see placement_ok) a tensor-parallel
+    // group leaves its node iff H > node size, a data-parallel group iff its
+    // stage's D*H devices do and D > 1
+    const bool net_h = c.node > 0 && x.H > c.node;
+    const bool net_d = c.node > 0 && x.D > 1 && x.D * x.H > c.node;
+    const double lat_h = net_h ? c.net_lat : c.lat;
+    x.lat_d = net_d ? c.net_lat : c.lat;
+    x.inv_l_h = net_h ? c.net_inv_l : c.inv_l;
+    x.inv_l_d = net_d ? c.net_inv_l : c.inv_l;
     const double ah = 2.0 * (double)(x.H - 1), ad = 2.0 * (double)(x.D - 1);
-    x.arl_h = ah * x.lat;
+    x.arl_h = ah * lat_h;
     x.arc_h = ah / (double)x.H;
-    x.arl_d = ad * x.lat;
+    x.arl_d = ad * x.lat_d;
     x.arc_d = ad / (double)x.D;
-    x.chl_d = (double)(x.D - 1) * x.lat;
+    x.chl_d = (double)(x.D - 1) * x.lat_d;
     x.mm = c.mm != 0;
     x.mm0 = c.mm_c0;
     x.mm1 = c.mm_c1;
@@ -138,11 +149,11 @@ __device__ __forceinline__ double cost_local(const Ctx &x, uint64_t flops, uint6
 }
 __device__ __forceinline__ double cost_ar_tp(const Ctx &x, uint64_t bytes)
 {
-    return x.arl_h + x.arc_h * ((double)bytes * x.inv_l);
+    return x.arl_h + x.arc_h * ((double)bytes * x.inv_l_h);
 }
 __device__ __forceinline__ double cost_ar_dp(const Ctx &x, uint64_t bytes)
 {
-    return x.arl_d + x.arc_d * ((double)bytes * x.inv_l);
+    return x.arl_d + x.arc_d * ((double)bytes * x.inv_l_d);
 }
 __device__ __forceinline__ double cost_send(const Ctx &x, uint64_t bytes)
 {
@@ -159,7 +170,26 @@ __device__ __forceinline__ double cost_mm(const Ctx &x, uint64_t flops, uint64_t
 // D - 1 link latencies plus the bytes crossing one link once
 __device__ __forceinline__ double cost_chain_d(const Ctx &x, uint64_t bytes)
 {
-    return x.chl_d + (double)bytes * x.inv_l;
+    return x.chl_d + (double)bytes * x.inv_l_d;
+}
+
+// Nodes of `node` devices must cut every tensor-parallel group, data-parallel
+// group and stage alike: node and D*H, and node and H, divide one another.
+__device__ __forceinline__ bool placement_ok(int node, int D, int H)
+{
+    if (node <= 0) return true;
+    const int DH = D * H;
+    return (node % DH == 0 || DH % node == 0) && (node % H == 0 || H % node == 0);
+}
+
+// whether the Sends between stage s and stage t (= s +- 1) cross nodes:
+// replica r of stage s is device s*D*H + r, and uniform placement makes the
+// answer the same for every r
+__device__ __forceinline__ bool send_spans(int node, int D, int H, int s, int t)
+{
+    if (node <= 0) return false;
+    const int DH = D * H;
+    return (s * DH) / node != (t * DH) / node;
 }
 
 // Uneven microbatches: the first rows % K get one extra row.

@@ -891,7 +891,8 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     bool ok = false;
     if (c >= 0) {
         st = g.cand[c];
-        ok = strategy_ok(M, st.D, st.H, st.P, st.K) && st.P <= g.p_bound && st.P <= W && st.K <= kMaxK;
+        ok = strategy_ok(M, st.D, st.H, st.P, st.K) && st.P <= g.p_bound && st.P <= W && st.K <= kMaxK &&
+             placement_ok(g.c.node, st.D, st.H);
     }
     const int P = ok ? st.P : 0, K = st.K;
     const bool train = M.mode != DSIM_INFER;
@@ -1196,7 +1197,8 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
             sdir = bwd ? -1 : 1;
             ssz = m * (bwd ? rb_b : rb_f);
             sfre = (TF || bwd || !train) ? ssz : 0;
-            scost = g.c.lat + (double)ssz * g.c.inv_l;
+            const bool net = send_spans(g.c.node, st.D, st.H, s, bwd ? s - 1 : s + 1);
+            scost = (net ? g.c.net_lat : g.c.lat) + (double)ssz * (net ? g.c.net_inv_l : g.c.inv_l);
         }
         const int l_dir = shr1(sdir), r_dir = shl1(sdir);
         const double l_cost = shr1(scost), r_cost = shl1(scost);

@@ -172,7 +172,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     // Ops are assumed valid; a cheap test marks any lane that meets an op it
     // cannot vouch for, and that lane is re-simulated by the exact path below.
     // Indices are clamped so that even an invalid op stays inside the arrays.
-    const int32_t fast_end = (int32_t)(__builtin_amdgcn_readfirstlane(wave_min) / kUnroll) * kUnroll;
+    // (with nodes, communication costs depend on which devices an op spans:
+    // every op takes the exact path)
+    const int32_t fast_end =
+        a.c.node ? 0 : (int32_t)(__builtin_amdgcn_readfirstlane(wave_min) / kUnroll) * kUnroll;
 
     const size_t blk = (size_t)blockIdx.x * kBlock;
     const uint32_t lane_b = (uint32_t)tid * 4u;
@@ -319,6 +322,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
         const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
         const uint32_t m = kind == 0u ? (1u << ia) : (kind == 1u ? ((1u << ia) | (1u << ib)) : ib);
         const double f = (double)flf, b = (double)byf;
+        // a communication op whose devices lie in more than one node crosses
+        // the network
+        bool net = false;
+        if (a.c.node && kind != 0u) {
+            const int lo = __ffs(m) - 1, hi = 31 - __clz(m);
+            net = lo / a.c.node != hi / a.c.node;
+        }
+        const double c_lat = net ? a.c.net_lat : lat, c_inv_l = net ? a.c.net_inv_l : inv_l;
         double cost;
         if (kind == 0u && (code >> 24) == 1u && a.c.mm) {
             // a matrix multiplication: the empirical regression of Sec. 4
@@ -327,14 +338,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             const double tf = f * inv_f, tb = b * inv_b;
             cost = launch + (tf > tb ? tf : tb);
         } else if (kind == 1u) {
-            cost = lat + b * inv_l;
+            cost = c_lat + b * c_inv_l;
         } else if (kind == 2u) {
             const double2 ar = s_cost[__popc(m)];
-            cost = ar.x + ar.y * (b * inv_l);
+            cost = (net ? a.c.ar_lat_net[__popc(m)] : ar.x) + ar.y * (b * c_inv_l);
         } else {
             // broadcast / reduce: a chain of n - 1 hops (Fig. 9's Send for n = 2)
             const int n = __popc(m);
-            cost = n > 1 ? (double)(n - 1) * lat + b * inv_l : 0.0;
+            cost = n > 1 ? (double)(n - 1) * c_lat + b * c_inv_l : 0.0;
         }
         double start = 0.0;
 #pragma unroll

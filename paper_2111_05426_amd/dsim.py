@@ -29,7 +29,8 @@ class dsim_device_model(C.Structure):
     _fields_ = [("flops_per_s", C.c_double), ("mem_bytes_per_s", C.c_double),
                 ("link_bytes_per_s", C.c_double), ("link_latency_s", C.c_double),
                 ("launch_s", C.c_double), ("mem_cap_bytes", C.c_uint64),
-                ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double)]
+                ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double),
+                ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double)]
 
 
 class dsim_model(C.Structure):
@@ -128,9 +129,11 @@ def _stream(stream):
 
 def device_model(spec):
     mm = getattr(spec, "matmul", None)
+    net = getattr(spec, "network", None)
     return dsim_device_model(spec.flops_per_s, spec.mem_bytes_per_s, spec.link_bytes_per_s,
                              spec.link_latency_s, spec.launch_s, int(spec.mem_cap_bytes), 1 if mm is not None else 0,
-                             *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))))
+                             *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))),
+                             *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)))
 
 
 def model_struct(spec):

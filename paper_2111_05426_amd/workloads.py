@@ -125,11 +125,13 @@ GPT3_175B_ZERO = replace(GPT3_175B, name="gpt3_175b_zero", model=replace(GPT3_17
 # (c0 = per-product dispatch, 1/c1 = 1.49 PFLOP/s, 1/c2 = 5.7 TB/s); other
 # compute ops the roofline with F = 1/c1, the bandwidth of a 4 GiB
 # device-to-device copy measured on the same GPU (4.94 TB/s, read + write)
-# and the same dispatch cost; links are one xGMI link's 153 GB/s with 5 us
-# latency (specification values: a single GPU cannot measure them); 288 GB
-# of HBM per device.
+# and the same dispatch cost; nodes of 8 GPUs joined by xGMI (one link's
+# 153 GB/s, 5 us) and a network of one 400 Gb/s NIC per GPU between nodes
+# (50 GB/s, 10 us) -- specification values: a single GPU cannot measure
+# them; 288 GB of HBM per device.
 MI355X = DeviceSpec(flops_per_s=1.493e15, mem_bytes_per_s=4.94e12, link_bytes_per_s=153e9, link_latency_s=5e-6,
-                    launch_s=1.557e-5, mem_cap_bytes=288_000_000_000, matmul=(1.557e-5, 6.699e-16, 1.743e-13))
+                    launch_s=1.557e-5, mem_cap_bytes=288_000_000_000, matmul=(1.557e-5, 6.699e-16, 1.743e-13),
+                    network=(8, 50e9, 10e-6))
 GPT3_175B_MI355X = replace(GPT3_175B, name="gpt3_175b_mi355x", device=MI355X)
 
 ALL = {w.name: w for w in (TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN, RANDOM_TABLES, GPT3_175B,

@@ -4,6 +4,8 @@ dsim_materialize_tables and simulated by dsim_simulate_tables, against the
 oracle's full-program simulation (times within 1e-12 relative and expected
 bit-identical; op counts, peaks and status exact) and against the
 parametric path on the same strategies."""
+from dataclasses import replace
+
 import numpy as np
 import pytest
 
@@ -146,16 +148,22 @@ def test_zero_programs_as_tables(torch_gpu, orc, case):
     assert differ > 0   # the replicas really differ somewhere
 
 
-@pytest.mark.parametrize("mm", [False, True], ids=["roofline", "matmul"])
+@pytest.mark.parametrize("mm", ["roofline", "matmul", "network"])
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_small_programs_as_tables(torch_gpu, orc, case, mm):
     name, model, strat = case
-    dev = DeviceSpec(mem_cap_bytes=10 ** 6, matmul=MM if mm else None)
+    dev = DeviceSpec(mem_cap_bytes=10 ** 6, matmul=MM if mm == "matmul" else None,
+                     network=(2, 4.7e9, 1.9e-5) if mm == "network" else None)
     o = orc.run_strategies(model, strat, dev, slice=False, row_width=int(strat[:, 2].max()), threads=8)
     assert np.any(o["status"] == 0)
     g = materialize_and_simulate(torch_gpu, model, strat, dev, 8, int(o["n_ops"].max()))
     check_against_oracle(g, o, strat, 8)
-    # invalid strategies are flagged by the materialiser itself
+    # invalid strategies are flagged by the materialiser itself (node
+    # placement is a precondition of the transform-driven simulation only:
+    # tables carry device ids and simulate any placement)
+    if mm == "network":
+        o = orc.run_strategies(model, strat, replace(dev, network=None), slice=False,
+                               row_width=int(strat[:, 2].max()), threads=8)
     bad = o["status"] & ST_BAD_STRATEGY != 0
     assert np.all(g["mat_status"][bad] == ST_BAD_STRATEGY) and np.all(g["table_ops"][bad] == 0)
 

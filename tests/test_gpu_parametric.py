@@ -139,6 +139,22 @@ def test_matmul_regression_vs_full_program(torch_gpu, orc, case, dev):
     compare(g, o, strat)
 
 
+# two-tier interconnect: nodes of 1, 2, 4, 8 devices and a slower network;
+# strategies whose placement the nodes cut unevenly are flagged on both sides
+NET_CASES = [SMALL[0], SMALL[2], SMALL[4], SMALL[5], SMALL[8], SMALL[13], SMALL[16], SMALL[20]]
+
+
+@pytest.mark.parametrize("node", [1, 2, 4, 8])
+@pytest.mark.parametrize("case", range(len(NET_CASES)), ids=[c[0] for c in NET_CASES])
+def test_network_vs_full_program(torch_gpu, orc, case, node):
+    name, model, strat = NET_CASES[case]
+    d = DeviceSpec(mem_cap_bytes=10 ** 6, network=(node, 4.7e9, 1.9e-5))
+    g = run_gpu(torch_gpu, model, strat, d)
+    o = orc.run_strategies(model, strat, d, slice=False, row_width=g["finish"].shape[1], threads=8)
+    assert np.any(o["status"] == 0)
+    compare(g, o, strat)
+
+
 GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(LARGE_MLP, name="large_mlp_mixed", model=replace(LARGE_MLP.model, mode=TRAIN_ADAM_MIXED)),
          replace(LARGE_MLP, name="large_mlp_gpipe", model=replace(LARGE_MLP.model, schedule=SCHED_GPIPE)),

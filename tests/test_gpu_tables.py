@@ -85,18 +85,19 @@ def results_np(r):
     return out
 
 
-@pytest.mark.parametrize("kinds", ["plain", "bcast_reduce", "matmul"])
+@pytest.mark.parametrize("kinds", ["plain", "bcast_reduce", "matmul", "network"])
 @pytest.mark.parametrize("n_dev", [1, 2, 3, 5, 8])
 @pytest.mark.parametrize("bad", [False, True])
 def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, kinds):
     from paper_2111_05426_amd import dsim
     from paper_2111_05426_amd.workloads import DeviceSpec
     torch = torch_gpu
-    rooted, classes = kinds == "bcast_reduce", kinds == "matmul"
-    rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted + 211 * classes)
+    rooted, classes, net = kinds in ("bcast_reduce", "network"), kinds == "matmul", kinds == "network"
+    rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted + 211 * classes + 307 * net)
     n_cand, max_ops = 777, 301   # several 256-lane blocks and a ragged tail
     t = random_tables(rng, n_cand, max_ops, n_dev, bad, rooted, classes)
-    dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5, matmul=(4.5e-6, 9.1e-15, 1.3e-12) if classes else None)
+    dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5, matmul=(4.5e-6, 9.1e-15, 1.3e-12) if classes else None,
+                     network=(max(1, n_dev // 2 - (n_dev == 5)), 3.3e9, 2.1e-5) if net else None)
     g = to_gpu(torch, t)
     init = torch.from_numpy(t["init"].view(np.int64)).cuda()
     rw = n_dev + 2

@@ -1138,6 +1138,25 @@ def test_network_pipeline_sends_cross_nodes(orc):
         assert r["makespan"] == K * lat
 
 
+@pytest.mark.parametrize("case", [(mlp(8, 64, 64, 4, TRAIN_ADAM), 4, 2, 2, 2, 2), (mlp(8, 64, 64, 2, TRAIN_SGD), 8, 1, 2, 3, 4),
+                                  (transformer(4, 32, 4, 8, 101, 16, 2, TRAIN_ADAM_MIXED), 4, 2, 2, 2, 4),
+                                  (transformer(4, 32, 4, 8, 101, 16, 2, TRAIN_ADAM, zero=1), 4, 2, 2, 2, 2),
+                                  (transformer(4, 32, 4, 8, 101, 16, 2, INFER), 2, 4, 4, 2, 8)])
+def test_network_projection_matches_full_program(orc, case):
+    """The projection onto one replica per stage charges every collective
+    for its whole group: crossing nodes or not, it equals the full
+    program."""
+    m, D, H, P, K, G = case
+    dev = replace(DEV, network=(G, *NET))
+    full = orc.sim_strategy(m, D, H, P, K, dev)
+    proj = orc.sim_strategy(m, D, H, P, K, dev, slice=True)
+    assert full["status"] == 0
+    assert proj["makespan"] == full["makespan"]
+    assert np.array_equal(proj["stage_finish"], full["stage_finish"])
+    assert np.array_equal(proj["stage_peak"], full["stage_peak"])
+    assert full["makespan"] > orc.sim_strategy(m, D, H, P, K, DEV)["makespan"]
+
+
 def test_network_placement_must_be_uniform(orc):
     """Nodes must cut every tensor group, data group and stage alike
     (node_size and D*H, node_size and H divide one another)."""
