@@ -54,13 +54,14 @@ def stored_traffic(kernel, workload, src):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline_random(spec, dev, budget_s=12.0):
+def cpu_baseline_random(spec, dev, budget_s=12.0, threads=None):
     """The oracle, as it stands, on strided candidates of the same workload
-    until ~budget_s seconds of wall time are spent."""
+    until ~budget_s seconds of wall time are spent (all host threads, up to
+    16, unless `threads` is given)."""
     import numpy as np
     import oracle
-    threads = max(1, min(os.cpu_count() or 1, 16))
-    chunk = 2048 * threads // 8
+    threads = threads or max(1, min(os.cpu_count() or 1, 16))
+    chunk = max(64, 2048 * threads // 8)
     done, t0 = 0, time.perf_counter()
     stride = 997
     # 997 is prime and does not divide n_cand, so the sample holds distinct candidates
@@ -239,12 +240,13 @@ def bench_grid_as_tables(torch, dsim, W, reps, n_dev=8):
 FP64_ADD_PEAK_T = 256 * 4 * 16 * 2.4e9 / 1e12
 
 
-def cpu_baseline_parametric(W, strat, budget_s=10.0):
+def cpu_baseline_parametric(W, strat, budget_s=10.0, threads=None):
     """The oracle (projection mode), as it stands, on strided candidates of
-    the grid until ~budget_s seconds of wall time are spent."""
+    the grid until ~budget_s seconds of wall time are spent (all host
+    threads, up to 16, unless `threads` is given)."""
     import numpy as np
     import oracle
-    threads = max(1, min(os.cpu_count() or 1, 16))
+    threads = threads or max(1, min(os.cpu_count() or 1, 16))
     order = np.arange(len(strat))[::7]
     done, t0 = 0, time.perf_counter()
     while time.perf_counter() - t0 < budget_s and done < len(order):
@@ -278,7 +280,9 @@ def bench_parametric_line(args, torch, dsim, W):
                      "walked_ops_per_launch": r["walked_ops"]},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline_parametric(W, dsim.dsim_create_grid(W.model, W.grid))
+        strat = dsim.dsim_create_grid(W.model, W.grid)
+        out["cpu_baseline"] = cpu_baseline_parametric(W, strat)
+        out["cpu_baseline"]["single_thread"] = cpu_baseline_parametric(W, strat, budget_s=4.0, threads=1)
     return out
 
 
@@ -338,6 +342,7 @@ def main():
         out["copy_calibration"] = copy_calibration(torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_random(W.tables, W.device)
+        out["cpu_baseline"]["single_thread"] = cpu_baseline_random(W.tables, W.device, budget_s=4.0, threads=1)
     print(json.dumps(out), flush=True)
 
 

@@ -90,7 +90,21 @@ def test_argument_errors_before_launch():
     m = dsim.model_struct(ALL["gpt2_small"].model)
     assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
     assert "NULL" in dsim.dsim_last_error()
-    for field, bad in (("schedule", 2), ("recompute", 2), ("recompute", -1)):
+    # device model: MatMul regression and network tier
+    tab4 = dsim.dsim_tables()
+    tab4.n_dev, tab4.max_ops = 4, 4
+    for spec, word in ((DeviceSpec(matmul=(-1e-6, 0.0, 0.0)), "regression"),
+                       (DeviceSpec(matmul=(0.0, float("inf"), 0.0)), "regression"),
+                       (DeviceSpec(network=(-1, 1e9, 0.0)), "node_size"),
+                       (DeviceSpec(network=(8, 0.0, 1e-6)), "network"),
+                       (DeviceSpec(network=(8, 1e9, float("nan"))), "network")):
+        bad = dsim.device_model(spec)
+        assert L.dsim_simulate_tables(C.byref(tab4), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
+        assert word in dsim.dsim_last_error()
+    bad = dsim.device_model(DeviceSpec())
+    bad.mm_enabled = 2
+    assert L.dsim_simulate_tables(C.byref(tab4), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
+    for field, bad in (("schedule", 2), ("recompute", 2), ("recompute", -1), ("zero", 3), ("zero", -1)):
         m = dsim.model_struct(ALL["gpt2_small_train"].model)
         setattr(m, field, bad)
         assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
