@@ -1378,10 +1378,11 @@ static void emit_split(mat *x, int s, int which)
 {
     int r, k;
     uint64_t rb = input_row_bytes(x), whole = rb * (uint64_t)x->rows;
+    int32_t *ids = malloc(sizeof(int32_t) * (size_t)x->K);
+    if (!ids) { x->g->failed = 1; return; }
     for (r = 0; r < x->R; r++) {
         int dv = dev_of(x, s, r);
         int32_t src = which == 0 ? x->X[s * x->R + r] : x->Y[s * x->R + r];
-        int32_t ids[4096];
         for (k = 0; k < x->K; k++) ids[k] = prog_tensor(x->g, dv, rb * (uint64_t)mb_rows(x, k), 0);
         op_begin(x->g, OR_COMPUTE, T_SPLIT, 0.0, (double)(2 * whole));
         op_dev(x->g, dv);
@@ -1390,6 +1391,7 @@ static void emit_split(mat *x, int s, int which)
         op_end(x->g, 0, mult_dev(x));
         for (k = 0; k < x->K; k++) *SV(x, s, r, k, which == 0 ? F_XK : F_YK) = ids[k];
     }
+    free(ids);
 }
 
 static void emit_send(mat *x, int s, int k, int fwd)
@@ -1543,7 +1545,7 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
             return 0;
         }
     }
-    if ((int64_t)D * H > 1024 || K > 4096) return -1;
+    if ((int64_t)D * H > 1024 || K > 16383) return -1;
     memset(&x, 0, sizeof x);
     prog_init(&g);
     x.M = M; x.g = &g; x.D = D; x.H = H; x.P = P; x.K = K; x.slice = slice;

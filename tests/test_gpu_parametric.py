@@ -253,6 +253,39 @@ def test_invalid_strategies(torch_gpu, orc):
     compare(g, o, strat)
 
 
+@pytest.mark.parametrize("case", [
+    ("one_layer", mlp(1, 64, 16, 4, TRAIN_ADAM), [(1, 1, 1, 1), (2, 1, 1, 8), (16, 1, 1, 1)]),
+    ("layer_per_stage", transformer(6, 32, 4, 8, 64, 8, 2, TRAIN_ADAM_MIXED), [(1, 2, 6, 8), (2, 1, 6, 4), (8, 1, 6, 1)]),
+    ("row_per_microbatch", mlp(4, 32, 24, 2, TRAIN_SGD, schedule=SCHED_GPIPE), [(1, 1, 4, 24), (3, 2, 2, 8), (24, 1, 2, 1)]),
+    ("tf_one_layer_infer", transformer(1, 32, 2, 4, 50, 3, 4, INFER), [(1, 1, 1, 3), (3, 2, 1, 1)]),
+    ("single_candidate", transformer(3, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, recompute=1), [(2, 2, 3, 3)]),
+])
+def test_degenerate_strategies(torch_gpu, orc, case):
+    """One layer, one layer per stage, one row per microbatch or per
+    replica, a lone candidate: parity with the full program."""
+    name, model, strat = case
+    strat = np.array(strat, np.int32)
+    g = run_gpu(torch_gpu, model, strat, DeviceSpec())
+    o = orc.run_strategies(model, strat, DeviceSpec(), slice=False, row_width=g["finish"].shape[1], threads=4)
+    assert np.all(o["status"] == 0)
+    compare(g, o, strat)
+
+
+def test_microbatch_limit(torch_gpu, orc):
+    """K up to 16,383 microbatches per candidate (then flagged); an empty
+    call is a no-op."""
+    from paper_2111_05426_amd import dsim
+    m = mlp(2, 16, 20000, 4, TRAIN_SGD)
+    strat = np.array([(1, 1, 2, 16383), (1, 1, 1, 16383), (1, 1, 2, 16384)], np.int32)
+    g = run_gpu(torch_gpu, m, strat, DeviceSpec(), 2)
+    o = orc.run_strategies(m, strat[:2], DeviceSpec(), slice=False, row_width=2, threads=2)
+    assert list(g["status"]) == [0, 0, 16]
+    compare({k: (v[:2] if isinstance(v, np.ndarray) else v) for k, v in g.items()}, o, strat[:2])
+    r = dsim.alloc_results(0, 2)
+    dsim.dsim_simulate_parametric(m, torch_gpu.zeros((0, 4), dtype=torch_gpu.int32, device="cuda"), DeviceSpec(), r)
+    torch_gpu.cuda.synchronize()
+
+
 def test_stage_limit_and_row_width(torch_gpu):
     """More than 64 pipeline stages, or more than results.row_width, is
     refused per candidate (DSIM_ST_BAD_STRATEGY), never overrun."""
