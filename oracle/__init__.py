@@ -24,7 +24,7 @@ TYPES = ["SPLIT", "GEMM", "RELU", "AR_TP", "LOSSGRAD", "RELUGRAD", "GEMMDW", "AD
          "GEMMDX", "SEND_F", "SEND_B", "AR_DP", "OPT",
          "LN", "QKV", "SCORES", "SOFTMAX", "AV", "OUTPROJ", "RESADD", "FC1", "GELU", "FC2",
          "EMBED", "LMHEAD", "XENT_STATS", "XENT_GRAD", "LN_B", "RESADD_B", "GELU_B", "AV_B",
-         "SOFTMAX_B", "SCORES_B", "EMBED_DW", "BCAST", "REDUCE", "GENERIC"]
+         "SOFTMAX_B", "SCORES_B", "EMBED_DW", "BCAST", "REDUCE", "STREAM", "GENERIC"]
 T = {name: i for i, name in enumerate(TYPES)}
 N_TYPES = len(TYPES)
 
@@ -45,7 +45,9 @@ class _Dev(C.Structure):
                 ("link_bytes_per_s", C.c_double), ("link_latency_s", C.c_double),
                 ("launch_s", C.c_double), ("mem_cap_bytes", C.c_uint64),
                 ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double),
-                ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double)]
+                ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double),
+                ("streams_per_gpu", C.c_int32), ("stream_bytes_per_s", C.c_double),
+                ("stream_latency_s", C.c_double)]
 
 
 class _Model(C.Structure):
@@ -53,7 +55,7 @@ class _Model(C.Structure):
                 ("n_heads", C.c_int32), ("d_model", C.c_int64), ("d_ff", C.c_int64),
                 ("seq_len", C.c_int64), ("vocab", C.c_int64), ("global_batch", C.c_int64),
                 ("elem_bytes", C.c_int32), ("schedule", C.c_int32), ("recompute", C.c_int32),
-                ("zero", C.c_int32)]
+                ("zero", C.c_int32), ("overlap", C.c_int32)]
 
 
 _lib = None
@@ -71,16 +73,18 @@ def lib():
 def _dev(d):
     mm = getattr(d, "matmul", None)
     net = getattr(d, "network", None)
+    st = getattr(d, "streams", None)
     return _Dev(d.flops_per_s, d.mem_bytes_per_s, d.link_bytes_per_s, d.link_latency_s,
                 d.launch_s, int(d.mem_cap_bytes), 1 if mm is not None else 0,
                 *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))),
-                *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)))
+                *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)),
+                *((int(st[0]), float(st[1]), float(st[2])) if st is not None else (0, 0.0, 0.0)))
 
 
 def _model(m):
     return _Model(m.family, m.mode, m.n_layers, m.n_heads, m.d_model, m.d_ff, m.seq_len,
                   m.vocab, m.global_batch, m.elem_bytes, getattr(m, "schedule", 0),
-                  getattr(m, "recompute", 0), getattr(m, "zero", 0))
+                  getattr(m, "recompute", 0), getattr(m, "zero", 0), getattr(m, "overlap", 0))
 
 
 def _p(a):
@@ -109,6 +113,15 @@ def cost_between_nodes(dev, kind, nbytes, n):
     f.restype = C.c_double
     f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_double, C.c_double, C.c_int, C.c_int]
     return f(C.byref(d), kind, 0.0, float(nbytes), int(n), 1)
+
+
+def cost_on_one_gpu(dev, kind, nbytes, n):
+    """Cost of a communication op whose devices are streams of one GPU."""
+    d = _dev(dev)
+    f = lib().or_cost_spans
+    f.restype = C.c_double
+    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_double, C.c_double, C.c_int, C.c_int]
+    return f(C.byref(d), kind, 0.0, float(nbytes), int(n), 2)
 
 
 def gen_table(seed, cand, n_ops, n_dev):
@@ -195,8 +208,10 @@ def sim_program(ops, tensors, n_dev, dev, with_trace=False):
 
 
 def sim_strategy(model, D, H, P, K, dev, slice=False, type_cost=None, want_devices=True):
-    """Materialise (D,H,P,K) on the model and simulate it.  Returns a dict."""
-    n_dev = D * H * P
+    """Materialise (D,H,P,K) on the model and simulate it.  Returns a dict.
+    With overlap every GPU has two devices (streams): 2g computes, 2g + 1
+    communicates."""
+    n_dev = (2 if getattr(model, "overlap", 0) else 1) * D * H * P
     sf = np.zeros(P, np.float64)
     sp = np.zeros(P, np.uint64)
     df = np.zeros(n_dev, np.float64) if want_devices else None

@@ -71,6 +71,8 @@ enum {
     T_RESADD_B, T_GELU_B, T_AV_B, T_SOFTMAX_B, T_SCORES_B, T_EMBED_DW,
     /* ZeRO */
     T_BCAST, T_REDUCE,
+    /* overlap: a gradient handed between the two streams of one GPU */
+    T_STREAM,
     T_GENERIC, T_NTYPES
 };
 
@@ -92,6 +94,15 @@ typedef struct {
      * interconnect. */
     int32_t node_size;
     double net_bytes_per_s, net_latency_s;
+    /* Streams (Sec. 2.2, Limitations: communication that overlaps
+     * computation is modelled with one device per stream, the streams of a
+     * GPU communicating at low or zero cost): with streams_per_gpu = S > 1,
+     * device d is a stream of GPU d / S, nodes hold node_size GPUs, and a
+     * send or collective whose devices all lie on one GPU costs
+     * stream_latency_s and stream_bytes_per_s (+inf: no byte term) in
+     * place of the links.  S = 0 or 1: every device is its own GPU. */
+    int32_t streams_per_gpu;
+    double stream_bytes_per_s, stream_latency_s;
 } or_device_model;
 
 typedef struct {
@@ -101,6 +112,8 @@ typedef struct {
     int32_t schedule;   /* 0: synchronous 1F1B (Sec. 4); 1: GPipe (all forwards, then all backwards) */
     int32_t recompute;  /* 1: activation recomputation (gradient checkpointing, Fig. 8), training only */
     int32_t zero;       /* 1: ZeRO parameter and gradient partitioning (Fig. 9), training only */
+    int32_t overlap;    /* 1: data-parallel gradient all-reduce on a second stream per GPU (Sec. 2.2,
+                           Limitations), overlapping the last backward pass; training, not with ZeRO */
 } or_model;
 
 /* ------------------------------------------------------------------------ */
@@ -115,15 +128,20 @@ static double cost_compute(const or_device_model *m, double flops, double bytes)
     return m->launch_s + (tf > tb ? tf : tb);
 }
 
-/* the link a communication op crosses: the network when its devices span
- * more than one node, the node's own links otherwise */
+/* The tier a communication op crosses (`spans`): 0 the links inside a node,
+ * 1 the network (its devices lie in more than one node), 2 the streams of
+ * one GPU (all its devices lie on one GPU). */
+enum { TIER_LINK = 0, TIER_NET = 1, TIER_STREAM = 2 };
+
 static double link_lat(const or_device_model *m, int spans)
 {
-    return spans && m->node_size > 0 ? m->net_latency_s : m->link_latency_s;
+    if (spans == TIER_STREAM && m->streams_per_gpu > 1) return m->stream_latency_s;
+    return spans == TIER_NET && m->node_size > 0 ? m->net_latency_s : m->link_latency_s;
 }
 static double link_bw(const or_device_model *m, int spans)
 {
-    return spans && m->node_size > 0 ? m->net_bytes_per_s : m->link_bytes_per_s;
+    if (spans == TIER_STREAM && m->streams_per_gpu > 1) return m->stream_bytes_per_s;
+    return spans == TIER_NET && m->node_size > 0 ? m->net_bytes_per_s : m->link_bytes_per_s;
 }
 
 static double cost_send(const or_device_model *m, double bytes, int spans)
@@ -155,14 +173,24 @@ static double cost_chain(const or_device_model *m, double bytes, int n, int span
     return (double)(n - 1) * link_lat(m, spans) + bytes * inv_l;
 }
 
-/* whether devices lie in more than one node (always 0 without nodes) */
+/* the tier of an op over the given devices: the streams of one GPU when
+ * every device lies on the same GPU (streams_per_gpu > 1), else the network
+ * when their GPUs lie in more than one node, else the links */
 static int spans_nodes(const or_device_model *m, const int32_t *devs, int64_t n)
 {
     int64_t q;
-    if (m->node_size <= 0 || n < 2) return 0;
+    int S = m->streams_per_gpu > 1 ? m->streams_per_gpu : 1;
+    if (n < 1) return TIER_LINK;
+    if (S > 1) {
+        int one_gpu = 1;
+        for (q = 1; q < n; q++)
+            if (devs[q] / S != devs[0] / S) one_gpu = 0;
+        if (one_gpu) return TIER_STREAM;
+    }
+    if (m->node_size <= 0 || n < 2) return TIER_LINK;
     for (q = 1; q < n; q++)
-        if (devs[q] / m->node_size != devs[0] / m->node_size) return 1;
-    return 0;
+        if (devs[q] / S / m->node_size != devs[0] / S / m->node_size) return TIER_NET;
+    return TIER_LINK;
 }
 static int mask_spans_nodes(const or_device_model *m, uint32_t mask)
 {
@@ -813,12 +841,15 @@ typedef struct {
     const or_model *M;
     or_prog *g;
     int D, H, P, K, slice, train, fam, mode, rc, zero;
+    int ov;               /* gradient all-reduce on the communication stream */
+    int S;                /* devices (streams) per GPU: 1, or 2 with ov */
     int R;                /* replicas materialised per stage */
     int64_t e, rows;      /* element bytes, rows (sequences) per replica */
     int *l0;              /* P+1 stage boundaries */
     int nl_max, nslot, nps;
     int32_t *sv;          /* per (s, r, k) saved tensor ids */
     int32_t *W, *OS, *G;  /* per (s, r, param slot) */
+    int32_t *GC;          /* per (s, r, param slot): the gradient's alias on the communication stream */
     int32_t *X, *Y;       /* per (s, r) resident inputs */
     int32_t *cur;         /* per r scratch */
     int32_t *tmp;         /* per r scratch */
@@ -833,11 +864,19 @@ static int rep_of(const mat *x, int d, int h)
     return x->zero ? d : 0;
 }
 
-static int dev_of(const mat *x, int s, int r)
+/* GPU of replica r of stage s: stage-major, then data replica, then tensor
+ * rank */
+static int gpu_of(const mat *x, int s, int r)
 {
     if (x->slice && x->zero) return s * x->D * x->H + r * x->H;
     return s * x->D * x->H + r;
 }
+
+/* device of the replica's computation: its GPU, or with overlap the GPU's
+ * first stream (device 2g); the GPU's second stream (2g + 1) carries the
+ * data-parallel gradient all-reduce */
+static int dev_of(const mat *x, int s, int r) { return x->S * gpu_of(x, s, r); }
+static int comm_of(const mat *x, int s, int r) { return x->S * gpu_of(x, s, r) + 1; }
 
 static int data_rep(const mat *x, int r)
 {
@@ -899,7 +938,7 @@ static void emit_ar_tp(mat *x, int s, int type, double bytes, const int32_t *t)
     for (d = 0; d < nd; d++) {
         int first = s * x->D * x->H + d * x->H;
         op_begin(x->g, OR_ALLREDUCE, type, 0.0, bytes);
-        op_group(x->g, first, first + x->H - 1);
+        op_group(x->g, x->S * first, x->S * (first + x->H - 1));
         for (h = 0; h < nh; h++) {
             int r = rep_of(x, d, h);
             op_dev(x->g, dev_of(x, s, r));
@@ -909,12 +948,14 @@ static void emit_ar_tp(mat *x, int s, int type, double bytes, const int32_t *t)
     }
 }
 
-/* the op being built runs over the D data replicas of tensor rank h */
-static void dp_group(mat *x, int s, int h)
+/* the op being built runs over the D data replicas of tensor rank h (on
+ * stream `stream` of their GPUs) */
+static void dp_group_on(mat *x, int s, int h, int stream)
 {
     int base = s * x->D * x->H;
-    op_group(x->g, base + h, base + (x->D - 1) * x->H + h);
+    op_group(x->g, x->S * (base + h) + stream, x->S * (base + (x->D - 1) * x->H + h) + stream);
 }
+static void dp_group(mat *x, int s, int h) { dp_group_on(x, s, h, 0); }
 
 /* all-reduce over the data-parallel group of every tensor rank */
 static void emit_ar_dp(mat *x, int s, double bytes, int p)
@@ -933,13 +974,52 @@ static void emit_ar_dp(mat *x, int s, double bytes, int p)
     }
 }
 
+/* Overlap (Sec. 2.2, Limitations: one device per stream, the streams of a
+ * GPU exchanging tensors at low or zero cost).  Once the last microbatch
+ * has finished a weight gradient, every replica hands it to its GPU's
+ * communication stream (a Send between the GPU's two streams; the copy
+ * aliases the gradient's memory, so it allocates nothing), and the
+ * communication streams of the D data replicas all-reduce it there while
+ * the computation stream goes on with the backward pass.  One data replica
+ * has nothing to reduce. */
+static void grad_final(mat *x, int s, int k, int p, uint64_t nparam)
+{
+    int r, d, h, nd, nh;
+    double by = (double)((uint64_t)x->e * nparam);
+    if (!x->ov || x->D <= 1 || k != x->K - 1) return;
+    for (r = 0; r < x->R; r++) {
+        int32_t c = prog_tensor(x->g, comm_of(x, s, r), 0, 0);
+        op_begin(x->g, OR_SEND, T_STREAM, 0.0, by);
+        op_dev(x->g, dev_of(x, s, r));
+        op_dev(x->g, comm_of(x, s, r));
+        op_in(x->g, *PW(x->G, x, s, r, p));
+        op_out(x->g, c);
+        op_end(x->g, 0, mult_dev(x));
+        *PW(x->GC, x, s, r, p) = c;
+    }
+    nd = x->slice ? 1 : x->D;
+    nh = x->slice ? 1 : x->H;
+    for (h = 0; h < nh; h++) {
+        op_begin(x->g, OR_ALLREDUCE, T_AR_DP, 0.0, by);
+        dp_group_on(x, s, h, 1);
+        for (d = 0; d < nd; d++) {
+            r = d * x->H + h;
+            op_dev(x->g, comm_of(x, s, r));
+            op_in(x->g, *PW(x->GC, x, s, r, p));
+        }
+        op_end(x->g, x->D, mult_dp(x));
+    }
+}
+
 /* gradient accumulation: microbatch 0's weight gradient becomes the
- * accumulator, later ones are added into it in place */
-static void accumulate(mat *x, int s, int p, uint64_t nparam, const int32_t *gw)
+ * accumulator, later ones are added into it in place; after microbatch k
+ * the gradient may be final (overlap) */
+static void accumulate(mat *x, int s, int k, int p, uint64_t nparam, const int32_t *gw)
 {
     int r;
     if (*PW(x->G, x, s, 0, p) < 0) {
         for (r = 0; r < x->R; r++) *PW(x->G, x, s, r, p) = gw[r];
+        grad_final(x, s, k, p, nparam);
         return;
     }
     for (r = 0; r < x->R; r++) {
@@ -950,6 +1030,7 @@ static void accumulate(mat *x, int s, int p, uint64_t nparam, const int32_t *gw)
         op_in(x->g, gw[r]);
         op_end(x->g, 0, mult_dev(x));
     }
+    grad_final(x, s, k, p, nparam);
 }
 
 static void gather_sv(mat *x, int s, int k, int f, int32_t *dst)
@@ -1049,7 +1130,7 @@ static void mlp_bwd(mat *x, int s, int k)
         else gather_sv(x, s, k, F_LAYER0 + (li - 1) * NLF + L_A, xin);
         emit_local(x, s, T_GEMMDW, (double)(2 * m * din * dout), (double)(e * (m * din + m * dout + din * dout)),
                    xin, tmp, NULL, (uint64_t)(e * din * dout), gw, 0, NULL);
-        accumulate(x, s, li, (uint64_t)(din * dout), gw);
+        accumulate(x, s, k, li, (uint64_t)(din * dout), gw);
         use_weight(x, s, li, w);
         emit_local(x, s, T_GEMMDX, (double)(2 * m * din * dout), (double)(e * (m * dout + din * dout + m * din)),
                    tmp, w, NULL, (uint64_t)(e * m * din), cur, 0, NULL);
@@ -1277,7 +1358,7 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.d * t.Vh),
                    (double)(t.e * (t.T * t.d + t.T * t.Vh + t.d * t.Vh)),
                    yf, dl, NULL, (uint64_t)(t.e * t.d * t.Vh), gw, 0, NULL);
-        accumulate(x, s, tf_slot_head(x), (uint64_t)(t.d * t.Vh), gw);
+        accumulate(x, s, k, tf_slot_head(x), (uint64_t)(t.d * t.Vh), gw);
         gather_sv(x, s, k, F_XL, xl);
         emit_local(x, s, T_LN_B, (double)(8 * t.T * t.d), (double)(3 * t.ACT),
                    dy, xl, NULL, (uint64_t)t.ACT, cur, 0, NULL);
@@ -1302,7 +1383,7 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.FH * t.d),
                    (double)(t.e * (t.T * t.FH + t.T * t.d + t.FH * t.d)),
                    a1, cur, NULL, (uint64_t)(t.e * t.FH * t.d), gw, 0, NULL);
-        accumulate(x, s, 4 * li + 3, (uint64_t)(t.FH * t.d), gw);
+        accumulate(x, s, k, 4 * li + 3, (uint64_t)(t.FH * t.d), gw);
         gather_sv(x, s, k, base + L_U, a1);
         emit_local(x, s, T_GELU_B, (double)(8 * t.T * t.FH), (double)(3 * t.FF),
                    dg, a1, NULL, (uint64_t)t.FF, du, 0, NULL);
@@ -1315,7 +1396,7 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.d * t.FH),
                    (double)(t.e * (t.T * t.d + t.T * t.FH + t.d * t.FH)),
                    a1, du, NULL, (uint64_t)(t.e * t.d * t.FH), gw, 0, NULL);
-        accumulate(x, s, 4 * li + 2, (uint64_t)(t.d * t.FH), gw);
+        accumulate(x, s, k, 4 * li + 2, (uint64_t)(t.d * t.FH), gw);
         gather_sv(x, s, k, base + L_X2, a1);
         emit_local(x, s, T_LN_B, (double)(8 * t.T * t.d), (double)(3 * t.ACT),
                    dy, a1, NULL, (uint64_t)t.ACT, dxa, 0, NULL);
@@ -1329,7 +1410,7 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.dH * t.d),
                    (double)(t.e * (t.T * t.dH + t.T * t.d + t.dH * t.d)),
                    a1, dx2, NULL, (uint64_t)(t.e * t.dH * t.d), gw, 0, NULL);
-        accumulate(x, s, 4 * li + 1, (uint64_t)(t.dH * t.d), gw);
+        accumulate(x, s, k, 4 * li + 1, (uint64_t)(t.dH * t.d), gw);
         gather_sv(x, s, k, base + L_PM, a1);
         gather_sv(x, s, k, base + L_QKV, a2);
         emit_local(x, s, T_AV_B, (double)(4 * t.T * t.s * t.dH), (double)(2 * t.S2 + 3 * t.OH),
@@ -1347,7 +1428,7 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.d * 3 * t.dH),
                    (double)(t.e * (t.T * t.d + t.T * 3 * t.dH + t.d * 3 * t.dH)),
                    a1, dq, NULL, (uint64_t)(t.e * t.d * 3 * t.dH), gw, 0, NULL);
-        accumulate(x, s, 4 * li + 0, (uint64_t)(t.d * 3 * t.dH), gw);
+        accumulate(x, s, k, 4 * li + 0, (uint64_t)(t.d * 3 * t.dH), gw);
         gather_sv(x, s, k, base + L_X, a1);
         emit_local(x, s, T_LN_B, (double)(8 * t.T * t.d), (double)(3 * t.ACT),
                    dy, a1, NULL, (uint64_t)t.ACT, dxa, 0, NULL);
@@ -1360,7 +1441,7 @@ static void tf_bwd(mat *x, int s, int k)
         else for (r = 0; r < x->R; r++) tok[r] = x->X[s * x->R + r];
         emit_local(x, s, T_EMBED_DW, (double)(t.T * t.d), (double)(t.ACT + t.IDS + t.e * t.Vh * t.d),
                    cur, tok, NULL, (uint64_t)(t.e * t.Vh * t.d), gw, 0, NULL);
-        accumulate(x, s, tf_slot_emb(x), (uint64_t)(t.Vh * t.d), gw);
+        accumulate(x, s, k, tf_slot_emb(x), (uint64_t)(t.Vh * t.d), gw);
     } else {
         store_sv(x, s, k, F_OUTG, cur);
     }
@@ -1453,7 +1534,20 @@ static void emit_wu_slot(mat *x, int s, int p, uint64_t n)
         }
         return;
     }
-    emit_ar_dp(x, s, (double)((uint64_t)x->e * n), p);
+    if (x->ov && x->D > 1) {
+        /* overlap: the reduced gradient comes back from the communication
+         * stream (into the gradient's own memory) before the optimizer */
+        for (r = 0; r < x->R; r++) {
+            op_begin(x->g, OR_SEND, T_STREAM, 0.0, (double)((uint64_t)x->e * n));
+            op_dev(x->g, comm_of(x, s, r));
+            op_dev(x->g, dev_of(x, s, r));
+            op_in(x->g, *PW(x->GC, x, s, r, p));
+            op_in(x->g, *PW(x->G, x, s, r, p));
+            op_end(x->g, 0, mult_dev(x));
+        }
+    } else {
+        emit_ar_dp(x, s, (double)((uint64_t)x->e * n), p);
+    }
     for (r = 0; r < x->R; r++) {
         op_begin(x->g, OR_COMPUTE, T_OPT, fl, by);
         op_dev(x->g, dev_of(x, s, r));
@@ -1546,16 +1640,20 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
         }
     }
     if ((int64_t)D * H > 1024 || K > 16383) return -1;
+    /* overlap: two streams per GPU (and no ZeRO); otherwise one device per GPU */
+    if (M->overlap ? (M->zero || dm->streams_per_gpu != 2) : dm->streams_per_gpu > 1) return -1;
     memset(&x, 0, sizeof x);
     prog_init(&g);
     x.M = M; x.g = &g; x.D = D; x.H = H; x.P = P; x.K = K; x.slice = slice;
     x.fam = M->family; x.mode = M->mode; x.train = M->mode != MODE_INFER;
     x.rc = x.train && M->recompute;
     x.zero = x.train && M->zero;
+    x.S = M->overlap ? 2 : 1;
+    x.ov = x.train && M->overlap;
     x.R = slice ? (x.zero ? D : 1) : D * H;
     x.e = M->elem_bytes;
     x.rows = M->global_batch / D;
-    n_dev = D * H * P;
+    n_dev = x.S * D * H * P;
     x.l0 = malloc(sizeof(int) * (size_t)(P + 1));
     if (!x.l0) return -3;
     {
@@ -1574,6 +1672,7 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     x.W = malloc(sizeof(int32_t) * (size_t)P * x.R * x.nps);
     x.OS = malloc(sizeof(int32_t) * (size_t)P * x.R * x.nps);
     x.G = malloc(sizeof(int32_t) * (size_t)P * x.R * x.nps);
+    x.GC = malloc(sizeof(int32_t) * (size_t)P * x.R * x.nps);
     x.X = malloc(sizeof(int32_t) * (size_t)P * x.R);
     x.Y = malloc(sizeof(int32_t) * (size_t)P * x.R);
     x.cur = malloc(sizeof(int32_t) * (size_t)x.R);
@@ -1590,10 +1689,11 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     emk = calloc((size_t)P, sizeof(int));
     fin = calloc((size_t)n_dev, sizeof(double));
     pk = calloc((size_t)n_dev, sizeof(uint64_t));
-    if (!x.sv || !x.W || !x.OS || !x.G || !x.X || !x.Y || !x.cur || !x.tmp || !seq_t || !seq_k ||
+    if (!x.sv || !x.W || !x.OS || !x.G || !x.GC || !x.X || !x.Y || !x.cur || !x.tmp || !seq_t || !seq_k ||
         !len || !pos || !nf || !nb || !nf0 || !nb0 || !em || !emk || !fin || !pk) { rc = -3; goto out; }
     memset(x.sv, 0xff, sizeof(int32_t) * (size_t)P * x.R * K * x.nslot);
     memset(x.G, 0xff, sizeof(int32_t) * (size_t)P * x.R * x.nps);
+    memset(x.GC, 0xff, sizeof(int32_t) * (size_t)P * x.R * x.nps);
     memset(x.OS, 0xff, sizeof(int32_t) * (size_t)P * x.R * x.nps);
     memset(x.W, 0xff, sizeof(int32_t) * (size_t)P * x.R * x.nps);
     /* resident tensors */
@@ -1703,9 +1803,9 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     for (s = 0; s < P; s++) {
         double f = 0.0;
         uint64_t q = 0;
-        for (r = 0; r < D * H; r++) {
-            if (fin[s * D * H + r] > f) f = fin[s * D * H + r];
-            if (pk[s * D * H + r] > q) q = pk[s * D * H + r];
+        for (r = 0; r < x.S * D * H; r++) {
+            if (fin[s * x.S * D * H + r] > f) f = fin[s * x.S * D * H + r];
+            if (pk[s * x.S * D * H + r] > q) q = pk[s * x.S * D * H + r];
         }
         if (stage_finish) stage_finish[s] = f;
         if (stage_peak) stage_peak[s] = q;
@@ -1715,7 +1815,7 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     res->n_ops = (uint64_t)g.program_ops;
     if (dm->mem_cap_bytes != 0 && res->cand_peak > dm->mem_cap_bytes) res->status |= ST_OVER_CAP;
 out:
-    free(x.l0); free(x.sv); free(x.W); free(x.OS); free(x.G); free(x.X); free(x.Y);
+    free(x.l0); free(x.sv); free(x.W); free(x.OS); free(x.G); free(x.GC); free(x.X); free(x.Y);
     free(x.cur); free(x.tmp);
     free(seq_t); free(seq_k); free(len); free(pos); free(nf); free(nb); free(nf0); free(nb0);
     free(em); free(emk); free(fin); free(pk);

@@ -46,6 +46,7 @@ class ModelSpec:
     schedule: int = 0   # SCHED_1F1B or SCHED_GPIPE
     recompute: int = 0  # 1: activation recomputation (gradient checkpointing), training only
     zero: int = 0       # 1: ZeRO parameter/gradient partitioning over the data-parallel replicas, training only
+    overlap: int = 0    # 1: two streams per GPU, the data-parallel gradient all-reduce overlapping the backward pass
 
 
 @dataclass(frozen=True)
@@ -63,6 +64,10 @@ class DeviceSpec:
     # and sends and collectives spanning nodes cross this network link;
     # None: one uniform interconnect
     network: tuple = None
+    # (streams_per_gpu, bytes/s, latency s): devices d are streams of GPU
+    # d // streams_per_gpu, and sends and collectives among the streams of
+    # one GPU cost this (bytes/s may be inf); None: one device per GPU
+    streams: tuple = None
 
 
 @dataclass(frozen=True)
@@ -92,13 +97,14 @@ class Workload:
     tables: RandomTablesSpec = None
 
 
-def mlp(n_layers, d, batch, elem_bytes, mode, schedule=0, recompute=0, zero=0):
-    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes, schedule, recompute, zero)
+def mlp(n_layers, d, batch, elem_bytes, mode, schedule=0, recompute=0, zero=0, overlap=0):
+    return ModelSpec(MLP, mode, n_layers, 1, d, d, 1, 1, batch, elem_bytes, schedule, recompute, zero, overlap)
 
 
-def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None, schedule=0, recompute=0, zero=0):
+def transformer(n_layers, d, heads, seq, vocab, batch, elem_bytes, mode, d_ff=None, schedule=0, recompute=0, zero=0,
+                overlap=0):
     return ModelSpec(TRANSFORMER, mode, n_layers, heads, d, d_ff or 4 * d, seq, vocab, batch, elem_bytes, schedule,
-                     recompute, zero)
+                     recompute, zero, overlap)
 
 
 TINY_MLP = Workload("tiny_mlp", mlp(4, 256, 64, 4, TRAIN_SGD), GridSpec(4, 0, 0, 4))

@@ -859,9 +859,14 @@ def test_bounds(orc, case):
 # ---------------------------------------------------------------------------
 def link(dev, devs):
     """(latency, bandwidth) of the link a communication op crosses: the
-    network when its devices lie in more than one node."""
+    streams' own when its devices are streams of one GPU, the network when
+    their GPUs lie in more than one node."""
+    st = getattr(dev, "streams", None)
+    S = st[0] if st is not None and st[0] > 1 else 1
+    if S > 1 and len({d // S for d in devs}) == 1:
+        return st[2], st[1]
     net = dev.network
-    if net is not None and net[0] > 0 and len({d // net[0] for d in devs}) > 1:
+    if net is not None and net[0] > 0 and len({d // S // net[0] for d in devs}) > 1:
         return net[2], net[1]
     return dev.link_latency_s, dev.link_bytes_per_s
 
@@ -981,6 +986,9 @@ def test_table_brute_force(orc, seed):
     dev = DEV if seed % 2 == 0 else replace(DEV, matmul=(3e-6, 1.3e-14, 2.1e-12))
     if seed % 3 == 1:
         dev = replace(dev, network=(int(rng.integers(1, 5)), 3.1e9, 1.7e-5))
+    if seed % 5 >= 3:
+        # streams: 2..4 per GPU, sometimes with no byte term at all
+        dev = replace(dev, streams=(int(rng.integers(2, 5)), [9.3e10, math.inf][seed % 2], 1.1e-6))
     r = orc.sim_table(tab, n_dev, dev, init_live=init)
     clk, peak, st = table_brute(tab, n_dev, dev, [int(v) for v in init])
     assert list(r["finish"]) == clk
@@ -1285,3 +1293,164 @@ def test_topk_against_sort(orc, seed):
     assert found == len(order)
     assert list(idx[:found]) == list(order)
     assert np.all(idx[found:] == -1) and np.all(np.isinf(mo[found:]))
+
+
+# ---------------------------------------------------------------------------
+# Streams and overlap (Sec. 2.2, Limitations: one device per stream, the
+# streams of one GPU communicating at low or zero cost)
+# ---------------------------------------------------------------------------
+STREAMS = (2, 64.0, 0.125)   # two streams per GPU, their own bandwidth and latency
+
+
+def test_table_stream_hand_trace(orc):
+    """Four devices, two streams per GPU, GPUs in nodes of one: a send
+    between the streams of GPU 0, a send from GPU 0 to GPU 1 (which crosses
+    the network), an all-reduce over the streams of GPU 1 and one over all
+    four."""
+    dev = DeviceSpec(1.0, 1.0, 4.0, 0.5, 0.25, 0, network=(1, 2.0, 1.5), streams=STREAMS)
+    code = np.array([1 | 0 << 8 | 1 << 16, 1 | 1 << 8 | 2 << 16, 2 | 0b1100 << 16, 2 | 0b1111 << 16], np.uint32)
+    tab = dict(code=code, flops=np.zeros(4, np.float32), bytes=np.array([8, 8, 8, 8], np.float32),
+               alloc=np.zeros(4, np.uint32), free=np.zeros(4, np.uint32))
+    r = orc.sim_table(tab, 4, dev)
+    # send 0->1 (one GPU): 0.125 + 8/64 = 0.25 on d0, d1
+    # send 1->2 (GPU 0 -> GPU 1, other node): 0.25 + 1.5 + 8/2 = 5.75 on d1, d2
+    # AR {2,3} (one GPU): 5.75 + 2*0.125 + (2/2)*(8/64) = 6.125 on d2, d3
+    # AR over all (two nodes): 6.125 + 6*1.5 + (6/4)*(8/2) = 21.125
+    assert list(r["finish"]) == [21.125] * 4
+    # without nodes the GPU-to-GPU hops take the links
+    r = orc.sim_table(tab, 4, replace(dev, network=None))
+    # 0.25; 0.25 + 0.5 + 2 = 2.75; 2.75 + 0.25 + 0.125 = 3.125; 3.125 + 3 + 1.5*2 = 9.125
+    assert list(r["finish"]) == [9.125] * 4
+
+
+def test_stream_cost_can_be_zero(orc):
+    """A stream hop with zero latency and unbounded bandwidth costs nothing,
+    whatever it carries."""
+    dev = replace(DEV, streams=(2, math.inf, 0.0))
+    assert orc.cost_on_one_gpu(dev, orc.SEND, 1e12, 2) == 0.0
+    assert orc.cost_on_one_gpu(dev, orc.ALLREDUCE, 1e12, 2) == 0.0
+    assert orc.cost_on_one_gpu(replace(DEV, streams=(2, 8.0, 0.5)), orc.SEND, 4.0, 2) == 1.0
+
+
+def test_overlap_by_hand(orc):
+    """The 2-layer MLP on D = 2 replicas (P = H = K = 1, SGD) with chosen op
+    durations: Gemm, Relu, loss and their gradients 1, a stream hand-over
+    1/2, a gradient all-reduce 3, an optimizer step 1.  Without overlap the
+    all-reduces follow the backward pass:
+      forward 4, loss 5, layer 1: 6, 7, 8, layer 0: 9, 10, 11,
+      then (all-reduce, step) per layer: 14, 15, 18, 19.
+    With overlap (computation stream c, communication stream m), layer 1's
+    weight gradient is final at 7: hand-over c = m = 7.5, all-reduce
+    m = 10.5, input gradient c = 8.5; layer 0: 9.5, 10.5, hand-over at
+    max(10.5, 10.5) -> 11, all-reduce m = 14, input gradient c = 12; the
+    update: hand-back at max(12, 14) -> 14.5, step 15.5, hand-back 16,
+    step 17."""
+    base = mlp(2, 64, 16, 4, TRAIN_SGD)
+    cost = {k: 1.0 for k in ("GEMM", "RELU", "LOSSGRAD", "RELUGRAD", "GEMMDW", "GEMMDX", "OPT")}
+    cost.update(STREAM=0.5, AR_DP=3.0)
+    plain = orc.sim_strategy(base, 2, 1, 1, 1, DEV, type_cost=cost)
+    assert plain["makespan"] == 19.0
+    dev = replace(DEV, streams=STREAMS)
+    ov = orc.sim_strategy(replace(base, overlap=1), 2, 1, 1, 1, dev, type_cost=cost)
+    assert list(ov["dev_finish"]) == [17.0, 16.0] * 2
+    assert ov["makespan"] == 17.0
+    # the communication stream allocates nothing; the computation stream's
+    # memory is that of the program without overlap
+    assert [int(v) for v in ov["dev_peak"][1::2]] == [0, 0]
+    assert np.array_equal(ov["dev_peak"][0::2], plain["dev_peak"])
+    # per replica and layer: two hand-overs; the all-reduce moves, one per layer
+    assert ov["n_ops"] == plain["n_ops"] + 2 * 2 * 2
+
+
+def test_overlap_without_partners_changes_nothing(orc):
+    """One data replica has no gradient to all-reduce: with overlap its
+    communication streams stay idle and everything else is unchanged."""
+    dev = replace(DEV, streams=STREAMS)
+    for m, H, P, K in ((mlp(4, 64, 48, 4, TRAIN_ADAM), 2, 2, 3),
+                       (transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM_MIXED, recompute=1), 2, 2, 2)):
+        plain = orc.sim_strategy(m, 1, H, P, K, DEV)
+        ov = orc.sim_strategy(replace(m, overlap=1), 1, H, P, K, dev)
+        assert ov["makespan"] == plain["makespan"] and ov["n_ops"] == plain["n_ops"]
+        assert np.array_equal(ov["dev_finish"][0::2], plain["dev_finish"])
+        assert np.array_equal(ov["dev_peak"][0::2], plain["dev_peak"])
+        assert not ov["dev_finish"][1::2].any() and not ov["dev_peak"][1::2].any()
+
+
+def test_overlap_with_free_communication_changes_nothing(orc):
+    """With free stream hand-overs and free gradient all-reduces the
+    communication stream never holds the computation stream back: every
+    computation stream finishes when the device does without overlap."""
+    dev = replace(DEV, streams=(2, math.inf, 0.0))
+    for m, D, H, P, K in ((mlp(4, 64, 48, 4, TRAIN_ADAM), 2, 2, 2, 3),
+                          (transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_SGD, schedule=SCHED_GPIPE), 2, 1, 2, 3)):
+        cost = {"AR_DP": 0.0}
+        plain = orc.sim_strategy(m, D, H, P, K, DEV, type_cost=cost)
+        ov = orc.sim_strategy(replace(m, overlap=1), D, H, P, K, dev, type_cost=cost)
+        assert np.array_equal(ov["dev_finish"][0::2], plain["dev_finish"])
+        assert ov["makespan"] == plain["makespan"]
+
+
+def test_overlap_hides_the_all_reduce(orc):
+    """When the gradient all-reduces are short next to the backward ops,
+    all of them but the last one's tail hide behind the backward pass: the
+    L-layer MLP on D = 2 (free hand-overs; backward ops 1, all-reduce a < 1,
+    step 1) ends at the backward pass's end, then the last gradient's
+    all-reduce minus the input gradient it overlaps (a - 1 < 0: nothing),
+    then the L steps, each preceded by a free hand-back."""
+    L, a = 4, 0.25
+    cost = {k: 1.0 for k in ("GEMM", "RELU", "LOSSGRAD", "RELUGRAD", "GEMMDW", "GEMMDX", "OPT")}
+    cost.update(STREAM=0.0, AR_DP=a)
+    m = mlp(L, 64, 16, 4, TRAIN_SGD)
+    ov = orc.sim_strategy(replace(m, overlap=1), 2, 1, 1, 1, replace(DEV, streams=STREAMS), type_cost=cost)
+    body = 2 * L + 1 + 3 * L
+    assert ov["makespan"] == body + L * 1.0
+    plain = orc.sim_strategy(m, 2, 1, 1, 1, DEV, type_cost=cost)
+    assert plain["makespan"] == body + L * (a + 1.0)
+
+
+OV_SYM_CASES = [
+    (mlp(6, 64, 48, 2, TRAIN_ADAM, overlap=1), 2, 2, 3, 5),
+    (mlp(4, 32, 48, 4, TRAIN_SGD, overlap=1, schedule=SCHED_GPIPE), 4, 1, 2, 3),
+    (transformer(4, 32, 4, 8, 100, 12, 2, TRAIN_ADAM_MIXED, overlap=1), 3, 2, 2, 3),
+    (transformer(5, 32, 4, 8, 101, 16, 2, TRAIN_ADAM, recompute=1, overlap=1), 4, 2, 2, 2),
+]
+
+
+@pytest.mark.parametrize("case", range(len(OV_SYM_CASES)))
+@pytest.mark.parametrize("net", [False, True])
+def test_overlap_projection_matches_full_program(orc, case, net):
+    """Every replica of a stage runs the same ops at the same times on both
+    streams; the projection onto one replica per stage (charging each
+    collective for its whole group) gives the full program's results."""
+    m, D, H, P, K = OV_SYM_CASES[case]
+    dev = replace(DEV, streams=(2, 5.1e11, 2e-6), network=(2, *NET) if net else None)
+    full = orc.sim_strategy(m, D, H, P, K, dev)
+    proj = orc.sim_strategy(m, D, H, P, K, dev, slice=True)
+    assert full["status"] == 0
+    fin = full["dev_finish"].reshape(P, D * H, 2)
+    pk = full["dev_peak"].reshape(P, D * H, 2)
+    assert np.all(fin == fin[:, :1]) and np.all(pk == pk[:, :1])
+    assert not pk[:, :, 1].any()
+    assert proj["makespan"] == full["makespan"]
+    assert np.array_equal(proj["stage_finish"], full["stage_finish"])
+    assert np.array_equal(proj["stage_peak"], full["stage_peak"])
+    assert proj["n_ops"] == full["n_ops"] and proj["cand_peak"] == full["cand_peak"]
+    plain = orc.sim_strategy(replace(m, overlap=0), D, H, P, K, replace(dev, streams=None))
+    assert np.array_equal(full["stage_peak"], plain["stage_peak"])
+    # two hand-overs per replica and parameter tensor
+    n_par = (m.n_layers if m.family == 0 else 4 * m.n_layers + 2)
+    assert full["n_ops"] == plain["n_ops"] + 2 * D * H * n_par
+
+
+def test_overlap_needs_two_streams_per_gpu(orc):
+    """The overlapped program places two streams on every GPU; a device
+    model that says otherwise, or ZeRO with overlap, is refused."""
+    m = mlp(4, 64, 48, 4, TRAIN_ADAM)
+    with pytest.raises(ValueError):
+        orc.sim_strategy(replace(m, overlap=1), 2, 1, 2, 1, DEV)
+    with pytest.raises(ValueError):
+        orc.sim_strategy(replace(m, overlap=1), 2, 1, 2, 1, replace(DEV, streams=(3, 1e9, 0.0)))
+    with pytest.raises(ValueError):
+        orc.sim_strategy(replace(m, overlap=1, zero=1), 2, 1, 2, 1, replace(DEV, streams=STREAMS))
+    with pytest.raises(ValueError):
+        orc.sim_strategy(m, 2, 1, 2, 1, replace(DEV, streams=STREAMS))
