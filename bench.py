@@ -146,7 +146,8 @@ def bench_random_tables(args, torch, dsim, W):
 
 
 PARAMETRIC = ("tiny_mlp", "large_mlp", "gpt2_small", "gpt2_small_train", "gpt3_175b", "gpt3_175b_gpipe",
-              "gpt3_175b_recompute", "gpt3_175b_zero", "gpt3_175b_mi355x")
+              "gpt3_175b_recompute", "gpt3_175b_zero", "gpt3_175b_overlap", "gpt3_175b_mi355x",
+              "gpt3_175b_mi355x_overlap")
 
 
 def bench_parametric(torch, dsim, W, reps, warmup=1):

@@ -94,7 +94,15 @@ DSIM_API const char *dsim_last_error(void);
  * d / node_size, and a send or collective whose devices lie in more than one
  * node crosses the network (net_bytes_per_s > 0, net_latency_s >= 0, both
  * finite) instead of the node's links (link_bytes_per_s, link_latency_s).
- * node_size = 0: one uniform interconnect, net_* ignored. */
+ * node_size = 0: one uniform interconnect, net_* ignored.
+ * streams_per_gpu = S > 1 models communication that overlaps computation the
+ * way Sec. 2.2 (Limitations) describes, one device per stream: device d is
+ * a stream of GPU d / S (nodes then hold node_size GPUs), and a send or
+ * collective whose devices are all streams of one GPU costs
+ * stream_latency_s (finite, >= 0) and stream_bytes_per_s (> 0, +inf for no
+ * byte term) in place of the links.  S = 0 or 1: every device is its own
+ * GPU, stream_* ignored.  The transform's devices follow model.overlap:
+ * S must be 2 with it and at most 1 without (else DSIM_EINVAL). */
 typedef struct {
     double flops_per_s, mem_bytes_per_s, link_bytes_per_s, link_latency_s, launch_s;
     uint64_t mem_cap_bytes;
@@ -102,6 +110,8 @@ typedef struct {
     double mm_c0, mm_c1, mm_c2;
     int32_t node_size;
     double net_bytes_per_s, net_latency_s;
+    int32_t streams_per_gpu;
+    double stream_bytes_per_s, stream_latency_s;
 } dsim_device_model;
 
 /* The sequential program the transform distributes (Sec. 4, Sec. 5):
@@ -139,7 +149,21 @@ typedef struct {
  *        all-reduce; every replica's gradient dies there) and only the owner
  *        runs the optimizer op, which consumes the reduced gradient.
  *        Broadcast and reduce over n devices cost (n-1) * lat +
- *        bytes * (1/B_link) (a pipelined chain; a Send for n = 2). */
+ *        bytes * (1/B_link) (a pipelined chain; a Send for n = 2).
+ *   overlap: 0 or 1 (not with zero).  1 = every GPU is two devices (Sec. 2.2,
+ *        Limitations: a device per stream), 2g computing and 2g + 1
+ *        communicating, and in training with D > 1 the data-parallel
+ *        gradient all-reduce runs on the communication streams, overlapping
+ *        the last backward block: once the last microbatch has finished a
+ *        weight gradient (its weight-gradient op, or its accumulation), each
+ *        replica hands it to its communication stream (a Send between the
+ *        GPU's two streams that allocates nothing: the streams share the
+ *        gradient's memory), and the communication streams of the D
+ *        replicas all-reduce it there; at the weight update each reduced
+ *        gradient is handed back (a Send, again allocating nothing) right
+ *        before its optimizer op.  Sends are blocking (Sec. 2.1), so a
+ *        hand-over waits for the communication stream's previous
+ *        all-reduce.  Requires device.streams_per_gpu == 2. */
 typedef struct {
     int32_t family, mode, n_layers, n_heads;
     int64_t d_model, d_ff, seq_len, vocab, global_batch;
@@ -147,6 +171,7 @@ typedef struct {
     int32_t schedule;
     int32_t recompute;
     int32_t zero;
+    int32_t overlap;
 } dsim_model;
 
 /* A candidate: data-parallel D, tensor-parallel H (the paper's T), pipeline
@@ -266,8 +291,10 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * taken in closed form per block, and its finish time is that of the owner
  * of its last parameter.  results.row_width must be >= every candidate's P;
  * a candidate with P > min(row_width, 64, n_layers) or K > 16383 gets
- * DSIM_ST_BAD_STRATEGY.  The transform: device p*(D*H) + d*H + h runs stage
- * p of data replica d, tensor rank h; contiguous stages (the first L mod P
+ * DSIM_ST_BAD_STRATEGY.  With model.overlap a stage's finish time and peak
+ * cover both streams of its GPUs.  The transform: GPU p*(D*H) + d*H + h
+ * runs stage p of data replica d, tensor rank h (one device per GPU, or
+ * two with model.overlap); contiguous stages (the first L mod P
  * get one extra layer); synchronous 1F1B (forward only in inference) with
  * uneven microbatches (the first rows mod K get one extra row); Megatron
  * column/row tensor parallelism; each gradient is all-reduced over the D
@@ -288,8 +315,10 @@ DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsi
  * n_cand strategies (device array `cand`) of `model` -- every op of every
  * device, the transform of Sec. 4 executed with the semantics of Sec. 2.1 --
  * as explicit op tables in the dsim_tables layout (op j of candidate c at
- * j * n_cand + c), so that dsim_simulate_tables simulates it.  Device
- * p*(D*H) + d*H + h runs stage p of data replica d, tensor rank h.  The
+ * j * n_cand + c), so that dsim_simulate_tables simulates it.  GPU
+ * g = p*(D*H) + d*H + h runs stage p of data replica d, tensor rank h, as
+ * device g, or with model.overlap as devices 2g (computation) and 2g + 1
+ * (communication), whose hand-overs are Sends of zero alloc and free.  The
  * program order interleaves devices, but each device's own op sequence is
  * the transform's: splits, then slot by slot the ready stages' blocks (a
  * compute op once per replica device, a tensor-parallel all-reduce once per
@@ -304,7 +333,7 @@ DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsi
  *   init_live: device array [n_cand * n_dev], bytes resident on each device
  *     at t = 0 (0 for devices the candidate does not use);
  *   status:    device array [n_cand]: 0, DSIM_ST_BAD_STRATEGY (the
- *     transform's preconditions fail, D*H*P > n_dev or K > 16383), or
+ *     transform's preconditions fail, more devices than n_dev (D*H*P, twice that with overlap) or K > 16383), or
  *     DSIM_ST_NOT_TABLE (more than max_ops ops, a FLOP or byte count not
  *     exact in fp32, or an alloc / free size above 2^32 - 1).
  * 1 <= n_dev <= 8, max_ops >= 0.  One GPU lane per candidate.

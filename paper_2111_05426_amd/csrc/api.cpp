@@ -46,6 +46,9 @@ CostConsts make_consts(const dsim_device_model &m)
     c.node = m.node_size > 0 ? m.node_size : 0;
     c.net_lat = c.node ? m.net_latency_s : 0.0;
     c.net_inv_l = c.node ? 1.0 / m.net_bytes_per_s : 0.0;
+    c.streams = m.streams_per_gpu > 1 ? m.streams_per_gpu : 0;
+    c.st_lat = c.streams ? m.stream_latency_s : 0.0;
+    c.st_inv_l = c.streams ? 1.0 / m.stream_bytes_per_s : 0.0;   // +inf bandwidth: no byte term
     c.ar_lat[0] = 0.0;
     c.ar_coef[0] = 0.0;
     for (int n = 1; n <= kMaxTableDev; ++n) {
@@ -53,6 +56,7 @@ CostConsts make_consts(const dsim_device_model &m)
         c.ar_lat[n] = two_a * m.link_latency_s;
         c.ar_coef[n] = two_a / (double)n;
         c.ar_lat_net[n] = two_a * c.net_lat;
+        c.ar_lat_st[n] = two_a * c.st_lat;
     }
     return c;
 }
@@ -73,6 +77,10 @@ static dsim_status check_device(const dsim_device_model *m)
     if (m->node_size < 0) return fail(DSIM_EINVAL, "node_size must be >= 0");
     if (m->node_size > 0 && (!finite_pos(m->net_bytes_per_s) || !finite_nonneg(m->net_latency_s)))
         return fail(DSIM_EINVAL, "network bandwidth must be finite and > 0, latency finite and >= 0");
+    if (m->streams_per_gpu < 0 || m->streams_per_gpu > (1 << 20))
+        return fail(DSIM_EINVAL, "streams_per_gpu must be in 0..2^20");
+    if (m->streams_per_gpu > 1 && (!(m->stream_bytes_per_s > 0.0) || !finite_nonneg(m->stream_latency_s)))
+        return fail(DSIM_EINVAL, "stream bandwidth must be > 0 (inf allowed), latency finite and >= 0");
     return DSIM_OK;
 }
 
@@ -90,6 +98,8 @@ static dsim_status check_model(const dsim_model *m)
         return fail(DSIM_EINVAL, "unknown schedule %d", m->schedule);
     if (m->recompute != 0 && m->recompute != 1) return fail(DSIM_EINVAL, "recompute must be 0 or 1");
     if (m->zero != 0 && m->zero != 1) return fail(DSIM_EINVAL, "zero must be 0 or 1");
+    if (m->overlap != 0 && m->overlap != 1) return fail(DSIM_EINVAL, "overlap must be 0 or 1");
+    if (m->overlap && m->zero) return fail(DSIM_EINVAL, "overlap and zero cannot be combined");
     if (m->family == DSIM_TRANSFORMER) {
         if (m->n_heads < 1 || m->d_ff < 1 || m->seq_len < 1 || m->vocab < 1)
             return fail(DSIM_EINVAL, "transformer needs n_heads, d_ff, seq_len, vocab >= 1");
@@ -191,6 +201,10 @@ dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strateg
     if (st) return st;
     st = check_device(device);
     if (st) return st;
+    if (model->overlap ? device->streams_per_gpu != 2 : device->streams_per_gpu > 1)
+        return fail(DSIM_EINVAL, "the transform places %s; the device model has streams_per_gpu = %d",
+                    model->overlap ? "two streams on every GPU (overlap)" : "one device on every GPU",
+                    device->streams_per_gpu);
     if (!results) return fail(DSIM_EINVAL, "results must not be NULL");
     if (n_cand < 0 || n_cand > ((int64_t)1 << 40)) return fail(DSIM_EINVAL, "bad n_cand");
     if (n_cand == 0) return DSIM_OK;

@@ -31,9 +31,13 @@ struct CostConsts {
     int32_t node;      // devices per node, 0 = one uniform interconnect
     double net_lat;    // network latency (ops spanning nodes)
     double net_inv_l;  // 1 / network bytes per second
+    int32_t streams;   // devices (streams) per GPU, 0 = one device per GPU
+    double st_lat;     // latency between the streams of one GPU
+    double st_inv_l;   // 1 / their bytes per second (0: no byte term)
     double ar_lat[kMaxTableDev + 1];
     double ar_coef[kMaxTableDev + 1];
     double ar_lat_net[kMaxTableDev + 1];   // (2(n-1)) * net_lat
+    double ar_lat_st[kMaxTableDev + 1];    // (2(n-1)) * st_lat
 };
 
 CostConsts make_consts(const dsim_device_model &m);

@@ -13,7 +13,11 @@
 // With ZeRO (Fig. 9) a weight read is preceded by a broadcast record from
 // its owner per tensor rank, the reading op also frees the copy on the other
 // replicas, and each gradient all-reduce becomes a reduce record onto the
-// owner followed by the owner's optimizer op.
+// owner followed by the owner's optimizer op.  With overlap every GPU g is
+// two devices, 2g computing and 2g + 1 communicating: the last backward
+// block hands each finished gradient over (a Send of zero alloc and free
+// per replica, then an all-reduce over the communication streams per tensor
+// rank), and the weight update hands each one back before its optimizer op.
 // The records go to the op-major, candidate-fastest table layout that
 // dsim_simulate_tables reads.
 #include "model.h"
@@ -47,9 +51,13 @@ struct Emit {
     int64_t c;
     int64_t j;          // records emitted so far (may pass max_ops: counted, not written)
     bool inexact;       // a value does not fit the record format exactly
-    int base;           // first device of the stage
+    int base;           // first GPU of the stage
     uint64_t pend;      // ZeRO: bytes of the broadcast copy the next op frees on non-owners
     int pend_owner;     // ZeRO: the replica that owns it
+    int S;              // devices per GPU: 1, or 2 with overlap
+
+    // the computation device of GPU gpu (its communication stream is the next one)
+    __device__ __forceinline__ uint32_t dv(int gpu) const { return (uint32_t)(S * gpu); }
 
     __device__ __forceinline__ void put(uint32_t code, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
     {
@@ -71,7 +79,7 @@ struct Emit {
     {
         for (int r = 0; r < x.D * x.H; ++r) {
             const uint64_t copy = (pend != 0 && r / x.H != pend_owner) ? pend : 0;
-            put(((uint32_t)(base + r) << 8) | (cls << 24), fl, by, al, fr + copy);
+            put((dv(base + r) << 8) | (cls << 24), fl, by, al, fr + copy);
         }
         pend = 0;
     }
@@ -85,7 +93,7 @@ struct Emit {
         if (!x.zero) return;
         const int o = grp % x.D;
         for (int h = 0; h < x.H; ++h)
-            put(3u | ((uint32_t)(base + o * x.H + h) << 8) | (dp_mask(h) << 16), 0, by, by, 0);
+            put(3u | (dv(base + o * x.H + h) << 8) | (dp_mask(h) << 16), 0, by, by, 0);
         pend = by;
         pend_owner = o;
     }
@@ -95,25 +103,27 @@ struct Emit {
     {
         const int o = grp % x.D;
         for (int h = 0; h < x.H; ++h)
-            put(4u | ((uint32_t)(base + o * x.H + h) << 8) | (dp_mask(h) << 16), 0, by, by, by);
+            put(4u | (dv(base + o * x.H + h) << 8) | (dp_mask(h) << 16), 0, by, by, by);
     }
     __device__ void owner_local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, int grp)
     {
         const int o = grp % x.D;
-        for (int h = 0; h < x.H; ++h) put((uint32_t)(base + o * x.H + h) << 8, fl, by, al, fr);
+        for (int h = 0; h < x.H; ++h) put(dv(base + o * x.H + h) << 8, fl, by, al, fr);
     }
-    // the D replicas of tensor rank h on this stage
-    __device__ uint32_t dp_mask(int h) const
+    // the D replicas of tensor rank h on this stage (stream 0: computation,
+    // 1: communication)
+    __device__ uint32_t dp_mask(int h, int stream = 0) const
     {
         uint32_t mask = 0;
-        for (int d = 0; d < x.D; ++d) mask |= 1u << (base + d * x.H + h);
+        for (int d = 0; d < x.D; ++d) mask |= 1u << (dv(base + d * x.H + h) + (uint32_t)stream);
         return mask;
     }
     __device__ void ar_tp(uint64_t by)
     {
         if (x.H <= 1) return;
         for (int d = 0; d < x.D; ++d) {
-            const uint32_t mask = ((1u << x.H) - 1u) << (base + d * x.H);
+            uint32_t mask = 0;
+            for (int h = 0; h < x.H; ++h) mask |= 1u << dv(base + d * x.H + h);
             put(2u | (mask << 16), 0, by, 0, 0);
         }
     }
@@ -126,7 +136,19 @@ struct Emit {
     {
         const int tbase = t * x.D * x.H;
         for (int r = 0; r < x.D * x.H; ++r)
-            put(1u | ((uint32_t)(base + r) << 8) | ((uint32_t)(tbase + r) << 16), 0, sz, sz, fre);
+            put(1u | (dv(base + r) << 8) | (dv(tbase + r) << 16), 0, sz, sz, fre);
+    }
+    // overlap: each replica hands the finished gradient to its communication
+    // stream (nothing allocated or freed), whose D replicas all-reduce it
+    __device__ void handover(uint64_t by)
+    {
+        for (int r = 0; r < x.D * x.H; ++r) put(1u | (dv(base + r) << 8) | ((dv(base + r) + 1u) << 16), 0, by, 0, 0);
+        for (int h = 0; h < x.H; ++h) put(2u | (dp_mask(h, 1) << 16), 0, by, 0, 0);
+    }
+    // overlap: the reduced gradient comes back to the computation stream
+    __device__ void handback(uint64_t by)
+    {
+        for (int r = 0; r < x.D * x.H; ++r) put(1u | ((dv(base + r) + 1u) << 8) | (dv(base + r) << 16), 0, by, 0, 0);
     }
 };
 
@@ -139,8 +161,9 @@ __global__ __launch_bounds__(kLanes) void k_materialize(const MatArgs g)
     if (c >= g.n_cand) return;
     const dsim_strategy st = g.cand[c];
     for (int dev = 0; dev < g.n_dev; ++dev) g.init_live[c * g.n_dev + dev] = 0;
+    const int S = g.m.overlap ? 2 : 1;
     const bool ok = strategy_ok(g.m, st.D, st.H, st.P, st.K) && st.K <= kMaxK &&
-                    (int64_t)st.D * st.H * st.P <= (int64_t)g.n_dev;
+                    (int64_t)S * st.D * st.H * st.P <= (int64_t)g.n_dev;
     if (!ok) {
         g.n_ops[c] = 0;
         g.status[c] = DSIM_ST_BAD_STRATEGY;
@@ -150,7 +173,7 @@ __global__ __launch_bounds__(kLanes) void k_materialize(const MatArgs g)
     Ctx x = {};
     make_ctx(g.m, none, st, x);
     const int DH = x.D * x.H;
-    Emit e{x, g, c, 0, false, 0, 0, 0};
+    Emit e{x, g, c, 0, false, 0, 0, 0, S};
     for (int s = 0; s < x.P; ++s) {
         if (x.zero) {
             // each data replica holds the groups it owns
@@ -159,8 +182,9 @@ __global__ __launch_bounds__(kLanes) void k_materialize(const MatArgs g)
             const uint64_t in = resident_inputs(x, s);
             for (int r = 0; r < DH; ++r) g.init_live[c * g.n_dev + s * DH + r] = in + z_owned(x, zs, r / x.H);
         } else {
+            // (a communication stream holds nothing)
             const uint64_t r0 = resident(x, s);
-            for (int r = 0; r < DH; ++r) g.init_live[c * g.n_dev + s * DH + r] = r0;
+            for (int r = 0; r < DH; ++r) g.init_live[c * g.n_dev + e.dv(s * DH + r)] = r0;
         }
         s_pos[s][lane] = 0;
         s_nf[s][lane] = 0;

@@ -28,6 +28,16 @@
 //                                        the gradients die there)
 //   o.owner_local(fl, by, al, fr, grp)   ZeRO: compute op on the owner of
 //                                        group grp only (its optimizer step)
+//   o.handover(bytes)                    overlap: the last microbatch has
+//                                        finished a weight gradient of
+//                                        `bytes`; every replica hands it to
+//                                        its GPU's communication stream (a
+//                                        Send between the GPU's two streams,
+//                                        allocating nothing), whose D
+//                                        replicas then all-reduce it there
+//   o.handback(bytes)                    overlap: the reduced gradient comes
+//                                        back to the computation stream
+//                                        (again a Send allocating nothing)
 //
 // Sinks: the parametric simulator (one replica per stage), the per-layer
 // cost recorder and the table materialiser.  Memory follows def/use
@@ -51,6 +61,7 @@ struct Ctx {
     int schedule;   // DSIM_SCHED_1F1B or DSIM_SCHED_GPIPE
     bool rc;        // activation recomputation (training only)
     bool zero;      // ZeRO partitioning (training only, D > 1)
+    bool ov;        // gradient all-reduce on the communication streams (training only, D > 1)
     uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
     uint64_t dH, FH, Vh, aH;
     double inv_f, inv_b, inv_l, lat, launch;
@@ -60,6 +71,7 @@ struct Ctx {
     double chl_d;   // (D - 1) * lat: latency part of a broadcast / reduce over the D replicas
     bool mm;        // matrix multiplications take the regression mm0 + mm1 * flops + mm2 * bytes
     double mm0, mm1, mm2;
+    double st_lat, st_inv_l;   // a Send between the two streams of one GPU
     uint64_t mult_dev, mult_tp, mult_dp;
 };
 
@@ -96,6 +108,7 @@ __device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const 
     x.train = M.mode != DSIM_INFER;
     x.rc = x.train && M.recompute != 0;
     x.zero = x.train && M.zero != 0 && x.D > 1;
+    x.ov = x.train && M.overlap != 0 && x.D > 1;
     x.q = x.L / x.P;
     x.r = x.L % x.P;
     x.e = (uint64_t)M.elem_bytes;
@@ -135,6 +148,8 @@ __device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const 
     x.mm0 = c.mm_c0;
     x.mm1 = c.mm_c1;
     x.mm2 = c.mm_c2;
+    x.st_lat = c.st_lat;
+    x.st_inv_l = c.st_inv_l;
     x.mult_dev = (uint64_t)x.D * (uint64_t)x.H;
     x.mult_tp = (uint64_t)x.D;
     x.mult_dp = (uint64_t)x.H;
@@ -165,6 +180,11 @@ __device__ __forceinline__ double cost_mm(const Ctx &x, uint64_t flops, uint64_t
 {
     if (!x.mm) return cost_local(x, flops, bytes);
     return (x.mm0 + x.mm1 * (double)flops) + x.mm2 * (double)bytes;
+}
+// a Send between the two streams of one GPU (overlap)
+__device__ __forceinline__ double cost_stream(const Ctx &x, uint64_t bytes)
+{
+    return x.st_lat + (double)bytes * x.st_inv_l;
 }
 // broadcast / reduce over the D replicas (ZeRO, Fig. 9): a pipelined chain,
 // D - 1 link latencies plus the bytes crossing one link once
@@ -242,10 +262,12 @@ __device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, in
 
 // One layer's backward.  frees_input: the stage's first layer, where the
 // stage input dies at the weight gradient; layer0: the model's first layer,
-// whose dX has no use and is not all-reduced; grp: the parameter group.
+// whose dX has no use and is not all-reduced; grp: the parameter group;
+// last: the stage's last backward block under overlap, which hands every
+// finished weight gradient over.
 template <class S>
 __device__ __forceinline__ void mlp_layer_bwd(const Ctx &x, S &o, uint64_t m, int kind, bool frees_input,
-                                              bool layer0, bool acc, int grp)
+                                              bool layer0, bool acc, int grp, bool last = false)
 {
     const uint64_t e = x.e;
     uint64_t din, dout;
@@ -254,6 +276,7 @@ __device__ __forceinline__ void mlp_layer_bwd(const Ctx &x, S &o, uint64_t m, in
     o.mm(2 * m * din * dout, e * (m * din + m * dout + din * dout), e * din * dout,
          frees_input ? e * m * din : 0);                                                // weight gradient
     if (acc) o.local(din * dout, 3 * e * din * dout, 0, e * din * dout);                // accumulate
+    if (last) o.handover(e * din * dout);
     o.bcast(e * din * dout, grp);
     o.mm(2 * m * din * dout, e * (m * dout + din * dout + m * din), e * m * din,
          e * m * dout + (layer0 ? e * m * din : 0));                                    // input gradient
@@ -368,7 +391,7 @@ __device__ __forceinline__ void tf_fwd_last(const Ctx &x, S &o, const TfSz &z)
 
 // last stage, before its layers' backward: loss, LM head and final LN grads
 template <class S>
-__device__ __forceinline__ void tf_bwd_last(const Ctx &x, S &o, const TfSz &z, bool acc)
+__device__ __forceinline__ void tf_bwd_last(const Ctx &x, S &o, const TfSz &z, bool acc, bool last = false)
 {
     const uint64_t T = z.T, d = x.d, e = x.e, Vh = x.Vh;
     o.local(3 * T * Vh, z.LOG + z.ST, z.ST, 0);                                   // loss statistics
@@ -379,29 +402,33 @@ __device__ __forceinline__ void tf_bwd_last(const Ctx &x, S &o, const TfSz &z, b
     o.ar_tp(z.ACT);
     o.mm(2 * T * d * Vh, e * (T * d + T * Vh + d * Vh), e * d * Vh, z.ACT + z.LOG);  // LM head dW
     if (acc) o.local(d * Vh, 3 * e * d * Vh, 0, e * d * Vh);
+    if (last) o.handover(e * d * Vh);
     o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                             // final LN grad
 }
 
 template <class S>
-__device__ __forceinline__ void tf_layer_bwd(const Ctx &x, S &o, const TfSz &z, bool acc, int grp)
+__device__ __forceinline__ void tf_layer_bwd(const Ctx &x, S &o, const TfSz &z, bool acc, int grp, bool last = false)
 {
     const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
     o.bcast(e * FH * d, grp);
     o.mm(2 * T * FH * d, e * (T * d + FH * d + T * FH), z.FF, 0);             // fc2 dX
     o.mm(2 * T * FH * d, e * (T * FH + T * d + FH * d), e * FH * d, z.FF);     // fc2 dW
     if (acc) o.local(FH * d, 3 * e * FH * d, 0, e * FH * d);
+    if (last) o.handover(e * FH * d);
     o.local(8 * T * FH, 3 * z.FF, z.FF, 2 * z.FF);                                // GeLU grad
     o.bcast(e * d * FH, grp);
     o.mm(2 * T * d * FH, e * (T * FH + d * FH + T * d), z.ACT, 0);             // fc1 dX
     o.ar_tp(z.ACT);
     o.mm(2 * T * d * FH, e * (T * d + T * FH + d * FH), e * d * FH, z.ACT + z.FF);  // fc1 dW
     if (acc) o.local(d * FH, 3 * e * d * FH, 0, e * d * FH);
+    if (last) o.handover(e * d * FH);
     o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                              // LN2 grad
     o.local(T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                  // residual merge
     o.bcast(e * dH * d, grp);
     o.mm(2 * T * dH * d, e * (T * d + dH * d + T * dH), z.OH, 0);              // out-proj dX
     o.mm(2 * T * dH * d, e * (T * dH + T * d + dH * d), e * dH * d, z.OH);     // out-proj dW
     if (acc) o.local(dH * d, 3 * e * dH * d, 0, e * dH * d);
+    if (last) o.handover(e * dH * d);
     o.mm(4 * T * S_ * dH, 2 * z.S2 + 3 * z.OH, z.S2 + z.QKV, z.OH);            // P.V grads
     o.local(5 * z.m * x.aH * S_ * S_, 3 * z.S2, z.S2, 2 * z.S2);                  // softmax grad
     o.mm(4 * T * S_ * dH, z.S2 + 4 * z.OH, 0, z.S2 + z.QKV);                   // Q.K^T grads
@@ -410,17 +437,19 @@ __device__ __forceinline__ void tf_layer_bwd(const Ctx &x, S &o, const TfSz &z, 
     o.ar_tp(z.ACT);
     o.mm(2 * T * d * 3 * dH, e * (T * d + T * 3 * dH + d * 3 * dH), e * d * 3 * dH, z.ACT + z.QKV);  // QKV dW
     if (acc) o.local(d * 3 * dH, 3 * e * d * 3 * dH, 0, e * d * 3 * dH);
+    if (last) o.handover(e * d * 3 * dH);
     o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                              // LN1 grad
     o.local(T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                  // residual merge
 }
 
 // stage 0, after its layers' backward: embedding gradient
 template <class S>
-__device__ __forceinline__ void tf_bwd_first(const Ctx &x, S &o, const TfSz &z, bool acc)
+__device__ __forceinline__ void tf_bwd_first(const Ctx &x, S &o, const TfSz &z, bool acc, bool last = false)
 {
     const uint64_t T = z.T, d = x.d, e = x.e, Vh = x.Vh;
     o.local(T * d, z.ACT + z.IDS + e * Vh * d, e * Vh * d, z.ACT + z.IDS);        // embedding dW
     if (acc) o.local(Vh * d, 3 * e * Vh * d, 0, e * Vh * d);
+    if (last) o.handover(e * Vh * d);
 }
 
 // ---------------------------------------------------------------------------
@@ -445,27 +474,30 @@ __device__ __forceinline__ void block_fwd(const Ctx &x, S &o, int s, int k)
     if (s == x.P - 1) tf_fwd_last(x, o, z);
 }
 
+// (under overlap the stage's last backward block, microbatch K - 1, hands
+// each weight gradient over as soon as it is finished)
 template <class S>
 __device__ __forceinline__ void block_bwd(const Ctx &x, S &o, int s, int k)
 {
     const uint64_t m = mb_rows(x, k);
     const bool acc = k >= 1;
+    const bool last = x.ov && k == x.K - 1;
     if (x.mlp) {
         const int l0 = stage_l0(x, s), l1 = l0 + stage_nl(x, s);
         if (s == x.P - 1) mlp_loss(x, o, m);
         if (x.rc)   // replay every layer but the last from the checkpoint
             for (int i = l0; i < l1 - 1; ++i) mlp_layer_fwd(x, o, m, mlp_kind(x, i), false, false, mlp_group(x, i));
         for (int i = l1 - 1; i >= l0; --i)
-            mlp_layer_bwd(x, o, m, mlp_kind(x, i), i == l0, i == 0, acc, mlp_group(x, i));
+            mlp_layer_bwd(x, o, m, mlp_kind(x, i), i == l0, i == 0, acc, mlp_group(x, i), last);
         return;
     }
     const TfSz z = tf_sizes(x, m);
-    if (s == x.P - 1) tf_bwd_last(x, o, z, acc);
+    if (s == x.P - 1) tf_bwd_last(x, o, z, acc, last);
     const int nl = stage_nl(x, s), l0 = stage_l0(x, s);
     if (x.rc)   // replay the layers from the checkpoint, the last one up to its GeLU
         for (int i = 0; i < nl; ++i) tf_layer_fwd(x, o, z, true, true, i < nl - 1, tf_group_layer(l0 + i));
-    for (int i = nl - 1; i >= 0; --i) tf_layer_bwd(x, o, z, acc, tf_group_layer(l0 + i));
-    if (s == 0) tf_bwd_first(x, o, z, acc);
+    for (int i = nl - 1; i >= 0; --i) tf_layer_bwd(x, o, z, acc, tf_group_layer(l0 + i), last);
+    if (s == 0) tf_bwd_first(x, o, z, acc, last);
 }
 
 // ---------------------------------------------------------------------------
@@ -496,7 +528,8 @@ __device__ __forceinline__ uint64_t opt_state(const Ctx &x, uint64_t N)
 // one parameter tensor of group grp: all-reduce its gradient over the D
 // replicas, then the optimizer op (in place), after which the gradient dies.
 // ZeRO: reduce the gradients onto the owner (they die there), whose
-// optimizer op consumes the reduced gradient.
+// optimizer op consumes the reduced gradient.  Overlap: the gradient was
+// all-reduced on the communication streams; it comes back first.
 template <class S>
 __device__ __forceinline__ void wu_param(const Ctx &x, S &o, uint64_t N, int grp)
 {
@@ -507,7 +540,8 @@ __device__ __forceinline__ void wu_param(const Ctx &x, S &o, uint64_t N, int grp
         o.owner_local(fl, by, 0, x.e * N, grp);
         return;
     }
-    o.ar_dp(x.e * N);
+    if (x.ov) o.handback(x.e * N);
+    else o.ar_dp(x.e * N);
     o.local(fl, by, 0, x.e * N);
 }
 

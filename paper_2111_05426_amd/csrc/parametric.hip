@@ -131,17 +131,42 @@ __device__ __forceinline__ int seg_class(const dsim_strategy &st, int p_bound)
 // ---------------------------------------------------------------------------
 // Sinks
 // ---------------------------------------------------------------------------
-// The lane's stage replica, op by op (splits and the weight update).  With
-// ZeRO, live counts the largest owned resident and z describes the stage's
-// ownership: a reduce samples the owner holding the reduced gradient and the
-// other replicas, then every gradient dies; the owner's optimizer op frees
-// the reduced gradient again (below that sample).
+// The lane's stage replica, op by op (splits, the weight update and, under
+// overlap, the last backward block).  With ZeRO, live counts the largest
+// owned resident and z describes the stage's ownership: a reduce samples the
+// owner holding the reduced gradient and the other replicas, then every
+// gradient dies; the owner's optimizer op frees the reduced gradient again
+// (below that sample).  Under overlap tm is the communication stream's
+// clock: a hand-over or hand-back is a Send between the two streams (both
+// clocks meet at its end), the all-reduce advances tm alone (every replica's
+// communication stream is at the same time).
 struct Walk {
     const Ctx &x;
     double clk;
     int64_t live, peak;
     uint64_t walked, nops;
     const ZStage *z;
+    double tm = 0.0;
+
+    __device__ __forceinline__ void meet(uint64_t by)
+    {
+        const double st = clk > tm ? clk : tm;
+        clk = st + cost_stream(x, by);
+        tm = clk;
+    }
+    __device__ __forceinline__ void handover(uint64_t by)
+    {
+        meet(by);
+        tm = tm + cost_ar_dp(x, by);
+        walked += 2;
+        nops += x.mult_dev + x.mult_dp;
+    }
+    __device__ __forceinline__ void handback(uint64_t by)
+    {
+        meet(by);
+        walked += 1;
+        nops += x.mult_dev;
+    }
 
     __device__ __forceinline__ void op(double c, uint64_t al, uint64_t fr)
     {
@@ -255,6 +280,9 @@ struct Record {
     {
         put(cost_local(x, fl, by));
     }
+    // recorded programs hold no last block of an overlapped stage
+    __device__ __forceinline__ void handover(uint64_t) {}
+    __device__ __forceinline__ void handback(uint64_t) {}
 };
 
 // Memory summary only (net bytes, peak above the start), no costs.
@@ -273,6 +301,8 @@ struct Mem {
     __device__ __forceinline__ void bcast(uint64_t, int) {}
     __device__ __forceinline__ void reduce(uint64_t, int) {}
     __device__ __forceinline__ void owner_local(uint64_t, uint64_t, uint64_t, uint64_t, int) {}
+    __device__ __forceinline__ void handover(uint64_t) {}   // allocates nothing
+    __device__ __forceinline__ void handback(uint64_t) {}
 };
 
 // ZeRO memory summary of ops that read the weights of one parameter group:
@@ -303,6 +333,8 @@ struct MemZ {
     }
     __device__ __forceinline__ void reduce(uint64_t, int) {}
     __device__ __forceinline__ void owner_local(uint64_t, uint64_t, uint64_t, uint64_t, int) {}
+    __device__ __forceinline__ void handover(uint64_t) {}   // allocates nothing
+    __device__ __forceinline__ void handback(uint64_t) {}
 };
 
 // Liveness of a forward unit.  kFwdBlock: as in a forward block (training
@@ -468,25 +500,43 @@ struct Count {
         walked += 1;
         nops += x.mult_dp;
     }
+    // overlap: a hand-over per replica and an all-reduce per tensor rank; a hand-back per replica
+    __device__ __forceinline__ void handover(uint64_t)
+    {
+        walked += 2;
+        nops += x.mult_dev + x.mult_dp;
+    }
+    __device__ __forceinline__ void handback(uint64_t)
+    {
+        walked += 1;
+        nops += x.mult_dev;
+    }
 };
 
 // ops of stage s's blocks and sends: K forward blocks; in training one
-// backward block without and K - 1 with gradient accumulation.  Op counts do
-// not depend on the microbatch size.
+// backward block without and K - 1 with gradient accumulation, the last of
+// which hands the gradients over under overlap.  Op counts do not depend on
+// the microbatch size.
 __device__ __forceinline__ void count_blocks(const Ctx &x, int s, uint64_t &walked, uint64_t &nops)
 {
-    Count f{x, 0, 0}, b0{x, 0, 0}, b1{x, 0, 0};
+    Count f{x, 0, 0}, b0{x, 0, 0}, b1{x, 0, 0}, bl{x, 0, 0};
     block_fwd(x, f, s, 0);
     const uint64_t K = (uint64_t)x.K;
     const uint64_t fs = s < x.P - 1 ? 1 : 0;   // Send after each forward block
     walked += K * (f.walked + fs);
     nops += K * (f.nops + fs * x.mult_dev);
     if (!x.train) return;
-    block_bwd(x, b0, s, 0);
-    block_bwd(x, b1, s, 1);
     const uint64_t bs = s > 0 ? 1 : 0;         // Send after each backward block
-    walked += b0.walked + (K - 1) * b1.walked + K * bs;
-    nops += b0.nops + (K - 1) * b1.nops + K * bs * x.mult_dev;
+    walked += K * bs;
+    nops += K * bs * x.mult_dev;
+    block_bwd(x, b0, s, 0);                    // microbatch 0 (the last one if K = 1)
+    walked += b0.walked;
+    nops += b0.nops;
+    if (K == 1) return;
+    block_bwd(x, b1, s, 1);                    // microbatches 1 .. K-2 (K >= 3)
+    block_bwd(x, bl, s, x.K - 1);              // microbatch K-1
+    walked += (K - 2) * b1.walked + bl.walked;
+    nops += (K - 2) * b1.nops + bl.nops;
 }
 
 // ---------------------------------------------------------------------------
@@ -863,9 +913,11 @@ __device__ void record_lane(const Ctx &x, int s, bool bwd, uint64_t m, bool acc,
 
 // WIDE: the launch for wide segments of a transformer; otherwise every class
 // of an MLP, or the narrow classes of a transformer.  RC: training with
-// activation recomputation; ZR: training with ZeRO (separate instantiations
-// keep the replay and the broadcasts out of the other kernels).
-template <bool TF, bool WIDE, bool RC, bool ZR>
+// activation recomputation; ZR: training with ZeRO; OV: training with the
+// gradient all-reduce on the communication streams (separate instantiations
+// keep the replay, the broadcasts and the two-stream walk out of the other
+// kernels).
+template <bool TF, bool WIDE, bool RC, bool ZR, bool OV>
 __device__ __forceinline__ void parametric_body(const ParArgs &g)
 {
     using Sh = Shape<TF, ZR>;
@@ -900,6 +952,8 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     int32_t status = (c >= 0 && !ok) ? DSIM_ST_BAD_STRATEGY : 0;
 
     double clk = 0.0;
+    double clkm = 0.0;   // overlap: the communication stream's clock
+    const bool ov_c = OV && train && M.overlap != 0 && st.D > 1;
     int64_t live = 0, peak = 0;
     uint64_t walked = 0, nops = 0;
     uint64_t mq = 0, rb_f = 0, rb_b = 0;   // rows of a short microbatch; Send bytes per row
@@ -1074,8 +1128,26 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
             const int nr = bwd ? n_r : 0, np = bwd ? n_part : 0;
             int64_t delta = 0, top = 0;
             bool lane_done = false;
+            if constexpr (OV) {
+                if (ov_c && bwd && k == K - 1) {
+                    // the last backward block under overlap hands each
+                    // finished gradient to the communication stream: walked
+                    // op by op with both clocks, memory as it goes
+                    Ctx x = {};
+                    make_ctx(M, g.c, st, x);
+                    x.mlp = !TF;
+                    Walk w{x, clk, live, live, 0, 0, nullptr};
+                    w.tm = clkm;
+                    block_bwd(x, w, s, k);
+                    clk = w.clk;
+                    clkm = w.tm;
+                    delta = w.live - live;
+                    top = w.peak - live;
+                    lane_done = true;
+                }
+            }
             if constexpr (!WIDE) {
-                if (!shared) {
+                if (!shared && !lane_done) {
                     double2 *pp = &L.a.prog[d][0][lane];
                     if ((bwd ? key_b : key_f) != key || (replay && bwd && key_f != mc)) {
                         Ctx x = {};
@@ -1245,8 +1317,11 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         ZStage zs;
         if (ZR && x.zero) z_stage(x, s, zs);
         Walk w{x, clk, live, peak, walked, nops, &zs};
+        w.tm = clkm;
         if (train) weight_update(x, w, s);
-        clk = w.clk;
+        // the stage's latest device (under overlap the computation stream
+        // ends last: its final op is an optimizer step after a hand-back)
+        clk = w.clk > w.tm ? w.clk : w.tm;
         live = w.live;
         peak = w.peak;
         walked = w.walked;
@@ -1284,36 +1359,40 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     }
 }
 
-template <bool TF, bool RC, bool ZR>
+template <bool TF, bool RC, bool ZR, bool OV>
 __global__ __launch_bounds__(kLanes) void k_parametric(const ParArgs g)
 {
-    parametric_body<TF, false, RC, ZR>(g);
+    parametric_body<TF, false, RC, ZR, OV>(g);
 }
 
 // wide segments of a transformer: two wavefronts per SIMD
-template <bool RC, bool ZR>
+template <bool RC, bool ZR, bool OV>
 __global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(2))) void k_parametric_wide(const ParArgs g)
 {
-    parametric_body<true, true, RC, ZR>(g);
+    parametric_body<true, true, RC, ZR, OV>(g);
 }
 
 // the kernel of a launch, by family, width class and model options
-template <bool RC, bool ZR>
+template <bool RC, bool ZR, bool OV>
 void launch_variant(bool tf, bool wide, dim3 grid, dim3 block, hipStream_t s, const ParArgs &g)
 {
-    if (!tf) hipLaunchKernelGGL((k_parametric<false, RC, ZR>), grid, block, 0, s, g);
-    else if (!wide) hipLaunchKernelGGL((k_parametric<true, RC, ZR>), grid, block, 0, s, g);
-    else hipLaunchKernelGGL((k_parametric_wide<RC, ZR>), grid, block, 0, s, g);
+    if (!tf) hipLaunchKernelGGL((k_parametric<false, RC, ZR, OV>), grid, block, 0, s, g);
+    else if (!wide) hipLaunchKernelGGL((k_parametric<true, RC, ZR, OV>), grid, block, 0, s, g);
+    else hipLaunchKernelGGL((k_parametric_wide<RC, ZR, OV>), grid, block, 0, s, g);
 }
 
-void launch_kernel(bool rc, bool zr, bool tf, bool wide, dim3 grid, dim3 block, hipStream_t s, const ParArgs &g)
+// (ZeRO and overlap exclude one another)
+void launch_kernel(bool rc, bool zr, bool ov, bool tf, bool wide, dim3 grid, dim3 block, hipStream_t s,
+                   const ParArgs &g)
 {
     if (rc) {
-        if (zr) launch_variant<true, true>(tf, wide, grid, block, s, g);
-        else launch_variant<true, false>(tf, wide, grid, block, s, g);
+        if (zr) launch_variant<true, true, false>(tf, wide, grid, block, s, g);
+        else if (ov) launch_variant<true, false, true>(tf, wide, grid, block, s, g);
+        else launch_variant<true, false, false>(tf, wide, grid, block, s, g);
     } else {
-        if (zr) launch_variant<false, true>(tf, wide, grid, block, s, g);
-        else launch_variant<false, false>(tf, wide, grid, block, s, g);
+        if (zr) launch_variant<false, true, false>(tf, wide, grid, block, s, g);
+        else if (ov) launch_variant<false, false, true>(tf, wide, grid, block, s, g);
+        else launch_variant<false, false, false>(tf, wide, grid, block, s, g);
     }
 }
 
@@ -1477,10 +1556,11 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     g.narrow_end = split ? kFirstWideClass : kClasses;
     const bool rc = m.mode != DSIM_INFER && m.recompute != 0;
     const bool zr = m.mode != DSIM_INFER && m.zero != 0;
+    const bool ov = m.mode != DSIM_INFER && m.overlap != 0;
     const bool tf = m.family == DSIM_TRANSFORMER;
     const dim3 grid((unsigned)waves), block(kLanes);
     if (!split) {
-        launch_kernel(rc, zr, tf, false, grid, block, s, g);
+        launch_kernel(rc, zr, ov, tf, false, grid, block, s, g);
     } else {
         // narrow segments on a side stream, wide ones on the caller's: the
         // two launches need different amounts of LDS per wavefront and run
@@ -1494,12 +1574,12 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
         if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
         bool side_launched = false;
         if (e == hipSuccess) {
-            launch_kernel(rc, zr, true, false, grid, block, side, g);
+            launch_kernel(rc, zr, ov, true, false, grid, block, side, g);
             e = hipGetLastError();
             side_launched = e == hipSuccess;
         }
         if (e == hipSuccess) {
-            launch_kernel(rc, zr, true, true, grid, block, s, g);
+            launch_kernel(rc, zr, ov, true, true, grid, block, s, g);
             e = hipGetLastError();
         }
         if (e == hipSuccess) e = hipEventRecord(join, side);

@@ -172,10 +172,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     // Ops are assumed valid; a cheap test marks any lane that meets an op it
     // cannot vouch for, and that lane is re-simulated by the exact path below.
     // Indices are clamped so that even an invalid op stays inside the arrays.
-    // (with nodes, communication costs depend on which devices an op spans:
-    // every op takes the exact path)
-    const int32_t fast_end =
-        a.c.node ? 0 : (int32_t)(__builtin_amdgcn_readfirstlane(wave_min) / kUnroll) * kUnroll;
+    // (with nodes or streams, communication costs depend on which devices an
+    // op spans: every op takes the exact path)
+    const int32_t fast_end = (a.c.node || a.c.streams)
+                                 ? 0
+                                 : (int32_t)(__builtin_amdgcn_readfirstlane(wave_min) / kUnroll) * kUnroll;
 
     const size_t blk = (size_t)blockIdx.x * kBlock;
     const uint32_t lane_b = (uint32_t)tid * 4u;
@@ -322,14 +323,20 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
         const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
         const uint32_t m = kind == 0u ? (1u << ia) : (kind == 1u ? ((1u << ia) | (1u << ib)) : ib);
         const double f = (double)flf, b = (double)byf;
-        // a communication op whose devices lie in more than one node crosses
-        // the network
-        bool net = false;
-        if (a.c.node && kind != 0u) {
+        // the tier a communication op crosses: the streams of one GPU when
+        // all its devices lie on one GPU (GPUs hold consecutive devices, so
+        // its lowest and highest device decide), the network when its GPUs
+        // lie in more than one node, the node's links otherwise
+        int tier = 0;
+        if ((a.c.node || a.c.streams) && kind != 0u) {
             const int lo = __ffs(m) - 1, hi = 31 - __clz(m);
-            net = lo / a.c.node != hi / a.c.node;
+            const int S = a.c.streams ? a.c.streams : 1;
+            const int glo = lo / S, ghi = hi / S;
+            if (a.c.streams && glo == ghi) tier = 2;
+            else if (a.c.node && glo / a.c.node != ghi / a.c.node) tier = 1;
         }
-        const double c_lat = net ? a.c.net_lat : lat, c_inv_l = net ? a.c.net_inv_l : inv_l;
+        const double c_lat = tier == 2 ? a.c.st_lat : (tier == 1 ? a.c.net_lat : lat);
+        const double c_inv_l = tier == 2 ? a.c.st_inv_l : (tier == 1 ? a.c.net_inv_l : inv_l);
         double cost;
         if (kind == 0u && (code >> 24) == 1u && a.c.mm) {
             // a matrix multiplication: the empirical regression of Sec. 4
@@ -341,7 +348,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             cost = c_lat + b * c_inv_l;
         } else if (kind == 2u) {
             const double2 ar = s_cost[__popc(m)];
-            cost = (net ? a.c.ar_lat_net[__popc(m)] : ar.x) + ar.y * (b * c_inv_l);
+            const int n = __popc(m);
+            cost = (tier == 2 ? a.c.ar_lat_st[n] : (tier == 1 ? a.c.ar_lat_net[n] : ar.x)) + ar.y * (b * c_inv_l);
         } else {
             // broadcast / reduce: a chain of n - 1 hops (Fig. 9's Send for n = 2)
             const int n = __popc(m);

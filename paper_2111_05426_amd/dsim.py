@@ -30,7 +30,9 @@ class dsim_device_model(C.Structure):
                 ("link_bytes_per_s", C.c_double), ("link_latency_s", C.c_double),
                 ("launch_s", C.c_double), ("mem_cap_bytes", C.c_uint64),
                 ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double),
-                ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double)]
+                ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double),
+                ("streams_per_gpu", C.c_int32), ("stream_bytes_per_s", C.c_double),
+                ("stream_latency_s", C.c_double)]
 
 
 class dsim_model(C.Structure):
@@ -38,7 +40,7 @@ class dsim_model(C.Structure):
                 ("n_heads", C.c_int32), ("d_model", C.c_int64), ("d_ff", C.c_int64),
                 ("seq_len", C.c_int64), ("vocab", C.c_int64), ("global_batch", C.c_int64),
                 ("elem_bytes", C.c_int32), ("schedule", C.c_int32), ("recompute", C.c_int32),
-                ("zero", C.c_int32)]
+                ("zero", C.c_int32), ("overlap", C.c_int32)]
 
 
 class dsim_strategy(C.Structure):
@@ -130,16 +132,18 @@ def _stream(stream):
 def device_model(spec):
     mm = getattr(spec, "matmul", None)
     net = getattr(spec, "network", None)
+    st = getattr(spec, "streams", None)
     return dsim_device_model(spec.flops_per_s, spec.mem_bytes_per_s, spec.link_bytes_per_s,
                              spec.link_latency_s, spec.launch_s, int(spec.mem_cap_bytes), 1 if mm is not None else 0,
                              *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))),
-                             *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)))
+                             *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)),
+                             *((int(st[0]), float(st[1]), float(st[2])) if st is not None else (0, 0.0, 0.0)))
 
 
 def model_struct(spec):
     return dsim_model(spec.family, spec.mode, spec.n_layers, spec.n_heads, spec.d_model, spec.d_ff,
                       spec.seq_len, spec.vocab, spec.global_batch, spec.elem_bytes, spec.schedule,
-                      spec.recompute, spec.zero)
+                      spec.recompute, spec.zero, getattr(spec, "overlap", 0))
 
 
 def dsim_create_grid(model, grid):

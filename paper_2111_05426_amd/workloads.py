@@ -24,6 +24,7 @@ to this project's configurations:
 The device constants (14e12 FLOP/s, 900e9 B/s memory, 25e9 B/s link, 5 us
 latency, 5 us launch) are the same for every workload.
 """
+import math
 from dataclasses import dataclass, replace
 
 MLP, TRANSFORMER = 0, 1
@@ -125,6 +126,12 @@ GPT3_175B_GPIPE = replace(GPT3_175B, name="gpt3_175b_gpipe", model=replace(GPT3_
 GPT3_175B_RECOMPUTE = replace(GPT3_175B, name="gpt3_175b_recompute", model=replace(GPT3_175B.model, recompute=1))
 # the same grid with ZeRO partitioning of weights, gradients and optimizer state
 GPT3_175B_ZERO = replace(GPT3_175B, name="gpt3_175b_zero", model=replace(GPT3_175B.model, zero=1))
+# the same grid with the data-parallel gradient all-reduce on a second stream
+# per GPU, overlapping the last backward pass; hand-overs between a GPU's two
+# streams cost nothing (they share its memory)
+STREAMS_FREE = (2, math.inf, 0.0)
+GPT3_175B_OVERLAP = replace(GPT3_175B, name="gpt3_175b_overlap", model=replace(GPT3_175B.model, overlap=1),
+                            device=replace(GPT3_175B.device, streams=STREAMS_FREE))
 
 # A cluster of MI355X: fp16 matrix multiplications take the regression fitted
 # on this GPU by `python -m paper_2111_05426_amd.calibrate --dtype fp16`
@@ -139,6 +146,10 @@ MI355X = DeviceSpec(flops_per_s=1.493e15, mem_bytes_per_s=4.94e12, link_bytes_pe
                     launch_s=1.557e-5, mem_cap_bytes=288_000_000_000, matmul=(1.557e-5, 6.699e-16, 1.743e-13),
                     network=(8, 50e9, 10e-6))
 GPT3_175B_MI355X = replace(GPT3_175B, name="gpt3_175b_mi355x", device=MI355X)
+GPT3_175B_MI355X_OVERLAP = replace(GPT3_175B_MI355X, name="gpt3_175b_mi355x_overlap",
+                                   model=replace(GPT3_175B.model, overlap=1),
+                                   device=replace(MI355X, streams=STREAMS_FREE))
 
 ALL = {w.name: w for w in (TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN, RANDOM_TABLES, GPT3_175B,
-                           GPT3_175B_GPIPE, GPT3_175B_RECOMPUTE, GPT3_175B_ZERO, GPT3_175B_MI355X)}
+                           GPT3_175B_GPIPE, GPT3_175B_RECOMPUTE, GPT3_175B_ZERO, GPT3_175B_OVERLAP, GPT3_175B_MI355X,
+                           GPT3_175B_MI355X_OVERLAP)}

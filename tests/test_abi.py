@@ -97,18 +97,39 @@ def test_argument_errors_before_launch():
                        (DeviceSpec(matmul=(0.0, float("inf"), 0.0)), "regression"),
                        (DeviceSpec(network=(-1, 1e9, 0.0)), "node_size"),
                        (DeviceSpec(network=(8, 0.0, 1e-6)), "network"),
-                       (DeviceSpec(network=(8, 1e9, float("nan"))), "network")):
+                       (DeviceSpec(network=(8, 1e9, float("nan"))), "network"),
+                       (DeviceSpec(streams=(-1, 1e9, 0.0)), "streams_per_gpu"),
+                       (DeviceSpec(streams=(2, 0.0, 0.0)), "stream bandwidth"),
+                       (DeviceSpec(streams=(2, float("nan"), 0.0)), "stream bandwidth"),
+                       (DeviceSpec(streams=(3, 1e9, -1e-6)), "stream bandwidth"),
+                       (DeviceSpec(streams=(2, float("inf"), float("inf"))), "stream bandwidth")):
         bad = dsim.device_model(spec)
         assert L.dsim_simulate_tables(C.byref(tab4), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
         assert word in dsim.dsim_last_error()
     bad = dsim.device_model(DeviceSpec())
     bad.mm_enabled = 2
     assert L.dsim_simulate_tables(C.byref(tab4), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
-    for field, bad in (("schedule", 2), ("recompute", 2), ("recompute", -1), ("zero", 3), ("zero", -1)):
+    for field, bad in (("schedule", 2), ("recompute", 2), ("recompute", -1), ("zero", 3), ("zero", -1),
+                       ("overlap", 2), ("overlap", -1)):
         m = dsim.model_struct(ALL["gpt2_small_train"].model)
         setattr(m, field, bad)
         assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
         assert field in dsim.dsim_last_error()
+    m = dsim.model_struct(ALL["gpt2_small_train"].model)
+    m.overlap, m.zero = 1, 1
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert "overlap and zero" in dsim.dsim_last_error()
+    # the transform's devices per GPU must match the device model's streams
+    two = dsim.device_model(DeviceSpec(streams=(2, 1e12, 1e-6)))
+    three = dsim.device_model(DeviceSpec(streams=(3, 1e12, 1e-6)))
+    m = dsim.model_struct(ALL["gpt2_small_train"].model)
+    for mm, d in ((0, two), (1, dev), (1, three)):
+        m.overlap = mm
+        assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(d), C.byref(res), None) == dsim.DSIM_EINVAL
+        assert "streams_per_gpu" in dsim.dsim_last_error()
+    m.overlap = 1
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(two), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert "NULL" in dsim.dsim_last_error()
     # materialiser: device count, op capacity, NULL buffers, bad model
     m = dsim.model_struct(ALL["tiny_mlp"].model)
     for nd in (0, 9):
@@ -118,3 +139,35 @@ def test_argument_errors_before_launch():
     assert L.dsim_materialize_tables(C.byref(m), None, 0, 10, 4, *([None] * 9)) == dsim.DSIM_OK
     m.family = 7
     assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_EINVAL
+
+
+def test_struct_layouts_match_header():
+    """Every struct of include/dsim.h and its ctypes mirror in the binding:
+    the same fields, in the same order, of the same C types."""
+    import re
+    with open(dsim.HEADER) as f:
+        text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+    ctypes_of = {"double": C.c_double, "float": C.c_float, "int32_t": C.c_int32, "int64_t": C.c_int64,
+                 "uint32_t": C.c_uint32, "uint64_t": C.c_uint64}
+    structs = re.findall(r"typedef struct\s*\{(.*?)\}\s*(dsim_\w+)\s*;", text, flags=re.S)
+    assert {n for _, n in structs} >= {"dsim_device_model", "dsim_model", "dsim_strategy", "dsim_grid_spec"}
+    for body, name in structs:
+        fields = []
+        for decl in body.split(";"):
+            decl = decl.strip()
+            if not decl:
+                continue
+            m = re.match(r"(const\s+)?(\w+)\s*(\*?)\s*(.*)$", decl)
+            ctype, ptr, names = m.group(2), m.group(3), m.group(4)
+            for nm in names.split(","):
+                nm = nm.strip()
+                star = ptr or nm.startswith("*")
+                fields.append((nm.lstrip("*").strip(), "ptr" if star else ctype))
+        mirror = getattr(dsim, name)
+        got = [(f[0], f[1]) for f in mirror._fields_]
+        assert [f[0] for f in got] == [f[0] for f in fields], name
+        for (fname, ctype), (_, ct) in zip(fields, got):
+            if ctype == "ptr":
+                assert ct in (C.c_void_p,) or hasattr(ct, "_type_") and issubclass(ct, C._Pointer), (name, fname)
+            else:
+                assert ct is ctypes_of[ctype], (name, fname, ctype, ct)

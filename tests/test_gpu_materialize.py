@@ -168,6 +168,51 @@ def test_small_programs_as_tables(torch_gpu, orc, case, mm):
     assert np.all(g["mat_status"][bad] == ST_BAD_STRATEGY) and np.all(g["table_ops"][bad] == 0)
 
 
+OV_CASES = [
+    ("mlp_ov", mlp(4, 64, 48, 4, TRAIN_ADAM, overlap=1), all_strats([1, 2, 4], [1, 2], [1, 2], [1, 2, 3], 4)),
+    ("mlp_ov_gpipe_rc", mlp(6, 32, 48, 2, TRAIN_SGD, schedule=SCHED_GPIPE, recompute=1, overlap=1),
+     all_strats([1, 2], [1, 2], [1, 3], [1, 2, 5], 4)),
+    ("tf_ov", transformer(4, 32, 4, 8, 101, 12, 2, TRAIN_ADAM_MIXED, overlap=1),
+     all_strats([1, 2, 3, 4], [1, 2], [1, 2], [1, 2, 3], 4)),
+    ("tf_ov_rc", transformer(5, 32, 4, 8, 101, 12, 2, TRAIN_ADAM, recompute=1, overlap=1),
+     all_strats([1, 2], [1, 2], [1, 2], [1, 3], 4)),
+    ("tf_ov_infer", transformer(4, 48, 6, 16, 97, 9, 2, INFER, overlap=1), all_strats([1, 3], [1, 2], [1, 2], [1, 3], 4)),
+]
+
+
+@pytest.mark.parametrize("net", [False, True])
+@pytest.mark.parametrize("case", OV_CASES, ids=[c[0] for c in OV_CASES])
+def test_overlap_programs_as_tables(torch_gpu, orc, case, net):
+    """Overlapped programs put two streams on every GPU (devices 2g and
+    2g + 1, hand-overs as Sends between them): device by device against the
+    oracle's full program, and per stage against the transform-driven
+    kernel."""
+    from paper_2111_05426_amd import dsim
+    name, model, strat = case
+    dev = DeviceSpec(streams=(2, 5.3e11, 1.7e-6), network=(1, 4.7e9, 1.9e-5) if net else None)
+    P = int(strat[:, 2].max())
+    o = orc.run_strategies(model, strat, dev, slice=False, row_width=P, threads=8)
+    assert np.all(o["status"] == 0)
+    g = materialize_and_simulate(torch_gpu, model, strat, dev, 8, int(o["n_ops"].max()))
+    assert np.all(g["mat_status"] == 0) and np.all(g["status"] == 0)
+    assert np.array_equal(g["table_ops"], o["n_ops"].astype(np.int64))
+    assert np.array_equal(g["makespan"], o["makespan"])
+    assert np.array_equal(g["cand_peak"].view(np.uint64), o["cand_peak"])
+    for i, (D, H, Pi, K) in enumerate(strat.tolist()):
+        r = orc.sim_strategy(model, D, H, Pi, K, dev)
+        n = 2 * D * H * Pi
+        assert np.array_equal(g["finish"][i, :n], r["dev_finish"]), (name, strat[i].tolist())
+        assert np.array_equal(g["peak"][i, :n].view(np.uint64), r["dev_peak"]), (name, strat[i].tolist())
+        assert np.array_equal(g["init_live"][i, :n].view(np.uint64), r["dev_resident"]), (name, strat[i].tolist())
+        assert not g["peak"][i, 1:n:2].any()   # communication streams hold nothing
+    rp = dsim.alloc_results(len(strat), P)
+    dsim.dsim_simulate_parametric(model, torch_gpu.from_numpy(strat).cuda(), dev, rp)
+    torch_gpu.cuda.synchronize()
+    assert np.array_equal(rp["makespan"].cpu().numpy(), g["makespan"])
+    assert np.array_equal(rp["finish"].cpu().numpy(), o["finish"])
+    assert np.array_equal(rp["n_ops"].cpu().numpy().astype(np.int64), g["table_ops"])
+
+
 def test_materialize_errors(torch_gpu, orc):
     m = mlp(4, 64, 48, 4, TRAIN_SGD)
     dev = DeviceSpec()

@@ -7,6 +7,7 @@ test_oracle_pins.py), on every candidate where that is cheap and on a seeded
 sample of the GPT-3-shaped grid.  Bar: status, op counts and peak bytes
 bit-exact; times within 1e-12 relative and expected bit-identical.
 """
+import math
 from dataclasses import replace
 
 import numpy as np
@@ -155,6 +156,25 @@ def test_network_vs_full_program(torch_gpu, orc, case, node):
     compare(g, o, strat)
 
 
+# overlap: two streams per GPU, the gradient all-reduce on the second; hand-
+# overs with a cost, free, or slow beside nodes of two GPUs
+OV_DEVICES = [DeviceSpec(mem_cap_bytes=10 ** 6, streams=(2, 5.3e11, 1.7e-6)),
+              DeviceSpec(mem_cap_bytes=10 ** 6, streams=(2, math.inf, 0.0)),
+              DeviceSpec(mem_cap_bytes=10 ** 6, streams=(2, 2.1e9, 4.3e-5), network=(2, 4.7e9, 1.9e-5))]
+OV_CASES = [(name, replace(model, overlap=1), strat) for name, model, strat in SMALL if not model.zero]
+
+
+@pytest.mark.parametrize("dev", range(len(OV_DEVICES)))
+@pytest.mark.parametrize("case", range(len(OV_CASES)), ids=[c[0] for c in OV_CASES])
+def test_overlap_vs_full_program(torch_gpu, orc, case, dev):
+    name, model, strat = OV_CASES[case]
+    d = OV_DEVICES[dev]
+    g = run_gpu(torch_gpu, model, strat, d)
+    o = orc.run_strategies(model, strat, d, slice=False, row_width=g["finish"].shape[1], threads=8)
+    assert np.any(o["status"] == 0)
+    compare(g, o, strat)
+
+
 GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(LARGE_MLP, name="large_mlp_mixed", model=replace(LARGE_MLP.model, mode=TRAIN_ADAM_MIXED)),
          replace(LARGE_MLP, name="large_mlp_gpipe", model=replace(LARGE_MLP.model, schedule=SCHED_GPIPE)),
@@ -166,7 +186,12 @@ GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_zero", model=replace(GPT2_SMALL_TRAIN.model, zero=1)),
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_matmul",
                  device=replace(GPT2_SMALL_TRAIN.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13))),
-         replace(LARGE_MLP, name="large_mlp_matmul", device=replace(LARGE_MLP.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13)))]
+         replace(LARGE_MLP, name="large_mlp_matmul", device=replace(LARGE_MLP.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13))),
+         replace(LARGE_MLP, name="large_mlp_overlap", model=replace(LARGE_MLP.model, overlap=1),
+                 device=replace(LARGE_MLP.device, streams=(2, 2.2e11, 3.1e-6))),
+         replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_overlap_rc",
+                 model=replace(GPT2_SMALL_TRAIN.model, overlap=1, recompute=1),
+                 device=replace(GPT2_SMALL_TRAIN.device, streams=(2, math.inf, 0.0)))]
 
 
 @pytest.mark.parametrize("w", GRIDS, ids=[w.name for w in GRIDS])
@@ -193,8 +218,9 @@ def test_workload_grid_vs_oracle(torch_gpu, orc, w):
     assert int(found.item()) == rf and np.array_equal(idx.cpu().numpy(), ri)
 
 
-@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"], ALL["gpt3_175b_zero"], ALL["gpt3_175b_mi355x"]],
-                         ids=["1f1b", "recompute", "zero", "mi355x_calibrated"])
+@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"], ALL["gpt3_175b_zero"], ALL["gpt3_175b_mi355x"],
+                               ALL["gpt3_175b_overlap"], ALL["gpt3_175b_mi355x_overlap"]],
+                         ids=["1f1b", "recompute", "zero", "mi355x_calibrated", "overlap", "mi355x_overlap"])
 def test_gpt3_grid_sampled(torch_gpu, orc, w):
     """The GPT-3-shaped grid at full size (39,965 strategies, the launch
     configuration the benchmark times, the 288e9-byte cap, top-16): a seeded

@@ -6,6 +6,8 @@ bit-exact; fp64 times within 1e-12 relative (both sides evaluate the same
 IEEE expressions in the same order with contraction off, so they are
 expected to be equal bit for bit, and the tests also record that).
 """
+from dataclasses import replace
+
 import numpy as np
 import pytest
 
@@ -85,19 +87,25 @@ def results_np(r):
     return out
 
 
-@pytest.mark.parametrize("kinds", ["plain", "bcast_reduce", "matmul", "network"])
+@pytest.mark.parametrize("kinds", ["plain", "bcast_reduce", "matmul", "network", "streams"])
 @pytest.mark.parametrize("n_dev", [1, 2, 3, 5, 8])
 @pytest.mark.parametrize("bad", [False, True])
 def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, kinds):
     from paper_2111_05426_amd import dsim
     from paper_2111_05426_amd.workloads import DeviceSpec
     torch = torch_gpu
-    rooted, classes, net = kinds in ("bcast_reduce", "network"), kinds == "matmul", kinds == "network"
-    rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted + 211 * classes + 307 * net)
+    rooted, classes, net = kinds in ("bcast_reduce", "network", "streams"), kinds == "matmul", kinds == "network"
+    streams = kinds == "streams"
+    rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted + 211 * classes + 307 * net + 401 * streams)
     n_cand, max_ops = 777, 301   # several 256-lane blocks and a ragged tail
     t = random_tables(rng, n_cand, max_ops, n_dev, bad, rooted, classes)
     dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5, matmul=(4.5e-6, 9.1e-15, 1.3e-12) if classes else None,
                      network=(max(1, n_dev // 2 - (n_dev == 5)), 3.3e9, 2.1e-5) if net else None)
+    if streams:
+        # two or three streams per GPU; GPUs in nodes of one for some sizes;
+        # no byte term between streams for others
+        dev = replace(dev, streams=(2 + n_dev % 2, np.inf if n_dev % 3 == 0 else 4.4e11, 1.3e-6),
+                      network=(1, 3.3e9, 2.1e-5) if n_dev in (3, 8) else None)
     g = to_gpu(torch, t)
     init = torch.from_numpy(t["init"].view(np.int64)).cuda()
     rw = n_dev + 2
