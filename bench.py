@@ -236,6 +236,44 @@ def bench_grid_as_tables(torch, dsim, W, reps, n_dev=8):
             "best": {"index": best, "strategy_DHPK": strat[best].tolist(), "makespan_s": float(out_mk[0].item())}}
 
 
+def bench_lowered_programs(torch, dsim, reps):
+    """Programs through the front end: GPT-2-shaped layers (4 layers, d 768,
+    12 heads) placed over 1-8 devices by hand (tensor x pipeline parallelism
+    1x1, 2x2, 4x2, 2x4, 1x4), batch 1-16 and sequence 64-1024, each
+    interpreted over the mixed abstract/concrete domain and lowered to an op
+    table on the host (timed once), then a step is dsim_simulate_tables over
+    all of them on the GPU."""
+    import numpy as np
+    from paper_2111_05426_amd import frontend as fe, programs
+    from paper_2111_05426_amd.workloads import DeviceSpec
+    cases = [(B, S, tp, pp) for tp, pp in ((1, 1), (2, 2), (4, 2), (2, 4), (1, 4))
+             for B in range(1, 17) for S in (64, 128, 256, 512, 1024)]
+    t0 = time.perf_counter()
+    tabs = [fe.lower(fe.parse(programs.gpt2_layers(B, S, n_layers=4, tp=tp, pp=pp)), {"%flat": [-1]}, n_dev=8)
+            for B, S, tp, pp in cases]
+    host_s = time.perf_counter() - t0
+    p = fe.pack(tabs)
+    n = len(cases)
+    g = {k: torch.from_numpy(np.ascontiguousarray(p[k]).view(np.int32 if p[k].dtype == np.uint32 else p[k].dtype)).cuda()
+         for k in ("code", "flops", "bytes", "alloc", "free", "n_ops")}
+    init = torch.from_numpy(p["init_live"].view(np.int64)).cuda()
+    res = dsim.alloc_results(n, 8)
+    dev = DeviceSpec()
+    ev = []
+    for i in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dsim.dsim_simulate_tables(g, n, 8, dev, res, init_live=init)
+        e1.record()
+        if i:
+            ev.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    return {"workload": "gpt2-shaped layer programs through the front end", "programs": n,
+            "records_per_table_max": int(p["code"].shape[0]), "records": int(p["n_ops"].sum()),
+            "host_interpret_and_lower_ms": host_s * 1e3, "kernel_ms": ms, "programs_per_s": n / (ms * 1e-3)}
+
+
 # fp64 add rate of the chip: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (half the
 # 78.6 TFLOP/s FMA figure, which counts two flops per lane-cycle)
 FP64_ADD_PEAK_T = 256 * 4 * 16 * 2.4e9 / 1e12
@@ -341,6 +379,7 @@ def main():
     if not args.no_parametric:
         out["parametric"] = [bench_parametric(torch, dsim, ALL[name], args.param_reps) for name in PARAMETRIC]
         out["grids_as_tables"] = [bench_grid_as_tables(torch, dsim, ALL["tiny_mlp"], args.param_reps)]
+        out["lowered_programs"] = bench_lowered_programs(torch, dsim, args.param_reps)
     if args.copy_calibration or not args.no_copy:
         # the achievable streaming rate on this GPU, beside the spec peak
         out["copy_calibration"] = copy_calibration(torch)

@@ -163,7 +163,8 @@ def sim_table(tab, n_dev, dev, init_live=None):
 def sim_program(ops, tensors, n_dev, dev, with_trace=False):
     """Simulate an explicit program.
 
-    ops: list of dicts {kind, devs, ins, outs, cost (optional), flops, bytes}
+    ops: list of dicts {kind, devs, ins, outs, cost (optional), flops, bytes,
+         matmul (optional: the empirical MatMul cost applies)}
     tensors: list of (device, size, flags)
     dev: object with the device-model attributes (flops_per_s, ...)
     """
@@ -187,17 +188,18 @@ def sim_program(ops, tensors, n_dev, dev, with_trace=False):
     t_dev = np.array([t[0] for t in tensors] or [0], np.int32)
     t_size = np.array([t[1] for t in tensors] or [0], np.uint64)
     t_flags = np.array([t[2] for t in tensors] or [0], np.int32)
+    mm = np.array([1 if o.get("matmul") else 0 for o in ops] or [0], np.int32)
     fin = np.zeros(n_dev, np.float64)
     pk = np.zeros(n_dev, np.uint64)
     ts = np.zeros(max(n, 1), np.float64)
     te = np.zeros(max(n, 1), np.float64)
     f = lib().or_sim_program
     f.argtypes = [C.c_int64] + [C.c_void_p] * 10 + [C.c_int64] + [C.c_void_p] * 3 + \
-        [C.c_int, C.POINTER(_Dev)] + [C.c_void_p] * 4
+        [C.c_int, C.POINTER(_Dev)] + [C.c_void_p] * 5
     d = _dev(dev)
     rc = f(n, _p(kind), _p(cost_), _p(fl), _p(by), _p(db), _p(dv), _p(ib), _p(iv), _p(ob), _p(ov),
            len(tensors), _p(t_dev), _p(t_size), _p(t_flags), n_dev, C.byref(d), _p(fin), _p(pk),
-           _p(ts), _p(te))
+           _p(ts), _p(te), _p(mm))
     if rc:
         raise ValueError("or_sim_program failed: %d" % rc)
     out = dict(finish=fin, peak=pk, makespan=float(fin.max()) if n_dev else 0.0)

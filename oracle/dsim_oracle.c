@@ -742,7 +742,8 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
                    const int64_t *out_beg, const int32_t *outs,
                    int64_t n_t, const int32_t *t_dev, const uint64_t *t_size,
                    const int32_t *t_flags, int n_dev, const or_device_model *m,
-                   double *finish, uint64_t *peak, double *tstart, double *tend)
+                   double *finish, uint64_t *peak, double *tstart, double *tend,
+                   const int32_t *is_matmul)
 {
     or_prog g;
     int64_t i, q;
@@ -750,7 +751,10 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
     prog_init(&g);
     for (q = 0; q < n_t; q++) prog_tensor(&g, t_dev[q], t_size[q], t_flags[q]);
     for (i = 0; i < n_ops; i++) {
-        op_begin(&g, kind[i], T_GENERIC, flops ? flops[i] : 0.0, bytes ? bytes[i] : 0.0);
+        /* is_matmul (optional): the op multiplies two matrices (Sec. 4's
+         * empirical MatMul cost applies when the device model has one) */
+        op_begin(&g, kind[i], is_matmul && is_matmul[i] ? T_GEMM : T_GENERIC,
+                 flops ? flops[i] : 0.0, bytes ? bytes[i] : 0.0);
         for (q = dev_beg[i]; q < dev_beg[i + 1]; q++) op_dev(&g, devs[q]);
         for (q = in_beg[i]; q < in_beg[i + 1]; q++) op_in(&g, ins[q]);
         for (q = out_beg[i]; q < out_beg[i + 1]; q++) op_out(&g, outs[q]);

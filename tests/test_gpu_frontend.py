@@ -1,0 +1,62 @@
+"""GPU parity of programs lowered by the front end: GPT-2-shaped layers with
+tensor and pipeline parallelism over 1..8 devices, swept over batch and
+sequence sizes, lowered to tables (mixed abstract/concrete interpretation,
+Sec. 3.3), packed as candidates and simulated by dsim_simulate_tables,
+against the oracle's own interpretation of each program simulated as a
+program over tensors.  Bar: times bit-identical, peaks and status exact."""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2111_05426_amd.workloads import DeviceSpec
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    from paper_2111_05426_amd import dsim
+    dsim.lib()
+    return torch
+
+
+CASES = [(B, S, tp, pp) for tp, pp in ((1, 1), (2, 2), (4, 2), (2, 4), (1, 4))
+         for B in (1, 2, 3, 5, 8, 13, 16) for S in (64, 128, 512, 1024)]
+
+
+@pytest.mark.parametrize("dev", [DeviceSpec(mem_cap_bytes=400_000_000),
+                                 DeviceSpec(matmul=(5.2e-6, 1.1e-15, 2.3e-13), network=(2, 4.9e10, 1.1e-5)),
+                                 DeviceSpec(streams=(2, math.inf, 0.0), network=(2, 4.9e10, 1.1e-5))],
+                         ids=["roofline_cap", "matmul_network", "streams"])
+def test_lowered_programs_vs_oracle(torch_gpu, dev):
+    from oracle import interp
+    from paper_2111_05426_amd import dsim, frontend as fe, programs
+    torch = torch_gpu
+    texts = [programs.gpt2_layers(B, S, n_layers=4, tp=tp, pp=pp) for B, S, tp, pp in CASES]
+    tabs = [fe.lower(fe.parse(t), {"%flat": [-1]}, n_dev=8) for t in texts]
+    p = fe.pack(tabs)
+    n = len(CASES)
+    print("%d lowered programs, %d records at most" % (n, p["code"].shape[0]), flush=True)
+    g = {k: torch.from_numpy(np.ascontiguousarray(p[k]).view(np.int32 if p[k].dtype == np.uint32 else p[k].dtype)).cuda()
+         for k in ("code", "flops", "bytes", "alloc", "free", "n_ops")}
+    init = torch.from_numpy(p["init_live"].view(np.int64)).cuda()
+    r = dsim.alloc_results(n, 8)
+    dsim.dsim_simulate_tables(g, n, 8, dev, r, init_live=init)
+    torch.cuda.synchronize()
+    mk = r["makespan"].cpu().numpy()
+    fin = r["finish"].cpu().numpy()
+    pk = r["peak"].cpu().numpy().view(np.uint64)
+    cp = r["cand_peak"].cpu().numpy().view(np.uint64)
+    st = r["status"].cpu().numpy()
+    for c, (text, case) in enumerate(zip(texts, CASES)):
+        o = interp.simulate(text, dev, {"%flat": [-1]}, n_dev=8)
+        assert np.array_equal(fin[c], o["finish"]), case
+        assert np.array_equal(pk[c], o["peak"]), case
+        assert mk[c] == o["makespan"], case
+        over = dev.mem_cap_bytes and int(o["peak"].max()) > dev.mem_cap_bytes
+        assert st[c] == (32 if over else 0) and cp[c] == o["peak"].max(), case
+    if dev.mem_cap_bytes:
+        assert np.any(st == 32) and np.any(st == 0)
