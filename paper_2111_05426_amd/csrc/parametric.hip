@@ -1285,17 +1285,20 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         const uint64_t starts = ballot(!linked);
         const uint64_t upto = starts & (lane == 63 ? ~0ull : ((2ull << lane) - 1));
         const int rpos = lane - (63 - __builtin_clzll(upto));
-        for (int r = 0;; ++r) {
+        // the last run position of the wave (a position without a Send
+        // changes nothing: its receivers need a sender there)
+        int last = 0;
+        for (int b = 32; b >= 1; b >>= 1)
+            if (ballot(rpos >= last + b) != 0) last += b;
+        for (int r = 0; r <= last; ++r) {
             const bool src = rpos == r && sdir != 0;
-            const uint64_t srcs = ballot(src), more = ballot(rpos > r);
-            if (srcs == 0 && more == 0) break;
-            if (srcs == 0) continue;
             const double cl = shr1(clk), cr = shl1(clk);
             const bool tl = rpos == r + 1 && from_left;
             const bool tr = rpos == r - 1 && from_right;
             const double a = ((src && sdir < 0) || tl) ? cl : cr;
-            const double mx = a > clk ? a : clk;
-            const double e = mx + (src ? scost : (tl ? l_cost : r_cost));
+            // clocks are sums of costs >= 0 from +0.0: never NaN or -0.0,
+            // so fmax is the plain larger value
+            const double e = fmax(a, clk) + (src ? scost : (tl ? l_cost : r_cost));
             if (src || tl || tr) clk = e;
         }
         if (live_stage) {
