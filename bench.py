@@ -359,8 +359,8 @@ def main():
                     help="time the 4 GiB copy (the default; kept for the profiling commands)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this simulator shards candidates across GPUs by design, but "
-              "multi-GPU runs are not part of this build (use --gpus 1)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the simulator would shard candidates across GPUs, but runs on "
+              "several GPUs are not supported (use --gpus 1)", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2111_05426_amd import dsim
