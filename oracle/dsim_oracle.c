@@ -386,6 +386,9 @@ static uint64_t sm64_at(uint64_t seed, uint64_t n)
     return z ^ (z >> 31);
 }
 
+/* output n (n >= 1) of SplitMix64 started from seed (tests) */
+uint64_t or_splitmix64(uint64_t seed, uint64_t n) { return sm64_at(seed, n); }
+
 static uint64_t draw(uint64_t seed, uint64_t c, uint64_t j, uint64_t f)
 {
     return sm64_at(seed, (c << 32) + (j << 5) + f + 1);
