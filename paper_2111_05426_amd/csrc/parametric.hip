@@ -925,7 +925,12 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     __shared__ typename std::conditional<WIDE, LdsWide<Sh>, LdsNarrow<Sh>>::type L;
 
     const int lane = threadIdx.x;
-    const uint32_t gl = blockIdx.x * (uint32_t)kLanes;
+    // wavefronts start widest class first (the wide launch, or the only
+    // one): those walk the longest pipelines, and starting them first
+    // shortens the tail
+    const bool widest_first = WIDE || g.narrow_end == kClasses;
+    const uint32_t blk = widest_first ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+    const uint32_t gl = blk * (uint32_t)kLanes;
     if (gl >= g.meta[16 + kClasses]) return;      // beyond the last class (whole wave)
     int cls = 0;
     while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
@@ -1577,7 +1582,11 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
         if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
         bool side_launched = false;
         if (e == hipSuccess) {
-            launch_kernel(rc, zr, ov, true, false, grid, block, side, g);
+            // the narrow classes (1, 2, 4 lanes per candidate) come first in
+            // the class layout: a grid over their lanes is enough
+            const int64_t narrow_waves = (n_cand * 4 + kLanes - 1) / kLanes + kClasses;
+            const dim3 grid_n((unsigned)(narrow_waves < waves ? narrow_waves : waves));
+            launch_kernel(rc, zr, ov, true, false, grid_n, block, side, g);
             e = hipGetLastError();
             side_launched = e == hipSuccess;
         }
