@@ -37,6 +37,7 @@ allocated on the op's device (a Send's receiver), and the tensors whose
 last reader it is are freed there.
 """
 import ast
+import math
 import re
 from dataclasses import dataclass, field
 
@@ -67,13 +68,13 @@ class Tensor:
     def nbytes(self):
         if self.shape is None:
             raise ValueError("cannot simulate: the shape of a %s tensor is unknown" % self.dtype)
-        return int(np.prod(self.shape, dtype=np.int64)) * ELEM_BYTES[self.dtype]
+        return math.prod(self.shape) * ELEM_BYTES[self.dtype]
 
     @property
     def numel(self):
         if self.shape is None:
             raise ValueError("cannot simulate: a shape is unknown")
-        return int(np.prod(self.shape, dtype=np.int64))
+        return math.prod(self.shape)
 
 
 @dataclass(frozen=True)
