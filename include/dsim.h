@@ -80,7 +80,10 @@ DSIM_API const char *dsim_last_error(void);
 /* Device constants of the simulated cluster (Sec. 4: the cost functions'
  * coefficients are device DRAM bandwidth, kernel launch overhead, network
  * bandwidth; F is the device's flop rate, Sec. 3.3).  All five doubles must
- * be finite and > 0 (latency and launch may be 0).  mem_cap_bytes = 0 means
+ * be finite and > 0 (latency and launch may be 0), and each rate's
+ * reciprocal finite too (costs multiply by 1/rate, so a rate below about
+ * 5.6e-309 is rejected).  Costs may still overflow to +inf; an all-reduce
+ * over a single device costs 0 whatever its bytes.  mem_cap_bytes = 0 means
  * no cap; otherwise candidates whose peak exceeds it get DSIM_ST_OVER_CAP.
  * mm_enabled = 1 gives matrix multiplications the empirical cost of Sec. 4
  * (a linear regression in the input sizes, fitted on single-op
@@ -92,15 +95,15 @@ DSIM_API const char *dsim_last_error(void);
  * mm_enabled = 0: every compute op takes the roofline.
  * node_size > 0 makes the interconnect two-tier: device d lies in node
  * d / node_size, and a send or collective whose devices lie in more than one
- * node crosses the network (net_bytes_per_s > 0, net_latency_s >= 0, both
- * finite) instead of the node's links (link_bytes_per_s, link_latency_s).
+ * node crosses the network (net_bytes_per_s > 0 with a finite reciprocal,
+ * net_latency_s >= 0, both finite) instead of the node's links (link_bytes_per_s, link_latency_s).
  * node_size = 0: one uniform interconnect, net_* ignored.
  * streams_per_gpu = S > 1 models communication that overlaps computation the
  * way Sec. 2.2 (Limitations) describes, one device per stream: device d is
  * a stream of GPU d / S (nodes then hold node_size GPUs), and a send or
  * collective whose devices are all streams of one GPU costs
- * stream_latency_s (finite, >= 0) and stream_bytes_per_s (> 0, +inf for no
- * byte term) in place of the links.  S = 0 or 1: every device is its own
+ * stream_latency_s (finite, >= 0) and stream_bytes_per_s (> 0 with a finite
+ * reciprocal, +inf for no byte term) in place of the links.  S = 0 or 1: every device is its own
  * GPU, stream_* ignored.  The transform's devices follow model.overlap:
  * S must be 2 with it and at most 1 without (else DSIM_EINVAL). */
 typedef struct {

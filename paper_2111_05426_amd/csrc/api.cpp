@@ -62,25 +62,30 @@ CostConsts make_consts(const dsim_device_model &m)
 }
 
 static bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
+// a rate whose reciprocal is finite too: every cost multiplies by 1/rate,
+// and an infinite 1/rate times a zero byte or flop count would be NaN
+static bool rate_ok(double v) { return finite_pos(v) && std::isfinite(1.0 / v); }
 static bool finite_nonneg(double v) { return std::isfinite(v) && v >= 0.0; }
 
 static dsim_status check_device(const dsim_device_model *m)
 {
     if (!m) return fail(DSIM_EINVAL, "device model is NULL");
-    if (!finite_pos(m->flops_per_s) || !finite_pos(m->mem_bytes_per_s) || !finite_pos(m->link_bytes_per_s))
-        return fail(DSIM_EINVAL, "device rates must be finite and > 0");
+    if (!rate_ok(m->flops_per_s) || !rate_ok(m->mem_bytes_per_s) || !rate_ok(m->link_bytes_per_s))
+        return fail(DSIM_EINVAL, "device rates must be finite and > 0, with finite reciprocals");
     if (!finite_nonneg(m->link_latency_s) || !finite_nonneg(m->launch_s))
         return fail(DSIM_EINVAL, "latency and launch must be finite and >= 0");
     if (m->mm_enabled != 0 && m->mm_enabled != 1) return fail(DSIM_EINVAL, "mm_enabled must be 0 or 1");
     if (m->mm_enabled && (!finite_nonneg(m->mm_c0) || !finite_nonneg(m->mm_c1) || !finite_nonneg(m->mm_c2)))
         return fail(DSIM_EINVAL, "MatMul regression coefficients must be finite and >= 0");
     if (m->node_size < 0) return fail(DSIM_EINVAL, "node_size must be >= 0");
-    if (m->node_size > 0 && (!finite_pos(m->net_bytes_per_s) || !finite_nonneg(m->net_latency_s)))
-        return fail(DSIM_EINVAL, "network bandwidth must be finite and > 0, latency finite and >= 0");
+    if (m->node_size > 0 && (!rate_ok(m->net_bytes_per_s) || !finite_nonneg(m->net_latency_s)))
+        return fail(DSIM_EINVAL, "network bandwidth must be finite and > 0 (finite reciprocal), latency finite and >= 0");
     if (m->streams_per_gpu < 0 || m->streams_per_gpu > (1 << 20))
         return fail(DSIM_EINVAL, "streams_per_gpu must be in 0..2^20");
-    if (m->streams_per_gpu > 1 && (!(m->stream_bytes_per_s > 0.0) || !finite_nonneg(m->stream_latency_s)))
-        return fail(DSIM_EINVAL, "stream bandwidth must be > 0 (inf allowed), latency finite and >= 0");
+    if (m->streams_per_gpu > 1 && (!(m->stream_bytes_per_s > 0.0) || !std::isfinite(1.0 / m->stream_bytes_per_s) ||
+                                   !finite_nonneg(m->stream_latency_s)))
+        return fail(DSIM_EINVAL, "stream bandwidth must be > 0 (inf allowed) with a finite reciprocal, latency finite "
+                                 "and >= 0");
     return DSIM_OK;
 }
 

@@ -710,7 +710,8 @@ template <int U2n>
 __device__ __forceinline__ double units_exact(const double2 (&r)[U2n], double clk, int n)
 {
     while (n > 0) {
-        if (clk >= 0x1p-500) {
+        // (an overflowed clock, +inf, stays +inf: op by op, n units)
+        if (clk >= 0x1p-500 && clk <= 0x1.fffffffffffffp+1023) {
             const int e = ilogb(clk);
             const double sc = ldexp(1.0, 52 - e);
             const double k = clk * sc;                 // integer in [2^52, 2^53)

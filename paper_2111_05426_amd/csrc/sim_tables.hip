@@ -126,7 +126,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     __shared__ ulonglong2 s_mem[ND][kBlock];   // (live, peak) bytes
     // per op class -- all-reduce over n = 0..ND devices, then compute, then
     // send -- the cost terms (base, coef) and (1/bandwidth, 1/flop rate or 0)
-    __shared__ double2 s_c1[ND + 3][kCopies], s_c2[ND + 3][kCopies];
+    // (one array: the second pair sits at a fixed offset from the first, so
+    // one address serves both loads)
+    __shared__ double2 s_ct[2][ND + 3][kCopies];
     __shared__ double2 s_cost[ND + 3];   // (base, coef) for the exact path
 
     const int tid = threadIdx.x;
@@ -136,8 +138,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     for (int i = tid; i < (ND + 3) * kCopies; i += kBlock) {
         const int e = i / kCopies, k = i % kCopies;
         const bool cmp = e == ND + 1;
-        s_c1[e][k] = make_double2(e <= ND ? a.c.ar_lat[e] : (cmp ? a.c.launch : a.c.lat), e <= ND ? a.c.ar_coef[e] : 1.0);
-        s_c2[e][k] = make_double2(cmp ? a.c.inv_b : a.c.inv_l, cmp ? a.c.inv_f : 0.0);
+        s_ct[0][e][k] = make_double2(e <= ND ? a.c.ar_lat[e] : (cmp ? a.c.launch : a.c.lat), e <= ND ? a.c.ar_coef[e] : 1.0);
+        // an all-reduce over one device costs nothing, whatever its bytes
+        // (zero weights keep an overflowing byte term out: 0 * inf is NaN)
+        s_ct[1][e][k] = make_double2(e <= 1 ? 0.0 : (cmp ? a.c.inv_b : a.c.inv_l), cmp ? a.c.inv_f : 0.0);
     }
 
     const int64_t c = (int64_t)blockIdx.x * kBlock + tid;
@@ -181,6 +185,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     const size_t blk = (size_t)blockIdx.x * kBlock;
     const uint32_t lane_b = (uint32_t)tid * 4u;
     bool suspect = false;
+    uint32_t fb_max = 0;   // largest flops or bytes bit pattern met on the fast path
 
     // two register sets of kUnroll op records: one is processed while the
     // other is in flight
@@ -218,33 +223,41 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             // selects, so the wavefront runs one straight sequence whatever
             // the op kinds of its lanes.
             const uint32_t code = cd[u];
-            const uint32_t kind = code & 0xffu, ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
-            const bool is_c = kind == 0u, is_s = kind == 1u, is_a = kind == 2u;
+            const uint32_t ia = (code >> 8) & 0xffu, ib = (code >> 16) & 0xffu;
+            bool is_c, is_s, is_a;
+            if constexpr ((ND & (ND - 1)) == 0) {
+                // one masked compare per kind tests the reserved byte, the
+                // kind and the device fields that must be < ND at once; an
+                // op that passes none is invalid, and the selects below
+                // treat it as an all-reduce over its (clamped) fields
+                constexpr uint32_t hi = ~(uint32_t)(ND - 1) & 0xffu;
+                constexpr uint32_t m0 = 0xff0000ffu | (hi << 8), m1 = m0 | (hi << 16), m2 = 0xff0000ffu;
+                is_c = (code & m0) == 0u;
+                is_s = (code & m1) == 1u;
+                is_a = (code & m2) == 2u;
+                const uint32_t ma = ib & ((1u << ND) - 1u);
+                suspect |= !(is_c | (is_s & (ia != ib)) | (is_a & (ma != 0u) & (ib == ma)));
+            } else {
+                const uint32_t kind = code & 0xffu;
+                is_c = kind == 0u;
+                is_s = kind == 1u;
+                is_a = kind == 2u;
+                suspect |= (code >= (1u << 24)) | (kind > 2u) | ((ia >= (uint32_t)ND) & !is_a) |
+                           (is_s & ((ib >= (uint32_t)ND) | (ia == ib))) | (is_a & ((ib == 0u) | (ib >= (1u << ND))));
+            }
+            // flops and bytes must be finite and >= 0: as integers, below
+            // the bits of +inf (negative values have the sign bit set)
+            fb_max = max(fb_max, max(fl[u], by[u]));
             const uint32_t ias = min(ia, (uint32_t)ND - 1u), ibs = min(ib, (uint32_t)ND - 1u);
             const uint32_t mc = 1u << ias, ms = mc | (1u << ibs), ma = ib & ((1u << ND) - 1u);
             const uint32_t m = is_c ? mc : (is_s ? ms : ma);
-            bool bad;
-            if constexpr ((ND & (ND - 1)) == 0) {
-                // one masked compare per kind: the reserved byte, the kind
-                // and the device fields that must be < ND
-                constexpr uint32_t hi = ~(uint32_t)(ND - 1) & 0xffu;
-                constexpr uint32_t m0 = 0xff0000ffu | (hi << 8), m1 = m0 | (hi << 16), m2 = 0xff0000ffu;
-                const bool ok = ((code & m0) == 0u) | (((code & m1) == 1u) & (ia != ib)) |
-                                (((code & m2) == 2u) & (ma != 0u) & (ib == ma));
-                bad = !ok | (max(fl[u], by[u]) >= 0x7f800000u);
-            } else {
-                bad = (code >= (1u << 24)) | (kind > 2u) | (max(fl[u], by[u]) >= 0x7f800000u) |
-                      ((ia >= (uint32_t)ND) & !is_a) | (is_s & ((ib >= (uint32_t)ND) | (ia == ib))) |
-                      (is_a & ((ib == 0u) | (ib >= (1u << ND))));
-            }
-            suspect |= bad;
 
             // op cost (Sec. 3.3 / Sec. 4 cost functions) as base + coef * x:
             // compute (launch, 1, max(flops/F, bytes/B)), send (lat, 1,
             // bytes/L), all-reduce over n devices (ar_lat[n], ar_coef[n],
             // bytes/L); multiplying by 1.0 is exact
             const uint32_t idx = is_c ? (uint32_t)ND + 1u : (is_s ? (uint32_t)ND + 2u : (uint32_t)__popc(m));
-            const double2 bc = s_c1[idx][tid & (kCopies - 1)], rw = s_c2[idx][tid & (kCopies - 1)];
+            const double2 bc = s_ct[0][idx][tid & (kCopies - 1)], rw = s_ct[1][idx][tid & (kCopies - 1)];
             // a non-compute class carries 0 as its flop reciprocal: a valid
             // op's flops are finite, so that term is +0 and the max is the
             // bandwidth term, as in the per-kind formulas
@@ -284,7 +297,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             const uint64_t lf0 = s_mem[fdev][tid].x;
             const uint64_t lt = tm.x + (uint64_t)alloc;
             // a compute op frees on the device it allocated on (lf0 == tm.x)
-            const uint64_t lf = lf0 + (uint64_t)(is_c ? alloc : 0u);
+            const uint64_t lf = is_c ? lt : lf0;
             s_mem[tdev][tid] = make_ulonglong2(lt, max_bits(lt, tm.y));
             suspect |= (uint64_t)fre > lf;
             s_mem[fdev][tid].x = lf - (uint64_t)fre;
@@ -298,6 +311,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
         if (j0 + 2 * kUnroll < fast_end) load_group(j0 + 2 * kUnroll, cdA, flA, byA, alA, frA);
         run_group(cdB, flB, byB, alB, frB);
     }
+
+    suspect |= fb_max >= 0x7f800000u;
 
     // ---- exact path: this lane's remaining ops, or all of them again if the
     // fast path met an op it could not vouch for -------------------------------
@@ -347,9 +362,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
         } else if (kind == 1u) {
             cost = c_lat + b * c_inv_l;
         } else if (kind == 2u) {
+            // over one device it costs nothing (its byte term may overflow)
             const double2 ar = s_cost[__popc(m)];
             const int n = __popc(m);
-            cost = (tier == 2 ? a.c.ar_lat_st[n] : (tier == 1 ? a.c.ar_lat_net[n] : ar.x)) + ar.y * (b * c_inv_l);
+            cost = n > 1 ? (tier == 2 ? a.c.ar_lat_st[n] : (tier == 1 ? a.c.ar_lat_net[n] : ar.x)) + ar.y * (b * c_inv_l)
+                         : 0.0;
         } else {
             // broadcast / reduce: a chain of n - 1 hops (Fig. 9's Send for n = 2)
             const int n = __popc(m);

@@ -69,6 +69,15 @@ def test_argument_errors_before_launch():
     assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
     bad = dsim.device_model(DeviceSpec(link_latency_s=float("nan")))
     assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
+    # rates whose reciprocal overflows (a zero byte count times 1/rate = inf
+    # would be NaN); a rate just above that limit is accepted
+    for spec in (DeviceSpec(flops_per_s=1e-310), DeviceSpec(mem_bytes_per_s=5e-309),
+                 DeviceSpec(link_bytes_per_s=1e-320)):
+        bad = dsim.device_model(spec)
+        assert L.dsim_simulate_tables(C.byref(tab), 10, C.byref(bad), C.byref(res), None) == dsim.DSIM_EINVAL
+        assert "reciprocal" in dsim.dsim_last_error()
+    slow = dsim.device_model(DeviceSpec(flops_per_s=1e-290, link_bytes_per_s=6e-309))
+    assert L.dsim_simulate_tables(C.byref(tab), 0, C.byref(slow), C.byref(res), None) == dsim.DSIM_OK
     # n_cand == 0 is a no-op
     assert L.dsim_simulate_tables(C.byref(tab), 0, C.byref(dev), C.byref(res), None) == dsim.DSIM_OK
     # argmin
@@ -98,6 +107,8 @@ def test_argument_errors_before_launch():
                        (DeviceSpec(network=(-1, 1e9, 0.0)), "node_size"),
                        (DeviceSpec(network=(8, 0.0, 1e-6)), "network"),
                        (DeviceSpec(network=(8, 1e9, float("nan"))), "network"),
+                       (DeviceSpec(network=(8, 1e-310, 0.0)), "network"),
+                       (DeviceSpec(streams=(2, 1e-310, 0.0)), "stream bandwidth"),
                        (DeviceSpec(streams=(-1, 1e9, 0.0)), "streams_per_gpu"),
                        (DeviceSpec(streams=(2, 0.0, 0.0)), "stream bandwidth"),
                        (DeviceSpec(streams=(2, float("nan"), 0.0)), "stream bandwidth"),

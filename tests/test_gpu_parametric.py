@@ -326,9 +326,14 @@ def test_stage_limit_and_row_width(torch_gpu):
 # (ties-to-even then depends on the clock's last bit); a large LM head beside
 # tiny layers with no launch cost makes whole layers round away against the
 # clock.  Both stress the exact long-run summation of repeated layers.
+# Rates near the smallest accepted ones put the clocks in the top binades of
+# the double range (near_overflow) or past it, to +inf, on some strategies
+# and not others (overflow).
 EDGE_DEVICES = [
     ("pow2", DeviceSpec(2.0 ** 40, 2.0 ** 36, 2.0 ** 30, 2.0 ** -18, 2.0 ** -16, 0)),
     ("pow2_nolaunch", DeviceSpec(2.0 ** 44, 2.0 ** 40, 2.0 ** 32, 0.0, 0.0, 0)),
+    ("near_overflow", DeviceSpec(1e-298, 1e-298, 1e-299, 0.0, 0.0, 0)),
+    ("overflow", DeviceSpec(1e-299, 1e-299, 1e-300, 1e-6, 0.0, 0)),
 ]
 EDGE_MODELS = [
     ("tf_long", transformer(24, 64, 4, 16, 1000, 16, 2, TRAIN_ADAM), all_strats([1, 2], [1, 2, 4], [1, 2, 3], [1, 2, 5, 16])),

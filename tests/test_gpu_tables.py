@@ -54,6 +54,13 @@ def random_tables(rng, n_cand, max_ops, n_dev, bad=False, rooted=False, classes=
     if bad:
         sel = rng.random((max_ops, n_cand)) < 0.002
         code = np.where(sel, rng.integers(0, 1 << 32, (max_ops, n_cand), dtype=np.uint64).astype(np.uint32), code)
+        # near-valid records: reserved byte 0, any of the five kinds or one
+        # beyond, device fields up to two past the last device (a send to
+        # itself, a compute op on a missing device, an empty or oversized
+        # all-reduce mask)
+        near = (rng.integers(0, 6, (max_ops, n_cand)) | (rng.integers(0, n_dev + 2, (max_ops, n_cand)) << 8) |
+                (rng.integers(0, min(1 << (n_dev + 1), 256), (max_ops, n_cand)) << 16)).astype(np.uint32)
+        code = np.where(rng.random((max_ops, n_cand)) < 0.003, near, code).astype(np.uint32)
         free = np.where(rng.random((max_ops, n_cand)) < 0.01, 10 ** 6, free).astype(np.uint32)
     else:
         free = np.minimum(free, alloc)
@@ -129,6 +136,35 @@ def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, kinds):
     assert np.array_equal(R["n_ops"], t["n_ops"].astype(np.int64))
     if bad:
         assert np.any(R["status"] & dsim.ST_MEM_UNDERFLOW)
+
+
+@pytest.mark.parametrize("n_dev", [3, 8])
+def test_tables_overflowing_costs(torch_gpu, orc, n_dev):
+    """Valid rates so slow that op costs and clocks overflow to +inf: both
+    sides reach the same infinite (and finite) times, and no NaN appears."""
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import DeviceSpec
+    torch = torch_gpu
+    rng = np.random.default_rng(4242 + n_dev)
+    n_cand, max_ops = 300, 257
+    t = random_tables(rng, n_cand, max_ops, n_dev)
+    dev = DeviceSpec(flops_per_s=1e-290, link_bytes_per_s=1e-300, launch_s=0.0)
+    g = to_gpu(torch, t)
+    init = torch.from_numpy(t["init"].view(np.int64)).cuda()
+    r = dsim.alloc_results(n_cand, n_dev)
+    dsim.dsim_simulate_tables(g, n_cand, n_dev, dev, r, init_live=init)
+    torch.cuda.synchronize()
+    R = results_np(r)
+    mk, fin = [], []
+    for c in range(n_cand):
+        n = int(t["n_ops"][c])
+        o = orc.sim_table({k: t[k][:n, c] for k in ("code", "flops", "bytes", "alloc", "free")}, n_dev, dev,
+                          init_live=t["init"][c])
+        mk.append(o["makespan"]); fin.append(o["finish"])
+    mk, fin = np.array(mk), np.array(fin)
+    assert np.isinf(mk).sum() > n_cand // 2 and np.isfinite(mk).sum() > 0 and not np.isnan(fin).any()
+    assert_times(R["makespan"], mk)
+    assert_times(R["finish"], fin)
 
 
 def gen_gpu(torch, seed, n_cand, n_ops, n_dev):
