@@ -274,7 +274,9 @@ typedef struct {
 
 /*
  * dsim_simulate_tables -- simulate n_cand explicit programs (Sec. 2.1, 3.3).
- * One GPU lane per candidate walks its ops in order.
+ * One GPU lane per candidate walks its ops in order.  n_cand <= 2^32 - 256
+ * (DSIM_ERANGE beyond); above 2^28 - 1 candidates every op takes the
+ * op-by-op path (same results, slower).
  */
 DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_cand,
                                  const dsim_device_model *device,
@@ -339,7 +341,8 @@ DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsi
  *     transform's preconditions fail, more devices than n_dev (D*H*P, twice that with overlap) or K > 16383), or
  *     DSIM_ST_NOT_TABLE (more than max_ops ops, a FLOP or byte count not
  *     exact in fp32, or an alloc / free size above 2^32 - 1).
- * 1 <= n_dev <= 8, max_ops >= 0.  One GPU lane per candidate.
+ * 1 <= n_dev <= 8, max_ops >= 0, n_cand <= 2^32 - 256.  One GPU lane per
+ * candidate.
  */
 DSIM_API dsim_status dsim_materialize_tables(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
                                     int32_t max_ops, int32_t n_dev, uint32_t *code, float *flops,

@@ -183,7 +183,8 @@ dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_cand, cons
     dsim_status st = check_device(device);
     if (st) return st;
     if (!tables || !results) return fail(DSIM_EINVAL, "tables and results must not be NULL");
-    if (n_cand < 0 || n_cand > ((int64_t)1 << 40)) return fail(DSIM_EINVAL, "bad n_cand");
+    if (n_cand < 0) return fail(DSIM_EINVAL, "bad n_cand");
+    if (n_cand > kMaxLaneCand) return fail(DSIM_ERANGE, "n_cand must be <= 2^32 - 256 for the table format");
     if (tables->n_dev < 1 || tables->n_dev > kMaxTableDev)
         return fail(DSIM_ERANGE, "n_dev must be 1..%d for the table format", kMaxTableDev);
     if (tables->max_ops < 0) return fail(DSIM_EINVAL, "max_ops must be >= 0");
@@ -250,7 +251,8 @@ dsim_status dsim_materialize_tables(const dsim_model *model, const dsim_strategy
     if (st) return st;
     if (n_dev < 1 || n_dev > kMaxTableDev) return fail(DSIM_ERANGE, "n_dev must be 1..%d", kMaxTableDev);
     if (max_ops < 0) return fail(DSIM_ERANGE, "max_ops must be >= 0");
-    if (n_cand < 0 || n_cand > ((int64_t)1 << 40)) return fail(DSIM_EINVAL, "bad n_cand");
+    if (n_cand < 0) return fail(DSIM_EINVAL, "bad n_cand");
+    if (n_cand > kMaxLaneCand) return fail(DSIM_ERANGE, "n_cand must be <= 2^32 - 256 for the table format");
     if (n_cand == 0) return DSIM_OK;
     if (!cand || !n_ops || !init_live || !status) return fail(DSIM_EINVAL, "cand, n_ops, init_live and status must not be NULL");
     if (max_ops > 0 && (!code || !flops || !bytes || !alloc_bytes || !free_bytes))

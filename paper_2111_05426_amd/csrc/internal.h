@@ -12,6 +12,9 @@ namespace dsim {
 
 // Largest device group of the explicit-table format.
 constexpr int kMaxTableDev = 8;
+// one GPU lane per candidate in a single dispatch, whose work-item count is
+// a 32-bit field
+constexpr int64_t kMaxLaneCand = ((int64_t)1 << 32) - 256;
 
 // Device-model constants as the kernels consume them.  Every reciprocal is
 // rounded once on the host.  For the table format (groups of at most 8) the

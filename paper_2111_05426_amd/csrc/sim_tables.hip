@@ -70,16 +70,21 @@ struct TabArgs {
 // so the per-lane address is just a 32-bit byte offset.
 constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kNonTemporal = 2;   // streamed once: do not keep in the caches
+// the fast path's loads reach kUnroll op rows (kUnroll * n_cand * 4 bytes)
+// from one descriptor with 32-bit offsets
+constexpr int64_t kMaxFastCand = (int64_t)(0xffffffffu / (4u * kUnroll));
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t group_rsrc(const void *base, uint32_t bytes)
 {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRsrcWord3);
 }
 
-// max of two finite non-negative doubles.  The compiler's fmax first
-// canonicalizes an operand it cannot prove canonical (a loop-carried clock),
-// one extra instruction per device and op; these operands are never NaN or
-// denormal-sensitive, so the bare instruction gives the same value.
+// max of two non-negative doubles.  The compiler's fmax first canonicalizes
+// an operand it cannot prove canonical (a loop-carried clock), one extra
+// instruction per device and op; the bare instruction gives the same value:
+// the operands are never -0.0 or signalling NaNs, and the one quiet NaN
+// that can occur (an overflowed end time times a 0.0 participation factor)
+// yields the other operand, the clock to keep, as with fmax.
 __device__ __forceinline__ double max_nn(double a, double b)
 {
     double r;
@@ -177,8 +182,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     // cannot vouch for, and that lane is re-simulated by the exact path below.
     // Indices are clamped so that even an invalid op stays inside the arrays.
     // (with nodes or streams, communication costs depend on which devices an
-    // op spans: every op takes the exact path)
-    const int32_t fast_end = (a.c.node || a.c.streams)
+    // op spans: every op takes the exact path; so do tables of more than
+    // kMaxFastCand candidates, whose op rows are too far apart for the 32-bit
+    // offsets of the fast path's loads)
+    const int32_t fast_end = (a.c.node || a.c.streams || a.n_cand > kMaxFastCand)
                                  ? 0
                                  : (int32_t)(__builtin_amdgcn_readfirstlane(wave_min) / kUnroll) * kUnroll;
 

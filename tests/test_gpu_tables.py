@@ -167,6 +167,58 @@ def test_tables_overflowing_costs(torch_gpu, orc, n_dev):
     assert_times(R["finish"], fin)
 
 
+@pytest.mark.parametrize("n_cand", [(1 << 28) - 1, 1 << 28])
+def test_tables_largest_fast_path_and_beyond(torch_gpu, orc, n_cand):
+    """The largest table the fast path takes (its loads reach four op rows,
+    16 * n_cand bytes, through 32-bit offsets) and one candidate more, which
+    the op-by-op path takes: sampled candidates, first and last included,
+    against the oracle.  About 40 GB of tables, built on the GPU."""
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import DeviceSpec
+    torch = torch_gpu
+    n_dev, max_ops = 8, 8
+    g = torch.Generator(device="cuda").manual_seed(77)
+    shape = (max_ops, n_cand)
+    kind = torch.randint(0, 10, shape, device="cuda", generator=g, dtype=torch.int32)
+    kind = torch.where(kind < 7, 0, torch.where(kind < 9, 1, 2))
+    a = torch.randint(0, n_dev, shape, device="cuda", generator=g, dtype=torch.int32)
+    b = (a + torch.randint(1, n_dev, shape, device="cuda", generator=g, dtype=torch.int32)) % n_dev
+    mask = torch.randint(1, 1 << n_dev, shape, device="cuda", generator=g, dtype=torch.int32)
+    code = torch.where(kind == 2, 2 | (mask << 16), kind | (a << 8) | (b << 16)).to(torch.int32)
+    del a, b, mask, kind
+    t = {"code": code,
+         "flops": torch.rand(shape, device="cuda", generator=g) * 1e9,
+         "bytes": torch.rand(shape, device="cuda", generator=g) * 1e7,
+         "alloc": torch.randint(0, 5000, shape, device="cuda", generator=g, dtype=torch.int32)}
+    t["free"] = torch.minimum(t["alloc"], torch.randint(0, 5000, shape, device="cuda", generator=g, dtype=torch.int32))
+    t["n_ops"] = torch.randint(0, max_ops + 1, (n_cand,), device="cuda", generator=g, dtype=torch.int32)
+    t["n_ops"][-300:] = max_ops
+    r = {"makespan": torch.empty(n_cand, dtype=torch.float64, device="cuda"),
+         "cand_peak": torch.empty(n_cand, dtype=torch.int64, device="cuda"),
+         "n_ops": torch.empty(n_cand, dtype=torch.int64, device="cuda"),
+         "status": torch.empty(n_cand, dtype=torch.int32, device="cuda"), "row_width": 0}
+    dev = DeviceSpec()
+    dsim.dsim_simulate_tables(t, n_cand, n_dev, dev, r)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(n_cand)
+    idx = np.unique(np.concatenate([[0, 1, n_cand - 257, n_cand - 1], rng.integers(0, n_cand, 200)]))
+    it = torch.from_numpy(idx).cuda()
+    cols = {k: t[k][:, it].cpu().numpy() for k in ("code", "flops", "bytes", "alloc", "free")}
+    nops = t["n_ops"][it].cpu().numpy()
+    for k in ("code", "alloc", "free"):
+        cols[k] = cols[k].view(np.uint32)
+    got = {k: r[k][it].cpu().numpy() for k in ("makespan", "cand_peak", "n_ops", "status")}
+    mk, cp, st = [], [], []
+    for i in range(len(idx)):
+        n = int(nops[i])
+        o = orc.sim_table({k: cols[k][:n, i] for k in cols}, n_dev, dev)
+        mk.append(o["makespan"]); cp.append(o["cand_peak"]); st.append(o["status"])
+    assert_times(got["makespan"], mk)
+    assert np.array_equal(got["cand_peak"].view(np.uint64), np.array(cp, np.uint64))
+    assert np.array_equal(got["status"], np.array(st, np.int32))
+    assert np.array_equal(got["n_ops"], nops.astype(np.int64))
+
+
 def gen_gpu(torch, seed, n_cand, n_ops, n_dev):
     from paper_2111_05426_amd import dsim
     g = dsim.alloc_tables(n_cand, n_ops)
