@@ -78,8 +78,12 @@ def test_argument_errors_before_launch():
         assert "reciprocal" in dsim.dsim_last_error()
     slow = dsim.device_model(DeviceSpec(flops_per_s=1e-290, link_bytes_per_s=6e-309))
     assert L.dsim_simulate_tables(C.byref(tab), 0, C.byref(slow), C.byref(res), None) == dsim.DSIM_OK
-    # n_cand == 0 is a no-op
+    # n_cand == 0 is a no-op; one lane per candidate in one dispatch caps it
     assert L.dsim_simulate_tables(C.byref(tab), 0, C.byref(dev), C.byref(res), None) == dsim.DSIM_OK
+    assert L.dsim_simulate_tables(C.byref(tab), (1 << 32) - 255, C.byref(dev), C.byref(res), None) == dsim.DSIM_ERANGE
+    assert "2^32" in dsim.dsim_last_error()
+    assert L.dsim_materialize_tables(C.byref(dsim.model_struct(ALL["tiny_mlp"].model)), None, 1 << 32, 10, 4,
+                                     *([None] * 9)) == dsim.DSIM_ERANGE
     # argmin
     assert L.dsim_argmin(None, None, None, 0, 0, 0, None, 0, None, None, None, None) == dsim.DSIM_ERANGE
     assert L.dsim_argmin(None, None, None, 0, 0, 65, None, 0, None, None, None, None) == dsim.DSIM_ERANGE
