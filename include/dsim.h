@@ -309,7 +309,9 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * Candidates are simulated one pipeline stage per GPU lane, grouped by P;
  * the grouping uses a temporary device buffer of about 4 bytes per
  * candidate, taken from and returned to the stream's memory pool
- * (hipMallocAsync / hipFreeAsync) inside the call.  n_cand < 2^31.
+ * (hipMallocAsync / hipFreeAsync) inside the call.  n_cand < 2^31, and
+ * n_cand * W below 2^32 - 2^9 lanes, W = min(row_width, 64, n_layers)
+ * rounded up to a power of two (DSIM_ERANGE otherwise: split the call).
  */
 DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strategy *cand,
                                      int64_t n_cand, const dsim_device_model *device,

@@ -1529,6 +1529,11 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     g.p_bound = pb;
     int wmax = 1;
     while (wmax < pb) wmax <<= 1;
+    // one dispatch covers every class at the widest segment: its work-item
+    // count (a 32-bit field) bounds the call
+    if ((n_cand * wmax + kLanes - 1) / kLanes + kClasses > (int64_t)(0xffffffffu / kLanes))
+        return fail(DSIM_ERANGE, "parametric: n_cand * %d lanes (the widest segment for row_width %d) exceed one "
+                                 "dispatch; split the call", wmax, pb);
     g.makespan = r.makespan;
     g.finish = r.finish;
     g.peak = r.peak;

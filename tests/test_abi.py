@@ -145,6 +145,14 @@ def test_argument_errors_before_launch():
     m.overlap = 1
     assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(two), C.byref(res), None) == dsim.DSIM_EINVAL
     assert "NULL" in dsim.dsim_last_error()
+    # one dispatch of the transform covers n_cand * (widest segment) lanes
+    m = dsim.model_struct(ALL["gpt3_175b"].model)
+    res64 = dsim.dsim_results()
+    res64.makespan = res64.cand_peak = res64.status = 8
+    res64.row_width = 64
+    fake = C.c_void_p(16)   # never dereferenced: the call fails before any launch
+    assert L.dsim_simulate_parametric(C.byref(m), fake, 1 << 27, C.byref(dev), C.byref(res64), None) == dsim.DSIM_ERANGE
+    assert "dispatch" in dsim.dsim_last_error()
     # materialiser: device count, op capacity, NULL buffers, bad model
     m = dsim.model_struct(ALL["tiny_mlp"].model)
     for nd in (0, 9):
