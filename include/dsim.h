@@ -383,7 +383,7 @@ DSIM_API dsim_status dsim_argmin(const double *makespan, const uint64_t *cand_pe
  * (its bytes) becomes a live buffer of the destination, each only while the
  * device holds fewer than 16.
  * Log-uniform means uniform over the fp32 bit patterns between the bounds.
- * Constraints: 2 <= n_dev <= 8, 0 <= n_ops < 2^27, 0 <= n_cand < 2^32.
+ * Constraints: 2 <= n_dev <= 8, 0 <= n_ops < 2^27, 0 <= n_cand <= 2^32 - 256.
  */
 DSIM_API dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, int32_t n_ops,
                                         int32_t n_dev, uint32_t *code, float *flops,

@@ -267,7 +267,7 @@ dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, int32_t n
 {
     if (n_dev < 2 || n_dev > kMaxTableDev) return fail(DSIM_ERANGE, "n_dev must be 2..%d", kMaxTableDev);
     if (n_ops < 0 || n_ops >= (1 << 27)) return fail(DSIM_ERANGE, "n_ops must be in [0, 2^27)");
-    if (n_cand < 0 || n_cand >= ((int64_t)1 << 32)) return fail(DSIM_ERANGE, "n_cand must be in [0, 2^32)");
+    if (n_cand < 0 || n_cand > kMaxLaneCand) return fail(DSIM_ERANGE, "n_cand must be in [0, 2^32 - 256]");
     if (n_cand == 0) return DSIM_OK;
     if (n_ops > 0 && (!code || !flops || !bytes || !alloc_bytes || !free_bytes))
         return fail(DSIM_EINVAL, "table buffers must not be NULL");

@@ -92,6 +92,7 @@ def test_argument_errors_before_launch():
     for nd in (1, 9):
         assert L.dsim_generate_random_tables(0, 10, 10, nd, *([None] * 7)) == dsim.DSIM_ERANGE
     assert L.dsim_generate_random_tables(0, 10, 1 << 27, 8, *([None] * 7)) == dsim.DSIM_ERANGE
+    assert L.dsim_generate_random_tables(0, (1 << 32) - 255, 10, 8, *([None] * 7)) == dsim.DSIM_ERANGE
     assert L.dsim_generate_random_tables(0, 10, 10, 8, *([None] * 7)) == dsim.DSIM_EINVAL
     # parametric: bad model / NULL candidates
     m = dsim.model_struct(ALL["tiny_mlp"].model)
