@@ -160,7 +160,10 @@ def test_network_vs_full_program(torch_gpu, orc, case, node):
 # overs with a cost, free, or slow beside nodes of two GPUs
 OV_DEVICES = [DeviceSpec(mem_cap_bytes=10 ** 6, streams=(2, 5.3e11, 1.7e-6)),
               DeviceSpec(mem_cap_bytes=10 ** 6, streams=(2, math.inf, 0.0)),
-              DeviceSpec(mem_cap_bytes=10 ** 6, streams=(2, 2.1e9, 4.3e-5), network=(2, 4.7e9, 1.9e-5))]
+              DeviceSpec(mem_cap_bytes=10 ** 6, streams=(2, 2.1e9, 4.3e-5), network=(2, 4.7e9, 1.9e-5)),
+              # rates so slow that clocks overflow to +inf on some strategies
+              DeviceSpec(3e-302, 3e-302, 1e-303, 1e-6, 0.0, 10 ** 6, streams=(2, 1e-303, 0.0)),
+              DeviceSpec(1e-301, 1e-301, 2e-303, 1e-6, 0.0, 10 ** 6, streams=(2, 2e-303, 0.0))]
 OV_CASES = [(name, replace(model, overlap=1), strat) for name, model, strat in SMALL if not model.zero]
 
 
