@@ -928,11 +928,13 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     const int lane = threadIdx.x;
     // wavefronts start widest class first (the wide launch, or the only
     // one): those walk the longest pipelines, and starting them first
-    // shortens the tail
+    // shortens the tail.  The grid is sized for the worst case; the
+    // wavefronts beyond the last class exit, and come last in either order.
     const bool widest_first = WIDE || g.narrow_end == kClasses;
-    const uint32_t blk = widest_first ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+    const uint32_t nw = g.meta[16 + kClasses] / (uint32_t)kLanes;   // wavefronts holding classes
+    if (blockIdx.x >= nw) return;
+    const uint32_t blk = widest_first ? nw - 1 - blockIdx.x : blockIdx.x;
     const uint32_t gl = blk * (uint32_t)kLanes;
-    if (gl >= g.meta[16 + kClasses]) return;      // beyond the last class (whole wave)
     int cls = 0;
     while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
     if (WIDE ? cls < kFirstWideClass : cls >= g.narrow_end) return;   // the other launch's classes
