@@ -180,7 +180,7 @@ OV_CASES = [
 ]
 
 
-@pytest.mark.parametrize("net", [False, True])
+@pytest.mark.parametrize("net", [False, True, "overflow"])
 @pytest.mark.parametrize("case", OV_CASES, ids=[c[0] for c in OV_CASES])
 def test_overlap_programs_as_tables(torch_gpu, orc, case, net):
     """Overlapped programs put two streams on every GPU (devices 2g and
@@ -190,6 +190,8 @@ def test_overlap_programs_as_tables(torch_gpu, orc, case, net):
     from paper_2111_05426_amd import dsim
     name, model, strat = case
     dev = DeviceSpec(streams=(2, 5.3e11, 1.7e-6), network=(1, 4.7e9, 1.9e-5) if net else None)
+    if net == "overflow":   # every tier so slow that some clocks overflow to +inf
+        dev = DeviceSpec(1e-301, 1e-301, 2e-303, 1e-6, 0.0, 0, streams=(2, 2e-303, 0.0), network=(1, 3e-303, 1.9e-5))
     P = int(strat[:, 2].max())
     o = orc.run_strategies(model, strat, dev, slice=False, row_width=P, threads=8)
     assert np.all(o["status"] == 0)
