@@ -1012,6 +1012,25 @@ def test_table_hand_trace(orc):
     assert [int(v) for v in r["peak"]] == [5, 7, 9]
 
 
+def test_single_device_allreduce_and_overflow(orc):
+    """An all-reduce over one device costs nothing (no peer to exchange with:
+    zero ring steps), even when its byte term alone would overflow; a send
+    whose byte term overflows ends at +inf on both of its devices, and +inf
+    then carries through the later ops of those devices, never NaN."""
+    dev = DeviceSpec(flops_per_s=1.0, mem_bytes_per_s=1.0, link_bytes_per_s=1e-300, link_latency_s=0.5, launch_s=0.0)
+    code = np.array([0 | 0 << 8, 2 | 0b001 << 16, 1 | 1 << 8 | 2 << 16, 0 | 2 << 8, 2 | 0b011 << 16], np.uint32)
+    tab = dict(code=code, flops=np.array([2, 0, 0, 1, 0], np.float32), bytes=np.array([0, 3e38, 1e10, 0, 0], np.float32),
+               alloc=np.zeros(5, np.uint32), free=np.zeros(5, np.uint32))
+    r = orc.sim_table(tab, 3, dev)
+    # d0: compute 2, then the all-reduce over {0} adds nothing -> 2;
+    # send 1 -> 2: 0.5 + 1e10 * 1e300 = inf on d1 and d2; d2 computes on:
+    # inf + 1 = inf; the all-reduce over {0, 1} starts at max(2, inf) = inf
+    fin = list(r["finish"])
+    assert fin[2] == math.inf and fin[1] == math.inf and fin[0] == math.inf
+    assert list(orc.sim_table({k: v[:2] for k, v in tab.items()}, 3, dev)["finish"]) == [2.0, 0.0, 0.0]
+    assert orc.cost(dev, orc.ALLREDUCE, 0.0, 3e38, 1) == 0.0 and orc.cost(dev, orc.SEND, 0.0, 1e10, 2) == math.inf
+
+
 # ---------------------------------------------------------------------------
 # Empirical MatMul cost (Sec. 4: a linear regression in the input sizes)
 # ---------------------------------------------------------------------------
