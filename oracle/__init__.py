@@ -244,6 +244,16 @@ def sim_strategy(model, D, H, P, K, dev, slice=False, type_cost=None, want_devic
                 flops_by_type={TYPES[i]: fbt[i] for i in range(N_TYPES)})
 
 
+def model_size_ok(model):
+    """Whether the model is within the size rule of the transform's integer
+    arithmetic (or_model_size_ok)."""
+    f = lib().or_model_size_ok
+    f.restype = C.c_int
+    f.argtypes = [C.POINTER(_Model)]
+    m = _model(model)
+    return bool(f(C.byref(m)))
+
+
 def create_grid(model, grid):
     f = lib().or_create_grid
     f.argtypes = [C.POINTER(_Model), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p,

@@ -1577,12 +1577,59 @@ static void emit_wu(mat *x, int s)
     if (s == x->P - 1) emit_wu_slot(x, s, tf_slot_head(x), tf_param(x, s, tf_slot_head(x)));
 }
 
+/* ------------------------------------------------------------------------ */
+/* Size rule of the transform's integer arithmetic.  Every op's flops,       */
+/* bytes, allocation and free, and every live-byte count, must stay below    */
+/* 2^62 (64-bit integers with room to spare), and op counts below 2^62 too:  */
+/* at most 65,536 layers, at most 2^24 devices per strategy (below).  With   */
+/* B rows, e bytes per element, L layers, width d (MLP), and for the         */
+/* transformer s tokens per sequence, T = B * s, F = d_ff, V = vocab, a      */
+/* heads, N1 = 3d^2 + dF + Vd and Kx = min(B, 16383) microbatches:           */
+/*   MLP  Q = 2Bd^2 + e(3Bd + d^2) + 64d^2                                   */
+/*        Z = L(16eBd + 8eKx d^2) + 32Ld^2 + 8eBd                            */
+/*   TF   Q = 2Td(3d + F + V + 2s) + (5 + 3e)Ba s^2 + (8 + 8e)T(d + F + V)   */
+/*            + (68 + 8e)N1 + 64T                                            */
+/*        Z = L(eT(64d + 16F + 16as) + 8eKx(4d^2 + 2dF)) + eT(8V + 16d)      */
+/*            + 48T + 16eKx Vd + 32(L(4d^2 + 2dF) + 2Vd)                      */
+/* Q bounds each op's quantities at any tensor degree H >= 1 and microbatch  */
+/* of at most B rows (each term is one of the op formulas, summed); Z bounds */
+/* the resident bytes plus every allocation of a stage's whole program (the */
+/* row-sized ones scale with the microbatch rows, which sum to at most B;    */
+/* the parameter-sized ones -- gradients, broadcast copies, the reduced      */
+/* gradient -- come at most four times per layer and microbatch plus once).  */
+/* Both are evaluated in fp64 and must be below 2^62.  Returns 1 when the    */
+/* model is within the rule, 0 otherwise. */
+int or_model_size_ok(const or_model *M)
+{
+    const double lim = 4611686018427387904.0;   /* 2^62 */
+    double B = (double)M->global_batch, e = (double)M->elem_bytes, L = (double)M->n_layers;
+    double d = (double)M->d_model, Kx, Q, Z;
+    if (M->n_layers > 65536) return 0;
+    Kx = B < 16383.0 ? B : 16383.0;
+    if (M->family == FAM_MLP) {
+        Q = 2.0 * B * d * d + e * (3.0 * B * d + d * d) + 64.0 * d * d;
+        Z = L * (16.0 * e * B * d + 8.0 * e * Kx * d * d) + 32.0 * L * d * d + 8.0 * e * B * d;
+    } else {
+        double s = (double)M->seq_len, F = (double)M->d_ff, V = (double)M->vocab, a = (double)M->n_heads;
+        double T = B * s, N1 = 3.0 * d * d + d * F + V * d;
+        Q = 2.0 * T * d * (3.0 * d + F + V + 2.0 * s) + (5.0 + 3.0 * e) * B * a * s * s +
+            (8.0 + 8.0 * e) * T * (d + F + V) + (68.0 + 8.0 * e) * N1 + 64.0 * T;
+        Z = L * (e * T * (64.0 * d + 16.0 * F + 16.0 * a * s) + 8.0 * e * Kx * (4.0 * d * d + 2.0 * d * F)) +
+            e * T * (8.0 * V + 16.0 * d) + 48.0 * T + 16.0 * e * Kx * V * d +
+            32.0 * (L * (4.0 * d * d + 2.0 * d * F) + 2.0 * V * d);
+    }
+    return Q < lim && Z < lim;
+}
+
 /* filters of a strategy (the grid's validity rules and the transform's
  * preconditions); returns 0 when valid */
 static int strategy_invalid(const or_model *M, int D, int H, int P, int K)
 {
     int64_t B = M->global_batch, L = M->n_layers;
     if (D < 1 || H < 1 || P < 1 || K < 1) return 1;
+    /* at most 2^24 devices: with at most 65,536 layers and 16,383
+     * microbatches every op count of the program stays below 2^62 */
+    if ((int64_t)D * H * P > ((int64_t)1 << 24)) return 1;
     if (M->elem_bytes < 1 || M->d_model < 1 || L < 1 || B < 1) return 1;
     if (B % D != 0) return 1;
     if ((int64_t)K > B / D) return 1;
@@ -1635,6 +1682,7 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     double *fin = NULL;
     uint64_t *pk = NULL;
     memset(res, 0, sizeof *res);
+    if (!or_model_size_ok(M)) return -5;
     if (strategy_invalid(M, D, H, P, K)) { res->status = ST_BAD_STRATEGY; return 0; }
     if (dm->node_size > 0) {
         /* nodes must cut every tensor-parallel group, data-parallel group
@@ -1860,6 +1908,7 @@ int or_create_grid(const or_model *M, int max_devices, int exact_devices, int k_
     int64_t n = 0;
     int P, K, H, D;
     if (max_devices < 1 || k_max < 1 || k_mode < 0 || k_mode > 2) return -1;
+    if (!or_model_size_ok(M)) return -5;
     for (P = 1; P <= max_devices; P *= 2) {
         for (K = 1; K <= k_max; K++) {
             if (k_mode == 0 && (K & (K - 1)) != 0) continue;
