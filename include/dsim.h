@@ -167,6 +167,24 @@ typedef struct {
  *        before its optimizer op.  Sends are blocking (Sec. 2.1), so a
  *        hand-over waits for the communication stream's previous
  *        all-reduce.  Requires device.streams_per_gpu == 2. */
+/* Size rule (every call taking a model returns DSIM_ERANGE beyond it): the
+ * transform computes every op's flops, bytes, allocation and free, and every
+ * live-byte count, in 64-bit integers.  A model must have n_layers <= 65536,
+ * each of d_model, d_ff, seq_len, vocab, global_batch <= 1e15, and, with
+ * B = global_batch, e = elem_bytes, L = n_layers, d = d_model, and for the
+ * transformer s = seq_len, F = d_ff, V = vocab, a = n_heads, T = B*s,
+ * N1 = 3d^2 + dF + Vd, Kx = min(B, 16383), both of
+ *   MLP  Q = 2Bd^2 + e(3Bd + d^2) + 64d^2
+ *        Z = L(16eBd + 8eKx d^2) + 32Ld^2 + 8eBd
+ *   TF   Q = 2Td(3d + F + V + 2s) + (5 + 3e)Ba s^2 + (8 + 8e)T(d + F + V)
+ *            + (68 + 8e)N1 + 64T
+ *        Z = L(eT(64d + 16F + 16as) + 8eKx(4d^2 + 2dF)) + eT(8V + 16d) + 48T
+ *            + 16eKx Vd + 32(L(4d^2 + 2dF) + 2Vd)
+ * evaluated in fp64, below 2^62.  Q bounds any single op quantity for every
+ * tensor degree and microbatch, Z the resident bytes plus all allocations
+ * of a stage's program.  A strategy with D*H*P > 2^24 devices is invalid
+ * (status DSIM_ST_BAD_STRATEGY), which with the layer and microbatch bounds
+ * keeps every op count below 2^62. */
 typedef struct {
     int32_t family, mode, n_layers, n_heads;
     int64_t d_model, d_ff, seq_len, vocab, global_batch;
@@ -196,7 +214,7 @@ typedef struct {
  * Host call.  Writes at most `cap` strategies to the host array `out`
  * (NULL: count only) and the total count to *n_out.  Order: P outermost,
  * then K, then H, then D innermost, each ascending.  A strategy is valid
- * when D | global_batch, K <= global_batch/D, P <= n_layers and H divides
+ * when D*H*P <= 2^24, D | global_batch, K <= global_batch/D, P <= n_layers and H divides
  * the sharded widths (MLP: d_model; transformer: n_heads, d_model, d_ff),
  * and, for the MLP with H > 1, every stage holds an even number of layers
  * (column/row-parallel pairs).  Returns DSIM_ENOSPC if out != NULL and the

@@ -110,11 +110,36 @@ static dsim_status check_model(const dsim_model *m)
             return fail(DSIM_EINVAL, "transformer needs n_heads, d_ff, seq_len, vocab >= 1");
         if (m->d_model % m->n_heads != 0) return fail(DSIM_EINVAL, "d_model must be a multiple of n_heads");
     }
-    // keep every size product of the transform inside 64 bits
     const double big = 1e15;
     if ((double)m->d_model > big || (double)m->global_batch > big || (double)m->d_ff > big ||
         (double)m->seq_len > big || (double)m->vocab > big)
         return fail(DSIM_ERANGE, "model dimensions too large");
+    if (m->n_layers > kMaxLayers) return fail(DSIM_ERANGE, "at most %d layers", kMaxLayers);
+    // the size rule (dsim.h): every op quantity below 2^62 (q) and every
+    // live-byte count below 2^62 (z), bounded in fp64 over any tensor degree
+    // and microbatch split
+    const double rows = (double)m->global_batch, eb = (double)m->elem_bytes, nl = (double)m->n_layers;
+    const double w = (double)m->d_model, kx = std::fmin(rows, (double)kMaxK);
+    double q, z;
+    if (m->family == DSIM_MLP) {
+        const double ww = w * w;
+        q = 2.0 * rows * ww + eb * (3.0 * rows * w + ww) + 64.0 * ww;
+        z = nl * (16.0 * eb * rows * w + 8.0 * eb * kx * ww) + 32.0 * nl * ww + 8.0 * eb * rows * w;
+    } else {
+        const double sq = (double)m->seq_len, ff = (double)m->d_ff, voc = (double)m->vocab;
+        const double hd = (double)m->n_heads, tok = rows * sq;
+        const double lay = 4.0 * w * w + 2.0 * w * ff;          // one layer's parameters
+        const double n1 = 3.0 * w * w + w * ff + voc * w;       // largest parameter slots
+        q = 2.0 * tok * w * (3.0 * w + ff + voc + 2.0 * sq) + (5.0 + 3.0 * eb) * rows * hd * sq * sq +
+            (8.0 + 8.0 * eb) * tok * (w + ff + voc) + (68.0 + 8.0 * eb) * n1 + 64.0 * tok;
+        z = nl * (eb * tok * (64.0 * w + 16.0 * ff + 16.0 * hd * sq) + 8.0 * eb * kx * lay) +
+            eb * tok * (8.0 * voc + 16.0 * w) + 48.0 * tok + 16.0 * eb * kx * voc * w +
+            32.0 * (nl * lay + 2.0 * voc * w);
+    }
+    const double lim = 0x1p62;
+    if (!(q < lim) || !(z < lim))
+        return fail(DSIM_ERANGE, "model beyond the size rule: op quantities up to %.3g, live bytes up to %.3g "
+                                 "(both must stay below 2^62)", q, z);
     return DSIM_OK;
 }
 
@@ -122,6 +147,7 @@ static dsim_status check_model(const dsim_model *m)
 static bool strategy_ok(const dsim_model &m, int D, int H, int P, int K)
 {
     if (D < 1 || H < 1 || P < 1 || K < 1) return false;
+    if ((int64_t)D * H * P > kMaxDevices) return false;
     const int64_t B = m.global_batch;
     if (B % D != 0 || (int64_t)K > B / D || P > m.n_layers) return false;
     if (m.family == DSIM_MLP) {

@@ -12,6 +12,12 @@ namespace dsim {
 
 // Largest device group of the explicit-table format.
 constexpr int kMaxTableDev = 8;
+// Microbatches per strategy; layers per model and devices per strategy (the
+// size rule): with at most kMaxLayers layers, kMaxK microbatches and
+// kMaxDevices devices every op count of a program stays below 2^62.
+constexpr int kMaxK = 16383;
+constexpr int kMaxLayers = 65536;
+constexpr int64_t kMaxDevices = (int64_t)1 << 24;
 // one GPU lane per candidate in a single dispatch, whose work-item count is
 // a 32-bit field
 constexpr int64_t kMaxLaneCand = ((int64_t)1 << 32) - 256;

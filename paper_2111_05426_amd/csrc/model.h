@@ -51,7 +51,6 @@
 namespace dsim {
 
 constexpr int kMaxStages = 64;
-constexpr int kMaxK = 16383;
 
 // Per-candidate constants.
 struct Ctx {
@@ -81,6 +80,7 @@ struct Ctx {
 __device__ inline bool strategy_ok(const dsim_model &m, int D, int H, int P, int K)
 {
     if (D < 1 || H < 1 || P < 1 || K < 1) return false;
+    if ((int64_t)D * H * P > kMaxDevices) return false;
     const int64_t B = m.global_batch;
     if (B % D != 0 || (int64_t)K > B / D || P > m.n_layers) return false;
     if (m.family == DSIM_MLP) {

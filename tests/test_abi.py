@@ -165,6 +165,54 @@ def test_argument_errors_before_launch():
     assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_EINVAL
 
 
+def _grid_rc(model):
+    L = dsim.lib()
+    m = dsim.model_struct(model)
+    g = dsim.dsim_grid_spec(1, 0, 0, 1, 0)
+    n = C.c_int64()
+    return L.dsim_create_grid(C.byref(m), C.byref(g), None, 0, C.byref(n))
+
+
+def test_size_rule_at_both_sides_of_the_bound(orc):
+    """The size rule (dsim.h) on the host: the largest Gemm of a one-layer
+    MLP at 2^61 flops is accepted, at 2^62 refused; a 65,537-layer model and
+    a 2^20-token GPT-3-shaped sequence are refused; the oracle agrees."""
+    d = 2 ** 20
+    cases = [(mlp(1, d, 2 ** 20, 2, TRAIN_SGD), dsim.DSIM_OK), (mlp(1, d, 2 ** 21, 2, TRAIN_SGD), dsim.DSIM_ERANGE),
+             (mlp(65536, 64, 64, 2, TRAIN_SGD), dsim.DSIM_OK), (mlp(65537, 64, 64, 2, TRAIN_SGD), dsim.DSIM_ERANGE),
+             (transformer(96, 12288, 96, 2 ** 16, 50257, 1536, 2, INFER), dsim.DSIM_OK),
+             (transformer(96, 12288, 96, 2 ** 20, 50257, 1536, 2, INFER), dsim.DSIM_ERANGE)]
+    for model, want in cases:
+        assert _grid_rc(model) == want, model
+        assert orc.model_size_ok(model) == (want == dsim.DSIM_OK)
+    assert "size rule" in (_grid_rc(cases[1][0]) and dsim.dsim_last_error())
+    L = dsim.lib()
+    dev = dsim.device_model(DeviceSpec())
+    res = dsim.dsim_results()
+    m = dsim.model_struct(cases[1][0])
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_ERANGE
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_ERANGE
+
+
+def test_size_rule_matches_oracle_on_random_models(orc):
+    rng = np.random.default_rng(7)
+    for i in range(400):
+        tf = i % 2 == 1
+        mode = int(rng.integers(0, 4))
+        e = int(rng.choice([1, 2, 4, 8]))
+        L = int(2 ** rng.uniform(0, 16.5))
+        B = int(2 ** rng.uniform(0, 40))
+        if tf:
+            a = int(2 ** rng.uniform(0, 10))
+            d = a * int(2 ** rng.uniform(0, 14))
+            model = transformer(L, d, a, int(2 ** rng.uniform(0, 22)), int(2 ** rng.uniform(1, 24)), B, e, mode,
+                                d_ff=int(2 ** rng.uniform(0, 20)))
+        else:
+            model = mlp(L, int(2 ** rng.uniform(0, 26)), B, e, mode)
+        ok = orc.model_size_ok(model)
+        assert (_grid_rc(model) == dsim.DSIM_OK) == ok, model
+
+
 def test_struct_layouts_match_header():
     """Every struct of include/dsim.h and its ctypes mirror in the binding:
     the same fields, in the same order, of the same C types."""

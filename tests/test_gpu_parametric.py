@@ -315,6 +315,26 @@ def test_microbatch_limit(torch_gpu, orc):
     torch_gpu.cuda.synchronize()
 
 
+def test_device_count_limit(torch_gpu, orc):
+    """More than 2^24 devices per strategy is invalid on both sides (the
+    size rule keeps every op count below 2^62); 2^24 devices simulate."""
+    m = mlp(4, 16, 2 ** 26, 2, TRAIN_SGD)
+    strat = np.array([(2 ** 25, 1, 1, 1), (2 ** 23, 2, 2, 1), (2 ** 22, 4, 4, 1), (2 ** 24, 1, 1, 1),
+                      (2 ** 22, 2, 2, 1)], np.int32)
+    g = run_gpu(torch_gpu, m, strat, DeviceSpec(), 4)
+    assert list(g["status"]) == [16, 16, 16, 0, 0]
+    for i in range(3):
+        o = orc.sim_strategy(m, *strat[i].tolist(), DeviceSpec(), slice=True, want_devices=False)
+        assert o["status"] == 16
+    # op count of 2^24 replicas: linear in D (every replica runs the same
+    # ops, one all-reduce per layer over all of them), from the oracle's
+    # whole programs at D = 2 and 4
+    n2 = orc.sim_strategy(m, 2, 1, 1, 1, DeviceSpec(), want_devices=False)["n_ops"]
+    n4 = orc.sim_strategy(m, 4, 1, 1, 1, DeviceSpec(), want_devices=False)["n_ops"]
+    per = (n4 - n2) // 2
+    assert g["n_ops"][3] == 2 ** 24 * per + (n2 - 2 * per) and g["makespan"][3] > 0
+
+
 def test_stage_limit_and_row_width(torch_gpu):
     """More than 64 pipeline stages, or more than results.row_width, is
     refused per candidate (DSIM_ST_BAD_STRATEGY), never overrun."""
