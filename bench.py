@@ -165,13 +165,15 @@ def bench_parametric(torch, dsim, W, reps, warmup=1):
     out_idx = torch.empty(k, dtype=torch.int64, device="cuda")
     out_mk = torch.empty(k, dtype=torch.float64, device="cuda")
     found = torch.empty(1, dtype=torch.int32, device="cuda")
+    pws = dsim.alloc_parametric_workspace(n)
+    side = torch.cuda.Stream()   # the split launch of large transformer grids runs on two streams
     dev = W.device
     ev = []
 
     def step(record):
         e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
         e0.record()
-        dsim.dsim_simulate_parametric(W.model, cand, dev, res)
+        dsim.dsim_simulate_parametric(W.model, cand, dev, res, workspace=pws, side_stream=side)
         e1.record()
         dsim.dsim_argmin(res["makespan"], res["cand_peak"], res["status"], dev.mem_cap_bytes, k, ws, out_idx,
                          out_mk, found)

@@ -24,8 +24,9 @@
  *     never throws, never exits.  dsim_last_error() describes the last
  *     failure of the calling thread.
  *   - Pointers documented as "device" are HIP device pointers; "host" ones
- *     are host memory.  The caller owns every buffer; the library keeps no
- *     allocation between calls.
+ *     are host memory.  The caller owns every buffer, workspaces included;
+ *     the library allocates no device memory and keeps nothing between
+ *     calls.
  *   - Kernels are enqueued on `hip_stream` (a hipStream_t, NULL = the null
  *     stream); results are valid once that stream has been synchronised.
  *   - Arguments are validated on the host before any launch.  Errors inside
@@ -247,8 +248,12 @@ DSIM_API dsim_status dsim_create_grid(const dsim_model *model, const dsim_grid_s
  *          reduce allocates on a and frees on every member.  Every touched
  *          device samples its peak after the allocation and before the
  *          free.
- *   n_ops: per candidate op count (<= max_ops); NULL = max_ops for all.
- *   init_live: [n_cand * n_dev] bytes live at t = 0; NULL = zero.
+ *   n_ops: per candidate op count; NULL = max_ops for all.  A count above
+ *          max_ops sets DSIM_ST_BAD_OP and max_ops ops are simulated.
+ *   init_live: [n_cand * n_dev] bytes live at t = 0; NULL = zero.  A
+ *          device's live bytes (init_live plus its allocations) must stay
+ *          below 2^64; candidates starting at 2^62 or more on some device
+ *          take a slower exact path (same results).
  *   n_dev: 1..8.
  * An invalid op is skipped (no time, no memory) and flagged in status.
  */
@@ -324,16 +329,26 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * replicas before its optimizer op; memory by def/use liveness (outputs
  * allocated, peak sampled, inputs at their last use freed; weights,
  * optimizer state and the replica's inputs resident from t = 0).
- * Candidates are simulated one pipeline stage per GPU lane, grouped by P;
- * the grouping uses a temporary device buffer of about 4 bytes per
- * candidate, taken from and returned to the stream's memory pool
- * (hipMallocAsync / hipFreeAsync) inside the call.  n_cand < 2^31, and
- * n_cand * W below 2^32 - 2^9 lanes, W = min(row_width, 64, n_layers)
- * rounded up to a power of two (DSIM_ERANGE otherwise: split the call).
+ * Candidates are simulated one pipeline stage per GPU lane, grouped by P
+ * through a permutation held in `workspace`: a device buffer of at least
+ * dsim_parametric_workspace(n_cand) bytes (about 4 bytes per candidate,
+ * DSIM_ENOSPC if shorter), owned by the caller, in use until hip_stream has
+ * passed the call; no word of it needs clearing.  Transformer grids of
+ * 8,192 or more candidates are simulated by two kernels, one for the
+ * candidates of 1 to 4 stages and one for the others; they run side by side
+ * when side_stream is a second stream (hip_stream's earlier work is awaited
+ * on it and the call's work on side_stream is awaited on hip_stream before
+ * anything later, through two events the call creates and destroys), and
+ * one after the other on hip_stream when side_stream is NULL or equal to
+ * it; the results are the same.  n_cand < 2^31, and n_cand * W below
+ * 2^32 - 2^9 lanes, W = min(row_width, 64, n_layers) rounded up to a power
+ * of two (DSIM_ERANGE otherwise: split the call).
  */
+DSIM_API size_t dsim_parametric_workspace(int64_t n_cand);
 DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strategy *cand,
                                      int64_t n_cand, const dsim_device_model *device,
-                                     const dsim_results *results, void *hip_stream);
+                                     const dsim_results *results, void *workspace, size_t ws_bytes,
+                                     void *side_stream, void *hip_stream);
 
 /*
  * dsim_materialize_tables -- write the whole distributed program of each of

@@ -225,9 +225,15 @@ dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_cand, cons
     return launch_sim_tables(*tables, n_cand, make_consts(*device), *results, (hipStream_t)hip_stream);
 }
 
+size_t dsim_parametric_workspace(int64_t n_cand)
+{
+    if (n_cand < 0 || n_cand > ((int64_t)1 << 40)) return 0;
+    return parametric_workspace(n_cand);
+}
+
 dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
                                      const dsim_device_model *device, const dsim_results *results,
-                                     void *hip_stream)
+                                     void *workspace, size_t ws_bytes, void *side_stream, void *hip_stream)
 {
     dsim_status st = check_model(model);
     if (st) return st;
@@ -245,7 +251,10 @@ dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strateg
         return fail(DSIM_EINVAL, "makespan, cand_peak and status must not be NULL");
     if ((results->finish || results->peak) && results->row_width < 1)
         return fail(DSIM_ENOSPC, "row_width must be >= 1");
-    return launch_parametric(*model, cand, n_cand, make_consts(*device), *results, (hipStream_t)hip_stream);
+    if (!workspace || ws_bytes < parametric_workspace(n_cand))
+        return fail(DSIM_ENOSPC, "workspace needs %zu bytes", parametric_workspace(n_cand));
+    return launch_parametric(*model, cand, n_cand, make_consts(*device), *results, workspace,
+                             (hipStream_t)hip_stream, (hipStream_t)side_stream);
 }
 
 size_t dsim_argmin_workspace(int64_t n, int32_t k)

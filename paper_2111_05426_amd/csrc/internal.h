@@ -65,8 +65,10 @@ size_t argmin_workspace(int64_t n, int32_t k);
 dsim_status launch_argmin(const double *mk, const uint64_t *pk, const int32_t *st, int64_t n,
                           uint64_t cap, int32_t k, void *ws, int64_t *out_idx, double *out_mk,
                           int32_t *out_found, hipStream_t s);
+size_t parametric_workspace(int64_t n_cand);
 dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand,
-                              const CostConsts &c, const dsim_results &r, hipStream_t s);
+                              const CostConsts &c, const dsim_results &r, void *ws, hipStream_t s,
+                              hipStream_t side);
 dsim_status launch_materialize(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, int32_t max_ops,
                                int32_t n_dev, uint32_t *code, float *flops, float *bytes, uint32_t *alloc,
                                uint32_t *freeb, uint32_t *n_ops, uint64_t *init_live, int32_t *status,

@@ -41,7 +41,6 @@
 // A counting-sort pre-pass groups the candidates by segment width into a
 // temporary permutation (stable, so the grid's own order keeps wavefronts
 // uniform in K).
-#include <mutex>
 #include <type_traits>
 
 #include "model.h"
@@ -1489,34 +1488,15 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strateg
 
 }  // namespace
 
-namespace {
-
-// One side stream per device (default priority), created on first use and
-// kept until the process ends.
-hipError_t side_stream(hipStream_t *out)
+size_t parametric_workspace(int64_t n_cand)
 {
-    static std::mutex mu;
-    static hipStream_t streams[64] = {};
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    std::lock_guard<std::mutex> lock(mu);
-    if (!streams[dev]) {
-        e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
-        if (e != hipSuccess) {
-            streams[dev] = nullptr;
-            return e;
-        }
-    }
-    *out = streams[dev];
-    return hipSuccess;
+    const int64_t nb = (n_cand + kScanBlock - 1) / kScanBlock;
+    // per-block class counts, the class table (32 words), the permutation
+    return (size_t)(nb * 8 + 32 + n_cand) * sizeof(uint32_t);
 }
 
-}  // namespace
-
 dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, const CostConsts &c,
-                              const dsim_results &r, hipStream_t s)
+                              const dsim_results &r, void *ws, hipStream_t s, hipStream_t side)
 {
     if (n_cand > (int64_t)0x7fffffff)
         return fail(DSIM_ERANGE, "parametric: at most 2^31 - 1 candidates per call");
@@ -1545,13 +1525,9 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     g.status = r.status;
     g.c = c;
 
-    // temporary: per-block class counts, class table, permutation
+    // workspace: per-block class counts, class table, permutation (every
+    // word is written before it is read: nothing needs clearing)
     const int64_t nb = (n_cand + kScanBlock - 1) / kScanBlock;
-    const size_t counts_b = (size_t)nb * 8 * sizeof(uint32_t), meta_b = 32 * sizeof(uint32_t);
-    const size_t perm_b = (size_t)n_cand * sizeof(uint32_t);
-    void *ws = nullptr;
-    hipError_t e = hipMallocAsync(&ws, counts_b + meta_b + perm_b, s);
-    if (e != hipSuccess) return hip_fail(e, "parametric: temporary buffer");
     uint32_t *counts = static_cast<uint32_t *>(ws);
     uint32_t *meta = counts + (size_t)nb * 8;
     uint32_t *perm = meta + 32;
@@ -1567,7 +1543,8 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     const int64_t waves = (n_cand * wmax + kLanes - 1) / kLanes + kClasses;
     // A large transformer grid splits: the narrow classes run beside the
     // wide ones (whose smaller LDS footprint lets two wavefronts share a
-    // SIMD).  Small grids and MLPs take one launch for every class.
+    // SIMD) when the caller gives a second stream, else after them on the
+    // one stream.  Small grids and MLPs take one launch for every class.
     const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
     g.narrow_end = split ? kFirstWideClass : kClasses;
     const bool rc = m.mode != DSIM_INFER && m.recompute != 0;
@@ -1575,49 +1552,42 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     const bool ov = m.mode != DSIM_INFER && m.overlap != 0;
     const bool tf = m.family == DSIM_TRANSFORMER;
     const dim3 grid((unsigned)waves), block(kLanes);
+    hipError_t e = hipSuccess;
     if (!split) {
         launch_kernel(rc, zr, ov, tf, false, grid, block, s, g);
-    } else {
-        // narrow segments on a side stream, wide ones on the caller's: the
-        // two launches need different amounts of LDS per wavefront and run
-        // side by side; the caller's stream waits for both
-        hipStream_t side = nullptr;
-        e = side_stream(&side);
-        hipEvent_t fork = nullptr, join = nullptr;
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
-        if (e == hipSuccess) e = hipEventRecord(fork, s);
-        if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
-        bool side_launched = false;
-        if (e == hipSuccess) {
-            // the narrow classes (1, 2, 4 lanes per candidate) come first in
-            // the class layout: a grid over their lanes is enough
-            const int64_t narrow_waves = (n_cand * 4 + kLanes - 1) / kLanes + kClasses;
-            const dim3 grid_n((unsigned)(narrow_waves < waves ? narrow_waves : waves));
-            launch_kernel(rc, zr, ov, true, false, grid_n, block, side, g);
-            e = hipGetLastError();
-            side_launched = e == hipSuccess;
-        }
-        if (e == hipSuccess) {
-            launch_kernel(rc, zr, ov, true, true, grid, block, s, g);
-            e = hipGetLastError();
-        }
-        if (e == hipSuccess) e = hipEventRecord(join, side);
-        if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
-        if (fork) (void)hipEventDestroy(fork);
-        if (join) (void)hipEventDestroy(join);
-        if (e != hipSuccess) {
-            // the side launch may still read the temporary buffer
-            if (side_launched) (void)hipStreamSynchronize(side);
-            (void)hipFreeAsync(ws, s);
-            return hip_fail(e, "parametric launch");
-        }
+        e = hipGetLastError();
+        return e == hipSuccess ? DSIM_OK : hip_fail(e, "parametric launch");
     }
-    e = hipGetLastError();
-    const hipError_t e2 = hipFreeAsync(ws, s);
-    if (e != hipSuccess) return hip_fail(e, "parametric launch");
-    if (e2 != hipSuccess) return hip_fail(e2, "parametric: temporary buffer release");
-    return DSIM_OK;
+    // the narrow classes (1, 2, 4 lanes per candidate) come first in the
+    // class layout: a grid over their lanes is enough
+    const int64_t narrow_waves = (n_cand * 4 + kLanes - 1) / kLanes + kClasses;
+    const dim3 grid_n((unsigned)(narrow_waves < waves ? narrow_waves : waves));
+    if (!side || side == s) {
+        launch_kernel(rc, zr, ov, true, true, grid, block, s, g);
+        launch_kernel(rc, zr, ov, true, false, grid_n, block, s, g);
+        e = hipGetLastError();
+        return e == hipSuccess ? DSIM_OK : hip_fail(e, "parametric launch");
+    }
+    // narrow segments on the side stream, wide ones on the caller's: the
+    // side stream waits for the pre-pass, the caller's stream for both
+    hipEvent_t fork = nullptr, join = nullptr;
+    e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(fork, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
+    if (e == hipSuccess) {
+        launch_kernel(rc, zr, ov, true, false, grid_n, block, side, g);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) {
+        launch_kernel(rc, zr, ov, true, true, grid, block, s, g);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = hipEventRecord(join, side);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+    if (fork) (void)hipEventDestroy(fork);
+    if (join) (void)hipEventDestroy(join);
+    return e == hipSuccess ? DSIM_OK : hip_fail(e, "parametric launch");
 }
 
 }  // namespace dsim

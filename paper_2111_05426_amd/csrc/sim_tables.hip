@@ -151,19 +151,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
 
     const int64_t c = (int64_t)blockIdx.x * kBlock + tid;
     const bool active = c < a.n_cand;
+    // the fast path compares live bytes as fp64 bit patterns, which order
+    // like the integers below 2^63 - 2^52: a lane starting at 2^62 or more
+    // live bytes on a device (its ops add less than 2^43) takes the exact path
+    bool big_init = false;
 #pragma unroll
     for (int d = 0; d < ND; ++d) {
         const uint64_t init = (active && a.init_live) ? a.init_live[c * ND + d] : 0;
+        big_init |= init >= (1ull << 62);
         s_mem[d][tid] = make_ulonglong2(init, init);
     }
     __syncthreads();
 
     uint32_t nops = active ? (a.n_ops ? a.n_ops[c] : (uint32_t)a.max_ops) : 0xffffffffu;
-    int32_t st = 0;
-    if (active && nops > (uint32_t)a.max_ops) {
-        st |= DSIM_ST_BAD_OP;
-        nops = (uint32_t)a.max_ops;
-    }
+    // a lane whose op count exceeds max_ops is flagged and simulates max_ops
+    // ops; the flag survives the exact path's restart (st0)
+    const int32_t st0 = (active && nops > (uint32_t)a.max_ops) ? DSIM_ST_BAD_OP : 0;
+    int32_t st = st0;
+    if (st0) nops = (uint32_t)a.max_ops;
     // ops every lane of the wavefront has (inactive lanes do not constrain it)
     uint32_t wave_min = nops;
 #pragma unroll
@@ -191,7 +196,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
 
     const size_t blk = (size_t)blockIdx.x * kBlock;
     const uint32_t lane_b = (uint32_t)tid * 4u;
-    bool suspect = false;
+    bool suspect = big_init;
     uint32_t fb_max = 0;   // largest flops or bytes bit pattern met on the fast path
 
     // two register sets of kUnroll op records: one is processed while the
@@ -326,7 +331,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     int32_t j = fast_end;
     if (suspect) {
         j = 0;
-        st = 0;
+        st = st0;
 #pragma unroll
         for (int d = 0; d < ND; ++d) {
             clk[d] = 0.0;

@@ -79,9 +79,11 @@ def lib():
                                        C.c_int64, C.POINTER(C.c_int64)]
         L.dsim_simulate_tables.argtypes = [C.POINTER(dsim_tables), C.c_int64, C.POINTER(dsim_device_model),
                                            C.POINTER(dsim_results), C.c_void_p]
+        L.dsim_parametric_workspace.restype = C.c_size_t
+        L.dsim_parametric_workspace.argtypes = [C.c_int64]
         L.dsim_simulate_parametric.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64,
                                                C.POINTER(dsim_device_model), C.POINTER(dsim_results),
-                                               C.c_void_p]
+                                               C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p]
         L.dsim_argmin_workspace.restype = C.c_size_t
         L.dsim_argmin_workspace.argtypes = [C.c_int64, C.c_int32]
         L.dsim_argmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_uint64, C.c_int32,
@@ -120,6 +122,63 @@ def _ptr(t):
     if isinstance(t, np.ndarray):
         return t.ctypes.data
     return t.data_ptr()
+
+
+class _Args:
+    """Checks the tensor arguments of one call before their addresses go to
+    the library: each a contiguous torch tensor of one of the given dtypes
+    with the given shape (None entries free) or element count; then, once
+    all of them have passed, that every one lies on a GPU.  Raises
+    ValueError: a mismatch would make a kernel read or write out of bounds."""
+
+    def __init__(self):
+        self.seen = []
+
+    def tensor(self, name, t, dtypes, shape=None, numel=None, optional=False):
+        if t is None:
+            if optional:
+                return
+            raise ValueError("%s is required" % name)
+        if not hasattr(t, "data_ptr") or not hasattr(t, "dtype"):
+            raise ValueError("%s must be a torch tensor" % name)
+        if t.dtype not in dtypes:
+            raise ValueError("%s must be of dtype %s, not %s" % (name, " or ".join(str(d) for d in dtypes),
+                                                                  t.dtype))
+        if shape is not None:
+            if t.dim() != len(shape) or any(w is not None and int(a) != int(w) for a, w in zip(t.shape, shape)):
+                raise ValueError("%s must have shape %s, not %s" % (name, tuple(shape), tuple(t.shape)))
+        if numel is not None and t.numel() < numel:
+            raise ValueError("%s holds %d elements, needs %d" % (name, t.numel(), numel))
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % name)
+        self.seen.append((name, t))
+
+    def results(self, results, n, row_width_min=1):
+        for name in ("makespan", "cand_peak", "status"):
+            if results.get(name) is None:
+                raise ValueError("results[%r] is required" % name)
+        self.tensor("results['makespan']", results["makespan"], _dt("float64"), shape=(n,))
+        self.tensor("results['cand_peak']", results["cand_peak"], _dt("int64", "uint64"), shape=(n,))
+        self.tensor("results['status']", results["status"], _dt("int32"), shape=(n,))
+        for name in ("n_ops", "walked_ops"):
+            self.tensor("results[%r]" % name, results.get(name), _dt("int64", "uint64"), shape=(n,), optional=True)
+        if results.get("finish") is not None or results.get("peak") is not None:
+            rw = int(results.get("row_width", 0))
+            if rw < row_width_min:
+                raise ValueError("results row_width %d must be >= %d" % (rw, row_width_min))
+            self.tensor("results['finish']", results.get("finish"), _dt("float64"), shape=(n, rw), optional=True)
+            self.tensor("results['peak']", results.get("peak"), _dt("int64", "uint64"), shape=(n, rw),
+                        optional=True)
+
+    def on_gpu(self):
+        for name, t in self.seen:
+            if t.device.type != "cuda":
+                raise ValueError("%s must be a GPU tensor, not on %s" % (name, t.device))
+
+
+def _dt(*names):
+    import torch
+    return tuple(getattr(torch, n) for n in names)
 
 
 def _stream(stream):
@@ -190,8 +249,19 @@ def alloc_tables(n_cand, max_ops, device="cuda"):
 
 def dsim_simulate_tables(tables, n_cand, n_dev, device, results, init_live=None, stream=None):
     """tables: dict of device tensors shaped (max_ops, n_cand) (code/alloc/free
-    as int32 bit patterns of the uint32 fields), optional n_ops (n_cand,)."""
-    max_ops = int(tables["code"].shape[0]) if tables["code"].dim() == 2 else int(tables["max_ops"])
+    as int32 bit patterns of the uint32 fields), optional n_ops (n_cand,);
+    init_live: optional (n_cand, n_dev) int64."""
+    n_cand = int(n_cand)
+    a = _Args()
+    a.tensor("tables['code']", tables.get("code"), _dt("int32", "uint32"), shape=(None, n_cand))
+    max_ops = int(tables["code"].shape[0])
+    for name, dts in (("flops", ("float32",)), ("bytes", ("float32",)), ("alloc", ("int32", "uint32")),
+                      ("free", ("int32", "uint32"))):
+        a.tensor("tables[%r]" % name, tables.get(name), _dt(*dts), shape=(max_ops, n_cand))
+    a.tensor("tables['n_ops']", tables.get("n_ops"), _dt("int32", "uint32"), shape=(n_cand,), optional=True)
+    a.tensor("init_live", init_live, _dt("int64", "uint64"), shape=(n_cand, int(n_dev)), optional=True)
+    a.results(results, n_cand, int(n_dev))
+    a.on_gpu()
     t = dsim_tables(_ptr(tables["code"]), _ptr(tables["flops"]), _ptr(tables["bytes"]), _ptr(tables["alloc"]),
                     _ptr(tables["free"]), _ptr(tables.get("n_ops")), _ptr(init_live), max_ops, n_dev)
     d = device_model(device)
@@ -200,14 +270,37 @@ def dsim_simulate_tables(tables, n_cand, n_dev, device, results, init_live=None,
            lib().dsim_simulate_tables(C.byref(t), n_cand, C.byref(d), C.byref(r), _stream(stream)))
 
 
-def dsim_simulate_parametric(model, cand, device, results, stream=None):
-    """cand: device int32 tensor (n, 4) of (D, H, P, K)."""
+def dsim_parametric_workspace(n_cand):
+    return int(lib().dsim_parametric_workspace(int(n_cand)))
+
+
+def alloc_parametric_workspace(n_cand, device="cuda"):
+    """A caller-owned workspace for dsim_simulate_parametric (torch uint8)."""
+    import torch
+    return torch.empty(max(dsim_parametric_workspace(n_cand), 16), dtype=torch.uint8, device=device)
+
+
+def dsim_simulate_parametric(model, cand, device, results, workspace=None, side_stream=None, stream=None):
+    """cand: device int32 tensor (n, 4) of (D, H, P, K).  workspace: a device
+    uint8 tensor of at least dsim_parametric_workspace(n) bytes (None: one
+    is allocated with torch for this call).  side_stream: a second stream
+    (torch.cuda.Stream or a raw handle) for the split launch of large
+    transformer grids, or None."""
+    a = _Args()
+    a.tensor("cand", cand, _dt("int32"), shape=(None, 4))
+    n = int(cand.shape[0])
+    a.results(results, n)
+    if workspace is None:
+        workspace = alloc_parametric_workspace(n, device=cand.device)
+    a.tensor("workspace", workspace, _dt("uint8"), numel=dsim_parametric_workspace(n))
+    a.on_gpu()
     m = model_struct(model)
     d = device_model(device)
     r = _results(results)
+    side = None if side_stream is None else getattr(side_stream, "cuda_stream", side_stream)
     _check("dsim_simulate_parametric",
-           lib().dsim_simulate_parametric(C.byref(m), _ptr(cand), int(cand.shape[0]), C.byref(d), C.byref(r),
-                                          _stream(stream)))
+           lib().dsim_simulate_parametric(C.byref(m), _ptr(cand), n, C.byref(d), C.byref(r), _ptr(workspace),
+                                          workspace.numel(), side, _stream(stream)))
 
 
 def dsim_argmin_workspace(n, k):
@@ -216,7 +309,17 @@ def dsim_argmin_workspace(n, k):
 
 def dsim_argmin(makespan, cand_peak, status, mem_cap, k, workspace, out_idx, out_makespan, out_found,
                 stream=None):
+    a = _Args()
+    a.tensor("makespan", makespan, _dt("float64"), shape=(None,))
     n = int(makespan.shape[0])
+    a.tensor("cand_peak", cand_peak, _dt("int64", "uint64"), shape=(n,))
+    a.tensor("status", status, _dt("int32"), shape=(n,))
+    k = int(k)
+    a.tensor("out_idx", out_idx, _dt("int64"), numel=k)
+    a.tensor("out_makespan", out_makespan, _dt("float64"), numel=k)
+    a.tensor("out_found", out_found, _dt("int32"), numel=1)
+    a.tensor("workspace", workspace, _dt("uint8", "int8", "int32", "int64", "float32", "float64"))
+    a.on_gpu()
     ws_bytes = workspace.numel() * workspace.element_size()
     _check("dsim_argmin",
            lib().dsim_argmin(_ptr(makespan), _ptr(cand_peak), _ptr(status), n, int(mem_cap), int(k),
@@ -225,6 +328,13 @@ def dsim_argmin(makespan, cand_peak, status, mem_cap, k, workspace, out_idx, out
 
 
 def dsim_generate_random_tables(seed, n_cand, n_ops, n_dev, tables, stream=None):
+    n_cand, n_ops = int(n_cand), int(n_ops)
+    a = _Args()
+    for name, dts in (("code", ("int32", "uint32")), ("flops", ("float32",)), ("bytes", ("float32",)),
+                      ("alloc", ("int32", "uint32")), ("free", ("int32", "uint32"))):
+        a.tensor("tables[%r]" % name, tables.get(name), _dt(*dts), shape=(n_ops, n_cand))
+    a.tensor("tables['n_ops']", tables.get("n_ops"), _dt("int32", "uint32"), shape=(n_cand,), optional=True)
+    a.on_gpu()
     _check("dsim_generate_random_tables",
            lib().dsim_generate_random_tables(seed, n_cand, n_ops, n_dev, _ptr(tables["code"]),
                                              _ptr(tables["flops"]), _ptr(tables["bytes"]),
@@ -237,6 +347,9 @@ def dsim_materialize_tables(model, cand, n_dev, max_ops, stream=None):
     (device int32 tensor of shape (n, 4)); returns the tables dict (with
     init_live, shape (n, n_dev)) and the per-candidate status tensor."""
     import torch
+    a = _Args()
+    a.tensor("cand", cand, _dt("int32"), shape=(None, 4))
+    a.on_gpu()
     n = int(cand.shape[0])
     t = alloc_tables(n, max_ops, device=cand.device)
     t["init_live"] = torch.empty((n, n_dev), dtype=torch.int64, device=cand.device)

@@ -13,8 +13,8 @@ from paper_2111_05426_amd.workloads import (ALL, DeviceSpec, GridSpec, INFER, TR
 def test_exports_every_declared_function():
     names = dsim.header_functions()
     assert set(names) == {"dsim_last_error", "dsim_create_grid", "dsim_simulate_tables",
-                          "dsim_simulate_parametric", "dsim_argmin_workspace", "dsim_argmin",
-                          "dsim_generate_random_tables", "dsim_materialize_tables"}
+                          "dsim_simulate_parametric", "dsim_parametric_workspace", "dsim_argmin_workspace",
+                          "dsim_argmin", "dsim_generate_random_tables", "dsim_materialize_tables"}
     L = dsim.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -97,12 +97,12 @@ def test_argument_errors_before_launch():
     # parametric: bad model / NULL candidates
     m = dsim.model_struct(ALL["tiny_mlp"].model)
     m.family = 7
-    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None, 0, None, None) == dsim.DSIM_EINVAL
     m = dsim.model_struct(ALL["gpt2_small"].model)
     m.d_model = 770
-    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None, 0, None, None) == dsim.DSIM_EINVAL
     m = dsim.model_struct(ALL["gpt2_small"].model)
-    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None, 0, None, None) == dsim.DSIM_EINVAL
     assert "NULL" in dsim.dsim_last_error()
     # device model: MatMul regression and network tier
     tab4 = dsim.dsim_tables()
@@ -129,11 +129,11 @@ def test_argument_errors_before_launch():
                        ("overlap", 2), ("overlap", -1)):
         m = dsim.model_struct(ALL["gpt2_small_train"].model)
         setattr(m, field, bad)
-        assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+        assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None, 0, None, None) == dsim.DSIM_EINVAL
         assert field in dsim.dsim_last_error()
     m = dsim.model_struct(ALL["gpt2_small_train"].model)
     m.overlap, m.zero = 1, 1
-    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None, 0, None, None) == dsim.DSIM_EINVAL
     assert "overlap and zero" in dsim.dsim_last_error()
     # the transform's devices per GPU must match the device model's streams
     two = dsim.device_model(DeviceSpec(streams=(2, 1e12, 1e-6)))
@@ -141,10 +141,10 @@ def test_argument_errors_before_launch():
     m = dsim.model_struct(ALL["gpt2_small_train"].model)
     for mm, d in ((0, two), (1, dev), (1, three)):
         m.overlap = mm
-        assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(d), C.byref(res), None) == dsim.DSIM_EINVAL
+        assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(d), C.byref(res), None, 0, None, None) == dsim.DSIM_EINVAL
         assert "streams_per_gpu" in dsim.dsim_last_error()
     m.overlap = 1
-    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(two), C.byref(res), None) == dsim.DSIM_EINVAL
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(two), C.byref(res), None, 0, None, None) == dsim.DSIM_EINVAL
     assert "NULL" in dsim.dsim_last_error()
     # one dispatch of the transform covers n_cand * (widest segment) lanes
     m = dsim.model_struct(ALL["gpt3_175b"].model)
@@ -152,7 +152,8 @@ def test_argument_errors_before_launch():
     res64.makespan = res64.cand_peak = res64.status = 8
     res64.row_width = 64
     fake = C.c_void_p(16)   # never dereferenced: the call fails before any launch
-    assert L.dsim_simulate_parametric(C.byref(m), fake, 1 << 27, C.byref(dev), C.byref(res64), None) == dsim.DSIM_ERANGE
+    assert L.dsim_simulate_parametric(C.byref(m), fake, 1 << 27, C.byref(dev), C.byref(res64), fake,
+                                      dsim.dsim_parametric_workspace(1 << 27), None, None) == dsim.DSIM_ERANGE
     assert "dispatch" in dsim.dsim_last_error()
     # materialiser: device count, op capacity, NULL buffers, bad model
     m = dsim.model_struct(ALL["tiny_mlp"].model)
@@ -190,7 +191,7 @@ def test_size_rule_at_both_sides_of_the_bound(orc):
     dev = dsim.device_model(DeviceSpec())
     res = dsim.dsim_results()
     m = dsim.model_struct(cases[1][0])
-    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None) == dsim.DSIM_ERANGE
+    assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None, 0, None, None) == dsim.DSIM_ERANGE
     assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_ERANGE
 
 
@@ -211,6 +212,28 @@ def test_size_rule_matches_oracle_on_random_models(orc):
             model = mlp(L, int(2 ** rng.uniform(0, 26)), B, e, mode)
         ok = orc.model_size_ok(model)
         assert (_grid_rc(model) == dsim.DSIM_OK) == ok, model
+
+
+def test_parametric_workspace_is_checked():
+    """dsim_simulate_parametric takes its grouping buffer from the caller:
+    about 4 bytes per candidate, DSIM_ENOSPC when it is missing or short
+    (checked before any launch)."""
+    L = dsim.lib()
+    assert dsim.dsim_parametric_workspace(-1) == 0
+    for n in (1, 255, 256, 257, 39965, 10 ** 6):
+        nb = (n + 255) // 256
+        assert dsim.dsim_parametric_workspace(n) == 4 * (8 * nb + 32 + n)
+    m = dsim.model_struct(ALL["gpt3_175b"].model)
+    dev = dsim.device_model(DeviceSpec())
+    res = dsim.dsim_results()
+    res.makespan = res.cand_peak = res.status = 8
+    res.row_width = 64
+    fake = C.c_void_p(16)   # never dereferenced: the calls fail before any launch
+    need = dsim.dsim_parametric_workspace(1000)
+    for ws, nbytes in ((None, need), (fake, need - 1), (fake, 0)):
+        assert L.dsim_simulate_parametric(C.byref(m), fake, 1000, C.byref(dev), C.byref(res), ws, nbytes, None,
+                                          None) == dsim.DSIM_ENOSPC
+        assert "workspace" in dsim.dsim_last_error()
 
 
 def test_struct_layouts_match_header():

@@ -30,13 +30,24 @@ def torch_gpu():
     return torch
 
 
-def run_gpu(torch, model, strat, dev, row_width=None):
+_SIDE = []
+
+
+def side_stream(torch):
+    """One second stream (default priority) for the split launch."""
+    if not _SIDE:
+        _SIDE.append(torch.cuda.Stream())
+    return _SIDE[0]
+
+
+def run_gpu(torch, model, strat, dev, row_width=None, side=True):
     from paper_2111_05426_amd import dsim
     strat = np.ascontiguousarray(strat, np.int32).reshape(-1, 4)
     rw = int(row_width or max(1, strat[:, 2].max()))
     r = dsim.alloc_results(len(strat), rw)
     cand = torch.from_numpy(strat).cuda()
-    dsim.dsim_simulate_parametric(model, cand, dev, r)
+    ws = dsim.alloc_parametric_workspace(len(strat))
+    dsim.dsim_simulate_parametric(model, cand, dev, r, workspace=ws, side_stream=side_stream(torch) if side else None)
     torch.cuda.synchronize()
     out = {k: v.cpu().numpy() for k, v in r.items() if k != "row_width"}
     out["cand"] = cand
@@ -260,6 +271,31 @@ def test_gpt3_grid_sampled(torch_gpu, orc, w):
     order = feas[np.lexsort((feas, mk_all[feas]))][:16]
     assert np.array_equal(top, order)
     assert np.array_equal(mk.cpu().numpy(), mk_all[order])
+
+
+@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_zero"], ALL["gpt3_175b_overlap"]],
+                         ids=["1f1b", "zero", "overlap"])
+def test_split_launch_on_one_stream(torch_gpu, w):
+    """The two kernels of a large transformer grid side by side (a second
+    stream) or one after the other on the caller's stream: the same results,
+    bit for bit, and a workspace reused by a second, smaller call."""
+    from paper_2111_05426_amd import dsim
+    strat = dsim.dsim_create_grid(w.model, w.grid)
+    a = run_gpu(torch_gpu, w.model, strat, w.device, 64, side=True)
+    b = run_gpu(torch_gpu, w.model, strat, w.device, 64, side=False)
+    for k in ("makespan", "finish", "peak", "cand_peak", "n_ops", "walked_ops", "status"):
+        assert np.array_equal(a[k], b[k]), k
+    # one workspace for two calls in a row, the second smaller
+    ws = dsim.alloc_parametric_workspace(len(strat))
+    sub = strat[::3]
+    for part in (strat, sub):
+        r = dsim.alloc_results(len(part), 64)
+        dsim.dsim_simulate_parametric(w.model, torch_gpu.from_numpy(np.ascontiguousarray(part)).cuda(), w.device,
+                                      r, workspace=ws, side_stream=side_stream(torch_gpu))
+        torch_gpu.cuda.synchronize()
+        ref = a if part is strat else {k: v[::3] for k, v in a.items() if isinstance(v, np.ndarray)}
+        for k in ("makespan", "cand_peak", "status"):
+            assert np.array_equal(r[k].cpu().numpy(), ref[k]), k
 
 
 def test_invalid_strategies(torch_gpu, orc):

@@ -139,6 +139,44 @@ def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, kinds):
 
 
 @pytest.mark.parametrize("n_dev", [3, 8])
+def test_tables_long_op_counts_and_large_resident_bytes(torch_gpu, orc, n_dev):
+    """Lanes whose op count exceeds max_ops are flagged (DSIM_ST_BAD_OP) and
+    simulate max_ops ops, also when another op of theirs (a broadcast or
+    reduce record, a free that would underflow) sends them to the exact
+    path; lanes starting with 2^62 or more live bytes on a device keep exact
+    integer peaks.  Against the oracle on the first max_ops ops."""
+    from paper_2111_05426_amd import dsim
+    from paper_2111_05426_amd.workloads import DeviceSpec
+    torch = torch_gpu
+    rng = np.random.default_rng(9090 + n_dev)
+    n_cand, max_ops = 520, 67
+    t = random_tables(rng, n_cand, max_ops, n_dev, bad=True, rooted=True)
+    over = rng.random(n_cand) < 0.4
+    t["n_ops"] = np.where(over, max_ops + rng.integers(1, 1000, n_cand), t["n_ops"]).astype(np.uint32)
+    big = rng.random((n_cand, n_dev)) < 0.2
+    t["init"] = np.where(big, (np.uint64(1) << np.uint64(62)) + rng.integers(0, 1 << 40, (n_cand, n_dev)).astype(
+        np.uint64), t["init"]).astype(np.uint64)
+    t["init"][0] = np.uint64((1 << 64) - (1 << 20))   # near the top of the u64 range
+    g = to_gpu(torch, t)
+    init = torch.from_numpy(t["init"].view(np.int64)).cuda()
+    dev = DeviceSpec()
+    r = dsim.alloc_results(n_cand, n_dev)
+    dsim.dsim_simulate_tables(g, n_cand, n_dev, dev, r, init_live=init)
+    torch.cuda.synchronize()
+    R = results_np(r)
+    for c in range(n_cand):
+        n = min(int(t["n_ops"][c]), max_ops)
+        o = orc.sim_table({k: t[k][:n, c] for k in ("code", "flops", "bytes", "alloc", "free")}, n_dev, dev,
+                          init_live=t["init"][c])
+        want = o["status"] | (dsim.ST_BAD_OP if t["n_ops"][c] > max_ops else 0)
+        assert R["status"][c] == want, c
+        assert_times(R["finish"][c], o["finish"])
+        assert np.array_equal(R["peak"][c].view(np.uint64), np.asarray(o["peak"], np.uint64)), c
+    assert np.all(R["n_ops"] == np.minimum(t["n_ops"], max_ops))
+    assert np.any(over & ((R["status"] & (dsim.ST_MEM_UNDERFLOW | dsim.ST_BAD_DEVICE)) != 0))
+
+
+@pytest.mark.parametrize("n_dev", [3, 8])
 def test_tables_overflowing_costs(torch_gpu, orc, n_dev):
     """Valid rates so slow that op costs and clocks overflow to +inf: both
     sides reach the same infinite (and finite) times, and no NaN appears."""
