@@ -351,6 +351,23 @@ DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsi
                                      void *side_stream, void *hip_stream);
 
 /*
+ * dsim_simulate_parametric_static -- dsim_simulate_parametric for callers
+ * that cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same simulation, results and
+ * argument checks, with the grouping workspace in a fixed buffer the
+ * library holds on each GPU it runs on (4.3 MB, kept until the process
+ * ends; its address is taken on the first call on a GPU), and every kernel
+ * on hip_stream (no second stream, no events).  The call allocates
+ * nothing.  n_cand <= 2^20 (DSIM_ERANGE beyond).  All calls on one GPU
+ * share that buffer: calls whose work overlaps on one GPU (different
+ * streams, or host threads, without ordering between them) race and give
+ * wrong results; calls ordered on one stream are safe.
+ */
+DSIM_API dsim_status dsim_simulate_parametric_static(const dsim_model *model, const dsim_strategy *cand,
+                                            int64_t n_cand, const dsim_device_model *device,
+                                            const dsim_results *results, void *hip_stream);
+
+/*
  * dsim_materialize_tables -- write the whole distributed program of each of
  * n_cand strategies (device array `cand`) of `model` -- every op of every
  * device, the transform of Sec. 4 executed with the semantics of Sec. 2.1 --

@@ -162,6 +162,29 @@ static bool strategy_ok(const dsim_model &m, int D, int H, int P, int K)
     return m.n_heads % H == 0 && m.d_model % H == 0 && m.d_ff % H == 0;
 }
 
+// arguments of the transform's simulation (both entry points)
+static dsim_status check_parametric(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
+                                    const dsim_device_model *device, const dsim_results *results)
+{
+    dsim_status st = check_model(model);
+    if (st) return st;
+    st = check_device(device);
+    if (st) return st;
+    if (model->overlap ? device->streams_per_gpu != 2 : device->streams_per_gpu > 1)
+        return fail(DSIM_EINVAL, "the transform places %s; the device model has streams_per_gpu = %d",
+                    model->overlap ? "two streams on every GPU (overlap)" : "one device on every GPU",
+                    device->streams_per_gpu);
+    if (!results) return fail(DSIM_EINVAL, "results must not be NULL");
+    if (n_cand < 0 || n_cand > ((int64_t)1 << 40)) return fail(DSIM_EINVAL, "bad n_cand");
+    if (n_cand == 0) return DSIM_OK;
+    if (!cand) return fail(DSIM_EINVAL, "candidate array must not be NULL");
+    if (!results->makespan || !results->cand_peak || !results->status)
+        return fail(DSIM_EINVAL, "makespan, cand_peak and status must not be NULL");
+    if ((results->finish || results->peak) && results->row_width < 1)
+        return fail(DSIM_ENOSPC, "row_width must be >= 1");
+    return DSIM_OK;
+}
+
 }  // namespace dsim
 
 using namespace dsim;
@@ -231,26 +254,28 @@ size_t dsim_parametric_workspace(int64_t n_cand)
     return parametric_workspace(n_cand);
 }
 
+dsim_status dsim_simulate_parametric_static(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
+                                            const dsim_device_model *device, const dsim_results *results,
+                                            void *hip_stream)
+{
+    dsim_status st = check_parametric(model, cand, n_cand, device, results);
+    if (st || n_cand == 0) return st;
+    if (n_cand > static_max_cand())
+        return fail(DSIM_ERANGE, "parametric (static): at most %lld candidates per call",
+                    (long long)static_max_cand());
+    void *ws = nullptr;
+    st = static_scratch(&ws);
+    if (st) return st;
+    return launch_parametric(*model, cand, n_cand, make_consts(*device), *results, ws, (hipStream_t)hip_stream,
+                             nullptr);
+}
+
 dsim_status dsim_simulate_parametric(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
                                      const dsim_device_model *device, const dsim_results *results,
                                      void *workspace, size_t ws_bytes, void *side_stream, void *hip_stream)
 {
-    dsim_status st = check_model(model);
-    if (st) return st;
-    st = check_device(device);
-    if (st) return st;
-    if (model->overlap ? device->streams_per_gpu != 2 : device->streams_per_gpu > 1)
-        return fail(DSIM_EINVAL, "the transform places %s; the device model has streams_per_gpu = %d",
-                    model->overlap ? "two streams on every GPU (overlap)" : "one device on every GPU",
-                    device->streams_per_gpu);
-    if (!results) return fail(DSIM_EINVAL, "results must not be NULL");
-    if (n_cand < 0 || n_cand > ((int64_t)1 << 40)) return fail(DSIM_EINVAL, "bad n_cand");
-    if (n_cand == 0) return DSIM_OK;
-    if (!cand) return fail(DSIM_EINVAL, "candidate array must not be NULL");
-    if (!results->makespan || !results->cand_peak || !results->status)
-        return fail(DSIM_EINVAL, "makespan, cand_peak and status must not be NULL");
-    if ((results->finish || results->peak) && results->row_width < 1)
-        return fail(DSIM_ENOSPC, "row_width must be >= 1");
+    dsim_status st = check_parametric(model, cand, n_cand, device, results);
+    if (st || n_cand == 0) return st;
     if (!workspace || ws_bytes < parametric_workspace(n_cand))
         return fail(DSIM_ENOSPC, "workspace needs %zu bytes", parametric_workspace(n_cand));
     return launch_parametric(*model, cand, n_cand, make_consts(*device), *results, workspace,

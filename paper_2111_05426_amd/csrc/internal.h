@@ -66,6 +66,11 @@ dsim_status launch_argmin(const double *mk, const uint64_t *pk, const int32_t *s
                           uint64_t cap, int32_t k, void *ws, int64_t *out_idx, double *out_mk,
                           int32_t *out_found, hipStream_t s);
 size_t parametric_workspace(int64_t n_cand);
+// the fixed scratch of dsim_simulate_parametric_static on the current GPU
+// (its address taken once per GPU) and the candidates it holds
+constexpr int kMaxGpus = 64;
+dsim_status static_scratch(void **out);
+int64_t static_max_cand();
 dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand,
                               const CostConsts &c, const dsim_results &r, void *ws, hipStream_t s,
                               hipStream_t side);

@@ -41,6 +41,7 @@
 // A counting-sort pre-pass groups the candidates by segment width into a
 // temporary permutation (stable, so the grid's own order keeps wavefronts
 // uniform in K).
+#include <mutex>
 #include <type_traits>
 
 #include "model.h"
@@ -1487,6 +1488,35 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strateg
 }
 
 }  // namespace
+
+// Scratch of dsim_simulate_parametric_static: the grouping workspace of at
+// most kStaticMaxCand candidates, one copy per GPU for the whole process.
+// Host code never uses this name as an address; it takes the device address
+// once per GPU (static_scratch).
+constexpr int64_t kStaticMaxCand = (int64_t)1 << 20;
+constexpr int64_t kStaticWords = (kStaticMaxCand / kScanBlock) * 8 + 32 + kStaticMaxCand;
+static __device__ __align__(256) uint32_t scratch[kStaticWords];
+
+dsim_status static_scratch(void **out)
+{
+    static std::mutex mu;
+    static void *addr[kMaxGpus] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "parametric (static): current device");
+    if (dev < 0 || dev >= kMaxGpus) return fail(DSIM_ERANGE, "parametric (static): device %d beyond %d", dev, kMaxGpus);
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail(e, "parametric (static): scratch address");
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return DSIM_OK;
+}
+
+int64_t static_max_cand() { return kStaticMaxCand; }
 
 size_t parametric_workspace(int64_t n_cand)
 {

@@ -84,6 +84,9 @@ def lib():
         L.dsim_simulate_parametric.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64,
                                                C.POINTER(dsim_device_model), C.POINTER(dsim_results),
                                                C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p]
+        L.dsim_simulate_parametric_static.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64,
+                                                      C.POINTER(dsim_device_model), C.POINTER(dsim_results),
+                                                      C.c_void_p]
         L.dsim_argmin_workspace.restype = C.c_size_t
         L.dsim_argmin_workspace.argtypes = [C.c_int64, C.c_int32]
         L.dsim_argmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_uint64, C.c_int32,
@@ -92,7 +95,8 @@ def lib():
             [C.c_void_p] * 7
         L.dsim_materialize_tables.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64, C.c_int32,
                                               C.c_int32] + [C.c_void_p] * 9
-        for name in ("dsim_create_grid", "dsim_simulate_tables", "dsim_simulate_parametric", "dsim_argmin",
+        for name in ("dsim_create_grid", "dsim_simulate_tables", "dsim_simulate_parametric",
+                     "dsim_simulate_parametric_static", "dsim_argmin",
                      "dsim_generate_random_tables", "dsim_materialize_tables"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -301,6 +305,21 @@ def dsim_simulate_parametric(model, cand, device, results, workspace=None, side_
     _check("dsim_simulate_parametric",
            lib().dsim_simulate_parametric(C.byref(m), _ptr(cand), n, C.byref(d), C.byref(r), _ptr(workspace),
                                           workspace.numel(), side, _stream(stream)))
+
+
+def dsim_simulate_parametric_static(model, cand, device, results, stream=None):
+    """dsim_simulate_parametric with the library's fixed scratch (no
+    allocation; at most 2^20 candidates; calls overlapping on one GPU race)."""
+    a = _Args()
+    a.tensor("cand", cand, _dt("int32"), shape=(None, 4))
+    n = int(cand.shape[0])
+    a.results(results, n)
+    a.on_gpu()
+    m = model_struct(model)
+    d = device_model(device)
+    r = _results(results)
+    _check("dsim_simulate_parametric_static",
+           lib().dsim_simulate_parametric_static(C.byref(m), _ptr(cand), n, C.byref(d), C.byref(r), _stream(stream)))
 
 
 def dsim_argmin_workspace(n, k):
