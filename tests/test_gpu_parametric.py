@@ -8,6 +8,7 @@ sample of the GPT-3-shaped grid.  Bar: status, op counts and peak bytes
 bit-exact; times within 1e-12 relative and expected bit-identical.
 """
 import math
+import os
 from dataclasses import replace
 
 import numpy as np
@@ -232,45 +233,106 @@ def test_workload_grid_vs_oracle(torch_gpu, orc, w):
     assert int(found.item()) == rf and np.array_equal(idx.cpu().numpy(), ri)
 
 
-@pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_recompute"], ALL["gpt3_175b_zero"], ALL["gpt3_175b_mi355x"],
-                               ALL["gpt3_175b_overlap"], ALL["gpt3_175b_mi355x_overlap"]],
-                         ids=["1f1b", "recompute", "zero", "mi355x_calibrated", "overlap", "mi355x_overlap"])
-def test_gpt3_grid_sampled(torch_gpu, orc, w):
-    """The GPT-3-shaped grid at full size (39,965 strategies, the launch
-    configuration the benchmark times, the 288e9-byte cap, top-16): a seeded
-    sample plus the selected top-16 and the extreme microbatch counts are
-    compared one by one with the oracle."""
-    from paper_2111_05426_amd import dsim
-    strat = dsim.dsim_create_grid(w.model, w.grid)
-    assert len(strat) == 39965
-    print("%s: simulating %d candidates" % (w.name, len(strat)), flush=True)
-    g = run_gpu(torch_gpu, w.model, strat, w.device, 64)
-    idx, mk, found = dsim.select_topk(g["gpu"]["makespan"], g["gpu"]["cand_peak"], g["gpu"]["status"],
-                                      w.device.mem_cap_bytes, w.top_k)
-    torch_gpu.cuda.synchronize()
-    top = idx.cpu().numpy()
-    assert int(found.item()) == 16
-    rng = np.random.default_rng(175)
+# The GPT-3-shaped grids at full size (39,965 strategies each, the launch
+# configuration the benchmark times: results row 64, a second stream, the
+# 288e9-byte cap, top-16).  The plain 1F1B grid is compared with the oracle's
+# projection on every strategy; each variant on every STRIDE-th strategy of
+# the grid plus its top-16 and the extreme microbatch counts (the ZeRO oracle
+# walks every data replica, hence its longer stride).
+GPT3_GRIDS = {"1f1b": (GPT3_175B, 1), "gpipe": (ALL["gpt3_175b_gpipe"], 8),
+              "recompute": (ALL["gpt3_175b_recompute"], 8), "zero": (ALL["gpt3_175b_zero"], 32),
+              "overlap": (ALL["gpt3_175b_overlap"], 8), "mi355x_calibrated": (ALL["gpt3_175b_mi355x"], 8),
+              "mi355x_overlap": (ALL["gpt3_175b_mi355x_overlap"], 8)}
+GPT3_CHUNKS = 8
+THREADS = max(1, min(16, os.cpu_count() or 1))
+# full-program oracle on every sampled strategy whose program has at most
+# 10^7 ops
+FULL_MAX_OPS = 10_000_000
+
+
+@pytest.fixture(scope="module")
+def gpt3_runs():
+    return {}
+
+
+def gpt3_run(torch, cache, key):
+    if key not in cache:
+        from paper_2111_05426_amd import dsim
+        w = GPT3_GRIDS[key][0]
+        strat = dsim.dsim_create_grid(w.model, w.grid)
+        assert len(strat) == 39965
+        print("%s: simulating %d candidates" % (w.name, len(strat)), flush=True)
+        g = run_gpu(torch, w.model, strat, w.device, 64)
+        idx, mk, found = dsim.select_topk(g["gpu"]["makespan"], g["gpu"]["cand_peak"], g["gpu"]["status"],
+                                          w.device.mem_cap_bytes, w.top_k)
+        torch.cuda.synchronize()
+        g = {k: v for k, v in g.items() if isinstance(v, np.ndarray)}
+        cache[key] = (w, strat, g, (idx.cpu().numpy(), mk.cpu().numpy(), int(found.item())))
+    return cache[key]
+
+
+def sub(g, pick):
+    return {k: v[pick] for k, v in g.items()}
+
+
+@pytest.mark.parametrize("chunk", range(GPT3_CHUNKS))
+def test_gpt3_grid_every_strategy(torch_gpu, orc, gpt3_runs, chunk):
+    """Every strategy of the GPT-3-shaped 1F1B grid against the oracle's
+    projection (an eighth of the grid per test)."""
+    w, strat, g, _ = gpt3_run(torch_gpu, gpt3_runs, "1f1b")
+    lo, hi = chunk * len(strat) // GPT3_CHUNKS, (chunk + 1) * len(strat) // GPT3_CHUNKS
+    print("oracle on strategies %d..%d (%d threads)" % (lo, hi, THREADS), flush=True)
+    o = orc.run_strategies(w.model, strat[lo:hi], w.device, slice=True, row_width=64, threads=THREADS)
+    compare(sub(g, slice(lo, hi)), o, strat[lo:hi])
+
+
+def variant_pick(strat, top, stride):
     K = strat[:, 3]
-    # the ZeRO oracle walks every data replica, so it samples fewer
-    n_pick = 100 if w.model.zero else 250
-    pick = np.unique(np.concatenate([rng.choice(len(strat), n_pick, replace=False), top,
+    return np.unique(np.concatenate([np.arange(0, len(strat), stride), top[top >= 0],
                                      np.nonzero(K == K.max())[0][:5], np.nonzero(K == 1)[0][:5]]))
-    print("%s: oracle on %d sampled candidates" % (w.name, len(pick)), flush=True)
-    o = orc.run_strategies(w.model, strat[pick], w.device, slice=True, row_width=64, threads=8)
-    sub = {k: (v[pick] if isinstance(v, np.ndarray) else v) for k, v in g.items()}
-    compare(sub, o, strat[pick])
-    # the projection itself against the full program, where that is small
-    small = pick[np.nonzero(o["n_ops"] <= 300_000)[0]][:24]
-    assert len(small) >= 5
-    of = orc.run_strategies(w.model, strat[small], w.device, slice=False, row_width=64, threads=8)
-    compare({k: (v[small] if isinstance(v, np.ndarray) else v) for k, v in g.items()}, of, strat[small])
-    # the selection is the ordered prefix of the feasible candidates
+
+
+@pytest.mark.parametrize("key", [k for k in GPT3_GRIDS if k != "1f1b"])
+def test_gpt3_variant_strided(torch_gpu, orc, gpt3_runs, key):
+    w, strat, g, (top, _, _) = gpt3_run(torch_gpu, gpt3_runs, key)
+    pick = variant_pick(strat, top, GPT3_GRIDS[key][1])
+    print("%s: oracle on %d strategies (every %d-th, the top-16, extreme K)" % (w.name, len(pick),
+                                                                              GPT3_GRIDS[key][1]), flush=True)
+    o = orc.run_strategies(w.model, strat[pick], w.device, slice=True, row_width=64, threads=THREADS)
+    compare(sub(g, pick), o, strat[pick])
+
+
+@pytest.mark.parametrize("key", list(GPT3_GRIDS))
+def test_gpt3_grid_full_program(torch_gpu, orc, gpt3_runs, key):
+    """The projection itself against the oracle's whole program (every
+    device of every replica) on a seeded sample of 250 strategies (100 for
+    ZeRO) plus the top-16: every one whose program has at most 10^7 ops."""
+    w, strat, g, (top, _, _) = gpt3_run(torch_gpu, gpt3_runs, key)
+    rng = np.random.default_rng(175)
+    pick = np.unique(np.concatenate([rng.choice(len(strat), 100 if w.model.zero else 250, replace=False),
+                                     top[top >= 0]]))
+    lim = FULL_MAX_OPS
+    small = pick[g["n_ops"][pick] <= lim]
+    print("%s: whole program on %d of %d sampled strategies (<= %d ops, %.3g ops in all)"
+          % (w.name, len(small), len(pick), lim, g["n_ops"][small].sum()), flush=True)
+    assert len(small) >= 20
+    of = orc.run_strategies(w.model, strat[small], w.device, slice=False, row_width=64, threads=THREADS)
+    compare(sub(g, small), of, strat[small])
+
+
+@pytest.mark.parametrize("key", list(GPT3_GRIDS))
+def test_gpt3_grid_selection(torch_gpu, gpt3_runs, key):
+    """The top-16 is the ordered prefix of the feasible strategies (status 0,
+    peak within 288e9 bytes), ties to the lower index."""
+    w, strat, g, (top, mk, found) = gpt3_run(torch_gpu, gpt3_runs, key)
     mk_all, st, cp = g["makespan"], g["status"], g["cand_peak"].view(np.uint64)
     feas = np.nonzero((st == 0) & (cp <= w.device.mem_cap_bytes))[0]
     order = feas[np.lexsort((feas, mk_all[feas]))][:16]
-    assert np.array_equal(top, order)
-    assert np.array_equal(mk.cpu().numpy(), mk_all[order])
+    assert found == len(order) and np.array_equal(top[:found], order)
+    assert np.array_equal(mk[:found], mk_all[order])
+    assert np.all(top[found:] == -1)
+    if key != "gpipe":   # no GPipe strategy fits 288e9 bytes
+        assert found == 16
 
 
 @pytest.mark.parametrize("w", [GPT3_175B, ALL["gpt3_175b_zero"], ALL["gpt3_175b_overlap"]],

@@ -6,6 +6,7 @@ bit-exact; fp64 times within 1e-12 relative (both sides evaluate the same
 IEEE expressions in the same order with contraction off, so they are
 expected to be equal bit for bit, and the tests also record that).
 """
+import os
 from dataclasses import replace
 
 import numpy as np
@@ -300,44 +301,70 @@ def test_generated_tables_simulate_vs_oracle(torch_gpu, orc):
     assert np.all(R["status"] == 0)
 
 
-def test_random_tables_full_size_sampled(torch_gpu, orc):
+FULL_CHUNKS = 4
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+@pytest.fixture(scope="module")
+def full_size_tables(torch_gpu):
     """The measured workload at its full size, in the launch configuration the
-    benchmark times: 1,000,000 candidates x 2,048 ops x 8 devices.  Sampled
-    candidates are checked one by one; the top-1 over all of them is checked
-    against the oracle's top-1 over the same simulated values' ordering."""
+    benchmark times (1,000,000 candidates x 2,048 ops x 8 devices, generated
+    on the GPU), simulated once; the results come back to the host."""
     from paper_2111_05426_amd import dsim
     from paper_2111_05426_amd.workloads import RANDOM_TABLES
     torch = torch_gpu
     spec = RANDOM_TABLES.tables
-    dev = RANDOM_TABLES.device
     print("full-size random tables: generating", flush=True)
     g = gen_gpu(torch, spec.seed, spec.n_cand, spec.n_ops, spec.n_dev)
     r = dsim.alloc_results(spec.n_cand, spec.n_dev)
-    dsim.dsim_simulate_tables(g, spec.n_cand, spec.n_dev, dev, r)
+    dsim.dsim_simulate_tables(g, spec.n_cand, spec.n_dev, RANDOM_TABLES.device, r)
     idx, mk, found = dsim.select_topk(r["makespan"], r["cand_peak"], r["status"], 0, 4)
     torch.cuda.synchronize()
     print("full-size random tables: simulated", flush=True)
     rng = np.random.default_rng(5)
-    sample = np.unique(np.concatenate([rng.integers(0, spec.n_cand, 1500), [0, spec.n_cand - 1],
-                                       idx.cpu().numpy()]))
-    s_t = torch.from_numpy(sample).cuda()
-    o = orc.run_random_tables(spec.seed, spec.n_ops, spec.n_dev, sample, dev, threads=8)
-    assert_times(r["makespan"][s_t].cpu().numpy(), o["makespan"])
-    assert_times(r["finish"][s_t].cpu().numpy(), o["finish"])
-    assert np.array_equal(r["peak"][s_t].cpu().numpy().view(np.uint64), o["peak"])
-    assert np.array_equal(r["status"][s_t].cpu().numpy(), o["status"])
-    # generator: sampled columns bit-exact
-    for c in sample[:40]:
+    cols = np.unique(np.concatenate([rng.integers(0, spec.n_cand, 40), [0, spec.n_cand - 1]]))
+    gen = {c: {k: g[k][:, int(c)].cpu().numpy() for k in ("code", "flops", "bytes", "alloc", "free")} for c in cols}
+    out = dict(spec=spec, dev=RANDOM_TABLES.device, res=results_np(r), gen=gen,
+               top=(idx.cpu().numpy(), mk.cpu().numpy(), int(found.item())))
+    del g, r
+    torch.cuda.empty_cache()
+    return out
+
+
+@pytest.mark.parametrize("chunk", range(FULL_CHUNKS))
+def test_random_tables_full_size_every_candidate(orc, full_size_tables, chunk):
+    """Every candidate of the full-size workload against the oracle, element
+    by element (a quarter of the million per test)."""
+    F = full_size_tables
+    spec, R = F["spec"], F["res"]
+    lo, hi = chunk * spec.n_cand // FULL_CHUNKS, (chunk + 1) * spec.n_cand // FULL_CHUNKS
+    print("oracle on candidates %d..%d (%d threads)" % (lo, hi, THREADS), flush=True)
+    o = orc.run_random_tables(spec.seed, spec.n_ops, spec.n_dev, np.arange(lo, hi), F["dev"], threads=THREADS)
+    assert_times(R["makespan"][lo:hi], o["makespan"])
+    assert_times(R["finish"][lo:hi], o["finish"])
+    assert np.array_equal(R["peak"][lo:hi].view(np.uint64), o["peak"])
+    assert np.array_equal(R["cand_peak"][lo:hi].view(np.uint64), o["cand_peak"])
+    assert np.array_equal(R["status"][lo:hi], o["status"])
+    assert np.array_equal(R["n_ops"][lo:hi].astype(np.uint64), o["n_ops"])
+
+
+def test_random_tables_full_size_generator_and_selection(orc, full_size_tables):
+    """Sampled generated columns bit for bit, and the top-4 over the million
+    equal to the ordered prefix of the simulated values."""
+    F = full_size_tables
+    spec, R = F["spec"], F["res"]
+    for c, cols in F["gen"].items():
         ref = orc.gen_table(spec.seed, int(c), spec.n_ops, spec.n_dev)
-        assert np.array_equal(g["code"][:, int(c)].cpu().numpy().view(np.uint32), ref["code"])
-        assert np.array_equal(g["bytes"][:, int(c)].cpu().numpy().view(np.uint32), ref["bytes"].view(np.uint32))
-        assert np.array_equal(g["alloc"][:, int(c)].cpu().numpy().view(np.uint32), ref["alloc"])
-    # selection over the million: ranks are consistent with the simulated values
-    mk_all = r["makespan"].cpu().numpy()
-    order = np.lexsort((np.arange(spec.n_cand), mk_all))[:4]
-    assert int(found.item()) == 4
-    assert np.array_equal(idx.cpu().numpy(), order)
-    assert_times(mk.cpu().numpy(), mk_all[order])
+        for k in ("code", "alloc", "free"):
+            assert np.array_equal(cols[k].view(np.uint32), ref[k]), (c, k)
+        for k in ("flops", "bytes"):
+            assert np.array_equal(cols[k].view(np.uint32), ref[k].view(np.uint32)), (c, k)
+    idx, mk, found = F["top"]
+    order = np.lexsort((np.arange(spec.n_cand), R["makespan"]))[:4]
+    assert found == 4 and np.array_equal(idx, order)
+    assert_times(mk, R["makespan"][order])
+    ri, rm, rf = orc.topk(R["makespan"], R["cand_peak"].view(np.uint64), R["status"], 0, 4)
+    assert rf == 4 and np.array_equal(ri, idx)
 
 
 @pytest.mark.parametrize("n", [0, 1, 255, 4097, 100_003, 1_000_000])
