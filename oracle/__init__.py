@@ -219,7 +219,7 @@ def sim_strategy(model, D, H, P, K, dev, slice=False, type_cost=None, want_devic
     df = np.zeros(n_dev, np.float64) if want_devices else None
     dp = np.zeros(n_dev, np.uint64) if want_devices else None
     dr = np.zeros(n_dev, np.uint64) if want_devices else None
-    fbt = np.zeros(N_TYPES, np.float64)
+    fbt = np.zeros(2 * N_TYPES, np.float64)
     tc = None
     if type_cost is not None:
         tc = np.full(N_TYPES, -1.0)
@@ -241,7 +241,8 @@ def sim_strategy(model, D, H, P, K, dev, slice=False, type_cost=None, want_devic
         raise ValueError("or_sim_strategy failed: %d" % rc)
     return dict(makespan=mk.value, cand_peak=cp.value, n_ops=no.value, status=st.value,
                 stage_finish=sf, stage_peak=sp, dev_finish=df, dev_peak=dp, dev_resident=dr,
-                flops_by_type={TYPES[i]: fbt[i] for i in range(N_TYPES)})
+                flops_by_type={TYPES[i]: fbt[i] for i in range(N_TYPES)},
+                bytes_by_type={TYPES[i]: fbt[N_TYPES + i] for i in range(N_TYPES)})
 
 
 def model_size_ok(model):

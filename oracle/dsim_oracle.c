@@ -1672,7 +1672,7 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
                         const or_device_model *dm, int slice, const double *type_cost,
                         double *stage_finish, uint64_t *stage_peak,
                         double *dev_finish, uint64_t *dev_peak, uint64_t *dev_resident,
-                        double *flops_by_type, or_result *res)
+                        double *by_type, or_result *res)
 {
     mat x;
     or_prog g;
@@ -1840,10 +1840,15 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     }
     if (x.train) for (s = 0; s < P; s++) emit_wu(&x, s);
     if (g.failed) { rc = -3; goto out; }
-    if (flops_by_type) {
+    if (by_type) {
+        /* per-type totals of the materialised ops: flops at [type], bytes
+         * at [T_NTYPES + type] */
         int64_t i;
-        for (i = 0; i < T_NTYPES; i++) flops_by_type[i] = 0.0;
-        for (i = 0; i < g.n_ops; i++) flops_by_type[g.type[i]] += g.flops[i];
+        for (i = 0; i < 2 * T_NTYPES; i++) by_type[i] = 0.0;
+        for (i = 0; i < g.n_ops; i++) {
+            by_type[g.type[i]] += g.flops[i];
+            by_type[T_NTYPES + g.type[i]] += g.bytes[i];
+        }
     }
     rc = prog_simulate(&g, n_dev, dm, type_cost, fin, pk, dev_resident, NULL, NULL);
     if (rc) goto out;
@@ -1883,12 +1888,12 @@ int or_sim_strategy(const or_model *M, int D, int H, int P, int K,
                     const or_device_model *dm, int slice, const double *type_cost,
                     double *stage_finish, uint64_t *stage_peak,
                     double *dev_finish, uint64_t *dev_peak, uint64_t *dev_resident,
-                    double *flops_by_type,
+                    double *by_type,
                     double *makespan, uint64_t *cand_peak, uint64_t *n_ops, int32_t *status)
 {
     or_result res;
     int rc = sim_strategy(M, D, H, P, K, dm, slice, type_cost, stage_finish, stage_peak,
-                          dev_finish, dev_peak, dev_resident, flops_by_type, &res);
+                          dev_finish, dev_peak, dev_resident, by_type, &res);
     *makespan = res.makespan;
     *cand_peak = res.cand_peak;
     *n_ops = res.n_ops;

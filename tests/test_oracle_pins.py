@@ -169,6 +169,138 @@ def test_table1_mlp_model_size(orc, name):
 # ---------------------------------------------------------------------------
 # Pipeline closed forms (Sec. 4: uniform stages, synchronous 1F1B)
 # ---------------------------------------------------------------------------
+# Slot order at P = 3, K = 4 by hand (Sec. 4's synchronous 1F1B; the
+# global order is this project's reading, as no listing covers P >= 3).
+# Stage s runs min(P-1-s, K) warm-up forwards, then backward/forward pairs,
+# then the remaining backwards.  In slot t each stage, ascending, runs its
+# next block if the block's input came from an earlier slot; then the slot's
+# Sends run ascending by source stage.  Worked out slot by slot:
+#   t0  s0 F0                      sends 0>1 F0
+#   t1  s0 F1  s1 F0               sends 0>1 F1, 1>2 F0
+#   t2  s0 F2  s1 F1  s2 F0        sends 0>1 F2, 1>2 F1
+#   t3                s2 B0        sends 2>1 B0
+#   t4         s1 B0  s2 F1        sends 1>0 B0
+#   t5  s0 B0  s1 F2  s2 B1        sends 1>2 F2, 2>1 B1
+#   t6  s0 F3  s1 B1  s2 F2        sends 0>1 F3, 1>0 B1
+#   t7  s0 B1  s1 F3  s2 B2        sends 1>2 F3, 2>1 B2
+#   t8         s1 B2  s2 F3        sends 1>0 B2
+#   t9  s0 B2         s2 B3        sends 2>1 B3
+#   t10        s1 B3               sends 1>0 B3
+#   t11 s0 B3
+# then each stage's weight update.  Each device's projection (splits first
+# on stages 0 and 2):
+P3K4 = {0: "SPLIT F0 s01 F1 s01 F2 s01 r10 B0 F3 s01 r10 B1 r10 B2 r10 B3 OPT",
+        1: "r01 F0 r01 s12 F1 r01 s12 r21 B0 s10 F2 s12 r21 B1 r01 s10 F3 s12 r21 B2 s10 r21 B3 s10 OPT",
+        2: "SPLIT r12 F0 r12 B0 s21 F1 B1 r12 s21 F2 B2 r12 s21 F3 B3 s21 OPT"}
+P3K4_COST = dict(SPLIT=0.0625, GEMM=3.0, RELU=0.5, LOSSGRAD=0.25, RELUGRAD=0.75, GEMMDW=2.0, GEMMDX=2.5,
+                 ADDGRAD=0.125, SEND_F=1.5, SEND_B=1.25, OPT=0.375, AR_TP=0.0, AR_DP=0.0)
+
+
+def p3k4_costs():
+    """The durations above, and 24 seeded sets of other dyadic durations per
+    op type (a different projection would change some finish time)."""
+    rng = random.Random(34)
+    out = [P3K4_COST]
+    for _ in range(24):
+        out.append({k: (rng.randrange(1, 256) / 64.0 if v else 0.0) for k, v in P3K4_COST.items()})
+    return out
+
+
+@pytest.mark.parametrize("ci", range(25))
+def test_1f1b_slot_order_p3_k4_by_hand(orc, ci):
+    """A 3-layer MLP on three stages with four microbatches and a different
+    duration per op type: each device's finish time from the projections
+    above (blocking Sends meet both devices' clocks) equals the oracle's."""
+    c = p3k4_costs()[ci]
+
+    def block(tok, stage):
+        if tok[0] == "F":
+            return [c["GEMM"], c["RELU"]]
+        k = int(tok[1])
+        ops = [c["LOSSGRAD"]] if stage == 2 else []
+        return ops + [c["RELUGRAD"], c["GEMMDW"]] + ([c["ADDGRAD"]] if k >= 1 else []) + [c["GEMMDX"]]
+
+    seq = {}
+    for dev, text in P3K4.items():
+        ops = []
+        for tok in text.split():
+            if tok in ("SPLIT", "OPT"):
+                ops.append(("op", c[tok]))
+            elif tok[0] in "FB":
+                ops += [("op", v) for v in block(tok, dev)]
+            else:   # s01 sends 0 -> 1, r01 receives it (one op of both devices)
+                a, b = int(tok[1]), int(tok[2])
+                ops.append(("send", (a, b), c["SEND_F"] if b > a else c["SEND_B"]))
+        seq[dev] = ops
+    clk, pos = [0.0] * 3, [0] * 3
+    while any(pos[d] < len(seq[d]) for d in seq):
+        moved = False
+        for d in seq:
+            while pos[d] < len(seq[d]) and seq[d][pos[d]][0] == "op":
+                clk[d] += seq[d][pos[d]][1]
+                pos[d] += 1
+                moved = True
+            if pos[d] < len(seq[d]):
+                _, (a, b), cost = seq[d][pos[d]]
+                o = b if d == a else a
+                if pos[o] < len(seq[o]) and seq[o][pos[o]][0] == "send" and seq[o][pos[o]][1] == (a, b):
+                    end = max(clk[a], clk[b]) + cost
+                    clk[a] = clk[b] = end
+                    pos[a] += 1
+                    pos[b] += 1
+                    moved = True
+        assert moved, "the hand-written projections deadlock"
+    r = orc.sim_strategy(mlp(3, 64, 64, 4, TRAIN_SGD), 1, 1, 3, 4, DEV, type_cost=c)
+    assert list(r["dev_finish"]) == clk
+    assert r["makespan"] == max(clk)
+
+
+def test_1f1b_slot_order_p3_k4_memory_by_hand(orc):
+    """The same projections, memory by hand from def/use (Sec. 3.3) in units
+    of one microbatch activation a = e*m*d and one weight w = e*d^2 (fp32
+    SGD, one layer per stage, m = B/4 rows): each device's peak."""
+    e, d, B, K = 4, 64, 64, 4
+    a, w = e * (B // K) * d, e * d * d
+    peaks = []
+    for dev, text in P3K4.items():
+        live = w + (K * a if dev in (0, 2) else 0)   # the weight; x (stage 0) or y (stage 2) rows
+        peak = live
+        k = {"F": 0, "B": 0}
+
+        def step(alloc, free):
+            nonlocal live, peak
+            live += alloc
+            peak = max(peak, live)
+            live -= free
+
+        for tok in text.split():
+            if tok == "SPLIT":
+                step(K * a, K * a)                   # the microbatch pieces; the whole input dies
+            elif tok == "OPT":
+                step(0, w)                           # SGD in place; the accumulated gradient dies
+            elif tok[0] == "F":                      # Gemm (its input stays: dW reads it), Relu
+                step(a, 0)
+                step(a, a)
+            elif tok[0] == "B":
+                kk = int(tok[1])
+                if dev == 2:
+                    step(a, a)                       # loss gradient; the targets y_k die
+                step(a, 2 * a)                       # ReluGrad: the incoming gradient and the Relu output die
+                step(w, a)                           # weight gradient: the stage input dies
+                if kk >= 1:
+                    step(0, w)                       # accumulated into microbatch 0's gradient
+                step(a, a if dev else 2 * a)         # input gradient: dh dies (stage 0: its dX too)
+            elif tok[0] == "s":
+                # sender: forward activations stay (the Relu mask), backward
+                # gradients die
+                step(0, a if int(tok[2]) < int(tok[1]) else 0)
+            else:
+                step(a, 0)                           # receiver allocates the message
+        peaks.append(peak)
+    r = orc.sim_strategy(mlp(3, d, B, e, TRAIN_SGD), 1, 1, 3, K, DEV)
+    assert [int(p) for p in r["dev_peak"]] == peaks
+
+
 @pytest.mark.parametrize("P", [1, 2, 3, 4, 8])
 @pytest.mark.parametrize("K", [1, 2, 3, 5, 8, 16])
 def test_1f1b_uniform_stages(orc, P, K):
