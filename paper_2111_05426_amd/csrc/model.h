@@ -95,7 +95,8 @@ __device__ inline bool strategy_ok(const dsim_model &m, int D, int H, int P, int
     return m.n_heads % H == 0 && m.d_model % H == 0 && m.d_ff % H == 0;
 }
 
-__device__ inline void make_ctx(const dsim_model &M, const CostConsts &c, const dsim_strategy &st, Ctx &x)
+template <class CC>
+__device__ inline void make_ctx(const dsim_model &M, const CC &c, const dsim_strategy &st, Ctx &x)
 {
     x.D = st.D;
     x.H = st.H;

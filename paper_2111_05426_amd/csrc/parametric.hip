@@ -100,6 +100,19 @@ static_assert(shape_nested<Shape<true, false>>() && shape_nested<Shape<false, fa
                   shape_nested<Shape<true, true>>() && shape_nested<Shape<false, true>>(),
               "forward regions must fit the backward ones");
 
+// the device-model constants the transform reads (the table format's
+// per-group-size rows stay out of the kernel arguments)
+struct ParConsts {
+    double inv_f, inv_b, inv_l, lat, launch;
+    uint64_t cap;
+    int32_t mm;
+    double mm_c0, mm_c1, mm_c2;
+    int32_t node;
+    double net_lat, net_inv_l;
+    int32_t streams;
+    double st_lat, st_inv_l;
+};
+
 struct ParArgs {
     dsim_model m;
     const dsim_strategy *cand;
@@ -116,7 +129,7 @@ struct ParArgs {
     uint64_t *n_ops;
     uint64_t *walked;
     int32_t *status;
-    CostConsts c;
+    ParConsts c;
 };
 
 __device__ __forceinline__ int seg_class(const dsim_strategy &st, int p_bound)
@@ -606,8 +619,13 @@ __device__ __forceinline__ int64_t run_top(const ZSeg &g, int d, int D)
 template <bool TF>
 __device__ int64_t zero_top(const Ctx &x, int s, const ZStage &z, bool bwd, uint64_t m, bool acc, int n, int n_r)
 {
-    ZSeg seg[5];
-    int ns = 0;
+    // five fixed slots (pre edge, first / replayed unit, the replay's partial
+    // unit, the units, suf edge); absent ones hold no unit (n = 0).  Every
+    // index below is a constant, so the list stays in registers.
+    constexpr int kSeg = 5;
+    ZSeg seg[kSeg];
+#pragma unroll
+    for (int i = 0; i < kSeg; ++i) seg[i] = ZSeg{0, 0, 0, 0, -1, 1};
     MemZ pre{x, 0, 0, 0, 0}, suf{x, 0, 0, 0, 0};
     record_edges<TF>(x, s, bwd, m, acc, pre, suf);
     int g_pre = -1, g_suf = -1;
@@ -618,35 +636,36 @@ __device__ int64_t zero_top(const Ctx &x, int s, const ZStage &z, bool bwd, uint
     } else if (bwd) {
         g_suf = z.gl_lo;   // the stage's first unit
     }
-    seg[ns++] = ZSeg{1, pre.cur, pre.tn, pre.to, g_pre, 1};
+    seg[0] = ZSeg{1, pre.cur, pre.tn, pre.to, g_pre, 1};
     if (!bwd) {
         MemZ u{x, 0, 0, 0, 0};
         record_unit<TF>(x, false, m, false, u);
         if (x.rc && n >= 1) {
             MemZ f{x, 0, 0, 0, 0};
             record_unit<TF>(x, false, m, false, f, kFwdFirst);
-            seg[ns++] = ZSeg{1, f.cur, f.tn, f.to, z.gl_lo, 1};
-            seg[ns++] = ZSeg{n - 1, u.cur, u.tn, u.to, z.gl_lo + 1, 1};
+            seg[1] = ZSeg{1, f.cur, f.tn, f.to, z.gl_lo, 1};
+            seg[3] = ZSeg{n - 1, u.cur, u.tn, u.to, z.gl_lo + 1, 1};
         } else {
-            seg[ns++] = ZSeg{n, u.cur, u.tn, u.to, z.gl_lo, 1};
+            seg[3] = ZSeg{n, u.cur, u.tn, u.to, z.gl_lo, 1};
         }
     } else {
         if (x.rc) {
             MemZ u{x, 0, 0, 0, 0}, q{x, 0, 0, 0, 0};
             record_unit<TF>(x, false, m, false, u, kFwdReplay);
             record_partial<TF>(x, m, q);
-            seg[ns++] = ZSeg{n_r, u.cur, u.tn, u.to, z.gl_lo, 1};
-            seg[ns++] = ZSeg{1, q.cur, q.tn, q.to, z.gl_hi - 1, 1};
+            seg[1] = ZSeg{n_r, u.cur, u.tn, u.to, z.gl_lo, 1};
+            seg[2] = ZSeg{1, q.cur, q.tn, q.to, z.gl_hi - 1, 1};
         }
         MemZ u{x, 0, 0, 0, 0};
         record_unit<TF>(x, true, m, acc, u);
-        seg[ns++] = ZSeg{n, u.cur, u.tn, u.to, z.gl_hi - 1, -1};
+        seg[3] = ZSeg{n, u.cur, u.tn, u.to, z.gl_hi - 1, -1};
     }
-    seg[ns++] = ZSeg{1, suf.cur, suf.tn, suf.to, g_suf, 1};
+    seg[4] = ZSeg{1, suf.cur, suf.tn, suf.to, g_suf, 1};
     const int D = x.D;
     // A, and the owner of the units at which it is reached
     int64_t a_none = INT64_MIN, at = 0;
-    for (int i = 0; i < ns; ++i) {
+#pragma unroll
+    for (int i = 0; i < kSeg; ++i) {
         if (seg[i].n <= 0) continue;
         const int64_t v = at + run_top(seg[i], -1, D);
         a_none = v > a_none ? v : a_none;
@@ -655,7 +674,8 @@ __device__ int64_t zero_top(const Ctx &x, int s, const ZStage &z, bool bwd, uint
     int owner = -1;
     bool shared = false;   // reached where every replica reaches it
     at = 0;
-    for (int i = 0; i < ns; ++i) {
+#pragma unroll
+    for (int i = 0; i < kSeg; ++i) {
         if (seg[i].n <= 0) continue;
         if (at + run_top(seg[i], -1, D) == a_none) {
             if (seg[i].gs < 0 || (seg[i].d == 0 && seg[i].n >= 2)) {
@@ -672,7 +692,8 @@ __device__ int64_t zero_top(const Ctx &x, int s, const ZStage &z, bool bwd, uint
     if (shared || owner < 0) return a_none;
     int64_t t_o = INT64_MIN;
     at = 0;
-    for (int i = 0; i < ns; ++i) {
+#pragma unroll
+    for (int i = 0; i < kSeg; ++i) {
         if (seg[i].n <= 0) continue;
         const int64_t v = at + run_top(seg[i], owner, D);
         t_o = v > t_o ? v : t_o;
@@ -819,6 +840,15 @@ __device__ __forceinline__ uint64_t shl1(uint64_t v)
 }
 
 __device__ __forceinline__ uint64_t ballot(bool b) { return __ballot(b); }
+
+// max of two clocks, which are never NaN or -0.0: the bare instruction
+// (fmax would canonicalize both operands first, two more dependent steps)
+__device__ __forceinline__ double max_nn(double a, double b)
+{
+    double r;
+    asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
 
 template <class T, class Op>
 __device__ __forceinline__ T seg_reduce(T v, int W, Op op)
@@ -1305,8 +1335,9 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
             const bool tr = rpos == r - 1 && from_right;
             const double a = ((src && sdir < 0) || tl) ? cl : cr;
             // clocks are sums of costs >= 0 from +0.0: never NaN or -0.0,
-            // so fmax is the plain larger value
-            const double e = fmax(a, clk) + (src ? scost : (tl ? l_cost : r_cost));
+            // so the bare maximum instruction gives the larger value (fmax
+            // would first canonicalize both operands)
+            const double e = max_nn(a, clk) + (src ? scost : (tl ? l_cost : r_cost));
             if (src || tl || tr) clk = e;
         }
         if (live_stage) {
@@ -1553,7 +1584,8 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     g.n_ops = r.n_ops;
     g.walked = r.walked_ops;
     g.status = r.status;
-    g.c = c;
+    g.c = ParConsts{c.inv_f, c.inv_b, c.inv_l, c.lat, c.launch, c.cap, c.mm, c.mm_c0, c.mm_c1, c.mm_c2,
+                    c.node, c.net_lat, c.net_inv_l, c.streams, c.st_lat, c.st_inv_l};
 
     // workspace: per-block class counts, class table, permutation (every
     // word is written before it is read: nothing needs clearing)

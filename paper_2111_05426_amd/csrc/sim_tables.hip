@@ -306,11 +306,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             const uint32_t tdev = is_s ? ibs : ias;
             const uint32_t fdev = ias;
             const ulonglong2 tm = s_mem[tdev][tid];
-            const uint64_t lf0 = s_mem[fdev][tid].x;
             const uint64_t lt = tm.x + (uint64_t)alloc;
-            // a compute op frees on the device it allocated on (lf0 == tm.x)
-            const uint64_t lf = is_c ? lt : lf0;
             s_mem[tdev][tid] = make_ulonglong2(lt, max_bits(lt, tm.y));
+            // read after that write: a compute op frees on the device it
+            // allocated on, and sees its own allocation
+            const uint64_t lf = s_mem[fdev][tid].x;
             suspect |= (uint64_t)fre > lf;
             s_mem[fdev][tid].x = lf - (uint64_t)fre;
         }
