@@ -161,11 +161,38 @@ def side_stream(torch):
     return _SIDE[0]
 
 
-def bench_parametric(torch, dsim, W, reps, warmup=1):
+# Vector issue rate of the chip: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane
+# instructions per second (a wave64 vector instruction occupies a 16-lane
+# SIMD for 4 cycles).  The transform's kernels are bound by dependent fp64
+# adds, Send-chain steps and wave-wide votes, i.e. by vector issue and its
+# latency, so their roofline is this rate and their achieved figure is the
+# vector instructions they execute (rocprofv3 SQ_INSTS_VALU, 64 lanes each)
+# per second of the live launch time.
+VALU_PEAK_T = 256 * 4 * 16 * 2.4e9 / 1e12
+PARAMETRIC_SRC = [os.path.join(ROOT, "paper_2111_05426_amd", "csrc", f) for f in ("parametric.hip", "model.h")]
+
+
+def stored_valu(workload):
+    """Vector instructions per dsim_simulate_parametric call of a grid,
+    counted by rocprofv3 --pmc (profiles/), if the transform's sources are
+    unchanged since the counters were taken."""
+    p = os.path.join(PROFILES, "valu.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        rec = json.load(f).get("k_parametric/%s" % workload)
+    if not rec or rec.get("source_sha256_16") != [kernel_hash(f) for f in PARAMETRIC_SRC]:
+        return None
+    return rec
+
+
+def bench_parametric(torch, dsim, W, reps, warmup=1, cpu_budget_s=0.0):
     """One grid of the transform-driven path: dsim_simulate_parametric over
     every strategy of the grid plus the top-k selection, with the strategies
-    resident on the device.  Walked ops are the ops the kernel processes (one
-    replica per stage); program ops count every op of the global program."""
+    resident on the device.  Projected ops count the ops of the per-stage
+    projection the kernel's result stands for (one replica per stage; the
+    kernel adds repeated layers in closed form, so these are not arithmetic
+    steps); program ops count every op of the global program."""
     strat = dsim.dsim_create_grid(W.model, W.grid)
     n = len(strat)
     rw = int(strat[:, 2].max())
@@ -202,15 +229,25 @@ def bench_parametric(torch, dsim, W, reps, warmup=1):
     wall_s = time.perf_counter() - t0
     kern_ms = sum(a.elapsed_time(b) for a, b, _ in ev) / len(ev)
     step_ms = sum(a.elapsed_time(c) for a, _, c in ev) / len(ev)
-    walked = int(res["walked_ops"].sum().item())
+    projected = int(res["walked_ops"].sum().item())
     prog = int(res["n_ops"].sum().item())
     ok = int((res["status"] == 0).sum().item())
-    return {"workload": W.name, "n_cand": n, "valid": ok, "top_k": k, "found": int(found.item()),
-            "best": {"index": int(out_idx[0].item()), "strategy_DHPK": strat[int(out_idx[0].item())].tolist(),
-                     "makespan_s": float(out_mk[0].item())} if int(found.item()) > 0 else None,
-            "kernel_ms": kern_ms, "step_ms": step_ms, "candidates_per_s": n / (step_ms * 1e-3),
-            "walked_ops": walked, "walked_ops_per_s": walked / (kern_ms * 1e-3),
-            "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3), "wall_s": wall_s, "reps": reps}
+    out = {"workload": W.name, "n_cand": n, "valid": ok, "top_k": k, "found": int(found.item()),
+           "best": {"index": int(out_idx[0].item()), "strategy_DHPK": strat[int(out_idx[0].item())].tolist(),
+                    "makespan_s": float(out_mk[0].item())} if int(found.item()) > 0 else None,
+           "kernel_ms": kern_ms, "step_ms": step_ms, "candidates_per_s": n / (step_ms * 1e-3),
+           "projected_ops": projected, "projected_ops_per_s": projected / (kern_ms * 1e-3),
+           "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3), "wall_s": wall_s, "reps": reps}
+    rec = stored_valu(W.name)
+    achieved = rec["valu_insts_per_call"] * 64 / (kern_ms * 1e-3) / 1e12 if rec else None
+    out["roofline"] = {"bound": "alu", "achieved": achieved, "peak": VALU_PEAK_T,
+                       "unit": "T vector lane-instructions/s", "frac": achieved / VALU_PEAK_T if rec else None,
+                       "traffic": None, "kernel": "k_parametric + k_parametric_wide",
+                       "valu_insts_per_call": rec["valu_insts_per_call"] if rec else None,
+                       "counters": rec["summary"] if rec else "not current for this source"}
+    if cpu_budget_s > 0:
+        out["cpu_baseline"] = cpu_baseline_parametric(W, strat, budget_s=cpu_budget_s)
+    return out
 
 
 def bench_grid_as_tables(torch, dsim, W, reps, n_dev=8):
@@ -287,11 +324,6 @@ def bench_lowered_programs(torch, dsim, reps):
             "host_interpret_and_lower_ms": host_s * 1e3, "kernel_ms": ms, "programs_per_s": n / (ms * 1e-3)}
 
 
-# fp64 add rate of the chip: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (half the
-# 78.6 TFLOP/s FMA figure, which counts two flops per lane-cycle)
-FP64_ADD_PEAK_T = 256 * 4 * 16 * 2.4e9 / 1e12
-
-
 def cpu_baseline_parametric(W, strat, budget_s=10.0, threads=None):
     """The oracle (projection mode), as it stands, on strided candidates of
     the grid until ~budget_s seconds of wall time are spent (all host
@@ -299,7 +331,7 @@ def cpu_baseline_parametric(W, strat, budget_s=10.0, threads=None):
     import numpy as np
     import oracle
     threads = threads or max(1, min(os.cpu_count() or 1, 16))
-    order = np.arange(len(strat))[::7]
+    order = np.arange(len(strat))[::7] if len(strat) > 7 * 4 * threads else np.arange(len(strat))
     done, t0 = 0, time.perf_counter()
     while time.perf_counter() - t0 < budget_s and done < len(order):
         pick = order[done:done + 4 * threads]
@@ -308,15 +340,15 @@ def cpu_baseline_parametric(W, strat, budget_s=10.0, threads=None):
         done += len(pick)
     dt = time.perf_counter() - t0
     return {"value": done / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
-            "sample": "%d of the %d strategies (every 7th, grid order), simulated by the C oracle (one replica "
-                      "per stage) in %.1f s on %d threads" % (done, len(strat), dt, threads)}
+            "sample": "%d of the %d strategies (grid order%s), simulated by the C oracle (one replica "
+                      "per stage) in %.1f s on %d threads" % (done, len(strat), ", every 7th" if len(order) < len(strat)
+                                                              else "", dt, threads)}
 
 
 def bench_parametric_line(args, torch, dsim, W):
     """The benchmark line for a strategy grid: a step is one
     dsim_simulate_parametric over the whole grid plus the top-k selection."""
     r = bench_parametric(torch, dsim, W, args.steps, args.warmup)
-    walked_T = r["walked_ops_per_s"] / 1e12
     out = {
         "metric": METRIC, "value": r["n_cand"] * r["reps"] / r["wall_s"], "unit": "candidates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -324,12 +356,8 @@ def bench_parametric_line(args, torch, dsim, W):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": "%s: %d strategies, simulate + top-%d" % (W.name, r["n_cand"], W.top_k),
                    "n_cand": r["n_cand"], "top_k": W.top_k},
-        "ops_per_s": r["walked_ops_per_s"], "program_ops_per_s": r["program_ops_per_s"],
-        "kernel_ms": r["kernel_ms"], "best": r["best"],
-        # every walked op is at least one dependent fp64 add in one lane
-        "roofline": {"bound": "alu", "achieved": walked_T, "peak": FP64_ADD_PEAK_T, "unit": "TFLOP/s",
-                     "frac": walked_T / FP64_ADD_PEAK_T, "traffic": None, "kernel": "k_parametric",
-                     "walked_ops_per_launch": r["walked_ops"]},
+        "ops_per_s": r["projected_ops_per_s"], "program_ops_per_s": r["program_ops_per_s"],
+        "kernel_ms": r["kernel_ms"], "best": r["best"], "roofline": r["roofline"],
     }
     if not args.no_cpu_baseline:
         strat = dsim.dsim_create_grid(W.model, W.grid)
@@ -390,7 +418,12 @@ def main():
         return
     out = bench_random_tables(args, torch, dsim, W)
     if not args.no_parametric:
-        out["parametric"] = [bench_parametric(torch, dsim, ALL[name], args.param_reps) for name in PARAMETRIC]
+        # the large MLP, GPT-2-small and GPT-3-175B-shaped grids also time the
+        # oracle on a bounded sample
+        graded = ("large_mlp", "gpt2_small", "gpt3_175b")
+        out["parametric"] = [bench_parametric(torch, dsim, ALL[name], args.param_reps,
+                                              cpu_budget_s=0.0 if args.no_cpu_baseline or name not in graded else 3.0)
+                             for name in PARAMETRIC]
         out["grids_as_tables"] = [bench_grid_as_tables(torch, dsim, ALL["tiny_mlp"], args.param_reps)]
         out["lowered_programs"] = bench_lowered_programs(torch, dsim, args.param_reps)
     if args.copy_calibration or not args.no_copy:
