@@ -280,7 +280,11 @@ typedef struct {
  *   cand_peak: max over devices of the peak.
  *   n_ops:     ops of the whole distributed program (each collective and
  *              each send counted once); may be NULL.
- *   walked_ops: ops the kernel processed for the candidate; may be NULL.
+ *   walked_ops: tables: the ops simulated (n_ops); parametric: the ops of
+ *              the per-stage projection the result stands for (every op of
+ *              one replica per stage, each collective and send once) -- not
+ *              arithmetic steps: repeated layers are summed in closed form;
+ *              may be NULL.
  *   status:    DSIM_ST_* bits, 0 = valid.
  *   row_width: columns of finish/peak (>= n_dev, or >= max P).
  */

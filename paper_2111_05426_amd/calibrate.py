@@ -1,10 +1,10 @@
 """Empirical MatMul cost for the simulator's device model.
 
 The paper's simulator gives matrix multiplications an empirical cost: a
-linear regression in the sizes of the input tensors, fitted on
-microbenchmarks that run a single op on inputs of various sizes (Sec. 4,
-implementation notes); some coefficients then play the part of hardware
-parameters such as launch overhead.  This module does that for the GPU it
+linear regression in the sizes of the input tensors, fitted on timings of
+that one op alone over a range of operand shapes (Sec. 4, implementation
+notes); some coefficients then play the part of hardware parameters such as
+launch overhead.  This module does that for the GPU it
 runs on:
 
     python -m paper_2111_05426_amd.calibrate [--dtype fp16] [--reps 20] [--out FILE]

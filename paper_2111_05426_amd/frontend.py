@@ -2,9 +2,10 @@
 mixed abstract/concrete domain, lowered to the explicit op tables that
 dsim_simulate_tables simulates.
 
-Sec. 3 builds every analysis on one abstract interpreter (Algorithm 1): the
-program runs op by op over a state that maps each variable to an abstract
-value, each op type having an abstract implementation.  For the simulator
+Sec. 3 builds every analysis on one abstract interpreter (Algorithm 1): it
+steps through the program's ops in order, keeping for every variable an
+abstract description instead of data, and evaluates each op type through an
+implementation that works on such descriptions.  For the simulator
 (Sec. 3.3) the values are abstract tensors -- element type, shape, device --
 and the cost of an op follows from the shapes of its inputs.  Ops such as
 Shape make a shape depend on the concrete value of a tensor, so the domain
