@@ -23,6 +23,7 @@ of the same workload as `cpu_baseline`.
 """
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -37,8 +38,15 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_hash(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """A hash of a kernel source's code: comments and blank lines removed and
+    runs of white space collapsed, so that a change of wording in a comment
+    keeps counters taken on the same code."""
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    lines = (" ".join(line.split()) for line in text.splitlines())
+    return hashlib.sha256("\n".join(line for line in lines if line).encode()).hexdigest()[:16]
 
 
 def stored_traffic(kernel, workload, src):

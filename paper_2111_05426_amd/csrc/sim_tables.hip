@@ -23,8 +23,8 @@
 // tables indexed by the op class (compute: launch, 1, 1/B, 1/F; send:
 // latency, 1, 1/L, 0; all-reduce over n devices: the ring terms for n, 1/L,
 // 0), so every lane runs one straight sequence.  The tables hold one copy per
-// lane of a 16-lane LDS phase: lanes of one phase reading different classes
-// then never meet in a bank.
+// lane of a 16-lane group, so that lanes reading different classes spread
+// over the banks (a 64-lane b128 read still takes several LDS cycles).
 //
 // The kernel is bound by issue rate (about 100 vector instructions per op)
 // more than by HBM: it has a fast path for the ops every lane of a wavefront
