@@ -332,7 +332,7 @@ def interpret(text, inputs=None, mixed=True):
     for outs, name, attrs, args in ops:
         a = [env[x] for x in args]
         res = run_op(name, attrs, a)
-        if not mixed:
+        if not mixed and any(is_c(r) for r in res):
             dev = one_device([as_type(x) for x in a])
             res = [as_type(r, dev) for r in res]
         for o, r in zip(outs, res):
