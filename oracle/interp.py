@@ -67,7 +67,7 @@ def as_type(v, dev=None):
     """The type of a concrete value."""
     if not is_c(v):
         return v
-    dt = "Float32" if v.dtype.kind == "f" else "Int32"
+    dt = "Float64" if v.dtype.kind == "f" else "Int32"
     if v.ndim == 0:
         return ("S", dt, dev)
     return ("T", dt, tuple(int(d) for d in v.shape), dev)
