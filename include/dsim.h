@@ -445,6 +445,104 @@ DSIM_API dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, 
                                         uint32_t *free_bytes, uint32_t *n_ops_out,
                                         void *hip_stream);
 
+/*
+ * Program front end (host only: no HIP call, no device memory; several
+ * threads may call it at once).
+ *
+ * Program text, one statement per line, `#` starting a comment:
+ *   func NAME(%p: TYPE [keep], ...)        -- first non-empty line
+ *   %out, ... = OpType[key = VALUE, ...](%in, ...)
+ *   return %v, ...                         -- ignored
+ * TYPE is Tensor[DTYPE, (d0, d1, ...), DEVICE], Tensor[DTYPE, ??, DEVICE]
+ * (shape unknown), DTYPE or DTYPE[DEVICE] (an abstract scalar); DTYPE one of
+ * Float64 Float32 Float16 BFloat16 Int64 Int32 Int8 Bool.  VALUE is a number,
+ * a quoted string or a (nested) list.  A parameter marked keep (weights)
+ * stays resident for the whole program.  Op types: Constant Shape Gather
+ * Unsqueeze Squeeze Concat Reshape Add Sub Mul Div Pow Relu Neg Sqrt Exp Tanh
+ * Erf Gelu Identity Cast Softmax LayerNormalization Transpose Flatten Split
+ * MatMul Gemm Send AllReduce, with ONNX's attributes (axis, axes, perm,
+ * split, transA, transB, to, value; Send's device).
+ *
+ * Inputs text (NULL or empty: none): one binding per line, `%name = VALUE`
+ * (a concrete value: a number or a rectangular nested list; int64 unless an
+ * entry is a float) or `%name: TYPE` (an abstract value); each name must be
+ * a parameter, and its binding replaces the declared type.
+ *
+ * Interpretation (Sec. 3, Algorithm 1; Sec. 3.3 and Fig. 4): the ops are
+ * stepped through in order over a state mapping each variable to a value,
+ * concrete (an int64 or fp64 array) or abstract (a tensor: element type,
+ * shape or unknown, device; or a scalar), each op evaluated by its most
+ * precise implementation for the kinds of its arguments (an op whose
+ * arguments are all concrete is evaluated; Shape of a tensor of known shape
+ * is concrete; Reshape of a tensor by a concrete target has a known shape).
+ * mixed = 0 gives the abstract-only interpretation: every concrete value is
+ * replaced by its type (shape arithmetic Int32, fp64 values Float64) as soon
+ * as it appears.
+ */
+
+/*
+ * dsim_interpret_program -- the final state of one interpretation as text:
+ * one line `%name = VALUE` per variable (parameters first, then each op's
+ * results in program order); VALUE is a concrete value as a number or a
+ * nested list (fp64 values with a '.', an exponent, inf or nan), a tensor
+ * as Tensor[DTYPE, (d0, ...), DEVICE] (?? for an unknown shape, None for no
+ * device), a scalar as its DTYPE.  out: host buffer of cap bytes, written
+ * NUL-terminated; *out_len (if out_len != NULL) = the bytes needed,
+ * terminator included.  DSIM_ENOSPC if cap is smaller (out == NULL with
+ * cap == 0 asks for the size); DSIM_EINVAL for a program that cannot be
+ * read or interpreted (the message names the line); DSIM_ERANGE for a size
+ * beyond 64 bits or a concrete value of more than 2^20 entries.
+ */
+DSIM_API dsim_status dsim_interpret_program(const char *program, const char *inputs, int32_t mixed,
+                                            char *out, size_t cap, size_t *out_len);
+
+/*
+ * dsim_lower_programs -- n_prog programs interpreted (mixed) and lowered to
+ * op tables in the dsim_tables layout, ready to be copied to the device for
+ * dsim_simulate_tables (Sec. 3.3).  Lowering: an op that yields no abstract
+ * tensor runs here and emits nothing; Reshape, Unsqueeze, Squeeze, Flatten
+ * and Identity are views sharing their input's memory and emit nothing;
+ * every other op on abstract tensors is one record: compute on the one
+ * device of its tensors (MatMul and Gemm cost class 1), Send (alloc on the
+ * receiver), AllReduce over the devices of its inputs (in place).  Compute
+ * bytes: every abstract input and output tensor; flops: 1 per output element
+ * for elementwise ops (Gelu 8, Softmax 5, LayerNormalization 8, Cast 0),
+ * 2 * (output elements) * k for MatMul and Gemm (+1 per element with a
+ * bias), 0 for Transpose, Concat, Split, Gather; Send and AllReduce: their
+ * input's bytes.  Memory per storage: allocated by the record that creates
+ * it, freed by its last reader (or its creator if unread); parameters are
+ * resident at t = 0 (init_live), keep ones never freed; a storage last read
+ * by an AllReduce stays live.
+ *   programs, inputs: host arrays of n_prog strings; inputs may be NULL and
+ *     its entries NULL (no inputs).
+ *   n_dev: 1..8, the width of init_live's rows; every device a program uses
+ *     must be below it (DSIM_ERANGE otherwise).
+ *   max_ops: rows of the output arrays.
+ *   code, flops, bytes, alloc_bytes, free_bytes: host arrays of
+ *     max_ops * n_prog records, op-major and program-fastest (record j of
+ *     program c at j * n_prog + c); rows from n_ops[c] on are zero.
+ *   n_ops: host array [n_prog]; init_live: host array [n_prog * n_dev].
+ *     All seven arrays NULL: nothing is written and max_ops is not
+ *     checked (a sizing pass).
+ *   max_ops_used, n_dev_used (may be NULL): the largest record count of any
+ *     program, and 1 + the highest device any program uses.
+ *   n_threads: host threads to use (<= 1: the calling thread only).
+ * Returns DSIM_EINVAL for a program that cannot be read, interpreted or
+ * simulated (an unknown shape, an op on tensors of several devices, a
+ * received tensor nothing reads), with the program's index and line in the
+ * message; DSIM_ERANGE for a value that does not fit the record format
+ * exactly (flops or bytes not exact in fp32, alloc or free >= 2^32) or a
+ * device >= n_dev; DSIM_ENOSPC if some program needs more than max_ops
+ * records (its n_ops entry is 0 and its column unwritten; *max_ops_used
+ * says how many are needed).  On any error but DSIM_ENOSPC the outputs are
+ * unspecified.
+ */
+DSIM_API dsim_status dsim_lower_programs(const char *const *programs, const char *const *inputs, int64_t n_prog,
+                                         int32_t n_dev, int32_t max_ops, uint32_t *code, float *flops,
+                                         float *bytes, uint32_t *alloc_bytes, uint32_t *free_bytes,
+                                         uint32_t *n_ops, uint64_t *init_live, int32_t *max_ops_used,
+                                         int32_t *n_dev_used, int32_t n_threads);
+
 #ifdef __cplusplus
 }
 #endif

@@ -95,9 +95,14 @@ def lib():
             [C.c_void_p] * 7
         L.dsim_materialize_tables.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64, C.c_int32,
                                               C.c_int32] + [C.c_void_p] * 9
+        L.dsim_interpret_program.argtypes = [C.c_char_p, C.c_char_p, C.c_int32, C.c_void_p, C.c_size_t,
+                                             C.POINTER(C.c_size_t)]
+        L.dsim_lower_programs.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int32, C.c_int32] + \
+            [C.c_void_p] * 7 + [C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.c_int32]
         for name in ("dsim_create_grid", "dsim_simulate_tables", "dsim_simulate_parametric",
                      "dsim_simulate_parametric_static", "dsim_argmin",
-                     "dsim_generate_random_tables", "dsim_materialize_tables"):
+                     "dsim_generate_random_tables", "dsim_materialize_tables", "dsim_interpret_program",
+                     "dsim_lower_programs"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib

@@ -15,7 +15,7 @@ def test_exports_every_declared_function():
     assert set(names) == {"dsim_last_error", "dsim_create_grid", "dsim_simulate_tables",
                           "dsim_simulate_parametric", "dsim_parametric_workspace", "dsim_argmin_workspace",
                           "dsim_argmin", "dsim_generate_random_tables", "dsim_materialize_tables",
-                          "dsim_simulate_parametric_static"}
+                          "dsim_simulate_parametric_static", "dsim_interpret_program", "dsim_lower_programs"}
     L = dsim.lib()
     for n in names:
         assert hasattr(L, n), n

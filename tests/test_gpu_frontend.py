@@ -1,9 +1,10 @@
 """GPU parity of programs lowered by the front end: GPT-2-shaped layers with
 tensor and pipeline parallelism over 1..8 devices, swept over batch and
-sequence sizes, lowered to tables (mixed abstract/concrete interpretation,
-Sec. 3.3), packed as candidates and simulated by dsim_simulate_tables,
-against the oracle's own interpretation of each program simulated as a
-program over tensors.  Bar: times bit-identical, peaks and status exact."""
+sequence sizes, and seeded random programs over 1..8 devices, lowered in one
+batch to candidate tables (dsim_lower_programs: mixed abstract/concrete
+interpretation, Sec. 3.3) and simulated by dsim_simulate_tables, against the
+oracle's own interpretation of each program simulated as a program over
+tensors.  Bar: times bit-identical, peaks and status exact."""
 import math
 
 import numpy as np
@@ -35,10 +36,16 @@ def test_lowered_programs_vs_oracle(torch_gpu, dev):
     from oracle import interp
     from paper_2111_05426_amd import dsim, frontend as fe, programs
     torch = torch_gpu
+    from random_programs import random_program
     texts = [programs.gpt2_layers(B, S, n_layers=4, tp=tp, pp=pp) for B, S, tp, pp in CASES]
-    tabs = [fe.lower(fe.parse(t), {"%flat": [-1]}, n_dev=8) for t in texts]
-    p = fe.pack(tabs)
-    n = len(CASES)
+    inputs = [{"%flat": [-1]}] * len(texts)
+    cases = list(CASES)
+    for seed in range(60):
+        texts.append(random_program(seed, n_ops=60 + seed, n_dev=1 + seed % 8))
+        inputs.append({})
+        cases.append(("random", seed))
+    p = fe.lower_batch(texts, inputs, n_dev=8, threads=8)
+    n = len(texts)
     print("%d lowered programs, %d records at most" % (n, p["code"].shape[0]), flush=True)
     g = {k: torch.from_numpy(np.ascontiguousarray(p[k]).view(np.int32 if p[k].dtype == np.uint32 else p[k].dtype)).cuda()
          for k in ("code", "flops", "bytes", "alloc", "free", "n_ops")}
@@ -51,8 +58,8 @@ def test_lowered_programs_vs_oracle(torch_gpu, dev):
     pk = r["peak"].cpu().numpy().view(np.uint64)
     cp = r["cand_peak"].cpu().numpy().view(np.uint64)
     st = r["status"].cpu().numpy()
-    for c, (text, case) in enumerate(zip(texts, CASES)):
-        o = interp.simulate(text, dev, {"%flat": [-1]}, n_dev=8)
+    for c, (text, inp, case) in enumerate(zip(texts, inputs, cases)):
+        o = interp.simulate(text, dev, inp, n_dev=8)
         assert np.array_equal(fin[c], o["finish"]), case
         assert np.array_equal(pk[c], o["peak"]), case
         assert mk[c] == o["makespan"], case

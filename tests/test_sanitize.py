@@ -52,3 +52,35 @@ def test_host_validation_under_sanitizers(tmp_path):
     rc, out = run([exe], env=sanitizer_env())
     assert rc == 0 and "runtime error" not in out and "AddressSanitizer" not in out, out
     assert "reached a launch" in out
+
+
+@pytest.mark.skipif(not os.path.exists(CLANG), reason="the ROCm clang is not installed")
+def test_front_end_under_sanitizers(tmp_path):
+    """The parser, interpreter and lowering over valid programs (Fig. 4's
+    snippet, GPT-2-shaped layers, random programs) and 4000 mutated ones."""
+    import json
+    import sys
+    sys.path.insert(0, HERE)
+    from random_programs import random_program
+    from paper_2111_05426_amd import programs
+    with open(os.path.join(HERE, "golden", "fig4_reshape.json")) as f:
+        fig4 = json.load(f)["program"]
+    texts = [fig4.replace("%3114", "%flat"), programs.gpt2_layers(3, 64, n_layers=2, tp=2, pp=2)] + \
+        [random_program(s, n_ops=30, n_dev=1 + s % 4) for s in range(6)]
+    files = []
+    for i, t in enumerate(texts):
+        files.append(str(tmp_path / ("p%d.txt" % i)))
+        with open(files[-1], "w") as f:
+            f.write(t)
+    exe = str(tmp_path / "frontend_driver")
+    rc, out = run([CLANG, "-std=c++17", "-O1", "-g", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
+                   "-I", os.path.join(ROOT, "include")] + SAN +
+                  ["-o", exe, os.path.join(HERE, "sanitize", "frontend_driver.cpp"),
+                   os.path.join(ROOT, "paper_2111_05426_amd", "csrc", "frontend.cpp"),
+                   os.path.join(HERE, "sanitize", "launch_stubs.cpp"),
+                   os.path.join(ROOT, "paper_2111_05426_amd", "csrc", "api.cpp"),
+                   "-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib"])
+    assert rc == 0, out
+    rc, out = run([exe] + files, env=dict(sanitizer_env(), ASAN_OPTIONS="detect_leaks=1"))
+    assert rc == 0 and "runtime error" not in out and "AddressSanitizer" not in out, out
+    assert "0 failures" in out
