@@ -47,7 +47,7 @@ class _Dev(C.Structure):
                 ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double),
                 ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double),
                 ("streams_per_gpu", C.c_int32), ("stream_bytes_per_s", C.c_double),
-                ("stream_latency_s", C.c_double)]
+                ("stream_latency_s", C.c_double), ("mm_c3", C.c_double), ("mm_floor", C.c_double)]
 
 
 class _Model(C.Structure):
@@ -71,14 +71,21 @@ def lib():
 
 
 def _dev(d):
+    """The device model: matmul is None, (c0, c1, c2) -- the linear form --
+    or (c0, c1, c2, c3, floor)."""
     mm = getattr(d, "matmul", None)
     net = getattr(d, "network", None)
     st = getattr(d, "streams", None)
+    mmv = tuple(float(v) for v in mm) if mm is not None else (0.0, 0.0, 0.0)
+    if len(mmv) == 3:
+        mmv = mmv + (0.0, 0.0)
+    if len(mmv) != 5:
+        raise ValueError("matmul must be (c0, c1, c2) or (c0, c1, c2, c3, floor)")
     return _Dev(d.flops_per_s, d.mem_bytes_per_s, d.link_bytes_per_s, d.link_latency_s,
-                d.launch_s, int(d.mem_cap_bytes), 1 if mm is not None else 0,
-                *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))),
+                d.launch_s, int(d.mem_cap_bytes), 1 if mm is not None else 0, *mmv[:3],
                 *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)),
-                *((int(st[0]), float(st[1]), float(st[2])) if st is not None else (0, 0.0, 0.0)))
+                *((int(st[0]), float(st[1]), float(st[2])) if st is not None else (0, 0.0, 0.0)),
+                *mmv[3:])
 
 
 def _model(m):
@@ -91,9 +98,10 @@ def _p(a):
     return a.ctypes.data_as(C.c_void_p) if a is not None else None
 
 
-def cost(dev, kind, flops, nbytes, n, type=None):
+def cost(dev, kind, flops, nbytes, n, type=None, k=0.0):
     """Cost of one op; with an op type name (TYPES), matrix multiplications
-    take the device's empirical MatMul regression when it has one."""
+    (reduction length k) take the device's empirical MatMul regression when
+    it has one."""
     d = _dev(dev)
     if type is None:
         f = lib().or_cost
@@ -102,8 +110,8 @@ def cost(dev, kind, flops, nbytes, n, type=None):
         return f(C.byref(d), kind, float(flops), float(nbytes), int(n))
     f = lib().or_cost_typed
     f.restype = C.c_double
-    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_int, C.c_double, C.c_double, C.c_int, C.c_int]
-    return f(C.byref(d), kind, TYPES.index(type), float(flops), float(nbytes), int(n), 0)
+    f.argtypes = [C.POINTER(_Dev), C.c_int, C.c_int, C.c_double, C.c_double, C.c_double, C.c_int, C.c_int]
+    return f(C.byref(d), kind, TYPES.index(type), float(flops), float(nbytes), float(k), int(n), 0)
 
 
 def cost_between_nodes(dev, kind, nbytes, n):
@@ -142,6 +150,7 @@ def sim_table(tab, n_dev, dev, init_live=None):
     """Simulate one candidate's explicit table (dict of equal-length arrays)."""
     n = len(tab["code"])
     arr = {k: np.ascontiguousarray(tab[k]) for k in ("code", "flops", "bytes", "alloc", "free")}
+    mmk = None if tab.get("mm_k") is None else np.ascontiguousarray(tab["mm_k"], np.uint32)
     fin = np.zeros(n_dev, np.float64)
     pk = np.zeros(n_dev, np.uint64)
     mk = C.c_double()
@@ -149,12 +158,12 @@ def sim_table(tab, n_dev, dev, init_live=None):
     st = C.c_int32()
     il = None if init_live is None else np.ascontiguousarray(init_live, np.uint64)
     f = lib().or_sim_table
-    f.argtypes = [C.c_int64, C.c_int] + [C.c_void_p] * 5 + [C.c_int64, C.c_void_p, C.POINTER(_Dev),
+    f.argtypes = [C.c_int64, C.c_int] + [C.c_void_p] * 6 + [C.c_int64, C.c_void_p, C.POINTER(_Dev),
                                                             C.POINTER(C.c_double), C.c_void_p, C.c_void_p,
                                                             C.POINTER(C.c_uint64), C.POINTER(C.c_int32)]
     d = _dev(dev)
     rc = f(n, n_dev, _p(arr["code"]), _p(arr["flops"]), _p(arr["bytes"]), _p(arr["alloc"]),
-           _p(arr["free"]), 1, _p(il), C.byref(d), C.byref(mk), _p(fin), _p(pk), C.byref(cp), C.byref(st))
+           _p(arr["free"]), _p(mmk), 1, _p(il), C.byref(d), C.byref(mk), _p(fin), _p(pk), C.byref(cp), C.byref(st))
     if rc:
         raise ValueError("or_sim_table failed: %d" % rc)
     return dict(makespan=mk.value, finish=fin, peak=pk, cand_peak=cp.value, status=st.value)
@@ -164,7 +173,8 @@ def sim_program(ops, tensors, n_dev, dev, with_trace=False):
     """Simulate an explicit program.
 
     ops: list of dicts {kind, devs, ins, outs, cost (optional), flops, bytes,
-         matmul (optional: the empirical MatMul cost applies)}
+         matmul (optional: the empirical MatMul cost applies), k (optional:
+         the product's reduction length)}
     tensors: list of (device, size, flags)
     dev: object with the device-model attributes (flops_per_s, ...)
     """
@@ -189,17 +199,18 @@ def sim_program(ops, tensors, n_dev, dev, with_trace=False):
     t_size = np.array([t[1] for t in tensors] or [0], np.uint64)
     t_flags = np.array([t[2] for t in tensors] or [0], np.int32)
     mm = np.array([1 if o.get("matmul") else 0 for o in ops] or [0], np.int32)
+    mmk = np.array([float(o.get("k", 0.0)) for o in ops] or [0.0], np.float64)
     fin = np.zeros(n_dev, np.float64)
     pk = np.zeros(n_dev, np.uint64)
     ts = np.zeros(max(n, 1), np.float64)
     te = np.zeros(max(n, 1), np.float64)
     f = lib().or_sim_program
     f.argtypes = [C.c_int64] + [C.c_void_p] * 10 + [C.c_int64] + [C.c_void_p] * 3 + \
-        [C.c_int, C.POINTER(_Dev)] + [C.c_void_p] * 5
+        [C.c_int, C.POINTER(_Dev)] + [C.c_void_p] * 6
     d = _dev(dev)
     rc = f(n, _p(kind), _p(cost_), _p(fl), _p(by), _p(db), _p(dv), _p(ib), _p(iv), _p(ob), _p(ov),
            len(tensors), _p(t_dev), _p(t_size), _p(t_flags), n_dev, C.byref(d), _p(fin), _p(pk),
-           _p(ts), _p(te), _p(mm))
+           _p(ts), _p(te), _p(mm), _p(mmk))
     if rc:
         raise ValueError("or_sim_program failed: %d" % rc)
     out = dict(finish=fin, peak=pk, makespan=float(fin.max()) if n_dev else 0.0)
@@ -219,7 +230,7 @@ def sim_strategy(model, D, H, P, K, dev, slice=False, type_cost=None, want_devic
     df = np.zeros(n_dev, np.float64) if want_devices else None
     dp = np.zeros(n_dev, np.uint64) if want_devices else None
     dr = np.zeros(n_dev, np.uint64) if want_devices else None
-    fbt = np.zeros(2 * N_TYPES, np.float64)
+    fbt = np.zeros(3 * N_TYPES, np.float64)
     tc = None
     if type_cost is not None:
         tc = np.full(N_TYPES, -1.0)
@@ -242,7 +253,8 @@ def sim_strategy(model, D, H, P, K, dev, slice=False, type_cost=None, want_devic
     return dict(makespan=mk.value, cand_peak=cp.value, n_ops=no.value, status=st.value,
                 stage_finish=sf, stage_peak=sp, dev_finish=df, dev_peak=dp, dev_resident=dr,
                 flops_by_type={TYPES[i]: fbt[i] for i in range(N_TYPES)},
-                bytes_by_type={TYPES[i]: fbt[N_TYPES + i] for i in range(N_TYPES)})
+                bytes_by_type={TYPES[i]: fbt[N_TYPES + i] for i in range(N_TYPES)},
+                k_by_type={TYPES[i]: fbt[2 * N_TYPES + i] for i in range(N_TYPES)})
 
 
 def model_size_ok(model):

@@ -81,8 +81,11 @@ typedef struct {
     uint64_t mem_cap_bytes;
     /* Empirical MatMul cost (Sec. 4: MatMul gets a linear regression in its
      * input sizes, fitted on single-op microbenchmarks): when mm_enabled,
-     * a matrix multiplication of `flops` flops touching `bytes` bytes costs
-     * (mm_c0 + mm_c1 * flops) + mm_c2 * bytes instead of the roofline. */
+     * a matrix multiplication of `flops` flops touching `bytes` bytes with
+     * reduction length k costs
+     *   max(mm_floor, ((mm_c0 + mm_c1 * flops) + mm_c2 * bytes) + mm_c3 * k)
+     * instead of the roofline (mm_c3 and mm_floor at the end of the struct;
+     * both 0 give the paper's linear form). */
     int32_t mm_enabled;
     double mm_c0, mm_c1, mm_c2;
     /* Two-tier interconnect (hardware topologies, Sec. 1; the paper models
@@ -103,6 +106,8 @@ typedef struct {
      * place of the links.  S = 0 or 1: every device is its own GPU. */
     int32_t streams_per_gpu;
     double stream_bytes_per_s, stream_latency_s;
+    /* the MatMul cost's reduction-length term and floor (see mm_enabled) */
+    double mm_c3, mm_floor;
 } or_device_model;
 
 typedef struct {
@@ -215,10 +220,15 @@ static int is_matmul(int type)
     }
 }
 
-/* linear regression cost of a matrix multiplication (Sec. 4) */
-static double cost_matmul(const or_device_model *m, double flops, double bytes)
+/* Regression cost of a matrix multiplication (Sec. 4): linear in the input
+ * sizes, plus a term in the reduction length k (the serial part of a
+ * product: few output tiles with a long k take time that neither the flops
+ * nor the bytes show), at least mm_floor (the per-product dispatch that an
+ * eagerly issued product never finishes sooner than). */
+static double cost_matmul(const or_device_model *m, double flops, double bytes, double k)
 {
-    return (m->mm_c0 + m->mm_c1 * flops) + m->mm_c2 * bytes;
+    double c = ((m->mm_c0 + m->mm_c1 * flops) + m->mm_c2 * bytes) + m->mm_c3 * k;
+    return m->mm_floor > c ? m->mm_floor : c;
 }
 
 /* cost of an op; spans: its devices lie in more than one node */
@@ -235,11 +245,12 @@ double or_cost(const or_device_model *m, int kind, double flops, double bytes, i
     return or_cost_spans(m, kind, flops, bytes, n, 0);
 }
 
-/* cost of an op of a given type: matrix multiplications take the empirical
- * regression when the device model carries one */
-double or_cost_typed(const or_device_model *m, int kind, int type, double flops, double bytes, int n, int spans)
+/* cost of an op of a given type: matrix multiplications (reduction length k)
+ * take the empirical regression when the device model carries one */
+double or_cost_typed(const or_device_model *m, int kind, int type, double flops, double bytes, double k, int n,
+                     int spans)
 {
-    if (kind == OR_COMPUTE && m->mm_enabled && is_matmul(type)) return cost_matmul(m, flops, bytes);
+    if (kind == OR_COMPUTE && m->mm_enabled && is_matmul(type)) return cost_matmul(m, flops, bytes, k);
     return or_cost_spans(m, kind, flops, bytes, n, spans);
 }
 
@@ -267,7 +278,7 @@ double or_cost_typed(const or_device_model *m, int kind, int type, double flops,
 /* ------------------------------------------------------------------------ */
 int or_sim_table(int64_t n_ops, int n_dev,
                  const uint32_t *code, const float *flops, const float *bytes,
-                 const uint32_t *alloc, const uint32_t *freeb, int64_t stride,
+                 const uint32_t *alloc, const uint32_t *freeb, const uint32_t *mm_k, int64_t stride,
                  const uint64_t *init_live, const or_device_model *m,
                  double *makespan, double *finish, uint64_t *peak,
                  uint64_t *cand_peak, int32_t *status)
@@ -302,7 +313,8 @@ int or_sim_table(int64_t n_ops, int n_dev,
         if (kind == OR_COMPUTE) {
             if (a >= n_dev) { st |= ST_BAD_DEVICE; continue; }
             mask = 1u << a;
-            if (cls == 1 && m->mm_enabled) cost = cost_matmul(m, (double)flops[o], (double)bytes[o]);
+            if (cls == 1 && m->mm_enabled)
+                cost = cost_matmul(m, (double)flops[o], (double)bytes[o], mm_k ? (double)mm_k[o] : 0.0);
             else cost = cost_compute(m, (double)flops[o], (double)bytes[o]);
         } else if (kind == OR_SEND) {
             if (a >= n_dev || b >= n_dev) { st |= ST_BAD_DEVICE; continue; }
@@ -498,6 +510,7 @@ typedef struct {
                                  (a projection materialises part of it); -1: its
                                  devices as listed */
     double *flops, *bytes;
+    double *kred;          /* reduction length of a matrix multiplication, 0 otherwise */
     double *ocost;         /* per-op duration override (< 0: cost model) */
     int64_t *dev_beg, *in_beg, *out_beg;
     int32_t *devs, *ins, *outs;
@@ -528,7 +541,7 @@ static void prog_init(or_prog *g) { memset(g, 0, sizeof *g); }
 static void prog_free(or_prog *g)
 {
     free(g->kind); free(g->type); free(g->nsz); free(g->gfirst); free(g->glast);
-    free(g->flops); free(g->bytes); free(g->ocost);
+    free(g->flops); free(g->bytes); free(g->kred); free(g->ocost);
     free(g->dev_beg); free(g->in_beg); free(g->out_beg);
     free(g->devs); free(g->ins); free(g->outs);
     free(g->t_dev); free(g->t_size); free(g->t_flags);
@@ -565,6 +578,7 @@ static void op_begin(or_prog *g, int kind, int type, double flops, double bytes)
         g->glast = grow(g->glast, g->cap_ops, i + 2, sizeof(int32_t), &c, &g->failed);
         g->flops = grow(g->flops, g->cap_ops, i + 2, sizeof(double), &c, &g->failed);
         g->bytes = grow(g->bytes, g->cap_ops, i + 2, sizeof(double), &c, &g->failed);
+        g->kred = grow(g->kred, g->cap_ops, i + 2, sizeof(double), &c, &g->failed);
         g->ocost = grow(g->ocost, g->cap_ops, i + 2, sizeof(double), &c, &g->failed);
         g->dev_beg = grow(g->dev_beg, g->cap_ops, i + 2, sizeof(int64_t), &c, &g->failed);
         g->in_beg = grow(g->in_beg, g->cap_ops, i + 2, sizeof(int64_t), &c, &g->failed);
@@ -579,6 +593,7 @@ static void op_begin(or_prog *g, int kind, int type, double flops, double bytes)
     g->glast[i] = -1;
     g->flops[i] = flops;
     g->bytes[i] = bytes;
+    g->kred[i] = 0.0;
     g->ocost[i] = -1.0;
     g->dev_beg[i] = g->n_devs;
     g->in_beg[i] = g->n_ins;
@@ -686,7 +701,8 @@ static int prog_simulate(const or_prog *g, int n_dev, const or_device_model *m,
             } else {
                 spans = spans_nodes(m, g->devs + g->dev_beg[i], g->dev_beg[i + 1] - g->dev_beg[i]);
             }
-            cost = or_cost_typed(m, g->kind[i], g->type[i], g->flops[i], g->bytes[i], g->nsz[i], spans);
+            cost = or_cost_typed(m, g->kind[i], g->type[i], g->flops[i], g->bytes[i], g->kred[i], g->nsz[i],
+                                 spans);
         }
         for (q = g->dev_beg[i]; q < g->dev_beg[i + 1]; q++) {
             d = g->devs[q];
@@ -746,7 +762,7 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
                    int64_t n_t, const int32_t *t_dev, const uint64_t *t_size,
                    const int32_t *t_flags, int n_dev, const or_device_model *m,
                    double *finish, uint64_t *peak, double *tstart, double *tend,
-                   const int32_t *is_matmul)
+                   const int32_t *is_matmul, const double *mm_k)
 {
     or_prog g;
     int64_t i, q;
@@ -762,6 +778,8 @@ int or_sim_program(int64_t n_ops, const int32_t *kind, const double *cost,
         for (q = in_beg[i]; q < in_beg[i + 1]; q++) op_in(&g, ins[q]);
         for (q = out_beg[i]; q < out_beg[i + 1]; q++) op_out(&g, outs[q]);
         if (!g.failed && cost) g.ocost[i] = cost[i];
+        /* mm_k (optional): a matrix multiplication's reduction length */
+        if (!g.failed && mm_k) g.kred[i] = mm_k[i];
         op_end(&g, 0, 1);
     }
     if (g.failed) { prog_free(&g); return -3; }
@@ -860,6 +878,7 @@ typedef struct {
     int32_t *X, *Y;       /* per (s, r) resident inputs */
     int32_t *cur;         /* per r scratch */
     int32_t *tmp;         /* per r scratch */
+    double mmk;           /* reduction length of the product emit_mm is emitting */
 } mat;
 
 /* Materialised replicas r of a stage: every (d, h) as r = d*H + h; in
@@ -925,6 +944,7 @@ static void emit_local(mat *x, int s, int type, double flops, double bytes,
         if (out_size) o1 = prog_tensor(x->g, dv, out_size, 0);
         if (out2_size) o2 = prog_tensor(x->g, dv, out2_size, 0);
         op_begin(x->g, OR_COMPUTE, type, flops, bytes);
+        if (!x->g->failed) x->g->kred[x->g->n_ops] = x->mmk;
         op_dev(x->g, dv);
         if (in1) op_in(x->g, in1[r]);
         if (in2) op_in(x->g, in2[r]);
@@ -935,6 +955,17 @@ static void emit_local(mat *x, int s, int type, double flops, double bytes,
         if (out_ids) out_ids[r] = o1;
         if (out2_ids) out2_ids[r] = o2;
     }
+}
+
+/* a matrix multiplication whose products reduce over k (the sum of the
+ * reduction lengths when one op stands for several products) */
+static void emit_mm(mat *x, int s, int type, int64_t k, double flops, double bytes,
+                    const int32_t *in1, const int32_t *in2, const int32_t *in3,
+                    uint64_t out_size, int32_t *out_ids, uint64_t out2_size, int32_t *out2_ids)
+{
+    x->mmk = (double)k;
+    emit_local(x, s, type, flops, bytes, in1, in2, in3, out_size, out_ids, out2_size, out2_ids);
+    x->mmk = 0.0;
 }
 
 /* all-reduce over the tensor-parallel group of every data replica */
@@ -1081,7 +1112,7 @@ static void mlp_layer(mat *x, int s, int k, int i, int32_t *cur, int32_t *tmp)
     int row;
     mlp_dims(x, i, &din, &dout, &row);
     use_weight(x, s, i - x->l0[s], w);
-    emit_local(x, s, T_GEMM, (double)(2 * m * din * dout), (double)(e * (m * din + din * dout + m * dout)),
+    emit_mm(x, s, T_GEMM, din, (double)(2 * m * din * dout), (double)(e * (m * din + din * dout + m * dout)),
                cur, w, NULL, (uint64_t)(e * m * dout), tmp, 0, NULL);
     if (row) emit_ar_tp(x, s, T_AR_TP, (double)(e * m * dout), tmp);
     emit_local(x, s, T_RELU, (double)(m * dout), (double)(2 * e * m * dout),
@@ -1135,11 +1166,11 @@ static void mlp_bwd(mat *x, int s, int k)
                    cur, a, NULL, (uint64_t)(e * m * dout), tmp, 0, NULL);
         if (i == x->l0[s]) gather_sv(x, s, k, F_IN, xin);
         else gather_sv(x, s, k, F_LAYER0 + (li - 1) * NLF + L_A, xin);
-        emit_local(x, s, T_GEMMDW, (double)(2 * m * din * dout), (double)(e * (m * din + m * dout + din * dout)),
+        emit_mm(x, s, T_GEMMDW, m, (double)(2 * m * din * dout), (double)(e * (m * din + m * dout + din * dout)),
                    xin, tmp, NULL, (uint64_t)(e * din * dout), gw, 0, NULL);
         accumulate(x, s, k, li, (uint64_t)(din * dout), gw);
         use_weight(x, s, li, w);
-        emit_local(x, s, T_GEMMDX, (double)(2 * m * din * dout), (double)(e * (m * dout + din * dout + m * din)),
+        emit_mm(x, s, T_GEMMDX, dout, (double)(2 * m * din * dout), (double)(e * (m * dout + din * dout + m * din)),
                    tmp, w, NULL, (uint64_t)(e * m * din), cur, 0, NULL);
         if (!row && x->H > 1 && i != 0) emit_ar_tp(x, s, T_AR_TP, (double)(e * m * din), cur);
     }
@@ -1156,7 +1187,7 @@ static uint64_t mlp_param(const mat *x, int s, int p)
 
 /* ---- Transformer (GPT-2 shaped decoder, Megatron tensor parallelism) --- */
 typedef struct {
-    int64_t m, T, s, d, dH, aH, FH, Vh, e;
+    int64_t m, T, s, d, dH, aH, hd, FH, Vh, e;
     int64_t ACT, QKV, OH, S2, FF, LOG, ST, IDS;
 } tfdims;
 
@@ -1170,6 +1201,7 @@ static void tf_dims(const mat *x, int k, tfdims *t)
     t->d = M->d_model;
     t->dH = M->d_model / x->H;
     t->aH = M->n_heads / x->H;
+    t->hd = M->d_model / M->n_heads;   /* one head's width */
     t->FH = M->d_ff / x->H;
     t->Vh = (M->vocab + x->H - 1) / x->H;
     t->ACT = t->e * t->T * t->d;
@@ -1265,24 +1297,24 @@ static void tf_layer(mat *x, int s, int k, int li, const tfdims *tp, int32_t *cu
     store_sv(x, s, k, base + L_X, cur);
     emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), cur, NULL, NULL, (uint64_t)t.ACT, y1, 0, NULL);
     use_weight(x, s, 4 * li + 0, w);
-    emit_local(x, s, T_QKV, (double)(2 * t.T * t.d * 3 * t.dH),
+    emit_mm(x, s, T_QKV, t.d, (double)(2 * t.T * t.d * 3 * t.dH),
                (double)(t.e * (t.T * t.d + t.d * 3 * t.dH + t.T * 3 * t.dH)),
                y1, w, NULL, (uint64_t)t.QKV, qkv, 0, NULL);
-    emit_local(x, s, T_SCORES, (double)(2 * t.T * t.s * t.dH), (double)(2 * t.OH + t.S2),
+    emit_mm(x, s, T_SCORES, t.hd, (double)(2 * t.T * t.s * t.dH), (double)(2 * t.OH + t.S2),
                qkv, NULL, NULL, (uint64_t)t.S2, S, 0, NULL);
     emit_local(x, s, T_SOFTMAX, (double)(5 * t.m * t.aH * t.s * t.s), (double)(2 * t.S2),
                S, NULL, NULL, (uint64_t)t.S2, pm, 0, NULL);
-    emit_local(x, s, T_AV, (double)(2 * t.T * t.s * t.dH), (double)(t.S2 + 2 * t.OH),
+    emit_mm(x, s, T_AV, t.s, (double)(2 * t.T * t.s * t.dH), (double)(t.S2 + 2 * t.OH),
                pm, qkv, NULL, (uint64_t)t.OH, o, 0, NULL);
     use_weight(x, s, 4 * li + 1, w);
-    emit_local(x, s, T_OUTPROJ, (double)(2 * t.T * t.dH * t.d),
+    emit_mm(x, s, T_OUTPROJ, t.dH, (double)(2 * t.T * t.dH * t.d),
                (double)(t.e * (t.T * t.dH + t.dH * t.d + t.T * t.d)),
                o, w, NULL, (uint64_t)t.ACT, z, 0, NULL);
     emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, z);
     emit_local(x, s, T_RESADD, (double)(t.T * t.d), (double)(3 * t.ACT), cur, z, NULL, (uint64_t)t.ACT, x2, 0, NULL);
     emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), x2, NULL, NULL, (uint64_t)t.ACT, y2, 0, NULL);
     use_weight(x, s, 4 * li + 2, w);
-    emit_local(x, s, T_FC1, (double)(2 * t.T * t.d * t.FH),
+    emit_mm(x, s, T_FC1, t.d, (double)(2 * t.T * t.d * t.FH),
                (double)(t.e * (t.T * t.d + t.d * t.FH + t.T * t.FH)),
                y2, w, NULL, (uint64_t)t.FF, u, 0, NULL);
     emit_local(x, s, T_GELU, (double)(8 * t.T * t.FH), (double)(2 * t.FF), u, NULL, NULL, (uint64_t)t.FF, ge, 0, NULL);
@@ -1296,7 +1328,7 @@ static void tf_layer(mat *x, int s, int k, int li, const tfdims *tp, int32_t *cu
     store_sv(x, s, k, base + L_GE, ge);
     if (!full) return;
     use_weight(x, s, 4 * li + 3, w);
-    emit_local(x, s, T_FC2, (double)(2 * t.T * t.FH * t.d),
+    emit_mm(x, s, T_FC2, t.FH, (double)(2 * t.T * t.FH * t.d),
                (double)(t.e * (t.T * t.FH + t.FH * t.d + t.T * t.d)),
                ge, w, NULL, (uint64_t)t.ACT, v, 0, NULL);
     emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, v);
@@ -1328,7 +1360,7 @@ static void tf_fwd(mat *x, int s, int k)
         store_sv(x, s, k, F_XL, cur);
         emit_local(x, s, T_LN, (double)(8 * t.T * t.d), (double)(2 * t.ACT), cur, NULL, NULL, (uint64_t)t.ACT, yf, 0, NULL);
         use_weight(x, s, tf_slot_head(x), w);
-        emit_local(x, s, T_LMHEAD, (double)(2 * t.T * t.d * t.Vh),
+        emit_mm(x, s, T_LMHEAD, t.d, (double)(2 * t.T * t.d * t.Vh),
                    (double)(t.e * (t.T * t.d + t.d * t.Vh + t.T * t.Vh)),
                    yf, w, NULL, (uint64_t)t.LOG, lg, 0, NULL);
         store_sv(x, s, k, F_YF, yf);
@@ -1357,12 +1389,12 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_XENT_GRAD, (double)(2 * t.T * t.Vh), (double)(2 * t.LOG + t.ST + t.IDS),
                    lg, st, lab, (uint64_t)t.LOG, dl, 0, NULL);
         use_weight(x, s, tf_slot_head(x), w);
-        emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.d * t.Vh),
+        emit_mm(x, s, T_GEMMDX, t.Vh, (double)(2 * t.T * t.d * t.Vh),
                    (double)(t.e * (t.T * t.Vh + t.d * t.Vh + t.T * t.d)),
                    dl, w, NULL, (uint64_t)t.ACT, dy, 0, NULL);
         emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, dy);
         gather_sv(x, s, k, F_YF, yf);
-        emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.d * t.Vh),
+        emit_mm(x, s, T_GEMMDW, t.T, (double)(2 * t.T * t.d * t.Vh),
                    (double)(t.e * (t.T * t.d + t.T * t.Vh + t.d * t.Vh)),
                    yf, dl, NULL, (uint64_t)(t.e * t.d * t.Vh), gw, 0, NULL);
         accumulate(x, s, k, tf_slot_head(x), (uint64_t)(t.d * t.Vh), gw);
@@ -1383,11 +1415,11 @@ static void tf_bwd(mat *x, int s, int k)
     for (i = x->l0[s + 1] - 1; i >= x->l0[s]; i--) {
         int li = i - x->l0[s], base = F_LAYER0 + li * NLF;
         use_weight(x, s, 4 * li + 3, w);
-        emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.FH * t.d),
+        emit_mm(x, s, T_GEMMDX, t.d, (double)(2 * t.T * t.FH * t.d),
                    (double)(t.e * (t.T * t.d + t.FH * t.d + t.T * t.FH)),
                    cur, w, NULL, (uint64_t)t.FF, dg, 0, NULL);
         gather_sv(x, s, k, base + L_GE, a1);
-        emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.FH * t.d),
+        emit_mm(x, s, T_GEMMDW, t.T, (double)(2 * t.T * t.FH * t.d),
                    (double)(t.e * (t.T * t.FH + t.T * t.d + t.FH * t.d)),
                    a1, cur, NULL, (uint64_t)(t.e * t.FH * t.d), gw, 0, NULL);
         accumulate(x, s, k, 4 * li + 3, (uint64_t)(t.FH * t.d), gw);
@@ -1395,12 +1427,12 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_GELU_B, (double)(8 * t.T * t.FH), (double)(3 * t.FF),
                    dg, a1, NULL, (uint64_t)t.FF, du, 0, NULL);
         use_weight(x, s, 4 * li + 2, w);
-        emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.d * t.FH),
+        emit_mm(x, s, T_GEMMDX, t.FH, (double)(2 * t.T * t.d * t.FH),
                    (double)(t.e * (t.T * t.FH + t.d * t.FH + t.T * t.d)),
                    du, w, NULL, (uint64_t)t.ACT, dy, 0, NULL);
         emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, dy);
         gather_sv(x, s, k, base + L_Y2, a1);
-        emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.d * t.FH),
+        emit_mm(x, s, T_GEMMDW, t.T, (double)(2 * t.T * t.d * t.FH),
                    (double)(t.e * (t.T * t.d + t.T * t.FH + t.d * t.FH)),
                    a1, du, NULL, (uint64_t)(t.e * t.d * t.FH), gw, 0, NULL);
         accumulate(x, s, k, 4 * li + 2, (uint64_t)(t.d * t.FH), gw);
@@ -1410,29 +1442,29 @@ static void tf_bwd(mat *x, int s, int k)
         emit_local(x, s, T_RESADD_B, (double)(t.T * t.d), (double)(3 * t.ACT),
                    cur, dxa, NULL, (uint64_t)t.ACT, dx2, 0, NULL);
         use_weight(x, s, 4 * li + 1, w);
-        emit_local(x, s, T_GEMMDX, (double)(2 * t.T * t.dH * t.d),
+        emit_mm(x, s, T_GEMMDX, t.d, (double)(2 * t.T * t.dH * t.d),
                    (double)(t.e * (t.T * t.d + t.dH * t.d + t.T * t.dH)),
                    dx2, w, NULL, (uint64_t)t.OH, dO, 0, NULL);
         gather_sv(x, s, k, base + L_O, a1);
-        emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.dH * t.d),
+        emit_mm(x, s, T_GEMMDW, t.T, (double)(2 * t.T * t.dH * t.d),
                    (double)(t.e * (t.T * t.dH + t.T * t.d + t.dH * t.d)),
                    a1, dx2, NULL, (uint64_t)(t.e * t.dH * t.d), gw, 0, NULL);
         accumulate(x, s, k, 4 * li + 1, (uint64_t)(t.dH * t.d), gw);
         gather_sv(x, s, k, base + L_PM, a1);
         gather_sv(x, s, k, base + L_QKV, a2);
-        emit_local(x, s, T_AV_B, (double)(4 * t.T * t.s * t.dH), (double)(2 * t.S2 + 3 * t.OH),
+        emit_mm(x, s, T_AV_B, t.hd + t.s, (double)(4 * t.T * t.s * t.dH), (double)(2 * t.S2 + 3 * t.OH),
                    dO, a1, a2, (uint64_t)t.S2, dP, (uint64_t)t.QKV, dq);
         emit_local(x, s, T_SOFTMAX_B, (double)(5 * t.m * t.aH * t.s * t.s), (double)(3 * t.S2),
                    dP, a1, NULL, (uint64_t)t.S2, dS, 0, NULL);
-        emit_local(x, s, T_SCORES_B, (double)(4 * t.T * t.s * t.dH), (double)(t.S2 + 4 * t.OH),
+        emit_mm(x, s, T_SCORES_B, 2 * t.s, (double)(4 * t.T * t.s * t.dH), (double)(t.S2 + 4 * t.OH),
                    dS, a2, dq, 0, NULL, 0, NULL);
         use_weight(x, s, 4 * li + 0, w);
-        emit_local(x, s, T_GEMMDX, (double)(2 * t.T * 3 * t.dH * t.d),
+        emit_mm(x, s, T_GEMMDX, 3 * t.dH, (double)(2 * t.T * 3 * t.dH * t.d),
                    (double)(t.e * (t.T * 3 * t.dH + 3 * t.dH * t.d + t.T * t.d)),
                    dq, w, NULL, (uint64_t)t.ACT, dy, 0, NULL);
         emit_ar_tp(x, s, T_AR_TP, (double)t.ACT, dy);
         gather_sv(x, s, k, base + L_Y1, a1);
-        emit_local(x, s, T_GEMMDW, (double)(2 * t.T * t.d * 3 * t.dH),
+        emit_mm(x, s, T_GEMMDW, t.T, (double)(2 * t.T * t.d * 3 * t.dH),
                    (double)(t.e * (t.T * t.d + t.T * 3 * t.dH + t.d * 3 * t.dH)),
                    a1, dq, NULL, (uint64_t)(t.e * t.d * 3 * t.dH), gw, 0, NULL);
         accumulate(x, s, k, 4 * li + 0, (uint64_t)(t.d * 3 * t.dH), gw);
@@ -1842,12 +1874,13 @@ static int sim_strategy(const or_model *M, int D, int H, int P, int K,
     if (g.failed) { rc = -3; goto out; }
     if (by_type) {
         /* per-type totals of the materialised ops: flops at [type], bytes
-         * at [T_NTYPES + type] */
+         * at [T_NTYPES + type], reduction lengths at [2 T_NTYPES + type] */
         int64_t i;
-        for (i = 0; i < 2 * T_NTYPES; i++) by_type[i] = 0.0;
+        for (i = 0; i < 3 * T_NTYPES; i++) by_type[i] = 0.0;
         for (i = 0; i < g.n_ops; i++) {
             by_type[g.type[i]] += g.flops[i];
             by_type[T_NTYPES + g.type[i]] += g.bytes[i];
+            by_type[2 * T_NTYPES + g.type[i]] += g.kred[i];
         }
     }
     rc = prog_simulate(&g, n_dev, dm, type_cost, fin, pk, dev_resident, NULL, NULL);
@@ -1883,7 +1916,8 @@ out:
     return rc;
 }
 
-/* Single strategy with every diagnostic output (tests). */
+/* Single strategy with every diagnostic output (tests).  by_type (optional):
+ * 3 * T_NTYPES per-type totals -- flops, bytes, reduction lengths. */
 int or_sim_strategy(const or_model *M, int D, int H, int P, int K,
                     const or_device_model *dm, int slice, const double *type_cost,
                     double *stage_finish, uint64_t *stage_peak,
@@ -2016,7 +2050,7 @@ static void *job_run(void *arg)
         for (i = J->lo; i < J->hi; i++) {
             int rc = or_gen_table(J->seed, J->cands[i], J->n_ops, J->n_dev, code, fl, by, al, fr, 1);
             if (rc) { J->rc = rc; break; }
-            or_sim_table(J->n_ops, J->n_dev, code, fl, by, al, fr, 1, NULL, J->dm,
+            or_sim_table(J->n_ops, J->n_dev, code, fl, by, al, fr, NULL, 1, NULL, J->dm,
                          &J->makespan[i], J->finish ? &J->finish[i * J->n_dev] : NULL,
                          J->peak ? &J->peak[i * J->n_dev] : NULL, &J->cand_peak[i], &J->status[i]);
             if (J->nops) J->nops[i] = (uint64_t)J->n_ops;

@@ -24,9 +24,9 @@ works in place, and a tensor whose last reader is an AllReduce stays live
 to the end; a parameter marked keep is never freed.  Costs: elementwise ops
 1 flop per output element (Gelu 8, Softmax 5, LayerNormalization 8, Cast 0),
 MatMul 2 * (output elements) * k, Gemm the same plus one per output element
-with a bias, Transpose / Concat / Split / Gather no flops; bytes = every
-abstract input and output tensor's size; Send and AllReduce move one input's
-bytes.
+with a bias (k, the reduction length, also enters the empirical MatMul
+cost), Transpose / Concat / Split / Gather no flops; bytes = every abstract
+input and output tensor's size; Send and AllReduce move one input's bytes.
 """
 import re
 
@@ -402,11 +402,13 @@ def program(text, inputs=None):
         dev = [r for r in res if is_t(r)][0][3]
         moved = sum(tbytes(v) for v in a if is_t(v)) + sum(tbytes(r) for r in res if is_t(r))
         out0 = res[0]
+        kred = 0
         if name == "MatMul":
-            flops = 2 * n_elems(out0[2]) * a[0][2][-1]
+            kred = a[0][2][-1]
+            flops = 2 * n_elems(out0[2]) * kred
         elif name == "Gemm":
-            k = a[0][2][0] if attrs.get("transA", 0) else a[0][2][1]
-            flops = 2 * n_elems(out0[2]) * k + (n_elems(out0[2]) if len(a) == 3 else 0)
+            kred = a[0][2][0] if attrs.get("transA", 0) else a[0][2][1]
+            flops = 2 * n_elems(out0[2]) * kred + (n_elems(out0[2]) if len(a) == 3 else 0)
         elif name in FLOPS_PER_ELEM:
             flops = FLOPS_PER_ELEM[name] * n_elems(out0[2])
         else:
@@ -418,7 +420,7 @@ def program(text, inputs=None):
                 tensors.append([r[3], tbytes(r), 0])
                 new.append(tid[o])
         prog.append(dict(kind=oracle.COMPUTE, devs=[dev], ins=t_in, outs=new, flops=float(flops),
-                         bytes=float(moved), matmul=name in ("MatMul", "Gemm")))
+                         bytes=float(moved), matmul=name in ("MatMul", "Gemm"), k=float(kred)))
     # a tensor whose last reader is an all-reduce stays live (in place)
     last = {}
     for i, op in enumerate(prog):

@@ -43,14 +43,14 @@ int main(void)
         int32_t st;
         or_device_model m = dev(i > 4, 0);
         if (or_gen_table(7, i, n, i, code, fl, by, al, fr, 1)) fails++;
-        or_sim_table(n, i, code, fl, by, al, fr, 1, init, &m, &mk, fin, pk, &cp, &st);
+        or_sim_table(n, i, code, fl, by, al, fr, NULL, 1, init, &m, &mk, fin, pk, &cp, &st);
         /* the same table with garbage records and frees too large */
         {
             int j;
             for (j = 0; j < n; j += 7) code[j] = (uint32_t)or_splitmix64(9, (uint64_t)j);
             for (j = 3; j < n; j += 11) fr[j] = 0xffffffffu;
             for (j = 5; j < n; j += 13) by[j] = -1.0f;
-            or_sim_table(n, i, code, fl, by, al, fr, 1, init, &m, &mk, fin, pk, &cp, &st);
+            or_sim_table(n, i, code, fl, by, al, fr, NULL, 1, init, &m, &mk, fin, pk, &cp, &st);
         }
     }
     /* every family, mode and variant over valid, invalid and uneven strategies */
@@ -67,7 +67,7 @@ int main(void)
                         for (sl = 0; sl <= 1; sl++) {
                             double sf[16], dfin[256];
                             uint64_t sp[16], dpk[256], dres[256], cp, no;
-                            double by_type[2 * T_NTYPES], mk;
+                            double by_type[3 * T_NTYPES], mk;
                             int32_t st;
                             int rc = or_sim_strategy(&M, S[s][0], S[s][1], S[s][2], S[s][3], &m, sl, NULL, sf, sp,
                                                      dfin, dpk, dres, by_type, &mk, &cp, &no, &st);

@@ -1009,7 +1009,9 @@ def table_brute(tab, n_dev, dev, init=None):
     live = list(init) if init is not None else [0] * n_dev
     peak = list(live)
     st = 0
-    for c, fl, by, al, fr in zip(tab["code"], tab["flops"], tab["bytes"], tab["alloc"], tab["free"]):
+    mmk = tab.get("mm_k")
+    mmk = [0] * len(tab["code"]) if mmk is None else mmk
+    for c, fl, by, al, fr, kk in zip(tab["code"], tab["flops"], tab["bytes"], tab["alloc"], tab["free"], mmk):
         c = int(c)
         k, a, b, cls = c & 255, (c >> 8) & 255, (c >> 16) & 255, c >> 24
         fin = lambda x: math.isfinite(float(x)) and float(x) >= 0 and not math.copysign(1.0, float(x)) < 0
@@ -1022,8 +1024,8 @@ def table_brute(tab, n_dev, dev, init=None):
                 continue
             devs = [a]
             if cls == 1 and dev.matmul is not None:
-                c0, c1, c2 = dev.matmul
-                cost = (c0 + c1 * float(fl)) + c2 * float(by)
+                c0, c1, c2, c3, floor = (tuple(dev.matmul) + (0.0, 0.0))[:5]
+                cost = max(floor, ((c0 + c1 * float(fl)) + c2 * float(by)) + c3 * float(kk))
             else:
                 x, y = float(fl) * inv(dev.flops_per_s), float(by) * inv(dev.mem_bytes_per_s)
                 cost = dev.launch_s + max(x, y)
@@ -1216,6 +1218,97 @@ def test_matmul_count_on_one_device(orc, case):
     a = orc.sim_strategy(m, 1, 1, 1, 1, replace(dev, matmul=(2.0 ** -12, 2.0 ** -42, 2.0 ** -38)))
     b = orc.sim_strategy(m, 1, 1, 1, 1, replace(dev, matmul=(2.0 ** -12 + d, 2.0 ** -42, 2.0 ** -38)))
     assert b["makespan"] - a["makespan"] == n_mm * d
+
+
+def _mlp_k_by_hand(L, d, B, H, train):
+    """Reduction lengths of an MLP's products on one stage, K = 1, summed over
+    the H tensor ranks, from the shapes: the Gemm X (B x din) . W (din x dout)
+    reduces over din, its weight gradient X^T dY over the B rows, its input
+    gradient dY W^T over dout; with H > 1 even layers are column-parallel
+    (din = d, dout = d/H) and odd ones row-parallel (din = d/H, dout = d)."""
+    k = {"GEMM": 0, "GEMMDW": 0, "GEMMDX": 0}
+    for i in range(L):
+        col, row = H > 1 and i % 2 == 0, H > 1 and i % 2 == 1
+        din, dout = (d // H if row else d), (d // H if col else d)
+        k["GEMM"] += H * din
+        if train:
+            k["GEMMDW"] += H * B
+            k["GEMMDX"] += H * dout
+    return {t: v for t, v in k.items() if v}
+
+
+@pytest.mark.parametrize("L, d, B, H, train", [(3, 64, 32, 1, True), (4, 64, 48, 2, True), (2, 96, 8, 4, True),
+                                               (5, 32, 16, 1, False), (4, 128, 8, 2, False)])
+def test_mlp_matmul_reduction_lengths(orc, L, d, B, H, train):
+    m = mlp(L, d, B, 4, TRAIN_SGD if train else INFER)
+    r = orc.sim_strategy(m, 1, H, 1, 1, DEV)
+    got = {t: v for t, v in r["k_by_type"].items() if v}
+    assert got == _mlp_k_by_hand(L, d, B, H, train)
+
+
+# a device on which only matrix multiplications take time: every other op's
+# cost is below 2^-900 s and vanishes when added to a clock of a second or more
+NEAR_FREE = DeviceSpec(2.0 ** 1000, 2.0 ** 1000, 2.0 ** 1000, 0.0, 0.0, 0)
+
+
+@pytest.mark.parametrize("m", [mlp(3, 64, 32, 4, TRAIN_SGD), mlp(4, 64, 48, 2, INFER),
+                               transformer(2, 32, 4, 8, 64, 4, 2, TRAIN_ADAM), transformer(3, 48, 6, 16, 50, 2, 2, INFER)],
+                         ids=["mlp_train", "mlp_infer", "gpt_train", "gpt_infer"])
+def test_matmul_reduction_term_and_floor_on_one_device(orc, m):
+    """On one device, with every other op free: regression (0, 0, 0, 1, 0)
+    makes each product cost its reduction length in seconds, so the
+    makespan is the sum of k over the program; a floor above every product's
+    k makes each cost the floor, so the makespan is (number of products) *
+    floor; a floor below every k changes nothing."""
+    r = orc.sim_strategy(m, 1, 1, 1, 1, replace(NEAR_FREE, matmul=(0.0, 0.0, 0.0, 1.0, 0.0)))
+    ks = r["k_by_type"]
+    total_k = sum(ks.values())
+    assert total_k > 0 and r["makespan"] == total_k
+    # count the products: raise c0 by one second on a floor-free regression
+    a = orc.sim_strategy(m, 1, 1, 1, 1, replace(NEAR_FREE, matmul=(1.0, 0.0, 0.0, 0.0, 0.0)))
+    n_mm = a["makespan"]
+    assert n_mm == int(n_mm) and n_mm >= 3
+    big = 2.0 ** 40
+    f = orc.sim_strategy(m, 1, 1, 1, 1, replace(NEAR_FREE, matmul=(0.0, 0.0, 0.0, 1.0, big)))
+    assert f["makespan"] == n_mm * big
+    low = orc.sim_strategy(m, 1, 1, 1, 1, replace(NEAR_FREE, matmul=(0.0, 0.0, 0.0, 1.0, 0.5)))
+    assert low["makespan"] == total_k
+
+
+def test_matmul_regression_with_reduction_term(orc):
+    """The cost of a product with reduction length k: the linear form plus
+    c3 * k, never below the floor; c3 = floor = 0 is the linear form
+    itself (power-of-two coefficients keep every sum exact)."""
+    c = (2.0 ** -17, 2.0 ** -50, 2.0 ** -40, 2.0 ** -30, 2.0 ** -15)
+    dev = replace(DEV, matmul=c)
+    lin = replace(DEV, matmul=c[:3])
+    for fl, by, k in ((2.0 ** 20, 2.0 ** 10, 0), (2.0 ** 34, 2.0 ** 26, 2.0 ** 12), (2.0 ** 40, 2.0 ** 30, 2.0 ** 16)):
+        base = orc.cost(lin, orc.COMPUTE, fl, by, 1, type="GEMM", k=k)
+        assert base == c[0] + fl * c[1] + by * c[2]            # k plays no part in the linear form
+        got = orc.cost(dev, orc.COMPUTE, fl, by, 1, type="GEMM", k=k)
+        assert got == max(c[4], base + k * c[3])
+        assert orc.cost(dev, orc.COMPUTE, fl, by, 1, type="RELU", k=k) == orc.cost(DEV, orc.COMPUTE, fl, by, 1)
+    # the floor binds for a small product and not for a large one
+    assert orc.cost(dev, orc.COMPUTE, 2.0 ** 20, 2.0 ** 10, 1, type="GEMM", k=64) == c[4]
+    assert orc.cost(dev, orc.COMPUTE, 2.0 ** 40, 2.0 ** 30, 1, type="GEMM", k=2.0 ** 16) > c[4]
+
+
+def test_table_matmul_reduction_lengths(orc):
+    """Class-1 table records take their reduction length from mm_k (absent:
+    0): by hand on a three-record table with power-of-two coefficients."""
+    c = (2.0 ** -17, 2.0 ** -50, 2.0 ** -40, 2.0 ** -30, 2.0 ** -16)
+    tab = dict(code=np.array([0 | 1 << 24, 0 | 1 << 24, 0 | 1 << 8 | 1 << 24], np.uint32),
+               flops=np.array([2.0 ** 34, 2.0 ** 34, 2.0 ** 20], np.float32),
+               bytes=np.array([2.0 ** 26, 2.0 ** 26, 2.0 ** 10], np.float32),
+               alloc=np.zeros(3, np.uint32), free=np.zeros(3, np.uint32),
+               mm_k=np.array([2 ** 12, 0, 7], np.uint32))
+    r = orc.sim_table(tab, 2, replace(DEV, matmul=c))
+    lin = 2.0 ** -17 + 2.0 ** -16 + 2.0 ** -14               # c0 + c1 * 2^34 + c2 * 2^26
+    assert r["status"] == 0
+    assert r["finish"][0] == (lin + 2.0 ** -18) + lin          # k = 4096, then k = 0
+    assert r["finish"][1] == 2.0 ** -16                        # the floor: k = 7 on a small product
+    no_k = orc.sim_table({k: v for k, v in tab.items() if k != "mm_k"}, 2, replace(DEV, matmul=c))
+    assert no_k["finish"][0] == lin + lin
 
 
 def test_table_matmul_class(orc):

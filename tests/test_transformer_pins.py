@@ -31,6 +31,7 @@ class Prog:
         self.initial = []     # live at t = 0
         self.ops = []         # (type, reads [(tensor, bytes read)], writes [(tensor, bytes written, new)])
         self.flops = {}       # matrix-product flops by type
+        self.kred = {}        # reduction lengths of the products by type
 
     def tensor(self, name, nbytes, keep=False, initial=False):
         self.size[name] = nbytes
@@ -54,11 +55,14 @@ class Prog:
                 w.append((t[0], t[1], len(t) > 2 and t[2]))
         self.ops.append((typ, r, w))
 
-    def mm(self, typ, M, Kd, N, reads, writes, count=1):
+    def mm(self, typ, M, Kd, N, reads, writes, count=1, ks=None):
         """A matrix product (M x Kd) . (Kd x N), `count` of them: 2*M*Kd*N
-        flops each."""
+        flops each.  ks: the reduction length of each distinct product the
+        op performs (default: the one product's Kd); the op's k is their
+        sum."""
         self.op(typ, reads, writes)
         self.flops[typ] = self.flops.get(typ, 0) + count * 2 * M * Kd * N
+        self.kred[typ] = self.kred.get(typ, 0) + sum(ks if ks is not None else (Kd,))
 
     def bytes_by_type(self):
         out = {}
@@ -172,10 +176,10 @@ def gpt_rank_program(L, d, a, s, V, F, B, e, H, train):
         p.mm("GEMMDW", dH, T, d, [n("o"), n("dx2")], [n("dWo")])
         # dP, and dV into a gradient buffer of Q, K and V allocated here
         p.mm("AV_B", s, d // a, s, [n("do"), n("p"), (n("qkv"), oh)], [n("dp"), (n("dqkv"), oh, True)],
-             count=2 * B * aH)   # dP = dO V^T and dV = P^T dO, per head
+             count=2 * B * aH, ks=(d // a, s))   # dP = dO V^T (over a head's width), dV = P^T dO (over s)
         p.op("SOFTMAX_B", [n("dp"), n("p")], [n("ds")])
         p.mm("SCORES_B", s, s, d // a, [n("ds"), (n("qkv"), 2 * oh)], [(n("dqkv"), 2 * oh)],
-             count=2 * B * aH)   # dQ = dS K and dK = dS^T Q in place, per head
+             count=2 * B * aH, ks=(s, s))   # dQ = dS K and dK = dS^T Q in place, per head, both over s
         p.mm("GEMMDX", T, 3 * dH, d, [n("dqkv"), n("Wqkv")], [n("dy1")])
         ar(n("dy1"))
         p.mm("GEMMDW", d, T, 3 * dH, [n("y1"), n("dqkv")], [n("dWqkv")])
@@ -220,6 +224,21 @@ def test_matmul_flops_of_every_type(orc, case, train):
     r = orc.sim_strategy(m, 1, H, 1, 1, DEV)
     for typ, v in hand.items():
         assert r["flops_by_type"][typ] == H * v, typ
+
+
+@pytest.mark.parametrize("train", [False, True], ids=["infer", "train"])
+@pytest.mark.parametrize("case", CASES, ids=["L%d_d%d_a%d_s%d_V%d_F%d_B%d_e%d_H%d" % c for c in CASES])
+def test_matmul_reduction_lengths_of_every_type(orc, case, train):
+    """The reduction length k of every product (the inner dimension of its
+    operands' shapes), summed per op type: the oracle's products carry the
+    k the empirical MatMul cost reads.  An op that stands for two products
+    (the attention gradients) carries the sum of theirs."""
+    L, d, a, s, V, F, B, e, H = case
+    hand = gpt_rank_program(L, d, a, s, V, F, B, e, H, train).kred
+    m = transformer(L, d, a, s, V, B, e, TRAIN_SGD if train else INFER, d_ff=F)
+    r = orc.sim_strategy(m, 1, H, 1, 1, DEV)
+    got = {k: v for k, v in r["k_by_type"].items() if v}
+    assert got == {k: H * v for k, v in hand.items()}
 
 
 @pytest.mark.parametrize("train", [False, True], ids=["infer", "train"])
