@@ -322,7 +322,7 @@ def bench_lowered_programs(torch, dsim, reps):
         host[th] = best
     n = len(cases)
     g = {k: torch.from_numpy(np.ascontiguousarray(p[k]).view(np.int32 if p[k].dtype == np.uint32 else p[k].dtype)).cuda()
-         for k in ("code", "flops", "bytes", "alloc", "free", "n_ops")}
+         for k in ("code", "flops", "bytes", "alloc", "free", "mm_k", "n_ops")}
     init = torch.from_numpy(p["init_live"].view(np.int64)).cuda()
     res = dsim.alloc_results(n, 8)
     dev = DeviceSpec()

@@ -87,13 +87,17 @@ DSIM_API const char *dsim_last_error(void);
  * over a single device costs 0 whatever its bytes.  mem_cap_bytes = 0 means
  * no cap; otherwise candidates whose peak exceeds it get DSIM_ST_OVER_CAP.
  * mm_enabled = 1 gives matrix multiplications the empirical cost of Sec. 4
- * (a linear regression in the input sizes, fitted on single-op
- * microbenchmarks): (mm_c0 + mm_c1 * flops) + mm_c2 * bytes, coefficients
- * finite and >= 0.  The transform's matrix multiplications are the dense
- * layer's Gemm and its two gradients, the transformer's QKV, output, fc1,
- * fc2 and LM-head products, the attention score and P.V products, and
- * their gradients; in explicit tables, compute records of cost class 1.
- * mm_enabled = 0: every compute op takes the roofline.
+ * (a regression in the input sizes, fitted on single-op microbenchmarks):
+ *   max(mm_floor, ((mm_c0 + mm_c1 * flops) + mm_c2 * bytes) + mm_c3 * k)
+ * with k the product's reduction length (the operands' inner dimension;
+ * an op standing for two products, the attention gradients, has the sum of
+ * theirs) and every coefficient finite and >= 0.  mm_c3 = mm_floor = 0 is
+ * the paper's linear form.  The transform's matrix multiplications are the
+ * dense layer's Gemm and its two gradients, the transformer's QKV, output,
+ * fc1, fc2 and LM-head products, the attention score and P.V products, and
+ * their gradients; in explicit tables, compute records of cost class 1,
+ * whose k comes from dsim_tables.mm_k.  mm_enabled = 0: every compute op
+ * takes the roofline (mm_* ignored).
  * node_size > 0 makes the interconnect two-tier: device d lies in node
  * d / node_size, and a send or collective whose devices lie in more than one
  * node crosses the network (net_bytes_per_s > 0 with a finite reciprocal,
@@ -116,6 +120,7 @@ typedef struct {
     double net_bytes_per_s, net_latency_s;
     int32_t streams_per_gpu;
     double stream_bytes_per_s, stream_latency_s;
+    double mm_c3, mm_floor;   /* the MatMul cost's reduction-length term and floor */
 } dsim_device_model;
 
 /* The sequential program the transform distributes (Sec. 4, Sec. 5):
@@ -255,6 +260,8 @@ DSIM_API dsim_status dsim_create_grid(const dsim_model *model, const dsim_grid_s
  *          below 2^64; candidates starting at 2^62 or more on some device
  *          take a slower exact path (same results).
  *   n_dev: 1..8.
+ *   mm_k:  per record, the reduction length of a class-1 record (ignored
+ *          on every other record); NULL = 0 for all.
  * An invalid op is skipped (no time, no memory) and flagged in status.
  */
 typedef struct {
@@ -264,6 +271,7 @@ typedef struct {
     const uint32_t *n_ops;
     const uint64_t *init_live;
     int32_t max_ops, n_dev;
+    const uint32_t *mm_k;
 } dsim_tables;
 
 /*
@@ -390,20 +398,24 @@ DSIM_API dsim_status dsim_simulate_parametric_static(const dsim_model *model, co
  * (alloc on b, free on a), all-reduce over a device mask.
  *   code, flops, bytes, alloc_bytes, free_bytes: device arrays of
  *     max_ops * n_cand records, written for j < n_ops[c];
+ *   mm_k:      device array of max_ops * n_cand entries or NULL: each
+ *     record's reduction length (that of its matrix multiplication, 0 on
+ *     other records), for dsim_tables.mm_k;
  *   n_ops:     device array [n_cand], the program's op count (0 on error);
  *   init_live: device array [n_cand * n_dev], bytes resident on each device
  *     at t = 0 (0 for devices the candidate does not use);
  *   status:    device array [n_cand]: 0, DSIM_ST_BAD_STRATEGY (the
  *     transform's preconditions fail, more devices than n_dev (D*H*P, twice that with overlap) or K > 16383), or
  *     DSIM_ST_NOT_TABLE (more than max_ops ops, a FLOP or byte count not
- *     exact in fp32, or an alloc / free size above 2^32 - 1).
+ *     exact in fp32, or an alloc / free size or a reduction length above
+ *     2^32 - 1).
  * 1 <= n_dev <= 8, max_ops >= 0, n_cand <= 2^32 - 256.  One GPU lane per
  * candidate.
  */
 DSIM_API dsim_status dsim_materialize_tables(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
                                     int32_t max_ops, int32_t n_dev, uint32_t *code, float *flops,
                                     float *bytes, uint32_t *alloc_bytes, uint32_t *free_bytes,
-                                    uint32_t *n_ops, uint64_t *init_live, int32_t *status,
+                                    uint32_t *mm_k, uint32_t *n_ops, uint64_t *init_live, int32_t *status,
                                     void *hip_stream);
 
 /*
@@ -521,9 +533,13 @@ DSIM_API dsim_status dsim_interpret_program(const char *program, const char *inp
  *   code, flops, bytes, alloc_bytes, free_bytes: host arrays of
  *     max_ops * n_prog records, op-major and program-fastest (record j of
  *     program c at j * n_prog + c); rows from n_ops[c] on are zero.
+ *   mm_k: host array of max_ops * n_prog entries, or NULL: each record's
+ *     reduction length (MatMul: its left operand's last dimension; Gemm:
+ *     the shared dimension; 0 on other records), for dsim_tables.mm_k;
+ *     a length of 2^32 or more is DSIM_ERANGE.
  *   n_ops: host array [n_prog]; init_live: host array [n_prog * n_dev].
- *     All seven arrays NULL: nothing is written and max_ops is not
- *     checked (a sizing pass).
+ *     All seven arrays (and mm_k) NULL: nothing is written and max_ops is
+ *     not checked (a sizing pass).
  *   max_ops_used, n_dev_used (may be NULL): the largest record count of any
  *     program, and 1 + the highest device any program uses.
  *   n_threads: host threads to use (<= 1: the calling thread only).
@@ -540,8 +556,8 @@ DSIM_API dsim_status dsim_interpret_program(const char *program, const char *inp
 DSIM_API dsim_status dsim_lower_programs(const char *const *programs, const char *const *inputs, int64_t n_prog,
                                          int32_t n_dev, int32_t max_ops, uint32_t *code, float *flops,
                                          float *bytes, uint32_t *alloc_bytes, uint32_t *free_bytes,
-                                         uint32_t *n_ops, uint64_t *init_live, int32_t *max_ops_used,
-                                         int32_t *n_dev_used, int32_t n_threads);
+                                         uint32_t *mm_k, uint32_t *n_ops, uint64_t *init_live,
+                                         int32_t *max_ops_used, int32_t *n_dev_used, int32_t n_threads);
 
 #ifdef __cplusplus
 }

@@ -43,6 +43,8 @@ CostConsts make_consts(const dsim_device_model &m)
     c.mm_c0 = m.mm_enabled ? m.mm_c0 : 0.0;
     c.mm_c1 = m.mm_enabled ? m.mm_c1 : 0.0;
     c.mm_c2 = m.mm_enabled ? m.mm_c2 : 0.0;
+    c.mm_c3 = m.mm_enabled ? m.mm_c3 : 0.0;
+    c.mm_floor = m.mm_enabled ? m.mm_floor : 0.0;
     c.node = m.node_size > 0 ? m.node_size : 0;
     c.net_lat = c.node ? m.net_latency_s : 0.0;
     c.net_inv_l = c.node ? 1.0 / m.net_bytes_per_s : 0.0;
@@ -75,7 +77,8 @@ static dsim_status check_device(const dsim_device_model *m)
     if (!finite_nonneg(m->link_latency_s) || !finite_nonneg(m->launch_s))
         return fail(DSIM_EINVAL, "latency and launch must be finite and >= 0");
     if (m->mm_enabled != 0 && m->mm_enabled != 1) return fail(DSIM_EINVAL, "mm_enabled must be 0 or 1");
-    if (m->mm_enabled && (!finite_nonneg(m->mm_c0) || !finite_nonneg(m->mm_c1) || !finite_nonneg(m->mm_c2)))
+    if (m->mm_enabled && (!finite_nonneg(m->mm_c0) || !finite_nonneg(m->mm_c1) || !finite_nonneg(m->mm_c2) ||
+                          !finite_nonneg(m->mm_c3) || !finite_nonneg(m->mm_floor)))
         return fail(DSIM_EINVAL, "MatMul regression coefficients must be finite and >= 0");
     if (m->node_size < 0) return fail(DSIM_EINVAL, "node_size must be >= 0");
     if (m->node_size > 0 && (!rate_ok(m->net_bytes_per_s) || !finite_nonneg(m->net_latency_s)))
@@ -304,7 +307,7 @@ dsim_status dsim_argmin(const double *makespan, const uint64_t *cand_peak, const
 
 dsim_status dsim_materialize_tables(const dsim_model *model, const dsim_strategy *cand, int64_t n_cand,
                                     int32_t max_ops, int32_t n_dev, uint32_t *code, float *flops, float *bytes,
-                                    uint32_t *alloc_bytes, uint32_t *free_bytes, uint32_t *n_ops,
+                                    uint32_t *alloc_bytes, uint32_t *free_bytes, uint32_t *mm_k, uint32_t *n_ops,
                                     uint64_t *init_live, int32_t *status, void *hip_stream)
 {
     dsim_status st = check_model(model);
@@ -318,7 +321,7 @@ dsim_status dsim_materialize_tables(const dsim_model *model, const dsim_strategy
     if (max_ops > 0 && (!code || !flops || !bytes || !alloc_bytes || !free_bytes))
         return fail(DSIM_EINVAL, "table buffers must not be NULL");
     return launch_materialize(*model, cand, n_cand, max_ops, n_dev, code, flops, bytes, alloc_bytes, free_bytes,
-                              n_ops, init_live, status, (hipStream_t)hip_stream);
+                              max_ops > 0 ? mm_k : nullptr, n_ops, init_live, status, (hipStream_t)hip_stream);
 }
 
 dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, int32_t n_ops, int32_t n_dev,

@@ -34,7 +34,9 @@
 // LayerNormalization 8, Cast 0), 2 * (output elements) * k for MatMul and
 // Gemm (plus one per output element for Gemm's bias), none for Transpose,
 // Concat, Split and Gather; Send and AllReduce move their (first) input's
-// bytes.
+// bytes.  A matrix product's record also carries its reduction length k
+// (MatMul: the left operand's last dimension; Gemm: the shared dimension),
+// which the empirical MatMul cost reads.
 #include <algorithm>
 #include <cerrno>
 #include <cmath>
@@ -1181,6 +1183,7 @@ struct Rec {
     uint8_t kind, cls;
     int32_t a, b;
     u128 flops, bytes;
+    uint64_t k;         // reduction length of a matrix multiplication
     int32_t off, n_created, n_read;
 };
 
@@ -1397,9 +1400,10 @@ struct Program {
     }
 
     void add_rec(int kind, int a, int b, int cls, u128 flops, u128 bytes, const int32_t *created, int nc,
-                 const int32_t *read, int nr)
+                 const int32_t *read, int nr, uint64_t k = 0)
     {
         Rec r;
+        r.k = k;
         r.kind = (uint8_t)kind;
         r.cls = (uint8_t)cls;
         r.a = a;
@@ -1479,6 +1483,7 @@ struct Program {
             if (is_t(r)) moved += nbytes(r);
         u128 flops = 0;
         int cls = 0;
+        uint64_t kred = 0;
         const Value &r0 = res[0];
         if (op == O_MATMUL || op == O_GEMM) {
             const Shape &sa = args[0]->shape;
@@ -1486,6 +1491,7 @@ struct Program {
             u128 m = (u128)(uint64_t)numel(r0.shape);
             flops = 2 * m * (u128)(uint64_t)k + (op == O_GEMM && n == 3 ? m : 0);
             cls = 1;
+            kred = (uint64_t)k;
         } else if (kEltFlops[op] >= 0) {
             flops = (u128)kEltFlops[op] * (u128)(uint64_t)numel(r0.shape);
         } else if (op != O_TRANSPOSE && op != O_CONCAT && op != O_SPLIT && op != O_GATHER) {
@@ -1505,7 +1511,7 @@ struct Program {
                 st_of[(size_t)(first_res + i)] = s;
                 cr[nc++] = s;
             }
-        add_rec(0, dev, 0, cls, flops, moved, cr, nc, rd, nr);
+        add_rec(0, dev, 0, cls, flops, moved, cr, nc, rd, nr, kred);
     }
 
     void statement(std::string_view l, bool mixed)
@@ -1638,7 +1644,7 @@ struct Program {
 
     // per-record frees, then the table columns (or nothing if code is NULL)
     void finish(int32_t max_ops, int64_t n_prog, int64_t c, uint32_t *code, float *flops, float *bytes,
-                uint32_t *alloc, uint32_t *freeb, uint64_t *init_live)
+                uint32_t *alloc, uint32_t *freeb, uint32_t *mm_k, uint64_t *init_live)
     {
         last.assign(st.size(), -1);
         for (size_t i = 0; i < recs.size(); ++i) {
@@ -1660,7 +1666,7 @@ struct Program {
                 if (r.kind == 1 && k < r.n_created) throw_fail(DSIM_EINVAL, "a received tensor nothing reads");
                 if (r.kind != 2) fr += st[(size_t)s].bytes;
             }
-            if (!exact_f32(r.flops) || !exact_f32(r.bytes) || (al >> 32) || (fr >> 32))
+            if (!exact_f32(r.flops) || !exact_f32(r.bytes) || (al >> 32) || (fr >> 32) || (r.k >> 32))
                 throw_fail(DSIM_ERANGE, "op %zu does not fit the table format exactly", i);
             if (!write) continue;
             size_t at = (size_t)i * (size_t)n_prog + (size_t)c;
@@ -1669,6 +1675,7 @@ struct Program {
             bytes[at] = (float)r.bytes;
             alloc[at] = (uint32_t)al;
             freeb[at] = (uint32_t)fr;
+            if (mm_k) mm_k[at] = (uint32_t)r.k;
         }
         if (!write) return;
         for (int64_t j = (int64_t)recs.size(); j < max_ops; ++j) {
@@ -1678,6 +1685,7 @@ struct Program {
             bytes[at] = 0.0f;
             alloc[at] = 0;
             freeb[at] = 0;
+            if (mm_k) mm_k[at] = 0;
         }
         for (int d = 0; d < n_dev; ++d) init_live[(size_t)c * (size_t)n_dev + (size_t)d] = init[d];
     }
@@ -1694,7 +1702,7 @@ struct Work {
 
 void lower_range(const char *const *programs, const char *const *inputs, int32_t n_dev, int32_t max_ops,
                  int64_t n_prog, uint32_t *code, float *flops, float *bytes, uint32_t *alloc, uint32_t *freeb,
-                 uint32_t *n_ops, uint64_t *init_live, Work &w)
+                 uint32_t *mm_k, uint32_t *n_ops, uint64_t *init_live, Work &w)
 {
     Program pr;
     pr.lowering = true;
@@ -1703,7 +1711,7 @@ void lower_range(const char *const *programs, const char *const *inputs, int32_t
         pr.reset();
         try {
             pr.run(programs[c], inputs && inputs[c] ? inputs[c] : "", true);
-            pr.finish(max_ops, n_prog, c, code, flops, bytes, alloc, freeb, init_live);
+            pr.finish(max_ops, n_prog, c, code, flops, bytes, alloc, freeb, mm_k, init_live);
         } catch (Failure &f) {
             w.failed = c;
             w.fail_info = f;
@@ -1753,8 +1761,8 @@ extern "C" DSIM_API dsim_status dsim_interpret_program(const char *program, cons
 extern "C" DSIM_API dsim_status dsim_lower_programs(const char *const *programs, const char *const *inputs,
                                                     int64_t n_prog, int32_t n_dev, int32_t max_ops,
                                                     uint32_t *code, float *flops, float *bytes,
-                                                    uint32_t *alloc_bytes, uint32_t *free_bytes, uint32_t *n_ops,
-                                                    uint64_t *init_live, int32_t *max_ops_used,
+                                                    uint32_t *alloc_bytes, uint32_t *free_bytes, uint32_t *mm_k,
+                                                    uint32_t *n_ops, uint64_t *init_live, int32_t *max_ops_used,
                                                     int32_t *n_dev_used, int32_t n_threads)
 {
     if (!programs && n_prog > 0) return fail(DSIM_EINVAL, "programs is NULL");
@@ -1765,6 +1773,7 @@ extern "C" DSIM_API dsim_status dsim_lower_programs(const char *const *programs,
                 (free_bytes != nullptr) + (n_ops != nullptr) + (init_live != nullptr);
     if (given != 0 && given != 7)
         return fail(DSIM_EINVAL, "give all of code, flops, bytes, alloc_bytes, free_bytes, n_ops and init_live, or none");
+    if (given == 0 && mm_k) return fail(DSIM_EINVAL, "mm_k without the other arrays");
     for (int64_t c = 0; c < n_prog; ++c)
         if (!programs[c]) return fail(DSIM_EINVAL, "program %lld is NULL", (long long)c);
     int64_t nt = std::max<int64_t>(1, std::min<int64_t>({(int64_t)n_threads, n_prog, 256}));
@@ -1774,8 +1783,8 @@ extern "C" DSIM_API dsim_status dsim_lower_programs(const char *const *programs,
         w[(size_t)t].hi = n_prog * (t + 1) / nt;
     }
     auto job = [&](int64_t t) {
-        lower_range(programs, inputs, n_dev, max_ops, n_prog, code, flops, bytes, alloc_bytes, free_bytes, n_ops,
-                    init_live, w[(size_t)t]);
+        lower_range(programs, inputs, n_dev, max_ops, n_prog, code, flops, bytes, alloc_bytes, free_bytes, mm_k,
+                    n_ops, init_live, w[(size_t)t]);
     };
     if (nt == 1) {
         job(0);

@@ -37,6 +37,7 @@ struct CostConsts {
     uint64_t cap;      // memory cap, 0 = none
     int32_t mm;        // matrix multiplications take the regression below
     double mm_c0, mm_c1, mm_c2;
+    double mm_c3, mm_floor;   // reduction-length term, floor
     int32_t node;      // devices per node, 0 = one uniform interconnect
     double net_lat;    // network latency (ops spanning nodes)
     double net_inv_l;  // 1 / network bytes per second
@@ -76,7 +77,7 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
                               hipStream_t side);
 dsim_status launch_materialize(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, int32_t max_ops,
                                int32_t n_dev, uint32_t *code, float *flops, float *bytes, uint32_t *alloc,
-                               uint32_t *freeb, uint32_t *n_ops, uint64_t *init_live, int32_t *status,
-                               hipStream_t s);
+                               uint32_t *freeb, uint32_t *mm_k, uint32_t *n_ops, uint64_t *init_live,
+                               int32_t *status, hipStream_t s);
 
 }  // namespace dsim

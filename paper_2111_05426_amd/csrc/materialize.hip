@@ -39,6 +39,7 @@ struct MatArgs {
     float *bytes;
     uint32_t *alloc;
     uint32_t *freeb;
+    uint32_t *mm_k;     // may be NULL
     uint32_t *n_ops;
     uint64_t *init_live;
     int32_t *status;
@@ -59,12 +60,14 @@ struct Emit {
     // the computation device of GPU gpu (its communication stream is the next one)
     __device__ __forceinline__ uint32_t dv(int gpu) const { return (uint32_t)(S * gpu); }
 
-    __device__ __forceinline__ void put(uint32_t code, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    __device__ __forceinline__ void put(uint32_t code, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr,
+                                        uint64_t k = 0)
     {
-        // flops and bytes must be exact in fp32, alloc and free in u32
+        // flops and bytes must be exact in fp32, alloc, free and the
+        // reduction length in u32
         const float ff = (float)fl, fb = (float)by;
         inexact |= fl >= (1ull << 62) || by >= (1ull << 62) || (uint64_t)ff != fl || (uint64_t)fb != by ||
-                   al > 0xffffffffull || fr > 0xffffffffull;
+                   al > 0xffffffffull || fr > 0xffffffffull || k > 0xffffffffull;
         if (j < (int64_t)g.max_ops) {
             const size_t o = (size_t)j * (size_t)g.n_cand + (size_t)c;
             g.code[o] = code;
@@ -72,20 +75,25 @@ struct Emit {
             g.bytes[o] = fb;
             g.alloc[o] = (uint32_t)al;
             g.freeb[o] = (uint32_t)fr;
+            if (g.mm_k) g.mm_k[o] = (uint32_t)k;
         }
         ++j;
     }
-    __device__ void compute(uint32_t cls, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    __device__ void compute(uint32_t cls, uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, uint64_t k)
     {
         for (int r = 0; r < x.D * x.H; ++r) {
             const uint64_t copy = (pend != 0 && r / x.H != pend_owner) ? pend : 0;
-            put((dv(base + r) << 8) | (cls << 24), fl, by, al, fr + copy);
+            put((dv(base + r) << 8) | (cls << 24), fl, by, al, fr + copy, k);
         }
         pend = 0;
     }
-    __device__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { compute(0u, fl, by, al, fr); }
-    // a matrix multiplication: cost class 1 of the table format
-    __device__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { compute(1u, fl, by, al, fr); }
+    __device__ void local(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { compute(0u, fl, by, al, fr, 0); }
+    // a matrix multiplication of reduction length k: cost class 1 of the
+    // table format
+    __device__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, uint64_t k)
+    {
+        compute(1u, fl, by, al, fr, k);
+    }
     // ZeRO: the owner's broadcast over the D replicas of each tensor rank
     // (kind 3, root = the owner: the others allocate their copy)
     __device__ void bcast(uint64_t by, int grp)
@@ -263,8 +271,8 @@ __global__ __launch_bounds__(kLanes) void k_materialize(const MatArgs g)
 
 dsim_status launch_materialize(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, int32_t max_ops,
                                int32_t n_dev, uint32_t *code, float *flops, float *bytes, uint32_t *alloc,
-                               uint32_t *freeb, uint32_t *n_ops, uint64_t *init_live, int32_t *status,
-                               hipStream_t s)
+                               uint32_t *freeb, uint32_t *mm_k, uint32_t *n_ops, uint64_t *init_live,
+                               int32_t *status, hipStream_t s)
 {
     MatArgs g;
     g.m = m;
@@ -277,6 +285,7 @@ dsim_status launch_materialize(const dsim_model &m, const dsim_strategy *cand, i
     g.bytes = bytes;
     g.alloc = alloc;
     g.freeb = freeb;
+    g.mm_k = mm_k;
     g.n_ops = n_ops;
     g.init_live = init_live;
     g.status = status;

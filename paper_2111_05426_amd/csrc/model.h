@@ -10,8 +10,9 @@
 //                                        stage: allocate `alloc` bytes of
 //                                        outputs, then free `free` bytes of
 //                                        tensors whose last use this is
-//   o.mm(flops, bytes, alloc, free)     the same for a matrix multiplication
-//                                        (the empirical MatMul cost applies)
+//   o.mm(flops, bytes, alloc, free, k) the same for a matrix multiplication
+//                                        of reduction length k (the empirical
+//                                        MatMul cost applies)
 //   o.ar_tp(bytes)                       all-reduce over the H ranks of each
 //                                        data replica (emitted only if H > 1)
 //   o.ar_dp(bytes)                       all-reduce over the D replicas of
@@ -62,14 +63,15 @@ struct Ctx {
     bool zero;      // ZeRO partitioning (training only, D > 1)
     bool ov;        // gradient all-reduce on the communication streams (training only, D > 1)
     uint64_t e, d, dff, seq, vocab, heads, rows, mq, mr;
-    uint64_t dH, FH, Vh, aH;
+    uint64_t dH, FH, Vh, aH, hd;   // hd: one attention head's width
     double inv_f, inv_b, inv_l, lat, launch;
     double inv_l_h, inv_l_d;   // 1 / bandwidth of the tensor- / data-parallel groups' link
     double lat_d;              // latency of the data-parallel groups' link
     double arl_h, arc_h, arl_d, arc_d;
     double chl_d;   // (D - 1) * lat: latency part of a broadcast / reduce over the D replicas
-    bool mm;        // matrix multiplications take the regression mm0 + mm1 * flops + mm2 * bytes
-    double mm0, mm1, mm2;
+    bool mm;        // matrix multiplications take the regression
+                    // max(mmf, ((mm0 + mm1 * flops) + mm2 * bytes) + mm3 * k)
+    double mm0, mm1, mm2, mm3, mmf;
     double st_lat, st_inv_l;   // a Send between the two streams of one GPU
     uint64_t mult_dev, mult_tp, mult_dp;
 };
@@ -125,6 +127,7 @@ __device__ inline void make_ctx(const dsim_model &M, const CC &c, const dsim_str
     x.FH = x.mlp ? 0 : x.dff / (uint64_t)x.H;
     x.Vh = x.mlp ? 0 : (x.vocab + (uint64_t)x.H - 1) / (uint64_t)x.H;
     x.aH = x.mlp ? 0 : x.heads / (uint64_t)x.H;
+    x.hd = x.mlp ? 0 : x.d / x.heads;
     x.inv_f = c.inv_f;
     x.inv_b = c.inv_b;
     x.inv_l = c.inv_l;
@@ -149,6 +152,8 @@ __device__ inline void make_ctx(const dsim_model &M, const CC &c, const dsim_str
     x.mm0 = c.mm_c0;
     x.mm1 = c.mm_c1;
     x.mm2 = c.mm_c2;
+    x.mm3 = c.mm_c3;
+    x.mmf = c.mm_floor;
     x.st_lat = c.st_lat;
     x.st_inv_l = c.st_inv_l;
     x.mult_dev = (uint64_t)x.D * (uint64_t)x.H;
@@ -175,12 +180,13 @@ __device__ __forceinline__ double cost_send(const Ctx &x, uint64_t bytes)
 {
     return x.lat + (double)bytes * x.inv_l;
 }
-// a matrix multiplication: the empirical regression of Sec. 4 when the
-// device model carries one, the roofline otherwise
-__device__ __forceinline__ double cost_mm(const Ctx &x, uint64_t flops, uint64_t bytes)
+// a matrix multiplication of reduction length k: the empirical regression of
+// Sec. 4 when the device model carries one, the roofline otherwise
+__device__ __forceinline__ double cost_mm(const Ctx &x, uint64_t flops, uint64_t bytes, uint64_t k)
 {
     if (!x.mm) return cost_local(x, flops, bytes);
-    return (x.mm0 + x.mm1 * (double)flops) + x.mm2 * (double)bytes;
+    const double c = ((x.mm0 + x.mm1 * (double)flops) + x.mm2 * (double)bytes) + x.mm3 * (double)k;
+    return x.mmf > c ? x.mmf : c;
 }
 // a Send between the two streams of one GPU (overlap)
 __device__ __forceinline__ double cost_stream(const Ctx &x, uint64_t bytes)
@@ -255,7 +261,7 @@ __device__ __forceinline__ void mlp_layer_fwd(const Ctx &x, S &o, uint64_t m, in
     uint64_t din, dout;
     mlp_dims(x, kind, din, dout);
     o.bcast(e * din * dout, grp);
-    o.mm(2 * m * din * dout, e * (m * din + din * dout + m * dout), e * m * dout, free_in ? e * m * din : 0);
+    o.mm(2 * m * din * dout, e * (m * din + din * dout + m * dout), e * m * dout, free_in ? e * m * din : 0, din);
     if (kind == kRow) o.ar_tp(e * m * dout);
     // Relu frees the pre-activation
     o.local(m * dout, 2 * e * m * dout, e * m * dout, e * m * dout + (dead_out ? e * m * dout : 0));
@@ -275,12 +281,12 @@ __device__ __forceinline__ void mlp_layer_bwd(const Ctx &x, S &o, uint64_t m, in
     mlp_dims(x, kind, din, dout);
     o.local(m * dout, 3 * e * m * dout, e * m * dout, 2 * e * m * dout);                 // ReluGrad: da and a die
     o.mm(2 * m * din * dout, e * (m * din + m * dout + din * dout), e * din * dout,
-         frees_input ? e * m * din : 0);                                                // weight gradient
+         frees_input ? e * m * din : 0, m);                                             // weight gradient
     if (acc) o.local(din * dout, 3 * e * din * dout, 0, e * din * dout);                // accumulate
     if (last) o.handover(e * din * dout);
     o.bcast(e * din * dout, grp);
     o.mm(2 * m * din * dout, e * (m * dout + din * dout + m * din), e * m * din,
-         e * m * dout + (layer0 ? e * m * din : 0));                                    // input gradient
+         e * m * dout + (layer0 ? e * m * din : 0), dout);                              // input gradient
     if (kind != kRow && x.H > 1 && !layer0) o.ar_tp(e * m * din);
 }
 
@@ -360,21 +366,21 @@ __device__ __forceinline__ void tf_layer_fwd(const Ctx &x, S &o, const TfSz &z, 
     const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
     o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                                  // LN1
     o.bcast(e * d * 3 * dH, grp);
-    o.mm(2 * T * d * 3 * dH, e * (T * d + d * 3 * dH + T * 3 * dH), z.QKV, save ? 0 : z.ACT);  // QKV
-    o.mm(2 * T * S_ * dH, 2 * z.OH + z.S2, z.S2, 0);                                       // scores
+    o.mm(2 * T * d * 3 * dH, e * (T * d + d * 3 * dH + T * 3 * dH), z.QKV, save ? 0 : z.ACT, d);  // QKV
+    o.mm(2 * T * S_ * dH, 2 * z.OH + z.S2, z.S2, 0, x.hd);                                 // scores
     o.local(5 * z.m * x.aH * S_ * S_, 2 * z.S2, z.S2, z.S2);                                  // softmax
-    o.mm(2 * T * S_ * dH, z.S2 + 2 * z.OH, z.OH, save ? 0 : z.S2 + z.QKV);                // P.V
+    o.mm(2 * T * S_ * dH, z.S2 + 2 * z.OH, z.OH, save ? 0 : z.S2 + z.QKV, S_);            // P.V
     o.bcast(e * dH * d, grp);
-    o.mm(2 * T * dH * d, e * (T * dH + dH * d + T * d), z.ACT, save ? 0 : z.OH);           // out-proj
+    o.mm(2 * T * dH * d, e * (T * dH + dH * d + T * d), z.ACT, save ? 0 : z.OH, dH);       // out-proj
     o.ar_tp(z.ACT);
     o.local(T * d, 3 * z.ACT, z.ACT, keep_in ? z.ACT : 2 * z.ACT);                           // residual
     o.local(8 * T * d, 2 * z.ACT, z.ACT, 0);                                                  // LN2
     o.bcast(e * d * FH, grp);
-    o.mm(2 * T * d * FH, e * (T * d + d * FH + T * FH), z.FF, save ? 0 : z.ACT);           // fc1
+    o.mm(2 * T * d * FH, e * (T * d + d * FH + T * FH), z.FF, save ? 0 : z.ACT, d);        // fc1
     o.local(8 * T * FH, 2 * z.FF, z.FF, save ? 0 : z.FF);                                    // GeLU
     if (!full) return;
     o.bcast(e * FH * d, grp);
-    o.mm(2 * T * FH * d, e * (T * FH + FH * d + T * d), z.ACT, save ? 0 : z.FF);           // fc2
+    o.mm(2 * T * FH * d, e * (T * FH + FH * d + T * d), z.ACT, save ? 0 : z.FF, FH);       // fc2
     o.ar_tp(z.ACT);
     o.local(T * d, 3 * z.ACT, z.ACT, save ? z.ACT : 2 * z.ACT);                              // residual
 }
@@ -387,7 +393,7 @@ __device__ __forceinline__ void tf_fwd_last(const Ctx &x, S &o, const TfSz &z)
     const bool tr = x.train;
     o.local(8 * T * d, 2 * z.ACT, z.ACT, tr ? 0 : z.ACT);                                  // final LN
     o.bcast(e * d * x.Vh, tf_group_head(x));
-    o.mm(2 * T * d * x.Vh, e * (T * d + d * x.Vh + T * x.Vh), z.LOG, tr ? 0 : z.ACT + z.LOG);  // LM head
+    o.mm(2 * T * d * x.Vh, e * (T * d + d * x.Vh + T * x.Vh), z.LOG, tr ? 0 : z.ACT + z.LOG, d);  // LM head
 }
 
 // last stage, before its layers' backward: loss, LM head and final LN grads
@@ -399,9 +405,9 @@ __device__ __forceinline__ void tf_bwd_last(const Ctx &x, S &o, const TfSz &z, b
     o.ar_tp(z.ST);
     o.local(2 * T * Vh, 2 * z.LOG + z.ST + z.IDS, z.LOG, z.LOG + z.ST + z.IDS);   // dlogits
     o.bcast(e * d * Vh, tf_group_head(x));
-    o.mm(2 * T * d * Vh, e * (T * Vh + d * Vh + T * d), z.ACT, 0);             // LM head dX
+    o.mm(2 * T * d * Vh, e * (T * Vh + d * Vh + T * d), z.ACT, 0, Vh);         // LM head dX
     o.ar_tp(z.ACT);
-    o.mm(2 * T * d * Vh, e * (T * d + T * Vh + d * Vh), e * d * Vh, z.ACT + z.LOG);  // LM head dW
+    o.mm(2 * T * d * Vh, e * (T * d + T * Vh + d * Vh), e * d * Vh, z.ACT + z.LOG, T);  // LM head dW
     if (acc) o.local(d * Vh, 3 * e * d * Vh, 0, e * d * Vh);
     if (last) o.handover(e * d * Vh);
     o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                             // final LN grad
@@ -412,31 +418,31 @@ __device__ __forceinline__ void tf_layer_bwd(const Ctx &x, S &o, const TfSz &z, 
 {
     const uint64_t T = z.T, d = x.d, dH = x.dH, FH = x.FH, e = x.e, S_ = x.seq;
     o.bcast(e * FH * d, grp);
-    o.mm(2 * T * FH * d, e * (T * d + FH * d + T * FH), z.FF, 0);             // fc2 dX
-    o.mm(2 * T * FH * d, e * (T * FH + T * d + FH * d), e * FH * d, z.FF);     // fc2 dW
+    o.mm(2 * T * FH * d, e * (T * d + FH * d + T * FH), z.FF, 0, d);          // fc2 dX
+    o.mm(2 * T * FH * d, e * (T * FH + T * d + FH * d), e * FH * d, z.FF, T);  // fc2 dW
     if (acc) o.local(FH * d, 3 * e * FH * d, 0, e * FH * d);
     if (last) o.handover(e * FH * d);
     o.local(8 * T * FH, 3 * z.FF, z.FF, 2 * z.FF);                                // GeLU grad
     o.bcast(e * d * FH, grp);
-    o.mm(2 * T * d * FH, e * (T * FH + d * FH + T * d), z.ACT, 0);             // fc1 dX
+    o.mm(2 * T * d * FH, e * (T * FH + d * FH + T * d), z.ACT, 0, FH);         // fc1 dX
     o.ar_tp(z.ACT);
-    o.mm(2 * T * d * FH, e * (T * d + T * FH + d * FH), e * d * FH, z.ACT + z.FF);  // fc1 dW
+    o.mm(2 * T * d * FH, e * (T * d + T * FH + d * FH), e * d * FH, z.ACT + z.FF, T);  // fc1 dW
     if (acc) o.local(d * FH, 3 * e * d * FH, 0, e * d * FH);
     if (last) o.handover(e * d * FH);
     o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                              // LN2 grad
     o.local(T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                                  // residual merge
     o.bcast(e * dH * d, grp);
-    o.mm(2 * T * dH * d, e * (T * d + dH * d + T * dH), z.OH, 0);              // out-proj dX
-    o.mm(2 * T * dH * d, e * (T * dH + T * d + dH * d), e * dH * d, z.OH);     // out-proj dW
+    o.mm(2 * T * dH * d, e * (T * d + dH * d + T * dH), z.OH, 0, d);          // out-proj dX
+    o.mm(2 * T * dH * d, e * (T * dH + T * d + dH * d), e * dH * d, z.OH, T);  // out-proj dW
     if (acc) o.local(dH * d, 3 * e * dH * d, 0, e * dH * d);
     if (last) o.handover(e * dH * d);
-    o.mm(4 * T * S_ * dH, 2 * z.S2 + 3 * z.OH, z.S2 + z.QKV, z.OH);            // P.V grads
+    o.mm(4 * T * S_ * dH, 2 * z.S2 + 3 * z.OH, z.S2 + z.QKV, z.OH, x.hd + S_);  // P.V grads: dP over hd, dV over S
     o.local(5 * z.m * x.aH * S_ * S_, 3 * z.S2, z.S2, 2 * z.S2);                  // softmax grad
-    o.mm(4 * T * S_ * dH, z.S2 + 4 * z.OH, 0, z.S2 + z.QKV);                   // Q.K^T grads
+    o.mm(4 * T * S_ * dH, z.S2 + 4 * z.OH, 0, z.S2 + z.QKV, 2 * S_);          // Q.K^T grads: dQ, dK over S
     o.bcast(e * d * 3 * dH, grp);
-    o.mm(2 * T * 3 * dH * d, e * (T * 3 * dH + 3 * dH * d + T * d), z.ACT, 0);  // QKV dX
+    o.mm(2 * T * 3 * dH * d, e * (T * 3 * dH + 3 * dH * d + T * d), z.ACT, 0, 3 * dH);  // QKV dX
     o.ar_tp(z.ACT);
-    o.mm(2 * T * d * 3 * dH, e * (T * d + T * 3 * dH + d * 3 * dH), e * d * 3 * dH, z.ACT + z.QKV);  // QKV dW
+    o.mm(2 * T * d * 3 * dH, e * (T * d + T * 3 * dH + d * 3 * dH), e * d * 3 * dH, z.ACT + z.QKV, T);  // QKV dW
     if (acc) o.local(d * 3 * dH, 3 * e * d * 3 * dH, 0, e * d * 3 * dH);
     if (last) o.handover(e * d * 3 * dH);
     o.local(8 * T * d, 3 * z.ACT, z.ACT, 2 * z.ACT);                              // LN1 grad

@@ -106,7 +106,7 @@ struct ParConsts {
     double inv_f, inv_b, inv_l, lat, launch;
     uint64_t cap;
     int32_t mm;
-    double mm_c0, mm_c1, mm_c2;
+    double mm_c0, mm_c1, mm_c2, mm_c3, mm_floor;
     int32_t node;
     double net_lat, net_inv_l;
     int32_t streams;
@@ -194,9 +194,9 @@ struct Walk {
     {
         op(cost_local(x, fl, by), al, fr);
     }
-    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, uint64_t k)
     {
-        op(cost_mm(x, fl, by), al, fr);
+        op(cost_mm(x, fl, by, k), al, fr);
     }
     __device__ __forceinline__ void ar_tp(uint64_t by)
     {
@@ -268,9 +268,9 @@ struct Record {
     {
         op(cost_local(x, fl, by), al, fr);
     }
-    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr)
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, uint64_t k)
     {
-        op(cost_mm(x, fl, by), al, fr);
+        op(cost_mm(x, fl, by, k), al, fr);
     }
     __device__ __forceinline__ void ar_tp(uint64_t by)
     {
@@ -308,7 +308,10 @@ struct Mem {
         top = a > top ? a : top;
         cur = a - (int64_t)fr;
     }
-    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { local(fl, by, al, fr); }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, uint64_t)
+    {
+        local(fl, by, al, fr);
+    }
     __device__ __forceinline__ void ar_tp(uint64_t) {}
     __device__ __forceinline__ void ar_dp(uint64_t) {}
     __device__ __forceinline__ void bcast(uint64_t, int) {}
@@ -334,7 +337,10 @@ struct MemZ {
         cur = a - (int64_t)fr;
         pend = 0;
     }
-    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { local(fl, by, al, fr); }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, uint64_t)
+    {
+        local(fl, by, al, fr);
+    }
     __device__ __forceinline__ void ar_tp(uint64_t) {}
     __device__ __forceinline__ void ar_dp(uint64_t) {}
     __device__ __forceinline__ void bcast(uint64_t by, int)
@@ -483,7 +489,10 @@ struct Count {
         walked += 1;
         nops += x.mult_dev;
     }
-    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr) { local(fl, by, al, fr); }
+    __device__ __forceinline__ void mm(uint64_t fl, uint64_t by, uint64_t al, uint64_t fr, uint64_t)
+    {
+        local(fl, by, al, fr);
+    }
     __device__ __forceinline__ void ar_tp(uint64_t)
     {
         if (x.H <= 1) return;
@@ -1585,7 +1594,7 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     g.walked = r.walked_ops;
     g.status = r.status;
     g.c = ParConsts{c.inv_f, c.inv_b, c.inv_l, c.lat, c.launch, c.cap, c.mm, c.mm_c0, c.mm_c1, c.mm_c2,
-                    c.node, c.net_lat, c.net_inv_l, c.streams, c.st_lat, c.st_inv_l};
+                    c.mm_c3, c.mm_floor, c.node, c.net_lat, c.net_inv_l, c.streams, c.st_lat, c.st_inv_l};
 
     // workspace: per-block class counts, class table, permutation (every
     // word is written before it is read: nothing needs clearing)

@@ -52,6 +52,7 @@ struct TabArgs {
     const uint32_t *freeb;
     const uint32_t *n_ops;
     const uint64_t *init_live;
+    const uint32_t *mm_k;   // reduction lengths of class-1 records (NULL: 0)
     int64_t n_cand;
     int32_t max_ops;
     int32_t row_width;
@@ -366,8 +367,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
         const double c_inv_l = tier == 2 ? a.c.st_inv_l : (tier == 1 ? a.c.net_inv_l : inv_l);
         double cost;
         if (kind == 0u && (code >> 24) == 1u && a.c.mm) {
-            // a matrix multiplication: the empirical regression of Sec. 4
-            cost = (a.c.mm_c0 + a.c.mm_c1 * f) + a.c.mm_c2 * b;
+            // a matrix multiplication: the empirical regression of Sec. 4,
+            // with its reduction-length term and floor
+            const double k = a.mm_k ? (double)a.mm_k[o] : 0.0;
+            const double lin = ((a.c.mm_c0 + a.c.mm_c1 * f) + a.c.mm_c2 * b) + a.c.mm_c3 * k;
+            cost = a.c.mm_floor > lin ? a.c.mm_floor : lin;
         } else if (kind == 0u) {
             const double tf = f * inv_f, tb = b * inv_b;
             cost = launch + (tf > tb ? tf : tb);
@@ -481,6 +485,7 @@ dsim_status launch_sim_tables(const dsim_tables &t, int64_t n_cand, const CostCo
     a.freeb = t.free_bytes;
     a.n_ops = t.n_ops;
     a.init_live = t.init_live;
+    a.mm_k = t.mm_k;
     a.n_cand = n_cand;
     a.max_ops = t.max_ops;
     a.row_width = r.row_width;

@@ -32,7 +32,7 @@ class dsim_device_model(C.Structure):
                 ("mm_enabled", C.c_int32), ("mm_c0", C.c_double), ("mm_c1", C.c_double), ("mm_c2", C.c_double),
                 ("node_size", C.c_int32), ("net_bytes_per_s", C.c_double), ("net_latency_s", C.c_double),
                 ("streams_per_gpu", C.c_int32), ("stream_bytes_per_s", C.c_double),
-                ("stream_latency_s", C.c_double)]
+                ("stream_latency_s", C.c_double), ("mm_c3", C.c_double), ("mm_floor", C.c_double)]
 
 
 class dsim_model(C.Structure):
@@ -55,7 +55,7 @@ class dsim_grid_spec(C.Structure):
 class dsim_tables(C.Structure):
     _fields_ = [("code", C.c_void_p), ("flops", C.c_void_p), ("bytes", C.c_void_p),
                 ("alloc_bytes", C.c_void_p), ("free_bytes", C.c_void_p), ("n_ops", C.c_void_p),
-                ("init_live", C.c_void_p), ("max_ops", C.c_int32), ("n_dev", C.c_int32)]
+                ("init_live", C.c_void_p), ("max_ops", C.c_int32), ("n_dev", C.c_int32), ("mm_k", C.c_void_p)]
 
 
 class dsim_results(C.Structure):
@@ -94,11 +94,11 @@ def lib():
         L.dsim_generate_random_tables.argtypes = [C.c_uint64, C.c_int64, C.c_int32, C.c_int32] + \
             [C.c_void_p] * 7
         L.dsim_materialize_tables.argtypes = [C.POINTER(dsim_model), C.c_void_p, C.c_int64, C.c_int32,
-                                              C.c_int32] + [C.c_void_p] * 9
+                                              C.c_int32] + [C.c_void_p] * 10
         L.dsim_interpret_program.argtypes = [C.c_char_p, C.c_char_p, C.c_int32, C.c_void_p, C.c_size_t,
                                              C.POINTER(C.c_size_t)]
         L.dsim_lower_programs.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int32, C.c_int32] + \
-            [C.c_void_p] * 7 + [C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.c_int32]
+            [C.c_void_p] * 8 + [C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.c_int32]
         for name in ("dsim_create_grid", "dsim_simulate_tables", "dsim_simulate_parametric",
                      "dsim_simulate_parametric_static", "dsim_argmin",
                      "dsim_generate_random_tables", "dsim_materialize_tables", "dsim_interpret_program",
@@ -198,14 +198,22 @@ def _stream(stream):
 
 
 def device_model(spec):
+    """dsim_device_model of a DeviceSpec; its matmul is None, (c0, c1, c2) or
+    (c0, c1, c2, c3, floor)."""
     mm = getattr(spec, "matmul", None)
     net = getattr(spec, "network", None)
     st = getattr(spec, "streams", None)
+    mmv = tuple(float(v) for v in mm) if mm is not None else (0.0, 0.0, 0.0)
+    if len(mmv) == 3:
+        mmv = mmv + (0.0, 0.0)
+    if len(mmv) != 5:
+        raise ValueError("matmul must be (c0, c1, c2) or (c0, c1, c2, c3, floor)")
     return dsim_device_model(spec.flops_per_s, spec.mem_bytes_per_s, spec.link_bytes_per_s,
                              spec.link_latency_s, spec.launch_s, int(spec.mem_cap_bytes), 1 if mm is not None else 0,
-                             *(float(v) for v in (mm if mm is not None else (0.0, 0.0, 0.0))),
+                             *mmv[:3],
                              *((int(net[0]), float(net[1]), float(net[2])) if net is not None else (0, 0.0, 0.0)),
-                             *((int(st[0]), float(st[1]), float(st[2])) if st is not None else (0, 0.0, 0.0)))
+                             *((int(st[0]), float(st[1]), float(st[2])) if st is not None else (0, 0.0, 0.0)),
+                             *mmv[3:])
 
 
 def model_struct(spec):
@@ -245,21 +253,24 @@ def _results(r):
                         _ptr(r.get("status")), int(r.get("row_width", 0)))
 
 
-def alloc_tables(n_cand, max_ops, device="cuda"):
+def alloc_tables(n_cand, max_ops, device="cuda", mm_k=False):
     import torch
     shape = (max_ops, n_cand)
-    return dict(code=torch.empty(shape, dtype=torch.int32, device=device),
-                flops=torch.empty(shape, dtype=torch.float32, device=device),
-                bytes=torch.empty(shape, dtype=torch.float32, device=device),
-                alloc=torch.empty(shape, dtype=torch.int32, device=device),
-                free=torch.empty(shape, dtype=torch.int32, device=device),
-                n_ops=torch.empty(n_cand, dtype=torch.int32, device=device))
+    t = dict(code=torch.empty(shape, dtype=torch.int32, device=device),
+             flops=torch.empty(shape, dtype=torch.float32, device=device),
+             bytes=torch.empty(shape, dtype=torch.float32, device=device),
+             alloc=torch.empty(shape, dtype=torch.int32, device=device),
+             free=torch.empty(shape, dtype=torch.int32, device=device),
+             n_ops=torch.empty(n_cand, dtype=torch.int32, device=device))
+    if mm_k:
+        t["mm_k"] = torch.empty(shape, dtype=torch.int32, device=device)
+    return t
 
 
 def dsim_simulate_tables(tables, n_cand, n_dev, device, results, init_live=None, stream=None):
     """tables: dict of device tensors shaped (max_ops, n_cand) (code/alloc/free
-    as int32 bit patterns of the uint32 fields), optional n_ops (n_cand,);
-    init_live: optional (n_cand, n_dev) int64."""
+    as int32 bit patterns of the uint32 fields), optional n_ops (n_cand,) and
+    mm_k (max_ops, n_cand); init_live: optional (n_cand, n_dev) int64."""
     n_cand = int(n_cand)
     a = _Args()
     a.tensor("tables['code']", tables.get("code"), _dt("int32", "uint32"), shape=(None, n_cand))
@@ -268,11 +279,13 @@ def dsim_simulate_tables(tables, n_cand, n_dev, device, results, init_live=None,
                       ("free", ("int32", "uint32"))):
         a.tensor("tables[%r]" % name, tables.get(name), _dt(*dts), shape=(max_ops, n_cand))
     a.tensor("tables['n_ops']", tables.get("n_ops"), _dt("int32", "uint32"), shape=(n_cand,), optional=True)
+    a.tensor("tables['mm_k']", tables.get("mm_k"), _dt("int32", "uint32"), shape=(max_ops, n_cand), optional=True)
     a.tensor("init_live", init_live, _dt("int64", "uint64"), shape=(n_cand, int(n_dev)), optional=True)
     a.results(results, n_cand, int(n_dev))
     a.on_gpu()
     t = dsim_tables(_ptr(tables["code"]), _ptr(tables["flops"]), _ptr(tables["bytes"]), _ptr(tables["alloc"]),
-                    _ptr(tables["free"]), _ptr(tables.get("n_ops")), _ptr(init_live), max_ops, n_dev)
+                    _ptr(tables["free"]), _ptr(tables.get("n_ops")), _ptr(init_live), max_ops, n_dev,
+                    _ptr(tables.get("mm_k")))
     d = device_model(device)
     r = _results(results)
     _check("dsim_simulate_tables",
@@ -375,14 +388,15 @@ def dsim_materialize_tables(model, cand, n_dev, max_ops, stream=None):
     a.tensor("cand", cand, _dt("int32"), shape=(None, 4))
     a.on_gpu()
     n = int(cand.shape[0])
-    t = alloc_tables(n, max_ops, device=cand.device)
+    t = alloc_tables(n, max_ops, device=cand.device, mm_k=True)
     t["init_live"] = torch.empty((n, n_dev), dtype=torch.int64, device=cand.device)
     status = torch.empty(n, dtype=torch.int32, device=cand.device)
     m = model_struct(model)
     _check("dsim_materialize_tables",
            lib().dsim_materialize_tables(C.byref(m), _ptr(cand), n, max_ops, n_dev, _ptr(t["code"]),
                                          _ptr(t["flops"]), _ptr(t["bytes"]), _ptr(t["alloc"]), _ptr(t["free"]),
-                                         _ptr(t["n_ops"]), _ptr(t["init_live"]), _ptr(status), _stream(stream)))
+                                         _ptr(t["mm_k"]), _ptr(t["n_ops"]), _ptr(t["init_live"]), _ptr(status),
+                                         _stream(stream)))
     return t, status
 
 

@@ -99,29 +99,31 @@ def _lower(texts, inputs, n_dev, threads):
     max_ops = max([t.count("\n") + 1 for t in texts] + [1])
     out = dict(code=np.empty((max_ops, n), np.uint32), flops=np.empty((max_ops, n), np.float32),
                bytes=np.empty((max_ops, n), np.float32), alloc=np.empty((max_ops, n), np.uint32),
-               free=np.empty((max_ops, n), np.uint32), n_ops=np.empty(n, np.uint32),
-               init_live=np.empty((n, n_dev), np.uint64))
+               free=np.empty((max_ops, n), np.uint32), mm_k=np.empty((max_ops, n), np.uint32),
+               n_ops=np.empty(n, np.uint32), init_live=np.empty((n, n_dev), np.uint64))
     used, devs = C.c_int32(0), C.c_int32(0)
     rc = L.dsim_lower_programs(C.cast(progs, C.c_void_p), None if inp is None else C.cast(inp, C.c_void_p), n,
                                n_dev, max_ops, *(out[k].ctypes.data for k in
-                                                 ("code", "flops", "bytes", "alloc", "free", "n_ops", "init_live")),
+                                                 ("code", "flops", "bytes", "alloc", "free", "mm_k", "n_ops",
+                                                  "init_live")),
                                C.byref(used), C.byref(devs), int(threads))
     if rc != 0:
         _fail("dsim_lower_programs", rc)
     m = used.value
-    for k in ("code", "flops", "bytes", "alloc", "free"):
+    for k in ("code", "flops", "bytes", "alloc", "free", "mm_k"):
         out[k] = out[k][:m]
     return out, devs.value
 
 
 def lower(text, inputs=None, n_dev=None):
     """One program interpreted (mixed) and lowered to its op table: dict(code,
-    flops, bytes, alloc, free, init_live, n_dev) of uint32 / float32 / uint64
-    arrays.  n_dev None: the devices the program uses."""
+    flops, bytes, alloc, free, mm_k, init_live, n_dev) of uint32 / float32 /
+    uint64 arrays (mm_k: each record's reduction length, 0 but on matrix
+    products).  n_dev None: the devices the program uses."""
     out, used = _lower([text], None if inputs is None else [inputs], 8 if n_dev is None else n_dev, 1)
     nd = used if n_dev is None else n_dev
     return dict(code=out["code"][:, 0].copy(), flops=out["flops"][:, 0].copy(), bytes=out["bytes"][:, 0].copy(),
-                alloc=out["alloc"][:, 0].copy(), free=out["free"][:, 0].copy(),
+                alloc=out["alloc"][:, 0].copy(), free=out["free"][:, 0].copy(), mm_k=out["mm_k"][:, 0].copy(),
                 init_live=out["init_live"][0, :nd].copy(), n_dev=nd)
 
 
@@ -142,12 +144,13 @@ def pack(tables):
     m = max([len(t["code"]) for t in tables] + [1])
     out = dict(code=np.zeros((m, n), np.uint32), flops=np.zeros((m, n), np.float32),
                bytes=np.zeros((m, n), np.float32), alloc=np.zeros((m, n), np.uint32),
-               free=np.zeros((m, n), np.uint32), n_ops=np.zeros(n, np.uint32),
+               free=np.zeros((m, n), np.uint32), mm_k=np.zeros((m, n), np.uint32), n_ops=np.zeros(n, np.uint32),
                init_live=np.zeros((n, nd), np.uint64), n_dev=nd)
     for c, t in enumerate(tables):
         k = len(t["code"])
-        for f in ("code", "flops", "bytes", "alloc", "free"):
-            out[f][:k, c] = t[f]
+        for f in ("code", "flops", "bytes", "alloc", "free", "mm_k"):
+            if t.get(f) is not None:
+                out[f][:k, c] = t[f]
         out["n_ops"][c] = k
         out["init_live"][c, :t["n_dev"]] = t["init_live"]
     return out

@@ -58,8 +58,10 @@ class DeviceSpec:
     link_latency_s: float = 5e-6
     launch_s: float = 5e-6
     mem_cap_bytes: int = 0
-    # (c0, c1, c2): matrix multiplications cost c0 + c1 * flops + c2 * bytes
-    # (an empirical regression fitted on microbenchmarks); None: the roofline
+    # (c0, c1, c2, c3, floor): a matrix multiplication of reduction length k
+    # costs max(floor, c0 + c1 * flops + c2 * bytes + c3 * k) (an empirical
+    # regression fitted on microbenchmarks); (c0, c1, c2) is the linear form
+    # (c3 = floor = 0); None: the roofline
     matmul: tuple = None
     # (node_size, bytes/s, latency s): devices d lie in node d // node_size,
     # and sends and collectives spanning nodes cross this network link;
@@ -135,16 +137,17 @@ GPT3_175B_OVERLAP = replace(GPT3_175B, name="gpt3_175b_overlap", model=replace(G
 
 # A cluster of MI355X: fp16 matrix multiplications take the regression fitted
 # on this GPU by `python -m paper_2111_05426_amd.calibrate --dtype fp16`
-# (c0 = per-product dispatch, 1/c1 = 1.49 PFLOP/s, 1/c2 = 5.7 TB/s); other
-# compute ops the roofline with F = 1/c1, the bandwidth of a 4 GiB
-# device-to-device copy measured on the same GPU (4.94 TB/s, read + write)
-# and the same dispatch cost; nodes of 8 GPUs joined by xGMI (one link's
-# 153 GB/s, 5 us) and a network of one 400 Gb/s NIC per GPU between nodes
-# (50 GB/s, 10 us) -- specification values: a single GPU cannot measure
-# them; 288 GB of HBM per device.
-MI355X = DeviceSpec(flops_per_s=1.493e15, mem_bytes_per_s=4.94e12, link_bytes_per_s=153e9, link_latency_s=5e-6,
-                    launch_s=1.557e-5, mem_cap_bytes=288_000_000_000, matmul=(1.557e-5, 6.699e-16, 1.743e-13),
-                    network=(8, 50e9, 10e-6))
+# (max(floor, c0 + c1 flops + c2 bytes + c3 k): floor = 19.4 us per-product
+# dispatch, 1/c1 = 1.81 PFLOP/s, 1/c2 = 4.6 TB/s, c3 = 2.8 ns per step of
+# the reduction length); other compute ops the roofline with F = 1/c1, the
+# bandwidth of a 4 GiB device-to-device copy measured on the same GPU
+# (4.94 TB/s, read + write) and the dispatch floor as their launch cost;
+# nodes of 8 GPUs joined by xGMI (one link's 153 GB/s, 5 us) and a network of
+# one 400 Gb/s NIC per GPU between nodes (50 GB/s, 10 us) -- specification
+# values: a single GPU cannot measure them; 288 GB of HBM per device.
+MI355X = DeviceSpec(flops_per_s=1.810e15, mem_bytes_per_s=4.94e12, link_bytes_per_s=153e9, link_latency_s=5e-6,
+                    launch_s=1.936e-5, mem_cap_bytes=288_000_000_000,
+                    matmul=(3.996e-6, 5.524e-16, 2.190e-13, 2.840e-9, 1.936e-5), network=(8, 50e9, 10e-6))
 GPT3_175B_MI355X = replace(GPT3_175B, name="gpt3_175b_mi355x", device=MI355X)
 GPT3_175B_MI355X_OVERLAP = replace(GPT3_175B_MI355X, name="gpt3_175b_mi355x_overlap",
                                    model=replace(GPT3_175B.model, overlap=1),

@@ -48,6 +48,7 @@ int main()
             dsim_device_model m = dev();
             m.flops_per_s = f; m.link_bytes_per_s = b; m.link_latency_s = b == inf ? nan : 1e-6;
             m.mm_enabled = f == 0.0 ? 2 : 1; m.mm_c0 = f; m.mm_c1 = b; m.mm_c2 = 1e-12;
+            m.mm_c3 = b; m.mm_floor = f;
             m.node_size = b < 0 ? -1 : 4; m.net_bytes_per_s = f; m.net_latency_s = 1e-5;
             m.streams_per_gpu = f > 1e300 ? (1 << 21) : 2; m.stream_bytes_per_s = b; m.stream_latency_s = 0.0;
             dsim_tables t;
@@ -79,8 +80,8 @@ int main()
                                              nullptr);
                     dsim_simulate_parametric_static(&m2, (const dsim_strategy *)p, 10, &dv, &res, nullptr);
                     dsim_materialize_tables(&m2, (const dsim_strategy *)p, 10, 100, 8, (uint32_t *)p, (float *)p,
-                                            (float *)p, (uint32_t *)p, (uint32_t *)p, (uint32_t *)p, (uint64_t *)p,
-                                            (int32_t *)p, nullptr);
+                                            (float *)p, (uint32_t *)p, (uint32_t *)p, (uint32_t *)p, (uint32_t *)p,
+                                            (uint64_t *)p, (int32_t *)p, nullptr);
                     calls += 4;
                 }
     // grid rules

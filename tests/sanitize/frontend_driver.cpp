@@ -109,7 +109,7 @@ static int exercise(const std::string &prog, const std::string &inputs, bool mus
     const char *ins[3] = {in, in, in};
     const char *const *insp = inputs.empty() && pick(2) ? nullptr : ins;
     dsim_status st = dsim_lower_programs(progs, insp, 3, 8, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                         nullptr, &used, &devs, 1);
+                                         nullptr, nullptr, &used, &devs, 1);
     ++g_calls;
     if (st != DSIM_OK) {
         if (must_lower) {
@@ -120,11 +120,12 @@ static int exercise(const std::string &prog, const std::string &inputs, bool mus
     }
     int32_t rows = used + (int32_t)pick(3);
     size_t cells = (size_t)rows * 3 + 1;
-    std::vector<uint32_t> code(cells), alloc(cells), freeb(cells), n_ops(3);
+    std::vector<uint32_t> code(cells), alloc(cells), freeb(cells), mm_k(cells), n_ops(3);
     std::vector<float> flops(cells), bytes(cells);
     std::vector<uint64_t> init(3 * 8);
     st = dsim_lower_programs(progs, insp, 3, 8, rows, code.data(), flops.data(), bytes.data(), alloc.data(),
-                             freeb.data(), n_ops.data(), init.data(), &used, &devs, 1 + (int32_t)pick(4));
+                             freeb.data(), pick(2) ? mm_k.data() : nullptr, n_ops.data(), init.data(), &used, &devs,
+                             1 + (int32_t)pick(4));
     ++g_calls;
     if (st != DSIM_OK) {   // the sizing pass accepted the same programs
         std::printf("full pass failed after the sizing pass: %s\n", dsim_last_error());
@@ -166,13 +167,15 @@ int main(int argc, char **argv)
     int32_t used = 0, devs = 0;
     uint32_t u = 0;
     if (dsim_lower_programs(nullptr, nullptr, 1, 8, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                            nullptr, &used, &devs, 1) != DSIM_EINVAL ||
+                            nullptr, nullptr, &used, &devs, 1) != DSIM_EINVAL ||
         dsim_lower_programs(one, nullptr, 1, 9, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                            &used, &devs, 1) != DSIM_ERANGE ||
+                            nullptr, &used, &devs, 1) != DSIM_ERANGE ||
         dsim_lower_programs(one, nullptr, 1, 8, -1, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                            nullptr, &used, &devs, 1) != DSIM_EINVAL ||
+                            nullptr, nullptr, &used, &devs, 1) != DSIM_EINVAL ||
         dsim_lower_programs(one, nullptr, 1, 8, 4, &u, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                            &used, &devs, 1) != DSIM_EINVAL ||
+                            nullptr, &used, &devs, 1) != DSIM_EINVAL ||
+        dsim_lower_programs(one, nullptr, 1, 8, 4, nullptr, nullptr, nullptr, nullptr, nullptr, &u, nullptr,
+                            nullptr, &used, &devs, 1) != DSIM_EINVAL ||
         dsim_interpret_program(nullptr, nullptr, 1, nullptr, 0, nullptr) != DSIM_EINVAL ||
         dsim_interpret_program(one[0], nullptr, 2, nullptr, 0, nullptr) != DSIM_EINVAL) {
         std::printf("an argument error was not reported\n");

@@ -41,8 +41,8 @@ dsim_status static_scratch(void **out)
 }
 int64_t static_max_cand() { return (int64_t)1 << 20; }
 dsim_status launch_materialize(const dsim_model &, const dsim_strategy *, int64_t, int32_t, int32_t, uint32_t *,
-                               float *, float *, uint32_t *, uint32_t *, uint32_t *, uint64_t *, int32_t *,
-                               hipStream_t)
+                               float *, float *, uint32_t *, uint32_t *, uint32_t *, uint32_t *, uint64_t *,
+                               int32_t *, hipStream_t)
 {
     ++g_launches;
     return DSIM_OK;

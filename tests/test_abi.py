@@ -84,7 +84,7 @@ def test_argument_errors_before_launch():
     assert L.dsim_simulate_tables(C.byref(tab), (1 << 32) - 255, C.byref(dev), C.byref(res), None) == dsim.DSIM_ERANGE
     assert "2^32" in dsim.dsim_last_error()
     assert L.dsim_materialize_tables(C.byref(dsim.model_struct(ALL["tiny_mlp"].model)), None, 1 << 32, 10, 4,
-                                     *([None] * 9)) == dsim.DSIM_ERANGE
+                                     *([None] * 10)) == dsim.DSIM_ERANGE
     # argmin
     assert L.dsim_argmin(None, None, None, 0, 0, 0, None, 0, None, None, None, None) == dsim.DSIM_ERANGE
     assert L.dsim_argmin(None, None, None, 0, 0, 65, None, 0, None, None, None, None) == dsim.DSIM_ERANGE
@@ -110,6 +110,9 @@ def test_argument_errors_before_launch():
     tab4.n_dev, tab4.max_ops = 4, 4
     for spec, word in ((DeviceSpec(matmul=(-1e-6, 0.0, 0.0)), "regression"),
                        (DeviceSpec(matmul=(0.0, float("inf"), 0.0)), "regression"),
+                       (DeviceSpec(matmul=(0.0, 0.0, 0.0, -1e-9, 0.0)), "regression"),
+                       (DeviceSpec(matmul=(0.0, 0.0, 0.0, 0.0, float("nan"))), "regression"),
+                       (DeviceSpec(matmul=(0.0, 0.0, 0.0, float("inf"), 1e-5)), "regression"),
                        (DeviceSpec(network=(-1, 1e9, 0.0)), "node_size"),
                        (DeviceSpec(network=(8, 0.0, 1e-6)), "network"),
                        (DeviceSpec(network=(8, 1e9, float("nan"))), "network"),
@@ -159,12 +162,12 @@ def test_argument_errors_before_launch():
     # materialiser: device count, op capacity, NULL buffers, bad model
     m = dsim.model_struct(ALL["tiny_mlp"].model)
     for nd in (0, 9):
-        assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, nd, *([None] * 9)) == dsim.DSIM_ERANGE
-    assert L.dsim_materialize_tables(C.byref(m), None, 1, -1, 4, *([None] * 9)) == dsim.DSIM_ERANGE
-    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_EINVAL
-    assert L.dsim_materialize_tables(C.byref(m), None, 0, 10, 4, *([None] * 9)) == dsim.DSIM_OK
+        assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, nd, *([None] * 10)) == dsim.DSIM_ERANGE
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, -1, 4, *([None] * 10)) == dsim.DSIM_ERANGE
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 10)) == dsim.DSIM_EINVAL
+    assert L.dsim_materialize_tables(C.byref(m), None, 0, 10, 4, *([None] * 10)) == dsim.DSIM_OK
     m.family = 7
-    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_EINVAL
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 10)) == dsim.DSIM_EINVAL
 
 
 def _grid_rc(model):
@@ -193,7 +196,7 @@ def test_size_rule_at_both_sides_of_the_bound(orc):
     res = dsim.dsim_results()
     m = dsim.model_struct(cases[1][0])
     assert L.dsim_simulate_parametric(C.byref(m), None, 1, C.byref(dev), C.byref(res), None, 0, None, None) == dsim.DSIM_ERANGE
-    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 9)) == dsim.DSIM_ERANGE
+    assert L.dsim_materialize_tables(C.byref(m), None, 1, 10, 4, *([None] * 10)) == dsim.DSIM_ERANGE
 
 
 def test_size_rule_matches_oracle_on_random_models(orc):

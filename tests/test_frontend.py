@@ -140,7 +140,9 @@ func f(%t: Tensor[Float32, (4, 6), 0], %c: Tensor[Int64, (24,), 0], %s: Tensor[I
 
 DEVICES = [DeviceSpec(), DeviceSpec(matmul=(5.2e-6, 1.1e-15, 2.3e-13)),
            DeviceSpec(network=(2, 4.9e10, 1.1e-5)),
-           DeviceSpec(streams=(2, math.inf, 0.0), network=(1, 4.9e10, 1.1e-5))]
+           DeviceSpec(streams=(2, math.inf, 0.0), network=(1, 4.9e10, 1.1e-5)),
+           # the reduction-length term and a floor that binds on small products
+           DeviceSpec(matmul=(1.3e-6, 6.7e-16, 1.7e-13, 2.6e-9, 1.5e-5))]
 
 
 @pytest.mark.parametrize("dev", range(len(DEVICES)))
@@ -195,7 +197,7 @@ def test_random_programs_simulate_like_the_oracle(orc, chunk):
     for seed, n in RAND[chunk::8]:
         src = random_program(seed, n_ops=n)
         t = fe.lower(src)
-        for d in (DEVICES[0], DEVICES[1], DEVICES[3]):
+        for d in (DEVICES[0], DEVICES[1], DEVICES[3], DEVICES[4]):
             a = orc.sim_table(t, t["n_dev"], d, init_live=t["init_live"])
             b = interp.simulate(src, d)
             assert a["status"] == 0, seed
@@ -228,10 +230,10 @@ def _raw(texts, n_dev=8, max_ops=512, arrays=True, threads=1):
     progs = (C.c_char_p * n)(*[t.encode() for t in texts])
     arr = dict(code=np.full((max_ops, n), 7, np.uint32), flops=np.zeros((max_ops, n), np.float32),
                bytes=np.zeros((max_ops, n), np.float32), alloc=np.zeros((max_ops, n), np.uint32),
-               free=np.zeros((max_ops, n), np.uint32), n_ops=np.full(n, 99, np.uint32),
-               init_live=np.zeros((n, n_dev), np.uint64))
-    ptrs = [arr[k].ctypes.data if arrays else None for k in ("code", "flops", "bytes", "alloc", "free", "n_ops",
-                                                              "init_live")]
+               free=np.zeros((max_ops, n), np.uint32), mm_k=np.zeros((max_ops, n), np.uint32),
+               n_ops=np.full(n, 99, np.uint32), init_live=np.zeros((n, n_dev), np.uint64))
+    ptrs = [arr[k].ctypes.data if arrays else None for k in ("code", "flops", "bytes", "alloc", "free", "mm_k",
+                                                              "n_ops", "init_live")]
     used, devs = C.c_int32(-1), C.c_int32(-1)
     rc = L.dsim_lower_programs(C.cast(progs, C.c_void_p), None, n, n_dev, max_ops, *ptrs, C.byref(used),
                                C.byref(devs), threads)
@@ -286,3 +288,19 @@ def test_error_names_the_first_failing_program_whatever_the_threads():
     for threads in (1, 2, 5, 16):
         rc, _, _, _ = _raw(texts, threads=threads)
         assert rc == dsim.DSIM_EINVAL and dsim.dsim_last_error().startswith("program 5: line 2")
+
+
+def test_matmul_records_carry_their_reduction_length():
+    """MatMul: the left operand's last dimension (batched too); Gemm: the
+    shared dimension, transposed or not; every other record 0."""
+    src = """
+func f(%x: Tensor[Float32, (8, 16), 0], %w: Tensor[Float32, (16, 4), 0] keep, %b: Tensor[Float32, (3, 5, 7), 0], %c: Tensor[Float32, (3, 7, 2), 0], %v: Tensor[Float32, (4, 16), 0] keep)
+%y = Gemm(%x, %w)
+%r = Relu(%y)
+%z = MatMul(%b, %c)
+%t = Transpose[perm = [1, 0]](%x)
+%u = Gemm[transA = 1, transB = 1](%t, %v)
+"""
+    t = fe.lower(src)
+    assert list(t["code"] >> 24) == [1, 0, 1, 0, 1]
+    assert list(t["mm_k"]) == [16, 0, 7, 0, 16]

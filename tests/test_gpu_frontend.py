@@ -29,7 +29,7 @@ CASES = [(B, S, tp, pp) for tp, pp in ((1, 1), (2, 2), (4, 2), (2, 4), (1, 4))
 
 
 @pytest.mark.parametrize("dev", [DeviceSpec(mem_cap_bytes=400_000_000),
-                                 DeviceSpec(matmul=(5.2e-6, 1.1e-15, 2.3e-13), network=(2, 4.9e10, 1.1e-5)),
+                                 DeviceSpec(matmul=(5.2e-6, 1.1e-15, 2.3e-13, 2.6e-9, 1.5e-5), network=(2, 4.9e10, 1.1e-5)),
                                  DeviceSpec(streams=(2, math.inf, 0.0), network=(2, 4.9e10, 1.1e-5))],
                          ids=["roofline_cap", "matmul_network", "streams"])
 def test_lowered_programs_vs_oracle(torch_gpu, dev):
@@ -48,7 +48,7 @@ def test_lowered_programs_vs_oracle(torch_gpu, dev):
     n = len(texts)
     print("%d lowered programs, %d records at most" % (n, p["code"].shape[0]), flush=True)
     g = {k: torch.from_numpy(np.ascontiguousarray(p[k]).view(np.int32 if p[k].dtype == np.uint32 else p[k].dtype)).cuda()
-         for k in ("code", "flops", "bytes", "alloc", "free", "n_ops")}
+         for k in ("code", "flops", "bytes", "alloc", "free", "mm_k", "n_ops")}
     init = torch.from_numpy(p["init_live"].view(np.int64)).cuda()
     r = dsim.alloc_results(n, 8)
     dsim.dsim_simulate_tables(g, n, 8, dev, r, init_live=init)

@@ -134,10 +134,14 @@ def test_small_models_vs_full_program(torch_gpu, orc, case):
 
 
 # empirical MatMul costs: random regression coefficients (and ones that make
-# matrix multiplications cheap or dominant) on models of every family/mode
+# matrix multiplications cheap or dominant) on models of every family/mode;
+# the reduction-length term alone, and with a floor that binds on the
+# smaller products
 MM_DEVICES = [DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(6.1e-6, 2.3e-14, 7.7e-13)),
               DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(0.0, 3.3e-16, 0.0)),
-              DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(2.0e-4, 1.9e-12, 4.1e-10))]
+              DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(2.0e-4, 1.9e-12, 4.1e-10)),
+              DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(0.0, 0.0, 0.0, 1.3e-7, 0.0)),
+              DeviceSpec(mem_cap_bytes=10 ** 6, matmul=(6.1e-6, 2.3e-14, 7.7e-13, 4.3e-9, 2.9e-5))]
 MM_CASES = [SMALL[0], SMALL[1], SMALL[3], SMALL[4], SMALL[6], SMALL[10], SMALL[13], SMALL[16], SMALL[19]]
 
 
@@ -200,8 +204,9 @@ GRIDS = [TINY_MLP, LARGE_MLP, GPT2_SMALL, GPT2_SMALL_TRAIN,
          replace(LARGE_MLP, name="large_mlp_zero", model=replace(LARGE_MLP.model, zero=1)),
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_zero", model=replace(GPT2_SMALL_TRAIN.model, zero=1)),
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_matmul",
-                 device=replace(GPT2_SMALL_TRAIN.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13))),
-         replace(LARGE_MLP, name="large_mlp_matmul", device=replace(LARGE_MLP.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13))),
+                 device=replace(GPT2_SMALL_TRAIN.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13, 2.3e-9, 1.7e-5))),
+         replace(LARGE_MLP, name="large_mlp_matmul",
+                 device=replace(LARGE_MLP.device, matmul=(8.0e-6, 1.1e-14, 2.9e-13, 2.3e-9, 1.7e-5))),
          replace(LARGE_MLP, name="large_mlp_overlap", model=replace(LARGE_MLP.model, overlap=1),
                  device=replace(LARGE_MLP.device, streams=(2, 2.2e11, 3.1e-6))),
          replace(GPT2_SMALL_TRAIN, name="gpt2_small_train_overlap_rc",

@@ -54,6 +54,11 @@ def random_case(seed):
     if rng.random() < 0.3:
         dev = replace(dev, matmul=(float(rng.uniform(0, 2e-5)), float(rng.uniform(1e-16, 1e-13)),
                                    float(rng.uniform(0, 1e-12))))
+        # half of them with the reduction-length term and a floor (drawn
+        # from a stream of their own, so the other draws stay as they were)
+        r2 = np.random.default_rng(20_000 + seed)
+        if r2.random() < 0.5:
+            dev = replace(dev, matmul=dev.matmul + (float(r2.uniform(0, 5e-8)), float(r2.uniform(0, 3e-5))))
     if rng.random() < 0.3:
         dev = replace(dev, network=(int(rng.choice([1, 2, 4])), float(rng.uniform(1e9, 5e10)), float(rng.uniform(0, 2e-5))))
     if overlap:

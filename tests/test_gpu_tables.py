@@ -74,13 +74,17 @@ def random_tables(rng, n_cand, max_ops, n_dev, bad=False, rooted=False, classes=
     n_ops = rng.integers(0, max_ops + 1, n_cand).astype(np.uint32)
     n_ops[:3] = [0, max_ops, 1][:min(3, n_cand)] if n_cand >= 3 else n_ops[:3]
     init = rng.integers(0, 10 ** 5, (n_cand, n_dev)).astype(np.uint64)
-    return dict(code=code, flops=fl, bytes=by, alloc=alloc, free=free, n_ops=n_ops, init=init)
+    out = dict(code=code, flops=fl, bytes=by, alloc=alloc, free=free, n_ops=n_ops, init=init)
+    if classes:   # reduction lengths, log-uniform up to 2^32 - 1 (read on class-1 records only)
+        out["mm_k"] = np.exp(rng.uniform(0.0, np.log(2.0 ** 32 - 1), (max_ops, n_cand))).astype(np.uint32)
+    return out
 
 
 def to_gpu(torch, t):
     g = {}
-    for k in ("code", "alloc", "free", "n_ops"):
-        g[k] = torch.from_numpy(t[k].view(np.int32)).cuda()
+    for k in ("code", "alloc", "free", "n_ops", "mm_k"):
+        if k in t:
+            g[k] = torch.from_numpy(t[k].view(np.int32)).cuda()
     for k in ("flops", "bytes"):
         g[k] = torch.from_numpy(t[k]).cuda()
     return g
@@ -107,7 +111,9 @@ def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, kinds):
     rng = np.random.default_rng(1000 + n_dev + 17 * bad + 101 * rooted + 211 * classes + 307 * net + 401 * streams)
     n_cand, max_ops = 777, 301   # several 256-lane blocks and a ragged tail
     t = random_tables(rng, n_cand, max_ops, n_dev, bad, rooted, classes)
-    dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5, matmul=(4.5e-6, 9.1e-15, 1.3e-12) if classes else None,
+    # the MatMul regression with its reduction-length term and a floor that
+    # binds on part of the records (the floor above c0 + the smallest terms)
+    dev = DeviceSpec(mem_cap_bytes=2 * 10 ** 5, matmul=(4.5e-6, 9.1e-15, 1.3e-12, 3.7e-14, 4.0e-5) if classes else None,
                      network=(max(1, n_dev // 2 - (n_dev == 5)), 3.3e9, 2.1e-5) if net else None)
     if streams:
         # two or three streams per GPU; GPUs in nodes of one for some sizes;
@@ -124,7 +130,7 @@ def test_tables_vs_oracle(torch_gpu, orc, n_dev, bad, kinds):
     mk, fin, pk, cp, st = [], [], [], [], []
     for c in range(n_cand):
         n = int(t["n_ops"][c])
-        tab = {k: t[k][:n, c] for k in ("code", "flops", "bytes", "alloc", "free")}
+        tab = {k: t[k][:n, c] for k in ("code", "flops", "bytes", "alloc", "free", "mm_k") if k in t}
         o = orc.sim_table(tab, n_dev, dev, init_live=t["init"][c])
         mk.append(o["makespan"]); fin.append(o["finish"]); pk.append(o["peak"])
         cp.append(o["cand_peak"]); st.append(o["status"])
