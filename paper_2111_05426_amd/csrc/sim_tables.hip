@@ -13,9 +13,10 @@
 // byte offset and no lane does 64-bit address arithmetic.  Two register sets
 // of kUnroll ops alternate: one is processed while the other is in flight.
 //
-// Per-lane state: the device clocks live in VGPRs (n_dev <= 8 fp64) and are
-// combined with the op's device mask as 1.0/0.0 factors, so an op touching any
-// subset of devices runs the same branch-free sequence; the per-device (live,
+// Per-lane state: the device clocks live in VGPRs (n_dev <= 8 fp64) and take
+// the op's device mask as their sign bits (set outside the op) while the
+// start is taken, so an op touching any subset of devices runs the same
+// branch-free sequence; the per-device (live,
 // peak) byte counters are indexed by a per-lane device id and live in LDS as
 // 16-byte pairs laid out [device][lane], so the 64 lanes of a wavefront
 // always hit 64 distinct pairs.  An op's cost is base + coef * x with
@@ -26,8 +27,9 @@
 // lane of a 16-lane group, so that lanes reading different classes spread
 // over the banks (a 64-lane b128 read still takes several LDS cycles).
 //
-// The kernel is bound by issue rate (about 100 vector instructions per op)
-// more than by HBM: it has a fast path for the ops every lane of a wavefront
+// The kernel runs close to the rate at which HBM returns its op records
+// (about 82 vector instructions per op keep the vector units partly busy
+// beside that); it has a fast path for the ops every lane of a wavefront
 // has, which assumes valid compute, send and all-reduce ops of cost class 0
 // (indices clamped, so even an invalid op stays in bounds) and only tests
 // whether each op is one; a lane that meets an op it cannot vouch for (a
@@ -80,17 +82,32 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t group_rsrc(const void *base, u
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRsrcWord3);
 }
 
-// max of two non-negative doubles.  The compiler's fmax first canonicalizes
-// an operand it cannot prove canonical (a loop-carried clock), one extra
-// instruction per device and op; the bare instruction gives the same value:
-// the operands are never -0.0 or signalling NaNs, and the one quiet NaN
-// that can occur (an overflowed end time times a 0.0 participation factor)
-// yields the other operand, the clock to keep, as with fmax.
+// max of two doubles that are never NaN.  The compiler's fmax first
+// canonicalizes an operand it cannot prove canonical (a loop-carried clock),
+// one extra instruction per device and op; the bare instruction gives the
+// same value (of +0.0 and -0.0 it may return either).
 __device__ __forceinline__ double max_nn(double a, double b)
 {
     double r;
     asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
     return r;
+}
+
+// max(|a|, b), the absolute value taken by the instruction's input modifier
+__device__ __forceinline__ double max_abs(double a, double b)
+{
+    double r;
+    asm("v_max_f64 %0, |%1|, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+// x with its sign bit replaced by bit 31 of s (one bit-field insert on the
+// high word; the low word is untouched)
+__device__ __forceinline__ double with_sign(double x, uint32_t s)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    const uint32_t hi = (s & 0x80000000u) | ((uint32_t)(b >> 32) & 0x7fffffffu);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | (b & 0xffffffffull)));
 }
 
 // max of two byte counts below 2^63 as one fp64 max of their bit patterns:
@@ -277,27 +294,33 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
             const double f = (double)__uint_as_float(fl[u]), b = (double)__uint_as_float(by[u]);
             const double cost = bc.x + bc.y * max_nn(f * rw.y, b * rw.x);
 
-            // synchronous start on the device set, common end.  sel[d] is 1.0
-            // for a participant, 0.0 otherwise.  Clocks are >= 0, so
-            // max(start, clk*sel) is the participants' max; every participant
-            // has clk <= start <= end, so max(clk, end*sel) sets participants
-            // to end and leaves the others unchanged (bit-exact).
-            double sel[ND];
+            // synchronous start on the device set, common end.  Bit 31 of
+            // xs[d] is set for a device outside the op; the clocks take it
+            // as their sign, so the max over all of them is the max over the
+            // participants (clocks are >= 0: outside clocks become <= -0.0,
+            // below every participant's).  The update takes max(|clk|, e)
+            // with e = end for a participant and -end outside: participants
+            // (clk <= start <= end) get end, the others keep their clock,
+            // bit-exact.  A clock may come out as -0.0 (max of +0.0 and
+            // -0.0), which compares equal to 0.0; the epilogue adds +0.0
+            // to every stored clock.
+            const uint32_t nm = ~m;
+            uint32_t xs[ND];
 #pragma unroll
-            for (int d = 0; d < ND; ++d) sel[d] = (double)((m >> d) & 1u);
+            for (int d = 0; d < ND; ++d) xs[d] = nm << (31 - d);
+#pragma unroll
+            for (int d = 0; d < ND; ++d) clk[d] = with_sign(clk[d], xs[d]);
             // pairwise max tree (max is exact, so the order does not matter)
             double v[ND];
 #pragma unroll
-            for (int d = 0; d < ND; ++d) v[d] = clk[d] * sel[d];
+            for (int d = 0; d < ND; ++d) v[d] = clk[d];
 #pragma unroll
             for (int w = 1; w < ND; w *= 2)
 #pragma unroll
-                for (int d = 0; d + w < ND; d += 2 * w) v[d] = __builtin_fmax(v[d], v[d + w]);
-            // every product is +0.0 or positive, so the tree's max is already
-            // the max over the participants starting from 0.0
+                for (int d = 0; d + w < ND; d += 2 * w) v[d] = max_nn(v[d], v[d + w]);
             const double end = v[0] + cost;
 #pragma unroll
-            for (int d = 0; d < ND; ++d) clk[d] = max_nn(clk[d], end * sel[d]);
+            for (int d = 0; d < ND; ++d) clk[d] = max_abs(clk[d], with_sign(end, xs[d]));
 
             // live memory: allocate on the target, sample, free on the
             // source (an all-reduce moves no memory).  A free that would
@@ -452,7 +475,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(kWavesPe
     if (a.finish) {
         double *row = a.finish + (size_t)c * a.row_width;
 #pragma unroll
-        for (int d = 0; d < ND; ++d) row[d] = clk[d];
+        for (int d = 0; d < ND; ++d) row[d] = clk[d] + 0.0;   // -0.0 -> +0.0
         for (int d = ND; d < a.row_width; ++d) row[d] = 0.0;
     }
     if (a.peak) {
