@@ -97,8 +97,9 @@ __device__ inline bool strategy_ok(const dsim_model &m, int D, int H, int P, int
     return m.n_heads % H == 0 && m.d_model % H == 0 && m.d_ff % H == 0;
 }
 
-template <class CC>
-__device__ inline void make_ctx(const dsim_model &M, const CC &c, const dsim_strategy &st, Ctx &x)
+// M: the model (dsim_model, in any address space); c: the device constants
+template <class MM, class CC>
+__device__ inline void make_ctx(const MM &M, const CC &c, const dsim_strategy &st, Ctx &x)
 {
     x.D = st.D;
     x.H = st.H;

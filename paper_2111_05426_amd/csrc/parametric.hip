@@ -957,6 +957,21 @@ __device__ void record_lane(const Ctx &x, int s, bool bwd, uint64_t m, bool acc,
 // gradient all-reduce on the communication streams (separate instantiations
 // keep the replay, the broadcasts and the two-stream walk out of the other
 // kernels).
+// The kernel's argument block (its only argument, at offset 0 of the
+// kernarg segment), addressed through a pointer the compiler cannot see
+// through.  The recording paths inside the slot loop and the weight update
+// after it read the model and the device constants through it: those values
+// are then loaded again with scalar loads where they are needed instead of
+// being kept live across the loop, where they would not fit the scalar
+// registers and would be spilled to vector-register lanes and read back in
+// every slot.
+template <class T> __device__ __forceinline__ const __attribute__((address_space(4))) T *kernel_args()
+{
+    auto p = (const __attribute__((address_space(4))) T *)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(p));
+    return p;
+}
+
 template <bool TF, bool WIDE, bool RC, bool ZR, bool OV>
 __device__ __forceinline__ void parametric_body(const ParArgs &g)
 {
@@ -1075,7 +1090,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     if (shared) {
         if (ok) {
             Ctx x = {};
-            make_ctx(M, g.c, st, x);
+            make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
             x.mlp = !TF;
             for (int key = s; key < kKeys; key += W) {
                 const bool bwd = key >= 2;
@@ -1181,7 +1196,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                     // finished gradient to the communication stream: walked
                     // op by op with both clocks, memory as it goes
                     Ctx x = {};
-                    make_ctx(M, g.c, st, x);
+                    make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
                     x.mlp = !TF;
                     Walk w{x, clk, live, live, 0, 0, nullptr};
                     w.tm = clkm;
@@ -1198,7 +1213,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                     double2 *pp = &L.a.prog[d][0][lane];
                     if ((bwd ? key_b : key_f) != key || (replay && bwd && key_f != mc)) {
                         Ctx x = {};
-                        make_ctx(M, g.c, st, x);
+                        make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
                         x.mlp = !TF;
                         if ((bwd ? key_b : key_f) != key) {
                             record_lane<TF, Sh>(x, s, bwd, m, acc, n, n_r, pp, L.a.sum[d][0][lane], L.a.sum[d][1][lane]);
@@ -1247,7 +1262,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
                 // stage ends its backward with its first unit
                 if (has_edges && (bwd ? key_b : key_f) != key) {
                     Ctx x = {};
-                    make_ctx(M, g.c, st, x);
+                    make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
                     x.mlp = !TF;
                     double *base = reinterpret_cast<double *>(ep);
                     Record rp{x, base, 2 * PST, 0, 0, 0};
@@ -1363,7 +1378,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     }
     if (live_stage && status == 0) {
         Ctx x = {};
-        make_ctx(M, g.c, st, x);
+        make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
         x.mlp = !TF;
         ZStage zs;
         if (ZR && x.zero) z_stage(x, s, zs);
