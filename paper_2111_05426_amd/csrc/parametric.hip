@@ -859,6 +859,83 @@ __device__ __forceinline__ double max_nn(double a, double b)
     return r;
 }
 
+// The Sends of one slot as prefix scans, exact.
+//
+// Along a run of linked Sends (positions r = 0, 1, ... in ascending source
+// stage), each Send starts at the later of the clock the previous Send left
+// on the shared stage and a clock no earlier Send of the run has touched,
+// and every stage it joins ends at start + cost:
+//   v_r = fl(max(v_{r-1}, z_r) + w_r),
+// z_r being the larger of the Send's own two stage clocks before the slot's
+// Sends (a stage without a Send that received one from its left carries
+// v_{r-1} on; any other position starts the recurrence afresh).  While every
+// v stays in the binade [2^E, 2^(E+1)) of the first one, rounding to nearest
+// adds each w_r as the whole number W_r of ulps 2^(E-52) nearest to it,
+// whatever v is, unless w_r lies exactly half way between two (then ties to
+// even depend on v).  In integer ulps K_r = z_r / ulp, with Q_r = W_0 + ... +
+// W_r, the recurrence is then v_r = Q_r + max_{i <= r} (K_i - Q_{i-1}): an
+// inclusive sum scan and an inclusive max scan, in exact integer-valued fp64
+// (below 2^53), over the positions of each segment.  A position that starts
+// afresh starts a segment.  Returns false, changing nothing, if some lane
+// leaves those conditions (a first value that is 0, not finite or below
+// 2^-1022; a cost that is not finite or a half-way case; a result past the
+// binade); the caller then walks the Sends step by step.  nlev: scan levels,
+// 2^nlev > the largest position.
+__device__ __forceinline__ bool send_scan(double &clk, int sdir, double scost, bool from_left, bool from_right,
+                                          int lane, int nlev)
+{
+    const double cl = shr1(clk), cr = shl1(clk);
+    const double z = sdir > 0 ? max_nn(clk, cr) : (sdir < 0 ? max_nn(clk, cl) : clk);
+    const bool carry = sdir < 0 || from_left;
+    const bool involved = sdir != 0 || from_left || from_right;
+    const uint64_t starts = ballot(!carry);
+    const uint64_t upto = starts & (lane == 63 ? ~0ull : ((2ull << lane) - 1));
+    const int spos = lane - (63 - __builtin_clzll(upto));
+    bool bad = false;
+    int e = INT_MIN;   // the binade of the segment's first value, at its first lane
+    if (!carry) {
+        e = 0;
+        if (involved) {
+            bad = !(z > 0.0 && z <= 0x1.fffffffffffffp+1023);
+            if (!bad) e = ilogb(z);
+            bad = bad || e < -1022;
+        }
+    }
+    for (int l = 0; l < nlev; ++l) {
+        const int o = 1 << l;
+        const int up = __shfl_up(e, (unsigned)o, kLanes);
+        if (spos >= o) e = e > up ? e : up;
+    }
+    const int sh = 52 - e;
+    const double K = ldexp(z, sh);
+    double w = 0.0;
+    if (sdir != 0) {
+        const double t = ldexp(scost, sh);
+        w = rint(t);
+        bad = bad || !(scost >= 0.0 && scost <= 0x1.fffffffffffffp+1023) || fabs(t - w) == 0.5;
+    }
+    double q = w;
+    for (int l = 0; l < nlev; ++l) {
+        const int o = 1 << l;
+        const double up = __shfl_up(q, (unsigned)o, kLanes);
+        if (spos >= o) q = q + up;
+    }
+    double y = K - (q - w);
+    for (int l = 0; l < nlev; ++l) {
+        const int o = 1 << l;
+        const double up = __shfl_up(y, (unsigned)o, kLanes);
+        if (spos >= o) y = y > up ? y : up;
+    }
+    const double v = q + y;
+    bad = bad || (involved && !(v < 0x1p53));
+    if (ballot(bad) != 0) return false;
+    const double vd = ldexp(v, -sh);
+    const double vr = shl1(vd);
+    if (from_right) clk = vr;
+    else if (sdir != 0 || from_left) clk = vd;
+    return true;
+}
+
 template <class T, class Op>
 __device__ __forceinline__ T seg_reduce(T v, int W, Op op)
 {
@@ -869,6 +946,7 @@ __device__ __forceinline__ T seg_reduce(T v, int W, Op op)
 // ---------------------------------------------------------------------------
 // The simulation kernel
 // ---------------------------------------------------------------------------
+constexpr int kScanMinRun = 12;   // the last run position from which the Sends take send_scan
 constexpr int kKeys = 6;          // forward: 2 row classes; backward: 2 row classes x accumulation
 constexpr int kMaxSegShared = 16; // segments of >= 4 lanes per wavefront
 
@@ -1352,6 +1430,8 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         int last = 0;
         for (int b = 32; b >= 1; b >>= 1)
             if (ballot(rpos >= last + b) != 0) last += b;
+        // long runs (pipeline fill and drain) take the scans, short ones the steps
+        if (last < kScanMinRun || !send_scan(clk, sdir, scost, from_left, from_right, lane, 32 - __clz(last))) {
         for (int r = 0; r <= last; ++r) {
             const bool src = rpos == r && sdir != 0;
             const double cl = shr1(clk), cr = shl1(clk);
@@ -1363,6 +1443,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
             // would first canonicalize both operands)
             const double e = max_nn(a, clk) + (src ? scost : (tl ? l_cost : r_cost));
             if (src || tl || tr) clk = e;
+        }
         }
         if (live_stage) {
             if (from_left) {

@@ -460,6 +460,7 @@ EDGE_DEVICES = [
     ("pow2_nolaunch", DeviceSpec(2.0 ** 44, 2.0 ** 40, 2.0 ** 32, 0.0, 0.0, 0)),
     ("near_overflow", DeviceSpec(1e-298, 1e-298, 1e-299, 0.0, 0.0, 0)),
     ("overflow", DeviceSpec(1e-299, 1e-299, 1e-300, 1e-6, 0.0, 0)),
+    ("default", DeviceSpec()),
 ]
 EDGE_MODELS = [
     ("tf_long", transformer(24, 64, 4, 16, 1000, 16, 2, TRAIN_ADAM), all_strats([1, 2], [1, 2, 4], [1, 2, 3], [1, 2, 5, 16])),
@@ -471,6 +472,16 @@ EDGE_MODELS = [
     ("mlp_long_rc", mlp(32, 128, 64, 2, TRAIN_ADAM, recompute=1), all_strats([1, 2], [1, 2], [1, 2, 4], [1, 3, 8, 32])),
     ("tf_long_zero", transformer(24, 64, 4, 16, 1000, 16, 2, TRAIN_ADAM, zero=1),
      all_strats([2, 4], [1, 2, 4], [1, 2, 3], [1, 2, 4])),
+    # deep pipelines: the Sends of pipeline fill and drain (and every
+    # forward and backward phase of GPipe) form runs of 12 and more, which
+    # the kernel sums as prefix scans while the clocks stay in one binade and
+    # no cost is a half-way case, else step by step; uneven microbatches
+    # (K = 7, 5, 3) give a run two costs
+    ("tf_deep_1f1b", transformer(64, 32, 4, 8, 100, 64, 2, TRAIN_ADAM),
+     all_strats([1, 2], [1, 2], [16, 32, 64], [1, 7, 32])),
+    ("tf_deep_gpipe", transformer(64, 32, 4, 8, 100, 64, 2, TRAIN_ADAM, schedule=SCHED_GPIPE),
+     all_strats([1], [1, 2], [16, 64], [5, 32])),
+    ("mlp_deep_infer", mlp(64, 64, 64, 2, INFER), all_strats([1, 2], [1], [32, 64], [3, 32])),
 ]
 
 
