@@ -978,12 +978,22 @@ def test_bounds(orc, case):
     r = orc.sim_strategy(m, D, H, P, K, DEV)
     res, pk = r["dev_resident"], r["dev_peak"]
     assert np.all(pk >= res)
-    # total work bounds the makespan from above; the busiest device from below
-    zero = {k: 0.0 for k in orc.TYPES}
     assert r["makespan"] > 0
-    assert r["makespan"] <= sum(r["stage_finish"]) * D * H + 1e-30
     assert r["makespan"] == max(r["dev_finish"])
-    del zero
+    # Every op of every type costing 1 (Sec. 2.1 semantics): an op starts
+    # when the last of its devices is free, so after i ops of the program no
+    # clock is past i, and the makespan is at most the program's op count;
+    # a device runs its ops one after another and every op occupies at
+    # least one device, so the busiest device holds at least the op count
+    # over the device count.  Both are whole numbers of ops.
+    u = orc.sim_strategy(m, D, H, P, K, DEV, type_cost={k: 1.0 for k in orc.TYPES})
+    n_dev = len(u["dev_finish"])
+    assert u["status"] == 0 and u["n_ops"] == r["n_ops"]
+    assert u["makespan"] == np.floor(u["makespan"]) and np.all(u["dev_finish"] == np.floor(u["dev_finish"]))
+    assert u["n_ops"] / n_dev <= u["makespan"] <= u["n_ops"]
+    # and a single device runs the whole program serially
+    one = orc.sim_strategy(m, 1, 1, 1, K, DEV, type_cost={k: 1.0 for k in orc.TYPES})
+    assert one["makespan"] == one["n_ops"]
 
 
 # ---------------------------------------------------------------------------
