@@ -946,6 +946,10 @@ __device__ __forceinline__ T seg_reduce(T v, int W, Op op)
 // ---------------------------------------------------------------------------
 // The simulation kernel
 // ---------------------------------------------------------------------------
+// a wavefront whose blocks repeat a unit at least this many times sums the
+// repeats binade-wise (units_exact), else unit by unit: below it the walk's
+// dependent adds cost less than the binade arithmetic
+constexpr int kFastUnits = 12;
 constexpr int kScanMinRun = 12;   // the last run position from which the Sends take send_scan
 constexpr int kKeys = 6;          // forward: 2 row classes; backward: 2 row classes x accumulation
 constexpr int kMaxSegShared = 16; // segments of >= 4 lanes per wavefront
@@ -1252,12 +1256,12 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         const bool all_fwd = ballot(ready && bwd) == 0;
 
         // long unit runs take the binade-wise path (uniform per wavefront)
-        const bool fast = ballot(ready && (bwd ? n_b : n_f) >= 3) != 0;
+        const bool fast = ballot(ready && (bwd ? n_b : n_f) >= kFastUnits) != 0;
         // under recomputation a wave with backward blocks walks the pre ops
         // and the replay first (forward lanes: their pre ops, no units), then
         // every lane's units and suf
         const bool replay = rc && !all_fwd;
-        const bool fast_r = replay && ballot(ready && bwd && n_r >= 3) != 0;
+        const bool fast_r = replay && ballot(ready && bwd && n_r >= kFastUnits) != 0;
         const int d = bwd ? 1 : 0;
         const int mc = k < mr ? 1 : 0;
         const uint64_t m = mq + (uint64_t)mc;
