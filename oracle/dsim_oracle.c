@@ -385,9 +385,12 @@ int or_sim_table(int64_t n_ops, int n_dev,
 /* Draws: r(c, j, f) is output number c*2^32 + j*2^5 + f + 1 of SplitMix64   */
 /* (Steele, Lea & Flood 2014) started from `seed`, i.e.                     */
 /* mix(seed + n * 0x9E3779B97F4A7C15).  range(r, n) = floor(hi32(r) * n /   */
-/* 2^32).  Log-uniform positive floats in [lo, hi] are drawn uniformly over */
-/* the fp32 bit patterns between lo and hi (equal mass per binade, the     */
-/* linear 2^f ~ 1 + f mantissa).                                            */
+/* 2^32).  A log-uniform float in [lo, hi] is 2^t rounded to fp32, with    */
+/* t = L(lo) + u (L(hi) - L(lo)), u = the top 53 bits of the draw / 2^53   */
+/* and L(b) the base-2 logarithm of the bound to double precision; 2^t =   */
+/* 2^floor(t) * e^(f ln 2), f = t - floor(t), with the exponential summed   */
+/* as its Taylor series up to the 13th power in Horner form (truncation     */
+/* below 1e-13 relative), all in fp64 without contraction.                  */
 /* ------------------------------------------------------------------------ */
 #define GEN_SLOTS 16
 static uint64_t sm64_at(uint64_t seed, uint64_t n)
@@ -411,14 +414,33 @@ static uint32_t urange(uint64_t r, uint32_t n)
     return (uint32_t)(((r >> 32) * (uint64_t)n) >> 32);
 }
 
-static float f32_of_bits(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
-static uint32_t bits_of_f32(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
 
-static float log_uniform(uint64_t r, float lo, float hi)
+/* base-2 logarithms of the bounds 1e3, 1e6, 1e9, 1e12 (nearest doubles) */
+#define LOG2_1E3 0x1.3ee7b471b3a95p+3
+#define LOG2_1E6 0x1.3ee7b471b3a95p+4
+#define LOG2_1E9 0x1.de5b8eaa8d7e0p+4
+#define LOG2_1E12 0x1.3ee7b471b3a95p+5
+
+/* e^y for 0 <= y < ln 2: sum of y^k / k!, k = 0..13, Horner form */
+static double exp_series(double y)
 {
-    uint32_t blo = bits_of_f32(lo), bhi = bits_of_f32(hi);
-    uint32_t span = bhi - blo + 1u;
-    return f32_of_bits(blo + urange(r, span));
+    static const double inv_fact[14] = {
+        1.0, 1.0, 0.5, 0x1.5555555555555p-3, 0x1.5555555555555p-5, 0x1.1111111111111p-7,
+        0x1.6c16c16c16c17p-10, 0x1.a01a01a01a01ap-13, 0x1.a01a01a01a01ap-16, 0x1.71de3a556c734p-19,
+        0x1.27e4fb7789f5cp-22, 0x1.ae64567f544e4p-26, 0x1.1eed8eff8d898p-29, 0x1.6124613a86d09p-33};
+    double s = inv_fact[13];
+    int k;
+    for (k = 12; k >= 0; k--) s = s * y + inv_fact[k];
+    return s;
+}
+
+static float log_uniform(uint64_t r, double log2_lo, double log2_hi)
+{
+    const double ln2 = 0x1.62e42fefa39efp-1;
+    double u = (double)(r >> 11) * 0x1p-53;
+    double t = log2_lo + u * (log2_hi - log2_lo);
+    double n = floor(t);
+    return (float)ldexp(exp_series((t - n) * ln2), (int)n);
 }
 
 /* the i-th (ascending) n_dev-bit mask with at least two bits set */
@@ -467,15 +489,15 @@ int or_gen_table(uint64_t seed, int64_t cand, int32_t n_ops, int32_t n_dev,
         if (kd < 7) {
             uint64_t r6 = draw(seed, c, (uint64_t)j, 6);
             code[o] = 0u | (a << 8);
-            flops[o] = log_uniform(draw(seed, c, (uint64_t)j, 3), 1e6f, 1e12f);
-            bytes[o] = log_uniform(draw(seed, c, (uint64_t)j, 4), 1e3f, 1e9f);
+            flops[o] = log_uniform(draw(seed, c, (uint64_t)j, 3), LOG2_1E6, LOG2_1E12);
+            bytes[o] = log_uniform(draw(seed, c, (uint64_t)j, 4), LOG2_1E3, LOG2_1E9);
             if ((r6 >> 63) && cnt[a] < GEN_SLOTS) {
-                al = (uint32_t)log_uniform(draw(seed, c, (uint64_t)j, 7), 1e3f, 1e9f);
+                al = (uint32_t)log_uniform(draw(seed, c, (uint64_t)j, 7), LOG2_1E3, LOG2_1E9);
                 slot[a][cnt[a]++] = al;
             }
         } else if (kd < 9) {
             uint32_t b = (a + 1u + urange(draw(seed, c, (uint64_t)j, 2), (uint32_t)(n_dev - 1))) % (uint32_t)n_dev;
-            uint32_t msg = (uint32_t)log_uniform(draw(seed, c, (uint64_t)j, 7), 1e3f, 1e9f);
+            uint32_t msg = (uint32_t)log_uniform(draw(seed, c, (uint64_t)j, 7), LOG2_1E3, LOG2_1E9);
             code[o] = 1u | (a << 8) | (b << 16);
             flops[o] = 0.0f;
             bytes[o] = (float)msg;
@@ -487,7 +509,7 @@ int or_gen_table(uint64_t seed, int64_t cand, int32_t n_ops, int32_t n_dev,
             uint32_t mask = nth_group_mask(n_dev, urange(draw(seed, c, (uint64_t)j, 2), n_masks));
             code[o] = 2u | (mask << 16);
             flops[o] = 0.0f;
-            bytes[o] = log_uniform(draw(seed, c, (uint64_t)j, 4), 1e3f, 1e9f);
+            bytes[o] = log_uniform(draw(seed, c, (uint64_t)j, 4), LOG2_1E3, LOG2_1E9);
         }
         alloc[o] = al;
         freeb[o] = fr;

@@ -1511,12 +1511,57 @@ def test_generator_shape(orc):
 
 
 def test_generator_log_uniform(orc):
-    """Equal mass per binade of [1e3, 1e9] bytes (log-uniform at binade scale)."""
-    vals = np.concatenate([orc.gen_table(7, c, 2048, 8)["bytes"] for c in range(20)])
-    e = np.floor(np.log2(vals.astype(np.float64)))
+    """Log-uniform bytes in [1e3, 1e9]: equal mass per binade, and inside a
+    binade a density proportional to 1/x, so log2(1.5) = 0.585 of a binade's
+    mass lies below 1.5 times its base (a mantissa uniform over the fp32 bit
+    patterns would put 0.5 there); ln x is uniform on [ln 1e3, ln 1e9]
+    (Kolmogorov-Smirnov distance)."""
+    tabs = [orc.gen_table(7, c, 2048, 8) for c in range(20)]
+    vals = np.concatenate([t["bytes"][(t["code"] & 0xff) != 1] for t in tabs]).astype(np.float64)
+    e = np.floor(np.log2(vals))
     lo, hi = int(np.ceil(np.log2(1e3))), int(np.floor(np.log2(1e9))) - 1
+    full = (e >= lo) & (e <= hi)
     counts = np.array([(e == k).sum() for k in range(lo, hi + 1)])
     assert counts.min() > 0.9 * counts.mean() and counts.max() < 1.1 * counts.mean()
+    below = np.mean(vals[full] < 1.5 * 2.0 ** e[full])
+    assert abs(below - np.log2(1.5)) < 0.01, below
+    x = np.sort((np.log(vals) - np.log(1e3)) / (np.log(1e9) - np.log(1e3)))
+    n = len(x)
+    ks = max(np.max(np.arange(1, n + 1) / n - x), np.max(x - np.arange(n) / n))
+    assert ks < 1.95 / np.sqrt(n), ks
+
+
+def test_generator_log_uniform_transform(orc):
+    """The draw behind each log-uniform value, recomputed here from the
+    SplitMix64 outputs: u = top 53 bits / 2^53, t = log2 lo + u (log2 hi -
+    log2 lo), value = 2^t rounded to fp32 (Python's own power function), for
+    the bytes (draw 4) of compute and all-reduce ops and the FLOPs (draw 3)
+    of compute ops: equal but for 2^t within a hair of a rounding boundary,
+    never more than one fp32 step apart."""
+    import ctypes as C
+    sm = orc.lib().or_splitmix64
+    sm.restype = C.c_uint64
+    sm.argtypes = [C.c_uint64, C.c_uint64]
+    seed, n_ops = 5, 2048
+    l3, l6, l9, l12 = np.log2(1e3), np.log2(1e6), np.log2(1e9), np.log2(1e12)
+    same = total = 0
+    for c in range(3):
+        tab = orc.gen_table(seed, c, n_ops, 8)
+        for j in range(n_ops):
+            base = (c << 32) + (j << 5) + 1
+            kd = ((sm(seed, base) >> 32) * 10) >> 32
+            checks = []
+            if kd < 7:
+                checks.append((tab["flops"][j], sm(seed, base + 3), l6, l12))
+            if kd < 7 or kd == 9:
+                checks.append((tab["bytes"][j], sm(seed, base + 4), l3, l9))
+            for got, r, a, b in checks:
+                u = float(r >> 11) * 2.0 ** -53
+                want = np.float32(2.0 ** (a + u * (b - a)))
+                total += 1
+                same += int(got == want)
+                assert abs(int(np.float32(got).view(np.int32)) - int(want.view(np.int32))) <= 1
+    assert same >= total - 5, (same, total)
 
 
 def test_generator_prng_reference_outputs(orc):
