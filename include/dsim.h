@@ -448,7 +448,9 @@ DSIM_API dsim_status dsim_argmin(const double *makespan, const uint64_t *cand_pe
  * op then allocates a new buffer with probability 1/2, and a send's message
  * (its bytes) becomes a live buffer of the destination, each only while the
  * device holds fewer than 16.
- * Log-uniform means uniform over the fp32 bit patterns between the bounds.
+ * Log-uniform in [lo, hi]: 2^t rounded to fp32, t = log2 lo + u (log2 hi -
+ * log2 lo), u = the top 53 bits of the draw / 2^53 (2^t from a fixed fp64
+ * Taylor series, reproducible bit for bit).
  * Constraints: 2 <= n_dev <= 8, 0 <= n_ops < 2^27, 0 <= n_cand <= 2^32 - 256.
  */
 DSIM_API dsim_status dsim_generate_random_tables(uint64_t seed, int64_t n_cand, int32_t n_ops,

@@ -20,8 +20,11 @@
 //   7 size of the new buffer (compute) or of the message (send), log-uniform
 //     in [1e3, 1e9] bytes; a send's message becomes a live buffer of the
 //     destination when the destination has < 16
-// Log-uniform in [lo, hi] means uniform over the fp32 bit patterns between lo
-// and hi: equal mass per binade, linear mantissa inside a binade.
+// Log-uniform in [lo, hi]: 2^t rounded once to fp32, t = log2(lo) + u
+// (log2(hi) - log2(lo)) with u the top 53 bits of the draw over 2^53 and
+// the logarithms taken as the nearest doubles; 2^t = 2^floor(t) e^(y),
+// y = (t - floor(t)) ln 2, e^y summed as its Taylor series up to y^13
+// (Horner form, fp64, no contraction: the oracle computes the same bits).
 #include "internal.h"
 
 namespace dsim {
@@ -55,10 +58,25 @@ __device__ __forceinline__ uint32_t pick(uint64_t r, uint32_t n)
     return (uint32_t)(((r >> 32) * (uint64_t)n) >> 32);
 }
 
-__device__ __forceinline__ float log_uniform(uint64_t r, float lo, float hi)
+// base-2 logarithms of the bounds (nearest doubles)
+constexpr double kLog2_1e3 = 0x1.3ee7b471b3a95p+3, kLog2_1e6 = 0x1.3ee7b471b3a95p+4;
+constexpr double kLog2_1e9 = 0x1.de5b8eaa8d7e0p+4, kLog2_1e12 = 0x1.3ee7b471b3a95p+5;
+
+__device__ __forceinline__ float log_uniform(uint64_t r, double log2_lo, double log2_hi)
 {
-    const uint32_t blo = __float_as_uint(lo), bhi = __float_as_uint(hi);
-    return __uint_as_float(blo + pick(r, bhi - blo + 1u));
+    // 1 / k! for k = 13 down to 0
+    constexpr double c[14] = {0x1.6124613a86d09p-33, 0x1.1eed8eff8d898p-29, 0x1.ae64567f544e4p-26,
+                              0x1.27e4fb7789f5cp-22, 0x1.71de3a556c734p-19, 0x1.a01a01a01a01ap-16,
+                              0x1.a01a01a01a01ap-13, 0x1.6c16c16c16c17p-10, 0x1.1111111111111p-7,
+                              0x1.5555555555555p-5, 0x1.5555555555555p-3, 0.5, 1.0, 1.0};
+    const double u = (double)(r >> 11) * 0x1p-53;
+    const double t = log2_lo + u * (log2_hi - log2_lo);
+    const double n = floor(t);
+    const double y = (t - n) * 0x1.62e42fefa39efp-1;
+    double e = c[0];
+#pragma unroll
+    for (int k = 1; k < 14; ++k) e = e * y + c[k];
+    return (float)ldexp(e, (int)n);
 }
 
 __global__ __launch_bounds__(kGenBlock) void k_gen_tables(const GenArgs g)
@@ -105,17 +123,17 @@ __global__ __launch_bounds__(kGenBlock) void k_gen_tables(const GenArgs g)
         if (kd < 7u) {
             const uint64_t r6 = splitmix_at(seed, base + 6);
             code = a << 8;
-            fl = log_uniform(splitmix_at(seed, base + 3), 1e6f, 1e12f);
-            by = log_uniform(splitmix_at(seed, base + 4), 1e3f, 1e9f);
+            fl = log_uniform(splitmix_at(seed, base + 3), kLog2_1e6, kLog2_1e12);
+            by = log_uniform(splitmix_at(seed, base + 4), kLog2_1e3, kLog2_1e9);
             const uint32_t na = s_cnt[a][tid];
             if ((r6 >> 63) && na < (uint32_t)kSlots) {
-                al = (uint32_t)log_uniform(splitmix_at(seed, base + 7), 1e3f, 1e9f);
+                al = (uint32_t)log_uniform(splitmix_at(seed, base + 7), kLog2_1e3, kLog2_1e9);
                 s_buf[a][na][tid] = al;
                 s_cnt[a][tid] = na + 1u;
             }
         } else if (kd < 9u) {
             const uint32_t b = (a + 1u + pick(splitmix_at(seed, base + 2), nd - 1u)) % nd;
-            const uint32_t msg = (uint32_t)log_uniform(splitmix_at(seed, base + 7), 1e3f, 1e9f);
+            const uint32_t msg = (uint32_t)log_uniform(splitmix_at(seed, base + 7), kLog2_1e3, kLog2_1e9);
             code = 1u | (a << 8) | (b << 16);
             by = (float)msg;
             const uint32_t nb = s_cnt[b][tid];
@@ -127,7 +145,7 @@ __global__ __launch_bounds__(kGenBlock) void k_gen_tables(const GenArgs g)
         } else {
             const uint32_t mask = s_masks[pick(splitmix_at(seed, base + 2), n_masks)];
             code = 2u | (mask << 16);
-            by = log_uniform(splitmix_at(seed, base + 4), 1e3f, 1e9f);
+            by = log_uniform(splitmix_at(seed, base + 4), kLog2_1e3, kLog2_1e9);
         }
         const size_t o = (size_t)j * N + (size_t)cand;
         __builtin_nontemporal_store(code, g.code + o);
