@@ -235,8 +235,13 @@ def bench_parametric(torch, dsim, W, reps, warmup=1, cpu_budget_s=0.0):
         step(True)
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t0
-    kern_ms = sum(a.elapsed_time(b) for a, b, _ in ev) / len(ev)
-    step_ms = sum(a.elapsed_time(c) for a, _, c in ev) / len(ev)
+    # per-call times from HIP events on the launch stream; the median over the
+    # calls is reported (a call's events also count any gap in which the GPU
+    # waits for the host to enqueue it, which now and then adds tens of ms)
+    kern_reps = sorted(a.elapsed_time(b) for a, b, _ in ev)
+    step_reps = sorted(a.elapsed_time(c) for a, _, c in ev)
+    kern_ms = kern_reps[len(kern_reps) // 2]
+    step_ms = step_reps[len(step_reps) // 2]
     projected = int(res["walked_ops"].sum().item())
     prog = int(res["n_ops"].sum().item())
     ok = int((res["status"] == 0).sum().item())
@@ -245,7 +250,8 @@ def bench_parametric(torch, dsim, W, reps, warmup=1, cpu_budget_s=0.0):
                     "makespan_s": float(out_mk[0].item())} if int(found.item()) > 0 else None,
            "kernel_ms": kern_ms, "step_ms": step_ms, "candidates_per_s": n / (step_ms * 1e-3),
            "projected_ops": projected, "projected_ops_per_s": projected / (kern_ms * 1e-3),
-           "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3), "wall_s": wall_s, "reps": reps}
+           "program_ops": prog, "program_ops_per_s": prog / (kern_ms * 1e-3), "wall_s": wall_s, "reps": reps,
+           "kernel_ms_reps": kern_reps, "kernel_ms_mean": sum(kern_reps) / len(kern_reps)}
     rec = stored_valu(W.name)
     achieved = rec["valu_insts_per_call"] * 64 / (kern_ms * 1e-3) / 1e12 if rec else None
     out["roofline"] = {"bound": "alu", "achieved": achieved, "peak": VALU_PEAK_T,
@@ -412,7 +418,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parametric", action="store_true",
                     help="skip the per-grid timings of the transform-driven kernel")
-    ap.add_argument("--param-reps", type=int, default=5)
+    ap.add_argument("--param-reps", type=int, default=7)
     ap.add_argument("--no-copy", action="store_true",
                     help="skip the plain 4 GiB device-to-device copy timed beside the kernel")
     ap.add_argument("--copy-calibration", action="store_true",
