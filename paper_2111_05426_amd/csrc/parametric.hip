@@ -978,19 +978,23 @@ template <class Sh> union LdsNarrow {
     LdsSeg<Sh> b;
 };
 
-// Wide segments (>= 8 lanes, transformer): at most 8 segments per
+// Wide segments (>= 16 lanes, transformer): at most 4 segments per
 // wavefront, and only stages 0 and P-1 have edge ops, so the edge programs
-// are kept per segment; middle stages walk a zero program.  About 14 KB,
-// which lets two wavefronts share a SIMD.
-constexpr int kMaxSegWide = 8;
-constexpr int kFirstWideClass = 3;   // segment width 8
+// are kept per segment; middle stages walk a zero program.  About 7 KB.
+// Their stages hold few layers, so the kernel adds units one by one: without
+// the binade arithmetic's registers four wavefronts share a SIMD.  With the
+// overlapped gradient all-reduce the wide kernel keeps that arithmetic (its
+// registers are taken anyway) and also takes segments of 8 lanes (8 per
+// wavefront, about 14 KB).
+template <bool OV> constexpr int first_wide_class() { return OV ? 3 : 4; }   // segment width 8 / 16
+inline int first_wide_class(bool ov) { return ov ? 3 : 4; }
 constexpr int64_t kSplitMinCand = 8192;
-template <class Sh> struct LdsWide {
-    double2 unit[kMaxSegWide][kKeys][Sh::U2];
-    int64_t usum[kMaxSegWide][kKeys][2];
-    int64_t xsum[kMaxSegWide][2][6];
-    double2 edge[kMaxSegWide][2][2][Sh::PRE2 + Sh::SUF2];   // [segment][stage 0, P-1][backward]
-    int64_t esum[kMaxSegWide][2][2][4];
+template <class Sh, int NS> struct LdsWide {
+    double2 unit[NS][kKeys][Sh::U2];
+    int64_t usum[NS][kKeys][2];
+    int64_t xsum[NS][2][6];
+    double2 edge[NS][2][2][Sh::PRE2 + Sh::SUF2];   // [segment][stage 0, P-1][backward]
+    int64_t esum[NS][2][2][4];
     double2 zero[Sh::PRE2 + Sh::SUF2];
     int64_t zsum[4];
 };
@@ -1059,7 +1063,8 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
 {
     using Sh = Shape<TF, ZR>;
     constexpr int PST = WIDE ? 1 : kLanes;   // double2 stride of a lane's edge program
-    __shared__ typename std::conditional<WIDE, LdsWide<Sh>, LdsNarrow<Sh>>::type L;
+    // at most 64 / 2^(first wide class) segments per wide wavefront
+    __shared__ typename std::conditional<WIDE, LdsWide<Sh, (kLanes >> first_wide_class<OV>())>, LdsNarrow<Sh>>::type L;
 
     const int lane = threadIdx.x;
     // wavefronts start widest class first (the wide launch, or the only
@@ -1067,13 +1072,16 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     // shortens the tail.  The grid is sized for the worst case; the
     // wavefronts beyond the last class exit, and come last in either order.
     const bool widest_first = WIDE || g.narrow_end == kClasses;
+    // the binade-wise unit sums: not in the wide kernels (but in the one
+    // with the overlapped all-reduce, whose registers it does not raise)
+    constexpr bool kBinadeSums = !WIDE || OV;
     const uint32_t nw = g.meta[16 + kClasses] / (uint32_t)kLanes;   // wavefronts holding classes
     if (blockIdx.x >= nw) return;
     const uint32_t blk = widest_first ? nw - 1 - blockIdx.x : blockIdx.x;
     const uint32_t gl = blk * (uint32_t)kLanes;
     int cls = 0;
     while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
-    if (WIDE ? cls < kFirstWideClass : cls >= g.narrow_end) return;   // the other launch's classes
+    if (WIDE ? cls < first_wide_class<OV>() : cls >= g.narrow_end) return;   // the other launch's classes
     const int W = 1 << cls;
     const bool shared = WIDE || W >= 4;
     const uint32_t local = gl + lane - g.meta[16 + cls];
@@ -1256,12 +1264,12 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
         const bool all_fwd = ballot(ready && bwd) == 0;
 
         // long unit runs take the binade-wise path (uniform per wavefront)
-        const bool fast = ballot(ready && (bwd ? n_b : n_f) >= kFastUnits) != 0;
+        const bool fast = kBinadeSums && ballot(ready && (bwd ? n_b : n_f) >= kFastUnits) != 0;
         // under recomputation a wave with backward blocks walks the pre ops
         // and the replay first (forward lanes: their pre ops, no units), then
         // every lane's units and suf
         const bool replay = rc && !all_fwd;
-        const bool fast_r = replay && ballot(ready && bwd && n_r >= kFastUnits) != 0;
+        const bool fast_r = kBinadeSums && replay && ballot(ready && bwd && n_r >= kFastUnits) != 0;
         const int d = bwd ? 1 : 0;
         const int mc = k < mr ? 1 : 0;
         const uint64_t m = mq + (uint64_t)mc;
@@ -1463,7 +1471,15 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     }
     if (live_stage && status == 0) {
         Ctx x = {};
-        make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
+        // (the narrow kernels of the transformer's recomputation, ZeRO and
+        // overlap variants and of the MLP's recomputation keep these values
+        // live across the loop instead: reading the argument block again
+        // here makes the register allocator reserve a private frame that no
+        // instruction uses)
+        if constexpr (WIDE || (!RC && !(TF && (ZR || OV))))
+            make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
+        else
+            make_ctx(M, g.c, st, x);
         x.mlp = !TF;
         ZStage zs;
         if (ZR && x.zero) z_stage(x, s, zs);
@@ -1717,7 +1733,7 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     // SIMD) when the caller gives a second stream, else after them on the
     // one stream.  Small grids and MLPs take one launch for every class.
     const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
-    g.narrow_end = split ? kFirstWideClass : kClasses;
+    g.narrow_end = split ? first_wide_class(m.mode != DSIM_INFER && m.overlap != 0) : kClasses;
     const bool rc = m.mode != DSIM_INFER && m.recompute != 0;
     const bool zr = m.mode != DSIM_INFER && m.zero != 0;
     const bool ov = m.mode != DSIM_INFER && m.overlap != 0;
@@ -1729,9 +1745,9 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
         e = hipGetLastError();
         return e == hipSuccess ? DSIM_OK : hip_fail(e, "parametric launch");
     }
-    // the narrow classes (1, 2, 4 lanes per candidate) come first in the
+    // the narrow classes (1 to 8 lanes per candidate) come first in the
     // class layout: a grid over their lanes is enough
-    const int64_t narrow_waves = (n_cand * 4 + kLanes - 1) / kLanes + kClasses;
+    const int64_t narrow_waves = (n_cand * (1 << (g.narrow_end - 1)) + kLanes - 1) / kLanes + kClasses;
     const dim3 grid_n((unsigned)(narrow_waves < waves ? narrow_waves : waves));
     if (!side || side == s) {
         launch_kernel(rc, zr, ov, true, true, grid, block, s, g);
