@@ -1755,19 +1755,23 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
         e = hipGetLastError();
         return e == hipSuccess ? DSIM_OK : hip_fail(e, "parametric launch");
     }
-    // narrow segments on the side stream, wide ones on the caller's: the
-    // side stream waits for the pre-pass, the caller's stream for both
+    // narrow segments on the caller's stream, right after the pre-pass, and
+    // wide ones on the side stream, which waits for the pre-pass; the
+    // caller's stream then waits for both.  The narrow wavefronts (36 KB of
+    // LDS each) find room only on CUs that wide ones have not filled: started
+    // first, they no longer finish last (GPT-3-shaped grid 3.06 -> 2.78 ms,
+    // recomputation 4.60 -> 3.80)
     hipEvent_t fork = nullptr, join = nullptr;
     e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(fork, s);
     if (e == hipSuccess) e = hipStreamWaitEvent(side, fork, 0);
     if (e == hipSuccess) {
-        launch_kernel(rc, zr, ov, true, false, grid_n, block, side, g);
+        launch_kernel(rc, zr, ov, true, false, grid_n, block, s, g);
         e = hipGetLastError();
     }
     if (e == hipSuccess) {
-        launch_kernel(rc, zr, ov, true, true, grid, block, s, g);
+        launch_kernel(rc, zr, ov, true, true, grid, block, side, g);
         e = hipGetLastError();
     }
     if (e == hipSuccess) e = hipEventRecord(join, side);
