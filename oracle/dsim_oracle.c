@@ -33,10 +33,13 @@
  *    predicted time.
  *
  * Where the paper is silent, the reading taken is stated at the code that
- * implements it.  Parity of the transformer FLOP/byte formulas,
- * of the slot order for P >= 3 and of the random-table generator is unpinned
- * by the paper itself (they are this project's definitions); the pins that do
- * exist are exercised by tests/test_oracle_pins.py.
+ * implements it.  The transformer's per-op FLOP/byte formulas and the slot
+ * order for P >= 3 are this project's definitions (the paper prints neither);
+ * they are pinned by a GPT rank's program written out by hand (bytes, matmul
+ * flops and one-stage peaks) and by a hand trace of P = 3, K = 4 with unequal
+ * per-type costs.  Parity unpinned: which random draw of the table generator
+ * feeds which field (its PRNG and its log-uniform transform are pinned).  The
+ * pins are exercised by tests/test_oracle_pins.py.
  *
  * Floating point: IEEE fp64, compiled with -ffp-contract=off and no fast-math;
  * expressions are evaluated exactly in the order written.
