@@ -850,6 +850,60 @@ __device__ __forceinline__ uint64_t shl1(uint64_t v)
 
 __device__ __forceinline__ uint64_t ballot(bool b) { return __ballot(b); }
 
+// DPP moves within the wavefront: row_shr:n (0x110 + n, lane i of a row of
+// 16 receives lane i - n of the same row), row_bcast:15 (0x142, lane 15 of
+// each row into the next row; rows 1 and 3 written) and row_bcast:31 (0x143,
+// lane 31 into rows 2 and 3).  Rows outside ROWS, and lanes whose source
+// lies outside the row, receive 0.
+template <int CTRL, int ROWS> __device__ __forceinline__ int dpp(int v)
+{
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xf, true);
+}
+template <int CTRL, int ROWS> __device__ __forceinline__ double dpp(double v)
+{
+    return __hiloint2double(dpp<CTRL, ROWS>(__double2hiint(v)), dpp<CTRL, ROWS>(__double2loint(v)));
+}
+
+// Inclusive scan by op over the segments of the wavefront: each lane
+// combines the values of its segment from the segment's first lane (spos = 0
+// there) up to itself.  Rows of 16 lanes scan first, treating a row's first
+// lane as a segment start (shift-and-combine over 2^nlev > the largest spos
+// positions); then lanes whose segment began in an earlier row take the
+// carries, lane 15 of rows 0 and 2 into rows 1 and 3, then lane 31 into rows
+// 2 and 3 (cross: some segment spans a row boundary; nlev and cross are
+// uniform).  op is exact and associative on the values met, so the result is
+// the plain left-to-right one.
+template <class T, class Op>
+__device__ __forceinline__ T seg_scan(T v, int spos, int lane, int nlev, bool cross, Op op)
+{
+    const int rl = lane & 15;
+    const int sr = spos < rl ? spos : rl;
+    T up;
+    if (nlev > 0) {
+        up = dpp<0x111, 0xf>(v);
+        v = sr >= 1 ? op(v, up) : v;
+    }
+    if (nlev > 1) {
+        up = dpp<0x112, 0xf>(v);
+        v = sr >= 2 ? op(v, up) : v;
+    }
+    if (nlev > 2) {
+        up = dpp<0x114, 0xf>(v);
+        v = sr >= 4 ? op(v, up) : v;
+    }
+    if (nlev > 3) {
+        up = dpp<0x118, 0xf>(v);
+        v = sr >= 8 ? op(v, up) : v;
+    }
+    if (cross) {
+        up = dpp<0x142, 0xa>(v);
+        v = ((lane & 16) != 0 && spos > rl) ? op(v, up) : v;
+        up = dpp<0x143, 0xc>(v);
+        v = (lane >= 32 && spos >= lane - 31) ? op(v, up) : v;
+    }
+    return v;
+}
+
 // max of two clocks, which are never NaN or -0.0: the bare instruction
 // (fmax would canonicalize both operands first, two more dependent steps)
 __device__ __forceinline__ double max_nn(double a, double b)
@@ -901,11 +955,8 @@ __device__ __forceinline__ bool send_scan(double &clk, int sdir, double scost, b
             bad = bad || e < -1022;
         }
     }
-    for (int l = 0; l < nlev; ++l) {
-        const int o = 1 << l;
-        const int up = __shfl_up(e, (unsigned)o, kLanes);
-        if (spos >= o) e = e > up ? e : up;
-    }
+    const bool cross = ballot(spos > (lane & 15)) != 0;
+    e = seg_scan(e, spos, lane, nlev, cross, [](int a, int b) { return a > b ? a : b; });
     const int sh = 52 - e;
     const double K = ldexp(z, sh);
     double w = 0.0;
@@ -914,18 +965,8 @@ __device__ __forceinline__ bool send_scan(double &clk, int sdir, double scost, b
         w = rint(t);
         bad = bad || !(scost >= 0.0 && scost <= 0x1.fffffffffffffp+1023) || fabs(t - w) == 0.5;
     }
-    double q = w;
-    for (int l = 0; l < nlev; ++l) {
-        const int o = 1 << l;
-        const double up = __shfl_up(q, (unsigned)o, kLanes);
-        if (spos >= o) q = q + up;
-    }
-    double y = K - (q - w);
-    for (int l = 0; l < nlev; ++l) {
-        const int o = 1 << l;
-        const double up = __shfl_up(y, (unsigned)o, kLanes);
-        if (spos >= o) y = y > up ? y : up;
-    }
+    const double q = seg_scan(w, spos, lane, nlev, cross, [](double a, double b) { return a + b; });
+    const double y = seg_scan(K - (q - w), spos, lane, nlev, cross, [](double a, double b) { return a > b ? a : b; });
     const double v = q + y;
     bad = bad || (involved && !(v < 0x1p53));
     if (ballot(bad) != 0) return false;
