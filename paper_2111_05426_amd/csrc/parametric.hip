@@ -1512,12 +1512,10 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     }
     if (live_stage && status == 0) {
         Ctx x = {};
-        // (the narrow kernels of the transformer's recomputation, ZeRO and
-        // overlap variants and of the MLP's recomputation keep these values
-        // live across the loop instead: reading the argument block again
-        // here makes the register allocator reserve a private frame that no
-        // instruction uses)
-        if constexpr (WIDE || (!RC && !(TF && (ZR || OV))))
+        // (the narrow kernels keep these values live across the loop
+        // instead: reading the argument block again here makes the register
+        // allocator reserve a private frame that no instruction uses)
+        if constexpr (WIDE)
             make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
         else
             make_ctx(M, g.c, st, x);
