@@ -5,7 +5,8 @@ and both end together; the slot's Sends run in ascending source order).
 
 Both functions below restate, for one 64-lane wavefront, what the kernel
 computes: `steps` the run-parallel loop, `scan` the segmented prefix scans
-in integer ulps.  Neither calls the library or the oracle; the GPU parity
+in integer ulps, each scan taken the way the kernel takes it (`seg_scan`:
+rows of 16 lanes first, then the carries of row_bcast:15 and row_bcast:31).  Neither calls the library or the oracle; the GPU parity
 tests check the kernel itself.  Here the model of the scan must give the
 same doubles as the step walk whenever it does not decline, on random slots
 with dead lanes, partial segments, both directions, pairs of opposite Sends,
@@ -39,6 +40,32 @@ def _positions(start_flags):
             st = i
         pos.append(i - st)
     return pos
+
+
+def seg_scan(v, spos, nlev, op):
+    """`seg_scan` of the kernel, lane by lane: DPP row_shr:o moves stay inside
+    rows of 16 lanes, row_bcast:15 hands lane 15 of rows 0 and 2 to rows 1
+    and 3, row_bcast:31 hands lane 31 to rows 2 and 3."""
+    v = list(v)
+    sr = [min(spos[i], i & 15) for i in range(64)]
+    for lev in range(min(nlev, 4)):
+        o = 1 << lev
+        up = [v[i - o] if (i & 15) >= o else 0 for i in range(64)]
+        v = [op(v[i], up[i]) if sr[i] >= o else v[i] for i in range(64)]
+    if any(spos[i] > (i & 15) for i in range(64)):
+        up = [v[(i & ~15) - 1] if (i >> 4) in (1, 3) else 0 for i in range(64)]
+        v = [op(v[i], up[i]) if ((i & 16) and spos[i] > (i & 15)) else v[i] for i in range(64)]
+        up = [v[31] if i >= 32 else 0 for i in range(64)]
+        v = [op(v[i], up[i]) if (i >= 32 and spos[i] >= i - 31) else v[i] for i in range(64)]
+    return v
+
+
+def plain_scan(v, spos, op):
+    out = list(v)
+    for i in range(64):
+        if spos[i] > 0:
+            out[i] = op(out[i - 1], v[i])
+    return out
 
 
 def steps(W, P, live, sdir, cost, clk):
@@ -90,14 +117,9 @@ def scan(W, P, live, sdir, cost, clk):
             Wu[i] = float(np.rint(t))
             if abs(t - Wu[i]) == 0.5:
                 return None
-    q, o = list(Wu), 1
-    while o <= max(spos):   # inclusive scans, Hillis-Steele order as on the GPU
-        q = [q[i] + q[i - o] if spos[i] >= o else q[i] for i in range(64)]
-        o *= 2
-    y, o = [K[i] - (q[i] - Wu[i]) for i in range(64)], 1
-    while o <= max(spos):
-        y = [max(y[i], y[i - o]) if spos[i] >= o else y[i] for i in range(64)]
-        o *= 2
+    nlev = max(spos).bit_length()   # 2^nlev > the largest position
+    q = seg_scan(Wu, spos, nlev, lambda a, b: a + b)
+    y = seg_scan([K[i] - (q[i] - Wu[i]) for i in range(64)], spos, nlev, max)
     v = [q[i] + y[i] for i in range(64)]
     if any(involved[i] and not v[i] < 2.0 ** 53 for i in range(64)):
         return None
@@ -173,3 +195,23 @@ def test_scan_model_long_forward_run():
     assert got is not None and got == steps(*slot)
     # stage s ends where its own Send ended; the last two share the last one
     assert got[63] == got[62] and got[0] < got[63]
+
+
+def test_seg_scan_rows_and_carries():
+    """The row-then-carry order gives the plain left-to-right segmented scan
+    for sums of integers (exact) and for maxima, on random segments that
+    start anywhere, span rows or cover the whole wavefront."""
+    rng = random.Random(7)
+    for trial in range(2000):
+        mode = rng.random()
+        if mode < 0.1:
+            starts = [i == 0 for i in range(64)]
+        else:
+            p = rng.choice([0.02, 0.1, 0.3, 0.7])
+            starts = [i == 0 or rng.random() < p for i in range(64)]
+        spos = _positions(starts)
+        nlev = max(spos).bit_length()
+        vals = [float(rng.randint(0, 2 ** 40)) for _ in range(64)]
+        assert seg_scan(vals, spos, nlev, lambda a, b: a + b) == plain_scan(vals, spos, lambda a, b: a + b), trial
+        ivals = [rng.randint(-2 ** 31, 2 ** 31) for _ in range(64)]
+        assert seg_scan(ivals, spos, nlev, max) == plain_scan(ivals, spos, max), trial
