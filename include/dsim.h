@@ -368,7 +368,7 @@ DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsi
  * that cannot allocate (code under HIP graph capture, tight serving loops,
  * harnesses that forbid allocation): the same simulation, results and
  * argument checks, with the grouping workspace in a fixed buffer the
- * library holds on each GPU it runs on (4.3 MB, kept until the process
+ * library holds on each GPU it runs on (4.5 MB, kept until the process
  * ends; its address is taken on the first call on a GPU), and every kernel
  * on hip_stream (no second stream, no events).  The call allocates
  * nothing.  n_cand <= 2^20 (DSIM_ERANGE beyond).  All calls on one GPU

@@ -120,7 +120,9 @@ struct ParArgs {
     int32_t row_width;
     int32_t p_bound;
     const uint32_t *perm;   // candidates grouped by segment class
-    const uint32_t *meta;   // [0,8) class totals, [8,16) first perm index, [16,24) first lane
+    const uint32_t *meta;   // [0,8) class totals, [8,16) first perm index, [16,24) first lane,
+                            // [24, 24 + kClasses - narrow_end) the wide launch's
+                            // classes in dispatch order (class << 29 | wavefronts)
     int32_t narrow_end;     // classes the narrow launch takes: [0, narrow_end)
     double *makespan;
     double *finish;
@@ -1108,17 +1110,32 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     __shared__ typename std::conditional<WIDE, LdsWide<Sh, (kLanes >> first_wide_class<OV>())>, LdsNarrow<Sh>>::type L;
 
     const int lane = threadIdx.x;
-    // wavefronts start widest class first (the wide launch, or the only
-    // one): those walk the longest pipelines, and starting them first
-    // shortens the tail.  The grid is sized for the worst case; the
-    // wavefronts beyond the last class exit, and come last in either order.
-    const bool widest_first = WIDE || g.narrow_end == kClasses;
     // the binade-wise unit sums: not in the wide kernels (but in the one
     // with the overlapped all-reduce, whose registers it does not raise)
     constexpr bool kBinadeSums = !WIDE || OV;
-    const uint32_t nw = g.meta[16 + kClasses] / (uint32_t)kLanes;   // wavefronts holding classes
-    if (blockIdx.x >= nw) return;
-    const uint32_t blk = widest_first ? nw - 1 - blockIdx.x : blockIdx.x;
+    // Wavefronts start longest first, so that short ones fill the tail.
+    // The wide launch takes its classes in the pre-pass's order (by the
+    // estimated length of their longest wavefront), the only launch its
+    // classes widest first; both take each class from its last wavefront
+    // (the strategy grid lists microbatch counts ascending).  The narrow
+    // launch beside a wide one runs its classes in lane order.  The grid is
+    // sized for the worst case; wavefronts beyond the launch's own exit.
+    uint32_t blk = 0xffffffffu;
+    if constexpr (WIDE) {
+        uint32_t b = blockIdx.x;
+        for (int i = 0; i < kClasses - first_wide_class<OV>(); ++i) {
+            const uint32_t e = g.meta[24 + i], n_w = e & 0x1fffffffu;
+            if (b < n_w) {
+                blk = g.meta[16 + (e >> 29)] / (uint32_t)kLanes + n_w - 1 - b;
+                break;
+            }
+            b -= n_w;
+        }
+    } else {
+        const uint32_t nw = g.meta[16 + kClasses] / (uint32_t)kLanes;   // wavefronts holding classes
+        if (blockIdx.x < nw) blk = g.narrow_end == kClasses ? nw - 1 - blockIdx.x : blockIdx.x;
+    }
+    if (blk == 0xffffffffu) return;
     const uint32_t gl = blk * (uint32_t)kLanes;
     int cls = 0;
     while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
@@ -1512,10 +1529,11 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     }
     if (live_stage && status == 0) {
         Ctx x = {};
-        // (the narrow kernels keep these values live across the loop
-        // instead: reading the argument block again here makes the register
-        // allocator reserve a private frame that no instruction uses)
-        if constexpr (WIDE)
+        // (the narrow kernels and the wide ZeRO one keep these values live
+        // across the loop instead: reading the argument block again here
+        // makes the register allocator reserve a private frame in them that
+        // no instruction uses)
+        if constexpr (WIDE && !(ZR && !RC))
             make_ctx(kernel_args<ParArgs>()->m, kernel_args<ParArgs>()->c, st, x);
         else
             make_ctx(M, g.c, st, x);
@@ -1603,32 +1621,68 @@ void launch_kernel(bool rc, bool zr, bool ov, bool tf, bool wide, dim3 grid, dim
 }
 
 // ---------------------------------------------------------------------------
-// Pre-pass: stable counting sort of the candidates by segment class
+// Pre-pass: stable counting sort of the candidates by segment class, and the
+// order in which the classes' wavefronts start
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kScanBlock) void k_class_count(const dsim_strategy *cand, int64_t n, int p_bound,
-                                                           uint32_t *counts)
+// per block: the class counts, then each class's largest wave_length
+constexpr int kCountRow = 16;
+// A slot's fixed work (schedule, Sends, memory updates) costs about as much
+// as walking this many layers of a transformer stage.
+constexpr uint32_t kSlotLayers = 8;
+
+// Relative length of the wavefront that simulates a candidate: slots (the
+// stage's blocks plus the pipeline's fill and drain) times the work of a
+// slot (a fixed part and the stage's share of the layers), in half layers.
+// Only orders the wide launch's classes.
+__device__ __forceinline__ uint32_t wave_length(const dsim_strategy &st, int n_layers, bool train)
 {
-    __shared__ uint32_t s_cnt[8];
-    if (threadIdx.x < 8) s_cnt[threadIdx.x] = 0;
+    const uint32_t P = (uint32_t)(st.P < 1 ? 1 : (st.P > kMaxStages ? kMaxStages : st.P));
+    const uint32_t K = (uint32_t)(st.K < 1 ? 1 : (st.K > kMaxK ? kMaxK : st.K));
+    const uint32_t L = (uint32_t)(n_layers < 1 ? 1 : (n_layers > 65536 ? 65536 : n_layers));
+    const uint32_t slots = (train ? 2u : 1u) * K + 2u * P;      // <= 32,894
+    const uint32_t work = 2u * kSlotLayers + (2u * L + P - 1) / P;   // <= 131,088
+    const uint64_t len = (uint64_t)slots * work;
+    return len > 0xffffffffu ? 0xffffffffu : (uint32_t)len;
+}
+
+__global__ __launch_bounds__(kScanBlock) void k_class_count(const dsim_strategy *cand, int64_t n, int p_bound,
+                                                           int n_layers, bool train, uint32_t *counts)
+{
+    __shared__ uint32_t s_cnt[8], s_len[8];
+    if (threadIdx.x < 8) {
+        s_cnt[threadIdx.x] = 0;
+        s_len[threadIdx.x] = 0;
+    }
     __syncthreads();
     const int64_t c = (int64_t)blockIdx.x * kScanBlock + threadIdx.x;
-    if (c < n) atomicAdd(&s_cnt[seg_class(cand[c], p_bound)], 1u);
+    if (c < n) {
+        const dsim_strategy st = cand[c];
+        const int j = seg_class(st, p_bound);
+        atomicAdd(&s_cnt[j], 1u);
+        atomicMax(&s_len[j], wave_length(st, n_layers, train));
+    }
     __syncthreads();
-    if (threadIdx.x < 8) counts[(size_t)blockIdx.x * 8 + threadIdx.x] = s_cnt[threadIdx.x];
+    if (threadIdx.x < 8) {
+        counts[(size_t)blockIdx.x * kCountRow + threadIdx.x] = s_cnt[threadIdx.x];
+        counts[(size_t)blockIdx.x * kCountRow + 8 + threadIdx.x] = s_len[threadIdx.x];
+    }
 }
 
 // counts[b][j] -> exclusive prefix over blocks b, per class j; meta as in
-// ParArgs.  One block.
-__global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int64_t nb, uint32_t *meta)
+// ParArgs, the classes from narrow_end on by their longest wave_length
+// (ties: the wider class first).  One block.
+__global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int64_t nb, int narrow_end,
+                                                          uint32_t *meta)
 {
     __shared__ uint32_t s_v[kScanBlock];
-    __shared__ uint32_t s_total[8];
+    __shared__ uint32_t s_total[8], s_len[8];
     const int t = threadIdx.x;
     for (int j = 0; j < kClasses; ++j) {
-        uint32_t carry = 0;
+        uint32_t carry = 0, len = 0;
         for (int64_t b0 = 0; b0 < nb; b0 += kScanBlock) {
             const int64_t b = b0 + t;
-            const uint32_t v = b < nb ? counts[(size_t)b * 8 + j] : 0;
+            const uint32_t v = b < nb ? counts[(size_t)b * kCountRow + j] : 0;
+            if (b < nb && j >= narrow_end) len = max(len, counts[(size_t)b * kCountRow + 8 + j]);
             s_v[t] = v;
             __syncthreads();
             for (int o = 1; o < kScanBlock; o <<= 1) {
@@ -1637,11 +1691,19 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int
                 s_v[t] += add;
                 __syncthreads();
             }
-            if (b < nb) counts[(size_t)b * 8 + j] = carry + s_v[t] - v;
+            if (b < nb) counts[(size_t)b * kCountRow + j] = carry + s_v[t] - v;
             carry += s_v[kScanBlock - 1];
             __syncthreads();
         }
-        if (t == 0) s_total[j] = carry;
+        if (t == 0) {
+            s_total[j] = carry;
+            s_len[j] = 0;
+        }
+        if (j >= narrow_end) {   // a wide class: its longest wavefront
+            for (int o = kLanes / 2; o > 0; o >>= 1) len = max(len, (uint32_t)__shfl_xor((int)len, o, kLanes));
+            __syncthreads();
+            if (t % kLanes == 0) atomicMax(&s_len[j], len);
+        }
         __syncthreads();
     }
     if (t == 0) {
@@ -1656,6 +1718,14 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int
         meta[kClasses] = 0;
         meta[8 + kClasses] = rank;
         meta[16 + kClasses] = lane;
+        uint32_t taken = 0;
+        for (int i = 0; i < kClasses - narrow_end; ++i) {
+            int best = -1;
+            for (int j = kClasses - 1; j >= narrow_end; --j)
+                if (!(taken >> j & 1u) && (best < 0 || s_len[j] > s_len[best])) best = j;
+            taken |= 1u << best;
+            meta[24 + i] = (uint32_t)best << 29 | (meta[16 + best + 1] - meta[16 + best]) / (uint32_t)kLanes;
+        }
     }
 }
 
@@ -1678,7 +1748,7 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strateg
     __syncthreads();
     if (j < kClasses) {
         for (int v = 0; v < wv; ++v) rank += s_wcnt[v][j];
-        perm[meta[8 + j] + offsets[(size_t)blockIdx.x * 8 + j] + rank] = (uint32_t)c;
+        perm[meta[8 + j] + offsets[(size_t)blockIdx.x * kCountRow + j] + rank] = (uint32_t)c;
     }
 }
 
@@ -1689,7 +1759,7 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strateg
 // Host code never uses this name as an address; it takes the device address
 // once per GPU (static_scratch).
 constexpr int64_t kStaticMaxCand = (int64_t)1 << 20;
-constexpr int64_t kStaticWords = (kStaticMaxCand / kScanBlock) * 8 + 32 + kStaticMaxCand;
+constexpr int64_t kStaticWords = (kStaticMaxCand / kScanBlock) * kCountRow + 32 + kStaticMaxCand;
 static __device__ __align__(256) uint32_t scratch[kStaticWords];
 
 dsim_status static_scratch(void **out)
@@ -1716,8 +1786,9 @@ int64_t static_max_cand() { return kStaticMaxCand; }
 size_t parametric_workspace(int64_t n_cand)
 {
     const int64_t nb = (n_cand + kScanBlock - 1) / kScanBlock;
-    // per-block class counts, the class table (32 words), the permutation
-    return (size_t)(nb * 8 + 32 + n_cand) * sizeof(uint32_t);
+    // per-block class counts and lengths, the class table (32 words), the
+    // permutation
+    return (size_t)(nb * kCountRow + 32 + n_cand) * sizeof(uint32_t);
 }
 
 dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, const CostConsts &c,
@@ -1755,24 +1826,26 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     // word is written before it is read: nothing needs clearing)
     const int64_t nb = (n_cand + kScanBlock - 1) / kScanBlock;
     uint32_t *counts = static_cast<uint32_t *>(ws);
-    uint32_t *meta = counts + (size_t)nb * 8;
+    uint32_t *meta = counts + (size_t)nb * kCountRow;
     uint32_t *perm = meta + 32;
     g.perm = perm;
     g.meta = meta;
 
-    hipLaunchKernelGGL(k_class_count, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb, counts);
-    hipLaunchKernelGGL(k_class_scan, dim3(1), dim3(kScanBlock), 0, s, counts, nb, meta);
-    hipLaunchKernelGGL(k_class_scatter, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb,
-                       (const uint32_t *)counts, (const uint32_t *)meta, perm);
-    // every class's lanes round up to whole wavefronts: at most one partial
-    // wavefront per class beyond n * wmax lanes
-    const int64_t waves = (n_cand * wmax + kLanes - 1) / kLanes + kClasses;
     // A large transformer grid splits: the narrow classes run beside the
     // wide ones (whose smaller LDS footprint lets two wavefronts share a
     // SIMD) when the caller gives a second stream, else after them on the
     // one stream.  Small grids and MLPs take one launch for every class.
     const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
     g.narrow_end = split ? first_wide_class(m.mode != DSIM_INFER && m.overlap != 0) : kClasses;
+
+    hipLaunchKernelGGL(k_class_count, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb, m.n_layers,
+                       m.mode != DSIM_INFER, counts);
+    hipLaunchKernelGGL(k_class_scan, dim3(1), dim3(kScanBlock), 0, s, counts, nb, g.narrow_end, meta);
+    hipLaunchKernelGGL(k_class_scatter, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb,
+                       (const uint32_t *)counts, (const uint32_t *)meta, perm);
+    // every class's lanes round up to whole wavefronts: at most one partial
+    // wavefront per class beyond n * wmax lanes
+    const int64_t waves = (n_cand * wmax + kLanes - 1) / kLanes + kClasses;
     const bool rc = m.mode != DSIM_INFER && m.recompute != 0;
     const bool zr = m.mode != DSIM_INFER && m.zero != 0;
     const bool ov = m.mode != DSIM_INFER && m.overlap != 0;

@@ -226,7 +226,7 @@ def test_parametric_workspace_is_checked():
     assert dsim.dsim_parametric_workspace(-1) == 0
     for n in (1, 255, 256, 257, 39965, 10 ** 6):
         nb = (n + 255) // 256
-        assert dsim.dsim_parametric_workspace(n) == 4 * (8 * nb + 32 + n)
+        assert dsim.dsim_parametric_workspace(n) == 4 * (16 * nb + 32 + n)
     m = dsim.model_struct(ALL["gpt3_175b"].model)
     dev = dsim.device_model(DeviceSpec())
     res = dsim.dsim_results()
