@@ -343,7 +343,7 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * optimizer state and the replica's inputs resident from t = 0).
  * Candidates are simulated one pipeline stage per GPU lane, grouped by P
  * through a permutation held in `workspace`: a device buffer of at least
- * dsim_parametric_workspace(n_cand) bytes (about 4 bytes per candidate,
+ * dsim_parametric_workspace(n_cand) bytes (about 12 bytes per candidate,
  * DSIM_ENOSPC if shorter), owned by the caller, in use until hip_stream has
  * passed the call; no word of it needs clearing.  Transformer grids of
  * 8,192 or more candidates are simulated by two kernels, one for the
@@ -368,7 +368,7 @@ DSIM_API dsim_status dsim_simulate_parametric(const dsim_model *model, const dsi
  * that cannot allocate (code under HIP graph capture, tight serving loops,
  * harnesses that forbid allocation): the same simulation, results and
  * argument checks, with the grouping workspace in a fixed buffer the
- * library holds on each GPU it runs on (4.5 MB, kept until the process
+ * library holds on each GPU it runs on (12.7 MB, kept until the process
  * ends; its address is taken on the first call on a GPU), and every kernel
  * on hip_stream (no second stream, no events).  The call allocates
  * nothing.  n_cand <= 2^20 (DSIM_ERANGE beyond).  All calls on one GPU

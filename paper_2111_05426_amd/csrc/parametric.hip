@@ -120,10 +120,9 @@ struct ParArgs {
     int32_t row_width;
     int32_t p_bound;
     const uint32_t *perm;   // candidates grouped by segment class
-    const uint32_t *meta;   // [0,8) class totals, [8,16) first perm index, [16,24) first lane,
-                            // [24, 24 + kClasses - narrow_end) the wide launch's
-                            // classes in dispatch order (class << 29 | wavefronts)
+    const uint32_t *meta;   // [0,8) class totals, [8,16) first perm index, [16,24) first lane
     int32_t narrow_end;     // classes the narrow launch takes: [0, narrow_end)
+    const uint32_t *order;  // the wide launch's wavefronts, longest first
     double *makespan;
     double *finish;
     uint64_t *peak;
@@ -1113,24 +1112,16 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     // the binade-wise unit sums: not in the wide kernels (but in the one
     // with the overlapped all-reduce, whose registers it does not raise)
     constexpr bool kBinadeSums = !WIDE || OV;
-    // Wavefronts start longest first, so that short ones fill the tail.
-    // The wide launch takes its classes in the pre-pass's order (by the
-    // estimated length of their longest wavefront), the only launch its
-    // classes widest first; both take each class from its last wavefront
-    // (the strategy grid lists microbatch counts ascending).  The narrow
-    // launch beside a wide one runs its classes in lane order.  The grid is
+    // Wavefronts start longest first, so that short ones fill the tail: the
+    // wide launch in the pre-pass's order (by the estimated length of each
+    // wavefront), the only launch widest class first, each class from its
+    // last wavefront (the strategy grid lists microbatch counts ascending).
+    // The narrow launch beside a wide one runs in lane order.  The grid is
     // sized for the worst case; wavefronts beyond the launch's own exit.
     uint32_t blk = 0xffffffffu;
     if constexpr (WIDE) {
-        uint32_t b = blockIdx.x;
-        for (int i = 0; i < kClasses - first_wide_class<OV>(); ++i) {
-            const uint32_t e = g.meta[24 + i], n_w = e & 0x1fffffffu;
-            if (b < n_w) {
-                blk = g.meta[16 + (e >> 29)] / (uint32_t)kLanes + n_w - 1 - b;
-                break;
-            }
-            b -= n_w;
-        }
+        const uint32_t n_wide = (g.meta[16 + kClasses] - g.meta[16 + first_wide_class<OV>()]) / (uint32_t)kLanes;
+        if (blockIdx.x < n_wide) blk = g.order[blockIdx.x];
     } else {
         const uint32_t nw = g.meta[16 + kClasses] / (uint32_t)kLanes;   // wavefronts holding classes
         if (blockIdx.x < nw) blk = g.narrow_end == kClasses ? nw - 1 - blockIdx.x : blockIdx.x;
@@ -1622,10 +1613,8 @@ void launch_kernel(bool rc, bool zr, bool ov, bool tf, bool wide, dim3 grid, dim
 
 // ---------------------------------------------------------------------------
 // Pre-pass: stable counting sort of the candidates by segment class, and the
-// order in which the classes' wavefronts start
+// order in which the wide launch's wavefronts start
 // ---------------------------------------------------------------------------
-// per block: the class counts, then each class's largest wave_length
-constexpr int kCountRow = 16;
 // A slot's fixed work (schedule, Sends, memory updates) costs about as much
 // as walking this many layers of a transformer stage.
 constexpr uint32_t kSlotLayers = 8;
@@ -1633,7 +1622,7 @@ constexpr uint32_t kSlotLayers = 8;
 // Relative length of the wavefront that simulates a candidate: slots (the
 // stage's blocks plus the pipeline's fill and drain) times the work of a
 // slot (a fixed part and the stage's share of the layers), in half layers.
-// Only orders the wide launch's classes.
+// Only orders the wide launch's wavefronts.
 __device__ __forceinline__ uint32_t wave_length(const dsim_strategy &st, int n_layers, bool train)
 {
     const uint32_t P = (uint32_t)(st.P < 1 ? 1 : (st.P > kMaxStages ? kMaxStages : st.P));
@@ -1645,44 +1634,35 @@ __device__ __forceinline__ uint32_t wave_length(const dsim_strategy &st, int n_l
     return len > 0xffffffffu ? 0xffffffffu : (uint32_t)len;
 }
 
+// (wave_len, when given: n + 8 words cleared for k_class_scatter)
 __global__ __launch_bounds__(kScanBlock) void k_class_count(const dsim_strategy *cand, int64_t n, int p_bound,
-                                                           int n_layers, bool train, uint32_t *counts)
+                                                           uint32_t *counts, uint32_t *wave_len)
 {
-    __shared__ uint32_t s_cnt[8], s_len[8];
-    if (threadIdx.x < 8) {
-        s_cnt[threadIdx.x] = 0;
-        s_len[threadIdx.x] = 0;
-    }
+    __shared__ uint32_t s_cnt[8];
+    if (threadIdx.x < 8) s_cnt[threadIdx.x] = 0;
     __syncthreads();
     const int64_t c = (int64_t)blockIdx.x * kScanBlock + threadIdx.x;
-    if (c < n) {
-        const dsim_strategy st = cand[c];
-        const int j = seg_class(st, p_bound);
-        atomicAdd(&s_cnt[j], 1u);
-        atomicMax(&s_len[j], wave_length(st, n_layers, train));
+    if (wave_len) {
+        if (c < n) wave_len[c] = 0;
+        if (c < 8) wave_len[n + c] = 0;
     }
+    if (c < n) atomicAdd(&s_cnt[seg_class(cand[c], p_bound)], 1u);
     __syncthreads();
-    if (threadIdx.x < 8) {
-        counts[(size_t)blockIdx.x * kCountRow + threadIdx.x] = s_cnt[threadIdx.x];
-        counts[(size_t)blockIdx.x * kCountRow + 8 + threadIdx.x] = s_len[threadIdx.x];
-    }
+    if (threadIdx.x < 8) counts[(size_t)blockIdx.x * 8 + threadIdx.x] = s_cnt[threadIdx.x];
 }
 
 // counts[b][j] -> exclusive prefix over blocks b, per class j; meta as in
-// ParArgs, the classes from narrow_end on by their longest wave_length
-// (ties: the wider class first).  One block.
-__global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int64_t nb, int narrow_end,
-                                                          uint32_t *meta)
+// ParArgs.  One block.
+__global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int64_t nb, uint32_t *meta)
 {
     __shared__ uint32_t s_v[kScanBlock];
-    __shared__ uint32_t s_total[8], s_len[8];
+    __shared__ uint32_t s_total[8];
     const int t = threadIdx.x;
     for (int j = 0; j < kClasses; ++j) {
-        uint32_t carry = 0, len = 0;
+        uint32_t carry = 0;
         for (int64_t b0 = 0; b0 < nb; b0 += kScanBlock) {
             const int64_t b = b0 + t;
-            const uint32_t v = b < nb ? counts[(size_t)b * kCountRow + j] : 0;
-            if (b < nb && j >= narrow_end) len = max(len, counts[(size_t)b * kCountRow + 8 + j]);
+            const uint32_t v = b < nb ? counts[(size_t)b * 8 + j] : 0;
             s_v[t] = v;
             __syncthreads();
             for (int o = 1; o < kScanBlock; o <<= 1) {
@@ -1691,19 +1671,11 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int
                 s_v[t] += add;
                 __syncthreads();
             }
-            if (b < nb) counts[(size_t)b * kCountRow + j] = carry + s_v[t] - v;
+            if (b < nb) counts[(size_t)b * 8 + j] = carry + s_v[t] - v;
             carry += s_v[kScanBlock - 1];
             __syncthreads();
         }
-        if (t == 0) {
-            s_total[j] = carry;
-            s_len[j] = 0;
-        }
-        if (j >= narrow_end) {   // a wide class: its longest wavefront
-            for (int o = kLanes / 2; o > 0; o >>= 1) len = max(len, (uint32_t)__shfl_xor((int)len, o, kLanes));
-            __syncthreads();
-            if (t % kLanes == 0) atomicMax(&s_len[j], len);
-        }
+        if (t == 0) s_total[j] = carry;
         __syncthreads();
     }
     if (t == 0) {
@@ -1718,20 +1690,52 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scan(uint32_t *counts, int
         meta[kClasses] = 0;
         meta[8 + kClasses] = rank;
         meta[16 + kClasses] = lane;
-        uint32_t taken = 0;
-        for (int i = 0; i < kClasses - narrow_end; ++i) {
-            int best = -1;
-            for (int j = kClasses - 1; j >= narrow_end; --j)
-                if (!(taken >> j & 1u) && (best < 0 || s_len[j] > s_len[best])) best = j;
-            taken |= 1u << best;
-            meta[24 + i] = (uint32_t)best << 29 | (meta[16 + best + 1] - meta[16 + best]) / (uint32_t)kLanes;
-        }
     }
 }
 
+// wave_length quantized: 16 steps per doubling
+constexpr int kLenBuckets = 512;
+constexpr int kOrderBlock = 1024;
+__device__ __forceinline__ int len_bucket(uint32_t len)
+{
+    if (len == 0) return 0;
+    const int e = 31 - __clz(len);
+    const uint32_t f = e >= 4 ? (len >> (e - 4)) & 15u : (len << (4 - e)) & 15u;
+    return e * 16 + (int)f;
+}
+
+// The wide launch's wavefronts longest first: a counting sort of
+// wave_len (each wavefront's longest candidate, from k_class_scatter) over
+// len_bucket, wavefronts of one bucket in any order.  One block.
+__global__ __launch_bounds__(kOrderBlock) void k_wave_order(const uint32_t *meta, int narrow_end,
+                                                           const uint32_t *wave_len, uint32_t *order)
+{
+    __shared__ uint32_t s_cnt[kLenBuckets];
+    const int t = threadIdx.x;
+    const uint32_t w_lo = meta[16 + narrow_end] / (uint32_t)kLanes, w_hi = meta[16 + kClasses] / (uint32_t)kLanes;
+    const uint32_t n_w = w_hi - w_lo;
+    for (int i = t; i < kLenBuckets; i += kOrderBlock) s_cnt[i] = 0;
+    __syncthreads();
+    for (uint32_t i = t; i < n_w; i += kOrderBlock) atomicAdd(&s_cnt[len_bucket(wave_len[i])], 1u);
+    __syncthreads();
+    if (t == 0) {   // bucket starts, longest bucket first
+        uint32_t pos = 0;
+        for (int i = kLenBuckets - 1; i >= 0; --i) {
+            const uint32_t k = s_cnt[i];
+            s_cnt[i] = pos;
+            pos += k;
+        }
+    }
+    __syncthreads();
+    for (uint32_t i = t; i < n_w; i += kOrderBlock) order[atomicAdd(&s_cnt[len_bucket(wave_len[i])], 1u)] = w_lo + i;
+}
+
+// (wave_len, when given: each wide wavefront's longest wave_length, the
+// wavefronts counted from the first wide one, class narrow_end)
 __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strategy *cand, int64_t n, int p_bound,
                                                              const uint32_t *offsets, const uint32_t *meta,
-                                                             uint32_t *perm)
+                                                             uint32_t *perm, int narrow_end, int n_layers,
+                                                             bool train, uint32_t *wave_len)
 {
     constexpr int kWaves = kScanBlock / kLanes;
     __shared__ uint32_t s_wcnt[kWaves][8];
@@ -1748,7 +1752,12 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strateg
     __syncthreads();
     if (j < kClasses) {
         for (int v = 0; v < wv; ++v) rank += s_wcnt[v][j];
-        perm[meta[8 + j] + offsets[(size_t)blockIdx.x * kCountRow + j] + rank] = (uint32_t)c;
+        const uint32_t slot = offsets[(size_t)blockIdx.x * 8 + j] + rank;
+        perm[meta[8 + j] + slot] = (uint32_t)c;
+        if (wave_len && j >= narrow_end) {
+            const uint32_t w = (meta[16 + j] + (slot << j)) / (uint32_t)kLanes - meta[16 + narrow_end] / (uint32_t)kLanes;
+            atomicMax(&wave_len[w], wave_length(cand[c], n_layers, train));
+        }
     }
 }
 
@@ -1759,7 +1768,7 @@ __global__ __launch_bounds__(kScanBlock) void k_class_scatter(const dsim_strateg
 // Host code never uses this name as an address; it takes the device address
 // once per GPU (static_scratch).
 constexpr int64_t kStaticMaxCand = (int64_t)1 << 20;
-constexpr int64_t kStaticWords = (kStaticMaxCand / kScanBlock) * kCountRow + 32 + kStaticMaxCand;
+constexpr int64_t kStaticWords = (kStaticMaxCand / kScanBlock) * 8 + 32 + 3 * kStaticMaxCand + 16;
 static __device__ __align__(256) uint32_t scratch[kStaticWords];
 
 dsim_status static_scratch(void **out)
@@ -1786,9 +1795,10 @@ int64_t static_max_cand() { return kStaticMaxCand; }
 size_t parametric_workspace(int64_t n_cand)
 {
     const int64_t nb = (n_cand + kScanBlock - 1) / kScanBlock;
-    // per-block class counts and lengths, the class table (32 words), the
-    // permutation
-    return (size_t)(nb * kCountRow + 32 + n_cand) * sizeof(uint32_t);
+    // per-block class counts, the class table (32 words), the permutation,
+    // the wide launch's wavefront order and lengths (at most n_cand +
+    // kClasses wavefronts each)
+    return (size_t)(nb * 8 + 32 + 3 * n_cand + 16) * sizeof(uint32_t);
 }
 
 dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, int64_t n_cand, const CostConsts &c,
@@ -1822,13 +1832,17 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     g.c = ParConsts{c.inv_f, c.inv_b, c.inv_l, c.lat, c.launch, c.cap, c.mm, c.mm_c0, c.mm_c1, c.mm_c2,
                     c.mm_c3, c.mm_floor, c.node, c.net_lat, c.net_inv_l, c.streams, c.st_lat, c.st_inv_l};
 
-    // workspace: per-block class counts, class table, permutation (every
-    // word is written before it is read: nothing needs clearing)
+    // workspace: per-block class counts, class table, permutation, wide
+    // wavefront order and lengths (every word is written before it is read:
+    // the caller clears nothing)
     const int64_t nb = (n_cand + kScanBlock - 1) / kScanBlock;
     uint32_t *counts = static_cast<uint32_t *>(ws);
-    uint32_t *meta = counts + (size_t)nb * kCountRow;
+    uint32_t *meta = counts + (size_t)nb * 8;
     uint32_t *perm = meta + 32;
+    uint32_t *order = perm + n_cand;
+    uint32_t *wave_len = order + n_cand + 8;
     g.perm = perm;
+    g.order = order;
     g.meta = meta;
 
     // A large transformer grid splits: the narrow classes run beside the
@@ -1838,11 +1852,15 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
     g.narrow_end = split ? first_wide_class(m.mode != DSIM_INFER && m.overlap != 0) : kClasses;
 
-    hipLaunchKernelGGL(k_class_count, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb, m.n_layers,
-                       m.mode != DSIM_INFER, counts);
-    hipLaunchKernelGGL(k_class_scan, dim3(1), dim3(kScanBlock), 0, s, counts, nb, g.narrow_end, meta);
+    hipLaunchKernelGGL(k_class_count, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb, counts,
+                       split ? wave_len : nullptr);
+    hipLaunchKernelGGL(k_class_scan, dim3(1), dim3(kScanBlock), 0, s, counts, nb, meta);
     hipLaunchKernelGGL(k_class_scatter, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb,
-                       (const uint32_t *)counts, (const uint32_t *)meta, perm);
+                       (const uint32_t *)counts, (const uint32_t *)meta, perm, g.narrow_end, m.n_layers,
+                       m.mode != DSIM_INFER, split ? wave_len : nullptr);
+    if (split)
+        hipLaunchKernelGGL(k_wave_order, dim3(1), dim3(kOrderBlock), 0, s, (const uint32_t *)meta, g.narrow_end,
+                           (const uint32_t *)wave_len, order);
     // every class's lanes round up to whole wavefronts: at most one partial
     // wavefront per class beyond n * wmax lanes
     const int64_t waves = (n_cand * wmax + kLanes - 1) / kLanes + kClasses;

@@ -220,13 +220,13 @@ def test_size_rule_matches_oracle_on_random_models(orc):
 
 def test_parametric_workspace_is_checked():
     """dsim_simulate_parametric takes its grouping buffer from the caller:
-    about 4 bytes per candidate, DSIM_ENOSPC when it is missing or short
+    about 12 bytes per candidate, DSIM_ENOSPC when it is missing or short
     (checked before any launch)."""
     L = dsim.lib()
     assert dsim.dsim_parametric_workspace(-1) == 0
     for n in (1, 255, 256, 257, 39965, 10 ** 6):
         nb = (n + 255) // 256
-        assert dsim.dsim_parametric_workspace(n) == 4 * (16 * nb + 32 + n)
+        assert dsim.dsim_parametric_workspace(n) == 4 * (8 * nb + 32 + 3 * n + 16)
     m = dsim.model_struct(ALL["gpt3_175b"].model)
     dev = dsim.device_model(DeviceSpec())
     res = dsim.dsim_results()
