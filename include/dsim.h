@@ -347,7 +347,8 @@ DSIM_API dsim_status dsim_simulate_tables(const dsim_tables *tables, int64_t n_c
  * DSIM_ENOSPC if shorter), owned by the caller, in use until hip_stream has
  * passed the call; no word of it needs clearing.  Transformer grids of
  * 8,192 or more candidates are simulated by two kernels, one for the
- * candidates of 1 to 8 stages (1 to 4 with the overlapped all-reduce) and
+ * candidates of 1 to 8 stages (1 to 4 with the overlapped all-reduce, or with
+ * ZeRO and no recomputation) and
  * one for the others; they run side by side
  * when side_stream is a second stream (hip_stream's earlier work is awaited
  * on it and the call's work on side_stream is awaited on hip_stream before

@@ -1028,8 +1028,10 @@ template <class Sh> union LdsNarrow {
 // overlapped gradient all-reduce the wide kernel keeps that arithmetic (its
 // registers are taken anyway) and also takes segments of 8 lanes (8 per
 // wavefront, about 14 KB).
-template <bool OV> constexpr int first_wide_class() { return OV ? 3 : 4; }   // segment width 8 / 16
-inline int first_wide_class(bool ov) { return ov ? 3 : 4; }
+// (ZeRO without recomputation moves its 8-lane segments to the wide launch
+// too: its narrow kernel holds 48 KB of LDS, three wavefronts per CU)
+template <bool OV, bool ZR> constexpr int first_wide_class() { return (OV || ZR) ? 3 : 4; }
+inline int first_wide_class(bool ov, bool zr) { return (ov || zr) ? 3 : 4; }
 constexpr int64_t kSplitMinCand = 8192;
 template <class Sh, int NS> struct LdsWide {
     double2 unit[NS][kKeys][Sh::U2];
@@ -1106,7 +1108,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     using Sh = Shape<TF, ZR>;
     constexpr int PST = WIDE ? 1 : kLanes;   // double2 stride of a lane's edge program
     // at most 64 / 2^(first wide class) segments per wide wavefront
-    __shared__ typename std::conditional<WIDE, LdsWide<Sh, (kLanes >> first_wide_class<OV>())>, LdsNarrow<Sh>>::type L;
+    __shared__ typename std::conditional<WIDE, LdsWide<Sh, (kLanes >> first_wide_class<OV, ZR && !RC>())>, LdsNarrow<Sh>>::type L;
 
     const int lane = threadIdx.x;
     // the binade-wise unit sums: not in the wide kernels (but in the one
@@ -1120,7 +1122,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     // sized for the worst case; wavefronts beyond the launch's own exit.
     uint32_t blk = 0xffffffffu;
     if constexpr (WIDE) {
-        const uint32_t n_wide = (g.meta[16 + kClasses] - g.meta[16 + first_wide_class<OV>()]) / (uint32_t)kLanes;
+        const uint32_t n_wide = (g.meta[16 + kClasses] - g.meta[16 + first_wide_class<OV, ZR && !RC>()]) / (uint32_t)kLanes;
         if (blockIdx.x < n_wide) blk = g.order[blockIdx.x];
     } else {
         const uint32_t nw = g.meta[16 + kClasses] / (uint32_t)kLanes;   // wavefronts holding classes
@@ -1130,7 +1132,7 @@ __device__ __forceinline__ void parametric_body(const ParArgs &g)
     const uint32_t gl = blk * (uint32_t)kLanes;
     int cls = 0;
     while (cls + 1 < kClasses && gl >= g.meta[16 + cls + 1]) ++cls;
-    if (WIDE ? cls < first_wide_class<OV>() : cls >= g.narrow_end) return;   // the other launch's classes
+    if (WIDE ? cls < first_wide_class<OV, ZR && !RC>() : cls >= g.narrow_end) return;   // the other launch's classes
     const int W = 1 << cls;
     const bool shared = WIDE || W >= 4;
     const uint32_t local = gl + lane - g.meta[16 + cls];
@@ -1850,7 +1852,8 @@ dsim_status launch_parametric(const dsim_model &m, const dsim_strategy *cand, in
     // SIMD) when the caller gives a second stream, else after them on the
     // one stream.  Small grids and MLPs take one launch for every class.
     const bool split = m.family == DSIM_TRANSFORMER && n_cand >= kSplitMinCand;
-    g.narrow_end = split ? first_wide_class(m.mode != DSIM_INFER && m.overlap != 0) : kClasses;
+    const bool zr_only = m.mode != DSIM_INFER && m.zero != 0 && m.recompute == 0;
+    g.narrow_end = split ? first_wide_class(m.mode != DSIM_INFER && m.overlap != 0, zr_only) : kClasses;
 
     hipLaunchKernelGGL(k_class_count, dim3((unsigned)nb), dim3(kScanBlock), 0, s, cand, n_cand, pb, counts,
                        split ? wave_len : nullptr);
